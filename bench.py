@@ -1,0 +1,293 @@
+#!/usr/bin/env python3
+"""Benchmark of the FlashConv hot path on one MI355X.
+
+Step (the headline): the H3-125M-shaped diagonal-SSM convolution, B=8, H=768,
+L=2048, fp16 I/O with fp32 arithmetic: kernel generation from the SSM
+parameters (h3_ssm_kernel), kernel spectrum (h3_kernel_spectrum) and the fused
+FFT convolution with skip term (h3_fftconv_spectral).  Inputs are resident in
+HBM; K steps rotate over enough input/output buffer sets (>= 512 MB) that
+every step reads u and writes y cold (not from the 256 MB Infinity Cache).
+
+value = algorithmic bytes of one step (u + y + k once per channel + D) / time,
+in GB/s.  The roofline object covers the dominant kernel (the fused conv),
+timed with HIP events on the stream it runs on.  Extra workloads (the shift
+kernel conv, the fused-limit bf16 conv, state passing at L = 128K, the layer
+forward, the small fp32 conv) are reported under "extra".  The float64 CPU
+oracle is timed on the same config-1 workload as "cpu_baseline".
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-extra] [--no-cpu]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def _dev_tensor(storage, dtype, dev):
+    import numpy as np
+    import torch
+    import workloads
+    if dtype == workloads.BF16:
+        t = torch.from_numpy(np.ascontiguousarray(storage).view(np.int16)).view(torch.bfloat16)
+    else:
+        t = torch.from_numpy(np.ascontiguousarray(storage))
+    return t.to(dev)
+
+
+def _f32(a, dev):
+    import numpy as np
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+
+
+class EventTimer:
+    """Per-stage HIP events on the current stream; durations averaged after sync."""
+
+    def __init__(self, stages):
+        import torch
+        self.stages = stages
+        self.torch = torch
+        self.ev = []
+
+    def step(self):
+        ev = [self.torch.cuda.Event(enable_timing=True) for _ in range(len(self.stages) + 1)]
+        self.ev.append(ev)
+        return ev
+
+    def averages(self):
+        out = {}
+        for i, s in enumerate(self.stages):
+            ts = [e[i].elapsed_time(e[i + 1]) for e in self.ev]
+            out[s] = sum(ts) / len(ts)
+        return out
+
+
+def bench_headline(h3, steps, warmup, dev):
+    """Config 1 step: kernel gen + spectrum + fused conv (diagonal SSM)."""
+    import torch
+    import workloads
+    w = workloads.config(1)
+    B, H, L = w.B, w.H, w.L
+    io_bytes = B * H * L * 2 * 2
+    nsets = max(2, -(-512 * 2 ** 20 // io_bytes))
+    u0 = _dev_tensor(w.u, w.dtype, dev)
+    us = [u0] + [u0.clone() for _ in range(nsets - 1)]
+    ys = [torch.empty_like(u0) for _ in range(nsets)]
+    A, Bp, C, dt = (_f32(w.ssm.A, dev), _f32(w.ssm.B, dev), _f32(w.ssm.C, dev), _f32(w.ssm.dt, dev))
+    D = _f32(w.D, dev)
+    k = torch.empty((H, L), dtype=torch.float32, device=dev)
+    K = torch.empty((H, L + 1, 2), dtype=torch.float32, device=dev)
+
+    def one(i, ev=None):
+        if ev: ev[0].record()
+        h3.ssm_kernel(A, Bp, C, dt, L, out=k)
+        if ev: ev[1].record()
+        h3.kernel_spectrum(k, out=K)
+        if ev: ev[2].record()
+        h3.fftconv_spectral(us[i % nsets], K, D, out=ys[i % nsets])
+        if ev: ev[3].record()
+
+    for i in range(warmup):
+        one(i)
+    torch.cuda.synchronize()
+    timer = EventTimer(["ssm_kernel", "kernel_spectrum", "fftconv"])
+    t0 = torch.cuda.Event(enable_timing=True); t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for i in range(steps):
+        one(i, timer.step())
+    t1.record()
+    torch.cuda.synchronize()
+    total_ms = t0.elapsed_time(t1)
+    per = timer.averages()
+    ms = total_ms / steps
+    step_bytes = B * H * L * (2 + 2) + H * L * 4 + H * 4
+    conv_bytes = B * H * L * (2 + 2) + H * (L + 1) * 8 + H * 4
+    conv_gbs = conv_bytes / (per["fftconv"] * 1e-3) / 1e9
+    return {
+        "w": w, "ms_per_step": ms, "step_bytes": step_bytes,
+        "value": step_bytes / (ms * 1e-3) / 1e9,
+        "gelem_per_s": B * H * L / (ms * 1e-3) / 1e9,
+        "stage_ms": per, "conv_bytes": conv_bytes, "conv_gbs": conv_gbs, "nsets": nsets,
+    }
+
+
+def _time_calls(fn, reps, warm):
+    import torch
+    for _ in range(warm):
+        fn(0)
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True); b = torch.cuda.Event(enable_timing=True)
+    a.record()
+    for i in range(reps):
+        fn(i)
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / reps
+
+
+def bench_extra(h3, dev, reps=10, warm=3):
+    import numpy as np
+    import torch
+    import oracle  # noqa: F401  (not used on the GPU path; kept out on purpose)
+    import workloads
+    ex = {}
+    # config 1, shift-SSM kernel (k_t = C_t, t < 64): spectrum + conv
+    w = workloads.config(1)
+    B, H, L = w.B, w.H, w.L
+    ks = np.zeros((H, L), np.float32); ks[:, :64] = w.shift_C
+    ks = _f32(ks, dev)
+    u = _dev_tensor(w.u, w.dtype, dev)
+    nsets = 12
+    us = [u] + [u.clone() for _ in range(nsets - 1)]
+    ys = [torch.empty_like(u) for _ in range(nsets)]
+    D = _f32(w.D, dev)
+    K = torch.empty((H, L + 1, 2), dtype=torch.float32, device=dev)
+    ms = _time_calls(lambda i: (h3.kernel_spectrum(ks, out=K),
+                                h3.fftconv_spectral(us[i % nsets], K, D, out=ys[i % nsets])), reps, warm)
+    by = B * H * L * 4 + H * L * 4 + H * 4
+    ex["cfg1_shift_conv"] = {"ms": ms, "GB_s": by / ms / 1e6, "pct_hbm_peak": 100 * by / ms / 1e6 / HBM_PEAK_GBS}
+    del us, ys
+
+    # config 2: bf16, B=16 H=256 L=8192: kernel gen + spectrum + conv
+    w = workloads.config(2)
+    B, H, L = w.B, w.H, w.L
+    u = _dev_tensor(w.u, w.dtype, dev)
+    nsets = 4
+    us = [u] + [u.clone() for _ in range(nsets - 1)]
+    ys = [torch.empty_like(u) for _ in range(nsets)]
+    A, Bp, C, dt = (_f32(w.ssm.A, dev), _f32(w.ssm.B, dev), _f32(w.ssm.C, dev), _f32(w.ssm.dt, dev))
+    D = _f32(w.D, dev)
+    k = torch.empty((H, L), dtype=torch.float32, device=dev)
+    K = torch.empty((H, L + 1, 2), dtype=torch.float32, device=dev)
+    ms = _time_calls(lambda i: (h3.ssm_kernel(A, Bp, C, dt, L, out=k), h3.kernel_spectrum(k, out=K),
+                                h3.fftconv_spectral(us[i % nsets], K, D, out=ys[i % nsets])), reps, warm)
+    by = B * H * L * 4 + H * L * 4 + H * 4
+    ex["cfg2_fused_limit_bf16"] = {"ms": ms, "GB_s": by / ms / 1e6, "pct_hbm_peak": 100 * by / ms / 1e6 / HBM_PEAK_GBS,
+                                   "gelem_per_s": B * H * L / ms / 1e6}
+    del us, ys
+
+    # config 3: state passing, B=2 H=1024 L=131072, chunk 8192, fp16
+    w = workloads.config(3)
+    B, H, L, m = w.B, w.H, w.L, w.m
+    u = _dev_tensor(w.u, w.dtype, dev)
+    y = torch.empty_like(u)
+    A, Bp, C, dt = (_f32(w.ssm.A, dev), _f32(w.ssm.B, dev), _f32(w.ssm.C, dev), _f32(w.ssm.dt, dev))
+    Ab, Bb = h3.ssm_discretize(A, Bp, dt)
+    D = _f32(w.D, dev)
+    ws = torch.empty(h3.workspace_size(h3.OP_STATEPASS, B, H, L, m, w.chunk, h3.F16), dtype=torch.uint8, device=dev)
+    ms = _time_calls(lambda i: h3.statepass_conv(u, Ab, Bb, C, D, w.chunk, out=y, workspace=ws), reps, warm)
+    by = B * H * L * 4 + 3 * H * m * 8 + H * 4 + 2 * B * H * m * 8
+    ex["cfg3_statepass_f16"] = {"ms": ms, "gelem_per_s": B * H * L / ms / 1e6, "GB_s": by / ms / 1e6,
+                                "pct_hbm_peak": 100 * by / ms / 1e6 / HBM_PEAK_GBS}
+    del u, y, ws
+
+    # config 4: H3 layer forward, bf16, B=4 L=2048 d=2560
+    w = workloads.config(4)
+    B, L, d = w.B, w.L, w.d
+    x = _dev_tensor(w.x, w.dtype, dev)
+    W = {n: _dev_tensor(w.W[n][0], w.dtype, dev) for n in "qkvo"}
+    A, Bp, C, dt = (_f32(w.diag.A, dev), _f32(w.diag.B, dev), _f32(w.diag.C, dev), _f32(w.diag.dt, dev))
+    dk = h3.ssm_kernel(A, Bp, C, dt, L)
+    sC = _f32(w.shift_C, dev); dD = _f32(w.diag_D, dev)
+    out = torch.empty_like(x)
+    ws = torch.empty(h3.workspace_size(h3.OP_LAYER, B, d, L, 64, 0, h3.BF16), dtype=torch.uint8, device=dev)
+    ms = _time_calls(lambda i: h3.layer_fwd(x, W["q"], W["k"], W["v"], W["o"], sC, None, dk, dD,
+                                            out=out, workspace=ws), reps, warm)
+    flops = 2.0 * B * L * d * d * 4
+    ex["cfg4_layer_bf16"] = {"ms": ms, "gemm_TFLOP_s": flops / ms / 1e9,
+                             "pct_mfma_bf16_peak": 100 * flops / ms / 1e9 / MFMA_BF16_PEAK_TFLOPS}
+    del x, W, out, ws
+
+    # config 0: fp32, B=1 H=64 L=1024 (latency bound)
+    w = workloads.config(0)
+    u = _dev_tensor(w.u, w.dtype, dev)
+    y = torch.empty_like(u)
+    A, Bp, C, dt = (_f32(w.ssm.A, dev), _f32(w.ssm.B, dev), _f32(w.ssm.C, dev), _f32(w.ssm.dt, dev))
+    D = _f32(w.D, dev)
+    k = torch.empty((w.H, w.L), dtype=torch.float32, device=dev)
+    K = torch.empty((w.H, w.L + 1, 2), dtype=torch.float32, device=dev)
+    ms = _time_calls(lambda i: (h3.ssm_kernel(A, Bp, C, dt, w.L, out=k), h3.kernel_spectrum(k, out=K),
+                                h3.fftconv_spectral(u, K, D, out=y)), 50, 5)
+    ex["cfg0_f32_latency_us"] = ms * 1e3
+    return ex
+
+
+def cpu_baseline(w, step_bytes):
+    """The float64 oracle on the whole config-1 workload: kernel generation for
+    every channel, then the direct causal convolution of every row."""
+    import numpy as np
+    import oracle
+    A, B, C, dt = w.ssm.complex64()
+    t = time.time()
+    k = oracle.ssm_kernel(A, B, C, dt, w.L)
+    oracle.causal_conv(w.u64, k, w.D.astype(np.float64))
+    el = time.time() - t
+    return {"value": step_bytes / el / 1e9, "unit": "GB/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"whole config-1 workload (B={w.B} H={w.H} L={w.L}): float64 kernel generation "
+                      f"+ direct O(L^2) causal conv, {el:.2f} s wall"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-extra", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the hot path shards trivially over rows, see DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2212_14052_amd as h3
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    h3.lib()
+    head = bench_headline(h3, args.steps, args.warmup, dev)
+    print(f"# headline done: {head['ms_per_step']*1e3:.1f} us/step", file=sys.stderr, flush=True)
+    extra = {} if args.no_extra else bench_extra(h3, dev)
+    if extra:
+        print("# extra done", file=sys.stderr, flush=True)
+    w = head["w"]
+    per = head["stage_ms"]
+    res = {
+        "metric": "FFT-conv HBM GB/s (% of peak) and Gelem/s at BxHxL; state-passing Gelem/s at L=128K",
+        "value": round(head["value"], 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(head["ms_per_step"], 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {"workload": "cfg1_h3_125m_diag_conv_f16", "B": w.B, "H": w.H, "L": w.L, "m": 64,
+                   "pct_hbm_peak": round(100 * head["value"] / HBM_PEAK_GBS, 2),
+                   "gelem_per_s": round(head["gelem_per_s"], 2),
+                   "stage_us": {k: round(v * 1e3, 2) for k, v in per.items()},
+                   "buffer_sets": head["nsets"]},
+        "roofline": {"bound": "hbm", "achieved": round(head["conv_gbs"], 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(head["conv_gbs"] / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "fftconv_kernel<4096, f16>", "bytes_per_launch": head["conv_bytes"]},
+    }
+    if extra:
+        res["extra"] = extra
+    if not args.no_cpu:
+        res["cpu_baseline"] = cpu_baseline(w, head["step_bytes"])
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,170 @@
+/*
+ * h3flash: MI355X (gfx950) FlashConv hot path of "Hungry Hungry Hippos"
+ * (Fu, Dao et al., arXiv 2212.14052).  C ABI of libh3flash.so.
+ *
+ * General conventions
+ *  - Every tensor pointer is a DEVICE pointer owned by the caller.  The library
+ *    allocates no device memory: scratch space is passed in as `workspace`
+ *    (size it with h3_workspace_size) and must not alias any other argument.
+ *  - Complex values are interleaved (re, im) float32 pairs.
+ *  - Tensors are dense, row-major, with the last dimension contiguous.
+ *    Sequence tensors are (B, H, L): row (b, h) is L contiguous elements.
+ *  - 16-bit I/O (H3_F16, H3_BF16) is read and written as IEEE half / bfloat16;
+ *    all arithmetic is float32 (matrix-core operands may be rounded to 16 bit,
+ *    accumulation is float32).  Stores round to nearest, ties to even.
+ *  - `stream` is a hipStream_t (NULL = the legacy default stream).  Every call
+ *    validates its arguments on the host, enqueues its kernels on `stream` and
+ *    returns without synchronising.  On a validation error nothing is launched.
+ *  - NaN and Inf in the inputs propagate to the outputs; they are not masked.
+ *  - Return value: H3_OK (0) or a negative h3_status.  No C++ exception crosses
+ *    this boundary.
+ *  - The library is stateless and may be called from several host threads.
+ */
+#ifndef H3FLASH_H
+#define H3FLASH_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    H3_OK = 0,
+    H3_EINVAL = -1,        /* null pointer, bad size, misaligned or aliased buffers    */
+    H3_EUNSUPPORTED = -2,  /* length / chunk / mode count / dtype outside what is built */
+    H3_EWORKSPACE = -3,    /* workspace missing or smaller than h3_workspace_size       */
+    H3_EDEVICE = -4        /* a kernel launch failed (hipGetLastError after launching)  */
+} h3_status;
+
+typedef enum { H3_F32 = 0, H3_F16 = 1, H3_BF16 = 2 } h3_dtype;
+
+/* Operation codes for h3_workspace_size. */
+enum { H3_OP_FFTCONV = 1, H3_OP_STATEPASS = 2, H3_OP_LAYER = 3 };
+
+/* Limits of this build. */
+#define H3_MAX_MODES 64     /* m: complex modes per channel of a diagonal SSM      */
+#define H3_MIN_LEN 16       /* smallest fused convolution length (and chunk)       */
+#define H3_FUSED_LIMIT 8192 /* longest fused convolution length (and chunk)        */
+#define H3_MAX_SHIFT 64     /* longest shift-SSM filter in h3_layer_fwd            */
+
+/*
+ * h3_ssm_discretize — zero-order-hold discretisation of H diagonal SSMs of m
+ * complex modes (the continuous SSM x' = Ax + Bu of Sec. 2.1, diagonal A as in
+ * Sec. 3.2):  Abar = exp(dt_h A),  Bbar = (exp(dt_h A) - 1) / A * B.
+ *   A, B       (H, m) complex, read.     dt (H) float32 > 0, read.
+ *   Abar, Bbar (H, m) complex, written.  Computed in float64, stored float32.
+ * Errors: EINVAL (null, H < 1, m < 1), EUNSUPPORTED (m > H3_MAX_MODES).
+ */
+int h3_ssm_discretize(const float *A, const float *B, const float *dt, int H, int m,
+                      float *Abar, float *Bbar, void *stream);
+
+/*
+ * h3_ssm_kernel — the SSM convolution kernel f = [CB, CAB, CA^2B, ...] of
+ * Sec. 2.1 for a diagonal SSM, from continuous parameters and step dt:
+ *   k[h, t] = 2 Re sum_{n<m} C[h,n] Bbar[h,n] exp(t dt_h A[h,n]),  t < L,
+ * with Bbar the ZOH input matrix above.  Each complex mode stands for a
+ * conjugate pair (hence 2 Re), so k is the impulse response of the recurrence
+ * y_t = 2 Re(C x_t) + D u_t.  Phases t*dt*Im(A) are reduced in float64.
+ *   A, B, C (H, m) complex; dt (H); k (H, L) float32, written.
+ * Errors: EINVAL (null, H, m or L < 1), EUNSUPPORTED (m > H3_MAX_MODES).
+ */
+int h3_ssm_kernel(const float *A, const float *B, const float *C, const float *dt,
+                  int H, int m, int L, float *k, void *stream);
+
+/*
+ * h3_fftconv — fused FFT convolution (Sec. 4.1; the convolution of Sec. 2.1):
+ *   y[b,h,:] = irfft(rfft(u[b,h,:], 2L) * rfft(k[h,:], 2L))[:L] + D[h] u[b,h,:]
+ * i.e. the causal linear convolution y_t = sum_{j<=t} k[h,j] u[b,h,t-j] + D u_t.
+ *   u, y  (B, H, L) of `dtype`; must not overlap.
+ *   k     (H, L) float32.   D (H) float32, or NULL for no skip term.
+ *   L     power of two in [H3_MIN_LEN, H3_FUSED_LIMIT].
+ *   workspace >= h3_workspace_size(H3_OP_FFTCONV, B, H, L, 0, 0, dtype) bytes
+ *   (holds the kernel spectra, H * (L + 1) complex).
+ * Errors: EINVAL, EUNSUPPORTED (L, dtype), EWORKSPACE, EDEVICE.
+ */
+int h3_fftconv(const void *u, const float *k, const float *D, void *y,
+               int B, int H, int L, int dtype,
+               void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * h3_kernel_spectrum — the kernel half of the fused convolution, split out so a
+ * spectrum can be reused across calls that share k (e.g. every batch row, or
+ * repeated inputs):  Kspec[h, f] = (1/2L) sum_{t<L} k[h,t] exp(-2 pi i f t / 2L),
+ * f = 0..L (the non-redundant half of the length-2L DFT of the zero-padded
+ * kernel, with the inverse transform's 1/2L folded in).
+ *   k (H, L) float32.  Kspec (H, L+1) complex, written.
+ *   L power of two in [H3_MIN_LEN, H3_FUSED_LIMIT].
+ * Errors: EINVAL, EUNSUPPORTED (L), EDEVICE.
+ */
+int h3_kernel_spectrum(const float *k, int H, int L, float *Kspec, void *stream);
+
+/*
+ * h3_fftconv_spectral — the fused convolution of h3_fftconv given the kernel
+ * spectrum from h3_kernel_spectrum (no workspace needed).
+ *   u, y (B, H, L) of `dtype`, not overlapping.  Kspec (H, L+1) complex.
+ *   D (H) float32 or NULL.
+ * Errors: EINVAL, EUNSUPPORTED (L, dtype), EDEVICE.
+ */
+int h3_fftconv_spectral(const void *u, const float *Kspec, const float *D, void *y,
+                        int B, int H, int L, int dtype, void *stream);
+
+/*
+ * h3_statepass_conv — state passing (Sec. 4.2, Algorithm 2) for a diagonal
+ * SSM given in discrete form, over sequences longer than the fused limit:
+ * the sequence is cut into L/chunk chunks; each chunk is a fused FFT
+ * convolution with the length-`chunk` kernel plus the contribution of the
+ * state carried in, and the state is advanced chunk to chunk.  The result is
+ * that of the recurrence (Proposition 2):
+ *   x_t = Abar x_{t-1} + Bbar u_t (per mode),  y_t = 2 Re(C . x_t) + D u_t,
+ *   x_{-1} = x0,  x_final = x_{L-1}.
+ *   u, y        (B, H, L) of `dtype`; must not overlap.
+ *   Abar, Bbar, C (H, m) complex.  D (H) float32 (NULL: no skip term).
+ *   x0          (B, H, m) complex, or NULL for the zero state.
+ *   x_final     (B, H, m) complex written, or NULL.
+ *   chunk       power of two in [H3_MIN_LEN, H3_FUSED_LIMIT] dividing L.
+ *   workspace >= h3_workspace_size(H3_OP_STATEPASS, B, H, L, m, chunk, dtype).
+ * Errors: EINVAL (null, sizes, L % chunk), EUNSUPPORTED (chunk, m, dtype),
+ *         EWORKSPACE, EDEVICE.
+ */
+int h3_statepass_conv(const void *u, const float *Abar, const float *Bbar,
+                      const float *C, const float *D, const float *x0,
+                      int B, int H, int L, int m, int chunk, int dtype,
+                      void *y, float *x_final,
+                      void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * h3_layer_fwd — H3 layer forward with head dimension 1 (Sec. 3.2,
+ * Algorithm 1):
+ *   Q = x Wq, K = x Wk, V = x Wv           (row-vector convention, (B,L,d)x(d,d))
+ *   Kbar = SSM_shift(K): Kbar_t = sum_{j<m_s} shift_C[c,j] K_{t-j} + shift_D[c] K_t
+ *   G = Kbar * V;  S = SSM_diag(G) = diag_k[c] (*) G + diag_D[c] G   (causal conv)
+ *   out = (Q * S) Wo
+ *   x, out   (B, L, d) of `dtype` (H3_F16 or H3_BF16); must not overlap.
+ *   Wq, Wk, Wv, Wo  (d, d) of `dtype`.
+ *   shift_C  (d, m_s) float32, m_s in [1, H3_MAX_SHIFT].  shift_D (d) or NULL.
+ *   diag_k   (d, L) float32 (e.g. from h3_ssm_kernel).  diag_D (d) or NULL.
+ *   L power of two in [H3_MIN_LEN, H3_FUSED_LIMIT]; d a multiple of 64.
+ *   workspace >= h3_workspace_size(H3_OP_LAYER, B, d, L, m_s, 0, dtype).
+ * Errors: EINVAL, EUNSUPPORTED (L, d, m_s, dtype), EWORKSPACE, EDEVICE.
+ */
+int h3_layer_fwd(const void *x, const void *Wq, const void *Wk, const void *Wv,
+                 const void *Wo, const float *shift_C, const float *shift_D,
+                 const float *diag_k, const float *diag_D,
+                 int B, int L, int d, int m_s, int dtype, void *out,
+                 void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * h3_workspace_size — bytes of workspace an operation needs (0 if the
+ * arguments are invalid).  H_or_d is H for the convolutions, d for the layer;
+ * m is the mode count (state passing) or the shift length (layer).
+ */
+size_t h3_workspace_size(int op, int B, int H_or_d, int L, int m, int chunk, int dtype);
+
+/* Human-readable name of a status code (static string). */
+const char *h3_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* H3FLASH_H */

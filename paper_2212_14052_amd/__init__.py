@@ -1,0 +1,227 @@
+"""MI355X-native FlashConv hot path of "Hungry Hungry Hippos" (arXiv 2212.14052).
+
+Thin Python binding over the C ABI of ``libh3flash.so`` (declared in
+``include/h3flash.h``).  Every function here only marshals arguments: tensors
+are PyTorch device tensors (PyTorch supplies device memory and the stream),
+and all arithmetic runs in the library's HIP kernels.  There is no fallback:
+if the library is missing, importing the ops raises.
+
+Complex parameters are accepted either as complex64 tensors or as float32
+tensors with a trailing dimension of 2 (re, im).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import torch
+
+__all__ = [
+    "H3Error", "lib", "ssm_discretize", "ssm_kernel", "fftconv", "statepass_conv",
+    "layer_fwd", "kernel_spectrum", "fftconv_spectral", "workspace_size", "status_string", "F32", "F16", "BF16",
+    "OP_FFTCONV", "OP_STATEPASS", "OP_LAYER", "FUSED_LIMIT", "MAX_MODES",
+]
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libh3flash.so")
+
+F32, F16, BF16 = 0, 1, 2
+OP_FFTCONV, OP_STATEPASS, OP_LAYER = 1, 2, 3
+FUSED_LIMIT = 8192
+MAX_MODES = 64
+
+_DTYPES = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
+
+_lib = None
+
+
+class H3Error(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn}: {status_string(status)} (status {status})")
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    """Load libh3flash.so (built by ``paper_2212_14052_amd.build``)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(
+                f"{LIB_PATH} is missing: build it with `python -m paper_2212_14052_amd.build` "
+                "(there is no non-HIP fallback)")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+        L.h3_ssm_discretize.argtypes = [vp, vp, vp, i, i, vp, vp, vp]
+        L.h3_ssm_kernel.argtypes = [vp, vp, vp, vp, i, i, i, vp, vp]
+        L.h3_fftconv.argtypes = [vp, vp, vp, vp, i, i, i, i, vp, sz, vp]
+        L.h3_kernel_spectrum.argtypes = [vp, i, i, vp, vp]
+        L.h3_fftconv_spectral.argtypes = [vp, vp, vp, vp, i, i, i, i, vp]
+        L.h3_statepass_conv.argtypes = [vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, vp, vp, vp, sz, vp]
+        L.h3_layer_fwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, vp, vp, sz, vp]
+        L.h3_workspace_size.argtypes = [i, i, i, i, i, i, i]
+        L.h3_workspace_size.restype = sz
+        L.h3_status_string.argtypes = [i]
+        L.h3_status_string.restype = ctypes.c_char_p
+        for fn in ("h3_ssm_discretize", "h3_ssm_kernel", "h3_fftconv", "h3_statepass_conv",
+                   "h3_layer_fwd", "h3_kernel_spectrum", "h3_fftconv_spectral"):
+            getattr(L, fn).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().h3_status_string(int(status)).decode()
+
+
+def workspace_size(op: int, B: int, H_or_d: int, L: int, m: int = 0, chunk: int = 0,
+                   dtype: int = F32) -> int:
+    return int(lib().h3_workspace_size(op, B, H_or_d, L, m, chunk, dtype))
+
+
+# ------------------------------------------------------------- helpers -----
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(dev: torch.device):
+    return ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+
+
+def _check(fn: str, status: int):
+    if status != 0:
+        raise H3Error(fn, status)
+
+
+def _cplx(t: torch.Tensor) -> torch.Tensor:
+    """complex64 or (..., 2) float32 -> contiguous (..., 2) float32."""
+    if t.is_complex():
+        t = torch.view_as_real(t.to(torch.complex64).contiguous())
+    if t.dtype != torch.float32 or t.shape[-1] != 2:
+        raise ValueError("complex parameters must be complex64 or float32 (..., 2)")
+    return t.contiguous()
+
+
+def _f32(t: Optional[torch.Tensor]) -> Optional[torch.Tensor]:
+    if t is None:
+        return None
+    return t.to(torch.float32).contiguous()
+
+
+def _dtype(t: torch.Tensor) -> int:
+    if t.dtype not in _DTYPES:
+        raise ValueError(f"unsupported dtype {t.dtype}")
+    return _DTYPES[t.dtype]
+
+
+def _workspace(nbytes: int, dev: torch.device, workspace: Optional[torch.Tensor]) -> torch.Tensor:
+    if workspace is not None:
+        if workspace.numel() * workspace.element_size() < nbytes:
+            raise ValueError("workspace too small")
+        return workspace
+    return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
+
+
+# ----------------------------------------------------------------- ops -----
+def ssm_discretize(A: torch.Tensor, B: torch.Tensor, dt: torch.Tensor):
+    """ZOH: Abar = exp(dt A), Bbar = (exp(dt A) - 1)/A * B.  Returns (Abar, Bbar)
+    as float32 (H, m, 2)."""
+    A, B, dt = _cplx(A), _cplx(B), _f32(dt)
+    H, m = A.shape[0], A.shape[1]
+    Ab = torch.empty_like(A); Bb = torch.empty_like(A)
+    _check("h3_ssm_discretize", lib().h3_ssm_discretize(
+        _ptr(A), _ptr(B), _ptr(dt), H, m, _ptr(Ab), _ptr(Bb), _stream(A.device)))
+    return Ab, Bb
+
+
+def ssm_kernel(A: torch.Tensor, B: torch.Tensor, C: torch.Tensor, dt: torch.Tensor, L: int,
+               out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """k[h, t] = 2 Re sum_n C Bbar exp(t dt A), (H, L) float32."""
+    A, B, C, dt = _cplx(A), _cplx(B), _cplx(C), _f32(dt)
+    H, m = A.shape[0], A.shape[1]
+    k = out if out is not None else torch.empty((H, L), dtype=torch.float32, device=A.device)
+    _check("h3_ssm_kernel", lib().h3_ssm_kernel(
+        _ptr(A), _ptr(B), _ptr(C), _ptr(dt), H, m, L, _ptr(k), _stream(A.device)))
+    return k
+
+
+def fftconv(u: torch.Tensor, k: torch.Tensor, D: Optional[torch.Tensor] = None,
+            out: Optional[torch.Tensor] = None,
+            workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """y = causal_conv(u, k) + D u over (B, H, L) rows, fused FFT."""
+    u = u.contiguous()
+    Bn, H, L = u.shape
+    k, D = _f32(k), _f32(D)
+    dt = _dtype(u)
+    y = out if out is not None else torch.empty_like(u)
+    ws = _workspace(workspace_size(OP_FFTCONV, Bn, H, L, 0, 0, dt), u.device, workspace)
+    _check("h3_fftconv", lib().h3_fftconv(
+        _ptr(u), _ptr(k), _ptr(D), _ptr(y), Bn, H, L, dt, _ptr(ws),
+        ws.numel() * ws.element_size(), _stream(u.device)))
+    return y
+
+
+def kernel_spectrum(k: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Kspec[h, f] = DFT_{2L}(k[h] zero-padded)[f] / 2L for f = 0..L; returns
+    float32 (H, L+1, 2)."""
+    k = _f32(k)
+    H, L = k.shape
+    K = out if out is not None else torch.empty((H, L + 1, 2), dtype=torch.float32, device=k.device)
+    _check("h3_kernel_spectrum", lib().h3_kernel_spectrum(_ptr(k), H, L, _ptr(K), _stream(k.device)))
+    return K
+
+
+def fftconv_spectral(u: torch.Tensor, Kspec: torch.Tensor, D: Optional[torch.Tensor] = None,
+                     out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Fused convolution given the kernel spectrum from kernel_spectrum."""
+    u = u.contiguous()
+    Bn, H, L = u.shape
+    D = _f32(D)
+    Kspec = _cplx(Kspec)
+    y = out if out is not None else torch.empty_like(u)
+    _check("h3_fftconv_spectral", lib().h3_fftconv_spectral(
+        _ptr(u), _ptr(Kspec), _ptr(D), _ptr(y), Bn, H, L, _dtype(u), _stream(u.device)))
+    return y
+
+
+def statepass_conv(u: torch.Tensor, Abar: torch.Tensor, Bbar: torch.Tensor, C: torch.Tensor,
+                   D: Optional[torch.Tensor], chunk: int, x0: Optional[torch.Tensor] = None,
+                   out: Optional[torch.Tensor] = None,
+                   workspace: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """State passing (Algorithm 2) for the diagonal SSM (Abar, Bbar, C, D).
+    Returns (y, x_final) with x_final float32 (B, H, m, 2)."""
+    u = u.contiguous()
+    Bn, H, L = u.shape
+    Abar, Bbar, C, D = _cplx(Abar), _cplx(Bbar), _cplx(C), _f32(D)
+    m = Abar.shape[1]
+    x0 = _cplx(x0) if x0 is not None else None
+    dt = _dtype(u)
+    y = out if out is not None else torch.empty_like(u)
+    xf = torch.empty((Bn, H, m, 2), dtype=torch.float32, device=u.device)
+    ws = _workspace(workspace_size(OP_STATEPASS, Bn, H, L, m, chunk, dt), u.device, workspace)
+    _check("h3_statepass_conv", lib().h3_statepass_conv(
+        _ptr(u), _ptr(Abar), _ptr(Bbar), _ptr(C), _ptr(D), _ptr(x0), Bn, H, L, m, chunk, dt,
+        _ptr(y), _ptr(xf), _ptr(ws), ws.numel() * ws.element_size(), _stream(u.device)))
+    return y, xf
+
+
+def layer_fwd(x: torch.Tensor, Wq: torch.Tensor, Wk: torch.Tensor, Wv: torch.Tensor,
+              Wo: torch.Tensor, shift_C: torch.Tensor, shift_D: Optional[torch.Tensor],
+              diag_k: torch.Tensor, diag_D: Optional[torch.Tensor],
+              out: Optional[torch.Tensor] = None,
+              workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """H3 layer forward (Algorithm 1, head dimension 1).  x: (B, L, d)."""
+    x = x.contiguous()
+    Bn, L, d = x.shape
+    dt = _dtype(x)
+    Ws = [w.to(x.dtype).contiguous() for w in (Wq, Wk, Wv, Wo)]
+    shift_C = _f32(shift_C)
+    m_s = shift_C.shape[1]
+    shift_D, diag_k, diag_D = _f32(shift_D), _f32(diag_k), _f32(diag_D)
+    o = out if out is not None else torch.empty_like(x)
+    ws = _workspace(workspace_size(OP_LAYER, Bn, d, L, m_s, 0, dt), x.device, workspace)
+    _check("h3_layer_fwd", lib().h3_layer_fwd(
+        _ptr(x), *[_ptr(w) for w in Ws], _ptr(shift_C), _ptr(shift_D), _ptr(diag_k),
+        _ptr(diag_D), Bn, L, d, m_s, dt, _ptr(o), _ptr(ws), ws.numel() * ws.element_size(),
+        _stream(x.device)))
+    return o

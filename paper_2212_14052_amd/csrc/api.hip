@@ -1,0 +1,245 @@
+// C ABI of libh3flash: argument validation and kernel dispatch.
+// Every check runs on the host before anything is enqueued.
+#include <stdint.h>
+
+#include "../../include/h3flash.h"
+#include "internal.h"
+
+using namespace h3;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool pow2_in(int x, int lo, int hi) { return x >= lo && x <= hi && (x & (x - 1)) == 0; }
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+size_t esize(int dtype) { return dtype == H3_F32 ? 4 : 2; }
+
+bool dtype_ok(int dtype) { return dtype == H3_F32 || dtype == H3_F16 || dtype == H3_BF16; }
+
+// [p, p + n) and [q, q + m) overlap?
+bool overlap(const void *p, size_t n, const void *q, size_t m) {
+    if (!p || !q || n == 0 || m == 0) return false;
+    uintptr_t a = (uintptr_t)p, b = (uintptr_t)q;
+    return a < b + m && b < a + n;
+}
+
+int launched(hipError_t e) { return e == hipSuccess ? H3_OK : H3_EDEVICE; }
+
+// Workspace layouts (each region 256-byte aligned).
+struct StatepassWs {
+    size_t k, kspec, states, corr_w, corr, total;
+};
+StatepassWs statepass_ws(int B, int H, int L, int m, int chunk) {
+    StatepassWs w;
+    const size_t nchunk = (size_t)(L / chunk);
+    w.k = 0;
+    w.kspec = w.k + align_up((size_t)H * chunk * sizeof(float));
+    w.states = w.kspec + align_up((size_t)H * (chunk + 1) * sizeof(float2));
+    w.corr_w = w.states + align_up((size_t)B * H * nchunk * m * sizeof(float2));
+    w.corr = w.corr_w + align_up((size_t)B * H * nchunk * m * sizeof(float2));
+    w.total = w.corr + align_up((size_t)B * H * L * sizeof(float));
+    return w;
+}
+
+struct LayerWs {
+    size_t wt_qkv, wt_o, qkv, o_cm, o_tm, kspec, total;
+};
+LayerWs layer_ws(int B, int d, int L) {
+    LayerWs w;
+    const size_t act = (size_t)B * d * L * 2;
+    w.wt_qkv = 0;
+    w.wt_o = w.wt_qkv + align_up((size_t)3 * d * d * 2);
+    w.qkv = w.wt_o + align_up((size_t)d * d * 2);
+    w.o_cm = w.qkv + align_up(3 * act);
+    w.o_tm = w.o_cm + align_up(act);
+    w.kspec = w.o_tm + align_up(act);
+    w.total = w.kspec + align_up((size_t)d * (L + 1) * sizeof(float2));
+    return w;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *h3_status_string(int status) {
+    switch (status) {
+        case H3_OK: return "ok";
+        case H3_EINVAL: return "invalid argument";
+        case H3_EUNSUPPORTED: return "unsupported size, mode count or dtype";
+        case H3_EWORKSPACE: return "workspace missing or too small";
+        case H3_EDEVICE: return "kernel launch failed";
+    }
+    return "unknown status";
+}
+
+size_t h3_workspace_size(int op, int B, int H, int L, int m, int chunk, int dtype) {
+    if (B < 1 || H < 1 || L < 1 || !dtype_ok(dtype)) return 0;
+    switch (op) {
+        case H3_OP_FFTCONV:
+            return align_up(fftconv_workspace(B, H, L));
+        case H3_OP_STATEPASS:
+            if (m < 1 || chunk < 1 || L % chunk) return 0;
+            return statepass_ws(B, H, L, m, chunk).total;
+        case H3_OP_LAYER:
+            return layer_ws(B, H, L).total;
+    }
+    return 0;
+}
+
+int h3_ssm_discretize(const float *A, const float *B, const float *dt, int H, int m, float *Abar,
+                      float *Bbar, void *stream) {
+    if (!A || !B || !dt || !Abar || !Bbar || H < 1 || m < 1) return H3_EINVAL;
+    if (m > H3_MAX_MODES) return H3_EUNSUPPORTED;
+    return launched(launch_discretize(A, B, dt, H, m, Abar, Bbar, (hipStream_t)stream));
+}
+
+int h3_ssm_kernel(const float *A, const float *B, const float *C, const float *dt, int H, int m,
+                  int L, float *k, void *stream) {
+    if (!A || !B || !C || !dt || !k || H < 1 || m < 1 || L < 1) return H3_EINVAL;
+    if (m > H3_MAX_MODES) return H3_EUNSUPPORTED;
+    return launched(launch_kernel_gen(0, A, B, C, dt, H, m, L, k, (hipStream_t)stream));
+}
+
+int h3_fftconv(const void *u, const float *k, const float *D, void *y, int B, int H, int L,
+               int dtype, void *workspace, size_t ws_bytes, void *stream) {
+    if (!u || !k || !y || B < 1 || H < 1 || L < 1) return H3_EINVAL;
+    if (!dtype_ok(dtype) || !pow2_in(L, H3_MIN_LEN, H3_FUSED_LIMIT)) return H3_EUNSUPPORTED;
+    const size_t io = (size_t)B * H * L * esize(dtype);
+    const size_t need = h3_workspace_size(H3_OP_FFTCONV, B, H, L, 0, 0, dtype);
+    if (!workspace || ws_bytes < need) return H3_EWORKSPACE;
+    if (!aligned16(u) || !aligned16(y) || !aligned16(k) || !aligned16(workspace)) return H3_EINVAL;
+    if (overlap(u, io, y, io) || overlap(workspace, need, u, io) || overlap(workspace, need, y, io) ||
+        overlap(workspace, need, k, (size_t)H * L * 4))
+        return H3_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    float2 *Kspec = (float2 *)workspace;
+    hipError_t e = launch_spectrum(k, H, L, Kspec, s);
+    if (e != hipSuccess) return H3_EDEVICE;
+    ConvArgs a{};
+    a.u = u; a.y = y; a.Kspec = Kspec; a.D = D;
+    a.B = B; a.H = H; a.L = L; a.nchunk = 1; a.pair_mode = 0; a.dtype = dtype;
+    a.corr = nullptr;
+    return launched(launch_fftconv(a, s));
+}
+
+int h3_kernel_spectrum(const float *k, int H, int L, float *Kspec, void *stream) {
+    if (!k || !Kspec || H < 1 || L < 1) return H3_EINVAL;
+    if (!pow2_in(L, H3_MIN_LEN, H3_FUSED_LIMIT)) return H3_EUNSUPPORTED;
+    if (!aligned16(k) || !aligned16(Kspec)) return H3_EINVAL;
+    if (overlap(k, (size_t)H * L * 4, Kspec, (size_t)H * (L + 1) * 8)) return H3_EINVAL;
+    return launched(launch_spectrum(k, H, L, (float2 *)Kspec, (hipStream_t)stream));
+}
+
+int h3_fftconv_spectral(const void *u, const float *Kspec, const float *D, void *y, int B, int H,
+                        int L, int dtype, void *stream) {
+    if (!u || !Kspec || !y || B < 1 || H < 1 || L < 1) return H3_EINVAL;
+    if (!dtype_ok(dtype) || !pow2_in(L, H3_MIN_LEN, H3_FUSED_LIMIT)) return H3_EUNSUPPORTED;
+    if (!aligned16(u) || !aligned16(y) || !aligned16(Kspec)) return H3_EINVAL;
+    const size_t io = (size_t)B * H * L * esize(dtype);
+    if (overlap(u, io, y, io) || overlap(Kspec, (size_t)H * (L + 1) * 8, y, io)) return H3_EINVAL;
+    ConvArgs a{};
+    a.u = u; a.y = y; a.Kspec = (const float2 *)Kspec; a.D = D;
+    a.B = B; a.H = H; a.L = L; a.nchunk = 1; a.pair_mode = 0; a.dtype = dtype;
+    a.corr = nullptr;
+    return launched(launch_fftconv(a, (hipStream_t)stream));
+}
+
+int h3_statepass_conv(const void *u, const float *Abar, const float *Bbar, const float *C,
+                      const float *D, const float *x0, int B, int H, int L, int m, int chunk,
+                      int dtype, void *y, float *x_final, void *workspace, size_t ws_bytes,
+                      void *stream) {
+    if (!u || !Abar || !Bbar || !C || !y || B < 1 || H < 1 || L < 1 || m < 1 || chunk < 1)
+        return H3_EINVAL;
+    if (L % chunk) return H3_EINVAL;
+    if (!dtype_ok(dtype) || m > H3_MAX_MODES || !pow2_in(chunk, H3_MIN_LEN, H3_FUSED_LIMIT))
+        return H3_EUNSUPPORTED;
+    const size_t io = (size_t)B * H * L * esize(dtype);
+    const size_t need = h3_workspace_size(H3_OP_STATEPASS, B, H, L, m, chunk, dtype);
+    if (!workspace || ws_bytes < need) return H3_EWORKSPACE;
+    if (!aligned16(u) || !aligned16(y) || !aligned16(workspace)) return H3_EINVAL;
+    const size_t xs = (size_t)B * H * m * 8;
+    if (overlap(u, io, y, io) || overlap(workspace, need, u, io) || overlap(workspace, need, y, io) ||
+        overlap(x_final, xs, y, io) || overlap(x_final, xs, u, io) || overlap(x_final, xs, workspace, need))
+        return H3_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    const int nchunk = L / chunk;
+    const StatepassWs w = statepass_ws(B, H, L, m, chunk);
+    char *ws = (char *)workspace;
+    float *kbuf = (float *)(ws + w.k);
+    float2 *Kspec = (float2 *)(ws + w.kspec);
+    float2 *states = (float2 *)(ws + w.states);
+    float2 *corr_W = (float2 *)(ws + w.corr_w);
+    float *corr = (float *)(ws + w.corr);
+    hipError_t e;
+    // f = [C Bbar, C Abar Bbar, ...] of length chunk, and its spectrum
+    if ((e = launch_kernel_gen(1, Abar, Bbar, C, nullptr, H, m, chunk, kbuf, s)) != hipSuccess) return H3_EDEVICE;
+    if ((e = launch_spectrum(kbuf, H, chunk, Kspec, s)) != hipSuccess) return H3_EDEVICE;
+    // s_c = M_ux u^(c) for every chunk, then the scan over chunks
+    if ((e = launch_chunk_states(u, Abar, Bbar, B, H, L, m, chunk, dtype, states, s)) != hipSuccess)
+        return H3_EDEVICE;
+    if ((e = launch_state_scan(Abar, C, x0, states, B, H, m, chunk, nchunk, corr_W, x_final, s)) !=
+        hipSuccess)
+        return H3_EDEVICE;
+    // M_xy x^(c) for every chunk
+    if ((e = launch_state_correction(Abar, corr_W, B, H, m, chunk, nchunk, corr, s)) != hipSuccess)
+        return H3_EDEVICE;
+    ConvArgs a{};
+    a.u = u; a.y = y; a.Kspec = Kspec; a.D = D;
+    a.B = B; a.H = H; a.L = chunk; a.nchunk = nchunk; a.pair_mode = 1; a.dtype = dtype;
+    a.corr = corr;
+    return launched(launch_fftconv(a, s));
+}
+
+int h3_layer_fwd(const void *x, const void *Wq, const void *Wk, const void *Wv, const void *Wo,
+                 const float *shift_C, const float *shift_D, const float *diag_k,
+                 const float *diag_D, int B, int L, int d, int m_s, int dtype, void *out,
+                 void *workspace, size_t ws_bytes, void *stream) {
+    if (!x || !Wq || !Wk || !Wv || !Wo || !shift_C || !diag_k || !out || B < 1 || L < 1 || d < 1 ||
+        m_s < 1)
+        return H3_EINVAL;
+    if ((dtype != H3_F16 && dtype != H3_BF16) || !pow2_in(L, H3_MIN_LEN, H3_FUSED_LIMIT) ||
+        d % 128 != 0 || ((long)B * L) % 128 != 0 || m_s > H3_MAX_SHIFT)
+        return H3_EUNSUPPORTED;
+    const size_t need = h3_workspace_size(H3_OP_LAYER, B, d, L, m_s, 0, dtype);
+    if (!workspace || ws_bytes < need) return H3_EWORKSPACE;
+    if (!aligned16(x) || !aligned16(out) || !aligned16(Wq) || !aligned16(Wk) || !aligned16(Wv) ||
+        !aligned16(Wo) || !aligned16(workspace))
+        return H3_EINVAL;
+    const size_t act = (size_t)B * L * d * 2;
+    if (overlap(x, act, out, act) || overlap(workspace, need, x, act) || overlap(workspace, need, out, act))
+        return H3_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    const LayerWs w = layer_ws(B, d, L);
+    char *ws = (char *)workspace;
+    char *wt_qkv = ws + w.wt_qkv;
+    void *wt_o = ws + w.wt_o;
+    char *qkv = ws + w.qkv;
+    void *o_cm = ws + w.o_cm;
+    void *o_tm = ws + w.o_tm;
+    float2 *Kspec = (float2 *)(ws + w.kspec);
+    const size_t wsz = (size_t)d * d * 2;
+    hipError_t e;
+    // Wt = W^T so that both GEMM operands are contiguous along the reduction
+    if ((e = launch_transpose_w(Wq, d, dtype, wt_qkv, s)) != hipSuccess) return H3_EDEVICE;
+    if ((e = launch_transpose_w(Wk, d, dtype, wt_qkv + wsz, s)) != hipSuccess) return H3_EDEVICE;
+    if ((e = launch_transpose_w(Wv, d, dtype, wt_qkv + 2 * wsz, s)) != hipSuccess) return H3_EDEVICE;
+    if ((e = launch_transpose_w(Wo, d, dtype, wt_o, s)) != hipSuccess) return H3_EDEVICE;
+    // [Q;K;V] (channel-major) = Wt_qkv . x^T
+    if ((e = launch_gemm_nt(wt_qkv, x, qkv, 3 * d, B * L, d, dtype, 1, d, L, s)) != hipSuccess)
+        return H3_EDEVICE;
+    if ((e = launch_spectrum(diag_k, d, L, Kspec, s)) != hipSuccess) return H3_EDEVICE;
+    const char *q = qkv, *kk = qkv + act, *v = qkv + 2 * act;
+    if ((e = launch_layer_mid(q, kk, v, shift_C, shift_D, m_s, Kspec, diag_D, B, d, L, dtype, o_cm,
+                              s)) != hipSuccess)
+        return H3_EDEVICE;
+    // O (B, d, L) -> (B, L, d), then out = O . Wo
+    if ((e = launch_transpose_batched(o_cm, o_tm, B, d, L, s)) != hipSuccess) return H3_EDEVICE;
+    return launched(launch_gemm_nt(o_tm, wt_o, out, B * L, d, d, dtype, 0, d, L, s));
+}
+
+}  // extern "C"

@@ -1,0 +1,62 @@
+// Internal launcher declarations of libh3flash (not part of the C ABI).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+
+#define H3_MAX_MODES_DEV 64
+
+namespace h3 {
+
+hipError_t launch_discretize(const float *A, const float *B, const float *dt, int H, int m,
+                             float *Abar, float *Bbar, hipStream_t s);
+// mode 0: P0 = A, P1 = B, dt used (continuous, ZOH).  mode 1: P0 = Abar, P1 = Bbar.
+hipError_t launch_kernel_gen(int mode, const float *P0, const float *P1, const float *C,
+                             const float *dt, int H, int m, int L, float *k, hipStream_t s);
+
+// Kernel spectra: Kspec[h][f] = (1/N) sum_{t<L} k[h][t] exp(-2 pi i f t / N),
+// f = 0..L, N = 2L.  Kspec: (H, L+1) float2.
+hipError_t launch_spectrum(const float *k, int H, int L, float2 *Kspec, hipStream_t s);
+
+// Fused FFT convolution over pairs of rows that share a channel.
+//   pair_mode 0: rows (b, h) of a (B, H, L) tensor, pairs (2j, 2j+1) along b.
+//   pair_mode 1: chunk rows of a (B, H, nchunk*L) tensor, pairs of
+//                consecutive chunks of one (b, h) row; corr (optional) holds the
+//                per-chunk initial-state correction inputs (see statepass).
+struct ConvArgs {
+    const void *u;
+    void *y;
+    const float2 *Kspec;   // (H, L+1)
+    const float *D;        // (H) or null
+    int B, H, L;           // L = convolution length (chunk length in mode 1)
+    int nchunk;            // mode 1: chunks per row
+    int pair_mode;
+    int dtype;
+    // state-passing initial-state term (mode 1 only, may be null):
+    // (B, H, nchunk * L) float32 added to the output
+    const float *corr;
+};
+hipError_t launch_fftconv(const ConvArgs &a, hipStream_t s);
+
+size_t fftconv_workspace(int B, int H, int L);
+
+// State passing pieces.
+hipError_t launch_chunk_states(const void *u, const float *Abar, const float *Bbar, int B, int H,
+                               int L, int m, int chunk, int dtype, float2 *states, hipStream_t s);
+hipError_t launch_state_scan(const float *Abar, const float *C, const float *x0,
+                             const float2 *states, int B, int H, int m, int chunk, int nchunk,
+                             float2 *corr_W, float *x_final, hipStream_t s);
+// corr[row, c*chunk + t] = 2 Re sum_n corr_W[row, c, n] Abar_n^t  (row = b*H + h)
+hipError_t launch_state_correction(const float *Abar, const float2 *corr_W, int B, int H, int m,
+                                   int chunk, int nchunk, float *corr, hipStream_t s);
+
+// Layer pieces.
+hipError_t launch_transpose_w(const void *W, int d, int dtype, void *Wt, hipStream_t s);
+hipError_t launch_transpose_batched(const void *in, void *out, int nb, int R, int C, hipStream_t s);
+hipError_t launch_gemm_nt(const void *A, const void *Bt, void *C, int M, int N, int K, int dtype,
+                          int out_mode, int d, int L, hipStream_t s);
+hipError_t launch_layer_mid(const void *q, const void *k, const void *v, const float *shift_C,
+                            const float *shift_D, int m_s, const float2 *Kspec,
+                            const float *diag_D, int B, int d, int L, int dtype, void *o,
+                            hipStream_t s);
+
+}  // namespace h3

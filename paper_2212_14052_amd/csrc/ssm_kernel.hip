@@ -1,0 +1,163 @@
+// SSM discretisation and convolution-kernel generation (gfx950).
+//
+// The kernel of a diagonal SSM (Sec. 2.1, f = [CB, CAB, CA^2B, ...]; diagonal A
+// as in Sec. 3.2) is evaluated as
+//     k[t] = 2 Re sum_n W_n exp(t lambda_n),   W_n = C_n Bbar_n,
+// with lambda_n = dt A_n (continuous parameters, ZOH) or lambda_n = log Abar_n
+// (discrete parameters).  Writing t = T a + b turns the sum into a small
+// complex matrix product  k[T a + b] = 2 Re sum_n P[a][n] Q[n][b]  with
+// P[a][n] = W_n exp(T a lambda_n) and Q[n][b] = exp(b lambda_n): only
+// (TT/T + T) * m complex exponentials per tile of TT outputs instead of TT * m,
+// each with its phase reduced in float64, and 2 FMAs per (output, mode).
+#include "common.h"
+#include "internal.h"
+
+namespace h3 {
+
+// Per-mode prologue: lambda (float64 complex) and W = C * Bbar (float32).
+// mode 0: continuous (A, B, dt) -> ZOH.  mode 1: discrete (Abar, Bbar).
+__device__ void mode_params(int mode, const float *P0, const float *P1, const float *C,
+                            const float *dt, int h, int m, int n, double2 *lam, float2 *W) {
+    long i = (long)h * m + n;
+    double cr = C[2 * i], ci = C[2 * i + 1];
+    double lr, li, br, bi;
+    if (mode == 0) {
+        double ar = P0[2 * i], ai = P0[2 * i + 1];
+        double bre = P1[2 * i], bim = P1[2 * i + 1];
+        double d = dt[h];
+        lr = d * ar; li = d * ai;
+        // exp(lambda) - 1 without cancellation for small |lambda|
+        double s = sin(li), hs = sin(0.5 * li);
+        double em1r = expm1(lr) * cos(li) - 2.0 * hs * hs;
+        double em1i = exp(lr) * s;
+        // (exp(lambda) - 1) / A
+        double den = ar * ar + ai * ai;
+        double qr = (em1r * ar + em1i * ai) / den;
+        double qi = (em1i * ar - em1r * ai) / den;
+        br = qr * bre - qi * bim;
+        bi = qr * bim + qi * bre;
+    } else {
+        double ar = P0[2 * i], ai = P0[2 * i + 1];
+        lr = 0.5 * log(ar * ar + ai * ai);
+        li = atan2(ai, ar);
+        br = P1[2 * i]; bi = P1[2 * i + 1];
+    }
+    *lam = make_double2(lr, li);
+    *W = make_float2((float)(cr * br - ci * bi), (float)(cr * bi + ci * br));
+}
+
+__global__ void discretize_kernel(const float *A, const float *B, const float *dt, int H, int m,
+                                  float *Abar, float *Bbar) {
+    int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= H * m) return;
+    int h = i / m;
+    double ar = A[2 * i], ai = A[2 * i + 1];
+    double bre = B[2 * i], bim = B[2 * i + 1];
+    double d = dt[h];
+    double lr = d * ar, li = d * ai;
+    double e = exp(lr);
+    double s = sin(li), hs = sin(0.5 * li);
+    Abar[2 * i] = (float)(e * cos(li));
+    Abar[2 * i + 1] = (float)(e * s);
+    double em1r = expm1(lr) * cos(li) - 2.0 * hs * hs;
+    double em1i = e * s;
+    double den = ar * ar + ai * ai;
+    double qr = (em1r * ar + em1i * ai) / den;
+    double qi = (em1i * ar - em1r * ai) / den;
+    Bbar[2 * i] = (float)(qr * bre - qi * bim);
+    Bbar[2 * i + 1] = (float)(qr * bim + qi * bre);
+}
+
+// One workgroup: one channel h, a tile of KG_TT outputs starting at t0.
+constexpr int KG_T = 32;                  // inner factor (b < KG_T)
+constexpr int KG_TT = 2048;               // outputs per workgroup
+constexpr int KG_A = KG_TT / KG_T;        // 64 outer steps per tile
+constexpr int KG_THREADS = 256;
+
+// mode 0/1: output row = channel h, W and lambda from the SSM parameters.
+// mode 2: output row o (o = row * div + chunk), channel (o / div) % H,
+//         lambda = log Abar (P0) of that channel and W given per output row in P1.
+__global__ __launch_bounds__(KG_THREADS) void kernel_gen(int mode, const float *P0, const float *P1,
+                                                         const float *C, const float *dt, int H,
+                                                         int m, int L, float *k, int div) {
+    __shared__ double2 lam_s[H3_MAX_MODES_DEV];
+    __shared__ float2 W_s[H3_MAX_MODES_DEV];
+    __shared__ float2 Q_s[H3_MAX_MODES_DEV][KG_T];       // exp(b lambda_n)
+    __shared__ float2 P_s[KG_A][H3_MAX_MODES_DEV + 1];   // W_n exp((t0 + T a) lambda_n)
+    const int ntile = (L + KG_TT - 1) / KG_TT;
+    const int orow = blockIdx.x / ntile;
+    const int t0 = (blockIdx.x % ntile) * KG_TT;
+    const int tid = threadIdx.x;
+    if (tid < m) {
+        if (mode < 2) {
+            mode_params(mode, P0, P1, C, dt, orow, m, tid, &lam_s[tid], &W_s[tid]);
+        } else {
+            const int h = (orow / div) % H;
+            const long i = (long)h * m + tid;
+            const double ar = P0[2 * i], ai = P0[2 * i + 1];
+            lam_s[tid] = make_double2(0.5 * log(ar * ar + ai * ai), atan2(ai, ar));
+            const long w = (long)orow * m + tid;
+            W_s[tid] = make_float2(P1[2 * w], P1[2 * w + 1]);
+        }
+    }
+    __syncthreads();
+    for (int i = tid; i < m * KG_T; i += KG_THREADS) {
+        int n = i / KG_T, b = i % KG_T;
+        double2 l = lam_s[n];
+        Q_s[n][b] = cexp_scaled((double)b, l.x, l.y);
+    }
+    for (int i = tid; i < m * KG_A; i += KG_THREADS) {
+        int a = i / m, n = i % m;
+        double2 l = lam_s[n];
+        P_s[a][n] = cmul(W_s[n], cexp_scaled((double)(t0 + KG_T * a), l.x, l.y));
+    }
+    __syncthreads();
+    // thread -> (b, 8 consecutive a)
+    const int b = tid % KG_T;
+    const int a0 = (tid / KG_T) * 8;
+    float acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = 0.f;
+    for (int n = 0; n < m; ++n) {
+        float2 q = Q_s[n][b];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            float2 p = P_s[a0 + j][n];
+            acc[j] = fmaf(p.x, q.x, acc[j]);
+            acc[j] = fmaf(-p.y, q.y, acc[j]);
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        int t = t0 + KG_T * (a0 + j) + b;
+        if (t < L) k[(long)orow * L + t] = 2.f * acc[j];
+    }
+}
+
+hipError_t launch_discretize(const float *A, const float *B, const float *dt, int H, int m,
+                             float *Abar, float *Bbar, hipStream_t s) {
+    int n = H * m;
+    hipLaunchKernelGGL(discretize_kernel, dim3((n + 255) / 256), dim3(256), 0, s, A, B, dt, H, m,
+                       Abar, Bbar);
+    return hipGetLastError();
+}
+
+hipError_t launch_kernel_gen(int mode, const float *P0, const float *P1, const float *C,
+                             const float *dt, int H, int m, int L, float *k, hipStream_t s) {
+    const long ntile = (L + KG_TT - 1) / KG_TT;
+    hipLaunchKernelGGL(kernel_gen, dim3((unsigned)(ntile * H)), dim3(KG_THREADS), 0, s, mode, P0, P1,
+                       C, dt, H, m, L, k, 1);
+    return hipGetLastError();
+}
+
+hipError_t launch_state_correction(const float *Abar, const float2 *corr_W, int B, int H, int m,
+                                   int chunk, int nchunk, float *corr, hipStream_t s) {
+    const long ntile = (chunk + KG_TT - 1) / KG_TT;
+    const long orows = (long)B * H * nchunk;
+    hipLaunchKernelGGL(kernel_gen, dim3((unsigned)(ntile * orows)), dim3(KG_THREADS), 0, s, 2, Abar,
+                       (const float *)corr_W, (const float *)nullptr, (const float *)nullptr, H, m,
+                       chunk, corr, nchunk);
+    return hipGetLastError();
+}
+
+}  // namespace h3

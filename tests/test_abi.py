@@ -1,0 +1,124 @@
+"""C ABI checks that need no GPU: the library loads, exports every function
+the header declares, sizes its workspaces, and rejects invalid arguments with
+the documented status before launching anything."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "h3flash.h")
+
+import paper_2212_14052_amd as h3
+
+OK, EINVAL, EUNSUP, EWS = 0, -1, -2, -3
+P = lambda v: ctypes.c_void_p(v)
+U, K, Y, W, X = 0x100000, 0x4000000, 0x8000000, 0xC000000, 0x10000000   # fake, aligned
+
+
+def declared_functions():
+    txt = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(h3_\w+)\s*\(", txt, re.M)))
+
+
+def test_library_exports_every_declared_function():
+    L = h3.lib()
+    names = declared_functions()
+    assert len(names) >= 7
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_status_strings():
+    assert h3.status_string(0) == "ok"
+    for s in (-1, -2, -3, -4):
+        assert h3.status_string(s) not in ("ok", "unknown status")
+    assert h3.status_string(7) == "unknown status"
+
+
+def test_workspace_sizes():
+    ws = h3.workspace_size(h3.OP_FFTCONV, 8, 768, 2048, 0, 0, h3.F16)
+    assert ws >= 768 * 2049 * 8
+    ws = h3.workspace_size(h3.OP_STATEPASS, 2, 1024, 131072, 64, 8192, h3.F16)
+    assert ws >= 2 * 1024 * 16 * 64 * 8 * 2
+    assert h3.workspace_size(h3.OP_STATEPASS, 2, 4, 100, 64, 64, h3.F16) == 0   # L % chunk
+    assert h3.workspace_size(99, 1, 1, 16, 0, 0, 0) == 0
+    assert h3.workspace_size(h3.OP_FFTCONV, 1, 1, 16, 0, 0, 7) == 0
+    assert h3.workspace_size(h3.OP_LAYER, 4, 2560, 2048, 64, 0, h3.BF16) > 4 * 2560 * 2048 * 2 * 5
+
+
+def fftconv(u=U, k=K, D=None, y=Y, B=2, H=4, L=64, dt=0, ws=W, wsb=1 << 24):
+    return h3.lib().h3_fftconv(P(u), P(k), P(D), P(y), B, H, L, dt, P(ws), wsb, None)
+
+
+def test_fftconv_validation():
+    assert fftconv(u=0) == EINVAL
+    assert fftconv(k=0) == EINVAL
+    assert fftconv(y=0) == EINVAL
+    assert fftconv(B=0) == EINVAL
+    assert fftconv(L=48) == EUNSUP                  # not a power of two
+    assert fftconv(L=8) == EUNSUP                   # below the minimum
+    assert fftconv(L=16384) == EUNSUP               # above the fused limit
+    assert fftconv(dt=3) == EUNSUP
+    assert fftconv(ws=0) == EWS
+    assert fftconv(wsb=16) == EWS
+    assert fftconv(u=U + 2) == EINVAL               # misaligned
+    assert fftconv(y=U + 64) == EINVAL              # overlaps u
+    assert fftconv(ws=U + 256) == EINVAL            # workspace overlaps u
+
+
+def statepass(u=U, A=K, Bb=K + 4096, C=K + 8192, D=None, x0=None, B=2, H=4, L=256, m=64,
+              chunk=64, dt=1, y=Y, xf=None, ws=W, wsb=1 << 26):
+    return h3.lib().h3_statepass_conv(P(u), P(A), P(Bb), P(C), P(D), P(x0), B, H, L, m, chunk, dt,
+                                      P(y), P(xf), P(ws), wsb, None)
+
+
+def test_statepass_validation():
+    assert statepass(u=0) == EINVAL
+    assert statepass(A=0) == EINVAL
+    assert statepass(L=250) == EINVAL               # chunk does not divide L
+    assert statepass(chunk=48, L=96) == EUNSUP
+    assert statepass(chunk=16384, L=16384) == EUNSUP
+    assert statepass(m=65) == EUNSUP
+    assert statepass(m=0) == EINVAL
+    assert statepass(dt=5) == EUNSUP
+    assert statepass(ws=0) == EWS
+    assert statepass(wsb=100) == EWS
+    assert statepass(y=U) == EINVAL                 # y aliases u
+    assert statepass(xf=Y + 16) == EINVAL           # x_final inside y
+
+
+def layer(x=U, B=2, L=64, d=128, m_s=64, dt=2, out=Y, ws=W, wsb=1 << 26, shift=K, diag=K + 65536):
+    return h3.lib().h3_layer_fwd(P(x), P(K), P(K), P(K), P(K), P(shift), None, P(diag), None,
+                                 B, L, d, m_s, dt, P(out), P(ws), wsb, None)
+
+
+def test_layer_validation():
+    assert layer(x=0) == EINVAL
+    assert layer(shift=0) == EINVAL
+    assert layer(dt=0) == EUNSUP                    # fp32 layer not built
+    assert layer(d=100) == EUNSUP
+    assert layer(m_s=65) == EUNSUP
+    assert layer(L=100) == EUNSUP
+    assert layer(B=1, L=64) == EUNSUP               # B*L not a multiple of 128
+    assert layer(ws=0) == EWS
+    assert layer(out=U) == EINVAL
+
+
+def test_discretize_and_kernel_validation():
+    L = h3.lib()
+    assert L.h3_ssm_discretize(None, P(K), P(K), 4, 8, P(Y), P(Y), None) == EINVAL
+    assert L.h3_ssm_discretize(P(K), P(K), P(K), 4, 65, P(Y), P(Y), None) == EUNSUP
+    assert L.h3_ssm_kernel(P(K), P(K), P(K), P(K), 4, 8, 0, P(Y), None) == EINVAL
+    assert L.h3_ssm_kernel(P(K), P(K), P(K), P(K), 4, 70, 16, P(Y), None) == EUNSUP
+
+
+def test_spectral_validation():
+    L = h3.lib()
+    assert L.h3_kernel_spectrum(None, 4, 64, P(Y), None) == EINVAL
+    assert L.h3_kernel_spectrum(P(K), 4, 100, P(Y), None) == EUNSUP
+    assert L.h3_kernel_spectrum(P(K), 4, 64, P(K + 64), None) == EINVAL      # overlap
+    assert L.h3_fftconv_spectral(P(U), P(K), None, P(U), 2, 4, 64, 0, None) == EINVAL
+    assert L.h3_fftconv_spectral(P(U), P(K), None, P(Y), 2, 4, 64, 9, None) == EUNSUP
+    assert L.h3_fftconv_spectral(P(U), P(K), None, P(Y), 2, 4, 32768, 1, None) == EUNSUP

@@ -1,0 +1,246 @@
+"""GPU parity: the HIP path (through the C ABI) against the float64 oracle on
+the same seeded, rounded inputs.
+
+Metric: err = max|y - y_oracle| / max|y_oracle| per output tensor.  Gates:
+1e-5 for float32 I/O, 2e-2 for fp16/bf16 I/O (fp32 accumulation).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from tests._util import cplx64, cplx_to_f32pairs, f32dev, rel_err, to_dev, to_np64
+
+pytestmark = pytest.mark.gpu
+
+TOL = {workloads.F32: 1e-5, workloads.F16: 2e-2, workloads.BF16: 2e-2}
+
+
+@pytest.fixture(scope="module")
+def h3():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2212_14052_amd as m
+    m.lib()
+    return m
+
+
+def _diag_params(w):
+    A, B, C, dt = w.ssm.complex64()
+    return A, B, C, dt
+
+
+# ------------------------------------------------------------ S1: kernel ---
+def test_discretize(h3):
+    w = workloads.config(0)
+    A, B, C, dt = _diag_params(w)
+    Ab, Bb = h3.ssm_discretize(f32dev(w.ssm.A), f32dev(w.ssm.B), f32dev(w.ssm.dt))
+    rA, rB = oracle.zoh(A, B, dt)
+    assert np.abs(cplx64(to_np64(Ab)) - rA).max() < 1e-6
+    assert rel_err(cplx64(to_np64(Bb)).view(np.float64), rB.view(np.float64)) < 1e-6
+
+
+@pytest.mark.parametrize("L,dt_lo,dt_hi", [(1024, 1e-3, 1e-1), (100, 1e-3, 1e-1), (8192, 1e-4, 1e-1),
+                                           (2049, 1e-2, 1e-1), (16, 1e-3, 1e-1)])
+def test_ssm_kernel(h3, L, dt_lo, dt_hi):
+    w = workloads.config(0, H=16, L=16, seed=7, dt_lo=dt_lo, dt_hi=dt_hi)
+    A, B, C, dt = _diag_params(w)
+    k = h3.ssm_kernel(f32dev(w.ssm.A), f32dev(w.ssm.B), f32dev(w.ssm.C), f32dev(w.ssm.dt), L)
+    ref = oracle.ssm_kernel(A, B, C, dt, L)
+    assert rel_err(to_np64(k), ref) < 2e-6
+
+
+# --------------------------------------------------------- S2-S4: conv ---
+def _conv_case(h3, B, H, L, dtype, seed, dt_lo=1e-3, dt_hi=1e-1, with_D=True):
+    w = workloads.conv_workload("t", B, H, L, dtype, seed, dt_lo=dt_lo, dt_hi=dt_hi)
+    A, Bm, C, dt = _diag_params(w)
+    k64 = oracle.ssm_kernel(A, Bm, C, dt, L)
+    k32 = k64.astype(np.float32)
+    D = w.D if with_D else None
+    y = h3.fftconv(to_dev(w.u, dtype), f32dev(k32), f32dev(D) if with_D else None)
+    torch.cuda.synchronize()
+    ref = oracle.causal_conv(w.u64, k32.astype(np.float64), D.astype(np.float64) if with_D else None)
+    return to_np64(y), ref
+
+
+@pytest.mark.parametrize("L", [16, 32, 64, 128, 256, 512, 1024, 2048, 4096, 8192])
+def test_fftconv_f32_all_lengths(h3, L):
+    y, ref = _conv_case(h3, 3, 5, L, workloads.F32, seed=L)
+    assert rel_err(y, ref) < TOL[workloads.F32]
+
+
+@pytest.mark.parametrize("dtype", [workloads.F16, workloads.BF16])
+@pytest.mark.parametrize("L", [16, 256, 2048, 8192])
+def test_fftconv_16bit(h3, dtype, L):
+    y, ref = _conv_case(h3, 4, 3, L, dtype, seed=L + 1, dt_lo=1e-4)
+    # compare against the oracle rounded to the output dtype as well
+    assert rel_err(y, ref) < TOL[dtype]
+
+
+def test_fftconv_no_skip_odd_batch(h3):
+    y, ref = _conv_case(h3, 1, 7, 512, workloads.F32, seed=3, with_D=False)
+    assert rel_err(y, ref) < 1e-5
+
+
+def test_fftconv_impulse_returns_kernel(h3):
+    H, L = 4, 1024
+    rng = np.random.default_rng(0)
+    k = rng.standard_normal((H, L)).astype(np.float32) * np.exp(-np.arange(L) / 300).astype(np.float32)
+    u = np.zeros((2, H, L), np.float32); u[:, :, 0] = 1.0
+    y = to_np64(h3.fftconv(f32dev(u), f32dev(k), None))
+    assert rel_err(y[0], k) < 1e-5 and rel_err(y[1], k) < 1e-5
+
+
+def test_fftconv_causality(h3):
+    H, L = 2, 2048
+    rng = np.random.default_rng(1)
+    k = rng.standard_normal((H, L)).astype(np.float32)
+    u = rng.standard_normal((2, H, L)).astype(np.float32)
+    y0 = to_np64(h3.fftconv(f32dev(u), f32dev(k), None))
+    u2 = u.copy(); u2[:, :, 1500] += 100.0
+    y1 = to_np64(h3.fftconv(f32dev(u2), f32dev(k), None))
+    # outputs before the perturbation move only by rounding noise of the FFT
+    assert np.abs(y1[..., :1500] - y0[..., :1500]).max() < 1e-4 * np.abs(y0).max()
+    assert np.abs(y1[..., 1500:] - y0[..., 1500:]).max() > 1.0
+
+
+def test_fftconv_deterministic(h3):
+    w = workloads.config(1, B=4, H=16, L=2048)
+    u = to_dev(w.u, w.dtype)
+    k = f32dev(np.random.default_rng(2).standard_normal((16, 2048)).astype(np.float32) * 0.01)
+    a = h3.fftconv(u, k, f32dev(w.D))
+    b = h3.fftconv(u, k, f32dev(w.D))
+    assert torch.equal(a, b)
+
+
+def _end_to_end_conv(h3, w, rows):
+    """S1 -> S2/S3 on the GPU at full size; oracle on the sampled rows."""
+    k = h3.ssm_kernel(f32dev(w.ssm.A), f32dev(w.ssm.B), f32dev(w.ssm.C), f32dev(w.ssm.dt), w.L)
+    y = h3.fftconv(to_dev(w.u, w.dtype), k, f32dev(w.D))
+    torch.cuda.synchronize()
+    A, B, C, dt = _diag_params(w)
+    y = y.view(w.B * w.H, w.L)
+    errs = []
+    ysel = to_np64(y[torch.tensor(rows, device=y.device)])
+    for i, r in enumerate(rows):
+        b, h = divmod(r, w.H)
+        kh = oracle.ssm_kernel(A[h:h + 1], B[h:h + 1], C[h:h + 1], dt[h:h + 1], w.L)
+        ref = oracle.causal_conv(w.u64[b, h][None, None], kh, np.array([w.D[h]], np.float64))
+        errs.append((ysel[i], ref[0, 0]))
+    ya = np.stack([e[0] for e in errs]); ra = np.stack([e[1] for e in errs])
+    return rel_err(ya, ra)
+
+
+def test_config0_end_to_end_f32(h3):
+    w = workloads.config(0)
+    err = _end_to_end_conv(h3, w, list(range(w.B * w.H)))
+    assert err < 1e-5, err
+
+
+def test_config1_full_size_sampled_rows(h3):
+    w = workloads.config(1)
+    rng = np.random.default_rng(11)
+    rows = sorted(rng.choice(w.B * w.H, 24, replace=False).tolist()) + [0, w.B * w.H - 1]
+    err = _end_to_end_conv(h3, w, rows)
+    assert err < 2e-2, err
+
+
+def test_config2_full_size_sampled_rows(h3):
+    w = workloads.config(2)
+    rng = np.random.default_rng(12)
+    rows = sorted(rng.choice(w.B * w.H, 12, replace=False).tolist()) + [w.B * w.H - 1]
+    err = _end_to_end_conv(h3, w, rows)
+    assert err < 2e-2, err
+
+
+# --------------------------------------------------------- S5: statepass ---
+def _sp_inputs(w):
+    A, B, C, dt = _diag_params(w)
+    Ab, Bb = oracle.zoh(A, B, dt)
+    # the GPU consumes fp32 discrete parameters; the oracle the same rounded values
+    Ab32, Bb32 = cplx_to_f32pairs(Ab), cplx_to_f32pairs(Bb)
+    return Ab32, Bb32, cplx64(Ab32), cplx64(Bb32), C
+
+
+@pytest.mark.parametrize("dtype,L,chunk", [(workloads.F32, 1024, 128), (workloads.F32, 512, 512),
+                                           (workloads.F16, 2048, 256), (workloads.BF16, 1024, 16),
+                                           (workloads.F32, 256, 16)])
+def test_statepass_small(h3, dtype, L, chunk):
+    w = workloads.statepass_workload("t", 3, 5, L, chunk, dtype, seed=L + chunk, dt_lo=1e-3,
+                                     dt_hi=1e-1, x0_scale=0.5)
+    Ab32, Bb32, Ab, Bb, C = _sp_inputs(w)
+    x0 = cplx64(w.x0)
+    y, xf = h3.statepass_conv(to_dev(w.u, dtype), f32dev(Ab32), f32dev(Bb32), f32dev(w.ssm.C),
+                              f32dev(w.D), chunk, x0=f32dev(w.x0))
+    torch.cuda.synchronize()
+    ry, rx = oracle.recurrence(w.u64, Ab, Bb, C, w.D.astype(np.float64), x0=x0)
+    assert rel_err(to_np64(y), ry) < TOL[dtype]
+    xg = cplx64(to_np64(xf))
+    assert np.abs(xg - rx).max() / np.abs(rx).max() < (1e-5 if dtype == workloads.F32 else 2e-2)
+
+
+def test_statepass_resume(h3):
+    w = workloads.statepass_workload("t", 2, 3, 1024, 128, workloads.F32, seed=5, dt_lo=1e-3, dt_hi=1e-1)
+    Ab32, Bb32, Ab, Bb, C = _sp_inputs(w)
+    u = f32dev(w.u)
+    args = (f32dev(Ab32), f32dev(Bb32), f32dev(w.ssm.C), f32dev(w.D))
+    y, xf = h3.statepass_conv(u, *args, 128)
+    y1, x1 = h3.statepass_conv(u[..., :512].contiguous(), *args, 128)
+    y2, x2 = h3.statepass_conv(u[..., 512:].contiguous(), *args, 256, x0=x1)
+    torch.cuda.synchronize()
+    assert rel_err(to_np64(torch.cat([y1, y2], -1)), to_np64(y)) < 1e-5
+    assert rel_err(to_np64(x2), to_np64(xf)) < 1e-5
+
+
+def test_config3_full_size_sampled_rows(h3):
+    w = workloads.config(3)
+    Ab32, Bb32, Ab, Bb, C = _sp_inputs(w)
+    y, xf = h3.statepass_conv(to_dev(w.u, w.dtype), f32dev(Ab32), f32dev(Bb32), f32dev(w.ssm.C),
+                              f32dev(w.D), w.chunk)
+    torch.cuda.synchronize()
+    rows = [0, 777, 1024 + 5, 2 * 1024 - 1]
+    y = y.view(w.B * w.H, w.L)
+    xf = xf.view(w.B * w.H, w.m, 2)
+    ys, rs, xs, rxs = [], [], [], []
+    for r in rows:
+        b, h = divmod(r, w.H)
+        ry, rx = oracle.recurrence(w.u64[b, h][None, None], Ab[h:h + 1], Bb[h:h + 1], C[h:h + 1],
+                                   w.D[h:h + 1].astype(np.float64))
+        ys.append(to_np64(y[r])); rs.append(ry[0, 0])
+        xs.append(cplx64(to_np64(xf[r]))); rxs.append(rx[0, 0])
+    assert rel_err(np.stack(ys), np.stack(rs)) < 2e-2
+    xs, rxs = np.stack(xs), np.stack(rxs)
+    assert np.abs(xs - rxs).max() / np.abs(rxs).max() < 2e-2
+
+
+# ------------------------------------------------------------- S6: layer ---
+def _layer_case(h3, w, b_sel=None):
+    d, L = w.d, w.L
+    A, B, C, dt = w.diag.complex64()
+    k64 = oracle.ssm_kernel(A, B, C, dt, L)
+    k32 = k64.astype(np.float32)
+    W = {n: to_dev(w.W[n][0], w.dtype) for n in "qkvo"}
+    out = h3.layer_fwd(to_dev(w.x, w.dtype), W["q"], W["k"], W["v"], W["o"], f32dev(w.shift_C), None,
+                       f32dev(k32), f32dev(w.diag_D))
+    torch.cuda.synchronize()
+    bs = list(range(w.B)) if b_sel is None else b_sel
+    ref = oracle.h3_layer(w.x64[bs], w.W["q"][1], w.W["k"][1], w.W["v"][1], w.W["o"][1],
+                          w.shift_C.astype(np.float64), k32.astype(np.float64),
+                          w.diag_D.astype(np.float64))
+    return to_np64(out[bs]), ref
+
+
+@pytest.mark.parametrize("dtype", [workloads.BF16, workloads.F16])
+def test_layer_small(h3, dtype):
+    w = workloads.layer_workload("t", 2, 256, 256, dtype, seed=21)
+    y, ref = _layer_case(h3, w)
+    assert rel_err(y, ref) < 2e-2
+
+
+def test_layer_config4_one_batch_element(h3):
+    w = workloads.config(4)
+    y, ref = _layer_case(h3, w, b_sel=[3])
+    assert rel_err(y, ref) < 2e-2
