@@ -243,15 +243,27 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-extra", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run a 512 MiB device-to-device copy 5 times (calibrates the "
+                         "FETCH_SIZE / WRITE_SIZE counters against a known byte count)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
               "(the hot path shards trivially over rows, see DESIGN.md)", file=sys.stderr)
         sys.exit(2)
     import torch
-    import paper_2212_14052_amd as h3
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.copy_probe:
+        n = 512 * 2 ** 20
+        src = torch.ones(n // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": n, "reps": 5}))
+        return
+    import paper_2212_14052_amd as h3
     h3.lib()
     head = bench_headline(h3, args.steps, args.warmup, dev)
     print(f"# headline done: {head['ms_per_step']*1e3:.1f} us/step", file=sys.stderr, flush=True)
