@@ -3,8 +3,9 @@
 
 Step (the headline): the H3-125M-shaped diagonal-SSM convolution, B=8, H=768,
 L=2048, fp16 I/O with fp32 arithmetic: kernel generation from the SSM
-parameters (h3_ssm_kernel), kernel spectrum (h3_kernel_spectrum) and the fused
-FFT convolution with skip term (h3_fftconv_spectral).  Inputs are resident in
+parameters (h3_ssm_kernel) and the fused FFT convolution with skip term
+(h3_fftconv: kernel spectrum, block FFT, pointwise product, inverse, skip, all
+in one kernel for this shape).  Inputs are resident in
 HBM; K steps rotate over enough input/output buffer sets (>= 512 MB) that
 every step reads u and writes y cold (not from the 256 MB Infinity Cache).
 
@@ -70,7 +71,7 @@ class EventTimer:
 
 
 def bench_headline(h3, steps, warmup, dev):
-    """Config 1 step: kernel gen + spectrum + fused conv (diagonal SSM)."""
+    """Config 1 step: kernel generation + fused FFT conv (diagonal SSM)."""
     import torch
     import workloads
     w = workloads.config(1)
@@ -83,21 +84,20 @@ def bench_headline(h3, steps, warmup, dev):
     A, Bp, C, dt = (_f32(w.ssm.A, dev), _f32(w.ssm.B, dev), _f32(w.ssm.C, dev), _f32(w.ssm.dt, dev))
     D = _f32(w.D, dev)
     k = torch.empty((H, L), dtype=torch.float32, device=dev)
-    K = torch.empty((H, L + 1, 2), dtype=torch.float32, device=dev)
+    ws = torch.empty(max(256, h3.workspace_size(h3.OP_FFTCONV, B, H, L, 0, 0, h3.F16)),
+                     dtype=torch.uint8, device=dev)
 
     def one(i, ev=None):
         if ev: ev[0].record()
         h3.ssm_kernel(A, Bp, C, dt, L, out=k)
         if ev: ev[1].record()
-        h3.kernel_spectrum(k, out=K)
+        h3.fftconv(us[i % nsets], k, D, out=ys[i % nsets], workspace=ws)
         if ev: ev[2].record()
-        h3.fftconv_spectral(us[i % nsets], K, D, out=ys[i % nsets])
-        if ev: ev[3].record()
 
     for i in range(warmup):
         one(i)
     torch.cuda.synchronize()
-    timer = EventTimer(["ssm_kernel", "kernel_spectrum", "fftconv"])
+    timer = EventTimer(["ssm_kernel", "fftconv"])
     t0 = torch.cuda.Event(enable_timing=True); t1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0.record()
@@ -108,8 +108,9 @@ def bench_headline(h3, steps, warmup, dev):
     total_ms = t0.elapsed_time(t1)
     per = timer.averages()
     ms = total_ms / steps
+    # u + y (fp16) + k (fp32, once per channel) + D
     step_bytes = B * H * L * (2 + 2) + H * L * 4 + H * 4
-    conv_bytes = B * H * L * (2 + 2) + H * (L + 1) * 8 + H * 4
+    conv_bytes = step_bytes
     conv_gbs = conv_bytes / (per["fftconv"] * 1e-3) / 1e9
     return {
         "w": w, "ms_per_step": ms, "step_bytes": step_bytes,
@@ -149,9 +150,8 @@ def bench_extra(h3, dev, reps=10, warm=3):
     us = [u] + [u.clone() for _ in range(nsets - 1)]
     ys = [torch.empty_like(u) for _ in range(nsets)]
     D = _f32(w.D, dev)
-    K = torch.empty((H, L + 1, 2), dtype=torch.float32, device=dev)
-    ms = _time_calls(lambda i: (h3.kernel_spectrum(ks, out=K),
-                                h3.fftconv_spectral(us[i % nsets], K, D, out=ys[i % nsets])), reps, warm)
+    ws = torch.empty(h3.workspace_size(h3.OP_FFTCONV, B, H, L, 0, 0, h3.F16), dtype=torch.uint8, device=dev)
+    ms = _time_calls(lambda i: h3.fftconv(us[i % nsets], ks, D, out=ys[i % nsets], workspace=ws), reps, warm)
     by = B * H * L * 4 + H * L * 4 + H * 4
     ex["cfg1_shift_conv"] = {"ms": ms, "GB_s": by / ms / 1e6, "pct_hbm_peak": 100 * by / ms / 1e6 / HBM_PEAK_GBS}
     del us, ys
@@ -166,9 +166,9 @@ def bench_extra(h3, dev, reps=10, warm=3):
     A, Bp, C, dt = (_f32(w.ssm.A, dev), _f32(w.ssm.B, dev), _f32(w.ssm.C, dev), _f32(w.ssm.dt, dev))
     D = _f32(w.D, dev)
     k = torch.empty((H, L), dtype=torch.float32, device=dev)
-    K = torch.empty((H, L + 1, 2), dtype=torch.float32, device=dev)
-    ms = _time_calls(lambda i: (h3.ssm_kernel(A, Bp, C, dt, L, out=k), h3.kernel_spectrum(k, out=K),
-                                h3.fftconv_spectral(us[i % nsets], K, D, out=ys[i % nsets])), reps, warm)
+    ws = torch.empty(h3.workspace_size(h3.OP_FFTCONV, B, H, L, 0, 0, h3.BF16), dtype=torch.uint8, device=dev)
+    ms = _time_calls(lambda i: (h3.ssm_kernel(A, Bp, C, dt, L, out=k),
+                                h3.fftconv(us[i % nsets], k, D, out=ys[i % nsets], workspace=ws)), reps, warm)
     by = B * H * L * 4 + H * L * 4 + H * 4
     ex["cfg2_fused_limit_bf16"] = {"ms": ms, "GB_s": by / ms / 1e6, "pct_hbm_peak": 100 * by / ms / 1e6 / HBM_PEAK_GBS,
                                    "gelem_per_s": B * H * L / ms / 1e6}
@@ -213,9 +213,9 @@ def bench_extra(h3, dev, reps=10, warm=3):
     A, Bp, C, dt = (_f32(w.ssm.A, dev), _f32(w.ssm.B, dev), _f32(w.ssm.C, dev), _f32(w.ssm.dt, dev))
     D = _f32(w.D, dev)
     k = torch.empty((w.H, w.L), dtype=torch.float32, device=dev)
-    K = torch.empty((w.H, w.L + 1, 2), dtype=torch.float32, device=dev)
-    ms = _time_calls(lambda i: (h3.ssm_kernel(A, Bp, C, dt, w.L, out=k), h3.kernel_spectrum(k, out=K),
-                                h3.fftconv_spectral(u, K, D, out=y)), 50, 5)
+    ws = torch.empty(h3.workspace_size(h3.OP_FFTCONV, w.B, w.H, w.L, 0, 0, h3.F32), dtype=torch.uint8, device=dev)
+    ms = _time_calls(lambda i: (h3.ssm_kernel(A, Bp, C, dt, w.L, out=k),
+                                h3.fftconv(u, k, D, out=y, workspace=ws)), 50, 5)
     ex["cfg0_f32_latency_us"] = ms * 1e3
     return ex
 
@@ -292,7 +292,7 @@ def main():
                    "buffer_sets": head["nsets"]},
         "roofline": {"bound": "hbm", "achieved": round(head["conv_gbs"], 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(head["conv_gbs"] / HBM_PEAK_GBS, 4), "traffic": None,
-                     "kernel": "fftconv_kernel<4096, f16>", "bytes_per_launch": head["conv_bytes"]},
+                     "kernel": "fftconv_mfma4096_kernel<f16>", "bytes_per_launch": head["conv_bytes"]},
     }
     if extra:
         res["extra"] = extra

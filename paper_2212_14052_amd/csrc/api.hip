@@ -117,13 +117,15 @@ int h3_fftconv(const void *u, const float *k, const float *D, void *y, int B, in
         overlap(workspace, need, k, (size_t)H * L * 4))
         return H3_EINVAL;
     hipStream_t s = (hipStream_t)stream;
+    ConvArgs a{};
+    a.u = u; a.y = y; a.D = D;
+    a.B = B; a.H = H; a.L = L; a.nchunk = 1; a.pair_mode = 0; a.dtype = dtype;
+    a.corr = nullptr;
+    if (fftconv_mfma_supported(L, dtype)) return launched(launch_fftconv_mfma(a, k, s));
     float2 *Kspec = (float2 *)workspace;
     hipError_t e = launch_spectrum(k, H, L, Kspec, s);
     if (e != hipSuccess) return H3_EDEVICE;
-    ConvArgs a{};
-    a.u = u; a.y = y; a.Kspec = Kspec; a.D = D;
-    a.B = B; a.H = H; a.L = L; a.nchunk = 1; a.pair_mode = 0; a.dtype = dtype;
-    a.corr = nullptr;
+    a.Kspec = Kspec;
     return launched(launch_fftconv(a, s));
 }
 

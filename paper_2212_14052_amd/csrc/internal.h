@@ -36,6 +36,10 @@ struct ConvArgs {
     const float *corr;
 };
 hipError_t launch_fftconv(const ConvArgs &a, hipStream_t s);
+// Matrix-core block-FFT variant (16-bit I/O, L = 2048): computes the kernel
+// spectrum from k itself; returns hipErrorInvalidValue for other shapes.
+hipError_t launch_fftconv_mfma(const ConvArgs &a, const float *k, hipStream_t s);
+bool fftconv_mfma_supported(int L, int dtype);
 
 size_t fftconv_workspace(int B, int H, int L);
 

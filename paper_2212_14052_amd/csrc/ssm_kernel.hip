@@ -134,6 +134,141 @@ __global__ __launch_bounds__(KG_THREADS) void kernel_gen(int mode, const float *
     }
 }
 
+// ------------------------------------------------------ matrix-core form ---
+// k[64 a + b] = 2 sum_n (Re P[a][n] Re Q[n][b] - Im P[a][n] Im Q[n][b]) is a real
+// matrix product with reduction length 2m (m <= 64, zero-padded to 128):
+//   Pm[a][k] = Re P[a][k] (k < 64), -Im P[a][k-64] (k >= 64)
+//   Qm[k][b] = Re Q[k][b] (k < 64),  Im Q[k-64][b] (k >= 64)
+// with P[a][n] = W_n z_n^{64 a}, Q[n][b] = z_n^b, z_n = exp(lambda_n), run as
+// 16x16x4 fp32 MFMAs (exact fp32 products, fp32 accumulation).  A workgroup (4
+// waves) produces rows a = a0 .. a0+15 (1024 outputs); wave w owns columns
+// b = 16 w .. 16 w + 15.  The powers z^e are formed in float64 by repeated
+// squaring and multiplication (relative error ~ e * 1e-16), so no phase is
+// ever reduced in float32.
+constexpr int KM_ROWS = 32;
+typedef float f4v_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ double2 zmul(double2 a, double2 b) {
+    return make_double2(a.x * b.x - a.y * b.y, a.x * b.y + a.y * b.x);
+}
+__device__ __forceinline__ double2 zpow(double2 z, int e) {
+    double2 r = make_double2(1.0, 0.0);
+    while (e) {
+        if (e & 1) r = zmul(r, z);
+        z = zmul(z, z);
+        e >>= 1;
+    }
+    return r;
+}
+
+__global__ __launch_bounds__(256) void kernel_gen_mfma(int mode, const float *P0, const float *P1,
+                                                       const float *C, const float *dt, int H,
+                                                       int m, int L, float *k, int div) {
+    __shared__ double2 z_s[H3_MAX_MODES_DEV];
+    __shared__ float2 W_s[H3_MAX_MODES_DEV];
+    __shared__ float Qm[128][64 + 16];       // [k][b]
+    __shared__ float Pm[KM_ROWS][128 + 4];   // [a][k]
+    const int nrt = (L / 64 + KM_ROWS - 1) / KM_ROWS;  // row tiles per output row
+    const int orow = blockIdx.x / nrt;
+    const int a0 = (blockIdx.x % nrt) * KM_ROWS;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    if (mode == 0) {
+        // ZOH from (A, B, dt): the three float64 transcendentals of each mode
+        // run on three waves in parallel, then one wave combines them.
+        __shared__ double pre[3][H3_MAX_MODES_DEV];
+        const int n = tid & 63, part = tid >> 6;
+        if (n < m && part < 3) {
+            const long i = (long)orow * m + n;
+            const double d = dt[orow];
+            const double lr = d * P0[2 * i], li = d * P0[2 * i + 1];
+            pre[part][n] = part == 0 ? expm1(lr) : part == 1 ? cos(li) : sin(li);
+        }
+        __syncthreads();
+        if (tid < H3_MAX_MODES_DEV) {
+            double2 z = make_double2(0.0, 0.0);
+            float2 Wn = make_float2(0.f, 0.f);
+            if (tid < m) {
+                const long i = (long)orow * m + tid;
+                const double em1 = pre[0][tid], cs = pre[1][tid], sn = pre[2][tid];
+                const double e = em1 + 1.0;
+                z = make_double2(e * cs, e * sn);
+                // exp(lambda) - 1 = (e cos - 1) + i e sin, with e cos - 1 = em1 cos + (cos - 1)
+                const double em1r = em1 * cs + (cs - 1.0), em1i = e * sn;
+                const double ar = P0[2 * i], ai = P0[2 * i + 1];
+                const double den = ar * ar + ai * ai;
+                const double qr = (em1r * ar + em1i * ai) / den, qi = (em1i * ar - em1r * ai) / den;
+                const double bre = P1[2 * i], bim = P1[2 * i + 1];
+                const double br = qr * bre - qi * bim, bi = qr * bim + qi * bre;
+                const double cr = C[2 * i], ci = C[2 * i + 1];
+                Wn = make_float2((float)(cr * br - ci * bi), (float)(cr * bi + ci * br));
+            }
+            z_s[tid] = z;
+            W_s[tid] = Wn;
+        }
+    } else if (tid < H3_MAX_MODES_DEV) {
+        double2 z = make_double2(0.0, 0.0);
+        float2 Wn = make_float2(0.f, 0.f);
+        if (tid < m) {
+            const int h = (mode == 1) ? orow : (orow / div) % H;
+            const long i = (long)h * m + tid;
+            z = make_double2(P0[2 * i], P0[2 * i + 1]);
+            if (mode == 1) {
+                const double cr = C[2 * i], ci = C[2 * i + 1], br = P1[2 * i], bi = P1[2 * i + 1];
+                Wn = make_float2((float)(cr * br - ci * bi), (float)(cr * bi + ci * br));
+            } else {
+                const long wi = (long)orow * m + tid;
+                Wn = make_float2(P1[2 * wi], P1[2 * wi + 1]);
+            }
+        }
+        z_s[tid] = z;
+        W_s[tid] = Wn;
+    }
+    __syncthreads();
+    {
+        // Q: thread -> (n = tid / 4, b = 16 (tid % 4) .. + 15)
+        const int n = tid >> 2, b0 = 16 * (tid & 3);
+        const double2 z = z_s[n];
+        double2 p = zpow(z, b0);
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            Qm[n][b0 + j] = (float)p.x;
+            Qm[64 + n][b0 + j] = (float)p.y;
+            p = zmul(p, z);
+        }
+        // P: thread -> (n = tid / 4, rows 8 (tid % 4) .. + 7)
+        const double2 z64 = zpow(z, 64);
+        const int ar0 = 8 * (tid & 3);
+        double2 q = zpow(z64, a0 + ar0);
+        const float2 Wn = W_s[n];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const float qr = (float)q.x, qi = (float)q.y;
+            Pm[ar0 + j][n] = Wn.x * qr - Wn.y * qi;
+            Pm[ar0 + j][64 + n] = -(Wn.x * qi + Wn.y * qr);
+            q = zmul(q, z64);
+        }
+    }
+    __syncthreads();
+    // wave w: two 16 x 16 tiles (rows a0 .. a0+15 and a0+16 .. a0+31) of
+    // columns 16 w .. 16 w + 15, reduction over k = 0..127 in steps of 4
+    f4v_t acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+    const int r = lane & 15, kq = lane >> 4;
+#pragma unroll 8
+    for (int k0 = 0; k0 < 128; k0 += 4) {
+        const float bv = Qm[k0 + kq][16 * w + r];
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(Pm[r][k0 + kq], bv, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(Pm[16 + r][k0 + kq], bv, acc1, 0, 0, 0);
+    }
+    // lane holds rows a0 + 4 kq + j (+16), column 16 w + r
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int a = a0 + 4 * kq + j;
+        const int t = 64 * a + 16 * w + r;
+        if (t < L) k[(long)orow * L + t] = 2.f * acc0[j];
+        if (t + 1024 < L) k[(long)orow * L + t + 1024] = 2.f * acc1[j];
+    }
+}
+
 hipError_t launch_discretize(const float *A, const float *B, const float *dt, int H, int m,
                              float *Abar, float *Bbar, hipStream_t s) {
     int n = H * m;
@@ -144,6 +279,12 @@ hipError_t launch_discretize(const float *A, const float *B, const float *dt, in
 
 hipError_t launch_kernel_gen(int mode, const float *P0, const float *P1, const float *C,
                              const float *dt, int H, int m, int L, float *k, hipStream_t s) {
+    if (L % 64 == 0) {
+        const long nrt = (L / 64 + KM_ROWS - 1) / KM_ROWS;
+        hipLaunchKernelGGL(kernel_gen_mfma, dim3((unsigned)(nrt * H)), dim3(256), 0, s, mode, P0, P1,
+                           C, dt, H, m, L, k, 1);
+        return hipGetLastError();
+    }
     const long ntile = (L + KG_TT - 1) / KG_TT;
     hipLaunchKernelGGL(kernel_gen, dim3((unsigned)(ntile * H)), dim3(KG_THREADS), 0, s, mode, P0, P1,
                        C, dt, H, m, L, k, 1);
@@ -152,8 +293,15 @@ hipError_t launch_kernel_gen(int mode, const float *P0, const float *P1, const f
 
 hipError_t launch_state_correction(const float *Abar, const float2 *corr_W, int B, int H, int m,
                                    int chunk, int nchunk, float *corr, hipStream_t s) {
-    const long ntile = (chunk + KG_TT - 1) / KG_TT;
     const long orows = (long)B * H * nchunk;
+    if (chunk % 64 == 0) {
+        const long nrt = (chunk / 64 + KM_ROWS - 1) / KM_ROWS;
+        hipLaunchKernelGGL(kernel_gen_mfma, dim3((unsigned)(nrt * orows)), dim3(256), 0, s, 2, Abar,
+                           (const float *)corr_W, (const float *)nullptr, (const float *)nullptr, H, m,
+                           chunk, corr, nchunk);
+        return hipGetLastError();
+    }
+    const long ntile = (chunk + KG_TT - 1) / KG_TT;
     hipLaunchKernelGGL(kernel_gen, dim3((unsigned)(ntile * orows)), dim3(KG_THREADS), 0, s, 2, Abar,
                        (const float *)corr_W, (const float *)nullptr, (const float *)nullptr, H, m,
                        chunk, corr, nchunk);

@@ -43,7 +43,7 @@ def test_discretize(h3):
     assert rel_err(cplx64(to_np64(Bb)).view(np.float64), rB.view(np.float64)) < 1e-6
 
 
-@pytest.mark.parametrize("L,dt_lo,dt_hi", [(1024, 1e-3, 1e-1), (100, 1e-3, 1e-1), (8192, 1e-4, 1e-1),
+@pytest.mark.parametrize("L,dt_lo,dt_hi", [(1024, 1e-3, 1e-1), (100, 1e-3, 1e-1), (8192, 1e-4, 1e-1), (64, 1e-2, 1e-1), (192, 1e-3, 1e-1),
                                            (2049, 1e-2, 1e-1), (16, 1e-3, 1e-1)])
 def test_ssm_kernel(h3, L, dt_lo, dt_hi):
     w = workloads.config(0, H=16, L=16, seed=7, dt_lo=dt_lo, dt_hi=dt_hi)
@@ -244,3 +244,42 @@ def test_layer_config4_one_batch_element(h3):
     w = workloads.config(4)
     y, ref = _layer_case(h3, w, b_sel=[3])
     assert rel_err(y, ref) < 2e-2
+
+
+# ------------------------------------------- matrix-core conv (L = 2048) ---
+@pytest.mark.parametrize("dtype", [workloads.F16, workloads.BF16])
+@pytest.mark.parametrize("B,H", [(1, 3), (5, 2), (16, 4), (8, 33)])
+def test_fftconv_mfma_shapes(h3, dtype, B, H):
+    y, ref = _conv_case(h3, B, H, 2048, dtype, seed=B * 100 + H, dt_lo=1e-4)
+    assert rel_err(y, ref) < TOL[dtype]
+
+
+@pytest.mark.parametrize("scale_u,scale_k", [(1e3, 1.0), (1e-3, 1.0), (1.0, 1e-5), (30.0, 10.0)])
+def test_fftconv_mfma_dynamic_range(h3, scale_u, scale_k):
+    """Inputs far from unit scale: the block FFT rescales by powers of two."""
+    rng = np.random.default_rng(5)
+    B, H, L = 4, 6, 2048
+    u = (rng.standard_normal((B, H, L)) * scale_u).astype(np.float32)
+    k = (rng.standard_normal((H, L)) * np.exp(-np.arange(L) / 400.0) * scale_k).astype(np.float32)
+    D = rng.standard_normal(H).astype(np.float32)
+    for dt in (workloads.BF16, workloads.F16):
+        s, u64 = workloads.round_to(u, dt)
+        y = to_np64(h3.fftconv(to_dev(s, dt), f32dev(k), f32dev(D)))
+        ref = oracle.causal_conv(u64, k.astype(np.float64), D.astype(np.float64))
+        assert rel_err(y, ref) < TOL[dt], (dt, rel_err(y, ref))
+
+
+def test_fftconv_mfma_zero_and_impulse(h3):
+    H, L = 3, 2048
+    rng = np.random.default_rng(6)
+    k = (rng.standard_normal((H, L)) * np.exp(-np.arange(L) / 300.0)).astype(np.float32)
+    u = np.zeros((2, H, L), np.float16)
+    y = to_np64(h3.fftconv(to_dev(u, workloads.F16), f32dev(k), None))
+    assert np.all(y == 0.0)
+    u[0, :, 0] = 1.0
+    u[1, :, 100] = 1.0
+    y = to_np64(h3.fftconv(to_dev(u, workloads.F16), f32dev(k), None))
+    kr = k.astype(np.float16).astype(np.float64)
+    assert rel_err(y[0], k) < 2e-2
+    assert rel_err(y[1, :, 100:], k[:, :L - 100]) < 2e-2
+    assert np.abs(y[1, :, :100]).max() < 1e-3 * np.abs(k).max()
