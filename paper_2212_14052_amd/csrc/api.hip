@@ -121,6 +121,7 @@ int h3_fftconv(const void *u, const float *k, const float *D, void *y, int B, in
     a.u = u; a.y = y; a.D = D;
     a.B = B; a.H = H; a.L = L; a.nchunk = 1; a.pair_mode = 0; a.dtype = dtype;
     a.corr = nullptr;
+    a.corr16 = 0;
     if (fftconv_mfma_supported(L, dtype)) return launched(launch_fftconv_mfma(a, k, s));
     float2 *Kspec = (float2 *)workspace;
     hipError_t e = launch_spectrum(k, H, L, Kspec, s);
@@ -148,6 +149,7 @@ int h3_fftconv_spectral(const void *u, const float *Kspec, const float *D, void 
     a.u = u; a.y = y; a.Kspec = (const float2 *)Kspec; a.D = D;
     a.B = B; a.H = H; a.L = L; a.nchunk = 1; a.pair_mode = 0; a.dtype = dtype;
     a.corr = nullptr;
+    a.corr16 = 0;
     return launched(launch_fftconv(a, (hipStream_t)stream));
 }
 
@@ -180,20 +182,28 @@ int h3_statepass_conv(const void *u, const float *Abar, const float *Bbar, const
     hipError_t e;
     // f = [C Bbar, C Abar Bbar, ...] of length chunk, and its spectrum
     if ((e = launch_kernel_gen(1, Abar, Bbar, C, nullptr, H, m, chunk, kbuf, s)) != hipSuccess) return H3_EDEVICE;
-    if ((e = launch_spectrum(kbuf, H, chunk, Kspec, s)) != hipSuccess) return H3_EDEVICE;
+    if (!fftconv_mfma_supported(chunk, dtype) &&
+        (e = launch_spectrum(kbuf, H, chunk, Kspec, s)) != hipSuccess)
+        return H3_EDEVICE;
     // s_c = M_ux u^(c) for every chunk, then the scan over chunks
     if ((e = launch_chunk_states(u, Abar, Bbar, B, H, L, m, chunk, dtype, states, s)) != hipSuccess)
         return H3_EDEVICE;
     if ((e = launch_state_scan(Abar, C, x0, states, B, H, m, chunk, nchunk, corr_W, x_final, s)) !=
         hipSuccess)
         return H3_EDEVICE;
-    // M_xy x^(c) for every chunk
-    if ((e = launch_state_correction(Abar, corr_W, B, H, m, chunk, nchunk, corr, s)) != hipSuccess)
-        return H3_EDEVICE;
+    // M_xy x^(c) for every chunk (in the I/O dtype when the matrix-core paths apply)
+    const bool fast = fftconv_mfma_supported(chunk, dtype) && state_correction_mfma_ok(chunk, dtype);
+    if (fast)
+        e = launch_state_correction_mfma(Abar, corr_W, B, H, m, chunk, nchunk, dtype, corr, s);
+    else
+        e = launch_state_correction(Abar, corr_W, B, H, m, chunk, nchunk, corr, s);
+    if (e != hipSuccess) return H3_EDEVICE;
     ConvArgs a{};
     a.u = u; a.y = y; a.Kspec = Kspec; a.D = D;
     a.B = B; a.H = H; a.L = chunk; a.nchunk = nchunk; a.pair_mode = 1; a.dtype = dtype;
     a.corr = corr;
+    a.corr16 = fast ? 1 : 0;
+    if (fftconv_mfma_supported(chunk, dtype)) return launched(launch_fftconv_mfma(a, kbuf, s));
     return launched(launch_fftconv(a, s));
 }
 

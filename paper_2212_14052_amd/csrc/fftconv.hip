@@ -151,8 +151,9 @@ __global__ __launch_bounds__(N / 16 >= 64 ? N / 16 : 64) void fftconv_kernel(Con
             float oa = w.x + d * ua[q * HALF + r];
             float ob = -w.y + d * ub[q * HALF + r];
             if (a.corr) {
-                oa += a.corr[pm.oa + n];
-                if (hb) ob += a.corr[pm.ob + n];
+                const float *cr = (const float *)a.corr;
+                oa += cr[pm.oa + n];
+                if (hb) ob += cr[pm.ob + n];
             }
             io::st(y, pm.oa + n, oa);
             if (hb) io::st(y, pm.ob + n, ob);

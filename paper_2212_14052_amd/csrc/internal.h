@@ -32,8 +32,9 @@ struct ConvArgs {
     int pair_mode;
     int dtype;
     // state-passing initial-state term (mode 1 only, may be null):
-    // (B, H, nchunk * L) float32 added to the output
-    const float *corr;
+    // (B, H, nchunk * L) added to the output; float32, or the I/O dtype if corr16
+    const void *corr;
+    int corr16;
 };
 hipError_t launch_fftconv(const ConvArgs &a, hipStream_t s);
 // Matrix-core block-FFT variant (16-bit I/O, L = 2048): computes the kernel
@@ -52,6 +53,9 @@ hipError_t launch_state_scan(const float *Abar, const float *C, const float *x0,
 // corr[row, c*chunk + t] = 2 Re sum_n corr_W[row, c, n] Abar_n^t  (row = b*H + h)
 hipError_t launch_state_correction(const float *Abar, const float2 *corr_W, int B, int H, int m,
                                    int chunk, int nchunk, float *corr, hipStream_t s);
+bool state_correction_mfma_ok(int chunk, int dtype);
+hipError_t launch_state_correction_mfma(const float *Abar, const float2 *corr_W, int B, int H, int m,
+                                        int chunk, int nchunk, int dtype, void *corr, hipStream_t s);
 
 // Layer pieces.
 hipError_t launch_transpose_w(const void *W, int d, int dtype, void *Wt, hipStream_t s);

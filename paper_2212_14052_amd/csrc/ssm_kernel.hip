@@ -166,7 +166,7 @@ __global__ __launch_bounds__(256) void kernel_gen_mfma(int mode, const float *P0
                                                        int m, int L, float *k, int div) {
     __shared__ double2 z_s[H3_MAX_MODES_DEV];
     __shared__ float2 W_s[H3_MAX_MODES_DEV];
-    __shared__ float Qm[128][64 + 16];       // [k][b]
+    __shared__ float Qt[64][128 + 4];        // [b][k]  (Qm transposed)
     __shared__ float Pm[KM_ROWS][128 + 4];   // [a][k]
     const int nrt = (L / 64 + KM_ROWS - 1) / KM_ROWS;  // row tiles per output row
     const int orow = blockIdx.x / nrt;
@@ -225,17 +225,21 @@ __global__ __launch_bounds__(256) void kernel_gen_mfma(int mode, const float *P0
     }
     __syncthreads();
     {
-        // Q: thread -> (n = tid / 4, b = 16 (tid % 4) .. + 15)
-        const int n = tid >> 2, b0 = 16 * (tid & 3);
-        const double2 z = z_s[n];
-        double2 p = zpow(z, b0);
+        // Q: thread -> (n = tid % 64, b = 16 (tid / 64) .. + 15); lanes vary n
+        {
+            const int n = tid & 63, b0 = 16 * (tid >> 6);
+            const double2 z = z_s[n];
+            double2 p = zpow(z, b0);
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-            Qm[n][b0 + j] = (float)p.x;
-            Qm[64 + n][b0 + j] = (float)p.y;
-            p = zmul(p, z);
+            for (int j = 0; j < 16; ++j) {
+                Qt[b0 + j][n] = (float)p.x;
+                Qt[b0 + j][64 + n] = (float)p.y;
+                p = zmul(p, z);
+            }
         }
         // P: thread -> (n = tid / 4, rows 8 (tid % 4) .. + 7)
+        const int n = tid >> 2;
+        const double2 z = z_s[n];
         const double2 z64 = zpow(z, 64);
         const int ar0 = 8 * (tid & 3);
         double2 q = zpow(z64, a0 + ar0);
@@ -255,7 +259,7 @@ __global__ __launch_bounds__(256) void kernel_gen_mfma(int mode, const float *P0
     const int r = lane & 15, kq = lane >> 4;
 #pragma unroll 8
     for (int k0 = 0; k0 < 128; k0 += 4) {
-        const float bv = Qm[k0 + kq][16 * w + r];
+        const float bv = Qt[16 * w + r][k0 + kq];
         acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(Pm[r][k0 + kq], bv, acc0, 0, 0, 0);
         acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(Pm[16 + r][k0 + kq], bv, acc1, 0, 0, 0);
     }

@@ -85,6 +85,324 @@ __global__ __launch_bounds__(CS_THREADS) void chunk_states_kernel(const void *u_
     }
 }
 
+// ------------------------------------------------- chunk sums, MFMA form ---
+// Same sums for 16-bit input and chunk % 1024 == 0.  Per channel,
+//   R[n][a] = sum_{b<64} Abar_n^{63-b} u_{64 a + b}
+// is a real matrix product (rows: Re / Im of 64 modes; reduction b; columns
+// a = 0 .. N'/64 - 1) on 16x16x32 MFMAs with the powers in 16-bit and the
+// input as it is stored; then
+//   s[n] = Bbar_n sum_a Abar_n^{N' - 64 (a + 1)} R[n][a]
+// in fp32 with the weights held in registers (powers in float64 first).
+// Workgroup: one channel and a set of its chunk rows; wave w owns modes
+// 16 w .. 16 w + 15 (row tile w of the real parts, w + 4 of the imaginary).
+// The chunk row is staged once in LDS (16-byte coalesced) for all four waves.
+typedef _Float16 sp_h8 __attribute__((ext_vector_type(8)));
+typedef __bf16 sp_b8 __attribute__((ext_vector_type(8)));
+typedef float sp_f4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ double2 sp_zmul(double2 a, double2 b) {
+    return make_double2(a.x * b.x - a.y * b.y, a.x * b.y + a.y * b.x);
+}
+__device__ __forceinline__ double2 sp_zpow(double2 z, int e) {
+    double2 r = make_double2(1.0, 0.0);
+    while (e) {
+        if (e & 1) r = sp_zmul(r, z);
+        z = sp_zmul(z, z);
+        e >>= 1;
+    }
+    return r;
+}
+
+template <int DT>
+__device__ __forceinline__ sp_f4 sp_mfma(uint4 a, uint4 b, sp_f4 c) {
+    if constexpr (DT == BF16)
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(sp_b8, a), __builtin_bit_cast(sp_b8, b), c, 0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(sp_h8, a), __builtin_bit_cast(sp_h8, b), c, 0, 0, 0);
+}
+template <int DT>
+__device__ __forceinline__ uint32_t sp_pack(float lo, float hi) {
+    if constexpr (DT == BF16) {
+        typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+        b2 v = {(__bf16)lo, (__bf16)hi};
+        return __builtin_bit_cast(uint32_t, v);
+    } else {
+        typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+        h2 v = {(_Float16)lo, (_Float16)hi};
+        return __builtin_bit_cast(uint32_t, v);
+    }
+}
+
+constexpr int SPM_NA = 128;    // columns a for chunk 8192; general: chunk / 64
+
+template <int DT>
+__global__ __launch_bounds__(256) void chunk_states_mfma(const uint16_t *u, const float *Abar,
+                                                         const float *Bbar, int B, int H, int L,
+                                                         int m, int chunk, int wg_per_ch,
+                                                         float2 *states) {
+    __shared__ __attribute__((aligned(16))) uint16_t us[2][SPM_NA * 72];   // rows of 64 + 8 pad
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int r16 = lane & 15, kg = lane >> 4;
+    const int h = blockIdx.x / wg_per_ch, part = blockIdx.x % wg_per_ch;
+    const int nchunk = L / chunk;
+    const int NA = chunk / 64;          // columns a, multiple of 16
+    const int NCT = NA / 16;            // column tiles
+    const int rows_per_ch = B * nchunk;
+    const int per = (rows_per_ch + wg_per_ch - 1) / wg_per_ch;
+    const int r0 = part * per, r1 = min(r0 + per, rows_per_ch);
+
+    // A operand (powers, 16-bit): rows n = 16 w + r16, reduction b = 32 ks + 8 kg + i
+    uint4 Are[2], Aim[2];
+    {
+        const int n = 16 * w + r16;
+        double2 z = make_double2(0.0, 0.0);
+        if (n < m) z = make_double2(Abar[2 * ((long)h * m + n)], Abar[2 * ((long)h * m + n) + 1]);
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            // b from 32 ks + 8 kg + 7 down to 32 ks + 8 kg: exponents 63 - b ascending
+            double2 p = sp_zpow(z, 63 - (32 * ks + 8 * kg + 7));
+            float pr[8], pi[8];
+#pragma unroll
+            for (int i = 7; i >= 0; --i) {
+                pr[i] = (float)p.x;
+                pi[i] = (float)p.y;
+                p = sp_zmul(p, z);
+            }
+            Are[ks] = make_uint4(sp_pack<DT>(pr[0], pr[1]), sp_pack<DT>(pr[2], pr[3]), sp_pack<DT>(pr[4], pr[5]), sp_pack<DT>(pr[6], pr[7]));
+            Aim[ks] = make_uint4(sp_pack<DT>(pi[0], pi[1]), sp_pack<DT>(pi[2], pi[3]), sp_pack<DT>(pi[4], pi[5]), sp_pack<DT>(pi[6], pi[7]));
+        }
+    }
+    // E weights for the lane's outputs: modes n = 16 w + 4 kg + j, columns a = 16 ct + r16
+    float2 E[SPM_NA / 16][4];
+    float2 Bb[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int n = 16 * w + 4 * kg + j;
+        double2 z = make_double2(0.0, 0.0);
+        Bb[j] = make_float2(0.f, 0.f);
+        if (n < m) {
+            const long i = (long)h * m + n;
+            z = make_double2(Abar[2 * i], Abar[2 * i + 1]);
+            Bb[j] = make_float2(Bbar[2 * i], Bbar[2 * i + 1]);
+        }
+        const double2 z1024 = sp_zpow(z, 1024);
+        // a descending from 16 (NCT-1) + r16: exponent chunk - 64 (a + 1) grows by 1024
+        double2 p = sp_zpow(z, chunk - 64 * (16 * (NCT - 1) + r16 + 1));
+#pragma unroll
+        for (int ct = SPM_NA / 16 - 1; ct >= 0; --ct) {
+            if (ct < NCT) {
+                E[ct][j] = make_float2((float)p.x, (float)p.y);
+                p = sp_zmul(p, z1024);
+            } else {
+                E[ct][j] = make_float2(0.f, 0.f);
+            }
+        }
+    }
+
+    const int nelem = chunk;                    // 16-bit elements per chunk row
+    auto stage = [&](int rr, int buf) {
+        const int bb = rr / nchunk, cc = rr % nchunk;
+        const uint16_t *src = u + ((long)bb * H + h) * L + (long)cc * chunk;
+        for (int i = tid; i < nelem / 8; i += 256) {
+            const uint4 v = *(const uint4 *)(src + 8 * i);
+            // row a = i / 8 (64 elements) padded by 8 elements to spread banks
+            *(uint4 *)&us[buf][(i >> 3) * 72 + 8 * (i & 7)] = v;
+        }
+    };
+    if (r0 < r1) stage(r0, 0);
+    __syncthreads();
+    for (int rr = r0; rr < r1; ++rr) {
+        const int buf = (rr - r0) & 1;
+        if (rr + 1 < r1) stage(rr + 1, buf ^ 1);
+        sp_f4 sre = {0.f, 0.f, 0.f, 0.f}, sim = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ct = 0; ct < SPM_NA / 16; ++ct) {
+            if (ct < NCT) {
+                sp_f4 accr = {0.f, 0.f, 0.f, 0.f}, acci = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks) {
+                    // B operand: column a = 16 ct + r16, reduction b = 32 ks + 8 kg .. + 7
+                    const uint4 bv = *(const uint4 *)&us[buf][(16 * ct + r16) * 72 + 32 * ks + 8 * kg];
+                    accr = sp_mfma<DT>(Are[ks], bv, accr);
+                    acci = sp_mfma<DT>(Aim[ks], bv, acci);
+                }
+                // lane: rows (modes) 4 kg + j, column a = 16 ct + r16
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    sre[j] = fmaf(E[ct][j].x, accr[j], fmaf(-E[ct][j].y, acci[j], sre[j]));
+                    sim[j] = fmaf(E[ct][j].x, acci[j], fmaf(E[ct][j].y, accr[j], sim[j]));
+                }
+            }
+        }
+        // reduce over the 16 columns held by lanes r16 = 0..15
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                sre[j] += __shfl_xor(sre[j], o);
+                sim[j] += __shfl_xor(sim[j], o);
+            }
+        if (r16 == 0) {
+            const int bb = rr / nchunk, cc = rr % nchunk;
+            const long crow = ((long)bb * H + h) * nchunk + cc;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int n = 16 * w + 4 * kg + j;
+                if (n < m) states[crow * m + n] = cmul(Bb[j], make_float2(sre[j], sim[j]));
+            }
+        }
+        __syncthreads();
+    }
+}
+
+bool chunk_states_mfma_ok(int chunk, int dtype) {
+    return (dtype == F16 || dtype == BF16) && chunk % 1024 == 0 && chunk / 64 <= SPM_NA;
+}
+
+hipError_t launch_chunk_states_mfma(const void *u, const float *Abar, const float *Bbar, int B, int H,
+                                    int L, int m, int chunk, int dtype, float2 *states, hipStream_t s) {
+    const int rows_per_ch = B * (L / chunk);
+    int wg = 1;
+    while (H * wg < 1024 && rows_per_ch / (2 * wg) >= 4) wg *= 2;
+    dim3 grid(H * wg), block(256);
+    if (dtype == BF16)
+        hipLaunchKernelGGL(chunk_states_mfma<BF16>, grid, block, 0, s, (const uint16_t *)u, Abar, Bbar, B, H, L, m, chunk, wg, states);
+    else
+        hipLaunchKernelGGL(chunk_states_mfma<F16>, grid, block, 0, s, (const uint16_t *)u, Abar, Bbar, B, H, L, m, chunk, wg, states);
+    return hipGetLastError();
+}
+
+// -------------------------------------------- initial-state term, MFMA form ---
+// corr[c N' + t] = 2 Re sum_n W_n Abar_n^t,  W_n = C_n x^(c)_n Abar_n  (so the
+// term is 2 Re sum_n C_n Abar_n^{t+1} x^(c)_n, the M_xy x^(c) of Algorithm 2).
+// With t = 64 a + b:  corr = 2 sum_k Pm[a][k] Qm[k][b],
+//   Pm[a][k] = Re (W_k E[a][k]) (k < 64), -Im (W_{k-64} E[a][k-64]) (k >= 64),
+//   Qm[k][b] = Re Abar_k^b (k < 64), Im Abar_{k-64}^b (k >= 64),
+//   E[a][n] = Abar_n^{64 a}.
+// Per channel the tables E and Q (powers in float64, stored fp16) sit in LDS;
+// per chunk row W is scaled by a power of two to max |W| in [1/2, 1) before
+// rounding to fp16, and the scale is undone in fp32.  Output in the I/O dtype.
+// Workgroup (4 waves): one channel, a set of its chunk rows; wave w owns row
+// tiles a = 16 (2w) .. 16 (2w + 1) + 15 of every chunk, all 64 columns b.
+typedef _Float16 cr_h2 __attribute__((ext_vector_type(2)));
+constexpr int CR_NA = 128;
+
+template <int DT>
+__global__ __launch_bounds__(256) void state_correction_mfma(const float *Abar, const float2 *corr_W,
+                                                             int B, int H, int m, int chunk, int nchunk,
+                                                             int wg_per_ch, uint16_t *corr) {
+    __shared__ __attribute__((aligned(16))) uint32_t Et[CR_NA][64 + 4];     // E[a][n], fp16 complex
+    __shared__ __attribute__((aligned(16))) uint16_t Qt[64][128 + 8];       // Qm[k][b] as [b][k]
+    __shared__ float2 Ws[64];
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int r16 = lane & 15, kg = lane >> 4;
+    const int h = blockIdx.x / wg_per_ch, part = blockIdx.x % wg_per_ch;
+    const int NA = chunk / 64;
+    const int rows_per_ch = B * nchunk;
+    const int per = (rows_per_ch + wg_per_ch - 1) / wg_per_ch;
+    const int r0 = part * per, r1 = min(r0 + per, rows_per_ch);
+    {
+        const int n = tid & 63, q = tid >> 6;
+        double2 z = make_double2(0.0, 0.0);
+        if (n < m) z = make_double2(Abar[2 * ((long)h * m + n)], Abar[2 * ((long)h * m + n) + 1]);
+        // Q: b = 16 q .. 16 q + 15
+        double2 p = sp_zpow(z, 16 * q);
+        for (int j = 0; j < 16; ++j) {
+            Qt[16 * q + j][n] = __builtin_bit_cast(uint16_t, (_Float16)p.x);
+            Qt[16 * q + j][64 + n] = __builtin_bit_cast(uint16_t, (_Float16)p.y);
+            p = sp_zmul(p, z);
+        }
+        // E: a = q, q + 4, ... (stride 4)
+        const double2 z64 = sp_zpow(z, 64), z256 = sp_zpow(z64, 4);
+        double2 e = sp_zpow(z64, q);
+        for (int a = q; a < NA; a += 4) {
+            cr_h2 v = {(_Float16)e.x, (_Float16)e.y};
+            Et[a][n] = __builtin_bit_cast(uint32_t, v);
+            e = sp_zmul(e, z256);
+        }
+    }
+    __syncthreads();
+    for (int rr = r0; rr < r1; ++rr) {
+        const int bb = rr / nchunk, cc = rr % nchunk;
+        const long crow = ((long)bb * H + h) * nchunk + cc;
+        // W for this chunk row, scaled
+        float2 wv = (lane < m) ? corr_W[crow * m + lane] : make_float2(0.f, 0.f);
+        float mx = fmaxf(fabsf(wv.x), fabsf(wv.y));
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+        int ew = 0;
+        if (mx > 0.f && mx < 3.0e38f) frexpf(mx, &ew);
+        wv = make_float2(ldexpf(wv.x, -ew), ldexpf(wv.y, -ew));
+        if (w == 0) Ws[lane] = wv;
+        __syncthreads();
+        // wave w: a-tiles 2w, 2w+1
+#pragma unroll
+        for (int at2 = 0; at2 < 2; ++at2) {
+            const int at = 2 * w + at2;
+            if (16 * at >= NA) break;
+            const int a = 16 * at + r16;
+            // A fragments: k = 32 ks + 8 kg + i; n = k mod 64
+            uint4 Af[4];
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                uint32_t re[4], im[4];
+#pragma unroll
+                for (int i2 = 0; i2 < 4; ++i2) {
+                    float pr[2], pim[2];
+#pragma unroll
+                    for (int ii = 0; ii < 2; ++ii) {
+                        const int n = 32 * ks + 8 * kg + 2 * i2 + ii;
+                        const cr_h2 e = __builtin_bit_cast(cr_h2, Et[a][n]);
+                        const float2 wn = Ws[n];
+                        const float er = (float)e.x, ei = (float)e.y;
+                        pr[ii] = wn.x * er - wn.y * ei;
+                        pim[ii] = -(wn.x * ei + wn.y * er);
+                    }
+                    re[i2] = sp_pack<F16>(pr[0], pr[1]);
+                    im[i2] = sp_pack<F16>(pim[0], pim[1]);
+                }
+                Af[ks] = make_uint4(re[0], re[1], re[2], re[3]);
+                Af[2 + ks] = make_uint4(im[0], im[1], im[2], im[3]);
+            }
+#pragma unroll
+            for (int bt = 0; bt < 4; ++bt) {
+                sp_f4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks) {
+                    const uint4 bv = *(const uint4 *)&Qt[16 * bt + r16][32 * ks + 8 * kg];
+                    acc = sp_mfma<F16>(Af[ks], bv, acc);
+                }
+                // lane: rows a = 16 at + 4 kg + j, column b = 16 bt + r16
+                const float sc = ldexpf(2.0f, ew);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int t = 64 * (16 * at + 4 * kg + j) + 16 * bt + r16;
+                    const float v = acc[j] * sc;
+                    corr[crow * chunk + t] = (DT == BF16) ? f32_to_bf16(v) : f32_to_f16(v);
+                }
+            }
+        }
+        __syncthreads();   // Ws is rewritten by the next chunk row
+    }
+}
+
+bool state_correction_mfma_ok(int chunk, int dtype) {
+    return (dtype == F16 || dtype == BF16) && chunk % 1024 == 0 && chunk / 64 <= CR_NA;
+}
+
+hipError_t launch_state_correction_mfma(const float *Abar, const float2 *corr_W, int B, int H, int m,
+                                        int chunk, int nchunk, int dtype, void *corr, hipStream_t s) {
+    const int rows_per_ch = B * nchunk;
+    int wg = 1;
+    while (H * wg < 1024 && rows_per_ch / (2 * wg) >= 4) wg *= 2;
+    dim3 grid(H * wg), block(256);
+    if (dtype == BF16)
+        hipLaunchKernelGGL(state_correction_mfma<BF16>, grid, block, 0, s, Abar, corr_W, B, H, m, chunk, nchunk, wg, (uint16_t *)corr);
+    else
+        hipLaunchKernelGGL(state_correction_mfma<F16>, grid, block, 0, s, Abar, corr_W, B, H, m, chunk, nchunk, wg, (uint16_t *)corr);
+    return hipGetLastError();
+}
+
 // ------------------------------------------------------------------ scan ---
 // One thread per (row, mode): x <- Abar^{N'} x + s_c across the chunks.
 // Writes corr_W[row, c, n] = C_n x^(c)_n Abar_n (so that the initial-state
@@ -117,6 +435,8 @@ __global__ void state_scan_kernel(const float *Abar, const float *C, const float
 
 hipError_t launch_chunk_states(const void *u, const float *Abar, const float *Bbar, int B, int H,
                                int L, int m, int chunk, int dtype, float2 *states, hipStream_t s) {
+    if (chunk_states_mfma_ok(chunk, dtype))
+        return launch_chunk_states_mfma(u, Abar, Bbar, B, H, L, m, chunk, dtype, states, s);
     const int nchunk = L / chunk;
     const long ncr = (long)B * H * nchunk;
     const size_t lds = (size_t)chunk * sizeof(float) +

@@ -167,7 +167,8 @@ def _sp_inputs(w):
 
 @pytest.mark.parametrize("dtype,L,chunk", [(workloads.F32, 1024, 128), (workloads.F32, 512, 512),
                                            (workloads.F16, 2048, 256), (workloads.BF16, 1024, 16),
-                                           (workloads.F32, 256, 16)])
+                                           (workloads.F32, 256, 16), (workloads.F16, 4096, 1024),
+                                           (workloads.BF16, 8192, 2048), (workloads.F16, 8192, 4096)])
 def test_statepass_small(h3, dtype, L, chunk):
     w = workloads.statepass_workload("t", 3, 5, L, chunk, dtype, seed=L + chunk, dt_lo=1e-3,
                                      dt_hi=1e-1, x0_scale=0.5)
@@ -283,3 +284,26 @@ def test_fftconv_mfma_zero_and_impulse(h3):
     assert rel_err(y[0], k) < 2e-2
     assert rel_err(y[1, :, 100:], k[:, :L - 100]) < 2e-2
     assert np.abs(y[1, :, :100]).max() < 1e-3 * np.abs(k).max()
+
+
+# ----------------------------------------- matrix-core conv (L = 8192) ---
+@pytest.mark.parametrize("dtype", [workloads.F16, workloads.BF16])
+@pytest.mark.parametrize("B,H", [(1, 2), (3, 3), (16, 2)])
+def test_fftconv_mfma16k_shapes(h3, dtype, B, H):
+    y, ref = _conv_case(h3, B, H, 8192, dtype, seed=B * 10 + H + 7, dt_lo=1e-4)
+    assert rel_err(y, ref) < TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype", [workloads.F16, workloads.BF16])
+def test_statepass_mfma_chunks(h3, dtype):
+    """Chunk 8192 (the fused limit) runs the matrix-core conv per chunk pair."""
+    w = workloads.statepass_workload("t", 2, 3, 4 * 8192, 8192, dtype, seed=77, dt_lo=1e-4,
+                                     dt_hi=1e-2, x0_scale=0.3)
+    Ab32, Bb32, Ab, Bb, C = _sp_inputs(w)
+    y, xf = h3.statepass_conv(to_dev(w.u, dtype), f32dev(Ab32), f32dev(Bb32), f32dev(w.ssm.C),
+                              f32dev(w.D), w.chunk, x0=f32dev(w.x0))
+    torch.cuda.synchronize()
+    ry, rx = oracle.recurrence(w.u64, Ab, Bb, C, w.D.astype(np.float64), x0=cplx64(w.x0))
+    assert rel_err(to_np64(y), ry) < TOL[dtype]
+    xg = cplx64(to_np64(xf))
+    assert np.abs(xg - rx).max() / np.abs(rx).max() < 2e-2
