@@ -28,6 +28,29 @@ template <> struct Mfma<BF16> {
     }
 };
 
+// Store one 32x32 accumulator tile (rows mb + 8(e/4) + e%4 for the lane,
+// column n) with the output layout chosen at compile time.
+template <int DT, int OUT>
+__device__ __forceinline__ void store_tile(uint16_t *C, const f32x16_t &acc, int mb, int n, int N, int d, int L) {
+    long nofs;
+    if constexpr (OUT == 0) {
+        nofs = n;
+    } else {
+        nofs = (long)(n / L) * ((long)d * L) + (n % L);
+    }
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+        const int m = mb + 8 * (e >> 2) + (e & 3);
+        const uint16_t o = (DT == BF16) ? f32_to_bf16(acc[e]) : f32_to_f16(acc[e]);
+        long dst;
+        if constexpr (OUT == 0)
+            dst = (long)m * N + nofs;
+        else
+            dst = (long)(m / d) * ((long)N * d) + (long)(m % d) * L + nofs;
+        C[dst] = o;
+    }
+}
+
 // ------------------------------------------------------------------ GEMM ---
 // C = A . Bt^T with A (M, K) and Bt (N, K) both K-contiguous (16-bit), fp32
 // accumulation, 16-bit result.  Tile 128 x 128 x 32, 4 waves of 64 x 64, each
@@ -38,10 +61,9 @@ template <> struct Mfma<BF16> {
 //             [(m / d)][(n / L)][(m % d)][(n % L)]  (three (B, d, L) tensors).
 constexpr int GB_M = 128, GB_N = 128, GB_K = 32, GB_LDK = GB_K + 8;
 
-template <int DT>
+template <int DT, int OUT>
 __global__ __launch_bounds__(256) void gemm_nt_kernel(const uint16_t *A, const uint16_t *Bt,
-                                                      uint16_t *C, int M, int N, int K,
-                                                      int out_mode, int d, int L) {
+                                                      uint16_t *C, int M, int N, int K, int d, int L) {
     __shared__ __attribute__((aligned(16))) uint16_t As[GB_M * GB_LDK];
     __shared__ __attribute__((aligned(16))) uint16_t Bs[GB_N * GB_LDK];
     const int nbn = N / GB_N;
@@ -51,21 +73,9 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(const uint16_t *A, const u
     const int wm = w >> 1, wn = w & 1;
     // global -> register staging: 2 x 16 B of A and of B per thread
     const int lr = t >> 2, lk = (t & 3) * 8;
-    uint4 ra[2], rb[2];
-    auto gload = [&](int k0) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            ra[i] = *(const uint4 *)(A + (long)(m0 + lr + 64 * i) * K + k0 + lk);
-            rb[i] = *(const uint4 *)(Bt + (long)(n0 + lr + 64 * i) * K + k0 + lk);
-        }
-    };
-    auto lstore = [&]() {
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            *(uint4 *)(As + (lr + 64 * i) * GB_LDK + lk) = ra[i];
-            *(uint4 *)(Bs + (lr + 64 * i) * GB_LDK + lk) = rb[i];
-        }
-    };
+    const uint16_t *ga = A + (long)(m0 + lr) * K + lk, *gb = Bt + (long)(n0 + lr) * K + lk;
+    const long g64 = 64L * K;
+    uint16_t *la = As + lr * GB_LDK + lk, *lb = Bs + lr * GB_LDK + lk;
     f32x16_t acc[2][2];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -74,12 +84,18 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(const uint16_t *A, const u
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-    gload(0);
-    lstore();
+    uint4 a0 = *(const uint4 *)(ga), a1 = *(const uint4 *)(ga + g64);
+    uint4 b0 = *(const uint4 *)(gb), b1 = *(const uint4 *)(gb + g64);
+    *(uint4 *)(la) = a0; *(uint4 *)(la + 64 * GB_LDK) = a1;
+    *(uint4 *)(lb) = b0; *(uint4 *)(lb + 64 * GB_LDK) = b1;
     __syncthreads();
     for (int k0 = 0; k0 < K; k0 += GB_K) {
         const bool more = k0 + GB_K < K;
-        if (more) gload(k0 + GB_K);
+        if (more) {
+            const int k1 = k0 + GB_K;
+            a0 = *(const uint4 *)(ga + k1); a1 = *(const uint4 *)(ga + g64 + k1);
+            b0 = *(const uint4 *)(gb + k1); b1 = *(const uint4 *)(gb + g64 + k1);
+        }
 #pragma unroll
         for (int ks = 0; ks < GB_K / 16; ++ks) {
             uint4 af[2], bf[2];
@@ -96,7 +112,8 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(const uint16_t *A, const u
         }
         __syncthreads();
         if (more) {
-            lstore();
+            *(uint4 *)(la) = a0; *(uint4 *)(la + 64 * GB_LDK) = a1;
+            *(uint4 *)(lb) = b0; *(uint4 *)(lb + 64 * GB_LDK) = b1;
             __syncthreads();
         }
     }
@@ -105,20 +122,94 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(const uint16_t *A, const u
     for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j)
+            store_tile<DT, OUT>(C, acc[i][j], m0 + wm * 64 + i * 32 + 4 * (lane >> 5),
+                                n0 + wn * 64 + j * 32 + (lane & 31), N, d, L);
+}
+
+// ------------------------------------------------------ GEMM, large tiles ---
+// Same contract as gemm_nt_kernel for M, N % 256 == 0 and K % 64 == 0.
+// Block tile 256 x 256 x 64, 8 waves as 2 (M) x 4 (N), each wave 128 x 64 =
+// 4 x 2 tiles of 32x32x16 MFMA (fp32 accumulators, 128 per lane).  LDS holds
+// two stages of A and B (rows padded to 72 elements: 16-byte fragment reads
+// of 8 consecutive rows hit 8 different bank groups); the next stage is
+// fetched into registers while the current one is multiplied, so one barrier
+// per K step suffices.  Consecutive blocks (same XCD after the remap) share
+// the A panel.
+constexpr int G2_M = 256, G2_N = 256, G2_K = 64, G2_LD = G2_K + 8, G2_T = 512;
+
+template <int DT, int OUT>
+__global__ __launch_bounds__(G2_T) void gemm_nt_256(const uint16_t *A, const uint16_t *Bt, uint16_t *C,
+                                                    int M, int N, int K, int d, int L) {
+    extern __shared__ __attribute__((aligned(16))) uint16_t g2_lds[];
+    uint16_t *As = g2_lds;                          // [2][256][72]
+    uint16_t *Bs = g2_lds + 2 * G2_M * G2_LD;       // [2][256][72]
+    const int nbn = N / G2_N;
+    const int blk = xcd_logical_block(blockIdx.x, gridDim.x);
+    const int m0 = (blk / nbn) * G2_M, n0 = (blk % nbn) * G2_N;
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+    const int wm = w >> 2, wn = w & 3;
+    // loader mapping: thread -> rows t / 8 + 64 i, 16-byte column chunk (t % 8) * 8
+    const int lr = t >> 3, lk = (t & 7) * 8;
+    const uint16_t *ga = A + (long)(m0 + lr) * K + lk, *gb = Bt + (long)(n0 + lr) * K + lk;
+    const long g64 = 64L * K;
+    uint16_t *la = As + lr * G2_LD + lk, *lb = Bs + lr * G2_LD + lk;
+    f32x16_t acc[4][2];
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int m = m0 + wm * 64 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-                const int n = n0 + wn * 64 + j * 32 + (lane & 31);
-                const uint16_t v = (DT == BF16) ? f32_to_bf16(acc[i][j][e]) : f32_to_f16(acc[i][j][e]);
-                long dst;
-                if (out_mode == 0) {
-                    dst = (long)m * N + n;
-                } else {
-                    dst = (long)(m / d) * ((long)N * d) + (long)(n / L) * ((long)d * L) +
-                          (long)(m % d) * L + (n % L);
-                }
-                C[dst] = v;
-            }
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+    uint4 a0 = *(const uint4 *)(ga), a1 = *(const uint4 *)(ga + g64), a2 = *(const uint4 *)(ga + 2 * g64),
+          a3 = *(const uint4 *)(ga + 3 * g64);
+    uint4 b0 = *(const uint4 *)(gb), b1 = *(const uint4 *)(gb + g64), b2 = *(const uint4 *)(gb + 2 * g64),
+          b3 = *(const uint4 *)(gb + 3 * g64);
+    constexpr int S64 = 64 * G2_LD, STAGE = G2_M * G2_LD;
+    *(uint4 *)(la) = a0; *(uint4 *)(la + S64) = a1; *(uint4 *)(la + 2 * S64) = a2; *(uint4 *)(la + 3 * S64) = a3;
+    *(uint4 *)(lb) = b0; *(uint4 *)(lb + S64) = b1; *(uint4 *)(lb + 2 * S64) = b2; *(uint4 *)(lb + 3 * S64) = b3;
+    __syncthreads();
+    const int nk = K / G2_K;
+    for (int kt = 0; kt < nk; ++kt) {
+        const int buf = kt & 1;
+        const bool more = kt + 1 < nk;
+        if (more) {
+            const int k1 = (kt + 1) * G2_K;
+            a0 = *(const uint4 *)(ga + k1); a1 = *(const uint4 *)(ga + g64 + k1);
+            a2 = *(const uint4 *)(ga + 2 * g64 + k1); a3 = *(const uint4 *)(ga + 3 * g64 + k1);
+            b0 = *(const uint4 *)(gb + k1); b1 = *(const uint4 *)(gb + g64 + k1);
+            b2 = *(const uint4 *)(gb + 2 * g64 + k1); b3 = *(const uint4 *)(gb + 3 * g64 + k1);
+        }
+        const uint16_t *as = As + buf * STAGE, *bs = Bs + buf * STAGE;
+#pragma unroll
+        for (int ks = 0; ks < G2_K / 16; ++ks) {
+            const int kk = ks * 16 + 8 * (lane >> 5);
+            uint4 af[4], bf[2];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                af[i] = *(const uint4 *)(as + (wm * 128 + i * 32 + (lane & 31)) * G2_LD + kk);
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                bf[j] = *(const uint4 *)(bs + (wn * 64 + j * 32 + (lane & 31)) * G2_LD + kk);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j) acc[i][j] = Mfma<DT>::run(af[i], bf[j], acc[i][j]);
+        }
+        if (more) {
+            uint16_t *sa = la + (buf ^ 1) * STAGE, *sb = lb + (buf ^ 1) * STAGE;
+            *(uint4 *)(sa) = a0; *(uint4 *)(sa + S64) = a1; *(uint4 *)(sa + 2 * S64) = a2; *(uint4 *)(sa + 3 * S64) = a3;
+            *(uint4 *)(sb) = b0; *(uint4 *)(sb + S64) = b1; *(uint4 *)(sb + 2 * S64) = b2; *(uint4 *)(sb + 3 * S64) = b3;
+        }
+        __syncthreads();
+    }
+    // epilogue: lane holds column (lane & 31) and rows 8(e/4) + 4(lane/32) + e%4
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+            store_tile<DT, OUT>(C, acc[i][j], m0 + wm * 128 + i * 32 + 4 * (lane >> 5),
+                                n0 + wn * 64 + j * 32 + (lane & 31), N, d, L);
 }
 
 // --------------------------------------------------------- transposes ------
@@ -250,16 +341,28 @@ hipError_t launch_transpose_batched(const void *in, void *out, int nb, int R, in
     return hipGetLastError();
 }
 
+template <int DT, int OUT>
+static hipError_t launch_gemm_t(const void *A, const void *Bt, void *C, int M, int N, int K, int d,
+                                int L, hipStream_t s) {
+    if (M % G2_M == 0 && N % G2_N == 0 && K % G2_K == 0) {
+        const size_t lds = (size_t)2 * (G2_M + G2_N) * G2_LD * sizeof(uint16_t);
+        (void)hipFuncSetAttribute((const void *)gemm_nt_256<DT, OUT>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        hipLaunchKernelGGL((gemm_nt_256<DT, OUT>), dim3((M / G2_M) * (N / G2_N)), dim3(G2_T), lds, s,
+                           (const uint16_t *)A, (const uint16_t *)Bt, (uint16_t *)C, M, N, K, d, L);
+    } else {
+        hipLaunchKernelGGL((gemm_nt_kernel<DT, OUT>), dim3((M / GB_M) * (N / GB_N)), dim3(256), 0, s,
+                           (const uint16_t *)A, (const uint16_t *)Bt, (uint16_t *)C, M, N, K, d, L);
+    }
+    return hipGetLastError();
+}
+
 hipError_t launch_gemm_nt(const void *A, const void *Bt, void *C, int M, int N, int K, int dtype,
                           int out_mode, int d, int L, hipStream_t s) {
-    const int nblk = (M / GB_M) * (N / GB_N);
     if (dtype == BF16)
-        hipLaunchKernelGGL(gemm_nt_kernel<BF16>, dim3(nblk), dim3(256), 0, s, (const uint16_t *)A,
-                           (const uint16_t *)Bt, (uint16_t *)C, M, N, K, out_mode, d, L);
-    else
-        hipLaunchKernelGGL(gemm_nt_kernel<F16>, dim3(nblk), dim3(256), 0, s, (const uint16_t *)A,
-                           (const uint16_t *)Bt, (uint16_t *)C, M, N, K, out_mode, d, L);
-    return hipGetLastError();
+        return out_mode ? launch_gemm_t<BF16, 1>(A, Bt, C, M, N, K, d, L, s)
+                        : launch_gemm_t<BF16, 0>(A, Bt, C, M, N, K, d, L, s);
+    return out_mode ? launch_gemm_t<F16, 1>(A, Bt, C, M, N, K, d, L, s)
+                    : launch_gemm_t<F16, 0>(A, Bt, C, M, N, K, d, L, s);
 }
 
 template <int N, int DT>
