@@ -710,6 +710,7 @@ bool fftconv_mfma_supported(int L, int dtype) {
 // handled here (N != 4096 or 32-bit I/O).
 hipError_t launch_fftconv_mfma(const ConvArgs &a, const float *k, hipStream_t s) {
     if (!fftconv_mfma_supported(a.L, a.dtype)) return hipErrorInvalidValue;
+    if (fftconv_wave_supported(a.L, a.dtype)) return launch_fftconv_wave(a, k, s);
     int pairs_per_ch;
     if (a.pair_mode == 0)
         pairs_per_ch = (a.B + 1) / 2;

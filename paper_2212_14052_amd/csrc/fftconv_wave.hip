@@ -1,0 +1,696 @@
+// Fused FFT convolution with one wavefront per transform (Sec. 4.1: kernel
+// fusion + block FFT), gfx950, 16-bit I/O, L = 2048, transform length
+// N = 2L = 4096 = 16^3.
+//
+// A wavefront holds a whole length-4096 complex signal in registers: lane
+// l = 16 g + c (g = l / 16, c = l % 16) keeps 64 packed-fp16 complex values
+// d[4 T + j], T, j = 0..15, 0..3.  Each of the three radix-16 layers of the
+// block FFT is 16 pairs of v_mfma_f32_16x16x32_f16 (real and imaginary rows of
+// the 16x16 DFT matrix), one pair per "tile" of 16 length-16 vectors.  The
+// three base-16 digits of an index live in three slots:
+//   C  = c           (the lane within a row of 16 lanes)
+//   G  = 4 g + j     (the row of 16 lanes and the register within a tile)
+//   T  = T           (the tile)
+// An MFMA always contracts the digit in slot G.  With the signal as the A
+// operand the output frequency lands in slot C and the digit that was in C
+// moves to G (the matrix core transposes for free); with the signal as the B
+// operand the frequency stays in G.  The one exchange of slot G with slot T
+// that the three layers need is done in registers with v_permlane32_swap and
+// v_permlane16_swap (gfx950), so no transform touches LDS.
+//
+// Forward DFT, input index p = 256 p2 + 16 p1 + p0, output X[k2 + 16 k1 +
+// 256 k0] (decimation in frequency):
+//   load           p2 : G, p1 : C, p0 : T
+//   L1 (signal A)  DFT over p2 -> k2 : C, p1 : G      then * w_256^{k2 p1}
+//   L2 (signal B)  DFT over p1 -> k1 : G              then * w_4096^{p0 (k2 + 16 k1)}
+//   swap G <-> T   p0 : G, k1 : T
+//   L3 (signal B)  DFT over p0 -> k0 : G
+// The second transform is the inverse DFT run backwards with conjugated
+// matrices and twiddles (L3^H, swap, conj twiddle, L2^H as A, conj twiddle,
+// L1^H as B) and ends in the load layout, so outputs are written where the
+// inputs were read.
+//
+// The skip term D u is folded into the kernel (k[0] += D): the length-2L
+// circular convolution of the zero-padded row with k + D delta equals the
+// causal convolution plus D u on t < L.
+//
+// Dynamic range: every DFT matrix carries a factor 1/4; the signal is scaled
+// by a power of two when its max |u| leaves [2^-4, 16) and the kernel spectrum
+// is normalised to max |K| in [1/2, 1), so no fp16 intermediate overflows; the
+// scale factors are powers of two and are undone in fp32 at the output.
+//
+// One workgroup of 4 waves handles the row pairs of one channel (or a share
+// of them): wave 0 first transforms the channel's kernel into LDS (the
+// spectrum never reaches HBM); every wave then streams its own pairs.
+#include "common.h"
+#include "internal.h"
+
+namespace h3 {
+namespace wv {
+
+typedef _Float16 h2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 h8_t __attribute__((ext_vector_type(8)));
+typedef float f4_t __attribute__((ext_vector_type(4)));
+typedef float f2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 b2_t __attribute__((ext_vector_type(2)));
+
+constexpr int N = 4096;
+constexpr int L = 2048;
+constexpr int NW = 4;           // waves per workgroup
+constexpr int NT = 64 * NW;
+
+// ------------------------------------------------- twiddle table (constant) --
+// w_4096^n = exp(-2 pi i n / 4096) for n < 4096, as float (re, im), evaluated
+// at compile time: the first quadrant from Taylor series of sin and cos on
+// [0, pi/4] (argument reduction by the octant symmetry), the other quadrants
+// by rotation by -i.
+struct Cf {
+    float re, im;
+};
+struct TwTable {
+    Cf v[N];
+};
+constexpr double cx_sin_small(double x) {  // |x| <= pi/4
+    double t = x, s = x;
+    for (int k = 1; k < 14; ++k) {
+        t *= -x * x / ((2.0 * k) * (2.0 * k + 1.0));
+        s += t;
+    }
+    return s;
+}
+constexpr double cx_cos_small(double x) {
+    double t = 1.0, s = 1.0;
+    for (int k = 1; k < 14; ++k) {
+        t *= -x * x / ((2.0 * k - 1.0) * (2.0 * k));
+        s += t;
+    }
+    return s;
+}
+constexpr TwTable make_tw_table() {
+    TwTable t{};
+    const double step = 6.283185307179586476925286766559 / N;
+    for (int n = 0; n <= N / 8; ++n) {  // angle in [0, pi/4]
+        const double c = cx_cos_small(n * step), s = cx_sin_small(n * step);
+        t.v[n] = Cf{(float)c, (float)-s};
+        // angle pi/2 - x: cos <-> sin
+        t.v[N / 4 - n] = Cf{(float)s, (float)-c};
+    }
+    for (int n = N / 4; n < N; ++n) {  // w^n = -i w^(n - N/4)
+        const Cf p = t.v[n - N / 4];
+        t.v[n] = Cf{p.im, -p.re};
+    }
+    return t;
+}
+// Everything the kernel stages into LDS at start-up, in LDS order, as float
+// pairs (rounded to fp16 while staging):
+//   y[(T * 64 + l) * 4 + j]  = w_4096^{T (c + 16 (4 g + j))}  (L2 twiddles)
+//   dft[l * 4 + i]           = w_16^{(4 g + i) c}              (DFT-16 entries)
+//   x[l * 4 + j]             = w_256^{c (4 g + j)}             (L1 twiddles)
+// with lane l = 16 g + c.
+struct ProTable {
+    Cf y[N];
+    Cf dft[256];
+    Cf x[256];
+};
+constexpr ProTable make_pro_table() {
+    const TwTable t = make_tw_table();
+    ProTable p{};
+    for (int T = 0; T < 16; ++T)
+        for (int l = 0; l < 64; ++l)
+            for (int j = 0; j < 4; ++j)
+                p.y[(T * 64 + l) * 4 + j] = t.v[(T * ((l & 15) + 16 * (4 * (l >> 4) + j))) & (N - 1)];
+    for (int l = 0; l < 64; ++l)
+        for (int i = 0; i < 4; ++i) {
+            p.dft[l * 4 + i] = t.v[(256 * (4 * (l >> 4) + i) * (l & 15)) & (N - 1)];
+            p.x[l * 4 + i] = t.v[(16 * (l & 15) * (4 * (l >> 4) + i)) & (N - 1)];
+        }
+    return p;
+}
+__device__ const ProTable kPro = make_pro_table();
+
+// ---------------------------------------------------------- small helpers ---
+__device__ __forceinline__ h2_t as_h2(uint32_t v) { return __builtin_bit_cast(h2_t, v); }
+__device__ __forceinline__ uint32_t as_u32(h2_t v) { return __builtin_bit_cast(uint32_t, v); }
+// (re, im) fp32 -> packed fp16, round to nearest even
+__device__ __forceinline__ uint32_t pk(float re, float im) {
+    const f2_t v = {re, im};
+    return as_u32(__builtin_convertvector(v, h2_t));
+}
+// a * w and a * conj(w) in packed fp16
+__device__ __forceinline__ uint32_t cmul(uint32_t a_, uint32_t w_) {
+    const h2_t a = as_h2(a_), w = as_h2(w_);
+    const h2_t t = a.xx * w;
+    const h2_t ws = {-w.y, w.x};
+    return as_u32(a.yy * ws + t);
+}
+// a * w with ws = (-w.im, w.re) supplied (loop-invariant twiddles)
+__device__ __forceinline__ uint32_t cmul2(uint32_t a_, uint32_t w_, uint32_t ws_) {
+    const h2_t a = as_h2(a_);
+    const h2_t t = a.xx * as_h2(w_);
+    return as_u32(a.yy * as_h2(ws_) + t);
+}
+// a * conj(w) with ws = (-w.im, w.re): (ar wr + ai wi, ai wr - ar wi)
+__device__ __forceinline__ uint32_t cmulc2(uint32_t a_, uint32_t w_, uint32_t ws_) {
+    const h2_t a = as_h2(a_), w = as_h2(w_), ws = as_h2(ws_);
+    const h2_t t = a.yy * w;                 // (ai wr, ai wi)
+    const h2_t u2 = {ws.y, ws.x};            // (wr, -wi)
+    return as_u32(a.xx * u2 + t.yx);         // (ar wr + ai wi, -ar wi + ai wr)
+}
+__device__ __forceinline__ uint32_t cmulc(uint32_t a_, uint32_t w_) {
+    const h2_t a = as_h2(a_), w = as_h2(w_);
+    const h2_t wc = {w.x, -w.y};
+    const h2_t t = a.xx * wc;
+    const h2_t ws = {w.y, w.x};
+    return as_u32(a.yy * ws + t);
+}
+__device__ __forceinline__ h8_t h8_of(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
+    return __builtin_bit_cast(h8_t, make_uint4(a, b, c, d));
+}
+__device__ __forceinline__ f4_t mfma(h8_t a, h8_t b) {
+    const f4_t z = {0.f, 0.f, 0.f, 0.f};
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, z, 0, 0, 0);
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+    return v;
+}
+// exponent e with max = m 2^e, m in [1/2, 1); 0 for 0 / non-finite
+__device__ __forceinline__ int exp_of(float m) {
+    if (!(m > 0.f) || !(m < 3.0e38f)) return 0;
+    int e;
+    frexpf(m, &e);
+    return e;
+}
+
+// 16x16 DFT (entries / 4) as the lane's 8 halves: point i = h / 2 of the
+// K range 4 g .. 4 g + 3, frequency c; the same values serve as A operand
+// (rows = frequency) and as B operand (columns = frequency).
+struct Dft {
+    h8_t re, im;
+};
+
+// Position of tile T's output jj after L2: "P layout".  The G <-> T swap
+// then leaves every L3 tile's four points in four consecutive registers.
+__device__ __forceinline__ constexpr int pidx(int T, int jj) { return 16 * (T >> 2) + 4 * jj + (T & 3); }
+
+template <bool SIG_A>
+__device__ __forceinline__ void quad_mfma(const uint32_t *q, const Dft &F, f4_t &re, f4_t &im) {
+    const h8_t x = h8_of(q[0], q[1], q[2], q[3]);
+    if constexpr (SIG_A) {
+        re = mfma(x, F.re);
+        im = mfma(x, F.im);
+    } else {
+        re = mfma(F.re, x);
+        im = mfma(F.im, x);
+    }
+}
+// One radix-16 layer over slot G on the NQ register quads d[4 tau .. 4 tau + 3].
+// Software-pipelined: the MFMAs of quad tau + 1 (and the LDS operand
+// pre(tau + 1) of its epilogue) are issued before the epilogue of quad tau,
+// and the scheduler may not hoist further (which would keep all 32 results
+// live).  epi(tau, re, im, p) gets the fp32 outputs of quad tau (frequency /
+// row 4 g + jj in element jj) and p = pre(tau).
+struct NoPre {
+    __device__ __forceinline__ uint4 operator()(int) const { return make_uint4(0, 0, 0, 0); }
+};
+template <bool SIG_A, int NQ = 16, class Pre, class Epi>
+__device__ __forceinline__ void layer(uint32_t *d, const Dft &F, Pre &&pre, Epi &&epi) {
+    f4_t re, im;
+    quad_mfma<SIG_A>(d, F, re, im);
+    uint4 pv = pre(0);
+#pragma unroll
+    for (int tau = 0; tau < NQ; ++tau) {
+        f4_t re1, im1;
+        uint4 pv1 = make_uint4(0, 0, 0, 0);
+        if (tau + 1 < NQ) {
+            quad_mfma<SIG_A>(d + 4 * (tau + 1), F, re1, im1);
+            pv1 = pre(tau + 1);
+        }
+        epi(tau, re, im, pv);
+        __builtin_amdgcn_sched_barrier(0);
+        re = re1;
+        im = im1;
+        pv = pv1;
+    }
+}
+
+// Exchange slot G's lane-row bits (lane bits 5, 4) with register-index bits
+// 5, 4.  An involution.
+__device__ __forceinline__ void swap_GT(uint32_t (&d)[64]) {
+#pragma unroll
+    for (int r = 0; r < 32; ++r) {
+        const auto s = __builtin_amdgcn_permlane32_swap(d[r], d[r + 32], false, false);
+        d[r] = s[0];
+        d[r + 32] = s[1];
+    }
+#pragma unroll
+    for (int r = 0; r < 64; ++r) {
+        if (r & 16) continue;
+        const auto s = __builtin_amdgcn_permlane16_swap(d[r], d[r + 16], false, false);
+        d[r] = s[0];
+        d[r + 16] = s[1];
+    }
+}
+
+// Per-lane constants staged in LDS (Lc[kind * 64 + lane]): 0/1 DFT real /
+// imaginary rows, 2/3 the conjugate DFT, 4 the L1 twiddles w_256^{c (4g+j)},
+// 5 the same as (-im, re).  Read right before each layer so that they do not
+// occupy registers across the pair pipeline.
+__device__ __forceinline__ Dft lds_dft(const uint4 *Lc, int lane, bool conj) {
+    asm volatile("" ::: "memory");   // re-read per layer, do not keep live
+    Dft F;
+    F.re = __builtin_bit_cast(h8_t, Lc[(conj ? 2 : 0) * 64 + lane]);
+    F.im = __builtin_bit_cast(h8_t, Lc[(conj ? 3 : 1) * 64 + lane]);
+    return F;
+}
+
+// Forward transform of a register-resident signal up to L3: L1 (signal A) +
+// w_256 twiddle, L2 (signal B) + w_4096 twiddle written in P layout, swap.
+__device__ __forceinline__ void forward_front(uint32_t (&d)[64], const uint4 *Lc, const uint4 *Ytab,
+                                              int lane) {
+    {
+        const Dft F = lds_dft(Lc, lane, false);
+        const uint4 X = Lc[4 * 64 + lane], Xs = Lc[5 * 64 + lane];
+        const uint32_t xw[4] = {X.x, X.y, X.z, X.w}, xs[4] = {Xs.x, Xs.y, Xs.z, Xs.w};
+        layer<true>(d, F, NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) d[4 * tau + jj] = cmul2(pk(re[jj], im[jj]), xw[jj], xs[jj]);
+        });
+    }
+    uint32_t e[64];
+    {
+        const Dft F = lds_dft(Lc, lane, false);
+        layer<false>(d, F, [&](int tau) { return Ytab[tau * 64 + lane]; },
+                     [&](int tau, f4_t re, f4_t im, uint4 y) {
+                         e[pidx(tau, 0)] = cmul(pk(re[0], im[0]), y.x);
+                         e[pidx(tau, 1)] = cmul(pk(re[1], im[1]), y.y);
+                         e[pidx(tau, 2)] = cmul(pk(re[2], im[2]), y.z);
+                         e[pidx(tau, 3)] = cmul(pk(re[3], im[3]), y.w);
+                     });
+    }
+#pragma unroll
+    for (int i = 0; i < 64; ++i) d[i] = e[i];
+    swap_GT(d);
+}
+
+// 16-bit I/O helpers
+template <int DT> __device__ __forceinline__ uint32_t pack_out(float lo, float hi);
+template <> __device__ __forceinline__ uint32_t pack_out<F16>(float lo, float hi) { return pk(lo, hi); }
+template <> __device__ __forceinline__ uint32_t pack_out<BF16>(float lo, float hi) {
+    const f2_t v = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, b2_t));
+}
+template <int DT> __device__ __forceinline__ float lo_f(uint32_t r) {
+    return DT == F16 ? (float)as_h2(r).x : __uint_as_float(r << 16);
+}
+template <int DT> __device__ __forceinline__ float hi_f(uint32_t r) {
+    return DT == F16 ? (float)as_h2(r).y : __uint_as_float(r & 0xffff0000u);
+}
+__device__ __forceinline__ h8_t h8_scale(h8_t v, _Float16 s) {
+    const h8_t sv = {s, s, s, s, s, s, s, s};
+    return v * sv;
+}
+
+}  // namespace wv
+
+// ============================================================================
+// CORR: 0 none, 1 float32 correction term, 2 correction term in the I/O dtype
+template <int DT, int CORR>
+__global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) void fftconv_wave4096_kernel(
+    ConvArgs a, const float *k, int wg_per_ch, int pairs_per_ch) {
+    using namespace wv;
+    __shared__ uint4 Ytab[16 * 64];   // twiddles w_4096^{T (c + 16 (4 g + j))}, per tile T and lane
+    __shared__ uint4 Ks[16 * 64];     // kernel spectrum per L3 quad and lane (also the spectrum's scratch)
+    __shared__ uint4 Lc[6 * 64];      // per-lane DFT rows and L1 twiddles
+    __shared__ float red[NW];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
+    const int g = lane >> 4, c = lane & 15;
+    const int h = blockIdx.x / wg_per_ch, part = blockIdx.x % wg_per_ch;
+    const int per = (pairs_per_ch + wg_per_ch - 1) / wg_per_ch;
+    const int q0 = part * per, q1 = min(q0 + per, pairs_per_ch);
+    const uint16_t *u = (const uint16_t *)a.u;
+    uint16_t *y = (uint16_t *)a.y;
+
+    auto rows = [&](int qq, long &oa, long &ob) {
+        if (a.pair_mode == 0) {
+            oa = ((long)(2 * qq) * a.H + h) * L;
+            ob = (2 * qq + 1 < a.B) ? ((long)(2 * qq + 1) * a.H + h) * L : -1;
+        } else {
+            const int ncp = (a.nchunk + 1) / 2;
+            const int bb = qq / ncp, cp = qq % ncp;
+            oa = (((long)bb * a.H + h) * a.nchunk + 2 * cp) * L;
+            ob = (2 * cp + 1 < a.nchunk) ? oa + L : -1;
+        }
+    };
+    // raw loads of a pair: lanes g < 2 hold points p2 = 4 g + j (j = 0..3),
+    // p1 = c, p0 = 0..15 of both rows (8 consecutive 16-bit values per uint4)
+    uint4 ra[8], rb[8];
+    auto issue_loads = [&](int qq) {
+        long oa, ob;
+        rows(qq, oa, ob);
+        const long obl = ob >= 0 ? ob : oa;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            ra[i] = make_uint4(0, 0, 0, 0);
+            rb[i] = make_uint4(0, 0, 0, 0);
+        }
+        if (g < 2) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const long off = 256 * (4 * g + j) + 16 * c;
+                ra[2 * j] = *(const uint4 *)(u + oa + off);
+                ra[2 * j + 1] = *(const uint4 *)(u + oa + off + 8);
+                rb[2 * j] = *(const uint4 *)(u + obl + off);
+                rb[2 * j + 1] = *(const uint4 *)(u + obl + off + 8);
+            }
+        }
+        if (ob < 0) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) rb[i] = make_uint4(0, 0, 0, 0);
+        }
+    };
+    const int qf = q0 + w;
+    if (qf < q1) issue_loads(qf);   // in flight during the kernel transform
+
+    // stage the constant tables (fp32 pairs -> fp16)
+#pragma unroll
+    for (int sidx = 0; sidx < 4; ++sidx) {
+        const int e = tid + NT * sidx;
+        const float4 v0 = ((const float4 *)kPro.y)[2 * e], v1 = ((const float4 *)kPro.y)[2 * e + 1];
+        Ytab[e] = make_uint4(pk(v0.x, v0.y), pk(v0.z, v0.w), pk(v1.x, v1.y), pk(v1.z, v1.w));
+    }
+    if (w == 0) {
+        const float4 *dt = (const float4 *)(kPro.dft + 4 * lane), *xt = (const float4 *)(kPro.x + 4 * lane);
+        const float4 f01 = dt[0], f23 = dt[1], x01 = xt[0], x23 = xt[1];
+        const float fr[4] = {f01.x, f01.z, f23.x, f23.z}, fi[4] = {f01.y, f01.w, f23.y, f23.w};
+        uint32_t o[6][4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float re = 0.25f * fr[i], im = 0.25f * fi[i];
+            // out.re = sum re(w) x.re - im(w) x.im ; out.im = sum im(w) x.re + re(w) x.im
+            o[0][i] = pk(re, -im);
+            o[1][i] = pk(im, re);
+            o[2][i] = pk(re, im);      // conjugate
+            o[3][i] = pk(-im, re);
+        }
+        const float xr[4] = {x01.x, x01.z, x23.x, x23.z}, xi[4] = {x01.y, x01.w, x23.y, x23.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            o[4][j] = pk(xr[j], xi[j]);
+            o[5][j] = pk(-xi[j], xr[j]);
+        }
+#pragma unroll
+        for (int kd = 0; kd < 6; ++kd) Lc[kd * 64 + lane] = make_uint4(o[kd][0], o[kd][1], o[kd][2], o[kd][3]);
+    }
+
+    // ---- kernel spectrum of channel h, all waves: wave w runs tiles
+    //      4 w .. 4 w + 3 of each layer, exchanging through Ks ----
+    int kexp;
+    {
+        uint32_t *S = (uint32_t *)Ks;   // quad layout: dword (tau * 64 + lane) * 4 + i
+        const float4 k0 = *(const float4 *)(k + (long)h * L + 8 * tid);
+        const float4 k1 = *(const float4 *)(k + (long)h * L + 8 * tid + 4);
+        float kv[8] = {k0.x, k0.y, k0.z, k0.w, k1.x, k1.y, k1.z, k1.w};
+        if (tid == 0 && a.D) kv[0] += a.D[h];   // k[0] += D
+        float mx = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) mx = fmaxf(mx, fabsf(kv[e]));
+        mx = wave_max(mx);
+        if (lane == 0) red[w] = mx;
+        // zero padding p >= 2048: lanes 32..63 of every quad
+#pragma unroll
+        for (int m = 0; m < 8; ++m) {
+            const int lin = tid + NT * m;                   // < 2048
+            const int tau = lin >> 7, l = 32 + ((lin >> 2) & 31), i = lin & 3;
+            S[(tau * 64 + l) * 4 + i] = 0u;
+        }
+        __syncthreads();
+        const int ek = exp_of(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3])));
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int p = 8 * tid + e;                      // < 2048
+            const int p2 = p >> 8, p1 = (p >> 4) & 15, p0 = p & 15;
+            S[(p0 * 64 + 16 * (p2 >> 2) + p1) * 4 + (p2 & 3)] = pk(ldexpf(kv[e], -ek), 0.f);
+        }
+        __syncthreads();
+        uint32_t dq[16];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const uint4 v = Ks[(4 * w + t) * 64 + lane];
+            dq[4 * t + 0] = v.x; dq[4 * t + 1] = v.y; dq[4 * t + 2] = v.z; dq[4 * t + 3] = v.w;
+        }
+        __syncthreads();   // every wave holds its L1 inputs: Ks may be rewritten
+        const Dft F = lds_dft(Lc, lane, false);
+        {
+            const uint4 X = Lc[4 * 64 + lane], Xs = Lc[5 * 64 + lane];
+            const uint32_t xw[4] = {X.x, X.y, X.z, X.w}, xs[4] = {Xs.x, Xs.y, Xs.z, Xs.w};
+            layer<true, 4>(dq, F, NoPre{}, [&](int t, f4_t re, f4_t im, uint4) {
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) dq[4 * t + jj] = cmul2(pk(re[jj], im[jj]), xw[jj], xs[jj]);
+            });
+        }
+        layer<false, 4>(dq, F, NoPre{}, [&](int t, f4_t re, f4_t im, uint4) {
+            const int T = 4 * w + t;
+            const uint4 yv = Ytab[T * 64 + lane];
+            const uint32_t o[4] = {cmul(pk(re[0], im[0]), yv.x), cmul(pk(re[1], im[1]), yv.y),
+                                   cmul(pk(re[2], im[2]), yv.z), cmul(pk(re[3], im[3]), yv.w)};
+            // after the swap: lane 16 (T >> 2) + c, L3 quad 4 g + jj, element T & 3
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) S[((4 * g + jj) * 64 + 16 * (T >> 2) + c) * 4 + (T & 3)] = o[jj];
+        });
+        __syncthreads();
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const uint4 v = Ks[(4 * w + t) * 64 + lane];
+            dq[4 * t + 0] = v.x; dq[4 * t + 1] = v.y; dq[4 * t + 2] = v.z; dq[4 * t + 3] = v.w;
+        }
+        layer<false, 4>(dq, F, NoPre{}, [&](int t, f4_t re, f4_t im, uint4) {
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) dq[4 * t + jj] = pk(re[jj], im[jj]);
+        });
+        h2_t hmx = {0, 0}, hmn = {0, 0};
+#pragma unroll
+        for (int i = 0; i < 16; i += 2) {
+            hmx = __builtin_elementwise_maximum(hmx, __builtin_elementwise_maximum(as_h2(dq[i]), as_h2(dq[i + 1])));
+            hmn = __builtin_elementwise_minimum(hmn, __builtin_elementwise_minimum(as_h2(dq[i]), as_h2(dq[i + 1])));
+        }
+        float km = fmaxf(fmaxf((float)hmx.x, (float)hmx.y), fmaxf(-(float)hmn.x, -(float)hmn.y));
+        km = wave_max(km);
+        __syncthreads();   // red[] reuse
+        if (lane == 0) red[w] = km;
+        __syncthreads();
+        const int e2 = exp_of(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3])));   // in [-6, 6]
+        const _Float16 s2 = (_Float16)ldexpf(1.0f, -e2);
+        const h2_t s22 = {s2, s2};
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            Ks[(4 * w + t) * 64 + lane] = make_uint4(as_u32(as_h2(dq[4 * t]) * s22), as_u32(as_h2(dq[4 * t + 1]) * s22),
+                                                   as_u32(as_h2(dq[4 * t + 2]) * s22), as_u32(as_h2(dq[4 * t + 3]) * s22));
+        kexp = 6 + ek + e2;
+        __syncthreads();   // Ks complete
+    }
+
+    // ---- row pairs of this wave ----
+    uint32_t d[64];
+    for (int qq = qf; qq < q1; qq += NW) {
+        // max |u|, then packing into (a + i b) complex fp16: p2 = 4 g + j : G,
+        // p1 = c : C, p0 = T : tile
+        float mx;
+        if (DT == F16) {
+            h2_t hmx = {0, 0}, hmn = {0, 0};
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const uint32_t v[8] = {ra[i].x, ra[i].y, ra[i].z, ra[i].w, rb[i].x, rb[i].y, rb[i].z, rb[i].w};
+#pragma unroll
+                for (int e = 0; e < 8; e += 2) {
+                    hmx = __builtin_elementwise_maximum(hmx, __builtin_elementwise_maximum(as_h2(v[e]), as_h2(v[e + 1])));
+                    hmn = __builtin_elementwise_minimum(hmn, __builtin_elementwise_minimum(as_h2(v[e]), as_h2(v[e + 1])));
+                }
+            }
+            mx = fmaxf(fmaxf((float)hmx.x, (float)hmx.y), fmaxf(-(float)hmn.x, -(float)hmn.y));
+        } else {
+            uint32_t mb = 0;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const uint32_t v[8] = {ra[i].x, ra[i].y, ra[i].z, ra[i].w, rb[i].x, rb[i].y, rb[i].z, rb[i].w};
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const uint32_t m = v[e] & 0x7fff7fffu;
+                    mb = max(mb, max(m & 0xffffu, m >> 16));
+                }
+            }
+            mx = __uint_as_float(mb << 16);
+        }
+        mx = wave_max(mx);
+        int eu = 0;
+        if (DT == BF16 || !(mx >= 0.0625f && mx < 16.0f)) eu = exp_of(mx);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+#pragma unroll
+            for (int hf = 0; hf < 2; ++hf) {
+                const uint4 va = ra[2 * j + hf], vb = rb[2 * j + hf];
+                const uint32_t A4[4] = {va.x, va.y, va.z, va.w}, B4[4] = {vb.x, vb.y, vb.z, vb.w};
+#pragma unroll
+                for (int s = 0; s < 4; ++s) {
+                    const int T = 8 * hf + 2 * s;
+                    if (DT == F16) {
+                        d[4 * T + j] = __builtin_amdgcn_perm(B4[s], A4[s], 0x05040100u);
+                        d[4 * (T + 1) + j] = __builtin_amdgcn_perm(B4[s], A4[s], 0x07060302u);
+                    } else {
+                        d[4 * T + j] = pk(ldexpf(lo_f<DT>(A4[s]), -eu), ldexpf(lo_f<DT>(B4[s]), -eu));
+                        d[4 * (T + 1) + j] = pk(ldexpf(hi_f<DT>(A4[s]), -eu), ldexpf(hi_f<DT>(B4[s]), -eu));
+                    }
+                }
+            }
+        }
+        if (DT == F16 && eu != 0) {
+            const _Float16 s = (_Float16)ldexpf(1.0f, -eu);
+            const h2_t s2 = {s, s};
+#pragma unroll
+            for (int i = 0; i < 64; ++i) d[i] = as_u32(as_h2(d[i]) * s2);
+        }
+
+        forward_front(d, Lc, Ytab, lane);
+        // L3 + pointwise product with the kernel spectrum (quads in P layout)
+        layer<false>(d, lds_dft(Lc, lane, false), [&](int tau) { return Ks[tau * 64 + lane]; },
+                     [&](int tau, f4_t re, f4_t im, uint4 kk) {
+            d[4 * tau + 0] = cmul(pk(re[0], im[0]), kk.x);
+            d[4 * tau + 1] = cmul(pk(re[1], im[1]), kk.y);
+            d[4 * tau + 2] = cmul(pk(re[2], im[2]), kk.z);
+            d[4 * tau + 3] = cmul(pk(re[3], im[3]), kk.w);
+        });
+        // inverse: L3^H, swap, conj twiddle (back to quad-per-tile layout),
+        // L2^H (signal A) + conj twiddle, L1^H
+        layer<false>(d, lds_dft(Lc, lane, true), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) d[4 * tau + jj] = pk(re[jj], im[jj]);
+        });
+        swap_GT(d);
+        {
+            uint32_t e[64];
+#pragma unroll
+            for (int T = 0; T < 16; ++T) {
+                const uint4 yv = Ytab[T * 64 + lane];
+                e[4 * T + 0] = cmulc(d[pidx(T, 0)], yv.x);
+                e[4 * T + 1] = cmulc(d[pidx(T, 1)], yv.y);
+                e[4 * T + 2] = cmulc(d[pidx(T, 2)], yv.z);
+                e[4 * T + 3] = cmulc(d[pidx(T, 3)], yv.w);
+            }
+#pragma unroll
+            for (int i = 0; i < 64; ++i) d[i] = e[i];
+        }
+        {
+            const uint4 X = Lc[4 * 64 + lane], Xs = Lc[5 * 64 + lane];
+            const uint32_t xw[4] = {X.x, X.y, X.z, X.w}, xs[4] = {Xs.x, Xs.y, Xs.z, Xs.w};
+            layer<true>(d, lds_dft(Lc, lane, true), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) d[4 * tau + jj] = cmulc2(pk(re[jj], im[jj]), xw[jj], xs[jj]);
+            });
+        }
+        // L1^H: outputs p2 = 4 g + i (kept for g < 2), p1 = c, p0 = tile.
+        // The output scale 2^(kexp + eu) rides on the DFT matrix as far as fp16
+        // allows; any remainder is applied in fp32.
+        long oa, ob;
+        rows(qq, oa, ob);
+        const int se = kexp + eu;
+        const int sf = min(max(se, -10), 14), srem = se - sf;
+        const float rem = ldexpf(1.0f, srem);
+        Dft Fs = lds_dft(Lc, lane, true);
+        Fs.re = h8_scale(Fs.re, (_Float16)ldexpf(1.0f, sf));
+        Fs.im = h8_scale(Fs.im, (_Float16)ldexpf(1.0f, sf));
+        float pr[8];   // previous (even) tile's outputs: rows a and b
+        layer<false>(d, Fs, NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+            float ya[4], yb[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                ya[i] = re[i];
+                yb[i] = im[i];
+            }
+            if (srem != 0) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    ya[i] *= rem;
+                    yb[i] *= rem;
+                }
+            }
+            if (CORR != 0 && g < 2) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const long p = 256 * (4 * g + i) + 16 * c + tau;
+                    if (CORR == 2) {
+                        const uint16_t *cr = (const uint16_t *)a.corr;
+                        ya[i] += lo_f<DT>(cr[oa + p]);
+                        if (ob >= 0) yb[i] += lo_f<DT>(cr[ob + p]);
+                    } else {
+                        const float *cr = (const float *)a.corr;
+                        ya[i] += cr[oa + p];
+                        if (ob >= 0) yb[i] += cr[ob + p];
+                    }
+                }
+            }
+            if ((tau & 1) == 0) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    pr[i] = ya[i];
+                    pr[4 + i] = yb[i];
+                }
+            } else {
+                // tiles tau - 1, tau: row a -> d[4 (tau - 1) + i], row b -> d[4 tau + i]
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    d[4 * (tau - 1) + i] = pack_out<DT>(pr[i], ya[i]);
+                    d[4 * tau + i] = pack_out<DT>(pr[4 + i], yb[i]);
+                }
+            }
+        });
+        if (g < 2) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const long off = 256 * (4 * g + i) + 16 * c;
+                // row a: dwords d[8 s + i] hold points 2 s, 2 s + 1
+                *(uint4 *)(y + oa + off) = make_uint4(d[i], d[8 + i], d[16 + i], d[24 + i]);
+                *(uint4 *)(y + oa + off + 8) = make_uint4(d[32 + i], d[40 + i], d[48 + i], d[56 + i]);
+                if (ob >= 0) {
+                    *(uint4 *)(y + ob + off) = make_uint4(d[4 + i], d[12 + i], d[20 + i], d[28 + i]);
+                    *(uint4 *)(y + ob + off + 8) = make_uint4(d[36 + i], d[44 + i], d[52 + i], d[60 + i]);
+                }
+            }
+        }
+        // next pair's loads, consumed at the top of the next iteration
+        if (qq + NW < q1) issue_loads(qq + NW);
+    }
+}
+
+bool fftconv_wave_supported(int L, int dtype) { return L == wv::L && (dtype == F16 || dtype == BF16); }
+
+hipError_t launch_fftconv_wave(const ConvArgs &a, const float *k, hipStream_t s) {
+    if (!fftconv_wave_supported(a.L, a.dtype)) return hipErrorInvalidValue;
+    int pairs_per_ch;
+    if (a.pair_mode == 0)
+        pairs_per_ch = (a.B + 1) / 2;
+    else
+        pairs_per_ch = a.B * ((a.nchunk + 1) / 2);
+    // split a channel over several workgroups only while the chip would hold
+    // fewer than ~2 waves per SIMD and each wave still gets a pair
+    int wg_per_ch = 1;
+    while ((long)a.H * wg_per_ch * wv::NW < 2048 && pairs_per_ch >= 2 * wv::NW * wg_per_ch) wg_per_ch *= 2;
+    dim3 grid(a.H * wg_per_ch), block(wv::NT);
+    const int corr = a.corr == nullptr ? 0 : (a.corr16 ? 2 : 1);
+#define H3_WAVE_LAUNCH(DTV, CV) \
+    hipLaunchKernelGGL((fftconv_wave4096_kernel<DTV, CV>), grid, block, 0, s, a, k, wg_per_ch, pairs_per_ch)
+    if (a.dtype == F16) {
+        if (corr == 0) H3_WAVE_LAUNCH(F16, 0);
+        else if (corr == 1) H3_WAVE_LAUNCH(F16, 1);
+        else H3_WAVE_LAUNCH(F16, 2);
+    } else {
+        if (corr == 0) H3_WAVE_LAUNCH(BF16, 0);
+        else if (corr == 1) H3_WAVE_LAUNCH(BF16, 1);
+        else H3_WAVE_LAUNCH(BF16, 2);
+    }
+#undef H3_WAVE_LAUNCH
+    return hipGetLastError();
+}
+
+}  // namespace h3

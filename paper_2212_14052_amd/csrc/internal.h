@@ -41,6 +41,10 @@ hipError_t launch_fftconv(const ConvArgs &a, hipStream_t s);
 // spectrum from k itself; returns hipErrorInvalidValue for other shapes.
 hipError_t launch_fftconv_mfma(const ConvArgs &a, const float *k, hipStream_t s);
 bool fftconv_mfma_supported(int L, int dtype);
+// One-wavefront-per-transform variant for L = 2048 (16-bit I/O); used by
+// launch_fftconv_mfma for that length.
+hipError_t launch_fftconv_wave(const ConvArgs &a, const float *k, hipStream_t s);
+bool fftconv_wave_supported(int L, int dtype);
 
 size_t fftconv_workspace(int B, int H, int L);
 
