@@ -292,7 +292,7 @@ def main():
                    "buffer_sets": head["nsets"]},
         "roofline": {"bound": "hbm", "achieved": round(head["conv_gbs"], 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(head["conv_gbs"] / HBM_PEAK_GBS, 4), "traffic": None,
-                     "kernel": "fftconv_mfma4096_kernel<f16>", "bytes_per_launch": head["conv_bytes"]},
+                     "kernel": "fftconv_wave4096_kernel<f16>", "bytes_per_launch": head["conv_bytes"]},
     }
     if extra:
         res["extra"] = extra

@@ -27,9 +27,17 @@ FLAGS = [
 ]
 
 
+# per-source extra flags
+EXTRA = {
+    # MFMA results in VGPRs: the fused conv's epilogues read every result
+    # with the VALU, so AGPR destinations only add copies
+    "fftconv_wave.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", src, "-o", obj]
+    cmd = [HIPCC, *FLAGS, *EXTRA.get(os.path.basename(src), []), "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{r.stdout}\n{r.stderr}")

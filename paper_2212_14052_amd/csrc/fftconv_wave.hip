@@ -323,7 +323,7 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
     __shared__ uint4 Ytab[16 * 64];   // twiddles w_4096^{T (c + 16 (4 g + j))}, per tile T and lane
     __shared__ uint4 Ks[16 * 64];     // kernel spectrum per L3 quad and lane (also the spectrum's scratch)
     __shared__ uint4 Lc[6 * 64];      // per-lane DFT rows and L1 twiddles
-    __shared__ float red[NW];
+    __shared__ float red[2 * NW];
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
     const int g = lane >> 4, c = lane & 15;
@@ -371,19 +371,41 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
             for (int i = 0; i < 8; ++i) rb[i] = make_uint4(0, 0, 0, 0);
         }
     };
-    const int qf = q0 + w;
-    if (qf < q1) issue_loads(qf);   // in flight during the kernel transform
+    // Loads in the order they are needed.  (1) this wave's L1 tiles of the
+    // kernel row: lane (g < 2, c) takes k[256 (4 g + j) + 16 c + 4 w + t],
+    // t = 0..3, for j = 0..3 (tile T = 4 w + t, point p2 = 4 g + j).
+    float4 kq[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        kq[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (g < 2) kq[j] = *(const float4 *)(k + (long)h * L + 256 * (4 * g + j) + 16 * c + 4 * w);
+    }
+    // (2) the constant tables
+    float4 ty[8];
+#pragma unroll
+    for (int sidx = 0; sidx < 4; ++sidx) {
+        const int e = tid + NT * sidx;
+        ty[2 * sidx] = ((const float4 *)kPro.y)[2 * e];
+        ty[2 * sidx + 1] = ((const float4 *)kPro.y)[2 * e + 1];
+    }
+    float4 tdx[4];
+    if (w == 0) {
+        const float4 *dt = (const float4 *)(kPro.dft + 4 * lane), *xt = (const float4 *)(kPro.x + 4 * lane);
+        tdx[0] = dt[0]; tdx[1] = dt[1]; tdx[2] = xt[0]; tdx[3] = xt[1];
+    }
+    // (3) this wave's first pair, in flight during the kernel transform
+    int qq = q0 + w;
+    bool have = qq < q1;
+    if (have) issue_loads(qq);
 
     // stage the constant tables (fp32 pairs -> fp16)
 #pragma unroll
     for (int sidx = 0; sidx < 4; ++sidx) {
-        const int e = tid + NT * sidx;
-        const float4 v0 = ((const float4 *)kPro.y)[2 * e], v1 = ((const float4 *)kPro.y)[2 * e + 1];
-        Ytab[e] = make_uint4(pk(v0.x, v0.y), pk(v0.z, v0.w), pk(v1.x, v1.y), pk(v1.z, v1.w));
+        const float4 v0 = ty[2 * sidx], v1 = ty[2 * sidx + 1];
+        Ytab[tid + NT * sidx] = make_uint4(pk(v0.x, v0.y), pk(v0.z, v0.w), pk(v1.x, v1.y), pk(v1.z, v1.w));
     }
     if (w == 0) {
-        const float4 *dt = (const float4 *)(kPro.dft + 4 * lane), *xt = (const float4 *)(kPro.x + 4 * lane);
-        const float4 f01 = dt[0], f23 = dt[1], x01 = xt[0], x23 = xt[1];
+        const float4 f01 = tdx[0], f23 = tdx[1], x01 = tdx[2], x23 = tdx[3];
         const float fr[4] = {f01.x, f01.z, f23.x, f23.z}, fi[4] = {f01.y, f01.w, f23.y, f23.w};
         uint32_t o[6][4];
 #pragma unroll
@@ -406,42 +428,28 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
     }
 
     // ---- kernel spectrum of channel h, all waves: wave w runs tiles
-    //      4 w .. 4 w + 3 of each layer, exchanging through Ks ----
-    int kexp;
+    //      4 w .. 4 w + 3 of L1 and L2 and quads 4 w .. 4 w + 3 of L3; the
+    //      swap between L2 and L3 goes through Ks.  Ks ends up holding
+    //      F(k + D delta) 2^-ek / 64; the pairs' L3 matrix carries 2^-e2.
+    int kexp, e2;
     {
-        uint32_t *S = (uint32_t *)Ks;   // quad layout: dword (tau * 64 + lane) * 4 + i
-        const float4 k0 = *(const float4 *)(k + (long)h * L + 8 * tid);
-        const float4 k1 = *(const float4 *)(k + (long)h * L + 8 * tid + 4);
-        float kv[8] = {k0.x, k0.y, k0.z, k0.w, k1.x, k1.y, k1.z, k1.w};
-        if (tid == 0 && a.D) kv[0] += a.D[h];   // k[0] += D
+        if (tid == 0 && a.D) kq[0].x += a.D[h];   // k[0] += D: lane 0, point 0 of tile 0
         float mx = 0.f;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) mx = fmaxf(mx, fabsf(kv[e]));
+        for (int j = 0; j < 4; ++j)
+            mx = fmaxf(mx, fmaxf(fmaxf(fabsf(kq[j].x), fabsf(kq[j].y)), fmaxf(fabsf(kq[j].z), fabsf(kq[j].w))));
         mx = wave_max(mx);
         if (lane == 0) red[w] = mx;
-        // zero padding p >= 2048: lanes 32..63 of every quad
+        __syncthreads();   // red, Ytab, Lc
+        const int ek = __builtin_amdgcn_readfirstlane(exp_of(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]))));
+        uint32_t dq[16];   // quad t = tile 4 w + t, element j
 #pragma unroll
-        for (int m = 0; m < 8; ++m) {
-            const int lin = tid + NT * m;                   // < 2048
-            const int tau = lin >> 7, l = 32 + ((lin >> 2) & 31), i = lin & 3;
-            S[(tau * 64 + l) * 4 + i] = 0u;
+        for (int j = 0; j < 4; ++j) {
+            dq[0 + j] = pk(ldexpf(kq[j].x, -ek), 0.f);
+            dq[4 + j] = pk(ldexpf(kq[j].y, -ek), 0.f);
+            dq[8 + j] = pk(ldexpf(kq[j].z, -ek), 0.f);
+            dq[12 + j] = pk(ldexpf(kq[j].w, -ek), 0.f);
         }
-        __syncthreads();
-        const int ek = exp_of(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3])));
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int p = 8 * tid + e;                      // < 2048
-            const int p2 = p >> 8, p1 = (p >> 4) & 15, p0 = p & 15;
-            S[(p0 * 64 + 16 * (p2 >> 2) + p1) * 4 + (p2 & 3)] = pk(ldexpf(kv[e], -ek), 0.f);
-        }
-        __syncthreads();
-        uint32_t dq[16];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            const uint4 v = Ks[(4 * w + t) * 64 + lane];
-            dq[4 * t + 0] = v.x; dq[4 * t + 1] = v.y; dq[4 * t + 2] = v.z; dq[4 * t + 3] = v.w;
-        }
-        __syncthreads();   // every wave holds its L1 inputs: Ks may be rewritten
         const Dft F = lds_dft(Lc, lane, false);
         {
             const uint4 X = Lc[4 * 64 + lane], Xs = Lc[5 * 64 + lane];
@@ -451,15 +459,18 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
                 for (int jj = 0; jj < 4; ++jj) dq[4 * t + jj] = cmul2(pk(re[jj], im[jj]), xw[jj], xs[jj]);
             });
         }
-        layer<false, 4>(dq, F, NoPre{}, [&](int t, f4_t re, f4_t im, uint4) {
-            const int T = 4 * w + t;
-            const uint4 yv = Ytab[T * 64 + lane];
-            const uint32_t o[4] = {cmul(pk(re[0], im[0]), yv.x), cmul(pk(re[1], im[1]), yv.y),
-                                   cmul(pk(re[2], im[2]), yv.z), cmul(pk(re[3], im[3]), yv.w)};
-            // after the swap: lane 16 (T >> 2) + c, L3 quad 4 g + jj, element T & 3
-#pragma unroll
-            for (int jj = 0; jj < 4; ++jj) S[((4 * g + jj) * 64 + 16 * (T >> 2) + c) * 4 + (T & 3)] = o[jj];
+        layer<false, 4>(dq, F, [&](int t) { return Ytab[(4 * w + t) * 64 + lane]; },
+                        [&](int t, f4_t re, f4_t im, uint4 yv) {
+            dq[4 * t + 0] = cmul(pk(re[0], im[0]), yv.x);
+            dq[4 * t + 1] = cmul(pk(re[1], im[1]), yv.y);
+            dq[4 * t + 2] = cmul(pk(re[2], im[2]), yv.z);
+            dq[4 * t + 3] = cmul(pk(re[3], im[3]), yv.w);
         });
+        // after the swap, tile T = 4 w + t output jj sits in lane 16 w + c,
+        // L3 quad 4 g + jj, element t: one 16-byte write per jj
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj)
+            Ks[(4 * g + jj) * 64 + 16 * w + c] = make_uint4(dq[jj], dq[4 + jj], dq[8 + jj], dq[12 + jj]);
         __syncthreads();
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
@@ -478,23 +489,21 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
         }
         float km = fmaxf(fmaxf((float)hmx.x, (float)hmx.y), fmaxf(-(float)hmn.x, -(float)hmn.y));
         km = wave_max(km);
-        __syncthreads();   // red[] reuse
-        if (lane == 0) red[w] = km;
-        __syncthreads();
-        const int e2 = exp_of(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3])));   // in [-6, 6]
-        const _Float16 s2 = (_Float16)ldexpf(1.0f, -e2);
-        const h2_t s22 = {s2, s2};
+        if (lane == 0) red[NW + w] = km;
 #pragma unroll
         for (int t = 0; t < 4; ++t)
-            Ks[(4 * w + t) * 64 + lane] = make_uint4(as_u32(as_h2(dq[4 * t]) * s22), as_u32(as_h2(dq[4 * t + 1]) * s22),
-                                                   as_u32(as_h2(dq[4 * t + 2]) * s22), as_u32(as_h2(dq[4 * t + 3]) * s22));
-        kexp = 6 + ek + e2;
+            Ks[(4 * w + t) * 64 + lane] = make_uint4(dq[4 * t], dq[4 * t + 1], dq[4 * t + 2], dq[4 * t + 3]);
         __syncthreads();   // Ks complete
+        e2 = __builtin_amdgcn_readfirstlane(
+            exp_of(fmaxf(fmaxf(red[NW], red[NW + 1]), fmaxf(red[NW + 2], red[NW + 3]))));   // in [-6, 6]
+        kexp = 6 + ek + e2;
     }
 
     // ---- row pairs of this wave ----
     uint32_t d[64];
-    for (int qq = qf; qq < q1; qq += NW) {
+    // One flag guards both the prefetch and the back edge, so the staged
+    // registers are dead between their unpacking and the next prefetch.
+    while (have) {
         // max |u|, then packing into (a + i b) complex fp16: p2 = 4 g + j : G,
         // p1 = c : C, p0 = T : tile
         float mx;
@@ -526,6 +535,7 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
         mx = wave_max(mx);
         int eu = 0;
         if (DT == BF16 || !(mx >= 0.0625f && mx < 16.0f)) eu = exp_of(mx);
+        eu = __builtin_amdgcn_readfirstlane(eu);   // equal in all lanes
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
 #pragma unroll
@@ -553,8 +563,12 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
         }
 
         forward_front(d, Lc, Ytab, lane);
-        // L3 + pointwise product with the kernel spectrum (quads in P layout)
-        layer<false>(d, lds_dft(Lc, lane, false), [&](int tau) { return Ks[tau * 64 + lane]; },
+        // L3 (matrix scaled by 2^-e2, the spectrum's normalisation) +
+        // pointwise product with the kernel spectrum (quads in P layout)
+        Dft F3 = lds_dft(Lc, lane, false);
+        F3.re = h8_scale(F3.re, (_Float16)ldexpf(1.0f, -e2));
+        F3.im = h8_scale(F3.im, (_Float16)ldexpf(1.0f, -e2));
+        layer<false>(d, F3, [&](int tau) { return Ks[tau * 64 + lane]; },
                      [&](int tau, f4_t re, f4_t im, uint4 kk) {
             d[4 * tau + 0] = cmul(pk(re[0], im[0]), kk.x);
             d[4 * tau + 1] = cmul(pk(re[1], im[1]), kk.y);
@@ -659,7 +673,9 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
             }
         }
         // next pair's loads, consumed at the top of the next iteration
-        if (qq + NW < q1) issue_loads(qq + NW);
+        qq += NW;
+        have = qq < q1;
+        if (have) issue_loads(qq);
     }
 }
 
