@@ -128,6 +128,69 @@ constexpr ProTable make_pro_table() {
 }
 __device__ const ProTable kPro = make_pro_table();
 
+// IEEE binary16 bits of x, round to nearest even (|x| < 65504, no NaN / inf).
+constexpr uint32_t h16_bits(double x) {
+    uint32_t sign = x < 0 ? 0x8000u : 0u;
+    double a = x < 0 ? -x : x;
+    if (a < 5.9604644775390625e-08 * 0.5) return sign;   // rounds to zero
+    int e = 0;
+    while (a >= 2.0) { a *= 0.5; ++e; }
+    while (a < 1.0) { a *= 2.0; --e; }
+    if (e < -14) {   // subnormal: multiple of 2^-24
+        double m = a;
+        for (int i = e; i < -24; ++i) m *= 0.5;
+        for (int i = -24; i < e; ++i) m *= 2.0;
+        const double fl = (double)(long long)m;
+        double r = m - fl;
+        long long q = (long long)fl;
+        if (r > 0.5 || (r == 0.5 && (q & 1))) ++q;
+        return sign | (uint32_t)q;
+    }
+    const double m = (a - 1.0) * 1024.0;
+    long long q = (long long)m;
+    const double r = m - (double)q;
+    if (r > 0.5 || (r == 0.5 && (q & 1))) ++q;
+    if (q == 1024) { q = 0; ++e; }
+    return sign | ((uint32_t)(e + 15) << 10) | (uint32_t)q;
+}
+constexpr uint32_t h2_bits(double re, double im) { return h16_bits(re) | (h16_bits(im) << 16); }
+
+// The same tables in fp16 and in LDS order, staged with LDS-direct loads:
+//   [0, 1024)      Ytab[T * 64 + l]: the four L2 twiddles of tile T, lane l
+//   [1024, 1408)   Lc[kind * 64 + l]: DFT rows (real, imaginary), conjugate
+//                  DFT rows, L1 twiddles w and (-im w, re w)
+constexpr int kTabY = 1024, kTabLc = 384, kTab = kTabY + kTabLc;   // in uint4
+struct HalfTable {
+    uint32_t v[4 * kTab];
+};
+constexpr HalfTable make_half_table() {
+    const TwTable t = make_tw_table();
+    HalfTable h{};
+    for (int T = 0; T < 16; ++T)
+        for (int l = 0; l < 64; ++l)
+            for (int j = 0; j < 4; ++j) {
+                const Cf w = t.v[(T * ((l & 15) + 16 * (4 * (l >> 4) + j))) & (N - 1)];
+                h.v[(T * 64 + l) * 4 + j] = h2_bits(w.re, w.im);
+            }
+    for (int l = 0; l < 64; ++l)
+        for (int i = 0; i < 4; ++i) {
+            const Cf w = t.v[(256 * (4 * (l >> 4) + i) * (l & 15)) & (N - 1)];
+            const double re = 0.25 * w.re, im = 0.25 * w.im;
+            // out.re = sum re(w) x.re - im(w) x.im ; out.im = sum im(w) x.re + re(w) x.im
+            h.v[4 * (kTabY + 0 * 64 + l) + i] = h2_bits(re, -im);
+            h.v[4 * (kTabY + 1 * 64 + l) + i] = h2_bits(im, re);
+            h.v[4 * (kTabY + 2 * 64 + l) + i] = h2_bits(re, im);    // conjugate
+            h.v[4 * (kTabY + 3 * 64 + l) + i] = h2_bits(-im, re);
+            const Cf x = t.v[(16 * (l & 15) * (4 * (l >> 4) + i)) & (N - 1)];
+            h.v[4 * (kTabY + 4 * 64 + l) + i] = h2_bits(x.re, x.im);
+            h.v[4 * (kTabY + 5 * 64 + l) + i] = h2_bits(-x.im, x.re);
+        }
+    return h;
+}
+__device__ const HalfTable kHalf = make_half_table();
+typedef __attribute__((address_space(1))) void gvoid_t;
+typedef __attribute__((address_space(3))) void lvoid_t;
+
 // ---------------------------------------------------------- small helpers ---
 __device__ __forceinline__ h2_t as_h2(uint32_t v) { return __builtin_bit_cast(h2_t, v); }
 __device__ __forceinline__ uint32_t as_u32(h2_t v) { return __builtin_bit_cast(uint32_t, v); }
@@ -170,10 +233,21 @@ __device__ __forceinline__ f4_t mfma(h8_t a, h8_t b) {
     const f4_t z = {0.f, 0.f, 0.f, 0.f};
     return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, z, 0, 0, 0);
 }
+// Maximum over the wavefront, returned wave-uniform: xor-swizzles within
+// each half (immediate patterns, no lane-address registers), then the two
+// halves' results read as scalars.
+template <int XOR> __device__ __forceinline__ float swz_xor(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), (XOR << 10) | 0x1F));
+}
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-    return v;
+    v = fmaxf(v, swz_xor<1>(v));
+    v = fmaxf(v, swz_xor<2>(v));
+    v = fmaxf(v, swz_xor<4>(v));
+    v = fmaxf(v, swz_xor<8>(v));
+    v = fmaxf(v, swz_xor<16>(v));
+    const float lo = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
+    const float hi = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
+    return fmaxf(lo, hi);
 }
 // exponent e with max = m 2^e, m in [1/2, 1); 0 for 0 / non-finite
 __device__ __forceinline__ int exp_of(float m) {
@@ -253,6 +327,9 @@ __device__ __forceinline__ void swap_GT(uint32_t (&d)[64]) {
     }
 }
 
+// s_waitcnt encoding (gfx9): vmcnt <= 16, lgkmcnt and expcnt unconstrained
+constexpr int kWaitVm16 = 0x4F70;
+
 // Per-lane constants staged in LDS (Lc[kind * 64 + lane]): 0/1 DFT real /
 // imaginary rows, 2/3 the conjugate DFT, 4 the L1 twiddles w_256^{c (4g+j)},
 // 5 the same as (-im, re).  Read right before each layer so that they do not
@@ -312,6 +389,54 @@ __device__ __forceinline__ h8_t h8_scale(h8_t v, _Float16 s) {
     return v * sv;
 }
 
+// L1^H with the output epilogue: fp32 outputs (times rem when REM), plus the
+// correction term (read for every lane: outputs of lanes g >= 2 and of a
+// missing row b are discarded), packed two tiles at a time into d (row a in
+// d[8 s + i], row b in d[8 s + 4 + i], points 2 s and 2 s + 1).
+template <int DT, int CORR, bool REM>
+__device__ __forceinline__ void out_layer(uint32_t (&d)[64], const Dft &Fs, float rem, const void *corr, long oa,
+                                          long obc, int lane) {
+    const int g = lane >> 4, c = lane & 15;
+    const int pbase = 256 * (4 * (g & 1)) + 16 * c;   // lanes g >= 2 alias g - 2 (in bounds)
+    float pr[8];   // previous (even) tile's outputs: rows a and b
+    layer<false>(d, Fs, NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+        float ya[4], yb[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            ya[i] = REM ? re[i] * rem : re[i];
+            yb[i] = REM ? im[i] * rem : im[i];
+        }
+        if (CORR != 0) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int p = pbase + 256 * i + tau;
+                if (CORR == 2) {
+                    const uint16_t *cr = (const uint16_t *)corr;
+                    ya[i] += lo_f<DT>(cr[oa + p]);
+                    yb[i] += lo_f<DT>(cr[obc + p]);
+                } else {
+                    const float *cr = (const float *)corr;
+                    ya[i] += cr[oa + p];
+                    yb[i] += cr[obc + p];
+                }
+            }
+        }
+        if ((tau & 1) == 0) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                pr[i] = ya[i];
+                pr[4 + i] = yb[i];
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                d[4 * (tau - 1) + i] = pack_out<DT>(pr[i], ya[i]);
+                d[4 * tau + i] = pack_out<DT>(pr[4 + i], yb[i]);
+            }
+        }
+    });
+}
+
 }  // namespace wv
 
 // ============================================================================
@@ -320,9 +445,9 @@ template <int DT, int CORR>
 __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) void fftconv_wave4096_kernel(
     ConvArgs a, const float *k, int wg_per_ch, int pairs_per_ch) {
     using namespace wv;
-    __shared__ uint4 Ytab[16 * 64];   // twiddles w_4096^{T (c + 16 (4 g + j))}, per tile T and lane
+    __shared__ uint4 Tab[kTab];       // Ytab (L2 twiddles per tile and lane) + Lc (per-lane constants)
     __shared__ uint4 Ks[16 * 64];     // kernel spectrum per L3 quad and lane (also the spectrum's scratch)
-    __shared__ uint4 Lc[6 * 64];      // per-lane DFT rows and L1 twiddles
+    uint4 *Ytab = Tab, *Lc = Tab + kTabY;
     __shared__ float red[2 * NW];
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
@@ -357,13 +482,14 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
             rb[i] = make_uint4(0, 0, 0, 0);
         }
         if (g < 2) {
+            const uint16_t *ua = u + oa, *ub = u + obl;   // wave-uniform bases
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const long off = 256 * (4 * g + j) + 16 * c;
-                ra[2 * j] = *(const uint4 *)(u + oa + off);
-                ra[2 * j + 1] = *(const uint4 *)(u + oa + off + 8);
-                rb[2 * j] = *(const uint4 *)(u + obl + off);
-                rb[2 * j + 1] = *(const uint4 *)(u + obl + off + 8);
+                const int off = 256 * (4 * g + j) + 16 * c;
+                ra[2 * j] = *(const uint4 *)(ua + off);
+                ra[2 * j + 1] = *(const uint4 *)(ua + off + 8);
+                rb[2 * j] = *(const uint4 *)(ub + off);
+                rb[2 * j + 1] = *(const uint4 *)(ub + off + 8);
             }
         }
         if (ob < 0) {
@@ -371,61 +497,30 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
             for (int i = 0; i < 8; ++i) rb[i] = make_uint4(0, 0, 0, 0);
         }
     };
-    // Loads in the order they are needed.  (1) this wave's L1 tiles of the
-    // kernel row: lane (g < 2, c) takes k[256 (4 g + j) + 16 c + 4 w + t],
-    // t = 0..3, for j = 0..3 (tile T = 4 w + t, point p2 = 4 g + j).
+    // Loads in the order they are needed: (1) the constant tables, straight
+    // into LDS (1 KB per wave and instruction, no registers)
+#pragma unroll
+    for (int r = 0; r < (kTab + NT - 1) / NT; ++r) {
+        const int base = r * NT + 64 * w;   // this wave's 64 uint4
+        if (base < kTab)
+            __builtin_amdgcn_global_load_lds((gvoid_t *)((const uint4 *)kHalf.v + base + lane),
+                                             (lvoid_t *)(Tab + base), 16, 0, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    // (2) this wave's L1 tiles of the kernel row: lane (g < 2, c) takes
+    // k[256 (4 g + j) + 16 c + 4 w + t], t = 0..3, for j = 0..3 (tile
+    // T = 4 w + t, point p2 = 4 g + j)
     float4 kq[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
         kq[j] = make_float4(0.f, 0.f, 0.f, 0.f);
         if (g < 2) kq[j] = *(const float4 *)(k + (long)h * L + 256 * (4 * g + j) + 16 * c + 4 * w);
     }
-    // (2) the constant tables
-    float4 ty[8];
-#pragma unroll
-    for (int sidx = 0; sidx < 4; ++sidx) {
-        const int e = tid + NT * sidx;
-        ty[2 * sidx] = ((const float4 *)kPro.y)[2 * e];
-        ty[2 * sidx + 1] = ((const float4 *)kPro.y)[2 * e + 1];
-    }
-    float4 tdx[4];
-    if (w == 0) {
-        const float4 *dt = (const float4 *)(kPro.dft + 4 * lane), *xt = (const float4 *)(kPro.x + 4 * lane);
-        tdx[0] = dt[0]; tdx[1] = dt[1]; tdx[2] = xt[0]; tdx[3] = xt[1];
-    }
+    __builtin_amdgcn_sched_barrier(0);
     // (3) this wave's first pair, in flight during the kernel transform
     int qq = q0 + w;
     bool have = qq < q1;
     if (have) issue_loads(qq);
-
-    // stage the constant tables (fp32 pairs -> fp16)
-#pragma unroll
-    for (int sidx = 0; sidx < 4; ++sidx) {
-        const float4 v0 = ty[2 * sidx], v1 = ty[2 * sidx + 1];
-        Ytab[tid + NT * sidx] = make_uint4(pk(v0.x, v0.y), pk(v0.z, v0.w), pk(v1.x, v1.y), pk(v1.z, v1.w));
-    }
-    if (w == 0) {
-        const float4 f01 = tdx[0], f23 = tdx[1], x01 = tdx[2], x23 = tdx[3];
-        const float fr[4] = {f01.x, f01.z, f23.x, f23.z}, fi[4] = {f01.y, f01.w, f23.y, f23.w};
-        uint32_t o[6][4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const float re = 0.25f * fr[i], im = 0.25f * fi[i];
-            // out.re = sum re(w) x.re - im(w) x.im ; out.im = sum im(w) x.re + re(w) x.im
-            o[0][i] = pk(re, -im);
-            o[1][i] = pk(im, re);
-            o[2][i] = pk(re, im);      // conjugate
-            o[3][i] = pk(-im, re);
-        }
-        const float xr[4] = {x01.x, x01.z, x23.x, x23.z}, xi[4] = {x01.y, x01.w, x23.y, x23.w};
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            o[4][j] = pk(xr[j], xi[j]);
-            o[5][j] = pk(-xi[j], xr[j]);
-        }
-#pragma unroll
-        for (int kd = 0; kd < 6; ++kd) Lc[kd * 64 + lane] = make_uint4(o[kd][0], o[kd][1], o[kd][2], o[kd][3]);
-    }
 
     // ---- kernel spectrum of channel h, all waves: wave w runs tiles
     //      4 w .. 4 w + 3 of L1 and L2 and quads 4 w .. 4 w + 3 of L3; the
@@ -440,6 +535,9 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
             mx = fmaxf(mx, fmaxf(fmaxf(fabsf(kq[j].x), fabsf(kq[j].y)), fmaxf(fabsf(kq[j].z), fabsf(kq[j].w))));
         mx = wave_max(mx);
         if (lane == 0) red[w] = mx;
+        // tables and kernel row landed; at most the 16 pair loads (issued
+        // last) still in flight
+        __builtin_amdgcn_s_waitcnt(kWaitVm16);
         __syncthreads();   // red, Ytab, Lc
         const int ek = __builtin_amdgcn_readfirstlane(exp_of(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]))));
         uint32_t dq[16];   // quad t = tile 4 w + t, element j
@@ -614,61 +712,25 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
         Dft Fs = lds_dft(Lc, lane, true);
         Fs.re = h8_scale(Fs.re, (_Float16)ldexpf(1.0f, sf));
         Fs.im = h8_scale(Fs.im, (_Float16)ldexpf(1.0f, sf));
-        float pr[8];   // previous (even) tile's outputs: rows a and b
-        layer<false>(d, Fs, NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
-            float ya[4], yb[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                ya[i] = re[i];
-                yb[i] = im[i];
-            }
-            if (srem != 0) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    ya[i] *= rem;
-                    yb[i] *= rem;
-                }
-            }
-            if (CORR != 0 && g < 2) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const long p = 256 * (4 * g + i) + 16 * c + tau;
-                    if (CORR == 2) {
-                        const uint16_t *cr = (const uint16_t *)a.corr;
-                        ya[i] += lo_f<DT>(cr[oa + p]);
-                        if (ob >= 0) yb[i] += lo_f<DT>(cr[ob + p]);
-                    } else {
-                        const float *cr = (const float *)a.corr;
-                        ya[i] += cr[oa + p];
-                        if (ob >= 0) yb[i] += cr[ob + p];
-                    }
-                }
-            }
-            if ((tau & 1) == 0) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    pr[i] = ya[i];
-                    pr[4 + i] = yb[i];
-                }
-            } else {
-                // tiles tau - 1, tau: row a -> d[4 (tau - 1) + i], row b -> d[4 tau + i]
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    d[4 * (tau - 1) + i] = pack_out<DT>(pr[i], ya[i]);
-                    d[4 * tau + i] = pack_out<DT>(pr[4 + i], yb[i]);
-                }
-            }
-        });
+        // branch-free epilogue (a branch inside it lets the compiler hoist
+        // all of the layer's MFMAs above it); the rare remainder scale picks
+        // a second instance of the layer instead
+        const long obc = ob >= 0 ? ob : oa;   // row b's correction read from row a if absent
+        if (srem == 0)
+            out_layer<DT, CORR, false>(d, Fs, 1.0f, a.corr, oa, obc, lane);
+        else
+            out_layer<DT, CORR, true>(d, Fs, rem, a.corr, oa, obc, lane);
         if (g < 2) {
+            uint16_t *ya_row = y + oa, *yb_row = y + obc;   // wave-uniform bases
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const long off = 256 * (4 * g + i) + 16 * c;
+                const int off = 256 * (4 * g + i) + 16 * c;
                 // row a: dwords d[8 s + i] hold points 2 s, 2 s + 1
-                *(uint4 *)(y + oa + off) = make_uint4(d[i], d[8 + i], d[16 + i], d[24 + i]);
-                *(uint4 *)(y + oa + off + 8) = make_uint4(d[32 + i], d[40 + i], d[48 + i], d[56 + i]);
+                *(uint4 *)(ya_row + off) = make_uint4(d[i], d[8 + i], d[16 + i], d[24 + i]);
+                *(uint4 *)(ya_row + off + 8) = make_uint4(d[32 + i], d[40 + i], d[48 + i], d[56 + i]);
                 if (ob >= 0) {
-                    *(uint4 *)(y + ob + off) = make_uint4(d[4 + i], d[12 + i], d[20 + i], d[28 + i]);
-                    *(uint4 *)(y + ob + off + 8) = make_uint4(d[36 + i], d[44 + i], d[52 + i], d[60 + i]);
+                    *(uint4 *)(yb_row + off) = make_uint4(d[4 + i], d[12 + i], d[20 + i], d[28 + i]);
+                    *(uint4 *)(yb_row + off + 8) = make_uint4(d[36 + i], d[44 + i], d[52 + i], d[60 + i]);
                 }
             }
         }
