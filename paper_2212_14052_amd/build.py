@@ -32,6 +32,7 @@ EXTRA = {
     # MFMA results in VGPRs: the fused conv's epilogues read every result
     # with the VALU, so AGPR destinations only add copies
     "fftconv_wave.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+    "fftconv_wave16k.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
 }
 
 

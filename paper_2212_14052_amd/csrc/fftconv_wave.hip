@@ -44,303 +44,19 @@
 // spectrum never reaches HBM); every wave then streams its own pairs.
 #include "common.h"
 #include "internal.h"
+#include "wave_common.h"
 
 namespace h3 {
 namespace wv {
 
-typedef _Float16 h2_t __attribute__((ext_vector_type(2)));
-typedef _Float16 h8_t __attribute__((ext_vector_type(8)));
-typedef float f4_t __attribute__((ext_vector_type(4)));
-typedef float f2_t __attribute__((ext_vector_type(2)));
-typedef __bf16 b2_t __attribute__((ext_vector_type(2)));
+using namespace wvc;
 
 constexpr int N = 4096;
 constexpr int L = 2048;
 constexpr int NW = 4;           // waves per workgroup
 constexpr int NT = 64 * NW;
 
-// ------------------------------------------------- twiddle table (constant) --
-// w_4096^n = exp(-2 pi i n / 4096) for n < 4096, as float (re, im), evaluated
-// at compile time: the first quadrant from Taylor series of sin and cos on
-// [0, pi/4] (argument reduction by the octant symmetry), the other quadrants
-// by rotation by -i.
-struct Cf {
-    float re, im;
-};
-struct TwTable {
-    Cf v[N];
-};
-constexpr double cx_sin_small(double x) {  // |x| <= pi/4
-    double t = x, s = x;
-    for (int k = 1; k < 14; ++k) {
-        t *= -x * x / ((2.0 * k) * (2.0 * k + 1.0));
-        s += t;
-    }
-    return s;
-}
-constexpr double cx_cos_small(double x) {
-    double t = 1.0, s = 1.0;
-    for (int k = 1; k < 14; ++k) {
-        t *= -x * x / ((2.0 * k - 1.0) * (2.0 * k));
-        s += t;
-    }
-    return s;
-}
-constexpr TwTable make_tw_table() {
-    TwTable t{};
-    const double step = 6.283185307179586476925286766559 / N;
-    for (int n = 0; n <= N / 8; ++n) {  // angle in [0, pi/4]
-        const double c = cx_cos_small(n * step), s = cx_sin_small(n * step);
-        t.v[n] = Cf{(float)c, (float)-s};
-        // angle pi/2 - x: cos <-> sin
-        t.v[N / 4 - n] = Cf{(float)s, (float)-c};
-    }
-    for (int n = N / 4; n < N; ++n) {  // w^n = -i w^(n - N/4)
-        const Cf p = t.v[n - N / 4];
-        t.v[n] = Cf{p.im, -p.re};
-    }
-    return t;
-}
-// Everything the kernel stages into LDS at start-up, in LDS order, as float
-// pairs (rounded to fp16 while staging):
-//   y[(T * 64 + l) * 4 + j]  = w_4096^{T (c + 16 (4 g + j))}  (L2 twiddles)
-//   dft[l * 4 + i]           = w_16^{(4 g + i) c}              (DFT-16 entries)
-//   x[l * 4 + j]             = w_256^{c (4 g + j)}             (L1 twiddles)
-// with lane l = 16 g + c.
-struct ProTable {
-    Cf y[N];
-    Cf dft[256];
-    Cf x[256];
-};
-constexpr ProTable make_pro_table() {
-    const TwTable t = make_tw_table();
-    ProTable p{};
-    for (int T = 0; T < 16; ++T)
-        for (int l = 0; l < 64; ++l)
-            for (int j = 0; j < 4; ++j)
-                p.y[(T * 64 + l) * 4 + j] = t.v[(T * ((l & 15) + 16 * (4 * (l >> 4) + j))) & (N - 1)];
-    for (int l = 0; l < 64; ++l)
-        for (int i = 0; i < 4; ++i) {
-            p.dft[l * 4 + i] = t.v[(256 * (4 * (l >> 4) + i) * (l & 15)) & (N - 1)];
-            p.x[l * 4 + i] = t.v[(16 * (l & 15) * (4 * (l >> 4) + i)) & (N - 1)];
-        }
-    return p;
-}
-__device__ const ProTable kPro = make_pro_table();
-
-// IEEE binary16 bits of x, round to nearest even (|x| < 65504, no NaN / inf).
-constexpr uint32_t h16_bits(double x) {
-    uint32_t sign = x < 0 ? 0x8000u : 0u;
-    double a = x < 0 ? -x : x;
-    if (a < 5.9604644775390625e-08 * 0.5) return sign;   // rounds to zero
-    int e = 0;
-    while (a >= 2.0) { a *= 0.5; ++e; }
-    while (a < 1.0) { a *= 2.0; --e; }
-    if (e < -14) {   // subnormal: multiple of 2^-24
-        double m = a;
-        for (int i = e; i < -24; ++i) m *= 0.5;
-        for (int i = -24; i < e; ++i) m *= 2.0;
-        const double fl = (double)(long long)m;
-        double r = m - fl;
-        long long q = (long long)fl;
-        if (r > 0.5 || (r == 0.5 && (q & 1))) ++q;
-        return sign | (uint32_t)q;
-    }
-    const double m = (a - 1.0) * 1024.0;
-    long long q = (long long)m;
-    const double r = m - (double)q;
-    if (r > 0.5 || (r == 0.5 && (q & 1))) ++q;
-    if (q == 1024) { q = 0; ++e; }
-    return sign | ((uint32_t)(e + 15) << 10) | (uint32_t)q;
-}
-constexpr uint32_t h2_bits(double re, double im) { return h16_bits(re) | (h16_bits(im) << 16); }
-
-// The same tables in fp16 and in LDS order, staged with LDS-direct loads:
-//   [0, 1024)      Ytab[T * 64 + l]: the four L2 twiddles of tile T, lane l
-//   [1024, 1408)   Lc[kind * 64 + l]: DFT rows (real, imaginary), conjugate
-//                  DFT rows, L1 twiddles w and (-im w, re w)
-constexpr int kTabY = 1024, kTabLc = 384, kTab = kTabY + kTabLc;   // in uint4
-struct HalfTable {
-    uint32_t v[4 * kTab];
-};
-constexpr HalfTable make_half_table() {
-    const TwTable t = make_tw_table();
-    HalfTable h{};
-    for (int T = 0; T < 16; ++T)
-        for (int l = 0; l < 64; ++l)
-            for (int j = 0; j < 4; ++j) {
-                const Cf w = t.v[(T * ((l & 15) + 16 * (4 * (l >> 4) + j))) & (N - 1)];
-                h.v[(T * 64 + l) * 4 + j] = h2_bits(w.re, w.im);
-            }
-    for (int l = 0; l < 64; ++l)
-        for (int i = 0; i < 4; ++i) {
-            const Cf w = t.v[(256 * (4 * (l >> 4) + i) * (l & 15)) & (N - 1)];
-            const double re = 0.25 * w.re, im = 0.25 * w.im;
-            // out.re = sum re(w) x.re - im(w) x.im ; out.im = sum im(w) x.re + re(w) x.im
-            h.v[4 * (kTabY + 0 * 64 + l) + i] = h2_bits(re, -im);
-            h.v[4 * (kTabY + 1 * 64 + l) + i] = h2_bits(im, re);
-            h.v[4 * (kTabY + 2 * 64 + l) + i] = h2_bits(re, im);    // conjugate
-            h.v[4 * (kTabY + 3 * 64 + l) + i] = h2_bits(-im, re);
-            const Cf x = t.v[(16 * (l & 15) * (4 * (l >> 4) + i)) & (N - 1)];
-            h.v[4 * (kTabY + 4 * 64 + l) + i] = h2_bits(x.re, x.im);
-            h.v[4 * (kTabY + 5 * 64 + l) + i] = h2_bits(-x.im, x.re);
-        }
-    return h;
-}
 __device__ const HalfTable kHalf = make_half_table();
-typedef __attribute__((address_space(1))) void gvoid_t;
-typedef __attribute__((address_space(3))) void lvoid_t;
-
-// ---------------------------------------------------------- small helpers ---
-__device__ __forceinline__ h2_t as_h2(uint32_t v) { return __builtin_bit_cast(h2_t, v); }
-__device__ __forceinline__ uint32_t as_u32(h2_t v) { return __builtin_bit_cast(uint32_t, v); }
-// (re, im) fp32 -> packed fp16, round to nearest even
-__device__ __forceinline__ uint32_t pk(float re, float im) {
-    const f2_t v = {re, im};
-    return as_u32(__builtin_convertvector(v, h2_t));
-}
-// a * w and a * conj(w) in packed fp16
-__device__ __forceinline__ uint32_t cmul(uint32_t a_, uint32_t w_) {
-    const h2_t a = as_h2(a_), w = as_h2(w_);
-    const h2_t t = a.xx * w;
-    const h2_t ws = {-w.y, w.x};
-    return as_u32(a.yy * ws + t);
-}
-// a * w with ws = (-w.im, w.re) supplied (loop-invariant twiddles)
-__device__ __forceinline__ uint32_t cmul2(uint32_t a_, uint32_t w_, uint32_t ws_) {
-    const h2_t a = as_h2(a_);
-    const h2_t t = a.xx * as_h2(w_);
-    return as_u32(a.yy * as_h2(ws_) + t);
-}
-// a * conj(w) with ws = (-w.im, w.re): (ar wr + ai wi, ai wr - ar wi)
-__device__ __forceinline__ uint32_t cmulc2(uint32_t a_, uint32_t w_, uint32_t ws_) {
-    const h2_t a = as_h2(a_), w = as_h2(w_), ws = as_h2(ws_);
-    const h2_t t = a.yy * w;                 // (ai wr, ai wi)
-    const h2_t u2 = {ws.y, ws.x};            // (wr, -wi)
-    return as_u32(a.xx * u2 + t.yx);         // (ar wr + ai wi, -ar wi + ai wr)
-}
-__device__ __forceinline__ uint32_t cmulc(uint32_t a_, uint32_t w_) {
-    const h2_t a = as_h2(a_), w = as_h2(w_);
-    const h2_t wc = {w.x, -w.y};
-    const h2_t t = a.xx * wc;
-    const h2_t ws = {w.y, w.x};
-    return as_u32(a.yy * ws + t);
-}
-__device__ __forceinline__ h8_t h8_of(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
-    return __builtin_bit_cast(h8_t, make_uint4(a, b, c, d));
-}
-__device__ __forceinline__ f4_t mfma(h8_t a, h8_t b) {
-    const f4_t z = {0.f, 0.f, 0.f, 0.f};
-    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, z, 0, 0, 0);
-}
-// Maximum over the wavefront, returned wave-uniform: xor-swizzles within
-// each half (immediate patterns, no lane-address registers), then the two
-// halves' results read as scalars.
-template <int XOR> __device__ __forceinline__ float swz_xor(float v) {
-    return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), (XOR << 10) | 0x1F));
-}
-__device__ __forceinline__ float wave_max(float v) {
-    v = fmaxf(v, swz_xor<1>(v));
-    v = fmaxf(v, swz_xor<2>(v));
-    v = fmaxf(v, swz_xor<4>(v));
-    v = fmaxf(v, swz_xor<8>(v));
-    v = fmaxf(v, swz_xor<16>(v));
-    const float lo = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
-    const float hi = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
-    return fmaxf(lo, hi);
-}
-// exponent e with max = m 2^e, m in [1/2, 1); 0 for 0 / non-finite
-__device__ __forceinline__ int exp_of(float m) {
-    if (!(m > 0.f) || !(m < 3.0e38f)) return 0;
-    int e;
-    frexpf(m, &e);
-    return e;
-}
-
-// 16x16 DFT (entries / 4) as the lane's 8 halves: point i = h / 2 of the
-// K range 4 g .. 4 g + 3, frequency c; the same values serve as A operand
-// (rows = frequency) and as B operand (columns = frequency).
-struct Dft {
-    h8_t re, im;
-};
-
-// Position of tile T's output jj after L2: "P layout".  The G <-> T swap
-// then leaves every L3 tile's four points in four consecutive registers.
-__device__ __forceinline__ constexpr int pidx(int T, int jj) { return 16 * (T >> 2) + 4 * jj + (T & 3); }
-
-template <bool SIG_A>
-__device__ __forceinline__ void quad_mfma(const uint32_t *q, const Dft &F, f4_t &re, f4_t &im) {
-    const h8_t x = h8_of(q[0], q[1], q[2], q[3]);
-    if constexpr (SIG_A) {
-        re = mfma(x, F.re);
-        im = mfma(x, F.im);
-    } else {
-        re = mfma(F.re, x);
-        im = mfma(F.im, x);
-    }
-}
-// One radix-16 layer over slot G on the NQ register quads d[4 tau .. 4 tau + 3].
-// Software-pipelined: the MFMAs of quad tau + 1 (and the LDS operand
-// pre(tau + 1) of its epilogue) are issued before the epilogue of quad tau,
-// and the scheduler may not hoist further (which would keep all 32 results
-// live).  epi(tau, re, im, p) gets the fp32 outputs of quad tau (frequency /
-// row 4 g + jj in element jj) and p = pre(tau).
-struct NoPre {
-    __device__ __forceinline__ uint4 operator()(int) const { return make_uint4(0, 0, 0, 0); }
-};
-template <bool SIG_A, int NQ = 16, class Pre, class Epi>
-__device__ __forceinline__ void layer(uint32_t *d, const Dft &F, Pre &&pre, Epi &&epi) {
-    f4_t re, im;
-    quad_mfma<SIG_A>(d, F, re, im);
-    uint4 pv = pre(0);
-#pragma unroll
-    for (int tau = 0; tau < NQ; ++tau) {
-        f4_t re1, im1;
-        uint4 pv1 = make_uint4(0, 0, 0, 0);
-        if (tau + 1 < NQ) {
-            quad_mfma<SIG_A>(d + 4 * (tau + 1), F, re1, im1);
-            pv1 = pre(tau + 1);
-        }
-        epi(tau, re, im, pv);
-        __builtin_amdgcn_sched_barrier(0);
-        re = re1;
-        im = im1;
-        pv = pv1;
-    }
-}
-
-// Exchange slot G's lane-row bits (lane bits 5, 4) with register-index bits
-// 5, 4.  An involution.
-__device__ __forceinline__ void swap_GT(uint32_t (&d)[64]) {
-#pragma unroll
-    for (int r = 0; r < 32; ++r) {
-        const auto s = __builtin_amdgcn_permlane32_swap(d[r], d[r + 32], false, false);
-        d[r] = s[0];
-        d[r + 32] = s[1];
-    }
-#pragma unroll
-    for (int r = 0; r < 64; ++r) {
-        if (r & 16) continue;
-        const auto s = __builtin_amdgcn_permlane16_swap(d[r], d[r + 16], false, false);
-        d[r] = s[0];
-        d[r + 16] = s[1];
-    }
-}
-
-// s_waitcnt encoding (gfx9): vmcnt <= 16, lgkmcnt and expcnt unconstrained
-constexpr int kWaitVm16 = 0x4F70;
-
-// Per-lane constants staged in LDS (Lc[kind * 64 + lane]): 0/1 DFT real /
-// imaginary rows, 2/3 the conjugate DFT, 4 the L1 twiddles w_256^{c (4g+j)},
-// 5 the same as (-im, re).  Read right before each layer so that they do not
-// occupy registers across the pair pipeline.
-__device__ __forceinline__ Dft lds_dft(const uint4 *Lc, int lane, bool conj) {
-    asm volatile("" ::: "memory");   // re-read per layer, do not keep live
-    Dft F;
-    F.re = __builtin_bit_cast(h8_t, Lc[(conj ? 2 : 0) * 64 + lane]);
-    F.im = __builtin_bit_cast(h8_t, Lc[(conj ? 3 : 1) * 64 + lane]);
-    return F;
-}
 
 // Forward transform of a register-resident signal up to L3: L1 (signal A) +
 // w_256 twiddle, L2 (signal B) + w_4096 twiddle written in P layout, swap.
@@ -370,25 +86,6 @@ __device__ __forceinline__ void forward_front(uint32_t (&d)[64], const uint4 *Lc
     for (int i = 0; i < 64; ++i) d[i] = e[i];
     swap_GT(d);
 }
-
-// 16-bit I/O helpers
-template <int DT> __device__ __forceinline__ uint32_t pack_out(float lo, float hi);
-template <> __device__ __forceinline__ uint32_t pack_out<F16>(float lo, float hi) { return pk(lo, hi); }
-template <> __device__ __forceinline__ uint32_t pack_out<BF16>(float lo, float hi) {
-    const f2_t v = {lo, hi};
-    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, b2_t));
-}
-template <int DT> __device__ __forceinline__ float lo_f(uint32_t r) {
-    return DT == F16 ? (float)as_h2(r).x : __uint_as_float(r << 16);
-}
-template <int DT> __device__ __forceinline__ float hi_f(uint32_t r) {
-    return DT == F16 ? (float)as_h2(r).y : __uint_as_float(r & 0xffff0000u);
-}
-__device__ __forceinline__ h8_t h8_scale(h8_t v, _Float16 s) {
-    const h8_t sv = {s, s, s, s, s, s, s, s};
-    return v * sv;
-}
-
 // L1^H with the output epilogue: fp32 outputs (times rem when REM), plus the
 // correction term (read for every lane: outputs of lanes g >= 2 and of a
 // missing row b are discarded), packed two tiles at a time into d (row a in
@@ -537,7 +234,10 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
         if (lane == 0) red[w] = mx;
         // tables and kernel row landed; at most the 16 pair loads (issued
         // last) still in flight
-        __builtin_amdgcn_s_waitcnt(kWaitVm16);
+        if (have)
+            __builtin_amdgcn_s_waitcnt(kWaitVm16);
+        else
+            __builtin_amdgcn_s_waitcnt(kWaitVm0);   // no pair loads: everything must land
         __syncthreads();   // red, Ytab, Lc
         const int ek = __builtin_amdgcn_readfirstlane(exp_of(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]))));
         uint32_t dq[16];   // quad t = tile 4 w + t, element j

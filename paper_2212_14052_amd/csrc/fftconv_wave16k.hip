@@ -1,0 +1,687 @@
+// Fused FFT convolution for L = 8192 (transform length N = 2L = 16384 =
+// 4 x 4096) with four wavefronts per row pair (Sec. 4.1: kernel fusion +
+// block FFT, at the fused-block length), gfx950, 16-bit I/O.
+//
+// With p = 4096 p3 + m (m < 4096; the zero-padded input vanishes for
+// p3 >= 2), decimating the frequency by four (f = 4 f' + k3) gives
+//   X[4 f' + k3] = DFT_4096[ w_16384^{k3 m} (x(m) + (-i)^{k3} x(4096 + m)) ](f').
+// Wave k3 of the workgroup runs block k3 through the register-resident
+// 4096-point pipeline of the one-wave kernel (three radix-16 layers on the
+// matrix cores; see wave_common.h).  The block twiddle
+//   w_16384^{k3 m} = w_64^{k3 p2} w_1024^{k3 p1} w_16384^{k3 p0},
+//   m = 256 p2 + 16 p1 + p0,
+// costs no instruction per point: the p2 factor scales the contraction side
+// of the first layer's DFT matrix, the p1 factor rides on that layer's lane
+// twiddles and the p0 factor scales the contraction side of the third
+// layer's matrix.  The first layer contracts x(m) and x(4096 + m) together
+// as two K steps of the MFMA (the second with (-i)^{k3} times the matrix),
+// so the radix-4 butterfly needs no vector instruction either.
+//
+// Inverse: y(4096 t3 + m) = sum_k3 i^{t3 k3} w_16384^{-k3 m} IDFT_4096[Y_k3](m)
+// for t3 = 0, 1 (outputs t < L only).  Each wave runs its block backwards up
+// to the last radix-16 layer (the p0 and p1 factors again folded into a layer
+// matrix and the lane twiddles).  The last layer's inputs are then exchanged
+// through LDS so that wave w holds tiles p0 = 4w .. 4w + 3 of all four
+// blocks, and the last layer, the w_64^{-k3 p2} factors and the radix-4
+// butterfly over k3 run as one 64-point contraction (four K steps of the MFMA
+// per output tile, two outputs t3 = 0, 1).
+//
+// The pair's input is staged once in LDS as interleaved complex (u_a, u_b)
+// values, in the order the first layer reads them; every wave reads all of it
+// and loads one quarter of it from HBM (prefetched into registers during the
+// previous pair).  The kernel spectrum block of each wave stays in registers.
+// D is folded into the kernel (k[0] += D).  16-bit inputs feed the first
+// layer as they are (fp16 or bf16 MFMA); everything after it is fp16 with
+// fp32 accumulation, with the power-of-two range control of the one-wave
+// kernel.
+#include "common.h"
+#include "internal.h"
+#include "wave_common.h"
+
+namespace h3 {
+namespace w16 {
+
+using namespace wvc;
+
+constexpr int N = 16384;
+constexpr int L = 8192;
+constexpr int NW = 4;           // waves per workgroup (one per frequency block)
+constexpr int NT = 64 * NW;
+constexpr int kU = 2048;        // uint4: input staging / last-layer exchange (32 KB)
+
+typedef __bf16 bf8_t __attribute__((ext_vector_type(8)));
+typedef unsigned short us2_t __attribute__((ext_vector_type(2)));
+
+// exp(-2 pi i n / nn) in double, any integer n (nn a multiple of 8)
+struct Cd {
+    double re, im;
+};
+constexpr Cd cwd(long n, long nn) {
+    n %= nn;
+    if (n < 0) n += nn;
+    const long q4 = nn / 4, q = n / q4, r = n % q4;
+    const double step = 6.283185307179586476925286766559 / (double)nn;
+    double c = 0, s = 0;   // cos, sin of 2 pi r / nn, r < nn / 4
+    if (2 * r <= q4) {
+        c = cx_cos_small(r * step);
+        s = cx_sin_small(r * step);
+    } else {
+        c = cx_sin_small((q4 - r) * step);
+        s = cx_cos_small((q4 - r) * step);
+    }
+    Cd v{c, -s};
+    for (long i = 0; i < q; ++i) v = Cd{v.im, -v.re};   // times -i
+    return v;
+}
+
+// LDS tables: the one-wave kernel's L2 twiddles and per-lane DFT rows, then
+// the last layer's matrix for each source block k3' as (real, imaginary)
+// rows: entries conj(w_64^{(4 k2 + k3') p2}) / 4 for output row p2 = c and
+// contraction point k2 = 4 g + i (lane l = 16 g + c).
+constexpr int kTabG1 = 8 * 64;
+constexpr int kTab16 = kTab + kTabG1;   // uint4
+struct Half16 {
+    uint32_t v[4 * kTab16];
+};
+constexpr Half16 make_half16() {
+    const HalfTable base = make_half_table();
+    Half16 t{};
+    for (int i = 0; i < 4 * kTab; ++i) t.v[i] = base.v[i];
+    for (int k3 = 0; k3 < 4; ++k3)
+        for (int l = 0; l < 64; ++l)
+            for (int i = 0; i < 4; ++i) {
+                const long g = l >> 4, c = l & 15;
+                const Cd v = cwd(-(4 * (4 * g + i) + k3) * c, 64);
+                const double re = 0.25 * v.re, im = 0.25 * v.im;
+                t.v[4 * (kTab + (2 * k3) * 64 + l) + i] = h2_bits(re, -im);
+                t.v[4 * (kTab + (2 * k3 + 1) * 64 + l) + i] = h2_bits(im, re);
+            }
+    return t;
+}
+__device__ const Half16 kHalf16 = make_half16();
+
+// Per-wave (k3) and per-lane factors, fp16 (re, im), 16 dwords per lane:
+//   [0..3]  w_64^{k3 (4g+i)} / 2      first layer, contraction point i
+//   [4..7]  w_1024^{k3 (4g+j)}         first layer's lane twiddles, row j
+//   [8..11] w_16384^{k3 (4g+i)}        third layer, contraction point i
+//   [12]    w_16384^{-k3 c}            inverse third layer, output row c
+//   [13]    w_1024^{-k3 c}             inverse second layer's lane twiddles
+struct Fac16 {
+    uint32_t v[4 * 64 * 16];
+};
+constexpr Fac16 make_fac16() {
+    Fac16 t{};
+    for (int k3 = 0; k3 < 4; ++k3)
+        for (int l = 0; l < 64; ++l) {
+            const long g = l >> 4, c = l & 15;
+            uint32_t *p = t.v + (k3 * 64 + l) * 16;
+            for (int i = 0; i < 4; ++i) {
+                const Cd a = cwd(k3 * (4 * g + i), 64);
+                p[i] = h2_bits(0.5 * a.re, 0.5 * a.im);
+                const Cd b = cwd(k3 * (4 * g + i), 1024);
+                p[4 + i] = h2_bits(b.re, b.im);
+                const Cd e = cwd(k3 * (4 * g + i), N);
+                p[8 + i] = h2_bits(e.re, e.im);
+            }
+            const Cd r3 = cwd(-k3 * c, N), rx = cwd(-k3 * c, 1024);
+            p[12] = h2_bits(r3.re, r3.im);
+            p[13] = h2_bits(rx.re, rx.im);
+        }
+    return t;
+}
+__device__ const Fac16 kFac16 = make_fac16();
+
+// ------------------------------------------------------------ derived rows --
+// A DFT-row pair (R, I) from a base imaginary row b (entries (Im w, Re w))
+// with every point multiplied by f[i]: I' = (Im w f, Re w f), R' = (Re w f,
+// -Im w f).  Covers a scaled contraction side (f per point) and a scaled
+// output row (the same f for all points).
+__device__ __forceinline__ void kinds_scaled(uint4 b4, const uint32_t (&f)[4], uint32_t (&R)[4],
+                                             uint32_t (&I)[4]) {
+    const uint32_t b[4] = {b4.x, b4.y, b4.z, b4.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const h2_t bb = as_h2(b[i]), ff = as_h2(f[i]);
+        const h2_t fs = {ff.y, ff.x}, fn = {ff.x, -ff.y};
+        const h2_t ii = bb.yy * fs + bb.xx * fn;
+        const h2_t rr = {ii.y, -ii.x};
+        I[i] = as_u32(ii);
+        R[i] = as_u32(rr);
+    }
+}
+__device__ __forceinline__ Dft dft_of(const uint32_t (&R)[4], const uint32_t (&I)[4]) {
+    Dft F;
+    F.re = h8_of(R[0], R[1], R[2], R[3]);
+    F.im = h8_of(I[0], I[1], I[2], I[3]);
+    return F;
+}
+// (-i)^k3 times a DFT-row pair: k3 = 0: (R, I); 1: (I, -R); 2: (-R, -I); 3: (-I, R)
+__device__ __forceinline__ void kinds_rot(int k3, const uint32_t (&R)[4], const uint32_t (&I)[4],
+                                          uint32_t (&Rb)[4], uint32_t (&Ib)[4]) {
+    const bool sw = (k3 & 1) != 0;
+    const uint32_t nr = k3 >= 2 ? 0x80008000u : 0u;
+    const uint32_t ni = (k3 == 1 || k3 == 2) ? 0x80008000u : 0u;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        Rb[i] = (sw ? I[i] : R[i]) ^ nr;
+        Ib[i] = (sw ? R[i] : I[i]) ^ ni;
+    }
+}
+// the same four rows as bf16, every entry times s
+__device__ __forceinline__ void kinds_bf16(const uint32_t (&R)[4], const uint32_t (&I)[4], float s, bf8_t &Rb,
+                                           bf8_t &Ib) {
+    float r[8], im[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        r[2 * i] = (float)as_h2(R[i]).x * s;
+        r[2 * i + 1] = (float)as_h2(R[i]).y * s;
+        im[2 * i] = (float)as_h2(I[i]).x * s;
+        im[2 * i + 1] = (float)as_h2(I[i]).y * s;
+    }
+    typedef float f8_t __attribute__((ext_vector_type(8)));
+    const f8_t vr = {r[0], r[1], r[2], r[3], r[4], r[5], r[6], r[7]};
+    const f8_t vi = {im[0], im[1], im[2], im[3], im[4], im[5], im[6], im[7]};
+    Rb = __builtin_convertvector(vr, bf8_t);
+    Ib = __builtin_convertvector(vi, bf8_t);
+}
+
+__device__ __forceinline__ f4_t mfma_acc(h8_t a, h8_t b, f4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f4_t mfma_acc(bf8_t a, bf8_t b, f4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// First layer: signal as the A operand, the two K steps x(m) (matrix Fa) and
+// x(4096 + m) (matrix Fb) accumulated; operands straight from the staging
+// buffer S (tile tau of half x at S[(16 x + tau) * 64 + lane]), two tiles
+// ahead.  epi(tau, re, im) as in layer().
+template <class OP, class Epi>
+__device__ __forceinline__ void layer1(const uint4 *S, int lane, const OP &Far, const OP &Fai, const OP &Fbr,
+                                       const OP &Fbi, Epi &&epi) {
+    const f4_t z = {0.f, 0.f, 0.f, 0.f};
+    auto mm = [&](uint4 x0, uint4 x1, f4_t &re, f4_t &im) {
+        const OP a0 = __builtin_bit_cast(OP, x0), a1 = __builtin_bit_cast(OP, x1);
+        re = mfma_acc(a1, Fbr, mfma_acc(a0, Far, z));
+        im = mfma_acc(a1, Fbi, mfma_acc(a0, Fai, z));
+    };
+    f4_t re, im;
+    mm(S[lane], S[16 * 64 + lane], re, im);
+    uint4 n0 = S[64 + lane], n1 = S[17 * 64 + lane];
+#pragma unroll
+    for (int tau = 0; tau < 16; ++tau) {
+        f4_t re1, im1;
+        uint4 m0 = make_uint4(0, 0, 0, 0), m1 = m0;
+        if (tau + 1 < 16) mm(n0, n1, re1, im1);
+        if (tau + 2 < 16) {
+            m0 = S[(tau + 2) * 64 + lane];
+            m1 = S[(16 + tau + 2) * 64 + lane];
+        }
+        epi(tau, re, im);
+        __builtin_amdgcn_sched_barrier(0);
+        re = re1;
+        im = im1;
+        n0 = m0;
+        n1 = m1;
+    }
+}
+
+// Second layer (signal B) + L2 twiddles into P layout, then the G <-> T swap.
+__device__ __forceinline__ void forward_mid(uint32_t (&d)[64], const uint4 *Lc, const uint4 *Ytab, int lane) {
+    uint32_t e[64];
+    const Dft F = lds_dft(Lc, lane, false);
+    layer<false>(d, F, [&](int tau) { return Ytab[tau * 64 + lane]; },
+                 [&](int tau, f4_t re, f4_t im, uint4 y) {
+                     e[pidx(tau, 0)] = cmul(pk(re[0], im[0]), y.x);
+                     e[pidx(tau, 1)] = cmul(pk(re[1], im[1]), y.y);
+                     e[pidx(tau, 2)] = cmul(pk(re[2], im[2]), y.z);
+                     e[pidx(tau, 3)] = cmul(pk(re[3], im[3]), y.w);
+                 });
+#pragma unroll
+    for (int i = 0; i < 64; ++i) d[i] = e[i];
+    swap_GT(d);
+}
+
+// Lane twiddles of the first layer (X = base w_256 times the wave's w_1024
+// factor) and of the inverse second layer (conj(base) times w_1024^{-k3 c}),
+// each with its (-im, re) companion for cmul2.
+__device__ __forceinline__ void twiddles_fwd(uint4 X, const uint32_t (&xf)[4], uint32_t (&xw)[4],
+                                             uint32_t (&xs)[4]) {
+    const uint32_t b[4] = {X.x, X.y, X.z, X.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const h2_t v = as_h2(cmul(b[j], xf[j]));
+        const h2_t s = {-v.y, v.x};
+        xw[j] = as_u32(v);
+        xs[j] = as_u32(s);
+    }
+}
+__device__ __forceinline__ void twiddles_inv(uint4 X, uint32_t xh, uint32_t (&xw)[4], uint32_t (&xs)[4]) {
+    const uint32_t b[4] = {X.x, X.y, X.z, X.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const h2_t v = as_h2(cmulc(xh, b[j]));
+        const h2_t s = {-v.y, v.x};
+        xw[j] = as_u32(v);
+        xs[j] = as_u32(s);
+    }
+}
+
+// Last layer for the wave's own tiles T = 4 w + tt: exchange, 64-point
+// contraction with the radix-4 butterfly, output epilogue and stores.
+//   D0 = sum_k3' G_k3' x_k3'           -> y(m)
+//   D1 = sum_k3' i^{k3'} G_k3' x_k3'   -> y(4096 + m)
+// (real parts row a, imaginary parts row b).  The exchange runs in two
+// halves (tiles tt = 0, 1, then 2, 3 of every quarter) through a 32 KB
+// buffer: slot ((source * 4 + destination) * 2 + tt % 2); every quarter,
+// the wave's own included, passes through LDS, so no register index depends
+// on the wave.
+template <int DT>
+__device__ __forceinline__ void last_layer(uint32_t (&d)[64], uint4 *U, const uint4 *G1, int w, int lane,
+                                           float sc, uint16_t *ya, uint16_t *yb, bool has_b) {
+    const int g = lane >> 4, c = lane & 15;
+    uint32_t pa0[8], pb0[8], pa1[8], pb1[8];   // packed outputs: [2 jj + half]
+    float qa0[4], qb0[4], qa1[4], qb1[4];       // previous (even) tile
+    const f4_t z = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+        if (half == 1) __syncthreads();   // the first half's reads are done
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int t2 = 0; t2 < 2; ++t2) {
+                const int T = 4 * q + 2 * half + t2;
+                U[((w * 4 + q) * 2 + t2) * 64 + lane] = make_uint4(d[4 * T], d[4 * T + 1], d[4 * T + 2], d[4 * T + 3]);
+            }
+        __syncthreads();
+#pragma unroll
+        for (int t2 = 0; t2 < 2; ++t2) {
+            const int tt = 2 * half + t2;
+            f4_t D0r = z, D0i = z, D1r = z, D1i = z;
+#pragma unroll
+            for (int k3p = 0; k3p < 4; ++k3p) {   // source wave = block k3'
+                asm volatile("" ::: "memory");   // matrices re-read per use, not held across the layer
+                const uint4 B4 = U[((k3p * 4 + w) * 2 + t2) * 64 + lane];
+                const uint4 nB4 = make_uint4(B4.x ^ 0x80008000u, B4.y ^ 0x80008000u, B4.z ^ 0x80008000u,
+                                             B4.w ^ 0x80008000u);
+                const h8_t b = __builtin_bit_cast(h8_t, B4), nb = __builtin_bit_cast(h8_t, nB4);
+                const h8_t Ar = __builtin_bit_cast(h8_t, G1[(2 * k3p) * 64 + lane]);
+                const h8_t Ai = __builtin_bit_cast(h8_t, G1[(2 * k3p + 1) * 64 + lane]);
+                D0r = mfma_acc(Ar, b, D0r);
+                D0i = mfma_acc(Ai, b, D0i);
+                if (k3p == 0) {
+                    D1r = mfma_acc(Ar, b, D1r);
+                    D1i = mfma_acc(Ai, b, D1i);
+                } else if (k3p == 1) {   // i P: (-Im P, Re P)
+                    D1r = mfma_acc(Ai, nb, D1r);
+                    D1i = mfma_acc(Ar, b, D1i);
+                } else if (k3p == 2) {   // -P
+                    D1r = mfma_acc(Ar, nb, D1r);
+                    D1i = mfma_acc(Ai, nb, D1i);
+                } else {                 // -i P: (Im P, -Re P)
+                    D1r = mfma_acc(Ai, b, D1r);
+                    D1i = mfma_acc(Ar, nb, D1i);
+                }
+            }
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const float a0 = D0r[jj] * sc, b0 = D0i[jj] * sc, a1 = D1r[jj] * sc, b1 = D1i[jj] * sc;
+                if (t2 == 0) {
+                    qa0[jj] = a0;
+                    qb0[jj] = b0;
+                    qa1[jj] = a1;
+                    qb1[jj] = b1;
+                } else {
+                    const int s = 2 * jj + half;
+                    pa0[s] = pack_out<DT>(qa0[jj], a0);
+                    pb0[s] = pack_out<DT>(qb0[jj], b0);
+                    pa1[s] = pack_out<DT>(qa1[jj], a1);
+                    pb1[s] = pack_out<DT>(qb1[jj], b1);
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+    // outputs m = 256 (4 g + jj) + 16 c + 4 w + (0..3): 8 bytes per row and t3
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+        const int m = 256 * (4 * g + jj) + 16 * c + 4 * w;
+        *(uint2 *)(ya + m) = make_uint2(pa0[2 * jj], pa0[2 * jj + 1]);
+        *(uint2 *)(ya + 4096 + m) = make_uint2(pa1[2 * jj], pa1[2 * jj + 1]);
+        if (has_b) {
+            *(uint2 *)(yb + m) = make_uint2(pb0[2 * jj], pb0[2 * jj + 1]);
+            *(uint2 *)(yb + 4096 + m) = make_uint2(pb1[2 * jj], pb1[2 * jj + 1]);
+        }
+    }
+}
+
+// Maximum |.| of 16-bit raw values (both halves of each dword)
+template <int DT> __device__ __forceinline__ float raw_max(const uint4 (&ra)[4], const uint4 (&rb)[4]);
+template <> __device__ __forceinline__ float raw_max<F16>(const uint4 (&ra)[4], const uint4 (&rb)[4]) {
+    h2_t hmx = {0, 0}, hmn = {0, 0};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const uint32_t v[8] = {ra[i].x, ra[i].y, ra[i].z, ra[i].w, rb[i].x, rb[i].y, rb[i].z, rb[i].w};
+#pragma unroll
+        for (int e = 0; e < 8; e += 2) {
+            hmx = __builtin_elementwise_maximum(hmx, __builtin_elementwise_maximum(as_h2(v[e]), as_h2(v[e + 1])));
+            hmn = __builtin_elementwise_minimum(hmn, __builtin_elementwise_minimum(as_h2(v[e]), as_h2(v[e + 1])));
+        }
+    }
+    return fmaxf(fmaxf((float)hmx.x, (float)hmx.y), fmaxf(-(float)hmn.x, -(float)hmn.y));
+}
+template <> __device__ __forceinline__ float raw_max<BF16>(const uint4 (&ra)[4], const uint4 (&rb)[4]) {
+    us2_t mb = {0, 0};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const uint32_t v[8] = {ra[i].x, ra[i].y, ra[i].z, ra[i].w, rb[i].x, rb[i].y, rb[i].z, rb[i].w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            mb = __builtin_elementwise_max(mb, __builtin_bit_cast(us2_t, v[e] & 0x7fff7fffu));
+    }
+    const uint32_t m = max((uint32_t)mb.x, (uint32_t)mb.y);
+    return __uint_as_float(m << 16);
+}
+
+}  // namespace w16
+
+// ============================================================================
+template <int DT>
+__global__ __launch_bounds__(w16::NT) __attribute__((amdgpu_waves_per_eu(2))) void fftconv_wave16k_kernel(
+    ConvArgs a, const float *k, int wg_per_ch, int pairs_per_ch) {
+    using namespace w16;
+    __shared__ uint4 Tab[kTab16];   // Ytab + Lc + last-layer matrices
+    __shared__ uint4 U[kU];         // pair staging, then the last-layer exchange
+    __shared__ float red[2 * NW];
+    const uint4 *Ytab = Tab, *Lc = Tab + kTabY, *G1 = Tab + kTab;
+    uint32_t *Ud = (uint32_t *)U;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // frequency block k3
+    const int g = lane >> 4, c = lane & 15;
+    const int h = blockIdx.x / wg_per_ch, part = blockIdx.x % wg_per_ch;
+    const int per = (pairs_per_ch + wg_per_ch - 1) / wg_per_ch;
+    const int q0 = part * per, q1 = min(q0 + per, pairs_per_ch);
+    const uint16_t *u = (const uint16_t *)a.u;
+    uint16_t *y = (uint16_t *)a.y;
+
+    auto rows = [&](int qq, long &oa, long &ob) {
+        if (a.pair_mode == 0) {
+            oa = ((long)(2 * qq) * a.H + h) * L;
+            ob = (2 * qq + 1 < a.B) ? ((long)(2 * qq + 1) * a.H + h) * L : -1;
+        } else {
+            const int ncp = (a.nchunk + 1) / 2;
+            const int bb = qq / ncp, cp = qq % ncp;
+            oa = (((long)bb * a.H + h) * a.nchunk + 2 * cp) * L;
+            ob = (2 * cp + 1 < a.nchunk) ? oa + L : -1;
+        }
+    };
+    // This wave's quarter of a pair: half x = w >> 1, lane rows g = 2 (w & 1)
+    // + gi; lane l holds c = l & 15, j = l >> 4, points m = 4096 x + 256 (4 g
+    // + j) + 16 c + 8 hh .. + 7 of both rows (ra/rb[2 gi + hh]).
+    const int xq = w >> 1, jq = lane >> 4;
+    uint4 ra[4], rb[4];
+    auto issue_loads = [&](int qq) {
+        long oa, ob;
+        rows(qq, oa, ob);
+        const uint16_t *ua = u + oa, *ub = u + (ob >= 0 ? ob : oa);   // wave-uniform bases
+#pragma unroll
+        for (int gi = 0; gi < 2; ++gi) {
+            const int off = 4096 * xq + 256 * (4 * (2 * (w & 1) + gi) + jq) + 16 * c;
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh) {
+                ra[2 * gi + hh] = *(const uint4 *)(ua + off + 8 * hh);
+                rb[2 * gi + hh] = *(const uint4 *)(ub + off + 8 * hh);
+            }
+        }
+        if (ob < 0) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) rb[i] = make_uint4(0, 0, 0, 0);
+        }
+    };
+    // staging position of point (x, T, lane row g, lane c, register j):
+    // dword ((16 x + T) * 64 + 16 g + c) * 4 + j  (conflict-free writes)
+    auto stage_at = [&](int gi, int T) { return ((16 * xq + T) * 64 + 16 * (2 * (w & 1) + gi) + c) * 4 + jq; };
+
+    // ---- start-up loads: tables into LDS, factors, kernel row, first pair ----
+#pragma unroll
+    for (int r = 0; r < (kTab16 + NT - 1) / NT; ++r) {
+        const int base = r * NT + 64 * w;
+        if (base < kTab16)
+            __builtin_amdgcn_global_load_lds((gvoid_t *)((const uint4 *)kHalf16.v + base + lane),
+                                             (lvoid_t *)(Tab + base), 16, 0, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    uint32_t f1[4], xf[4], f3[4], g3, xh;
+    {
+        const uint4 *fp = (const uint4 *)kFac16.v + (w * 64 + lane) * 4;
+        const uint4 v0 = fp[0], v1 = fp[1], v2 = fp[2], v3 = fp[3];
+        f1[0] = v0.x; f1[1] = v0.y; f1[2] = v0.z; f1[3] = v0.w;
+        xf[0] = v1.x; xf[1] = v1.y; xf[2] = v1.z; xf[3] = v1.w;
+        f3[0] = v2.x; f3[1] = v2.y; f3[2] = v2.z; f3[3] = v2.w;
+        g3 = v3.x;
+        xh = v3.y;
+    }
+    float4 kq[8];   // [4 gi + s]: points m = ... + 16 c + 4 s .. + 3
+#pragma unroll
+    for (int gi = 0; gi < 2; ++gi) {
+        const int off = 4096 * xq + 256 * (4 * (2 * (w & 1) + gi) + jq) + 16 * c;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) kq[4 * gi + s] = *(const float4 *)(k + (long)h * L + off + 4 * s);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    if (q0 < q1) issue_loads(q0);
+
+    // ---- kernel spectrum block w of channel h (F(k + D delta) 2^-ek / 128) ----
+    uint32_t K[64];
+    int kexp;
+    uint32_t d[64];
+    {
+        if (tid == 0 && a.D) kq[0].x += a.D[h];   // point m = 0: wave 0, lane 0
+        float mx = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+            mx = fmaxf(mx, fmaxf(fmaxf(fabsf(kq[i].x), fabsf(kq[i].y)), fmaxf(fabsf(kq[i].z), fabsf(kq[i].w))));
+        mx = wave_max(mx);
+        if (lane == 0) red[w] = mx;
+        // tables, factors and kernel row landed; only the first pair's 8
+        // loads (issued last, if any) may still be in flight
+        if (q0 < q1)
+            __builtin_amdgcn_s_waitcnt(kWaitVm8);
+        else
+            __builtin_amdgcn_s_waitcnt(kWaitVm0);
+        __syncthreads();
+        const int ek = __builtin_amdgcn_readfirstlane(exp_of(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]))));
+#pragma unroll
+        for (int gi = 0; gi < 2; ++gi)
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const float4 v = kq[4 * gi + s];
+                Ud[stage_at(gi, 4 * s + 0)] = pk(ldexpf(v.x, -ek), 0.f);
+                Ud[stage_at(gi, 4 * s + 1)] = pk(ldexpf(v.y, -ek), 0.f);
+                Ud[stage_at(gi, 4 * s + 2)] = pk(ldexpf(v.z, -ek), 0.f);
+                Ud[stage_at(gi, 4 * s + 3)] = pk(ldexpf(v.w, -ek), 0.f);
+            }
+        __syncthreads();
+        {
+            uint32_t R[4], I[4], Rb[4], Ib[4];
+            kinds_scaled(Lc[1 * 64 + lane], f1, R, I);
+            kinds_rot(w, R, I, Rb, Ib);
+            const Dft Fa = dft_of(R, I), Fb = dft_of(Rb, Ib);
+            uint32_t xw[4], xs[4];
+            twiddles_fwd(Lc[4 * 64 + lane], xf, xw, xs);
+            layer1(U, lane, Fa.re, Fa.im, Fb.re, Fb.im, [&](int tau, f4_t re, f4_t im) {
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) d[4 * tau + jj] = cmul2(pk(re[jj], im[jj]), xw[jj], xs[jj]);
+            });
+        }
+        forward_mid(d, Lc, Ytab, lane);
+        {
+            uint32_t R[4], I[4];
+            kinds_scaled(Lc[1 * 64 + lane], f3, R, I);
+            layer<false>(d, dft_of(R, I), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) K[4 * tau + jj] = pk(re[jj], im[jj]);
+            });
+        }
+        h2_t hmx = {0, 0}, hmn = {0, 0};
+#pragma unroll
+        for (int i = 0; i < 64; i += 2) {
+            hmx = __builtin_elementwise_maximum(hmx, __builtin_elementwise_maximum(as_h2(K[i]), as_h2(K[i + 1])));
+            hmn = __builtin_elementwise_minimum(hmn, __builtin_elementwise_minimum(as_h2(K[i]), as_h2(K[i + 1])));
+        }
+        float km = fmaxf(fmaxf((float)hmx.x, (float)hmx.y), fmaxf(-(float)hmn.x, -(float)hmn.y));
+        km = wave_max(km);
+        if (lane == 0) red[NW + w] = km;
+        __syncthreads();   // red; every wave is done reading the staged kernel row
+        const int e2 = __builtin_amdgcn_readfirstlane(
+            exp_of(fmaxf(fmaxf(red[NW], red[NW + 1]), fmaxf(red[NW + 2], red[NW + 3]))));
+        kexp = 6 + ek + e2;
+        const _Float16 s2 = (_Float16)ldexpf(1.0f, -e2);
+        const h2_t s22 = {s2, s2};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) f3[i] = as_u32(as_h2(f3[i]) * s22);   // pairs' third layer carries 2^-e2
+    }
+
+    // ---- row pairs: all four waves on each pair ----
+    for (int qq = q0; qq < q1; ++qq) {
+        // the per-wave factors are loop-invariant; opaque here so that their
+        // swizzled and negated forms are not hoisted out of the loop as well
+#pragma unroll
+        for (int i = 0; i < 4; ++i) asm volatile("" : "+v"(f1[i]), "+v"(xf[i]), "+v"(f3[i]));
+        asm volatile("" : "+v"(g3), "+v"(xh));
+        float mx = raw_max<DT>(ra, rb);
+        mx = wave_max(mx);
+        if (lane == 0) red[w] = mx;
+        __syncthreads();   // red; the previous pair's exchange reads are done
+        const float gm = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+        int eu = 0;
+        if (DT == BF16 || !(gm >= 0.0625f && gm < 16.0f)) eu = exp_of(gm);
+        eu = __builtin_amdgcn_readfirstlane(eu);
+        // interleave (u_a, u_b) and stage; fp16 inputs out of range are
+        // scaled here, bf16 inputs through the first layer's matrix
+#pragma unroll
+        for (int gi = 0; gi < 2; ++gi)
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh) {
+                const uint4 va = ra[2 * gi + hh], vb = rb[2 * gi + hh];
+                const uint32_t A4[4] = {va.x, va.y, va.z, va.w}, B4[4] = {vb.x, vb.y, vb.z, vb.w};
+#pragma unroll
+                for (int s = 0; s < 4; ++s) {
+                    uint32_t lo = __builtin_amdgcn_perm(B4[s], A4[s], 0x05040100u);
+                    uint32_t hi = __builtin_amdgcn_perm(B4[s], A4[s], 0x07060302u);
+                    if (DT == F16 && eu != 0) {
+                        lo = pk(ldexpf((float)as_h2(lo).x, -eu), ldexpf((float)as_h2(lo).y, -eu));
+                        hi = pk(ldexpf((float)as_h2(hi).x, -eu), ldexpf((float)as_h2(hi).y, -eu));
+                    }
+                    Ud[stage_at(gi, 8 * hh + 2 * s)] = lo;
+                    Ud[stage_at(gi, 8 * hh + 2 * s + 1)] = hi;
+                }
+            }
+        const bool more = qq + 1 < q1;
+        if (more) issue_loads(qq + 1);
+        __syncthreads();   // staged pair visible
+        {
+            uint32_t R[4], I[4], Rb[4], Ib[4];
+            kinds_scaled(Lc[1 * 64 + lane], f1, R, I);
+            kinds_rot(w, R, I, Rb, Ib);
+            uint32_t xw[4], xs[4];
+            twiddles_fwd(Lc[4 * 64 + lane], xf, xw, xs);
+            auto epi = [&](int tau, f4_t re, f4_t im) {
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) d[4 * tau + jj] = cmul2(pk(re[jj], im[jj]), xw[jj], xs[jj]);
+            };
+            if (DT == F16) {
+                const Dft Fa = dft_of(R, I), Fb = dft_of(Rb, Ib);
+                layer1(U, lane, Fa.re, Fa.im, Fb.re, Fb.im, epi);
+            } else {
+                const float s = ldexpf(1.0f, -eu);
+                bf8_t Far, Fai, Fbr, Fbi;
+                kinds_bf16(R, I, s, Far, Fai);
+                kinds_bf16(Rb, Ib, s, Fbr, Fbi);
+                layer1(U, lane, Far, Fai, Fbr, Fbi, epi);
+            }
+        }
+        __syncthreads();   // every wave is done reading the staged pair
+        forward_mid(d, Lc, Ytab, lane);
+        {
+            // third layer (contraction side times w_16384^{k3 p0} 2^-e2) and
+            // the pointwise product with the kernel spectrum block
+            uint32_t R[4], I[4];
+            kinds_scaled(Lc[1 * 64 + lane], f3, R, I);
+            layer<false>(d, dft_of(R, I), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                    // opaque per use: otherwise the (-im, re) companion of every
+                    // spectrum value is hoisted out of the pair loop (64 more VGPRs)
+                    uint32_t kk = K[4 * tau + jj];
+                    asm volatile("" : "+v"(kk));
+                    d[4 * tau + jj] = cmul(pk(re[jj], im[jj]), kk);
+                }
+            });
+        }
+        {
+            // inverse third layer: output rows times w_16384^{-k3 c}
+            uint32_t R[4], I[4];
+            const uint32_t gg[4] = {g3, g3, g3, g3};
+            kinds_scaled(Lc[3 * 64 + lane], gg, R, I);
+            layer<false>(d, dft_of(R, I), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) d[4 * tau + jj] = pk(re[jj], im[jj]);
+            });
+        }
+        swap_GT(d);
+        {
+            uint32_t e[64];
+#pragma unroll
+            for (int T = 0; T < 16; ++T) {
+                const uint4 yv = Ytab[T * 64 + lane];
+                e[4 * T + 0] = cmulc(d[pidx(T, 0)], yv.x);
+                e[4 * T + 1] = cmulc(d[pidx(T, 1)], yv.y);
+                e[4 * T + 2] = cmulc(d[pidx(T, 2)], yv.z);
+                e[4 * T + 3] = cmulc(d[pidx(T, 3)], yv.w);
+            }
+#pragma unroll
+            for (int i = 0; i < 64; ++i) d[i] = e[i];
+        }
+        {
+            uint32_t xw[4], xs[4];
+            twiddles_inv(Lc[4 * 64 + lane], xh, xw, xs);
+            layer<true>(d, lds_dft(Lc, lane, true), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) d[4 * tau + jj] = cmul2(pk(re[jj], im[jj]), xw[jj], xs[jj]);
+            });
+        }
+        // the inverse second layer's outputs are complete here (otherwise its
+        // epilogues drift into the exchange and keep MFMA results live)
+#pragma unroll
+        for (int i = 0; i < 64; ++i) asm volatile("" ::"v"(d[i]));
+        long oa, ob;
+        rows(qq, oa, ob);
+        const float sc = ldexpf(1.0f, kexp + eu);
+        uint16_t *ya = y + oa, *yb = y + (ob >= 0 ? ob : oa);
+        last_layer<DT>(d, U, G1, w, lane, sc, ya, yb, ob >= 0);
+    }
+}
+
+bool fftconv_wave16k_supported(int L, int dtype) { return L == w16::L && (dtype == F16 || dtype == BF16); }
+
+hipError_t launch_fftconv_wave16k(const ConvArgs &a, const float *k, hipStream_t s) {
+    if (!fftconv_wave16k_supported(a.L, a.dtype) || a.corr != nullptr) return hipErrorInvalidValue;
+    int pairs_per_ch;
+    if (a.pair_mode == 0)
+        pairs_per_ch = (a.B + 1) / 2;
+    else
+        pairs_per_ch = a.B * ((a.nchunk + 1) / 2);
+    // two workgroups fit a CU: split a channel while fewer than ~2 per CU
+    // and each still gets two pairs
+    int wg_per_ch = 1;
+    while ((long)a.H * wg_per_ch < 512 && pairs_per_ch >= 4 * wg_per_ch) wg_per_ch *= 2;
+    dim3 grid(a.H * wg_per_ch), block(w16::NT);
+    if (a.dtype == F16)
+        hipLaunchKernelGGL(fftconv_wave16k_kernel<F16>, grid, block, 0, s, a, k, wg_per_ch, pairs_per_ch);
+    else
+        hipLaunchKernelGGL(fftconv_wave16k_kernel<BF16>, grid, block, 0, s, a, k, wg_per_ch, pairs_per_ch);
+    return hipGetLastError();
+}
+
+}  // namespace h3

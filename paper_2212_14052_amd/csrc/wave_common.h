@@ -1,0 +1,309 @@
+// Register-resident block-FFT building blocks shared by the one-wavefront-
+// per-transform convolution kernels (gfx950, wave64).
+//
+// A wavefront holds a length-4096 complex signal (packed fp16) in registers:
+// lane l = 16 g + c keeps d[4 T + j], T = 0..15, j = 0..3.  A radix-16 layer
+// contracts the base-16 digit in slot G = 4 g + j with pairs of
+// v_mfma_f32_16x16x32_f16 (real and imaginary rows of the DFT-16 matrix).
+// With the signal as the A operand the output frequency lands in slot C = c
+// and the digit that was in C moves to G; with the signal as the B operand
+// the frequency stays in G.  swap_GT exchanges slot G with the tile slot T
+// in registers.  The compile-time tables hold the L2 twiddles w_4096 (per
+// tile and lane) and the per-lane DFT-16 rows and L1 twiddles in fp16.
+#pragma once
+#include "common.h"
+
+namespace h3 {
+namespace wvc {
+
+typedef _Float16 h2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 h8_t __attribute__((ext_vector_type(8)));
+typedef float f4_t __attribute__((ext_vector_type(4)));
+typedef float f2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 b2_t __attribute__((ext_vector_type(2)));
+
+constexpr int kN = 4096;   // block transform length 16^3
+
+// ------------------------------------------------- twiddle table (constant) --
+// w_4096^n = exp(-2 pi i n / 4096) for n < 4096, as float (re, im), evaluated
+// at compile time: the first quadrant from Taylor series of sin and cos on
+// [0, pi/4] (argument reduction by the octant symmetry), the other quadrants
+// by rotation by -i.
+struct Cf {
+    float re, im;
+};
+struct TwTable {
+    Cf v[kN];
+};
+constexpr double cx_sin_small(double x) {  // |x| <= pi/4
+    double t = x, s = x;
+    for (int k = 1; k < 14; ++k) {
+        t *= -x * x / ((2.0 * k) * (2.0 * k + 1.0));
+        s += t;
+    }
+    return s;
+}
+constexpr double cx_cos_small(double x) {
+    double t = 1.0, s = 1.0;
+    for (int k = 1; k < 14; ++k) {
+        t *= -x * x / ((2.0 * k - 1.0) * (2.0 * k));
+        s += t;
+    }
+    return s;
+}
+constexpr TwTable make_tw_table() {
+    TwTable t{};
+    const double step = 6.283185307179586476925286766559 / kN;
+    for (int n = 0; n <= kN / 8; ++n) {  // angle in [0, pi/4]
+        const double c = cx_cos_small(n * step), s = cx_sin_small(n * step);
+        t.v[n] = Cf{(float)c, (float)-s};
+        // angle pi/2 - x: cos <-> sin
+        t.v[kN / 4 - n] = Cf{(float)s, (float)-c};
+    }
+    for (int n = kN / 4; n < kN; ++n) {  // w^n = -i w^(n - kN/4)
+        const Cf p = t.v[n - kN / 4];
+        t.v[n] = Cf{p.im, -p.re};
+    }
+    return t;
+}
+// IEEE binary16 bits of x, round to nearest even (|x| < 65504, no NaN / inf).
+constexpr uint32_t h16_bits(double x) {
+    uint32_t sign = x < 0 ? 0x8000u : 0u;
+    double a = x < 0 ? -x : x;
+    if (a < 5.9604644775390625e-08 * 0.5) return sign;   // rounds to zero
+    int e = 0;
+    while (a >= 2.0) { a *= 0.5; ++e; }
+    while (a < 1.0) { a *= 2.0; --e; }
+    if (e < -14) {   // subnormal: multiple of 2^-24
+        double m = a;
+        for (int i = e; i < -24; ++i) m *= 0.5;
+        for (int i = -24; i < e; ++i) m *= 2.0;
+        const double fl = (double)(long long)m;
+        double r = m - fl;
+        long long q = (long long)fl;
+        if (r > 0.5 || (r == 0.5 && (q & 1))) ++q;
+        return sign | (uint32_t)q;
+    }
+    const double m = (a - 1.0) * 1024.0;
+    long long q = (long long)m;
+    const double r = m - (double)q;
+    if (r > 0.5 || (r == 0.5 && (q & 1))) ++q;
+    if (q == 1024) { q = 0; ++e; }
+    return sign | ((uint32_t)(e + 15) << 10) | (uint32_t)q;
+}
+constexpr uint32_t h2_bits(double re, double im) { return h16_bits(re) | (h16_bits(im) << 16); }
+
+// The same tables in fp16 and in LDS order, staged with LDS-direct loads:
+//   [0, 1024)      Ytab[T * 64 + l]: the four L2 twiddles of tile T, lane l
+//   [1024, 1408)   Lc[kind * 64 + l]: DFT rows (real, imaginary), conjugate
+//                  DFT rows, L1 twiddles w and (-im w, re w)
+constexpr int kTabY = 1024, kTabLc = 384, kTab = kTabY + kTabLc;   // in uint4
+struct HalfTable {
+    uint32_t v[4 * kTab];
+};
+constexpr HalfTable make_half_table() {
+    const TwTable t = make_tw_table();
+    HalfTable h{};
+    for (int T = 0; T < 16; ++T)
+        for (int l = 0; l < 64; ++l)
+            for (int j = 0; j < 4; ++j) {
+                const Cf w = t.v[(T * ((l & 15) + 16 * (4 * (l >> 4) + j))) & (kN - 1)];
+                h.v[(T * 64 + l) * 4 + j] = h2_bits(w.re, w.im);
+            }
+    for (int l = 0; l < 64; ++l)
+        for (int i = 0; i < 4; ++i) {
+            const Cf w = t.v[(256 * (4 * (l >> 4) + i) * (l & 15)) & (kN - 1)];
+            const double re = 0.25 * w.re, im = 0.25 * w.im;
+            // out.re = sum re(w) x.re - im(w) x.im ; out.im = sum im(w) x.re + re(w) x.im
+            h.v[4 * (kTabY + 0 * 64 + l) + i] = h2_bits(re, -im);
+            h.v[4 * (kTabY + 1 * 64 + l) + i] = h2_bits(im, re);
+            h.v[4 * (kTabY + 2 * 64 + l) + i] = h2_bits(re, im);    // conjugate
+            h.v[4 * (kTabY + 3 * 64 + l) + i] = h2_bits(-im, re);
+            const Cf x = t.v[(16 * (l & 15) * (4 * (l >> 4) + i)) & (kN - 1)];
+            h.v[4 * (kTabY + 4 * 64 + l) + i] = h2_bits(x.re, x.im);
+            h.v[4 * (kTabY + 5 * 64 + l) + i] = h2_bits(-x.im, x.re);
+        }
+    return h;
+}
+typedef __attribute__((address_space(1))) void gvoid_t;
+typedef __attribute__((address_space(3))) void lvoid_t;
+
+// ---------------------------------------------------------- small helpers ---
+__device__ __forceinline__ h2_t as_h2(uint32_t v) { return __builtin_bit_cast(h2_t, v); }
+__device__ __forceinline__ uint32_t as_u32(h2_t v) { return __builtin_bit_cast(uint32_t, v); }
+// (re, im) fp32 -> packed fp16, round to nearest even
+__device__ __forceinline__ uint32_t pk(float re, float im) {
+    const f2_t v = {re, im};
+    return as_u32(__builtin_convertvector(v, h2_t));
+}
+// a * w and a * conj(w) in packed fp16
+__device__ __forceinline__ uint32_t cmul(uint32_t a_, uint32_t w_) {
+    const h2_t a = as_h2(a_), w = as_h2(w_);
+    const h2_t t = a.xx * w;
+    const h2_t ws = {-w.y, w.x};
+    return as_u32(a.yy * ws + t);
+}
+// a * w with ws = (-w.im, w.re) supplied (loop-invariant twiddles)
+__device__ __forceinline__ uint32_t cmul2(uint32_t a_, uint32_t w_, uint32_t ws_) {
+    const h2_t a = as_h2(a_);
+    const h2_t t = a.xx * as_h2(w_);
+    return as_u32(a.yy * as_h2(ws_) + t);
+}
+// a * conj(w) with ws = (-w.im, w.re): (ar wr + ai wi, ai wr - ar wi)
+__device__ __forceinline__ uint32_t cmulc2(uint32_t a_, uint32_t w_, uint32_t ws_) {
+    const h2_t a = as_h2(a_), w = as_h2(w_), ws = as_h2(ws_);
+    const h2_t t = a.yy * w;                 // (ai wr, ai wi)
+    const h2_t u2 = {ws.y, ws.x};            // (wr, -wi)
+    return as_u32(a.xx * u2 + t.yx);         // (ar wr + ai wi, -ar wi + ai wr)
+}
+__device__ __forceinline__ uint32_t cmulc(uint32_t a_, uint32_t w_) {
+    const h2_t a = as_h2(a_), w = as_h2(w_);
+    const h2_t wc = {w.x, -w.y};
+    const h2_t t = a.xx * wc;
+    const h2_t ws = {w.y, w.x};
+    return as_u32(a.yy * ws + t);
+}
+__device__ __forceinline__ h8_t h8_of(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
+    return __builtin_bit_cast(h8_t, make_uint4(a, b, c, d));
+}
+__device__ __forceinline__ f4_t mfma(h8_t a, h8_t b) {
+    const f4_t z = {0.f, 0.f, 0.f, 0.f};
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, z, 0, 0, 0);
+}
+// Maximum over the wavefront, returned wave-uniform: xor-swizzles within
+// each half (immediate patterns, no lane-address registers), then the two
+// halves' results read as scalars.
+template <int XOR> __device__ __forceinline__ float swz_xor(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), (XOR << 10) | 0x1F));
+}
+__device__ __forceinline__ float wave_max(float v) {
+    v = fmaxf(v, swz_xor<1>(v));
+    v = fmaxf(v, swz_xor<2>(v));
+    v = fmaxf(v, swz_xor<4>(v));
+    v = fmaxf(v, swz_xor<8>(v));
+    v = fmaxf(v, swz_xor<16>(v));
+    const float lo = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
+    const float hi = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
+    return fmaxf(lo, hi);
+}
+// exponent e with max = m 2^e, m in [1/2, 1); 0 for 0 / non-finite
+__device__ __forceinline__ int exp_of(float m) {
+    if (!(m > 0.f) || !(m < 3.0e38f)) return 0;
+    int e;
+    frexpf(m, &e);
+    return e;
+}
+
+// 16x16 DFT (entries / 4) as the lane's 8 halves: point i = h / 2 of the
+// K range 4 g .. 4 g + 3, frequency c; the same values serve as A operand
+// (rows = frequency) and as B operand (columns = frequency).
+struct Dft {
+    h8_t re, im;
+};
+
+// Position of tile T's output jj after L2: "P layout".  The G <-> T swap
+// then leaves every L3 tile's four points in four consecutive registers.
+__device__ __forceinline__ constexpr int pidx(int T, int jj) { return 16 * (T >> 2) + 4 * jj + (T & 3); }
+
+template <bool SIG_A>
+__device__ __forceinline__ void quad_mfma(const uint32_t *q, const Dft &F, f4_t &re, f4_t &im) {
+    h8_t x = h8_of(q[0], q[1], q[2], q[3]);
+    // The empty volatile asm keeps the MFMAs of a tile after the previous
+    // tile's sched_barrier: the intrinsics themselves are pure, and the IR
+    // passes would otherwise hoist a whole layer's MFMAs to its start.
+    asm volatile("" : "+v"(x));
+    if constexpr (SIG_A) {
+        re = mfma(x, F.re);
+        im = mfma(x, F.im);
+    } else {
+        re = mfma(F.re, x);
+        im = mfma(F.im, x);
+    }
+}
+// One radix-16 layer over slot G on the NQ register quads d[4 tau .. 4 tau + 3].
+// Software-pipelined: the MFMAs of quad tau + 1 (and the LDS operand
+// pre(tau + 1) of its epilogue) are issued before the epilogue of quad tau,
+// and the scheduler may not hoist further (which would keep all 32 results
+// live).  epi(tau, re, im, p) gets the fp32 outputs of quad tau (frequency /
+// row 4 g + jj in element jj) and p = pre(tau).
+struct NoPre {
+    __device__ __forceinline__ uint4 operator()(int) const { return make_uint4(0, 0, 0, 0); }
+};
+template <bool SIG_A, int NQ = 16, class Pre, class Epi>
+__device__ __forceinline__ void layer(uint32_t *d, const Dft &F, Pre &&pre, Epi &&epi) {
+    f4_t re, im;
+    quad_mfma<SIG_A>(d, F, re, im);
+    uint4 pv = pre(0);
+#pragma unroll
+    for (int tau = 0; tau < NQ; ++tau) {
+        f4_t re1, im1;
+        uint4 pv1 = make_uint4(0, 0, 0, 0);
+        if (tau + 1 < NQ) {
+            quad_mfma<SIG_A>(d + 4 * (tau + 1), F, re1, im1);
+            pv1 = pre(tau + 1);
+        }
+        epi(tau, re, im, pv);
+        __builtin_amdgcn_sched_barrier(0);
+        re = re1;
+        im = im1;
+        pv = pv1;
+    }
+}
+
+// Exchange slot G's lane-row bits (lane bits 5, 4) with register-index bits
+// 5, 4.  An involution.
+__device__ __forceinline__ void swap_GT(uint32_t (&d)[64]) {
+#pragma unroll
+    for (int r = 0; r < 32; ++r) {
+        const auto s = __builtin_amdgcn_permlane32_swap(d[r], d[r + 32], false, false);
+        d[r] = s[0];
+        d[r + 32] = s[1];
+    }
+#pragma unroll
+    for (int r = 0; r < 64; ++r) {
+        if (r & 16) continue;
+        const auto s = __builtin_amdgcn_permlane16_swap(d[r], d[r + 16], false, false);
+        d[r] = s[0];
+        d[r + 16] = s[1];
+    }
+}
+
+// s_waitcnt encoding (gfx9): vmcnt <= 16, lgkmcnt and expcnt unconstrained
+constexpr int kWaitVm16 = 0x4F70;
+constexpr int kWaitVm8 = 0x0F78;   // vmcnt <= 8
+constexpr int kWaitVm0 = 0x0F70;   // vmcnt = 0
+
+// Per-lane constants staged in LDS (Lc[kind * 64 + lane]): 0/1 DFT real /
+// imaginary rows, 2/3 the conjugate DFT, 4 the L1 twiddles w_256^{c (4g+j)},
+// 5 the same as (-im, re).  Read right before each layer so that they do not
+// occupy registers across the pair pipeline.
+__device__ __forceinline__ Dft lds_dft(const uint4 *Lc, int lane, bool conj) {
+    asm volatile("" ::: "memory");   // re-read per layer, do not keep live
+    Dft F;
+    F.re = __builtin_bit_cast(h8_t, Lc[(conj ? 2 : 0) * 64 + lane]);
+    F.im = __builtin_bit_cast(h8_t, Lc[(conj ? 3 : 1) * 64 + lane]);
+    return F;
+}
+
+
+// 16-bit I/O helpers
+template <int DT> __device__ __forceinline__ uint32_t pack_out(float lo, float hi);
+template <> __device__ __forceinline__ uint32_t pack_out<F16>(float lo, float hi) { return pk(lo, hi); }
+template <> __device__ __forceinline__ uint32_t pack_out<BF16>(float lo, float hi) {
+    const f2_t v = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, b2_t));
+}
+template <int DT> __device__ __forceinline__ float lo_f(uint32_t r) {
+    return DT == F16 ? (float)as_h2(r).x : __uint_as_float(r << 16);
+}
+template <int DT> __device__ __forceinline__ float hi_f(uint32_t r) {
+    return DT == F16 ? (float)as_h2(r).y : __uint_as_float(r & 0xffff0000u);
+}
+__device__ __forceinline__ h8_t h8_scale(h8_t v, _Float16 s) {
+    const h8_t sv = {s, s, s, s, s, s, s, s};
+    return v * sv;
+}
+
+
+}  // namespace wvc
+}  // namespace h3
