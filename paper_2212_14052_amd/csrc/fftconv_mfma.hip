@@ -711,7 +711,7 @@ bool fftconv_mfma_supported(int L, int dtype) {
 hipError_t launch_fftconv_mfma(const ConvArgs &a, const float *k, hipStream_t s) {
     if (!fftconv_mfma_supported(a.L, a.dtype)) return hipErrorInvalidValue;
     if (fftconv_wave_supported(a.L, a.dtype)) return launch_fftconv_wave(a, k, s);
-    if (fftconv_wave16k_supported(a.L, a.dtype) && a.corr == nullptr) return launch_fftconv_wave16k(a, k, s);
+    if (fftconv_wave16k_supported(a.L, a.dtype)) return launch_fftconv_wave16k(a, k, s);
     int pairs_per_ch;
     if (a.pair_mode == 0)
         pairs_per_ch = (a.B + 1) / 2;

@@ -276,12 +276,50 @@ __device__ __forceinline__ void twiddles_inv(uint4 X, uint32_t xh, uint32_t (&xw
 // buffer: slot ((source * 4 + destination) * 2 + tt % 2); every quarter,
 // the wave's own included, passes through LDS, so no register index depends
 // on the wave.
-template <int DT>
+// One source block's contribution to the two output tiles of a half:
+// D0 += G b, D1 += i^{k3'} G b, with the rotation done by choosing the
+// matrix row kind and the sign of the data.
+template <int K3P>
+__device__ __forceinline__ void last_acc(uint4 gr4, uint4 gi4, uint4 b4, f4_t (&D)[4]) {
+    const h8_t Ar = __builtin_bit_cast(h8_t, gr4), Ai = __builtin_bit_cast(h8_t, gi4);
+    const h8_t b = __builtin_bit_cast(h8_t, b4);
+    D[0] = mfma_acc(Ar, b, D[0]);
+    D[1] = mfma_acc(Ai, b, D[1]);
+    if constexpr (K3P == 0) {
+        D[2] = mfma_acc(Ar, b, D[2]);
+        D[3] = mfma_acc(Ai, b, D[3]);
+    } else {
+        const h8_t nb = __builtin_bit_cast(
+            h8_t, make_uint4(b4.x ^ 0x80008000u, b4.y ^ 0x80008000u, b4.z ^ 0x80008000u, b4.w ^ 0x80008000u));
+        if constexpr (K3P == 1) {   // i P: (-Im P, Re P)
+            D[2] = mfma_acc(Ai, nb, D[2]);
+            D[3] = mfma_acc(Ar, b, D[3]);
+        } else if constexpr (K3P == 2) {   // -P
+            D[2] = mfma_acc(Ar, nb, D[2]);
+            D[3] = mfma_acc(Ai, nb, D[3]);
+        } else {   // -i P: (Im P, -Re P)
+            D[2] = mfma_acc(Ai, b, D[2]);
+            D[3] = mfma_acc(Ar, nb, D[3]);
+        }
+    }
+}
+
+// Last layer for the wave's own tiles T = 4 w + tt: exchange, 64-point
+// contraction with the radix-4 butterfly, output epilogue and stores.
+//   D0 = sum_k3' G_k3' x_k3'           -> y(m)
+//   D1 = sum_k3' i^{k3'} G_k3' x_k3'   -> y(4096 + m)
+// (real parts row a, imaginary parts row b).  The exchange runs in two
+// halves (tiles tt = 0, 1, then 2, 3 of every quarter) through a 32 KB
+// buffer: slot ((source * 4 + destination) * 2 + tt % 2); every quarter,
+// the wave's own included, passes through LDS, so no register index depends
+// on the wave.  Source blocks are visited in order with their operands
+// loaded one block ahead.
+template <int DT, int CORR>
 __device__ __forceinline__ void last_layer(uint32_t (&d)[64], uint4 *U, const uint4 *G1, int w, int lane,
-                                           float sc, uint16_t *ya, uint16_t *yb, bool has_b) {
+                                           float sc, uint16_t *ya, uint16_t *yb, bool has_b, const void *cra,
+                                           const void *crb) {
     const int g = lane >> 4, c = lane & 15;
     uint32_t pa0[8], pb0[8], pa1[8], pb1[8];   // packed outputs: [2 jj + half]
-    float qa0[4], qb0[4], qa1[4], qb1[4];       // previous (even) tile
     const f4_t z = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
@@ -294,63 +332,91 @@ __device__ __forceinline__ void last_layer(uint32_t (&d)[64], uint4 *U, const ui
                 U[((w * 4 + q) * 2 + t2) * 64 + lane] = make_uint4(d[4 * T], d[4 * T + 1], d[4 * T + 2], d[4 * T + 3]);
             }
         __syncthreads();
+        f4_t D[2][4] = {{z, z, z, z}, {z, z, z, z}};
+        uint4 gr = G1[lane], gi = G1[64 + lane];
+        uint4 b0 = U[((0 * 4 + w) * 2 + 0) * 64 + lane], b1 = U[((0 * 4 + w) * 2 + 1) * 64 + lane];
 #pragma unroll
-        for (int t2 = 0; t2 < 2; ++t2) {
-            const int tt = 2 * half + t2;
-            f4_t D0r = z, D0i = z, D1r = z, D1i = z;
-#pragma unroll
-            for (int k3p = 0; k3p < 4; ++k3p) {   // source wave = block k3'
-                asm volatile("" ::: "memory");   // matrices re-read per use, not held across the layer
-                const uint4 B4 = U[((k3p * 4 + w) * 2 + t2) * 64 + lane];
-                const uint4 nB4 = make_uint4(B4.x ^ 0x80008000u, B4.y ^ 0x80008000u, B4.z ^ 0x80008000u,
-                                             B4.w ^ 0x80008000u);
-                const h8_t b = __builtin_bit_cast(h8_t, B4), nb = __builtin_bit_cast(h8_t, nB4);
-                const h8_t Ar = __builtin_bit_cast(h8_t, G1[(2 * k3p) * 64 + lane]);
-                const h8_t Ai = __builtin_bit_cast(h8_t, G1[(2 * k3p + 1) * 64 + lane]);
-                D0r = mfma_acc(Ar, b, D0r);
-                D0i = mfma_acc(Ai, b, D0i);
-                if (k3p == 0) {
-                    D1r = mfma_acc(Ar, b, D1r);
-                    D1i = mfma_acc(Ai, b, D1i);
-                } else if (k3p == 1) {   // i P: (-Im P, Re P)
-                    D1r = mfma_acc(Ai, nb, D1r);
-                    D1i = mfma_acc(Ar, b, D1i);
-                } else if (k3p == 2) {   // -P
-                    D1r = mfma_acc(Ar, nb, D1r);
-                    D1i = mfma_acc(Ai, nb, D1i);
-                } else {                 // -i P: (Im P, -Re P)
-                    D1r = mfma_acc(Ai, b, D1r);
-                    D1i = mfma_acc(Ar, nb, D1i);
-                }
+        for (int k3p = 0; k3p < 4; ++k3p) {
+            uint4 ngr = gr, ngi = gi, nb0 = b0, nb1 = b1;
+            if (k3p + 1 < 4) {
+                ngr = G1[(2 * k3p + 2) * 64 + lane];
+                ngi = G1[(2 * k3p + 3) * 64 + lane];
+                nb0 = U[(((k3p + 1) * 4 + w) * 2 + 0) * 64 + lane];
+                nb1 = U[(((k3p + 1) * 4 + w) * 2 + 1) * 64 + lane];
             }
-#pragma unroll
-            for (int jj = 0; jj < 4; ++jj) {
-                const float a0 = D0r[jj] * sc, b0 = D0i[jj] * sc, a1 = D1r[jj] * sc, b1 = D1i[jj] * sc;
-                if (t2 == 0) {
-                    qa0[jj] = a0;
-                    qb0[jj] = b0;
-                    qa1[jj] = a1;
-                    qb1[jj] = b1;
-                } else {
-                    const int s = 2 * jj + half;
-                    pa0[s] = pack_out<DT>(qa0[jj], a0);
-                    pb0[s] = pack_out<DT>(qb0[jj], b0);
-                    pa1[s] = pack_out<DT>(qa1[jj], a1);
-                    pb1[s] = pack_out<DT>(qb1[jj], b1);
-                }
+            if (k3p == 0) {
+                last_acc<0>(gr, gi, b0, D[0]);
+                last_acc<0>(gr, gi, b1, D[1]);
+            } else if (k3p == 1) {
+                last_acc<1>(gr, gi, b0, D[0]);
+                last_acc<1>(gr, gi, b1, D[1]);
+            } else if (k3p == 2) {
+                last_acc<2>(gr, gi, b0, D[0]);
+                last_acc<2>(gr, gi, b1, D[1]);
+            } else {
+                last_acc<3>(gr, gi, b0, D[0]);
+                last_acc<3>(gr, gi, b1, D[1]);
             }
             __builtin_amdgcn_sched_barrier(0);
+            gr = ngr;
+            gi = ngi;
+            b0 = nb0;
+            b1 = nb1;
+        }
+        // tiles 2 half (D[0]) and 2 half + 1 (D[1]) are consecutive points
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+            const int s = 2 * jj + half;
+            pa0[s] = pack_out<DT>(D[0][0][jj] * sc, D[1][0][jj] * sc);
+            pb0[s] = pack_out<DT>(D[0][1][jj] * sc, D[1][1][jj] * sc);
+            pa1[s] = pack_out<DT>(D[0][2][jj] * sc, D[1][2][jj] * sc);
+            pb1[s] = pack_out<DT>(D[0][3][jj] * sc, D[1][3][jj] * sc);
         }
     }
-    // outputs m = 256 (4 g + jj) + 16 c + 4 w + (0..3): 8 bytes per row and t3
+    // outputs m = 256 (4 g + jj) + 16 c + 4 w + (0..3) of both rows go
+    // through LDS (rows a, b as 8192 halves each), then out as 16-byte
+    // chunks, each wave a contiguous quarter of the pair
+    __syncthreads();   // every exchange read is done
+    uint2 *Uo = (uint2 *)U;
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
-        const int m = 256 * (4 * g + jj) + 16 * c + 4 * w;
-        *(uint2 *)(ya + m) = make_uint2(pa0[2 * jj], pa0[2 * jj + 1]);
-        *(uint2 *)(ya + 4096 + m) = make_uint2(pa1[2 * jj], pa1[2 * jj + 1]);
-        if (has_b) {
-            *(uint2 *)(yb + m) = make_uint2(pb0[2 * jj], pb0[2 * jj + 1]);
-            *(uint2 *)(yb + 4096 + m) = make_uint2(pb1[2 * jj], pb1[2 * jj + 1]);
+        const int m4 = (256 * (4 * g + jj) + 16 * c + 4 * w) >> 2;
+        Uo[m4] = make_uint2(pa0[2 * jj], pa0[2 * jj + 1]);
+        Uo[1024 + m4] = make_uint2(pa1[2 * jj], pa1[2 * jj + 1]);
+        Uo[2048 + m4] = make_uint2(pb0[2 * jj], pb0[2 * jj + 1]);
+        Uo[3072 + m4] = make_uint2(pb1[2 * jj], pb1[2 * jj + 1]);
+    }
+    __syncthreads();
+    uint16_t *yrow = w < 2 ? ya : yb;   // wave w: row w >> 1, half w & 1
+    const void *crow = w < 2 ? cra : crb;
+    if (w < 2 || has_b) {
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+            const int i8 = (w & 1) * 512 + r * 64 + lane;   // uint4 index within the row
+            uint4 v = U[(w >> 1) * 1024 + i8];
+            if constexpr (CORR != 0) {
+                // state-passing initial-state term, added to the 16-bit outputs
+                float cv[8];
+                if constexpr (CORR == 1) {
+                    const float4 c0 = ((const float4 *)crow)[2 * i8], c1 = ((const float4 *)crow)[2 * i8 + 1];
+                    cv[0] = c0.x; cv[1] = c0.y; cv[2] = c0.z; cv[3] = c0.w;
+                    cv[4] = c1.x; cv[5] = c1.y; cv[6] = c1.z; cv[7] = c1.w;
+                } else {
+                    const uint4 cr = ((const uint4 *)crow)[i8];
+                    const uint32_t cw[4] = {cr.x, cr.y, cr.z, cr.w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        cv[2 * e] = lo_f<DT>(cw[e]);
+                        cv[2 * e + 1] = hi_f<DT>(cw[e]);
+                    }
+                }
+                uint32_t vw[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    vw[e] = pack_out<DT>(lo_f<DT>(vw[e]) + cv[2 * e], hi_f<DT>(vw[e]) + cv[2 * e + 1]);
+                v = make_uint4(vw[0], vw[1], vw[2], vw[3]);
+            }
+            *(uint4 *)(yrow + 8 * i8) = v;
         }
     }
 }
@@ -386,7 +452,8 @@ template <> __device__ __forceinline__ float raw_max<BF16>(const uint4 (&ra)[4],
 }  // namespace w16
 
 // ============================================================================
-template <int DT>
+// CORR: 0 none, 1 float32 correction term, 2 correction term in the I/O dtype
+template <int DT, int CORR>
 __global__ __launch_bounds__(w16::NT) __attribute__((amdgpu_waves_per_eu(2))) void fftconv_wave16k_kernel(
     ConvArgs a, const float *k, int wg_per_ch, int pairs_per_ch) {
     using namespace w16;
@@ -659,14 +726,23 @@ __global__ __launch_bounds__(w16::NT) __attribute__((amdgpu_waves_per_eu(2))) vo
         rows(qq, oa, ob);
         const float sc = ldexpf(1.0f, kexp + eu);
         uint16_t *ya = y + oa, *yb = y + (ob >= 0 ? ob : oa);
-        last_layer<DT>(d, U, G1, w, lane, sc, ya, yb, ob >= 0);
+        const long obc = ob >= 0 ? ob : oa;
+        const void *cra = nullptr, *crb = nullptr;
+        if (CORR == 1) {
+            cra = (const float *)a.corr + oa;
+            crb = (const float *)a.corr + obc;
+        } else if (CORR == 2) {
+            cra = (const uint16_t *)a.corr + oa;
+            crb = (const uint16_t *)a.corr + obc;
+        }
+        last_layer<DT, CORR>(d, U, G1, w, lane, sc, ya, yb, ob >= 0, cra, crb);
     }
 }
 
 bool fftconv_wave16k_supported(int L, int dtype) { return L == w16::L && (dtype == F16 || dtype == BF16); }
 
 hipError_t launch_fftconv_wave16k(const ConvArgs &a, const float *k, hipStream_t s) {
-    if (!fftconv_wave16k_supported(a.L, a.dtype) || a.corr != nullptr) return hipErrorInvalidValue;
+    if (!fftconv_wave16k_supported(a.L, a.dtype)) return hipErrorInvalidValue;
     int pairs_per_ch;
     if (a.pair_mode == 0)
         pairs_per_ch = (a.B + 1) / 2;
@@ -677,10 +753,19 @@ hipError_t launch_fftconv_wave16k(const ConvArgs &a, const float *k, hipStream_t
     int wg_per_ch = 1;
     while ((long)a.H * wg_per_ch < 512 && pairs_per_ch >= 4 * wg_per_ch) wg_per_ch *= 2;
     dim3 grid(a.H * wg_per_ch), block(w16::NT);
-    if (a.dtype == F16)
-        hipLaunchKernelGGL(fftconv_wave16k_kernel<F16>, grid, block, 0, s, a, k, wg_per_ch, pairs_per_ch);
-    else
-        hipLaunchKernelGGL(fftconv_wave16k_kernel<BF16>, grid, block, 0, s, a, k, wg_per_ch, pairs_per_ch);
+    const int corr = a.corr == nullptr ? 0 : (a.corr16 ? 2 : 1);
+#define H3_W16_LAUNCH(DTV, CV) \
+    hipLaunchKernelGGL((fftconv_wave16k_kernel<DTV, CV>), grid, block, 0, s, a, k, wg_per_ch, pairs_per_ch)
+    if (a.dtype == F16) {
+        if (corr == 0) H3_W16_LAUNCH(F16, 0);
+        else if (corr == 1) H3_W16_LAUNCH(F16, 1);
+        else H3_W16_LAUNCH(F16, 2);
+    } else {
+        if (corr == 0) H3_W16_LAUNCH(BF16, 0);
+        else if (corr == 1) H3_W16_LAUNCH(BF16, 1);
+        else H3_W16_LAUNCH(BF16, 2);
+    }
+#undef H3_W16_LAUNCH
     return hipGetLastError();
 }
 

@@ -45,8 +45,8 @@ bool fftconv_mfma_supported(int L, int dtype);
 // launch_fftconv_mfma for that length.
 hipError_t launch_fftconv_wave(const ConvArgs &a, const float *k, hipStream_t s);
 bool fftconv_wave_supported(int L, int dtype);
-// Four-wavefronts-per-pair variant for L = 8192 (16-bit I/O, no correction
-// term); used by launch_fftconv_mfma for that length.
+// Four-wavefronts-per-pair variant for L = 8192 (16-bit I/O); used by
+// launch_fftconv_mfma for that length.
 hipError_t launch_fftconv_wave16k(const ConvArgs &a, const float *k, hipStream_t s);
 bool fftconv_wave16k_supported(int L, int dtype);
 
