@@ -188,6 +188,26 @@ int h3_statepass_conv(const void *u, const float *Abar, const float *Bbar, const
     // s_c = M_ux u^(c) for every chunk, then the scan over chunks
     if ((e = launch_chunk_states(u, Abar, Bbar, B, H, L, m, chunk, dtype, states, s)) != hipSuccess)
         return H3_EDEVICE;
+    if (fftconv_wave16k_supported(chunk, dtype)) {
+        // chunk = 8192: the conv computes M_xy x^(c) itself from normalised
+        // weights (scan output) and per-channel power tables, both kept in
+        // the correction-term region
+        char *cr = ws + w.corr;
+        uint4 *ctab = (uint4 *)cr;
+        uint32_t *w16 = (uint32_t *)(cr + align_up((size_t)H * CORR_TAB_U4 * sizeof(uint4)));
+        int *wexp = (int *)((char *)w16 + align_up((size_t)B * H * nchunk * 64 * sizeof(uint32_t)));
+        if ((e = launch_state_scan_w16(Abar, C, x0, states, B, H, m, chunk, nchunk, w16, wexp, x_final, s)) !=
+            hipSuccess)
+            return H3_EDEVICE;
+        if ((e = launch_corr_tables(Abar, H, m, ctab, s)) != hipSuccess) return H3_EDEVICE;
+        ConvArgs a{};
+        a.u = u; a.y = y; a.Kspec = Kspec; a.D = D;
+        a.B = B; a.H = H; a.L = chunk; a.nchunk = nchunk; a.pair_mode = 1; a.dtype = dtype;
+        a.corr = w16;
+        a.corr_tab = ctab;
+        a.corr_e = wexp;
+        return launched(launch_fftconv_mfma(a, kbuf, s));
+    }
     if ((e = launch_state_scan(Abar, C, x0, states, B, H, m, chunk, nchunk, corr_W, x_final, s)) !=
         hipSuccess)
         return H3_EDEVICE;

@@ -106,6 +106,7 @@ __device__ const Half16 kHalf16 = make_half16();
 //   [8..11] w_16384^{k3 (4g+i)}        third layer, contraction point i
 //   [12]    w_16384^{-k3 c}            inverse third layer, output row c
 //   [13]    w_1024^{-k3 c}             inverse second layer's lane twiddles
+//   [14,15] w_64^{-c}, w_64^{-2c}      last layer's rows, when not tabulated
 struct Fac16 {
     uint32_t v[4 * 64 * 16];
 };
@@ -126,6 +127,9 @@ constexpr Fac16 make_fac16() {
             const Cd r3 = cwd(-k3 * c, N), rx = cwd(-k3 * c, 1024);
             p[12] = h2_bits(r3.re, r3.im);
             p[13] = h2_bits(rx.re, rx.im);
+            const Cd g1 = cwd(-c, 64), g2 = cwd(-2 * c, 64);
+            p[14] = h2_bits(g1.re, g1.im);
+            p[15] = h2_bits(g2.re, g2.im);
         }
     return t;
 }
@@ -267,15 +271,6 @@ __device__ __forceinline__ void twiddles_inv(uint4 X, uint32_t xh, uint32_t (&xw
     }
 }
 
-// Last layer for the wave's own tiles T = 4 w + tt: exchange, 64-point
-// contraction with the radix-4 butterfly, output epilogue and stores.
-//   D0 = sum_k3' G_k3' x_k3'           -> y(m)
-//   D1 = sum_k3' i^{k3'} G_k3' x_k3'   -> y(4096 + m)
-// (real parts row a, imaginary parts row b).  The exchange runs in two
-// halves (tiles tt = 0, 1, then 2, 3 of every quarter) through a 32 KB
-// buffer: slot ((source * 4 + destination) * 2 + tt % 2); every quarter,
-// the wave's own included, passes through LDS, so no register index depends
-// on the wave.
 // One source block's contribution to the two output tiles of a half:
 // D0 += G b, D1 += i^{k3'} G b, with the rotation done by choosing the
 // matrix row kind and the sign of the data.
@@ -304,6 +299,65 @@ __device__ __forceinline__ void last_acc(uint4 gr4, uint4 gi4, uint4 b4, f4_t (&
     }
 }
 
+// Fused initial-state term (state passing, chunk = 8192): for this wave's
+// quarter of the pair (row w >> 1, t in [4096 (w & 1), + 4096)), with
+// t = 64 a + b,  corr(t) = 2 Re sum_n Abar_n^b V_n(a),  V_n(a) = W_n Abar_n^{64 a},
+// as 16 tiles D[b][a] of 16 x 16 on the matrix cores (K = 64 modes as (re, im)
+// pairs): the A operand Abar_n^b comes from the per-channel table in LDS, the
+// B operand V from the row's weights W (normalised to max |W| in [1/2, 1),
+// fp16) times Abar_n^{64 a}, stepping a by 16 with Abar_n^1024.  A lane ends
+// up with four consecutive t: they are added in fp32 to the staged 16-bit
+// outputs and stored as 8 bytes.
+template <int DT>
+__device__ __forceinline__ void fused_state_term(const uint4 *U, const uint4 *CT, const uint4 (&wq)[4], int ew,
+                                                 int w, int lane, uint16_t *yrow) {
+    const int g = lane >> 4, c = lane & 15;
+    const uint4 *CA = CT, *T64 = CT + 1024, *Zt = CT + 1536;
+    const float scorr = ldexpf(2.0f, ew);
+    // wq[kb]: normalised W of modes 16 kb + 4 g + q in dword q
+    uint32_t V[16];   // [4 kb + q]: (Re V, -Im V) of mode 16 kb + 4 g + q, column a = 64 (w & 1) + c
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+        const uint4 tq = T64[((w & 1) * 4 + kb) * 64 + lane];
+        // conj(V) = conj(W) conj(Abar^{64 a}), stored (Re V, -Im V)
+        V[4 * kb + 0] = cmulc(wq[kb].x ^ 0x80000000u, tq.x);
+        V[4 * kb + 1] = cmulc(wq[kb].y ^ 0x80000000u, tq.y);
+        V[4 * kb + 2] = cmulc(wq[kb].z ^ 0x80000000u, tq.z);
+        V[4 * kb + 3] = cmulc(wq[kb].w ^ 0x80000000u, tq.w);
+    }
+    const f4_t z = {0.f, 0.f, 0.f, 0.f};
+    const uint2 *Uo = (const uint2 *)U;
+    const int row = w >> 1;
+#pragma unroll
+    for (int jb = 0; jb < 4; ++jb) {
+        if (jb > 0) {
+            // a += 16: V <- V Abar^1024, i.e. the stored conj(V) times conj(Abar^1024)
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) {
+                const uint4 zq = Zt[kb * 4 + g];
+                V[4 * kb + 0] = cmulc(V[4 * kb + 0], zq.x);
+                V[4 * kb + 1] = cmulc(V[4 * kb + 1], zq.y);
+                V[4 * kb + 2] = cmulc(V[4 * kb + 2], zq.z);
+                V[4 * kb + 3] = cmulc(V[4 * kb + 3], zq.w);
+            }
+        }
+#pragma unroll
+        for (int ib = 0; ib < 4; ++ib) {
+            f4_t D = z;
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+                D = mfma_acc(__builtin_bit_cast(h8_t, CA[(ib * 4 + kb) * 64 + lane]),
+                             h8_of(V[4 * kb], V[4 * kb + 1], V[4 * kb + 2], V[4 * kb + 3]), D);
+            // rows b = 16 ib + 4 g + jj, column a = 64 (w & 1) + 16 jb + c
+            const int t = 4096 * (w & 1) + 1024 * jb + 64 * c + 16 * ib + 4 * g;
+            const uint2 o = Uo[row * 2048 + (t >> 2)];
+            const uint2 r = make_uint2(pack_out<DT>(fmaf(D[0], scorr, lo_f<DT>(o.x)), fmaf(D[1], scorr, hi_f<DT>(o.x))),
+                                       pack_out<DT>(fmaf(D[2], scorr, lo_f<DT>(o.y)), fmaf(D[3], scorr, hi_f<DT>(o.y))));
+            *(uint2 *)(yrow + t) = r;
+        }
+    }
+}
+
 // Last layer for the wave's own tiles T = 4 w + tt: exchange, 64-point
 // contraction with the radix-4 butterfly, output epilogue and stores.
 //   D0 = sum_k3' G_k3' x_k3'           -> y(m)
@@ -313,14 +367,39 @@ __device__ __forceinline__ void last_acc(uint4 gr4, uint4 gi4, uint4 b4, f4_t (&
 // buffer: slot ((source * 4 + destination) * 2 + tt % 2); every quarter,
 // the wave's own included, passes through LDS, so no register index depends
 // on the wave.  Source blocks are visited in order with their operands
-// loaded one block ahead.
+// loaded one block ahead.  G_k3' comes from the LDS table G1, or (CORR 3,
+// whose LDS holds the state-term tables instead) from the conjugate DFT rows
+// times the lane's w_64^{-k3' c} (gf[k3' - 1]).
 template <int DT, int CORR>
-__device__ __forceinline__ void last_layer(uint32_t (&d)[64], uint4 *U, const uint4 *G1, int w, int lane,
-                                           float sc, uint16_t *ya, uint16_t *yb, bool has_b, const void *cra,
-                                           const void *crb) {
+__device__ __forceinline__ void last_layer(uint32_t (&d)[64], uint4 *U, const uint4 *G1, const uint4 *Lc,
+                                           const uint32_t (&gf)[3], int w, int lane, float sc, uint16_t *ya,
+                                           uint16_t *yb, bool has_b, const void *cra, const void *crb, int ewa,
+                                           int ewb) {
     const int g = lane >> 4, c = lane & 15;
     uint32_t pa0[8], pb0[8], pa1[8], pb1[8];   // packed outputs: [2 jj + half]
     const f4_t z = {0.f, 0.f, 0.f, 0.f};
+    // this wave's share of the read-out below: row w >> 1, 16-byte pieces
+    // i8 = (w & 1) 512 + 64 r + lane
+    uint16_t *yrow = w < 2 ? ya : yb;
+    const void *crow = w < 2 ? cra : crb;
+    const bool active = w < 2 || has_b;
+    uint4 c16[8];   // 16-bit correction term, loaded while the last layer runs
+    uint4 wq[4];    // fused state term: the row's weights W for the lane's 16 modes
+    auto kinds = [&](int k3p, uint4 &gr, uint4 &gi) {
+        if constexpr (CORR != 3) {
+            gr = G1[(2 * k3p) * 64 + lane];
+            gi = G1[(2 * k3p + 1) * 64 + lane];
+        } else if (k3p == 0) {
+            gr = Lc[2 * 64 + lane];
+            gi = Lc[3 * 64 + lane];
+        } else {
+            uint32_t R[4], I[4];
+            const uint32_t ff[4] = {gf[k3p - 1], gf[k3p - 1], gf[k3p - 1], gf[k3p - 1]};
+            kinds_scaled(Lc[3 * 64 + lane], ff, R, I);
+            gr = make_uint4(R[0], R[1], R[2], R[3]);
+            gi = make_uint4(I[0], I[1], I[2], I[3]);
+        }
+    };
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
         if (half == 1) __syncthreads();   // the first half's reads are done
@@ -331,16 +410,21 @@ __device__ __forceinline__ void last_layer(uint32_t (&d)[64], uint4 *U, const ui
                 const int T = 4 * q + 2 * half + t2;
                 U[((w * 4 + q) * 2 + t2) * 64 + lane] = make_uint4(d[4 * T], d[4 * T + 1], d[4 * T + 2], d[4 * T + 3]);
             }
+        if (CORR == 2 && half == 1) {
+#pragma unroll
+            for (int r = 0; r < 8; ++r)
+                c16[r] = active ? ((const uint4 *)crow)[(w & 1) * 512 + r * 64 + lane] : make_uint4(0, 0, 0, 0);
+        }
         __syncthreads();
         f4_t D[2][4] = {{z, z, z, z}, {z, z, z, z}};
-        uint4 gr = G1[lane], gi = G1[64 + lane];
+        uint4 gr, gi;
+        kinds(0, gr, gi);
         uint4 b0 = U[((0 * 4 + w) * 2 + 0) * 64 + lane], b1 = U[((0 * 4 + w) * 2 + 1) * 64 + lane];
 #pragma unroll
         for (int k3p = 0; k3p < 4; ++k3p) {
             uint4 ngr = gr, ngi = gi, nb0 = b0, nb1 = b1;
             if (k3p + 1 < 4) {
-                ngr = G1[(2 * k3p + 2) * 64 + lane];
-                ngi = G1[(2 * k3p + 3) * 64 + lane];
+                kinds(k3p + 1, ngr, ngi);
                 nb0 = U[(((k3p + 1) * 4 + w) * 2 + 0) * 64 + lane];
                 nb1 = U[(((k3p + 1) * 4 + w) * 2 + 1) * 64 + lane];
             }
@@ -362,6 +446,11 @@ __device__ __forceinline__ void last_layer(uint32_t (&d)[64], uint4 *U, const ui
             gi = ngi;
             b0 = nb0;
             b1 = nb1;
+        }
+        if (CORR == 3 && half == 1) {
+            // the row's weights for modes 16 kb + 4 g + (0..3): one uint4 per kb
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) wq[kb] = active ? ((const uint4 *)crow)[4 * kb + g] : make_uint4(0, 0, 0, 0);
         }
         // tiles 2 half (D[0]) and 2 half + 1 (D[1]) are consecutive points
 #pragma unroll
@@ -387,9 +476,11 @@ __device__ __forceinline__ void last_layer(uint32_t (&d)[64], uint4 *U, const ui
         Uo[3072 + m4] = make_uint2(pb1[2 * jj], pb1[2 * jj + 1]);
     }
     __syncthreads();
-    uint16_t *yrow = w < 2 ? ya : yb;   // wave w: row w >> 1, half w & 1
-    const void *crow = w < 2 ? cra : crb;
-    if (w < 2 || has_b) {
+    if constexpr (CORR == 3) {
+        if (active) fused_state_term<DT>(U, G1, wq, w < 2 ? ewa : ewb, w, lane, yrow);
+        return;
+    }
+    if (active) {
 #pragma unroll
         for (int r = 0; r < 8; ++r) {
             const int i8 = (w & 1) * 512 + r * 64 + lane;   // uint4 index within the row
@@ -402,7 +493,7 @@ __device__ __forceinline__ void last_layer(uint32_t (&d)[64], uint4 *U, const ui
                     cv[0] = c0.x; cv[1] = c0.y; cv[2] = c0.z; cv[3] = c0.w;
                     cv[4] = c1.x; cv[5] = c1.y; cv[6] = c1.z; cv[7] = c1.w;
                 } else {
-                    const uint4 cr = ((const uint4 *)crow)[i8];
+                    const uint4 cr = c16[r];
                     const uint32_t cw[4] = {cr.x, cr.y, cr.z, cr.w};
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
@@ -452,12 +543,16 @@ template <> __device__ __forceinline__ float raw_max<BF16>(const uint4 (&ra)[4],
 }  // namespace w16
 
 // ============================================================================
-// CORR: 0 none, 1 float32 correction term, 2 correction term in the I/O dtype
+// CORR: 0 none, 1 float32 correction term, 2 correction term in the I/O dtype,
+// 3 the term computed here from the chunk's weights W
 template <int DT, int CORR>
 __global__ __launch_bounds__(w16::NT) __attribute__((amdgpu_waves_per_eu(2))) void fftconv_wave16k_kernel(
     ConvArgs a, const float *k, int wg_per_ch, int pairs_per_ch) {
     using namespace w16;
-    __shared__ uint4 Tab[kTab16];   // Ytab + Lc + last-layer matrices
+    // Ytab + Lc, then the last layer's matrices, or (CORR 3) the channel's
+    // state-term tables
+    constexpr int kTabAll = CORR == 3 ? kTab + CORR_TAB_U4 : kTab16;
+    __shared__ uint4 Tab[kTabAll];
     __shared__ uint4 U[kU];         // pair staging, then the last-layer exchange
     __shared__ float red[2 * NW];
     const uint4 *Ytab = Tab, *Lc = Tab + kTabY, *G1 = Tab + kTab;
@@ -511,14 +606,16 @@ __global__ __launch_bounds__(w16::NT) __attribute__((amdgpu_waves_per_eu(2))) vo
 
     // ---- start-up loads: tables into LDS, factors, kernel row, first pair ----
 #pragma unroll
-    for (int r = 0; r < (kTab16 + NT - 1) / NT; ++r) {
-        const int base = r * NT + 64 * w;
-        if (base < kTab16)
-            __builtin_amdgcn_global_load_lds((gvoid_t *)((const uint4 *)kHalf16.v + base + lane),
-                                             (lvoid_t *)(Tab + base), 16, 0, 0);
+    for (int r = 0; r < (kTabAll + NT - 1) / NT; ++r) {
+        const int base = r * NT + 64 * w;   // kTab and CORR_TAB_U4 are multiples of 64
+        if (base < kTabAll) {
+            const uint4 *src = (CORR != 3 || base < kTab) ? (const uint4 *)kHalf16.v + base
+                                                         : a.corr_tab + (long)h * CORR_TAB_U4 + (base - kTab);
+            __builtin_amdgcn_global_load_lds((gvoid_t *)(src + lane), (lvoid_t *)(Tab + base), 16, 0, 0);
+        }
     }
     __builtin_amdgcn_sched_barrier(0);
-    uint32_t f1[4], xf[4], f3[4], g3, xh;
+    uint32_t f1[4], xf[4], f3[4], g3, xh, gf[3];
     {
         const uint4 *fp = (const uint4 *)kFac16.v + (w * 64 + lane) * 4;
         const uint4 v0 = fp[0], v1 = fp[1], v2 = fp[2], v3 = fp[3];
@@ -527,6 +624,9 @@ __global__ __launch_bounds__(w16::NT) __attribute__((amdgpu_waves_per_eu(2))) vo
         f3[0] = v2.x; f3[1] = v2.y; f3[2] = v2.z; f3[3] = v2.w;
         g3 = v3.x;
         xh = v3.y;
+        gf[0] = v3.z;
+        gf[1] = v3.w;
+        gf[2] = cmul(v3.z, v3.w);   // w_64^{-3c}
     }
     float4 kq[8];   // [4 gi + s]: points m = ... + 16 c + 4 s .. + 3
 #pragma unroll
@@ -735,7 +835,14 @@ __global__ __launch_bounds__(w16::NT) __attribute__((amdgpu_waves_per_eu(2))) vo
             cra = (const uint16_t *)a.corr + oa;
             crb = (const uint16_t *)a.corr + obc;
         }
-        last_layer<DT, CORR>(d, U, G1, w, lane, sc, ya, yb, ob >= 0, cra, crb);
+        int ewa = 0, ewb = 0;
+        if (CORR == 3) {   // normalised weights W of chunk rows oa / L, obc / L
+            cra = (const uint32_t *)a.corr + (oa / L) * 64;
+            crb = (const uint32_t *)a.corr + (obc / L) * 64;
+            ewa = a.corr_e[oa / L];
+            ewb = a.corr_e[obc / L];
+        }
+        last_layer<DT, CORR>(d, U, G1, Lc, gf, w, lane, sc, ya, yb, ob >= 0, cra, crb, ewa, ewb);
     }
 }
 
@@ -753,17 +860,20 @@ hipError_t launch_fftconv_wave16k(const ConvArgs &a, const float *k, hipStream_t
     int wg_per_ch = 1;
     while ((long)a.H * wg_per_ch < 512 && pairs_per_ch >= 4 * wg_per_ch) wg_per_ch *= 2;
     dim3 grid(a.H * wg_per_ch), block(w16::NT);
-    const int corr = a.corr == nullptr ? 0 : (a.corr16 ? 2 : 1);
+    const int corr = a.corr == nullptr ? 0 : a.corr_tab != nullptr ? 3 : (a.corr16 ? 2 : 1);
+    if (corr == 3 && (a.pair_mode != 1 || a.corr_e == nullptr)) return hipErrorInvalidValue;
 #define H3_W16_LAUNCH(DTV, CV) \
     hipLaunchKernelGGL((fftconv_wave16k_kernel<DTV, CV>), grid, block, 0, s, a, k, wg_per_ch, pairs_per_ch)
     if (a.dtype == F16) {
         if (corr == 0) H3_W16_LAUNCH(F16, 0);
         else if (corr == 1) H3_W16_LAUNCH(F16, 1);
-        else H3_W16_LAUNCH(F16, 2);
+        else if (corr == 2) H3_W16_LAUNCH(F16, 2);
+        else H3_W16_LAUNCH(F16, 3);
     } else {
         if (corr == 0) H3_W16_LAUNCH(BF16, 0);
         else if (corr == 1) H3_W16_LAUNCH(BF16, 1);
-        else H3_W16_LAUNCH(BF16, 2);
+        else if (corr == 2) H3_W16_LAUNCH(BF16, 2);
+        else H3_W16_LAUNCH(BF16, 3);
     }
 #undef H3_W16_LAUNCH
     return hipGetLastError();

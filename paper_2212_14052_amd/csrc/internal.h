@@ -35,6 +35,13 @@ struct ConvArgs {
     // (B, H, nchunk * L) added to the output; float32, or the I/O dtype if corr16
     const void *corr;
     int corr16;
+    // fused initial-state term (mode 1, L = 8192 conv only): when corr_tab is
+    // set, corr holds the normalised weights (B, H, nchunk, 64) fp16 complex
+    // and corr_e their exponents (B, H, nchunk), as written by
+    // launch_state_scan_w16, and corr_tab the per-channel tables written by
+    // launch_corr_tables
+    const uint4 *corr_tab;
+    const int *corr_e;
 };
 hipError_t launch_fftconv(const ConvArgs &a, hipStream_t s);
 // Matrix-core block-FFT variant (16-bit I/O, L = 2048): computes the kernel
@@ -62,6 +69,14 @@ hipError_t launch_state_scan(const float *Abar, const float *C, const float *x0,
 hipError_t launch_state_correction(const float *Abar, const float2 *corr_W, int B, int H, int m,
                                    int chunk, int nchunk, float *corr, hipStream_t s);
 bool state_correction_mfma_ok(int chunk, int dtype);
+// Per-channel tables for the fused initial-state term of the L = 8192 conv
+// (CORR_TAB_U4 uint4 per channel, the last 48 unused; m <= 64).
+constexpr int CORR_TAB_U4 = 1600;
+hipError_t launch_corr_tables(const float *Abar, int H, int m, uint4 *tab, hipStream_t s);
+// Scan variant for the fused term: normalised fp16 weights and exponents.
+hipError_t launch_state_scan_w16(const float *Abar, const float *C, const float *x0, const float2 *states,
+                                 int B, int H, int m, int chunk, int nchunk, uint32_t *w16, int *wexp,
+                                 float *x_final, hipStream_t s);
 hipError_t launch_state_correction_mfma(const float *Abar, const float2 *corr_W, int B, int H, int m,
                                         int chunk, int nchunk, int dtype, void *corr, hipStream_t s);
 

@@ -136,7 +136,7 @@ __device__ __forceinline__ uint32_t sp_pack(float lo, float hi) {
 constexpr int SPM_NA = 128;    // columns a for chunk 8192; general: chunk / 64
 
 template <int DT>
-__global__ __launch_bounds__(256) void chunk_states_mfma(const uint16_t *u, const float *Abar,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void chunk_states_mfma(const uint16_t *u, const float *Abar,
                                                          const float *Bbar, int B, int H, int L,
                                                          int m, int chunk, int wg_per_ch,
                                                          float2 *states) {
@@ -172,8 +172,11 @@ __global__ __launch_bounds__(256) void chunk_states_mfma(const uint16_t *u, cons
             Aim[ks] = make_uint4(sp_pack<DT>(pi[0], pi[1]), sp_pack<DT>(pi[2], pi[3]), sp_pack<DT>(pi[4], pi[5]), sp_pack<DT>(pi[6], pi[7]));
         }
     }
-    // E weights for the lane's outputs: modes n = 16 w + 4 kg + j, columns a = 16 ct + r16
-    float2 E[SPM_NA / 16][4];
+    // E weights for the lane's outputs: modes n = 16 w + 4 kg + j, columns
+    // a = 16 ct + r16, weight Abar_n^{chunk - 64 (a + 1)}.  Column tiles run
+    // from the last down, the weight growing by Abar_n^1024 per tile (fp32;
+    // the starting weight and the step in float64 first).
+    float2 E0[4], Z1024[4];
     float2 Bb[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -186,37 +189,45 @@ __global__ __launch_bounds__(256) void chunk_states_mfma(const uint16_t *u, cons
             Bb[j] = make_float2(Bbar[2 * i], Bbar[2 * i + 1]);
         }
         const double2 z1024 = sp_zpow(z, 1024);
-        // a descending from 16 (NCT-1) + r16: exponent chunk - 64 (a + 1) grows by 1024
-        double2 p = sp_zpow(z, chunk - 64 * (16 * (NCT - 1) + r16 + 1));
-#pragma unroll
-        for (int ct = SPM_NA / 16 - 1; ct >= 0; --ct) {
-            if (ct < NCT) {
-                E[ct][j] = make_float2((float)p.x, (float)p.y);
-                p = sp_zmul(p, z1024);
-            } else {
-                E[ct][j] = make_float2(0.f, 0.f);
-            }
-        }
+        const double2 p = sp_zpow(z, chunk - 64 * (16 * (NCT - 1) + r16 + 1));
+        E0[j] = make_float2((float)p.x, (float)p.y);
+        Z1024[j] = make_float2((float)z1024.x, (float)z1024.y);
     }
 
-    const int nelem = chunk;                    // 16-bit elements per chunk row
-    auto stage = [&](int rr, int buf) {
+    // A chunk row is chunk / 8 <= 1024 16-byte pieces: piece i = tid + 256 q,
+    // q < 4, loaded one row ahead into registers (so the loads overlap a
+    // whole row's compute) and stored into the other LDS buffer after it.
+    const int npiece = chunk / 8;
+    uint4 pf[4];
+    auto load_row = [&](int rr) {
         const int bb = rr / nchunk, cc = rr % nchunk;
         const uint16_t *src = u + ((long)bb * H + h) * L + (long)cc * chunk;
-        for (int i = tid; i < nelem / 8; i += 256) {
-            const uint4 v = *(const uint4 *)(src + 8 * i);
-            // row a = i / 8 (64 elements) padded by 8 elements to spread banks
-            *(uint4 *)&us[buf][(i >> 3) * 72 + 8 * (i & 7)] = v;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int i = tid + 256 * q;
+            pf[q] = i < npiece ? *(const uint4 *)(src + 8 * i) : make_uint4(0, 0, 0, 0);
         }
     };
-    if (r0 < r1) stage(r0, 0);
+    auto store_row = [&](int buf) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int i = tid + 256 * q;
+            // row a = i / 8 (64 elements) padded by 8 elements to spread banks
+            if (i < npiece) *(uint4 *)&us[buf][(i >> 3) * 72 + 8 * (i & 7)] = pf[q];
+        }
+    };
+    if (r0 < r1) {
+        load_row(r0);
+        store_row(0);
+    }
+    if (r0 + 1 < r1) load_row(r0 + 1);
     __syncthreads();
     for (int rr = r0; rr < r1; ++rr) {
         const int buf = (rr - r0) & 1;
-        if (rr + 1 < r1) stage(rr + 1, buf ^ 1);
         sp_f4 sre = {0.f, 0.f, 0.f, 0.f}, sim = {0.f, 0.f, 0.f, 0.f};
+        float2 E[4] = {E0[0], E0[1], E0[2], E0[3]};
 #pragma unroll
-        for (int ct = 0; ct < SPM_NA / 16; ++ct) {
+        for (int ct = SPM_NA / 16 - 1; ct >= 0; --ct) {
             if (ct < NCT) {
                 sp_f4 accr = {0.f, 0.f, 0.f, 0.f}, acci = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -229,8 +240,9 @@ __global__ __launch_bounds__(256) void chunk_states_mfma(const uint16_t *u, cons
                 // lane: rows (modes) 4 kg + j, column a = 16 ct + r16
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    sre[j] = fmaf(E[ct][j].x, accr[j], fmaf(-E[ct][j].y, acci[j], sre[j]));
-                    sim[j] = fmaf(E[ct][j].x, acci[j], fmaf(E[ct][j].y, accr[j], sim[j]));
+                    sre[j] = fmaf(E[j].x, accr[j], fmaf(-E[j].y, acci[j], sre[j]));
+                    sim[j] = fmaf(E[j].x, acci[j], fmaf(E[j].y, accr[j], sim[j]));
+                    E[j] = cmul(E[j], Z1024[j]);
                 }
             }
         }
@@ -251,6 +263,9 @@ __global__ __launch_bounds__(256) void chunk_states_mfma(const uint16_t *u, cons
                 if (n < m) states[crow * m + n] = cmul(Bb[j], make_float2(sre[j], sim[j]));
             }
         }
+        // the other buffer was last read before the previous barrier
+        if (rr + 1 < r1) store_row(buf ^ 1);
+        if (rr + 2 < r1) load_row(rr + 2);
         __syncthreads();
     }
 }
@@ -282,7 +297,7 @@ hipError_t launch_chunk_states_mfma(const void *u, const float *Abar, const floa
 // Per channel the tables E and Q (powers in float64, stored fp16) sit in LDS;
 // per chunk row W is scaled by a power of two to max |W| in [1/2, 1) before
 // rounding to fp16, and the scale is undone in fp32.  Output in the I/O dtype.
-// Workgroup (4 waves): one channel, a set of its chunk rows; wave w owns row
+// Workgroup (4 waves): one channel, a set of its chunk rows; wave w owns
 // tiles a = 16 (2w) .. 16 (2w + 1) + 15 of every chunk, all 64 columns b.
 typedef _Float16 cr_h2 __attribute__((ext_vector_type(2)));
 constexpr int CR_NA = 128;
@@ -322,11 +337,17 @@ __global__ __launch_bounds__(256) void state_correction_mfma(const float *Abar, 
         }
     }
     __syncthreads();
-    for (int rr = r0; rr < r1; ++rr) {
+    auto crow_of = [&](int rr) {
         const int bb = rr / nchunk, cc = rr % nchunk;
-        const long crow = ((long)bb * H + h) * nchunk + cc;
+        return ((long)bb * H + h) * nchunk + cc;
+    };
+    // W of the next chunk row is loaded one row ahead
+    float2 wnext = (r0 < r1 && lane < m) ? corr_W[crow_of(r0) * m + lane] : make_float2(0.f, 0.f);
+    for (int rr = r0; rr < r1; ++rr) {
+        const long crow = crow_of(rr);
         // W for this chunk row, scaled
-        float2 wv = (lane < m) ? corr_W[crow * m + lane] : make_float2(0.f, 0.f);
+        float2 wv = wnext;
+        if (rr + 1 < r1 && lane < m) wnext = corr_W[crow_of(rr + 1) * m + lane];
         float mx = fmaxf(fabsf(wv.x), fabsf(wv.y));
 #pragma unroll
         for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
@@ -364,22 +385,30 @@ __global__ __launch_bounds__(256) void state_correction_mfma(const float *Abar, 
                 Af[ks] = make_uint4(re[0], re[1], re[2], re[3]);
                 Af[2 + ks] = make_uint4(im[0], im[1], im[2], im[3]);
             }
+            // transposed product D[b][a] = sum_k Qm[k][b] Pm[a][k]: the Q tile
+            // is the A operand and the P fragment the B operand (same
+            // registers and addresses), so a lane ends up with four
+            // consecutive t and writes them as one 8-byte store
+            const float sc = ldexpf(2.0f, ew);
 #pragma unroll
             for (int bt = 0; bt < 4; ++bt) {
                 sp_f4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int ks = 0; ks < 4; ++ks) {
-                    const uint4 bv = *(const uint4 *)&Qt[16 * bt + r16][32 * ks + 8 * kg];
-                    acc = sp_mfma<F16>(Af[ks], bv, acc);
+                    const uint4 qv = *(const uint4 *)&Qt[16 * bt + r16][32 * ks + 8 * kg];
+                    acc = sp_mfma<F16>(qv, Af[ks], acc);
                 }
-                // lane: rows a = 16 at + 4 kg + j, column b = 16 bt + r16
-                const float sc = ldexpf(2.0f, ew);
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int t = 64 * (16 * at + 4 * kg + j) + 16 * bt + r16;
-                    const float v = acc[j] * sc;
-                    corr[crow * chunk + t] = (DT == BF16) ? f32_to_bf16(v) : f32_to_f16(v);
+                // lane: rows b = 16 bt + 4 kg + j, column a = 16 at + r16
+                const int t = 64 * (16 * at + r16) + 16 * bt + 4 * kg;
+                uint2 o;
+                if (DT == BF16) {
+                    o.x = (uint32_t)f32_to_bf16(acc[0] * sc) | ((uint32_t)f32_to_bf16(acc[1] * sc) << 16);
+                    o.y = (uint32_t)f32_to_bf16(acc[2] * sc) | ((uint32_t)f32_to_bf16(acc[3] * sc) << 16);
+                } else {
+                    o.x = sp_pack<F16>(acc[0] * sc, acc[1] * sc);
+                    o.y = sp_pack<F16>(acc[2] * sc, acc[3] * sc);
                 }
+                *(uint2 *)(corr + crow * chunk + t) = o;
             }
         }
         __syncthreads();   // Ws is rewritten by the next chunk row
@@ -400,6 +429,51 @@ hipError_t launch_state_correction_mfma(const float *Abar, const float2 *corr_W,
         hipLaunchKernelGGL(state_correction_mfma<BF16>, grid, block, 0, s, Abar, corr_W, B, H, m, chunk, nchunk, wg, (uint16_t *)corr);
     else
         hipLaunchKernelGGL(state_correction_mfma<F16>, grid, block, 0, s, Abar, corr_W, B, H, m, chunk, nchunk, wg, (uint16_t *)corr);
+    return hipGetLastError();
+}
+
+// ---------------------------- per-channel tables of the fused state term ---
+// For the L = 8192 conv with the initial-state term fused in (its read-out
+// computes 2 Re sum_n Abar_n^b V_n(a), t = 64 a + b, V_n(a) = W_n Abar_n^{64 a},
+// on the matrix cores), per channel, in fp16 (re, im) pairs:
+//   [0, 1024)     Abar_n^b as the A operand: uint4 (ib * 4 + kb) * 64 + 16 g + c
+//                 holds b = 16 ib + c and modes n = 16 kb + 4 g + q in dword q
+//   [1024, 1536)  Abar_n^{64 a}, a = 64 h2 + c: uint4 (h2 * 4 + kb) * 64 + 16 g + c,
+//                 modes n = 16 kb + 4 g + q in dword q
+//   [1536, 1552)  Abar_n^1024: uint4 kb * 4 + g, modes n = 16 kb + 4 g + q
+// Modes n >= m hold powers of 0 (their weights W_n are zero).  Powers in float64.
+__device__ __forceinline__ uint32_t ct_h2(double2 p) {
+    typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+    h2 v = {(_Float16)p.x, (_Float16)p.y};
+    return __builtin_bit_cast(uint32_t, v);
+}
+__global__ __launch_bounds__(256) void corr_tables_kernel(const float *Abar, int H, int m, uint4 *tab) {
+    const int h = blockIdx.x, tid = threadIdx.x, n = tid & 63, q4 = tid >> 6;
+    uint32_t *t = (uint32_t *)(tab + (long)h * CORR_TAB_U4);
+    double2 z = make_double2(0.0, 0.0);
+    if (n < m) z = make_double2(Abar[2 * ((long)h * m + n)], Abar[2 * ((long)h * m + n) + 1]);
+    const int kb = n >> 4, g = (n >> 2) & 3, q = n & 3;
+    // b = 16 q4 + i: ib = q4, c = i
+    double2 p = sp_zpow(z, 16 * q4);
+    for (int i = 0; i < 16; ++i) {
+        t[((q4 * 4 + kb) * 64 + 16 * g + i) * 4 + q] = ct_h2(p);
+        p = sp_zmul(p, z);
+    }
+    // a = 64 h2 + c with h2 = q4 >> 1, c = 8 (q4 & 1) + i
+    const int h2 = q4 >> 1;
+    const double2 z64 = sp_zpow(z, 64);
+    double2 e = sp_zpow(z64, 64 * h2 + 8 * (q4 & 1));
+    for (int i = 0; i < 8; ++i) {
+        const int c = 8 * (q4 & 1) + i;
+        t[(1024 + (h2 * 4 + kb) * 64 + 16 * g + c) * 4 + q] = ct_h2(e);
+        e = sp_zmul(e, z64);
+    }
+    if (q4 == 0) t[(1536 + kb * 4 + g) * 4 + q] = ct_h2(sp_zpow(z, 1024));
+}
+
+hipError_t launch_corr_tables(const float *Abar, int H, int m, uint4 *tab, hipStream_t s) {
+    if (m > 64) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(corr_tables_kernel, dim3(H), dim3(256), 0, s, Abar, H, m, tab);
     return hipGetLastError();
 }
 
@@ -431,6 +505,57 @@ __global__ void state_scan_kernel(const float *Abar, const float *C, const float
         x_final[2 * gid] = x.x;
         x_final[2 * gid + 1] = x.y;
     }
+}
+
+// The same scan for the fused state term: one wavefront per (batch, channel)
+// row, lane n = mode (modes n >= m idle).  For every chunk the weights
+// W_n = C_n Abar_n x^(c)_n are written normalised, W / 2^e with max |W| in
+// [1/2, 1), as fp16 (re, im) pairs, 64 per chunk row (zero beyond m), with
+// the exponent e per chunk row.
+__global__ __launch_bounds__(256) void state_scan_w16_kernel(const float *Abar, const float *C, const float *x0,
+                                                             const float2 *states, int B, int H, int m, int chunk,
+                                                             int nchunk, uint32_t *w16, int *wexp, float *x_final) {
+    const long row = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int n = threadIdx.x & 63;
+    if (row >= (long)B * H) return;   // whole wavefronts leave together
+    const int h = (int)(row % H);
+    const bool on = n < m;
+    const long i = (long)h * m + n;
+    float2 cab = make_float2(0.f, 0.f), AN = make_float2(0.f, 0.f), x = make_float2(0.f, 0.f);
+    if (on) {
+        const double ar = Abar[2 * i], ai = Abar[2 * i + 1];
+        cab = cmul(make_float2(C[2 * i], C[2 * i + 1]), make_float2((float)ar, (float)ai));
+        AN = cexp_scaled((double)chunk, 0.5 * log(ar * ar + ai * ai), atan2(ai, ar));
+        if (x0) x = make_float2(x0[2 * (row * m + n)], x0[2 * (row * m + n) + 1]);
+    }
+    for (int c = 0; c < nchunk; ++c) {
+        const float2 W = cmul(cab, x);
+        float mx = fmaxf(fabsf(W.x), fabsf(W.y));
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+        int e = 0;
+        if (mx > 0.f && mx < 3.0e38f) frexpf(mx, &e);
+        typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+        const h2 v = {(_Float16)ldexpf(W.x, -e), (_Float16)ldexpf(W.y, -e)};
+        const long rc = row * nchunk + c;
+        w16[rc * 64 + n] = __builtin_bit_cast(uint32_t, v);
+        if (n == 0) wexp[rc] = e;
+        if (on) x = cadd(cmul(AN, x), states[rc * m + n]);
+    }
+    if (x_final && on) {
+        x_final[2 * (row * m + n)] = x.x;
+        x_final[2 * (row * m + n) + 1] = x.y;
+    }
+}
+
+hipError_t launch_state_scan_w16(const float *Abar, const float *C, const float *x0, const float2 *states,
+                                 int B, int H, int m, int chunk, int nchunk, uint32_t *w16, int *wexp,
+                                 float *x_final, hipStream_t s) {
+    if (m > 64) return hipErrorInvalidValue;
+    const long rows = (long)B * H;
+    hipLaunchKernelGGL(state_scan_w16_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, Abar, C, x0,
+                       states, B, H, m, chunk, nchunk, w16, wexp, x_final);
+    return hipGetLastError();
 }
 
 hipError_t launch_chunk_states(const void *u, const float *Abar, const float *Bbar, int B, int H,
