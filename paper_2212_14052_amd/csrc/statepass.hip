@@ -448,8 +448,12 @@ __device__ __forceinline__ uint32_t ct_h2(double2 p) {
     return __builtin_bit_cast(uint32_t, v);
 }
 __global__ __launch_bounds__(256) void corr_tables_kernel(const float *Abar, int H, int m, uint4 *tab) {
+    // the channel's table is assembled in LDS, then written out in 16-byte pieces
+    __shared__ uint4 ts[CORR_TAB_U4];
     const int h = blockIdx.x, tid = threadIdx.x, n = tid & 63, q4 = tid >> 6;
-    uint32_t *t = (uint32_t *)(tab + (long)h * CORR_TAB_U4);
+    uint32_t *t = (uint32_t *)ts;
+    for (int i = tid; i < CORR_TAB_U4; i += 256) ts[i] = make_uint4(0, 0, 0, 0);   // unused tail
+    __syncthreads();
     double2 z = make_double2(0.0, 0.0);
     if (n < m) z = make_double2(Abar[2 * ((long)h * m + n)], Abar[2 * ((long)h * m + n) + 1]);
     const int kb = n >> 4, g = (n >> 2) & 3, q = n & 3;
@@ -469,6 +473,9 @@ __global__ __launch_bounds__(256) void corr_tables_kernel(const float *Abar, int
         e = sp_zmul(e, z64);
     }
     if (q4 == 0) t[(1536 + kb * 4 + g) * 4 + q] = ct_h2(sp_zpow(z, 1024));
+    __syncthreads();
+    uint4 *dst = tab + (long)h * CORR_TAB_U4;
+    for (int i = tid; i < CORR_TAB_U4; i += 256) dst[i] = ts[i];
 }
 
 hipError_t launch_corr_tables(const float *Abar, int H, int m, uint4 *tab, hipStream_t s) {
