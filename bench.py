@@ -36,17 +36,20 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0
 # 2.0 (fetch) and x 1.0 (write).  Valid only for the kernel source the
 # counters were taken on: the sha256 prefix of that source is checked at run
 # time and the figure reported as null after any change.
-TRAFFIC_SRC = "paper_2212_14052_amd/csrc/fftconv_wave.hip"
-TRAFFIC_SHA256 = "62eb06cd7940da68"
+TRAFFIC_SRC = ("paper_2212_14052_amd/csrc/fftconv_wave.hip", "paper_2212_14052_amd/csrc/wave_common.h")
+TRAFFIC_SHA256 = "0000000000000000"
 TRAFFIC_FETCH_KIB, TRAFFIC_WRITE_KIB = 15643.3, 26112.0
 FETCH_FACTOR, WRITE_FACTOR = 2.0, 1.0
 
 
 def measured_traffic():
     import hashlib
-    with open(os.path.join(ROOT, TRAFFIC_SRC), "rb") as f:
-        if hashlib.sha256(f.read()).hexdigest()[:16] != TRAFFIC_SHA256:
-            return None
+    h = hashlib.sha256()
+    for src in TRAFFIC_SRC:
+        with open(os.path.join(ROOT, src), "rb") as f:
+            h.update(f.read())
+    if h.hexdigest()[:16] != TRAFFIC_SHA256:
+        return None
     return round(TRAFFIC_FETCH_KIB * 1024 * FETCH_FACTOR + TRAFFIC_WRITE_KIB * 1024 * WRITE_FACTOR)
 
 
@@ -153,12 +156,33 @@ def _time_calls(fn, reps, warm):
     return a.elapsed_time(b) / reps
 
 
-def bench_extra(h3, dev, reps=10, warm=3):
+EXTRA_KEYS = ("cfg1_shift", "cfg2", "cfg3", "cfg4", "cfg0")
+
+
+def bench_extra(h3, dev, reps=10, warm=3, only=None):
+    """The other workloads; `only` (one of EXTRA_KEYS) restricts to one of them."""
     import numpy as np
     import torch
-    import oracle  # noqa: F401  (not used on the GPU path; kept out on purpose)
     import workloads
     ex = {}
+
+    def want(key):
+        return only is None or only == key
+
+    if want("cfg1_shift"):
+        _extra_cfg1_shift(h3, dev, reps, warm, ex, np, torch, workloads)
+    if want("cfg2"):
+        _extra_cfg2(h3, dev, reps, warm, ex, np, torch, workloads)
+    if want("cfg3"):
+        _extra_cfg3(h3, dev, reps, warm, ex, np, torch, workloads)
+    if want("cfg4"):
+        _extra_cfg4(h3, dev, reps, warm, ex, np, torch, workloads)
+    if want("cfg0"):
+        _extra_cfg0(h3, dev, reps, warm, ex, np, torch, workloads)
+    return ex
+
+
+def _extra_cfg1_shift(h3, dev, reps, warm, ex, np, torch, workloads):
     # config 1, shift-SSM kernel (k_t = C_t, t < 64): spectrum + conv
     w = workloads.config(1)
     B, H, L = w.B, w.H, w.L
@@ -173,8 +197,9 @@ def bench_extra(h3, dev, reps=10, warm=3):
     ms = _time_calls(lambda i: h3.fftconv(us[i % nsets], ks, D, out=ys[i % nsets], workspace=ws), reps, warm)
     by = B * H * L * 4 + H * L * 4 + H * 4
     ex["cfg1_shift_conv"] = {"ms": ms, "GB_s": by / ms / 1e6, "pct_hbm_peak": 100 * by / ms / 1e6 / HBM_PEAK_GBS}
-    del us, ys
 
+
+def _extra_cfg2(h3, dev, reps, warm, ex, np, torch, workloads):
     # config 2: bf16, B=16 H=256 L=8192: kernel gen + spectrum + conv
     w = workloads.config(2)
     B, H, L = w.B, w.H, w.L
@@ -191,8 +216,9 @@ def bench_extra(h3, dev, reps=10, warm=3):
     by = B * H * L * 4 + H * L * 4 + H * 4
     ex["cfg2_fused_limit_bf16"] = {"ms": ms, "GB_s": by / ms / 1e6, "pct_hbm_peak": 100 * by / ms / 1e6 / HBM_PEAK_GBS,
                                    "gelem_per_s": B * H * L / ms / 1e6}
-    del us, ys
 
+
+def _extra_cfg3(h3, dev, reps, warm, ex, np, torch, workloads):
     # config 3: state passing, B=2 H=1024 L=131072, chunk 8192, fp16
     w = workloads.config(3)
     B, H, L, m = w.B, w.H, w.L, w.m
@@ -206,8 +232,9 @@ def bench_extra(h3, dev, reps=10, warm=3):
     by = B * H * L * 4 + 3 * H * m * 8 + H * 4 + 2 * B * H * m * 8
     ex["cfg3_statepass_f16"] = {"ms": ms, "gelem_per_s": B * H * L / ms / 1e6, "GB_s": by / ms / 1e6,
                                 "pct_hbm_peak": 100 * by / ms / 1e6 / HBM_PEAK_GBS}
-    del u, y, ws
 
+
+def _extra_cfg4(h3, dev, reps, warm, ex, np, torch, workloads):
     # config 4: H3 layer forward, bf16, B=4 L=2048 d=2560
     w = workloads.config(4)
     B, L, d = w.B, w.L, w.d
@@ -223,8 +250,9 @@ def bench_extra(h3, dev, reps=10, warm=3):
     flops = 2.0 * B * L * d * d * 4
     ex["cfg4_layer_bf16"] = {"ms": ms, "gemm_TFLOP_s": flops / ms / 1e9,
                              "pct_mfma_bf16_peak": 100 * flops / ms / 1e9 / MFMA_BF16_PEAK_TFLOPS}
-    del x, W, out, ws
 
+
+def _extra_cfg0(h3, dev, reps, warm, ex, np, torch, workloads):
     # config 0: fp32, B=1 H=64 L=1024 (latency bound)
     w = workloads.config(0)
     u = _dev_tensor(w.u, w.dtype, dev)
@@ -236,7 +264,6 @@ def bench_extra(h3, dev, reps=10, warm=3):
     ms = _time_calls(lambda i: (h3.ssm_kernel(A, Bp, C, dt, w.L, out=k),
                                 h3.fftconv(u, k, D, out=y, workspace=ws)), 50, 5)
     ex["cfg0_f32_latency_us"] = ms * 1e3
-    return ex
 
 
 def cpu_baseline(w, step_bytes):
@@ -262,13 +289,15 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-extra", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--only", choices=EXTRA_KEYS, default=None,
+                    help="run only this one of the other workloads (for per-kernel profiles)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a 512 MiB device-to-device copy 5 times (calibrates the "
                          "FETCH_SIZE / WRITE_SIZE counters against a known byte count)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
-              "(the hot path shards trivially over rows, see DESIGN.md)", file=sys.stderr)
+              "(every GPU runs whole rows; a multi-GPU run would split the rows)", file=sys.stderr)
         sys.exit(2)
     import torch
     dev = torch.device("cuda:0")
@@ -286,7 +315,7 @@ def main():
     h3.lib()
     head = bench_headline(h3, args.steps, args.warmup, dev)
     print(f"# headline done: {head['ms_per_step']*1e3:.1f} us/step", file=sys.stderr, flush=True)
-    extra = {} if args.no_extra else bench_extra(h3, dev)
+    extra = {} if args.no_extra else bench_extra(h3, dev, only=args.only)
     if extra:
         print("# extra done", file=sys.stderr, flush=True)
     w = head["w"]
