@@ -70,28 +70,6 @@ def _f32(a, dev):
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
 
 
-class EventTimer:
-    """Per-stage HIP events on the current stream; durations averaged after sync."""
-
-    def __init__(self, stages):
-        import torch
-        self.stages = stages
-        self.torch = torch
-        self.ev = []
-
-    def step(self):
-        ev = [self.torch.cuda.Event(enable_timing=True) for _ in range(len(self.stages) + 1)]
-        self.ev.append(ev)
-        return ev
-
-    def averages(self):
-        out = {}
-        for i, s in enumerate(self.stages):
-            ts = [e[i].elapsed_time(e[i + 1]) for e in self.ev]
-            out[s] = sum(ts) / len(ts)
-        return out
-
-
 def bench_headline(h3, steps, warmup, dev):
     """Config 1 step: kernel generation + fused FFT conv (diagonal SSM)."""
     import torch
@@ -109,27 +87,30 @@ def bench_headline(h3, steps, warmup, dev):
     ws = torch.empty(max(256, h3.workspace_size(h3.OP_FFTCONV, B, H, L, 0, 0, h3.F16)),
                      dtype=torch.uint8, device=dev)
 
-    def one(i, ev=None):
-        if ev: ev[0].record()
+    def one(i):
         h3.ssm_kernel(A, Bp, C, dt, L, out=k)
-        if ev: ev[1].record()
         h3.fftconv(us[i % nsets], k, D, out=ys[i % nsets], workspace=ws)
-        if ev: ev[2].record()
 
     for i in range(warmup):
         one(i)
     torch.cuda.synchronize()
-    timer = EventTimer(["ssm_kernel", "fftconv"])
+    # Timed region: K back-to-back steps bracketed by two events (no per-step
+    # host work beyond the two library calls, so the GPU never waits on Python).
     t0 = torch.cuda.Event(enable_timing=True); t1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
     t0.record()
     for i in range(steps):
-        one(i, timer.step())
+        one(i)
     t1.record()
     torch.cuda.synchronize()
-    total_ms = t0.elapsed_time(t1)
-    per = timer.averages()
-    ms = total_ms / steps
+    ms = t0.elapsed_time(t1) / steps
+    # Per-launch duration of each kernel of the step, each timed over K
+    # back-to-back launches on the stream the library runs on (torch's current
+    # stream, passed to the library by the binding).
+    per = {
+        "ssm_kernel": _time_calls(lambda i: h3.ssm_kernel(A, Bp, C, dt, L, out=k), steps, 3),
+        "fftconv": _time_calls(lambda i: h3.fftconv(us[i % nsets], k, D, out=ys[i % nsets], workspace=ws),
+                               steps, 3),
+    }
     # u + y (fp16) + k (fp32, once per channel) + D
     step_bytes = B * H * L * (2 + 2) + H * L * 4 + H * 4
     conv_bytes = step_bytes
@@ -266,20 +247,27 @@ def _extra_cfg0(h3, dev, reps, warm, ex, np, torch, workloads):
     ex["cfg0_f32_latency_us"] = ms * 1e3
 
 
-def cpu_baseline(w, step_bytes):
-    """The float64 oracle on the whole config-1 workload: kernel generation for
-    every channel, then the direct causal convolution of every row."""
+def cpu_baseline(w, step_bytes, min_seconds=10.0, max_reps=64):
+    """The float64 oracle on the whole config-1 workload (kernel generation for
+    every channel, then the direct causal convolution of every row), repeated
+    until at least `min_seconds` of wall time have passed."""
     import numpy as np
     import oracle
     A, B, C, dt = w.ssm.complex64()
+    D = w.D.astype(np.float64)
+    reps = 0
     t = time.time()
-    k = oracle.ssm_kernel(A, B, C, dt, w.L)
-    oracle.causal_conv(w.u64, k, w.D.astype(np.float64))
+    while reps < max_reps:
+        k = oracle.ssm_kernel(A, B, C, dt, w.L)
+        oracle.causal_conv(w.u64, k, D)
+        reps += 1
+        if time.time() - t >= min_seconds:
+            break
     el = time.time() - t
-    return {"value": step_bytes / el / 1e9, "unit": "GB/s", "cores": oracle.num_threads(),
+    return {"value": reps * step_bytes / el / 1e9, "unit": "GB/s", "cores": oracle.num_threads(),
             "kind": "oracle",
-            "sample": f"whole config-1 workload (B={w.B} H={w.H} L={w.L}): float64 kernel generation "
-                      f"+ direct O(L^2) causal conv, {el:.2f} s wall"}
+            "sample": f"whole config-1 workload (B={w.B} H={w.H} L={w.L}) x {reps}: float64 kernel "
+                      f"generation + direct O(L^2) causal conv, {el:.2f} s wall"}
 
 
 def main():

@@ -137,15 +137,25 @@ __global__ __launch_bounds__(KG_THREADS) void kernel_gen(int mode, const float *
 // ------------------------------------------------------ matrix-core form ---
 // k[64 a + b] = 2 sum_n (Re P[a][n] Re Q[n][b] - Im P[a][n] Im Q[n][b]) is a real
 // matrix product with reduction length 2m (m <= 64, zero-padded to 128):
-//   Pm[a][k] = Re P[a][k] (k < 64), -Im P[a][k-64] (k >= 64)
-//   Qm[k][b] = Re Q[k][b] (k < 64),  Im Q[k-64][b] (k >= 64)
+//   Pm[a][j] = Re P[a][j] (j < 64), -Im P[a][j-64] (j >= 64)
+//   Qm[j][b] = Re Q[j][b] (j < 64),  Im Q[j-64][b] (j >= 64)
 // with P[a][n] = W_n z_n^{64 a}, Q[n][b] = z_n^b, z_n = exp(lambda_n), run as
 // 16x16x4 fp32 MFMAs (exact fp32 products, fp32 accumulation).  A workgroup (4
-// waves) produces rows a = a0 .. a0+15 (1024 outputs); wave w owns columns
+// waves) produces rows a = a0 .. a0+31 (2048 outputs); wave w owns columns
 // b = 16 w .. 16 w + 15.  The powers z^e are formed in float64 by repeated
 // squaring and multiplication (relative error ~ e * 1e-16), so no phase is
 // ever reduced in float32.
+//
+// Every wave derives z_n and W_n for mode n = lane itself (the global loads are
+// issued first, the three float64 transcendentals of the ZOH run on three
+// waves in parallel), so the power tables are built straight from registers:
+// one barrier before the tables are complete, none around the mode setup
+// beyond the exchange of the transcendentals.
+//
+// The reduction index is permuted so that MFMA step s of lane (r, q) uses
+// j = 32 q + s: four consecutive steps read one 16-byte LDS word.
 constexpr int KM_ROWS = 32;
+constexpr int KM_LD = 128 + 4;   // LDS row pitch in floats
 typedef float f4v_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ double2 zmul(double2 a, double2 b) {
@@ -161,107 +171,99 @@ __device__ __forceinline__ double2 zpow(double2 z, int e) {
     return r;
 }
 
+// mode 0: continuous (A, B, dt), ZOH.  mode 1: discrete (Abar, Bbar), W = C Bbar.
+// mode 2: discrete Abar of channel (orow / div) % H, W given per output row in P1.
 __global__ __launch_bounds__(256) void kernel_gen_mfma(int mode, const float *P0, const float *P1,
                                                        const float *C, const float *dt, int H,
                                                        int m, int L, float *k, int div) {
-    __shared__ double2 z_s[H3_MAX_MODES_DEV];
-    __shared__ float2 W_s[H3_MAX_MODES_DEV];
-    __shared__ float Qt[64][128 + 4];        // [b][k]  (Qm transposed)
-    __shared__ float Pm[KM_ROWS][128 + 4];   // [a][k]
+    __shared__ double pre[3][H3_MAX_MODES_DEV];
+    __shared__ float Qt[64][KM_LD];          // [b][j]  (Qm transposed)
+    __shared__ float Pm[KM_ROWS][KM_LD];     // [a][j]
     const int nrt = (L / 64 + KM_ROWS - 1) / KM_ROWS;  // row tiles per output row
     const int orow = blockIdx.x / nrt;
     const int a0 = (blockIdx.x % nrt) * KM_ROWS;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    if (mode == 0) {
-        // ZOH from (A, B, dt): the three float64 transcendentals of each mode
-        // run on three waves in parallel, then one wave combines them.
-        __shared__ double pre[3][H3_MAX_MODES_DEV];
-        const int n = tid & 63, part = tid >> 6;
-        if (n < m && part < 3) {
-            const long i = (long)orow * m + n;
-            const double d = dt[orow];
-            const double lr = d * P0[2 * i], li = d * P0[2 * i + 1];
-            pre[part][n] = part == 0 ? expm1(lr) : part == 1 ? cos(li) : sin(li);
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int n = lane;
+    const bool act = n < m;
+    const int h = (mode == 2) ? (orow / div) % H : orow;
+    // ---- loads first (every wave, lane n = mode n)
+    double ar = 0.0, ai = 0.0, pr = 0.0, pi = 0.0, cr = 0.0, ci = 0.0, d = 0.0;
+    if (act) {
+        const long i = (long)h * m + n;
+        const float2 a2 = *(const float2 *)(P0 + 2 * i);
+        ar = a2.x; ai = a2.y;
+        const long pi_ = (mode == 2) ? (long)orow * m + n : i;
+        const float2 p2 = *(const float2 *)(P1 + 2 * pi_);
+        pr = p2.x; pi = p2.y;
+        if (mode != 2) {
+            const float2 c2 = *(const float2 *)(C + 2 * i);
+            cr = c2.x; ci = c2.y;
         }
-        __syncthreads();
-        if (tid < H3_MAX_MODES_DEV) {
-            double2 z = make_double2(0.0, 0.0);
-            float2 Wn = make_float2(0.f, 0.f);
-            if (tid < m) {
-                const long i = (long)orow * m + tid;
-                const double em1 = pre[0][tid], cs = pre[1][tid], sn = pre[2][tid];
-                const double e = em1 + 1.0;
-                z = make_double2(e * cs, e * sn);
-                // exp(lambda) - 1 = (e cos - 1) + i e sin, with e cos - 1 = em1 cos + (cos - 1)
-                const double em1r = em1 * cs + (cs - 1.0), em1i = e * sn;
-                const double ar = P0[2 * i], ai = P0[2 * i + 1];
-                const double den = ar * ar + ai * ai;
-                const double qr = (em1r * ar + em1i * ai) / den, qi = (em1i * ar - em1r * ai) / den;
-                const double bre = P1[2 * i], bim = P1[2 * i + 1];
-                const double br = qr * bre - qi * bim, bi = qr * bim + qi * bre;
-                const double cr = C[2 * i], ci = C[2 * i + 1];
-                Wn = make_float2((float)(cr * br - ci * bi), (float)(cr * bi + ci * br));
-            }
-            z_s[tid] = z;
-            W_s[tid] = Wn;
-        }
-    } else if (tid < H3_MAX_MODES_DEV) {
-        double2 z = make_double2(0.0, 0.0);
-        float2 Wn = make_float2(0.f, 0.f);
-        if (tid < m) {
-            const int h = (mode == 1) ? orow : (orow / div) % H;
-            const long i = (long)h * m + tid;
-            z = make_double2(P0[2 * i], P0[2 * i + 1]);
-            if (mode == 1) {
-                const double cr = C[2 * i], ci = C[2 * i + 1], br = P1[2 * i], bi = P1[2 * i + 1];
-                Wn = make_float2((float)(cr * br - ci * bi), (float)(cr * bi + ci * br));
-            } else {
-                const long wi = (long)orow * m + tid;
-                Wn = make_float2(P1[2 * wi], P1[2 * wi + 1]);
-            }
-        }
-        z_s[tid] = z;
-        W_s[tid] = Wn;
+        if (mode == 0) d = dt[h];
     }
-    __syncthreads();
-    {
-        // Q: thread -> (n = tid % 64, b = 16 (tid / 64) .. + 15); lanes vary n
-        {
-            const int n = tid & 63, b0 = 16 * (tid >> 6);
-            const double2 z = z_s[n];
-            double2 p = zpow(z, b0);
-#pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                Qt[b0 + j][n] = (float)p.x;
-                Qt[b0 + j][64 + n] = (float)p.y;
-                p = zmul(p, z);
-            }
+    // ---- z_n = exp(lambda_n) and W_n, in every wave
+    double2 z = make_double2(0.0, 0.0);
+    float2 Wn = make_float2(0.f, 0.f);
+    if (mode == 0) {
+        const double lr = d * ar, li = d * ai;
+        if (w < 3 && act) pre[w][n] = w == 0 ? expm1(lr) : w == 1 ? cos(li) : sin(li);
+        __syncthreads();
+        if (act) {
+            const double em1 = pre[0][n], cs = pre[1][n], sn = pre[2][n];
+            const double e = em1 + 1.0;
+            z = make_double2(e * cs, e * sn);
+            // exp(lambda) - 1 = (e cos - 1) + i e sin, with e cos - 1 = em1 cos + (cos - 1)
+            const double em1r = em1 * cs + (cs - 1.0), em1i = e * sn;
+            const double den = ar * ar + ai * ai;
+            const double qr = (em1r * ar + em1i * ai) / den, qi = (em1i * ar - em1r * ai) / den;
+            const double br = qr * pr - qi * pi, bi = qr * pi + qi * pr;   // Bbar = (e^lambda - 1)/A * B
+            Wn = make_float2((float)(cr * br - ci * bi), (float)(cr * bi + ci * br));
         }
-        // P: thread -> (n = tid / 4, rows 8 (tid % 4) .. + 7)
-        const int n = tid >> 2;
-        const double2 z = z_s[n];
+    } else if (act) {
+        z = make_double2(ar, ai);
+        if (mode == 1)
+            Wn = make_float2((float)(cr * pr - ci * pi), (float)(cr * pi + ci * pr));
+        else
+            Wn = make_float2((float)pr, (float)pi);
+    }
+    // ---- Q rows b = 16 w .. 16 w + 15 and P rows 8 w .. 8 w + 7 of mode n
+    {
+        double2 p = zpow(z, 16 * w);
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            Qt[16 * w + j][n] = (float)p.x;
+            Qt[16 * w + j][64 + n] = (float)p.y;
+            p = zmul(p, z);
+        }
         const double2 z64 = zpow(z, 64);
-        const int ar0 = 8 * (tid & 3);
-        double2 q = zpow(z64, a0 + ar0);
-        const float2 Wn = W_s[n];
+        double2 q = zpow(z64, a0 + 8 * w);
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             const float qr = (float)q.x, qi = (float)q.y;
-            Pm[ar0 + j][n] = Wn.x * qr - Wn.y * qi;
-            Pm[ar0 + j][64 + n] = -(Wn.x * qi + Wn.y * qr);
+            Pm[8 * w + j][n] = Wn.x * qr - Wn.y * qi;
+            Pm[8 * w + j][64 + n] = -(Wn.x * qi + Wn.y * qr);
             q = zmul(q, z64);
         }
     }
     __syncthreads();
     // wave w: two 16 x 16 tiles (rows a0 .. a0+15 and a0+16 .. a0+31) of
-    // columns 16 w .. 16 w + 15, reduction over k = 0..127 in steps of 4
+    // columns 16 w .. 16 w + 15; lane (r, q) at step s uses reduction index 32 q + s
     f4v_t acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
     const int r = lane & 15, kq = lane >> 4;
-#pragma unroll 8
-    for (int k0 = 0; k0 < 128; k0 += 4) {
-        const float bv = Qt[16 * w + r][k0 + kq];
-        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(Pm[r][k0 + kq], bv, acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(Pm[16 + r][k0 + kq], bv, acc1, 0, 0, 0);
+#pragma unroll
+    for (int s4 = 0; s4 < 32; s4 += 4) {
+        const float4 bv = *(const float4 *)&Qt[16 * w + r][32 * kq + s4];
+        const float4 p0 = *(const float4 *)&Pm[r][32 * kq + s4];
+        const float4 p1 = *(const float4 *)&Pm[16 + r][32 * kq + s4];
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(p0.x, bv.x, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(p1.x, bv.x, acc1, 0, 0, 0);
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(p0.y, bv.y, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(p1.y, bv.y, acc1, 0, 0, 0);
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(p0.z, bv.z, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(p1.z, bv.z, acc1, 0, 0, 0);
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(p0.w, bv.w, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(p1.w, bv.w, acc1, 0, 0, 0);
     }
     // lane holds rows a0 + 4 kq + j (+16), column 16 w + r
 #pragma unroll
