@@ -264,13 +264,26 @@ int h3_layer_fwd(const void *x, const void *Wq, const void *Wk, const void *Wv, 
     // [Q;K;V] (channel-major) = Wt_qkv . x^T
     if ((e = launch_gemm_nt(wt_qkv, x, qkv, 3 * d, B * L, d, dtype, 1, d, L, s)) != hipSuccess)
         return H3_EDEVICE;
-    if ((e = launch_spectrum(diag_k, d, L, Kspec, s)) != hipSuccess) return H3_EDEVICE;
     const char *q = qkv, *kk = qkv + act, *v = qkv + 2 * act;
-    if ((e = launch_layer_mid(q, kk, v, shift_C, shift_D, m_s, Kspec, diag_D, B, d, L, dtype, o_cm,
-                              s)) != hipSuccess)
-        return H3_EDEVICE;
-    // O (B, d, L) -> (B, L, d), then out = O . Wo
-    if ((e = launch_transpose_batched(o_cm, o_tm, B, d, L, s)) != hipSuccess) return H3_EDEVICE;
+    if (fftconv_mfma_supported(L, dtype) && L % 64 == 0) {
+        // G = (shift SSM of K) * V  ->  o_cm;  S = diag conv of G (+ D G)  ->  K's slot (K is dead);
+        // O (B, L, d) = (Q * S)^T  ->  o_tm
+        if ((e = launch_shift_gate(kk, v, shift_C, shift_D, m_s, B, d, L, dtype, o_cm, s)) != hipSuccess)
+            return H3_EDEVICE;
+        ConvArgs ca{};
+        ca.u = o_cm; ca.y = (void *)kk; ca.D = diag_D;
+        ca.B = B; ca.H = d; ca.L = L; ca.nchunk = 1; ca.pair_mode = 0; ca.dtype = dtype;
+        if ((e = launch_fftconv_mfma(ca, diag_k, s)) != hipSuccess) return H3_EDEVICE;
+        if ((e = launch_gate_transpose(q, kk, o_tm, B, d, L, dtype, s)) != hipSuccess) return H3_EDEVICE;
+    } else {
+        if ((e = launch_spectrum(diag_k, d, L, Kspec, s)) != hipSuccess) return H3_EDEVICE;
+        if ((e = launch_layer_mid(q, kk, v, shift_C, shift_D, m_s, Kspec, diag_D, B, d, L, dtype, o_cm,
+                                  s)) != hipSuccess)
+            return H3_EDEVICE;
+        // O (B, d, L) -> (B, L, d)
+        if ((e = launch_transpose_batched(o_cm, o_tm, B, d, L, s)) != hipSuccess) return H3_EDEVICE;
+    }
+    // out = O . Wo
     return launched(launch_gemm_nt(o_tm, wt_o, out, B * L, d, d, dtype, 0, d, L, s));
 }
 

@@ -83,6 +83,12 @@ hipError_t launch_state_correction_mfma(const float *Abar, const float2 *corr_W,
 // Layer pieces.
 hipError_t launch_transpose_w(const void *W, int d, int dtype, void *Wt, hipStream_t s);
 hipError_t launch_transpose_batched(const void *in, void *out, int nb, int R, int C, hipStream_t s);
+// O (B, L, d) token-major = (Q * S)^T per batch slice, Q and S (B, d, L); R = d, C = L.
+hipError_t launch_gate_transpose(const void *q, const void *sv, void *out, int nb, int R, int C, int dtype,
+                                 hipStream_t s);
+// G = (shift FIR of K + shift_D K) * V over (B, d, L) rows (m_s <= 64, L % 16 == 0).
+hipError_t launch_shift_gate(const void *k, const void *v, const float *shift_C, const float *shift_D, int m_s,
+                             int B, int d, int L, int dtype, void *g, hipStream_t s);
 hipError_t launch_gemm_nt(const void *A, const void *Bt, void *C, int M, int N, int K, int dtype,
                           int out_mode, int d, int L, hipStream_t s);
 hipError_t launch_layer_mid(const void *q, const void *k, const void *v, const float *shift_C,

@@ -233,6 +233,165 @@ __global__ __launch_bounds__(256) void transpose16_kernel(const uint16_t *in, ui
     }
 }
 
+// ------------------------------------------- transposes, 16-byte accesses ---
+// out (C, R) = in (R, C)^T per batch slice (GATE = 0), or the gated transpose
+// out (C, R) = (in * in2)^T with the product rounded once (GATE = 1).  A 64 x 64
+// tile per workgroup; every global access moves 8 consecutive 16-bit values.
+// Requires R % 8 == 0 and C % 8 == 0 (the callers' shapes are multiples of 64).
+template <int DT, int GATE>
+__global__ __launch_bounds__(256) void transpose_tile_kernel(const uint16_t *in, const uint16_t *in2,
+                                                             uint16_t *out, int R, int Cc) {
+    __shared__ uint16_t tile[64][64 + 8];   // [c][r]: stored transposed
+    const int tr = (R + 63) / 64, tc = (Cc + 63) / 64;
+    const int b = blockIdx.x / (tr * tc), rem = blockIdx.x % (tr * tc);
+    const int r0 = (rem / tc) * 64, c0 = (rem % tc) * 64;
+    const long off = (long)b * R * Cc;
+    const int t = threadIdx.x;
+    // read: thread -> (row r0 + t / 8 + 32 h, columns c0 + 8 (t % 8) .. + 7)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int i = t / 8 + 32 * h, cj = 8 * (t % 8);
+        const int r = r0 + i, c = c0 + cj;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (r < R && c < Cc) {
+            v = *(const uint4 *)(in + off + (long)r * Cc + c);
+            if (GATE) {
+                const uint4 g = *(const uint4 *)(in2 + off + (long)r * Cc + c);
+                const uint32_t a4[4] = {v.x, v.y, v.z, v.w}, g4[4] = {g.x, g.y, g.z, g.w};
+                uint32_t o4[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float lo = (DT == BF16 ? bf16_to_f32(a4[e] & 0xffffu) : f16_to_f32(a4[e] & 0xffffu)) *
+                                     (DT == BF16 ? bf16_to_f32(g4[e] & 0xffffu) : f16_to_f32(g4[e] & 0xffffu));
+                    const float hi = (DT == BF16 ? bf16_to_f32(a4[e] >> 16) : f16_to_f32(a4[e] >> 16)) *
+                                     (DT == BF16 ? bf16_to_f32(g4[e] >> 16) : f16_to_f32(g4[e] >> 16));
+                    const uint32_t l16 = DT == BF16 ? f32_to_bf16(lo) : f32_to_f16(lo);
+                    const uint32_t h16 = DT == BF16 ? f32_to_bf16(hi) : f32_to_f16(hi);
+                    o4[e] = l16 | (h16 << 16);
+                }
+                v = make_uint4(o4[0], o4[1], o4[2], o4[3]);
+            }
+        }
+        const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            tile[cj + 2 * e][i] = (uint16_t)(w4[e] & 0xffffu);
+            tile[cj + 2 * e + 1][i] = (uint16_t)(w4[e] >> 16);
+        }
+    }
+    __syncthreads();
+    // write: thread -> (column c0 + t / 8 + 32 h, rows r0 + 8 (t % 8) .. + 7)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int i = t / 8 + 32 * h, rj = 8 * (t % 8);
+        const int c = c0 + i, r = r0 + rj;
+        if (c < Cc && r < R) *(uint4 *)(out + off + (long)c * R + r) = *(const uint4 *)&tile[i][rj];
+    }
+}
+
+// ------------------------------------------------- shift SSM and gating ----
+// G[b, c, t] = (sum_{j < m_s} shift_C[c, j] K[b, c, t - j] + shift_D[c] K[b, c, t]) V[b, c, t]
+// (Sec. 3.2: the shift SSM's kernel is its taps, Algorithm 1 then gates with V),
+// on (B, d, L) rows, fp32 arithmetic, one rounding to the I/O dtype.  One
+// workgroup of 128 threads per row tile of 2048 outputs; thread -> 16
+// consecutive outputs.  The taps are wave-uniform (scalar registers); the
+// thread's window K[t0 - 63 .. t0 + 15] comes from the row staged in LDS.
+constexpr int SG_T = 128, SG_R = 16, SG_TILE = SG_T * SG_R;
+template <int DT>
+__global__ __launch_bounds__(SG_T) void shift_gate_kernel(const uint16_t *k, const uint16_t *v,
+                                                          const float *shift_C, const float *shift_D,
+                                                          int m_s, int d, int L, uint16_t *g) {
+    __shared__ __attribute__((aligned(16))) float ks[64 + SG_TILE];   // K[t_tile - 64 .. t_tile + SG_TILE - 1]
+    __shared__ __attribute__((aligned(16))) float taps_s[64];
+    const int ntile = (L + SG_TILE - 1) / SG_TILE;
+    const long row = blockIdx.x / ntile;
+    const int tt = (blockIdx.x % ntile) * SG_TILE;
+    const int c = (int)(row % d);
+    const uint16_t *kr = k + row * L;
+    // every global load first, unconditional and in straight-line code
+    // (addresses clamped into the row), so one memory round trip serves the
+    // workgroup: this thread's V values, then its share of the K window
+    const int t0 = SG_R * threadIdx.x;   // within the tile
+    const bool act = tt + t0 < L;
+    const long o = row * L + min(tt + t0, L - SG_R);
+    uint4 vpre[SG_R / 8];
+#pragma unroll
+    for (int h = 0; h < SG_R / 8; ++h) vpre[h] = *(const uint4 *)(v + o + 8 * h);
+    constexpr int NKS = (64 + SG_TILE) / 8;   // 16-byte pieces of the window
+    constexpr int PER = (NKS + SG_T - 1) / SG_T;
+    uint4 kw[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+        const int t = tt - 64 + 8 * (threadIdx.x + u * SG_T);
+        kw[u] = *(const uint4 *)(kr + min(max(t, 0), L - 8));   // zeroed below where out of the row
+    }
+    const float tapv = threadIdx.x < 64 ? shift_C[(long)c * m_s + min((int)threadIdx.x, m_s - 1)] : 0.f;
+    const float ds = shift_D ? shift_D[c] : 0.f;
+    if (threadIdx.x < 64) taps_s[threadIdx.x] = (int)threadIdx.x < m_s ? tapv : 0.f;
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+        const int i = threadIdx.x + u * SG_T;
+        const int t = tt - 64 + 8 * i;
+        if (i < NKS) {
+            const bool in = t >= 0 && t + 8 <= L;   // before the row start: causal zeros
+            const uint32_t w4[4] = {kw[u].x, kw[u].y, kw[u].z, kw[u].w};
+            float f[8];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                f[2 * e] = in ? (DT == BF16 ? bf16_to_f32(w4[e] & 0xffffu) : f16_to_f32(w4[e] & 0xffffu)) : 0.f;
+                f[2 * e + 1] = in ? (DT == BF16 ? bf16_to_f32(w4[e] >> 16) : f16_to_f32(w4[e] >> 16)) : 0.f;
+            }
+            *(float4 *)&ks[8 * i] = make_float4(f[0], f[1], f[2], f[3]);
+            *(float4 *)&ks[8 * i + 4] = make_float4(f[4], f[5], f[6], f[7]);
+        }
+    }
+    __syncthreads();
+    if (!act) return;
+    float win[SG_R + 64];   // K[t0 - 64 .. t0 + 15]
+#pragma unroll
+    for (int i = 0; i < (SG_R + 64) / 4; ++i) {
+        const float4 q = *(const float4 *)&ks[t0 + 4 * i];
+        win[4 * i] = q.x; win[4 * i + 1] = q.y; win[4 * i + 2] = q.z; win[4 * i + 3] = q.w;
+    }
+    float acc[SG_R];
+#pragma unroll
+    for (int r = 0; r < SG_R; ++r) acc[r] = ds * win[64 + r];
+    // taps 16 at a time (broadcast LDS reads), one tap across the 16 accumulators per group
+#pragma unroll
+    for (int jq = 0; jq < 64; jq += 16) {
+        float tq[16];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float4 q = *(const float4 *)&taps_s[jq + 4 * i];
+            tq[4 * i] = q.x; tq[4 * i + 1] = q.y; tq[4 * i + 2] = q.z; tq[4 * i + 3] = q.w;
+        }
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+#pragma unroll
+            for (int r = 0; r < SG_R; ++r) acc[r] = fmaf(tq[j], win[64 + r - jq - j], acc[r]);
+            // keep the order tap-major: 16 independent FMAs between two uses
+            // of an accumulator (the scheduler would otherwise run the 64
+            // taps of one output as one dependent chain)
+            asm volatile("" : "+v"(acc[0]), "+v"(acc[1]), "+v"(acc[2]), "+v"(acc[3]), "+v"(acc[4]), "+v"(acc[5]),
+                         "+v"(acc[6]), "+v"(acc[7]), "+v"(acc[8]), "+v"(acc[9]), "+v"(acc[10]), "+v"(acc[11]),
+                         "+v"(acc[12]), "+v"(acc[13]), "+v"(acc[14]), "+v"(acc[15]));
+        }
+    }
+#pragma unroll
+    for (int h = 0; h < SG_R / 8; ++h) {
+        const uint32_t v4[4] = {vpre[h].x, vpre[h].y, vpre[h].z, vpre[h].w};
+        uint32_t o4[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float lo = acc[8 * h + 2 * e] * (DT == BF16 ? bf16_to_f32(v4[e] & 0xffffu) : f16_to_f32(v4[e] & 0xffffu));
+            const float hi = acc[8 * h + 2 * e + 1] * (DT == BF16 ? bf16_to_f32(v4[e] >> 16) : f16_to_f32(v4[e] >> 16));
+            o4[e] = (uint32_t)(DT == BF16 ? f32_to_bf16(lo) : f32_to_f16(lo)) |
+                    ((uint32_t)(DT == BF16 ? f32_to_bf16(hi) : f32_to_f16(hi)) << 16);
+        }
+        *(uint4 *)(g + o + 8 * h) = make_uint4(o4[0], o4[1], o4[2], o4[3]);
+    }
+}
+
 // ------------------------------------------------------- fused middle ------
 // Per pair of rows (batches 2j, 2j+1) of channel c, all (B, d, L):
 //   G = (sum_{j<m_s} shift_C[c,j] K_{t-j} + shift_D[c] K_t) * V_t
@@ -328,16 +487,44 @@ __global__ __launch_bounds__(N / 16 >= 64 ? N / 16 : 64) void layer_mid_kernel(
 // --------------------------------------------------------------- launch ----
 hipError_t launch_transpose_w(const void *W, int d, int dtype, void *Wt, hipStream_t s) {
     (void)dtype;
-    const int tiles = ((d + 63) / 64) * ((d + 63) / 64);
-    hipLaunchKernelGGL(transpose16_kernel, dim3(tiles), dim3(256), 0, s, (const uint16_t *)W,
-                       (uint16_t *)Wt, d, d);
-    return hipGetLastError();
+    return launch_transpose_batched(W, Wt, 1, d, d, s);
 }
 
 hipError_t launch_transpose_batched(const void *in, void *out, int nb, int R, int C, hipStream_t s) {
     const int tiles = ((R + 63) / 64) * ((C + 63) / 64);
-    hipLaunchKernelGGL(transpose16_kernel, dim3(nb * tiles), dim3(256), 0, s, (const uint16_t *)in,
-                       (uint16_t *)out, R, C);
+    if (R % 8 == 0 && C % 8 == 0)
+        hipLaunchKernelGGL((transpose_tile_kernel<F16, 0>), dim3(nb * tiles), dim3(256), 0, s,
+                           (const uint16_t *)in, (const uint16_t *)nullptr, (uint16_t *)out, R, C);
+    else
+        hipLaunchKernelGGL(transpose16_kernel, dim3(nb * tiles), dim3(256), 0, s, (const uint16_t *)in,
+                           (uint16_t *)out, R, C);
+    return hipGetLastError();
+}
+
+hipError_t launch_gate_transpose(const void *q, const void *sv, void *out, int nb, int R, int C, int dtype,
+                                 hipStream_t s) {
+    if (R % 8 != 0 || C % 8 != 0) return hipErrorInvalidValue;
+    const int tiles = ((R + 63) / 64) * ((C + 63) / 64);
+    if (dtype == BF16)
+        hipLaunchKernelGGL((transpose_tile_kernel<BF16, 1>), dim3(nb * tiles), dim3(256), 0, s,
+                           (const uint16_t *)q, (const uint16_t *)sv, (uint16_t *)out, R, C);
+    else
+        hipLaunchKernelGGL((transpose_tile_kernel<F16, 1>), dim3(nb * tiles), dim3(256), 0, s,
+                           (const uint16_t *)q, (const uint16_t *)sv, (uint16_t *)out, R, C);
+    return hipGetLastError();
+}
+
+hipError_t launch_shift_gate(const void *k, const void *v, const float *shift_C, const float *shift_D, int m_s,
+                             int B, int d, int L, int dtype, void *g, hipStream_t s) {
+    if (m_s > 64 || L % 16 != 0) return hipErrorInvalidValue;
+    const long rows = (long)B * d;
+    const long grid = rows * ((L + SG_TILE - 1) / SG_TILE);
+    if (dtype == BF16)
+        hipLaunchKernelGGL(shift_gate_kernel<BF16>, dim3((unsigned)grid), dim3(SG_T), 0, s, (const uint16_t *)k,
+                           (const uint16_t *)v, shift_C, shift_D, m_s, d, L, (uint16_t *)g);
+    else
+        hipLaunchKernelGGL(shift_gate_kernel<F16>, dim3((unsigned)grid), dim3(SG_T), 0, s, (const uint16_t *)k,
+                           (const uint16_t *)v, shift_C, shift_D, m_s, d, L, (uint16_t *)g);
     return hipGetLastError();
 }
 
