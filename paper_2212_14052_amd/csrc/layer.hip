@@ -15,6 +15,7 @@ namespace h3 {
 typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f4_t __attribute__((ext_vector_type(4)));
 
 template <int DT> struct Mfma;
 template <> struct Mfma<F16> {
@@ -392,6 +393,108 @@ __global__ __launch_bounds__(SG_T) void shift_gate_kernel(const uint16_t *k, con
     }
 }
 
+// Matrix-core form of the same shift SSM and gating (L % 1024 == 0).  The
+// 64-tap filter over 64-sample blocks is a banded Toeplitz product: with
+// t = 64 a + r,
+//   Kbar[64 a + r] = sum_{s < 128} T[r][s] K[64 (a - 1) + s],
+//   T[r][s] = shift_C[r + 64 - s] for 0 <= r + 64 - s < 64 (+ shift_D on s = r + 64),
+// so per row: a (64 x 128) . (128 x L/64) product on 16x16x32 MFMAs (fp32
+// accumulation; the taps rounded to the I/O dtype).  T's band touches three of
+// the four 32-wide reduction chunks of every 16-row block.  One wave per (b, c)
+// row; the lane's MFMA result is four consecutive t of one block a, gated by V
+// and stored as one 8-byte piece.
+template <int DT>
+__device__ __forceinline__ f4_t sg_mfma(uint4 a, uint4 b, f4_t c) {
+    if constexpr (DT == BF16)
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8_t, a), __builtin_bit_cast(half8_t, b), c, 0, 0, 0);
+}
+template <int DT>
+__device__ __forceinline__ uint32_t sg_pack(float lo, float hi) {
+    return (uint32_t)(DT == BF16 ? f32_to_bf16(lo) : f32_to_f16(lo)) |
+           ((uint32_t)(DT == BF16 ? f32_to_bf16(hi) : f32_to_f16(hi)) << 16);
+}
+template <int DT>
+__device__ __forceinline__ float sg_f(uint32_t h16) {
+    return DT == BF16 ? bf16_to_f32(h16) : f16_to_f32(h16);
+}
+constexpr int SGM_W = 4;   // waves (channels) per workgroup
+template <int DT>
+__global__ __launch_bounds__(64 * SGM_W) void shift_gate_mfma_kernel(const uint16_t *k, const uint16_t *v,
+                                                                      const float *shift_C, const float *shift_D,
+                                                                      int m_s, int B, int d, int L, uint16_t *g) {
+    __shared__ float taps[SGM_W][64 + 1];   // taps[w][j] = shift_C[c, j], [64] = shift_D[c]
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int c = blockIdx.x * SGM_W + w;   // this wave's channel: rows b d + c, b < B
+    if (c >= d) return;                      // no barrier below: a spare wave may leave
+    const int col = lane & 15, kg = lane >> 4;
+    const int nab = L / 1024;                // 16-column blocks of 64-sample columns per row
+    const int nit = B * nab;
+    // loads of item it = (row b, column block ab): B fragments (chunk kc,
+    // column a = 16 ab + col: K[64 (a - 1) + 32 kc + 8 kg .. + 7], zeros before
+    // the row start) and V at the lane's outputs t = 64 a + 16 rb + 4 kg .. + 3
+    uint4 Bf[4];
+    uint2 Vq[4];
+    auto issue = [&](int it) {
+        const long ro = ((long)(it / nab) * d + c) * L;
+        const int a = 16 * (it % nab) + col;
+#pragma unroll
+        for (int kc = 0; kc < 4; ++kc) Bf[kc] = *(const uint4 *)(k + ro + max(64 * (a - 1) + 32 * kc + 8 * kg, 0));
+#pragma unroll
+        for (int rb = 0; rb < 4; ++rb) Vq[rb] = *(const uint2 *)(v + ro + 64 * a + 16 * rb + 4 * kg);
+    };
+    issue(0);   // in flight while the Toeplitz fragments are built
+    taps[w][lane] = lane < m_s ? shift_C[(long)c * m_s + lane] : 0.f;
+    if (lane == 0) taps[w][64] = shift_D ? shift_D[c] : 0.f;
+    __builtin_amdgcn_wave_barrier();
+    // A fragments: block rb, chunk kc = kc0(rb) + q; element i: r = 16 rb + col, s = 32 kc + 8 kg + i
+    uint4 Af[4][3];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) {
+#pragma unroll
+        for (int q = 0; q < 3; ++q) {
+            const int kc = (rb < 2 ? 0 : 1) + q;
+            uint32_t e4[4];
+#pragma unroll
+            for (int i2 = 0; i2 < 4; ++i2) {
+                float f2[2];
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int r = 16 * rb + col, sidx = 32 * kc + 8 * kg + 2 * i2 + h;
+                    const int j = r + 64 - sidx;
+                    float val = 0.f;
+                    if (j >= 0 && j < 64) val = taps[w][j] + (j == 0 ? taps[w][64] : 0.f);
+                    f2[h] = val;
+                }
+                e4[i2] = sg_pack<DT>(f2[0], f2[1]);
+            }
+            Af[rb][q] = make_uint4(e4[0], e4[1], e4[2], e4[3]);
+        }
+    }
+    for (int it = 0; it < nit; ++it) {
+        const long ro = ((long)(it / nab) * d + c) * L;
+        const int a = 16 * (it % nab) + col;
+        uint4 B4[4];
+        uint2 V4[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            B4[i] = 64 * (a - 1) + 32 * i + 8 * kg >= 0 ? Bf[i] : make_uint4(0, 0, 0, 0);
+            V4[i] = Vq[i];
+        }
+        if (it + 1 < nit) issue(it + 1);   // the next item's loads overlap this item's products
+#pragma unroll
+        for (int rb = 0; rb < 4; ++rb) {
+            f4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int q = 0; q < 3; ++q) acc = sg_mfma<DT>(Af[rb][q], B4[(rb < 2 ? 0 : 1) + q], acc);
+            const float g0 = acc[0] * sg_f<DT>(V4[rb].x & 0xffffu), g1 = acc[1] * sg_f<DT>(V4[rb].x >> 16);
+            const float g2 = acc[2] * sg_f<DT>(V4[rb].y & 0xffffu), g3 = acc[3] * sg_f<DT>(V4[rb].y >> 16);
+            *(uint2 *)(g + ro + 64 * a + 16 * rb + 4 * kg) = make_uint2(sg_pack<DT>(g0, g1), sg_pack<DT>(g2, g3));
+        }
+    }
+}
+
 // ------------------------------------------------------- fused middle ------
 // Per pair of rows (batches 2j, 2j+1) of channel c, all (B, d, L):
 //   G = (sum_{j<m_s} shift_C[c,j] K_{t-j} + shift_D[c] K_t) * V_t
@@ -518,6 +621,16 @@ hipError_t launch_shift_gate(const void *k, const void *v, const float *shift_C,
                              int B, int d, int L, int dtype, void *g, hipStream_t s) {
     if (m_s > 64 || L % 16 != 0) return hipErrorInvalidValue;
     const long rows = (long)B * d;
+    if (L % 1024 == 0) {
+        const int grid = (d + SGM_W - 1) / SGM_W;
+        if (dtype == BF16)
+            hipLaunchKernelGGL(shift_gate_mfma_kernel<BF16>, dim3(grid), dim3(64 * SGM_W), 0, s,
+                               (const uint16_t *)k, (const uint16_t *)v, shift_C, shift_D, m_s, B, d, L, (uint16_t *)g);
+        else
+            hipLaunchKernelGGL(shift_gate_mfma_kernel<F16>, dim3(grid), dim3(64 * SGM_W), 0, s,
+                               (const uint16_t *)k, (const uint16_t *)v, shift_C, shift_D, m_s, B, d, L, (uint16_t *)g);
+        return hipGetLastError();
+    }
     const long grid = rows * ((L + SG_TILE - 1) / SG_TILE);
     if (dtype == BF16)
         hipLaunchKernelGGL(shift_gate_kernel<BF16>, dim3((unsigned)grid), dim3(SG_T), 0, s, (const uint16_t *)k,
