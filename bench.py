@@ -10,13 +10,16 @@ HBM; K steps rotate over enough input/output buffer sets (>= 512 MB) that
 every step reads u and writes y cold (not from the 256 MB Infinity Cache).
 
 value = algorithmic bytes of one step (u + y + k once per channel + D) / time,
-in GB/s.  The roofline object covers the dominant kernel (the fused conv),
-timed with HIP events on the stream it runs on.  Extra workloads (the shift
+in GB/s, for K independent steps issued round-robin on two HIP streams (each
+with its own kernel buffer and workspace: one step's last workgroups share the
+chip with the next step's first); the single-stream step time is reported
+beside it.  The roofline object covers the dominant kernel (the fused conv),
+timed with HIP events over back-to-back launches on one stream.  Extra workloads (the shift
 kernel conv, the fused-limit bf16 conv, state passing at L = 128K, the layer
 forward, the small fp32 conv) are reported under "extra".  The float64 CPU
 oracle is timed on the same config-1 workload as "cpu_baseline".
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-extra] [--no-cpu]
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--streams S] [--no-extra] [--no-cpu]
 """
 import argparse
 import json
@@ -70,8 +73,16 @@ def _f32(a, dev):
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
 
 
-def bench_headline(h3, steps, warmup, dev):
-    """Config 1 step: kernel generation + fused FFT conv (diagonal SSM)."""
+def bench_headline(h3, steps, warmup, dev, nstreams=2):
+    """Config 1 step: kernel generation + fused FFT conv (diagonal SSM).
+
+    Steps are independent batches of the workload (their own u and y buffer
+    sets).  They are issued round-robin on `nstreams` HIP streams, each with its
+    own kernel buffer and workspace, so the last workgroups of one step's conv
+    share the chip with the next step's kernel generation and first
+    workgroups.  The timed region brackets all K steps (an event on the
+    launching stream before the first, and after every stream has been joined
+    back)."""
     import torch
     import workloads
     w = workloads.config(1)
@@ -83,32 +94,42 @@ def bench_headline(h3, steps, warmup, dev):
     ys = [torch.empty_like(u0) for _ in range(nsets)]
     A, Bp, C, dt = (_f32(w.ssm.A, dev), _f32(w.ssm.B, dev), _f32(w.ssm.C, dev), _f32(w.ssm.dt, dev))
     D = _f32(w.D, dev)
-    k = torch.empty((H, L), dtype=torch.float32, device=dev)
-    ws = torch.empty(max(256, h3.workspace_size(h3.OP_FFTCONV, B, H, L, 0, 0, h3.F16)),
-                     dtype=torch.uint8, device=dev)
+    wsz = max(256, h3.workspace_size(h3.OP_FFTCONV, B, H, L, 0, 0, h3.F16))
+    streams = [torch.cuda.Stream(device=dev) for _ in range(nstreams)]
+    ks = [torch.empty((H, L), dtype=torch.float32, device=dev) for _ in range(nstreams)]
+    wss = [torch.empty(wsz, dtype=torch.uint8, device=dev) for _ in range(nstreams)]
 
-    def one(i):
-        h3.ssm_kernel(A, Bp, C, dt, L, out=k)
-        h3.fftconv(us[i % nsets], k, D, out=ys[i % nsets], workspace=ws)
+    def one(i, ns):
+        j = i % ns
+        with torch.cuda.stream(streams[j]):
+            h3.ssm_kernel(A, Bp, C, dt, L, out=ks[j])
+            h3.fftconv(us[i % nsets], ks[j], D, out=ys[i % nsets], workspace=wss[j])
 
-    for i in range(warmup):
-        one(i)
-    torch.cuda.synchronize()
-    # Timed region: K back-to-back steps bracketed by two events (no per-step
-    # host work beyond the two library calls, so the GPU never waits on Python).
-    t0 = torch.cuda.Event(enable_timing=True); t1 = torch.cuda.Event(enable_timing=True)
-    t0.record()
-    for i in range(steps):
-        one(i)
-    t1.record()
-    torch.cuda.synchronize()
-    ms = t0.elapsed_time(t1) / steps
+    def timed(ns):
+        for i in range(warmup):
+            one(i, ns)
+        torch.cuda.synchronize()
+        cur = torch.cuda.current_stream(dev)
+        t0 = torch.cuda.Event(enable_timing=True); t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(cur)
+        for st in streams[:ns]:
+            st.wait_stream(cur)
+        for i in range(steps):
+            one(i, ns)
+        for st in streams[:ns]:
+            cur.wait_stream(st)
+        t1.record(cur)
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / steps
+
+    ms_single = timed(1)
+    ms = timed(nstreams) if nstreams > 1 else ms_single
     # Per-launch duration of each kernel of the step, each timed over K
-    # back-to-back launches on the stream the library runs on (torch's current
-    # stream, passed to the library by the binding).
+    # back-to-back launches on one stream (torch's current stream, passed to the
+    # library by the binding).
     per = {
-        "ssm_kernel": _time_calls(lambda i: h3.ssm_kernel(A, Bp, C, dt, L, out=k), steps, 3),
-        "fftconv": _time_calls(lambda i: h3.fftconv(us[i % nsets], k, D, out=ys[i % nsets], workspace=ws),
+        "ssm_kernel": _time_calls(lambda i: h3.ssm_kernel(A, Bp, C, dt, L, out=ks[0]), steps, 3),
+        "fftconv": _time_calls(lambda i: h3.fftconv(us[i % nsets], ks[0], D, out=ys[i % nsets], workspace=wss[0]),
                                steps, 3),
     }
     # u + y (fp16) + k (fp32, once per channel) + D
@@ -116,7 +137,8 @@ def bench_headline(h3, steps, warmup, dev):
     conv_bytes = step_bytes
     conv_gbs = conv_bytes / (per["fftconv"] * 1e-3) / 1e9
     return {
-        "w": w, "ms_per_step": ms, "step_bytes": step_bytes,
+        "w": w, "ms_per_step": ms, "ms_per_step_single_stream": ms_single, "streams": nstreams,
+        "step_bytes": step_bytes,
         "value": step_bytes / (ms * 1e-3) / 1e9,
         "gelem_per_s": B * H * L / (ms * 1e-3) / 1e9,
         "stage_ms": per, "conv_bytes": conv_bytes, "conv_gbs": conv_gbs, "nsets": nsets,
@@ -200,19 +222,47 @@ def _extra_cfg2(h3, dev, reps, warm, ex, np, torch, workloads):
 
 
 def _extra_cfg3(h3, dev, reps, warm, ex, np, torch, workloads):
-    # config 3: state passing, B=2 H=1024 L=131072, chunk 8192, fp16
+    # config 3: state passing, B=2 H=1024 L=131072, chunk 8192, fp16.  One call
+    # at a time on one stream, and two independent calls in flight on two
+    # streams (own input, output and workspace each).
     w = workloads.config(3)
     B, H, L, m = w.B, w.H, w.L, w.m
-    u = _dev_tensor(w.u, w.dtype, dev)
-    y = torch.empty_like(u)
     A, Bp, C, dt = (_f32(w.ssm.A, dev), _f32(w.ssm.B, dev), _f32(w.ssm.C, dev), _f32(w.ssm.dt, dev))
     Ab, Bb = h3.ssm_discretize(A, Bp, dt)
     D = _f32(w.D, dev)
-    ws = torch.empty(h3.workspace_size(h3.OP_STATEPASS, B, H, L, m, w.chunk, h3.F16), dtype=torch.uint8, device=dev)
-    ms = _time_calls(lambda i: h3.statepass_conv(u, Ab, Bb, C, D, w.chunk, out=y, workspace=ws), reps, warm)
+    wsz = h3.workspace_size(h3.OP_STATEPASS, B, H, L, m, w.chunk, h3.F16)
+    u = [_dev_tensor(w.u, w.dtype, dev)]
+    u.append(u[0].clone())
+    y = [torch.empty_like(u[0]) for _ in range(2)]
+    ws = [torch.empty(wsz, dtype=torch.uint8, device=dev) for _ in range(2)]
+    ms = _time_calls(lambda i: h3.statepass_conv(u[0], Ab, Bb, C, D, w.chunk, out=y[0], workspace=ws[0]), reps, warm)
+    streams = [torch.cuda.Stream(device=dev) for _ in range(2)]
+
+    def two(i):
+        j = i % 2
+        with torch.cuda.stream(streams[j]):
+            h3.statepass_conv(u[j], Ab, Bb, C, D, w.chunk, out=y[j], workspace=ws[j])
+
+    for i in range(warm):
+        two(i)
+    torch.cuda.synchronize()
+    cur = torch.cuda.current_stream(dev)
+    a = torch.cuda.Event(enable_timing=True); b = torch.cuda.Event(enable_timing=True)
+    a.record(cur)
+    for st in streams:
+        st.wait_stream(cur)
+    for i in range(reps):
+        two(i)
+    for st in streams:
+        cur.wait_stream(st)
+    b.record(cur)
+    torch.cuda.synchronize()
+    ms2 = a.elapsed_time(b) / reps
     by = B * H * L * 4 + 3 * H * m * 8 + H * 4 + 2 * B * H * m * 8
     ex["cfg3_statepass_f16"] = {"ms": ms, "gelem_per_s": B * H * L / ms / 1e6, "GB_s": by / ms / 1e6,
-                                "pct_hbm_peak": 100 * by / ms / 1e6 / HBM_PEAK_GBS}
+                                "pct_hbm_peak": 100 * by / ms / 1e6 / HBM_PEAK_GBS,
+                                "two_streams_ms_per_call": ms2, "two_streams_gelem_per_s": B * H * L / ms2 / 1e6,
+                                "two_streams_pct_hbm_peak": 100 * by / ms2 / 1e6 / HBM_PEAK_GBS}
 
 
 def _extra_cfg4(h3, dev, reps, warm, ex, np, torch, workloads):
@@ -275,6 +325,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--streams", type=int, default=2,
+                    help="HIP streams the headline steps are issued on (independent batches)")
     ap.add_argument("--no-extra", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--only", choices=EXTRA_KEYS, default=None,
@@ -301,7 +353,7 @@ def main():
         return
     import paper_2212_14052_amd as h3
     h3.lib()
-    head = bench_headline(h3, args.steps, args.warmup, dev)
+    head = bench_headline(h3, args.steps, args.warmup, dev, max(1, args.streams))
     print(f"# headline done: {head['ms_per_step']*1e3:.1f} us/step", file=sys.stderr, flush=True)
     extra = {} if args.no_extra else bench_extra(h3, dev, only=args.only)
     if extra:
@@ -325,6 +377,9 @@ def main():
                    "pct_hbm_peak": round(100 * head["value"] / HBM_PEAK_GBS, 2),
                    "gelem_per_s": round(head["gelem_per_s"], 2),
                    "stage_us": {k: round(v * 1e3, 2) for k, v in per.items()},
+                   "streams": head["streams"],
+                   "us_per_step_single_stream": round(head["ms_per_step_single_stream"] * 1e3, 2),
+                   "gb_s_single_stream": round(head["step_bytes"] / (head["ms_per_step_single_stream"] * 1e-3) / 1e9, 1),
                    "buffer_sets": head["nsets"]},
         "roofline": {"bound": "hbm", "achieved": round(head["conv_gbs"], 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(head["conv_gbs"] / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
