@@ -52,6 +52,21 @@ __device__ __forceinline__ void store_tile(uint16_t *C, const f32x16_t &acc, int
     }
 }
 
+// Output-tile order for the GEMMs: the hardware block index is first remapped
+// so that consecutive logical indices run on one XCD (its own L2), then
+// logical indices walk groups of GROUP_M tile rows column by column, so the
+// 32 or so tiles an XCD runs at once form a GROUP_M x 8 block that shares
+// GROUP_M A panels and 8 B panels (a 1 x 32 row would share one A panel and
+// no B panel).
+constexpr int GEMM_GROUP_M = 4;
+__device__ __forceinline__ void gemm_tile(int nbm, int nbn, int &tm, int &tn) {
+    const int l = xcd_logical_block(blockIdx.x, gridDim.x);
+    const int g = l / (GEMM_GROUP_M * nbn), rem = l - g * GEMM_GROUP_M * nbn;
+    const int gm = min(GEMM_GROUP_M, nbm - g * GEMM_GROUP_M);
+    tm = g * GEMM_GROUP_M + rem % gm;
+    tn = rem / gm;
+}
+
 // ------------------------------------------------------------------ GEMM ---
 // C = A . Bt^T with A (M, K) and Bt (N, K) both K-contiguous (16-bit), fp32
 // accumulation, 16-bit result.  Tile 128 x 128 x 32, 4 waves of 64 x 64, each
@@ -67,9 +82,9 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(const uint16_t *A, const u
                                                       uint16_t *C, int M, int N, int K, int d, int L) {
     __shared__ __attribute__((aligned(16))) uint16_t As[GB_M * GB_LDK];
     __shared__ __attribute__((aligned(16))) uint16_t Bs[GB_N * GB_LDK];
-    const int nbn = N / GB_N;
-    const int blk = xcd_logical_block(blockIdx.x, gridDim.x);
-    const int m0 = (blk / nbn) * GB_M, n0 = (blk % nbn) * GB_N;
+    int tm, tn;
+    gemm_tile(M / GB_M, N / GB_N, tm, tn);
+    const int m0 = tm * GB_M, n0 = tn * GB_N;
     const int t = threadIdx.x, lane = t & 63, w = t >> 6;
     const int wm = w >> 1, wn = w & 1;
     // global -> register staging: 2 x 16 B of A and of B per thread
@@ -134,8 +149,7 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(const uint16_t *A, const u
 // two stages of A and B (rows padded to 72 elements: 16-byte fragment reads
 // of 8 consecutive rows hit 8 different bank groups); the next stage is
 // fetched into registers while the current one is multiplied, so one barrier
-// per K step suffices.  Consecutive blocks (same XCD after the remap) share
-// the A panel.
+// per K step suffices.  Tiles run in the grouped order of gemm_tile.
 constexpr int G2_M = 256, G2_N = 256, G2_K = 64, G2_LD = G2_K + 8, G2_T = 512;
 
 template <int DT, int OUT>
@@ -144,9 +158,9 @@ __global__ __launch_bounds__(G2_T) void gemm_nt_256(const uint16_t *A, const uin
     extern __shared__ __attribute__((aligned(16))) uint16_t g2_lds[];
     uint16_t *As = g2_lds;                          // [2][256][72]
     uint16_t *Bs = g2_lds + 2 * G2_M * G2_LD;       // [2][256][72]
-    const int nbn = N / G2_N;
-    const int blk = xcd_logical_block(blockIdx.x, gridDim.x);
-    const int m0 = (blk / nbn) * G2_M, n0 = (blk % nbn) * G2_N;
+    int tm, tn;
+    gemm_tile(M / G2_M, N / G2_N, tm, tn);
+    const int m0 = tm * G2_M, n0 = tn * G2_N;
     const int t = threadIdx.x, lane = t & 63, w = t >> 6;
     const int wm = w >> 2, wn = w & 3;
     // loader mapping: thread -> rows t / 8 + 64 i, 16-byte column chunk (t % 8) * 8
