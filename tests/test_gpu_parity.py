@@ -241,6 +241,28 @@ def test_layer_small(h3, dtype):
     assert rel_err(y, ref) < 2e-2
 
 
+# L = 2048 and 8192 take the matrix-core shift SSM, the wave FFT conv and the
+# gated transpose; an odd batch leaves the last row pair half empty, fewer than
+# 64 shift taps leave zeros in the Toeplitz band, and a shift D adds to its
+# diagonal.
+@pytest.mark.parametrize("dtype", [workloads.BF16, workloads.F16])
+@pytest.mark.parametrize("B,L,m_s,with_D", [(3, 2048, 17, True), (1, 8192, 64, False), (2, 2048, 64, True)])
+def test_layer_wave_path(h3, dtype, B, L, m_s, with_D):
+    w = workloads.layer_workload("t", B, L, 128, dtype, seed=31 + B + m_s, m_shift=m_s)
+    rng = np.random.default_rng(77)
+    sD = rng.standard_normal(w.d).astype(np.float32) if with_D else None
+    A, Bm, C, dt = w.diag.complex64()
+    k32 = oracle.ssm_kernel(A, Bm, C, dt, L).astype(np.float32)
+    W = {n: to_dev(w.W[n][0], w.dtype) for n in "qkvo"}
+    out = h3.layer_fwd(to_dev(w.x, w.dtype), W["q"], W["k"], W["v"], W["o"], f32dev(w.shift_C),
+                       f32dev(sD) if with_D else None, f32dev(k32), f32dev(w.diag_D))
+    torch.cuda.synchronize()
+    ref = oracle.h3_layer(w.x64, w.W["q"][1], w.W["k"][1], w.W["v"][1], w.W["o"][1],
+                          w.shift_C.astype(np.float64), k32.astype(np.float64), w.diag_D.astype(np.float64),
+                          shift_D=sD.astype(np.float64) if with_D else None)
+    assert rel_err(to_np64(out), ref) < 2e-2
+
+
 def test_layer_config4_one_batch_element(h3):
     w = workloads.config(4)
     y, ref = _layer_case(h3, w, b_sel=[3])
