@@ -3,9 +3,12 @@
  * (Fu, Dao et al., arXiv 2212.14052).  C ABI of libh3flash.so.
  *
  * General conventions
- *  - Every tensor pointer is a DEVICE pointer owned by the caller.  The library
- *    allocates no device memory: scratch space is passed in as `workspace`
- *    (size it with h3_workspace_size) and must not alias any other argument.
+ *  - Every tensor pointer is a DEVICE pointer owned by the caller.  Scratch
+ *    space is passed in as `workspace` (size it with h3_workspace_size) and
+ *    must not alias any other argument.  The library's own kernels allocate no
+ *    device memory; h3_layer_fwd's projections run through hipBLASLt, whose
+ *    per-device handle (created on the first layer call on a device and kept
+ *    until the process ends) may hold memory of its own.
  *  - Complex values are interleaved (re, im) float32 pairs.
  *  - Tensors are dense, row-major, with the last dimension contiguous.
  *    Sequence tensors are (B, H, L): row (b, h) is L contiguous elements.
@@ -18,7 +21,10 @@
  *  - NaN and Inf in the inputs propagate to the outputs; they are not masked.
  *  - Return value: H3_OK (0) or a negative h3_status.  No C++ exception crosses
  *    this boundary.
- *  - The library is stateless and may be called from several host threads.
+ *  - The only state the library keeps is host-side and belongs to
+ *    h3_layer_fwd: one hipBLASLt handle per device and one GEMM plan per
+ *    shape, built on first use under a mutex.  Every entry point may be called
+ *    from several host threads.
  */
 #ifndef H3FLASH_H
 #define H3FLASH_H

@@ -47,8 +47,9 @@ StatepassWs statepass_ws(int B, int H, int L, int m, int chunk) {
 }
 
 struct LayerWs {
-    size_t wt_qkv, wt_o, qkv, o_cm, o_tm, kspec, total;
+    size_t wt_qkv, wt_o, qkv, o_cm, o_tm, kspec, gemm, total;
 };
+constexpr size_t kLayerGemmWs = (size_t)64 << 20;   // hipBLASLt algorithm workspace
 LayerWs layer_ws(int B, int d, int L) {
     LayerWs w;
     const size_t act = (size_t)B * d * L * 2;
@@ -58,7 +59,8 @@ LayerWs layer_ws(int B, int d, int L) {
     w.o_cm = w.qkv + align_up(3 * act);
     w.o_tm = w.o_cm + align_up(act);
     w.kspec = w.o_tm + align_up(act);
-    w.total = w.kspec + align_up((size_t)d * (L + 1) * sizeof(float2));
+    w.gemm = w.kspec + align_up((size_t)d * (L + 1) * sizeof(float2));
+    w.total = w.gemm + kLayerGemmWs;
     return w;
 }
 
@@ -261,8 +263,17 @@ int h3_layer_fwd(const void *x, const void *Wq, const void *Wk, const void *Wv, 
     if ((e = launch_transpose_w(Wk, d, dtype, wt_qkv + wsz, s)) != hipSuccess) return H3_EDEVICE;
     if ((e = launch_transpose_w(Wv, d, dtype, wt_qkv + 2 * wsz, s)) != hipSuccess) return H3_EDEVICE;
     if ((e = launch_transpose_w(Wo, d, dtype, wt_o, s)) != hipSuccess) return H3_EDEVICE;
-    // [Q;K;V] (channel-major) = Wt_qkv . x^T
-    if ((e = launch_gemm_nt(wt_qkv, x, qkv, 3 * d, B * L, d, dtype, 1, d, L, s)) != hipSuccess)
+    // [Q;K;V] (channel-major) = Wt_qkv . x^T: per projection j and batch b,
+    // (d, L) block j B d L + b d L = Wt_j (d, d) . x_b (L, d)^T
+    void *gws = ws + w.gemm;
+    bool lt = true;
+    for (int j = 0; j < 3 && lt; ++j) {
+        e = launch_gemm_lt(wt_qkv + j * wsz, x, qkv + j * act, d, L, d, B, 0, (long)L * d, (long)d * L, dtype, gws,
+                           kLayerGemmWs, s);
+        if (e == hipErrorNotSupported && j == 0) lt = false;
+        else if (e != hipSuccess) return H3_EDEVICE;
+    }
+    if (!lt && (e = launch_gemm_nt(wt_qkv, x, qkv, 3 * d, B * L, d, dtype, 1, d, L, s)) != hipSuccess)
         return H3_EDEVICE;
     const char *q = qkv, *kk = qkv + act, *v = qkv + 2 * act;
     if (fftconv_mfma_supported(L, dtype) && L % 64 == 0) {
@@ -284,7 +295,9 @@ int h3_layer_fwd(const void *x, const void *Wq, const void *Wk, const void *Wv, 
         if ((e = launch_transpose_batched(o_cm, o_tm, B, d, L, s)) != hipSuccess) return H3_EDEVICE;
     }
     // out = O . Wo
-    return launched(launch_gemm_nt(o_tm, wt_o, out, B * L, d, d, dtype, 0, d, L, s));
+    e = launch_gemm_lt(o_tm, wt_o, out, B * L, d, d, 1, 0, 0, 0, dtype, gws, kLayerGemmWs, s);
+    if (e == hipErrorNotSupported) return launched(launch_gemm_nt(o_tm, wt_o, out, B * L, d, d, dtype, 0, d, L, s));
+    return e == hipSuccess ? launched(hipSuccess) : H3_EDEVICE;
 }
 
 }  // extern "C"

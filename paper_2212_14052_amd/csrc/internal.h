@@ -89,6 +89,12 @@ hipError_t launch_gate_transpose(const void *q, const void *sv, void *out, int n
 // G = (shift FIR of K + shift_D K) * V over (B, d, L) rows (m_s <= 64, L % 16 == 0).
 hipError_t launch_shift_gate(const void *k, const void *v, const float *shift_C, const float *shift_D, int m_s,
                              int B, int d, int L, int dtype, void *g, hipStream_t s);
+// hipBLASLt GEMM in the same convention as launch_gemm_nt (row-major, K
+// contiguous): C = A . Bt^T, batched with element strides sa, sb, sc (0 =
+// shared operand).  hipErrorNotSupported when no algorithm fits (the caller
+// then uses launch_gemm_nt); ws / ws_bytes: workspace slice for the algorithm.
+hipError_t launch_gemm_lt(const void *A, const void *Bt, void *C, int M, int N, int K, int batch, long sa, long sb,
+                          long sc, int dtype, void *ws, size_t ws_bytes, hipStream_t s);
 hipError_t launch_gemm_nt(const void *A, const void *Bt, void *C, int M, int N, int K, int dtype,
                           int out_mode, int d, int L, hipStream_t s);
 hipError_t launch_layer_mid(const void *q, const void *k, const void *v, const float *shift_C,

@@ -89,7 +89,7 @@ def test_statepass_validation():
     assert statepass(xf=Y + 16) == EINVAL           # x_final inside y
 
 
-def layer(x=U, B=2, L=64, d=128, m_s=64, dt=2, out=Y, ws=W, wsb=1 << 26, shift=K, diag=K + 65536):
+def layer(x=U, B=2, L=64, d=128, m_s=64, dt=2, out=Y, ws=W, wsb=1 << 28, shift=K, diag=K + 65536):
     return h3.lib().h3_layer_fwd(P(x), P(K), P(K), P(K), P(K), P(shift), None, P(diag), None,
                                  B, L, d, m_s, dt, P(out), P(ws), wsb, None)
 
