@@ -142,16 +142,21 @@ int h3_statepass_conv(const void *u, const float *Abar, const float *Bbar,
 /*
  * h3_layer_fwd — H3 layer forward with head dimension 1 (Sec. 3.2,
  * Algorithm 1):
- *   Q = x Wq, K = x Wk, V = x Wv           (row-vector convention, (B,L,d)x(d,d))
+ *   Q = x Wq^T, K = x Wk^T, V = x Wv^T     (Q[b,t,c] = sum_j x[b,t,j] Wq[c,j])
  *   Kbar = SSM_shift(K): Kbar_t = sum_{j<m_s} shift_C[c,j] K_{t-j} + shift_D[c] K_t
  *   G = Kbar * V;  S = SSM_diag(G) = diag_k[c] (*) G + diag_D[c] G   (causal conv)
- *   out = (Q * S) Wo
+ *   out = (Q * S) Wo^T
  *   x, out   (B, L, d) of `dtype` (H3_F16 or H3_BF16); must not overlap.
- *   Wq, Wk, Wv, Wo  (d, d) of `dtype`.
+ *   Wq, Wk, Wv, Wo  (d, d) of `dtype`, stored (out, in) as a linear layer's
+ *   weight: the paper's projection matrices transposed.  Must not overlap
+ *   out or the workspace.
  *   shift_C  (d, m_s) float32, m_s in [1, H3_MAX_SHIFT].  shift_D (d) or NULL.
  *   diag_k   (d, L) float32 (e.g. from h3_ssm_kernel).  diag_D (d) or NULL.
  *   L power of two in [H3_MIN_LEN, H3_FUSED_LIMIT]; d a multiple of 64.
  *   workspace >= h3_workspace_size(H3_OP_LAYER, B, d, L, m_s, 0, dtype).
+ * The four projections run through hipBLASLt; the library's own matrix-core
+ * GEMM runs instead for shapes hipBLASLt rejects, or for every call while the
+ * environment variable H3FLASH_GEMM is "native" (read on each call).
  * Errors: EINVAL, EUNSUPPORTED (L, d, m_s, dtype), EWORKSPACE, EDEVICE.
  */
 int h3_layer_fwd(const void *x, const void *Wq, const void *Wk, const void *Wv,

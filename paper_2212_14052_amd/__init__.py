@@ -210,7 +210,8 @@ def layer_fwd(x: torch.Tensor, Wq: torch.Tensor, Wk: torch.Tensor, Wv: torch.Ten
               diag_k: torch.Tensor, diag_D: Optional[torch.Tensor],
               out: Optional[torch.Tensor] = None,
               workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """H3 layer forward (Algorithm 1, head dimension 1).  x: (B, L, d)."""
+    """H3 layer forward (Algorithm 1, head dimension 1).  x: (B, L, d); the
+    weights (d, d) are stored (out, in) like a linear layer's: Q = x Wq^T."""
     x = x.contiguous()
     Bn, L, d = x.shape
     dt = _dtype(x)

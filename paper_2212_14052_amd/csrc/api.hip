@@ -1,6 +1,8 @@
 // C ABI of libh3flash: argument validation and kernel dispatch.
 // Every check runs on the host before anything is enqueued.
 #include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
 
 #include "../../include/h3flash.h"
 #include "internal.h"
@@ -47,15 +49,13 @@ StatepassWs statepass_ws(int B, int H, int L, int m, int chunk) {
 }
 
 struct LayerWs {
-    size_t wt_qkv, wt_o, qkv, o_cm, o_tm, kspec, gemm, total;
+    size_t qkv, o_cm, o_tm, kspec, gemm, total;
 };
 constexpr size_t kLayerGemmWs = (size_t)64 << 20;   // hipBLASLt algorithm workspace
 LayerWs layer_ws(int B, int d, int L) {
     LayerWs w;
     const size_t act = (size_t)B * d * L * 2;
-    w.wt_qkv = 0;
-    w.wt_o = w.wt_qkv + align_up((size_t)3 * d * d * 2);
-    w.qkv = w.wt_o + align_up((size_t)d * d * 2);
+    w.qkv = 0;
     w.o_cm = w.qkv + align_up(3 * act);
     w.o_tm = w.o_cm + align_up(act);
     w.kspec = w.o_tm + align_up(act);
@@ -247,34 +247,31 @@ int h3_layer_fwd(const void *x, const void *Wq, const void *Wk, const void *Wv, 
     const size_t act = (size_t)B * L * d * 2;
     if (overlap(x, act, out, act) || overlap(workspace, need, x, act) || overlap(workspace, need, out, act))
         return H3_EINVAL;
+    const size_t wbytes = (size_t)d * d * 2;
+    for (const void *W : {Wq, Wk, Wv, Wo})
+        if (overlap(W, wbytes, out, act) || overlap(W, wbytes, workspace, need)) return H3_EINVAL;
     hipStream_t s = (hipStream_t)stream;
     const LayerWs w = layer_ws(B, d, L);
     char *ws = (char *)workspace;
-    char *wt_qkv = ws + w.wt_qkv;
-    void *wt_o = ws + w.wt_o;
     char *qkv = ws + w.qkv;
     void *o_cm = ws + w.o_cm;
     void *o_tm = ws + w.o_tm;
     float2 *Kspec = (float2 *)(ws + w.kspec);
-    const size_t wsz = (size_t)d * d * 2;
     hipError_t e;
-    // Wt = W^T so that both GEMM operands are contiguous along the reduction
-    if ((e = launch_transpose_w(Wq, d, dtype, wt_qkv, s)) != hipSuccess) return H3_EDEVICE;
-    if ((e = launch_transpose_w(Wk, d, dtype, wt_qkv + wsz, s)) != hipSuccess) return H3_EDEVICE;
-    if ((e = launch_transpose_w(Wv, d, dtype, wt_qkv + 2 * wsz, s)) != hipSuccess) return H3_EDEVICE;
-    if ((e = launch_transpose_w(Wo, d, dtype, wt_o, s)) != hipSuccess) return H3_EDEVICE;
-    // [Q;K;V] (channel-major) = Wt_qkv . x^T: per projection j and batch b,
-    // (d, L) block j B d L + b d L = Wt_j (d, d) . x_b (L, d)^T
+    // [Q;K;V] channel-major: per projection j and batch b the (d, L) block
+    // j B d L + b d L is W_j (d, d) . x_b (L, d)^T, both operands contiguous
+    // along the reduction (weights are stored (out, in)).
     void *gws = ws + w.gemm;
-    bool lt = true;
-    for (int j = 0; j < 3 && lt; ++j) {
-        e = launch_gemm_lt(wt_qkv + j * wsz, x, qkv + j * act, d, L, d, B, 0, (long)L * d, (long)d * L, dtype, gws,
-                           kLayerGemmWs, s);
-        if (e == hipErrorNotSupported && j == 0) lt = false;
-        else if (e != hipSuccess) return H3_EDEVICE;
+    const void *Wqkv[3] = {Wq, Wk, Wv};
+    const char *gsel = getenv("H3FLASH_GEMM");
+    const bool native = gsel && strcmp(gsel, "native") == 0;
+    for (int j = 0; j < 3; ++j) {
+        e = native ? hipErrorNotSupported
+                   : launch_gemm_lt(Wqkv[j], true, x, true, qkv + j * act, d, L, d, B, 0, (long)L * d, (long)d * L,
+                                    dtype, gws, kLayerGemmWs, s);
+        if (e == hipErrorNotSupported) e = launch_gemm_nt(Wqkv[j], x, qkv + j * act, d, B * L, d, dtype, 1, d, L, s);
+        if (e != hipSuccess) return H3_EDEVICE;
     }
-    if (!lt && (e = launch_gemm_nt(wt_qkv, x, qkv, 3 * d, B * L, d, dtype, 1, d, L, s)) != hipSuccess)
-        return H3_EDEVICE;
     const char *q = qkv, *kk = qkv + act, *v = qkv + 2 * act;
     if (fftconv_mfma_supported(L, dtype) && L % 64 == 0) {
         // G = (shift SSM of K) * V  ->  o_cm;  S = diag conv of G (+ D G)  ->  K's slot (K is dead);
@@ -294,9 +291,10 @@ int h3_layer_fwd(const void *x, const void *Wq, const void *Wk, const void *Wv, 
         // O (B, d, L) -> (B, L, d)
         if ((e = launch_transpose_batched(o_cm, o_tm, B, d, L, s)) != hipSuccess) return H3_EDEVICE;
     }
-    // out = O . Wo
-    e = launch_gemm_lt(o_tm, wt_o, out, B * L, d, d, 1, 0, 0, 0, dtype, gws, kLayerGemmWs, s);
-    if (e == hipErrorNotSupported) return launched(launch_gemm_nt(o_tm, wt_o, out, B * L, d, d, dtype, 0, d, L, s));
+    // out = O (M, K) . Wo (N, K)^T
+    e = native ? hipErrorNotSupported
+               : launch_gemm_lt(o_tm, true, Wo, true, out, B * L, d, d, 1, 0, 0, 0, dtype, gws, kLayerGemmWs, s);
+    if (e == hipErrorNotSupported) return launched(launch_gemm_nt(o_tm, Wo, out, B * L, d, d, dtype, 0, d, L, s));
     return e == hipSuccess ? launched(hipSuccess) : H3_EDEVICE;
 }
 

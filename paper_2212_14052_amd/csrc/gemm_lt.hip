@@ -1,10 +1,13 @@
 // The layer's Q/K/V/O projections (Algorithm 1: Q = u W_Q, ..., out = O W_O)
 // are plain GEMMs and run through hipBLASLt (fp32 accumulation, 16-bit in and
-// out).  Operands follow the library's row-major "NT" convention,
-//   C (M, N) = A (M, K) . Bt (N, K)^T   (all row-major, K contiguous),
-// which hipBLASLt (column-major) sees as D (N x M) = Bt^T-op . A:  matrix "A"
-// of the call is Bt as a K x N column-major array (op T), matrix "B" is A as a
-// K x M column-major array (op N), D is N x M with leading dimension N.
+// out).  C (M, N) is row-major; A is given either as (M, K) row-major ("K
+// contiguous") or as (K, M) row-major, and B either as (N, K) row-major or as
+// (K, N) row-major.  hipBLASLt is column-major, so the call computes
+// D = C^T (N x M, leading dimension N) = B^T . A^T:
+//   its matrix "A" is our B:  (N, K) row-major = K x N column-major, op T;
+//                             (K, N) row-major = N x K column-major, op N;
+//   its matrix "B" is our A:  (M, K) row-major = K x M column-major, op N;
+//                             (K, M) row-major = M x K column-major, op T.
 // Batched over `batch` with element strides sa, sb, sc (0 = shared operand).
 //
 // Host-side state: one hipBLASLt handle per device and one plan (descriptors
@@ -33,17 +36,22 @@ struct LtPlan {
 
 std::mutex g_lt_mu;
 std::map<int, hipblasLtHandle_t> g_lt_handles;
-using LtKey = std::tuple<int, int, int, int, int, int, long, long, long, size_t>;
+using LtKey = std::tuple<int, int, int, int, int, int, long, long, long, size_t, bool, bool>;
 std::map<LtKey, LtPlan> g_lt_plans;
 
-bool make_plan(hipblasLtHandle_t h, hipDataType t, int M, int N, int K, int batch, long sa, long sb, long sc,
-               size_t ws_bytes, LtPlan &p) {
+bool make_plan(hipblasLtHandle_t h, hipDataType t, int M, int N, int K, bool a_kc, bool b_kc, int batch, long sa,
+               long sb, long sc, size_t ws_bytes, LtPlan &p) {
     if (hipblasLtMatmulDescCreate(&p.desc, HIPBLAS_COMPUTE_32F, HIP_R_32F) != HIPBLAS_STATUS_SUCCESS) return false;
-    const hipblasOperation_t ta = HIPBLAS_OP_T, tb = HIPBLAS_OP_N;
+    const hipblasOperation_t ta = b_kc ? HIPBLAS_OP_T : HIPBLAS_OP_N;
+    const hipblasOperation_t tb = a_kc ? HIPBLAS_OP_N : HIPBLAS_OP_T;
     hipblasLtMatmulDescSetAttribute(p.desc, HIPBLASLT_MATMUL_DESC_TRANSA, &ta, sizeof(ta));
     hipblasLtMatmulDescSetAttribute(p.desc, HIPBLASLT_MATMUL_DESC_TRANSB, &tb, sizeof(tb));
-    if (hipblasLtMatrixLayoutCreate(&p.la, t, K, N, K) != HIPBLAS_STATUS_SUCCESS) return false;   // Bt
-    if (hipblasLtMatrixLayoutCreate(&p.lb, t, K, M, K) != HIPBLAS_STATUS_SUCCESS) return false;   // A
+    const hipblasStatus_t s1 = b_kc ? hipblasLtMatrixLayoutCreate(&p.la, t, K, N, K)    // our B
+                                    : hipblasLtMatrixLayoutCreate(&p.la, t, N, K, N);
+    if (s1 != HIPBLAS_STATUS_SUCCESS) return false;
+    const hipblasStatus_t s2 = a_kc ? hipblasLtMatrixLayoutCreate(&p.lb, t, K, M, K)    // our A
+                                    : hipblasLtMatrixLayoutCreate(&p.lb, t, M, K, M);
+    if (s2 != HIPBLAS_STATUS_SUCCESS) return false;
     if (hipblasLtMatrixLayoutCreate(&p.lc, t, N, M, N) != HIPBLAS_STATUS_SUCCESS) return false;   // C = D
     if (batch > 1) {
         const int32_t bc = batch;
@@ -73,8 +81,8 @@ bool make_plan(hipblasLtHandle_t h, hipDataType t, int M, int N, int K, int batc
 
 }  // namespace
 
-hipError_t launch_gemm_lt(const void *A, const void *Bt, void *C, int M, int N, int K, int batch, long sa, long sb,
-                          long sc, int dtype, void *ws, size_t ws_bytes, hipStream_t s) {
+hipError_t launch_gemm_lt(const void *A, bool a_kc, const void *B, bool b_kc, void *C, int M, int N, int K, int batch,
+                          long sa, long sb, long sc, int dtype, void *ws, size_t ws_bytes, hipStream_t s) {
     if (dtype != F16 && dtype != BF16) return hipErrorNotSupported;
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return hipErrorNotSupported;
@@ -86,17 +94,17 @@ hipError_t launch_gemm_lt(const void *A, const void *Bt, void *C, int M, int N, 
         if (hipblasLtCreate(&h) != HIPBLAS_STATUS_SUCCESS) return hipErrorNotSupported;
         hit = g_lt_handles.emplace(dev, h).first;
     }
-    const LtKey key{dev, dtype, M, N, K, batch, sa, sb, sc, ws_bytes};
+    const LtKey key{dev, dtype, M, N, K, batch, sa, sb, sc, ws_bytes, a_kc, b_kc};
     auto pit = g_lt_plans.find(key);
     if (pit == g_lt_plans.end()) {
         LtPlan p;
-        p.ok = make_plan(hit->second, t, M, N, K, batch, sa, sb, sc, ws_bytes, p);
+        p.ok = make_plan(hit->second, t, M, N, K, a_kc, b_kc, batch, sa, sb, sc, ws_bytes, p);
         pit = g_lt_plans.emplace(key, p).first;
     }
     const LtPlan &p = pit->second;
     if (!p.ok) return hipErrorNotSupported;
     const float alpha = 1.f, beta = 0.f;
-    const hipblasStatus_t st = hipblasLtMatmul(hit->second, p.desc, &alpha, Bt, p.la, A, p.lb, &beta, C, p.lc, C,
+    const hipblasStatus_t st = hipblasLtMatmul(hit->second, p.desc, &alpha, B, p.la, A, p.lb, &beta, C, p.lc, C,
                                                p.lc, &p.algo, p.ws ? ws : nullptr, p.ws, s);
     return st == HIPBLAS_STATUS_SUCCESS ? hipSuccess : hipErrorLaunchFailure;
 }

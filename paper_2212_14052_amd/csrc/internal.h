@@ -81,7 +81,6 @@ hipError_t launch_state_correction_mfma(const float *Abar, const float2 *corr_W,
                                         int chunk, int nchunk, int dtype, void *corr, hipStream_t s);
 
 // Layer pieces.
-hipError_t launch_transpose_w(const void *W, int d, int dtype, void *Wt, hipStream_t s);
 hipError_t launch_transpose_batched(const void *in, void *out, int nb, int R, int C, hipStream_t s);
 // O (B, L, d) token-major = (Q * S)^T per batch slice, Q and S (B, d, L); R = d, C = L.
 hipError_t launch_gate_transpose(const void *q, const void *sv, void *out, int nb, int R, int C, int dtype,
@@ -89,12 +88,14 @@ hipError_t launch_gate_transpose(const void *q, const void *sv, void *out, int n
 // G = (shift FIR of K + shift_D K) * V over (B, d, L) rows (m_s <= 64, L % 16 == 0).
 hipError_t launch_shift_gate(const void *k, const void *v, const float *shift_C, const float *shift_D, int m_s,
                              int B, int d, int L, int dtype, void *g, hipStream_t s);
-// hipBLASLt GEMM in the same convention as launch_gemm_nt (row-major, K
-// contiguous): C = A . Bt^T, batched with element strides sa, sb, sc (0 =
-// shared operand).  hipErrorNotSupported when no algorithm fits (the caller
-// then uses launch_gemm_nt); ws / ws_bytes: workspace slice for the algorithm.
-hipError_t launch_gemm_lt(const void *A, const void *Bt, void *C, int M, int N, int K, int batch, long sa, long sb,
-                          long sc, int dtype, void *ws, size_t ws_bytes, hipStream_t s);
+// hipBLASLt GEMM, C (M, N) row-major = A . B with A given as (M, K)
+// row-major when a_kc (K contiguous) else as (K, M) row-major, and B given as
+// (N, K) row-major when b_kc else as (K, N) row-major; batched with element
+// strides sa, sb, sc (0 = shared operand).  hipErrorNotSupported, before
+// anything is enqueued, when no algorithm fits (the caller then uses
+// launch_gemm_nt); ws / ws_bytes: workspace slice for the algorithm.
+hipError_t launch_gemm_lt(const void *A, bool a_kc, const void *B, bool b_kc, void *C, int M, int N, int K, int batch,
+                          long sa, long sb, long sc, int dtype, void *ws, size_t ws_bytes, hipStream_t s);
 hipError_t launch_gemm_nt(const void *A, const void *Bt, void *C, int M, int N, int K, int dtype,
                           int out_mode, int d, int L, hipStream_t s);
 hipError_t launch_layer_mid(const void *q, const void *k, const void *v, const float *shift_C,

@@ -602,11 +602,6 @@ __global__ __launch_bounds__(N / 16 >= 64 ? N / 16 : 64) void layer_mid_kernel(
 }
 
 // --------------------------------------------------------------- launch ----
-hipError_t launch_transpose_w(const void *W, int d, int dtype, void *Wt, hipStream_t s) {
-    (void)dtype;
-    return launch_transpose_batched(W, Wt, 1, d, d, s);
-}
-
 hipError_t launch_transpose_batched(const void *in, void *out, int nb, int R, int C, hipStream_t s) {
     const int tiles = ((R + 63) / 64) * ((C + 63) / 64);
     if (R % 8 == 0 && C % 8 == 0)

@@ -223,7 +223,7 @@ def _layer_case(h3, w, b_sel=None):
     A, B, C, dt = w.diag.complex64()
     k64 = oracle.ssm_kernel(A, B, C, dt, L)
     k32 = k64.astype(np.float32)
-    W = {n: to_dev(w.W[n][0], w.dtype) for n in "qkvo"}
+    W = {n: to_dev(w.weight_out_in(n), w.dtype) for n in "qkvo"}
     out = h3.layer_fwd(to_dev(w.x, w.dtype), W["q"], W["k"], W["v"], W["o"], f32dev(w.shift_C), None,
                        f32dev(k32), f32dev(w.diag_D))
     torch.cuda.synchronize()
@@ -253,7 +253,7 @@ def test_layer_wave_path(h3, dtype, B, L, m_s, with_D):
     sD = rng.standard_normal(w.d).astype(np.float32) if with_D else None
     A, Bm, C, dt = w.diag.complex64()
     k32 = oracle.ssm_kernel(A, Bm, C, dt, L).astype(np.float32)
-    W = {n: to_dev(w.W[n][0], w.dtype) for n in "qkvo"}
+    W = {n: to_dev(w.weight_out_in(n), w.dtype) for n in "qkvo"}
     out = h3.layer_fwd(to_dev(w.x, w.dtype), W["q"], W["k"], W["v"], W["o"], f32dev(w.shift_C),
                        f32dev(sD) if with_D else None, f32dev(k32), f32dev(w.diag_D))
     torch.cuda.synchronize()
@@ -261,6 +261,16 @@ def test_layer_wave_path(h3, dtype, B, L, m_s, with_D):
                           w.shift_C.astype(np.float64), k32.astype(np.float64), w.diag_D.astype(np.float64),
                           shift_D=sD.astype(np.float64) if with_D else None)
     assert rel_err(to_np64(out), ref) < 2e-2
+
+
+# The library's own matrix-core GEMM (used where hipBLASLt rejects a shape),
+# forced through the documented switch, on both mixing paths.
+@pytest.mark.parametrize("L", [256, 2048])
+def test_layer_native_gemm(h3, monkeypatch, L):
+    monkeypatch.setenv("H3FLASH_GEMM", "native")
+    w = workloads.layer_workload("t", 2, L, 256, workloads.BF16, seed=23 + L)
+    y, ref = _layer_case(h3, w)
+    assert rel_err(y, ref) < 2e-2
 
 
 def test_layer_config4_one_batch_element(h3):
