@@ -115,7 +115,8 @@ def recurrence(u, Abar, Bbar, C, D, x0=None):
     y = np.empty(u.shape, np.float64)
     xf = np.empty(u.shape[:-1] + (m,), np.complex128)
     x0p = _r(np.asarray(x0, np.complex128).reshape(R, m)) if x0 is not None else None
-    lib().oracle_ssm_recurrence(_p(u), _p(_r(Abar)), _p(_r(Bbar)), _p(_r(C)), _p(_r(D)),
+    Dp = _r(D) if D is not None else None
+    lib().oracle_ssm_recurrence(_p(u), _p(_r(Abar)), _p(_r(Bbar)), _p(_r(C)), _p(Dp),
                                 _p(x0p), R, H, L, m, _p(y), _p(xf.view(np.float64)))
     return y, xf
 
@@ -129,7 +130,8 @@ def statepass(u, Abar, Bbar, C, D, chunk: int, x0=None):
     y = np.empty(u.shape, np.float64)
     xf = np.empty(u.shape[:-1] + (m,), np.complex128)
     x0p = _r(np.asarray(x0, np.complex128).reshape(R, m)) if x0 is not None else None
-    lib().oracle_statepass(_p(u), _p(_r(Abar)), _p(_r(Bbar)), _p(_r(C)), _p(_r(D)),
+    Dp = _r(D) if D is not None else None
+    lib().oracle_statepass(_p(u), _p(_r(Abar)), _p(_r(Bbar)), _p(_r(C)), _p(Dp),
                            _p(x0p), R, H, L, m, chunk, _p(y), _p(xf.view(np.float64)))
     return y, xf
 

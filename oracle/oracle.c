@@ -131,7 +131,7 @@ void oracle_causal_conv(const double *u, const double *k, const double *D,
  * Explicit recurrence of the diagonal SSM (Sec. 2.1, discrete form):
  *   x_t = Abar x_{t-1} + Bbar u_t,   y_t = 2 Re(C . x_t) + D u_t,
  * with x_{-1} = x0 (NULL: zero).  Modes are independent, so "Abar x" is the
- * elementwise product.  u, y: (R, L); Abar, Bbar, C: (H, m) complex; D: (H);
+ * elementwise product.  u, y: (R, L); Abar, Bbar, C: (H, m) complex; D: (H) or NULL (no skip);
  * x0, x_final: (R, m) complex (x_final = x_{L-1}; may be NULL).
  */
 void oracle_ssm_recurrence(const double *u, const double *Abar, const double *Bbar,
@@ -151,7 +151,7 @@ void oracle_ssm_recurrence(const double *u, const double *Abar, const double *Bb
                 x[n] = ld(Abar, i) * x[n] + ld(Bbar, i) * ut;
                 s += ld(C, i) * x[n];
             }
-            y[(long)r * L + t] = 2.0 * creal(s) + D[h] * ut;
+            y[(long)r * L + t] = 2.0 * creal(s) + (D ? D[h] * ut : 0.0);
         }
         if (x_final)
             for (int n = 0; n < m; ++n) st(x_final, (long)r * m + n, x[n]);
@@ -205,7 +205,7 @@ void oracle_statepass(const double *u, const double *Abar, const double *Bbar,
             for (int t = 0; t < chunk; ++t) {
                 cplx s = 0;
                 for (int n = 0; n < m; ++n) s += Mxy[(long)n * chunk + t] * x[n];
-                yc[t] = 2.0 * creal(s) + conv[t] + D[h] * uc[t];
+                yc[t] = 2.0 * creal(s) + conv[t] + (D ? D[h] * uc[t] : 0.0);
             }
             for (int n = 0; n < m; ++n) {
                 cplx s = 0;
