@@ -159,7 +159,7 @@ def _time_calls(fn, reps, warm):
     return a.elapsed_time(b) / reps
 
 
-EXTRA_KEYS = ("cfg1_shift", "cfg2", "cfg3", "cfg4", "cfg0")
+EXTRA_KEYS = ("cfg1_shift", "cfg2", "cfg3", "cfg4", "cfg0", "step")
 
 
 def bench_extra(h3, dev, reps=10, warm=3, only=None):
@@ -182,6 +182,8 @@ def bench_extra(h3, dev, reps=10, warm=3, only=None):
         _extra_cfg4(h3, dev, reps, warm, ex, np, torch, workloads)
     if want("cfg0"):
         _extra_cfg0(h3, dev, reps, warm, ex, np, torch, workloads)
+    if want("step"):
+        _extra_step(h3, dev, reps, warm, ex, np, torch, workloads)
     return ex
 
 
@@ -295,6 +297,36 @@ def _extra_cfg0(h3, dev, reps, warm, ex, np, torch, workloads):
     ms = _time_calls(lambda i: (h3.ssm_kernel(A, Bp, C, dt, w.L, out=k),
                                 h3.fftconv(u, k, D, out=y, workspace=ws)), 50, 5)
     ex["cfg0_f32_latency_us"] = ms * 1e3
+
+
+def _extra_step(h3, dev, reps, warm, ex, np, torch, workloads):
+    # recurrent step mode (generation): one token per row, B=64 H=768 m=64,
+    # fp16 tokens, fp32 complex state; the timed calls rotate over 24 states
+    # (604 MB) so that every call reads and writes its state in HBM
+    B, H, m, nset = 64, 768, 64, 24
+    rng = np.random.default_rng(7)
+    ssm = workloads.make_diag_ssm(rng, H, m, 1e-3, 1e-1)
+    A, Bp, dt = _f32(ssm.A, dev), _f32(ssm.B, dev), _f32(ssm.dt, dev)
+    Ab, Bb = h3.ssm_discretize(A, Bp, dt)
+    C, D = _f32(ssm.C, dev), _f32(rng.standard_normal(H), dev)
+    xs = [torch.zeros((B, H, m, 2), dtype=torch.float32, device=dev) for _ in range(nset)]
+    u = torch.from_numpy(rng.standard_normal((nset, B, H)).astype(np.float16)).to(dev)
+    y = torch.empty((B, H), dtype=torch.float16, device=dev)
+    h3.ssm_step(u[0], Ab, Bb, C, D, xs[0], out=y)   # argument checks once, through the binding
+    # then the C entry point with prebuilt arguments, so that host overhead
+    # per call stays below the kernel's duration
+    import ctypes
+    lib, vp = h3.lib(), ctypes.c_void_p
+    st = vp(torch.cuda.current_stream(dev).cuda_stream)
+    pa = [vp(t.data_ptr()) for t in (Ab, Bb, C, D)]
+    calls = [(vp(u[j].data_ptr()), vp(xs[j].data_ptr())) for j in range(nset)]
+    yp = vp(y.data_ptr())
+    ms = _time_calls(lambda i: lib.h3_ssm_step(calls[i % nset][0], *pa, B, H, m, 1, h3.F16, calls[i % nset][1],
+                                                yp, st), 4 * nset, nset)
+    nbytes = 2 * B * H * m * 8 + 3 * H * m * 8 + H * 4 + 2 * B * H * 2
+    ex["step_decode_f16"] = {"us": ms * 1e3, "GB_s": nbytes / (ms * 1e-3) / 1e9,
+                             "pct_hbm_peak": 100 * nbytes / (ms * 1e-3) / 8e12,
+                             "tokens_per_s": B / (ms * 1e-3), "bytes_per_call": nbytes}
 
 
 def cpu_baseline(w, step_bytes, min_seconds=10.0, max_reps=64):

@@ -140,6 +140,28 @@ int h3_statepass_conv(const void *u, const float *Abar, const float *Bbar,
                       void *workspace, size_t ws_bytes, void *stream);
 
 /*
+ * h3_ssm_step — recurrent (step) mode of a diagonal SSM, for generation
+ * (Sec. 2, the recurrent view; Sec. 5 generation): advances the carried state
+ * over T new tokens per (b, h) row,
+ *   x_n <- Abar_n x_n + Bbar_n u_t,   y_t = 2 Re(C . x) + D u_t,  t = 0..T-1,
+ * which is the recurrence whose impulse response is k, so a state written by
+ * h3_statepass_conv (x_final) continues that sequence.
+ *   u, y        (B, H, T) of `dtype` (T = 1: one token per row); must not
+ *               overlap each other or the state.
+ *   Abar, Bbar, C (H, m) complex (e.g. from h3_ssm_discretize).  D (H)
+ *               float32 or NULL.
+ *   x           (B, H, m) complex, read and overwritten with the state after
+ *               the last token (the caller owns it between calls).
+ *   m in [1, H3_MAX_MODES].  Arithmetic in float32.  Pointers aligned to
+ *   their element size (8 bytes for complex).
+ * Errors: EINVAL (null, sizes, alignment, overlap), EUNSUPPORTED (m, dtype),
+ *         EDEVICE.
+ */
+int h3_ssm_step(const void *u, const float *Abar, const float *Bbar, const float *C,
+                const float *D, int B, int H, int m, int T, int dtype,
+                float *x, void *y, void *stream);
+
+/*
  * h3_layer_fwd — H3 layer forward with head dimension 1 (Sec. 3.2,
  * Algorithm 1):
  *   Q = x Wq^T, K = x Wk^T, V = x Wv^T     (Q[b,t,c] = sum_j x[b,t,j] Wq[c,j])

@@ -19,7 +19,7 @@ import torch
 
 __all__ = [
     "H3Error", "lib", "ssm_discretize", "ssm_kernel", "fftconv", "statepass_conv",
-    "layer_fwd", "kernel_spectrum", "fftconv_spectral", "workspace_size", "status_string", "F32", "F16", "BF16",
+    "layer_fwd", "ssm_step", "kernel_spectrum", "fftconv_spectral", "workspace_size", "status_string", "F32", "F16", "BF16",
     "OP_FFTCONV", "OP_STATEPASS", "OP_LAYER", "FUSED_LIMIT", "MAX_MODES",
 ]
 
@@ -59,12 +59,13 @@ def lib() -> ctypes.CDLL:
         L.h3_fftconv_spectral.argtypes = [vp, vp, vp, vp, i, i, i, i, vp]
         L.h3_statepass_conv.argtypes = [vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, vp, vp, vp, sz, vp]
         L.h3_layer_fwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, vp, vp, sz, vp]
+        L.h3_ssm_step.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, vp, vp, vp]
         L.h3_workspace_size.argtypes = [i, i, i, i, i, i, i]
         L.h3_workspace_size.restype = sz
         L.h3_status_string.argtypes = [i]
         L.h3_status_string.restype = ctypes.c_char_p
         for fn in ("h3_ssm_discretize", "h3_ssm_kernel", "h3_fftconv", "h3_statepass_conv",
-                   "h3_layer_fwd", "h3_kernel_spectrum", "h3_fftconv_spectral"):
+                   "h3_layer_fwd", "h3_kernel_spectrum", "h3_fftconv_spectral", "h3_ssm_step"):
             getattr(L, fn).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -203,6 +204,28 @@ def statepass_conv(u: torch.Tensor, Abar: torch.Tensor, Bbar: torch.Tensor, C: t
         _ptr(u), _ptr(Abar), _ptr(Bbar), _ptr(C), _ptr(D), _ptr(x0), Bn, H, L, m, chunk, dt,
         _ptr(y), _ptr(xf), _ptr(ws), ws.numel() * ws.element_size(), _stream(u.device)))
     return y, xf
+
+
+def ssm_step(u: torch.Tensor, Abar: torch.Tensor, Bbar: torch.Tensor, C: torch.Tensor,
+             D: Optional[torch.Tensor], x: torch.Tensor,
+             out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Recurrent step mode: advance the state ``x`` (B, H, m, 2) float32, in
+    place, over the tokens ``u`` (B, H) or (B, H, T); returns y shaped like u."""
+    if x.dtype != torch.float32 or x.dim() != 4 or x.shape[-1] != 2 or not x.is_contiguous():
+        raise ValueError("x must be a contiguous float32 (B, H, m, 2) tensor (it is updated in place)")
+    Bn, H, m = x.shape[0], x.shape[1], x.shape[2]
+    uu = u.contiguous()
+    if uu.dim() == 2:
+        uu = uu.unsqueeze(-1)
+    if uu.dim() != 3 or uu.shape[0] != Bn or uu.shape[1] != H:
+        raise ValueError("u must be (B, H) or (B, H, T) with the state's B and H")
+    T = uu.shape[2]
+    Abar, Bbar, C, D = _cplx(Abar), _cplx(Bbar), _cplx(C), _f32(D)
+    y = out if out is not None else torch.empty_like(u)
+    _check("h3_ssm_step", lib().h3_ssm_step(
+        _ptr(uu), _ptr(Abar), _ptr(Bbar), _ptr(C), _ptr(D), Bn, H, m, T, _dtype(uu), _ptr(x), _ptr(y),
+        _stream(x.device)))
+    return y
 
 
 def layer_fwd(x: torch.Tensor, Wq: torch.Tensor, Wk: torch.Tensor, Wv: torch.Tensor,

@@ -100,6 +100,22 @@ int h3_ssm_discretize(const float *A, const float *B, const float *dt, int H, in
     return launched(launch_discretize(A, B, dt, H, m, Abar, Bbar, (hipStream_t)stream));
 }
 
+int h3_ssm_step(const void *u, const float *Abar, const float *Bbar, const float *C, const float *D, int B, int H,
+                int m, int T, int dtype, float *x, void *y, void *stream) {
+    if (!u || !Abar || !Bbar || !C || !x || !y || B < 1 || H < 1 || m < 1 || T < 1) return H3_EINVAL;
+    if (!dtype_ok(dtype) || m > H3_MAX_MODES) return H3_EUNSUPPORTED;
+    const size_t io = (size_t)B * H * T * esize(dtype), xs = (size_t)B * H * m * 8, ps = (size_t)H * m * 8;
+    const uintptr_t ea = esize(dtype) - 1;
+    if (((uintptr_t)u & ea) || ((uintptr_t)y & ea) || ((uintptr_t)x & 7) || ((uintptr_t)Abar & 7) ||
+        ((uintptr_t)Bbar & 7) || ((uintptr_t)C & 7) || ((uintptr_t)D & 3))
+        return H3_EINVAL;
+    if (overlap(u, io, y, io) || overlap(x, xs, u, io) || overlap(x, xs, y, io) || overlap(x, xs, Abar, ps) ||
+        overlap(x, xs, Bbar, ps) || overlap(x, xs, C, ps) || overlap(x, xs, D, (size_t)H * 4) ||
+        overlap(y, io, Abar, ps) || overlap(y, io, Bbar, ps) || overlap(y, io, C, ps) || overlap(y, io, D, (size_t)H * 4))
+        return H3_EINVAL;
+    return launched(launch_ssm_step(u, Abar, Bbar, C, D, B, H, m, T, dtype, x, y, (hipStream_t)stream));
+}
+
 int h3_ssm_kernel(const float *A, const float *B, const float *C, const float *dt, int H, int m,
                   int L, float *k, void *stream) {
     if (!A || !B || !C || !dt || !k || H < 1 || m < 1 || L < 1) return H3_EINVAL;

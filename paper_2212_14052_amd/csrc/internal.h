@@ -13,6 +13,11 @@ hipError_t launch_discretize(const float *A, const float *B, const float *dt, in
 hipError_t launch_kernel_gen(int mode, const float *P0, const float *P1, const float *C,
                              const float *dt, int H, int m, int L, float *k, hipStream_t s);
 
+// Recurrent step mode: T tokens per (b, h) row from the carried state x
+// (B, H, m) complex, updated in place; u, y (B, H, T).
+hipError_t launch_ssm_step(const void *u, const float *Abar, const float *Bbar, const float *C, const float *D,
+                           int B, int H, int m, int T, int dtype, float *x, void *y, hipStream_t s);
+
 // Kernel spectra: Kspec[h][f] = (1/N) sum_{t<L} k[h][t] exp(-2 pi i f t / N),
 // f = 0..L, N = 2L.  Kspec: (H, L+1) float2.
 hipError_t launch_spectrum(const float *k, int H, int L, float2 *Kspec, hipStream_t s);

@@ -122,3 +122,21 @@ def test_spectral_validation():
     assert L.h3_fftconv_spectral(P(U), P(K), None, P(U), 2, 4, 64, 0, None) == EINVAL
     assert L.h3_fftconv_spectral(P(U), P(K), None, P(Y), 2, 4, 64, 9, None) == EUNSUP
     assert L.h3_fftconv_spectral(P(U), P(K), None, P(Y), 2, 4, 32768, 1, None) == EUNSUP
+
+
+def step(u=U, A=K, Bb=K + 4096, C=K + 8192, D=None, B=2, H=4, m=64, T=1, dt=1, x=X, y=Y):
+    return h3.lib().h3_ssm_step(P(u), P(A), P(Bb), P(C), P(D), B, H, m, T, dt, P(x), P(y), None)
+
+
+def test_step_validation():
+    assert step(u=0) == EINVAL
+    assert step(x=0) == EINVAL
+    assert step(T=0) == EINVAL
+    assert step(m=0) == EINVAL
+    assert step(m=65) == EUNSUP
+    assert step(dt=3) == EUNSUP
+    assert step(x=X + 4) == EINVAL                   # complex state not 8-byte aligned
+    assert step(u=U + 1) == EINVAL                   # 16-bit tokens misaligned
+    assert step(y=U) == EINVAL                       # y aliases u
+    assert step(y=X + 64) == EINVAL                  # y inside the state
+    assert step(x=K + 256) == EINVAL                 # state overlaps Abar

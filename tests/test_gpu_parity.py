@@ -196,6 +196,69 @@ def test_statepass_resume(h3):
     assert rel_err(to_np64(x2), to_np64(xf)) < 1e-5
 
 
+# ------------------------------------------------- recurrent step mode ---
+def _step_inputs(B, H, m, T, dtype, seed):
+    rng = np.random.default_rng(seed)
+    u_s, u64 = workloads.round_to(rng.standard_normal((B, H, T)), dtype)
+    ssm = workloads.make_diag_ssm(rng, H, m, 1e-3, 1e-1)
+    A, Bm, C, dt = ssm.complex64()
+    Ab, Bb = oracle.zoh(A, Bm, dt)
+    Ab32, Bb32 = cplx_to_f32pairs(Ab), cplx_to_f32pairs(Bb)
+    D = workloads.f32(rng.standard_normal(H))
+    x0 = cplx_to_f32pairs((rng.standard_normal((B, H, m)) + 1j * rng.standard_normal((B, H, m))) * 0.5)
+    return u_s, u64, Ab32, Bb32, ssm.C, D, x0
+
+
+# T = 1 is one generated token; T > 1 keeps the state in registers over
+# several tokens; m = 1 and 17 leave lanes without modes; H = 33 and odd B
+# leave the last workgroup partly empty.
+@pytest.mark.parametrize("dtype", [workloads.F32, workloads.F16, workloads.BF16])
+@pytest.mark.parametrize("B,H,m,T", [(1, 1, 1, 1), (3, 5, 17, 7), (2, 33, 64, 64), (4, 768, 64, 1)])
+def test_ssm_step(h3, dtype, B, H, m, T):
+    u_s, u64, Ab32, Bb32, C32, D, x0 = _step_inputs(B, H, m, T, dtype, seed=B * 1000 + H * 10 + m + T)
+    x = f32dev(x0)
+    y = h3.ssm_step(to_dev(u_s, dtype), f32dev(Ab32), f32dev(Bb32), f32dev(C32), f32dev(D), x)
+    torch.cuda.synchronize()
+    ry, rx = oracle.recurrence(u64, cplx64(Ab32), cplx64(Bb32), cplx64(C32), D.astype(np.float64), x0=cplx64(x0))
+    assert rel_err(to_np64(y), ry) < TOL[dtype]
+    xg = cplx64(to_np64(x))
+    assert np.abs(xg - rx).max() / np.abs(rx).max() < 1e-5
+
+
+def test_ssm_step_chained_tokens_and_no_skip(h3):
+    """Eight one-token calls through the same state equal one call over eight
+    tokens, and both equal the recurrence (D absent)."""
+    B, H, m, T = 2, 40, 64, 8
+    u_s, u64, Ab32, Bb32, C32, _, x0 = _step_inputs(B, H, m, T, workloads.F32, seed=3)
+    args = (f32dev(Ab32), f32dev(Bb32), f32dev(C32), None)
+    u = f32dev(u_s)
+    x1 = f32dev(x0)
+    y_all = h3.ssm_step(u, *args, x1)
+    x2 = f32dev(x0)
+    y_one = torch.cat([h3.ssm_step(u[..., t].contiguous(), *args, x2).unsqueeze(-1) for t in range(T)], -1)
+    torch.cuda.synchronize()
+    ry, rx = oracle.recurrence(u64, cplx64(Ab32), cplx64(Bb32), cplx64(C32), None, x0=cplx64(x0))
+    assert rel_err(to_np64(y_all), ry) < 1e-5
+    assert rel_err(to_np64(y_one), ry) < 1e-5
+    assert rel_err(to_np64(x1), to_np64(x2)) < 1e-6
+
+
+def test_ssm_step_continues_statepass(h3):
+    """A prompt through state passing, then generation from its final state,
+    equals the recurrence over prompt + generated tokens."""
+    w = workloads.statepass_workload("t", 2, 6, 2048 + 16, 2048, workloads.F16, seed=9, dt_lo=1e-3,
+                                     dt_hi=1e-1)
+    Ab32, Bb32, Ab, Bb, C = _sp_inputs(w)
+    args = (f32dev(Ab32), f32dev(Bb32), f32dev(w.ssm.C), f32dev(w.D))
+    u = to_dev(w.u, w.dtype)
+    y1, xf = h3.statepass_conv(u[..., :2048].contiguous(), *args, 2048)
+    y2 = h3.ssm_step(u[..., 2048:].contiguous(), *args, xf)
+    torch.cuda.synchronize()
+    ry, rx = oracle.recurrence(w.u64, Ab, Bb, C, w.D.astype(np.float64))
+    assert rel_err(to_np64(torch.cat([y1, y2], -1)), ry) < 2e-2
+    assert rel_err(to_np64(y2), ry[..., 2048:]) < 2e-2
+
+
 def test_config3_full_size_sampled_rows(h3):
     w = workloads.config(3)
     Ab32, Bb32, Ab, Bb, C = _sp_inputs(w)

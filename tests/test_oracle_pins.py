@@ -211,6 +211,36 @@ def test_recurrence_equals_convolution_plus_initial_state_term():
     np.testing.assert_allclose(y1 - y0, free, atol=1e-11)
 
 
+def test_recurrence_token_by_token_and_final_state_closed_form():
+    """Step mode (generation) chains one-token recurrences through the state:
+    that must equal one pass over the whole sequence, and the final state must
+    equal its closed form x_{L-1} = Abar^L x0 + sum_i Abar^{L-1-i} Bbar u_i
+    (the unrolled recurrence of Sec. 2, written with explicit powers)."""
+    rng = np.random.default_rng(19)
+    H, m, L, Bn = 3, 5, 40, 2
+    A, B, C, dt = _rand_diag(rng, H, m)
+    D = rng.standard_normal(H)
+    Ab, Bb = oracle.zoh(A, B, dt)
+    u = rng.standard_normal((Bn, H, L))
+    x0 = rng.standard_normal((Bn, H, m)) + 1j * rng.standard_normal((Bn, H, m))
+    y, xf = oracle.recurrence(u, Ab, Bb, C, D, x0=x0)
+    x, ys = x0, []
+    for t in range(L):
+        yt, x = oracle.recurrence(u[..., t:t + 1], Ab, Bb, C, D, x0=x)
+        ys.append(yt)
+    np.testing.assert_allclose(np.concatenate(ys, -1), y, atol=1e-12)
+    np.testing.assert_allclose(x, xf, atol=1e-12)
+    i = np.arange(L)
+    pw = Ab[:, :, None] ** (L - 1 - i)[None, None, :]                  # (H, m, L)
+    closed = Ab[None] ** L * x0 + Bb[None] * np.einsum("hnl,bhl->bhn", pw, u)
+    np.testing.assert_allclose(xf, closed, atol=1e-11)
+    # an absent D is no skip term, in the recurrence and in state passing
+    y0, x0f = oracle.recurrence(u, Ab, Bb, C, None, x0=x0)
+    np.testing.assert_array_equal(y0, oracle.recurrence(u, Ab, Bb, C, np.zeros(H), x0=x0)[0])
+    np.testing.assert_allclose(y - y0, D[None, :, None] * u, atol=1e-12)
+    np.testing.assert_allclose(oracle.statepass(u, Ab, Bb, C, None, 8, x0=x0)[0], y0, atol=1e-10)
+
+
 def test_toy_diag_ssm_cumulative_sum_exact():
     """Appendix C.1 remark: a diagonal SSM with A = 1, B = 1 acts as a
     cumulative sum.  With complex-mode convention C = 1/2 gives 2 Re(C x) = x."""
