@@ -35,6 +35,7 @@ def lib():
         L.oracle_ssm_kernel.argtypes = [_dp, _dp, _dp, _dp, i, i, i, _dp]
         L.oracle_ssm_kernel_discrete.argtypes = [_dp, _dp, _dp, i, i, i, _dp]
         L.oracle_causal_conv.argtypes = [_dp, _dp, _dp, i, i, i, _dp]
+        L.oracle_causal_conv_bwd.argtypes = [_dp, _dp, _dp, _dp, i, i, i, _dp, _dp, _dp]
         L.oracle_ssm_recurrence.argtypes = [_dp, _dp, _dp, _dp, _dp, _dp, i, i, i, i, _dp, _dp]
         L.oracle_statepass.argtypes = [_dp, _dp, _dp, _dp, _dp, _dp, i, i, i, i, i, _dp, _dp]
         L.oracle_shift_ssm.argtypes = [_dp, _dp, _dp, i, i, i, i, _dp]
@@ -103,6 +104,23 @@ def causal_conv(u, k, D=None) -> np.ndarray:
     Dp = _r(D) if D is not None else None
     lib().oracle_causal_conv(_p(u), _p(k), _p(Dp), R, H, L, _p(y))
     return y
+
+
+def causal_conv_bwd(u, k, D, dy):
+    """Gradients of y = causal_conv(u, k, D) for output gradient dy, by their
+    definitions (backward-pass appendix): returns (du, dk, dD) with
+    du[b,h,t] = sum_{s>=t} k[h,s-t] dy[b,h,s] + D[h] dy[b,h,t],
+    dk[h,j] = sum_b sum_{t>=j} dy[b,h,t] u[b,h,t-j],  dD[h] = sum_{b,t} dy u."""
+    u = _r(u); k = _r(k); dy = _r(dy)
+    H, L = k.shape
+    assert u.shape == dy.shape and u.shape[-1] == L and u.shape[-2] == H
+    R = u.size // L
+    du = np.empty(u.shape, np.float64)
+    dk = np.empty((H, L), np.float64)
+    dD = np.empty(H, np.float64)
+    Dp = _r(D) if D is not None else None
+    lib().oracle_causal_conv_bwd(_p(u), _p(k), _p(Dp), _p(dy), R, H, L, _p(du), _p(dk), _p(dD))
+    return du, dk, dD
 
 
 # ------------------------------------------------------------------ S5 -----

@@ -12,6 +12,8 @@
  *   - ZOH discretisation of a diagonal SSM,
  *   - the SSM convolution kernel f = [CB, CAB, CA^2B, ...]     (Sec. 2.1),
  *   - the direct O(L^2) causal convolution y = f * u + D u     (Sec. 2.1),
+ *     and its gradients du, df, dD by their definitions (backward-pass
+ *     appendix),
  *   - the explicit recurrence x_i = A x_{i-1} + B u_i,
  *     y_i = C x_i + D u_i                                       (Sec. 2.1),
  *   - the state-passing algorithm (Sec. 4.2, Algorithm 2), used only to pin
@@ -123,6 +125,50 @@ void oracle_causal_conv(const double *u, const double *k, const double *D,
             for (int j = 0; j <= t; ++j) s += kh[j] * ur[t - j];
             if (D) s += D[h] * ur[t];
             yr[t] = s;
+        }
+    }
+}
+
+/*
+ * Gradients of the causal convolution y = f * u + D u (the backward pass of
+ * the appendix on FlashConv's backward), by their definitions: for a loss
+ * with output gradient dy,
+ *   du[r,t] = sum_{s=t}^{L-1} k[h,s-t] dy[r,s] + D[h] dy[r,t],
+ *   dk[h,j] = sum_{b} sum_{t=j}^{L-1} dy[b,h,t] u[b,h,t-j],
+ *   dD[h]   = sum_{b} sum_{t} dy[b,h,t] u[b,h,t],
+ * with rows r = b*H + h, R = B*H.  D may be NULL (no skip term in du); each
+ * of du, dk, dD may be NULL (not computed).
+ */
+void oracle_causal_conv_bwd(const double *u, const double *k, const double *D, const double *dy,
+                            int R, int H, int L, double *du, double *dk, double *dD)
+{
+    const int B = R / H;
+    if (du) {
+#pragma omp parallel for schedule(dynamic, 1)
+        for (int r = 0; r < R; ++r) {
+            int h = r % H;
+            const double *kh = k + (long)h * L, *g = dy + (long)r * L;
+            for (int t = 0; t < L; ++t) {
+                double s = 0.0;
+                for (int q = t; q < L; ++q) s += kh[q - t] * g[q];
+                if (D) s += D[h] * g[t];
+                du[(long)r * L + t] = s;
+            }
+        }
+    }
+    if (dk || dD) {
+#pragma omp parallel for schedule(dynamic, 1)
+        for (int h = 0; h < H; ++h) {
+            for (int j = 0; j < L; ++j) {
+                if (!dk && j > 0) break;
+                double s = 0.0;
+                for (int b = 0; b < B; ++b) {
+                    const double *ur = u + ((long)b * H + h) * L, *g = dy + ((long)b * H + h) * L;
+                    for (int t = j; t < L; ++t) s += g[t] * ur[t - j];
+                }
+                if (dk) dk[(long)h * L + j] = s;
+                if (j == 0 && dD) dD[h] = s;
+            }
         }
     }
 }

@@ -188,6 +188,64 @@ def test_conv_linear_time_invariant_causal():
     assert np.abs(yp[..., 120:] - y1[..., 120:]).max() > 0
 
 
+# --------------------------------------------------- conv backward pass -----
+def test_conv_bwd_adjoint_identity():
+    """The gradients are the adjoint of the (pinned) forward convolution:
+    <dy, conv(u, k, D)> = <du, u> = <dk, k> + <dD, D>  (the forward is
+    bilinear in u and (k, D))."""
+    rng = np.random.default_rng(31)
+    Bn, H, L = 3, 4, 96
+    u = rng.standard_normal((Bn, H, L)); k = rng.standard_normal((H, L)) / 8
+    D = rng.standard_normal(H); dy = rng.standard_normal((Bn, H, L))
+    y = oracle.causal_conv(u, k, D)
+    du, dk, dD = oracle.causal_conv_bwd(u, k, D, dy)
+    J = np.sum(dy * y)
+    assert abs(np.sum(du * u) - J) < 1e-10 * abs(J) + 1e-9
+    assert abs(np.sum(dk * k) + np.sum(dD * D) - J) < 1e-10 * abs(J) + 1e-9
+
+
+def test_conv_bwd_unit_perturbations():
+    """The forward is linear in each of u, k, D, so a unit change of one entry
+    changes J = <dy, y> by exactly the gradient at that entry."""
+    rng = np.random.default_rng(32)
+    Bn, H, L = 2, 3, 40
+    u = rng.standard_normal((Bn, H, L)); k = rng.standard_normal((H, L))
+    D = rng.standard_normal(H); dy = rng.standard_normal((Bn, H, L))
+    J0 = np.sum(dy * oracle.causal_conv(u, k, D))
+    du, dk, dD = oracle.causal_conv_bwd(u, k, D, dy)
+    for (b, h, t) in [(0, 0, 0), (1, 2, 39), (0, 1, 17), (1, 0, 5)]:
+        u2 = u.copy(); u2[b, h, t] += 1.0
+        assert abs(np.sum(dy * oracle.causal_conv(u2, k, D)) - J0 - du[b, h, t]) < 1e-9
+    for (h, j) in [(0, 0), (2, 39), (1, 11)]:
+        k2 = k.copy(); k2[h, j] += 1.0
+        assert abs(np.sum(dy * oracle.causal_conv(u, k2, D)) - J0 - dk[h, j]) < 1e-9
+    for h in range(H):
+        D2 = D.copy(); D2[h] += 1.0
+        assert abs(np.sum(dy * oracle.causal_conv(u, k, D2)) - J0 - dD[h]) < 1e-9
+    du0, _, _ = oracle.causal_conv_bwd(u, k, None, dy)      # no D: no skip term
+    np.testing.assert_allclose(du - du0, D[None, :, None] * dy, atol=1e-12)
+
+
+def test_conv_bwd_matches_autograd():
+    """Against reverse-mode differentiation (float64 CPU autograd) of the
+    convolution written as a 1-D correlation with the flipped kernel."""
+    import torch
+    rng = np.random.default_rng(33)
+    Bn, H, L = 2, 3, 33
+    u = torch.tensor(rng.standard_normal((Bn, H, L)), requires_grad=True)
+    k = torch.tensor(rng.standard_normal((H, L)), requires_grad=True)
+    D = torch.tensor(rng.standard_normal(H), requires_grad=True)
+    dy = rng.standard_normal((Bn, H, L))
+    # y[b,h,t] = sum_j k[h,j] u[b,h,t-j]: grouped conv1d over left-padded u
+    y = torch.nn.functional.conv1d(torch.nn.functional.pad(u, (L - 1, 0)), k.flip(-1).unsqueeze(1), groups=H)
+    y = y + D[None, :, None] * u
+    (y * torch.tensor(dy)).sum().backward()
+    du, dk, dD = oracle.causal_conv_bwd(u.detach().numpy(), k.detach().numpy(), D.detach().numpy(), dy)
+    np.testing.assert_allclose(du, u.grad.numpy(), atol=1e-11)
+    np.testing.assert_allclose(dk, k.grad.numpy(), atol=1e-11)
+    np.testing.assert_allclose(dD, D.grad.numpy(), atol=1e-11)
+
+
 # ----------------------------------------------------------- recurrence -----
 def test_recurrence_equals_convolution_plus_initial_state_term():
     """Sec. 2.1: from an initial state x0, y_t = (C Abar^{t+1} x0 term) +
