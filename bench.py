@@ -159,7 +159,7 @@ def _time_calls(fn, reps, warm):
     return a.elapsed_time(b) / reps
 
 
-EXTRA_KEYS = ("cfg1_shift", "cfg2", "cfg3", "cfg4", "cfg0", "step")
+EXTRA_KEYS = ("cfg1_shift", "cfg2", "cfg3", "cfg4", "cfg0", "step", "bwd")
 
 
 def bench_extra(h3, dev, reps=10, warm=3, only=None):
@@ -184,6 +184,8 @@ def bench_extra(h3, dev, reps=10, warm=3, only=None):
         _extra_cfg0(h3, dev, reps, warm, ex, np, torch, workloads)
     if want("step"):
         _extra_step(h3, dev, reps, warm, ex, np, torch, workloads)
+    if want("bwd"):
+        _extra_bwd(h3, dev, reps, warm, ex, np, torch, workloads)
     return ex
 
 
@@ -297,6 +299,30 @@ def _extra_cfg0(h3, dev, reps, warm, ex, np, torch, workloads):
     ms = _time_calls(lambda i: (h3.ssm_kernel(A, Bp, C, dt, w.L, out=k),
                                 h3.fftconv(u, k, D, out=y, workspace=ws)), 50, 5)
     ex["cfg0_f32_latency_us"] = ms * 1e3
+
+
+def _extra_bwd(h3, dev, reps, warm, ex, np, torch, workloads):
+    # backward pass of the fused conv at config 1's shape (B=8 H=768 L=2048,
+    # fp16): du, dk, dD for one output gradient; calls rotate over 6 input sets
+    # (u, dy, du: 75 MB each) so that they stream from HBM
+    w = workloads.config(1)
+    B, H, L, nset = w.B, w.H, w.L, 6
+    rng = np.random.default_rng(11)
+    k = torch.from_numpy((rng.standard_normal((H, L)) * np.exp(-np.arange(L) / 300.0)).astype(np.float32)).to(dev)
+    D = _f32(w.D, dev)
+    us = [torch.from_numpy(rng.standard_normal((B, H, L)).astype(np.float16)).to(dev) for _ in range(nset)]
+    dys = [torch.from_numpy(rng.standard_normal((B, H, L)).astype(np.float16)).to(dev) for _ in range(nset)]
+    ws = torch.empty(h3.workspace_size(h3.OP_FFTCONV, B, H, L, 0, 0, h3.F16), dtype=torch.uint8, device=dev)
+    ms_all = _time_calls(lambda i: h3.fftconv_bwd(us[i % nset], k, D, dys[i % nset], workspace=ws), 4 * nset, nset)
+    ms_du = _time_calls(lambda i: h3.fftconv_bwd(None, k, D, dys[i % nset], want_dk=False, want_dD=False,
+                                                 workspace=ws), 4 * nset, nset)
+    ms_dk = _time_calls(lambda i: h3.fftconv_bwd(us[i % nset], k, D, dys[i % nset], want_du=False, workspace=ws),
+                        4 * nset, nset)
+    io = B * H * L * 2
+    alg = 3 * io + 2 * H * L * 4 + 2 * H * 4   # u, dy read, du written; k read, dk written; D, dD
+    ex["bwd_cfg1_f16"] = {"us": ms_all * 1e3, "GB_s": alg / (ms_all * 1e-3) / 1e9,
+                          "pct_hbm_peak": 100 * alg / (ms_all * 1e-3) / 8e12, "bytes": alg,
+                          "du_us": ms_du * 1e3, "dk_dD_us": ms_dk * 1e3}
 
 
 def _extra_step(h3, dev, reps, warm, ex, np, torch, workloads):

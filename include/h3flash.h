@@ -140,6 +140,28 @@ int h3_statepass_conv(const void *u, const float *Abar, const float *Bbar,
                       void *workspace, size_t ws_bytes, void *stream);
 
 /*
+ * h3_fftconv_bwd — backward pass of the fused convolution (the appendix on
+ * FlashConv's backward pass): for y = h3_fftconv(u, k, D) and an output
+ * gradient dy,
+ *   du[b,h,t] = sum_{s>=t} k[h,s-t] dy[b,h,s] + D[h] dy[b,h,t]
+ *               (the same fused kernel with the conjugated kernel spectrum),
+ *   dk[h,j]   = sum_b sum_{t>=j} dy[b,h,t] u[b,h,t-j]
+ *               (Re IFFT of sum_b conj(F u_b) . F dy_b, one transform pair per
+ *               row pair and one inverse per channel),
+ *   dD[h]     = sum_{b,t} dy[b,h,t] u[b,h,t].
+ *   u, dy, du   (B, H, L) of `dtype`; u may be NULL when only du is asked.
+ *   k (H, L) float32; D (H) float32 or NULL (then du has no skip term).
+ *   dk (H, L) float32, dD (H) float32.  Each of du, dk, dD may be NULL (not
+ *   computed), not all three.  Outputs overlap no input, output or the
+ *   workspace.  L as for h3_fftconv.
+ *   workspace >= h3_workspace_size(H3_OP_FFTCONV, B, H, L, 0, 0, dtype).
+ * Errors: EINVAL, EUNSUPPORTED (L, dtype), EWORKSPACE, EDEVICE.
+ */
+int h3_fftconv_bwd(const void *u, const float *k, const float *D, const void *dy,
+                   int B, int H, int L, int dtype, void *du, float *dk, float *dD,
+                   void *workspace, size_t ws_bytes, void *stream);
+
+/*
  * h3_ssm_step — recurrent (step) mode of a diagonal SSM, for generation
  * (Sec. 2, the recurrent view; Sec. 5 generation): advances the carried state
  * over T new tokens per (b, h) row,

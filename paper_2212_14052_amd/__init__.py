@@ -19,7 +19,7 @@ import torch
 
 __all__ = [
     "H3Error", "lib", "ssm_discretize", "ssm_kernel", "fftconv", "statepass_conv",
-    "layer_fwd", "ssm_step", "kernel_spectrum", "fftconv_spectral", "workspace_size", "status_string", "F32", "F16", "BF16",
+    "layer_fwd", "ssm_step", "fftconv_bwd", "kernel_spectrum", "fftconv_spectral", "workspace_size", "status_string", "F32", "F16", "BF16",
     "OP_FFTCONV", "OP_STATEPASS", "OP_LAYER", "FUSED_LIMIT", "MAX_MODES",
 ]
 
@@ -60,12 +60,13 @@ def lib() -> ctypes.CDLL:
         L.h3_statepass_conv.argtypes = [vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, vp, vp, vp, sz, vp]
         L.h3_layer_fwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, vp, vp, sz, vp]
         L.h3_ssm_step.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, vp, vp, vp]
+        L.h3_fftconv_bwd.argtypes = [vp, vp, vp, vp, i, i, i, i, vp, vp, vp, vp, sz, vp]
         L.h3_workspace_size.argtypes = [i, i, i, i, i, i, i]
         L.h3_workspace_size.restype = sz
         L.h3_status_string.argtypes = [i]
         L.h3_status_string.restype = ctypes.c_char_p
         for fn in ("h3_ssm_discretize", "h3_ssm_kernel", "h3_fftconv", "h3_statepass_conv",
-                   "h3_layer_fwd", "h3_kernel_spectrum", "h3_fftconv_spectral", "h3_ssm_step"):
+                   "h3_layer_fwd", "h3_kernel_spectrum", "h3_fftconv_spectral", "h3_ssm_step", "h3_fftconv_bwd"):
             getattr(L, fn).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -204,6 +205,29 @@ def statepass_conv(u: torch.Tensor, Abar: torch.Tensor, Bbar: torch.Tensor, C: t
         _ptr(u), _ptr(Abar), _ptr(Bbar), _ptr(C), _ptr(D), _ptr(x0), Bn, H, L, m, chunk, dt,
         _ptr(y), _ptr(xf), _ptr(ws), ws.numel() * ws.element_size(), _stream(u.device)))
     return y, xf
+
+
+def fftconv_bwd(u: Optional[torch.Tensor], k: torch.Tensor, D: Optional[torch.Tensor], dy: torch.Tensor,
+                want_du: bool = True, want_dk: bool = True, want_dD: bool = True,
+                workspace: Optional[torch.Tensor] = None):
+    """Backward pass of fftconv for output gradient dy (B, H, L).  Returns
+    (du, dk, dD); an output not asked for is None."""
+    dy = dy.contiguous()
+    Bn, H, L = dy.shape
+    dt = _dtype(dy)
+    if u is not None:
+        u = u.contiguous()
+        if u.shape != dy.shape or u.dtype != dy.dtype:
+            raise ValueError("u must match dy in shape and dtype")
+    k, D = _f32(k), _f32(D)
+    du = torch.empty_like(dy) if want_du else None
+    dk = torch.empty((H, L), dtype=torch.float32, device=dy.device) if want_dk else None
+    dD = torch.empty((H,), dtype=torch.float32, device=dy.device) if want_dD else None
+    ws = _workspace(workspace_size(OP_FFTCONV, Bn, H, L, 0, 0, dt), dy.device, workspace)
+    _check("h3_fftconv_bwd", lib().h3_fftconv_bwd(
+        _ptr(u), _ptr(k), _ptr(D), _ptr(dy), Bn, H, L, dt, _ptr(du), _ptr(dk), _ptr(dD), _ptr(ws),
+        ws.numel() * ws.element_size(), _stream(dy.device)))
+    return du, dk, dD
 
 
 def ssm_step(u: torch.Tensor, Abar: torch.Tensor, Bbar: torch.Tensor, C: torch.Tensor,

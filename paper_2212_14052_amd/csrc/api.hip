@@ -148,6 +148,55 @@ int h3_fftconv(const void *u, const float *k, const float *D, void *y, int B, in
     return launched(launch_fftconv(a, s));
 }
 
+int h3_fftconv_bwd(const void *u, const float *k, const float *D, const void *dy, int B, int H, int L, int dtype,
+                   void *du, float *dk, float *dD, void *workspace, size_t ws_bytes, void *stream) {
+    if (!dy || !k || B < 1 || H < 1 || L < 1 || (!du && !dk && !dD)) return H3_EINVAL;
+    if ((dk || dD) && !u) return H3_EINVAL;
+    if (!dtype_ok(dtype) || !pow2_in(L, H3_MIN_LEN, H3_FUSED_LIMIT)) return H3_EUNSUPPORTED;
+    const size_t io = (size_t)B * H * L * esize(dtype), kb = (size_t)H * L * 4, db = (size_t)H * 4;
+    const size_t need = h3_workspace_size(H3_OP_FFTCONV, B, H, L, 0, 0, dtype);
+    if (!workspace || ws_bytes < need) return H3_EWORKSPACE;
+    if ((u && !aligned16(u)) || !aligned16(dy) || (du && !aligned16(du)) || !aligned16(k) || (dk && !aligned16(dk)) ||
+        ((uintptr_t)dD & 3) || !aligned16(workspace))
+        return H3_EINVAL;
+    // outputs overlap no input, no other output and not the workspace
+    const void *outs[3] = {du, dk, dD};
+    const size_t osz[3] = {io, kb, db};
+    for (int i = 0; i < 3; ++i) {
+        if (!outs[i]) continue;
+        if (overlap(outs[i], osz[i], u, io) || overlap(outs[i], osz[i], dy, io) || overlap(outs[i], osz[i], k, kb) ||
+            overlap(outs[i], osz[i], D, db) || overlap(outs[i], osz[i], workspace, need))
+            return H3_EINVAL;
+        for (int j = i + 1; j < 3; ++j)
+            if (outs[j] && overlap(outs[i], osz[i], outs[j], osz[j])) return H3_EINVAL;
+    }
+    if (overlap(workspace, need, u, io) || overlap(workspace, need, dy, io) || overlap(workspace, need, k, kb))
+        return H3_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e;
+    if (du) {
+        // du = dy correlated with k (+ D dy): the forward convolution with the
+        // conjugated kernel spectrum
+        ConvArgs a{};
+        a.u = dy; a.y = du; a.D = D;
+        a.B = B; a.H = H; a.L = L; a.nchunk = 1; a.pair_mode = 0; a.dtype = dtype;
+        a.conj_k = 1;
+        if (fftconv_wave_supported(L, dtype) || fftconv_wave16k_supported(L, dtype)) {
+            e = launch_fftconv_mfma(a, k, s);
+        } else {
+            float2 *Kspec = (float2 *)workspace;
+            e = launch_spectrum(k, H, L, Kspec, s);
+            if (e == hipSuccess) {
+                a.Kspec = Kspec;
+                e = launch_fftconv(a, s);
+            }
+        }
+        if (e != hipSuccess) return H3_EDEVICE;
+    }
+    if (dk || dD) return launched(launch_conv_wgrad(u, dy, B, H, L, dtype, dk, dD, s));
+    return launched(hipSuccess);
+}
+
 int h3_kernel_spectrum(const float *k, int H, int L, float *Kspec, void *stream) {
     if (!k || !Kspec || H < 1 || L < 1) return H3_EINVAL;
     if (!pow2_in(L, H3_MIN_LEN, H3_FUSED_LIMIT)) return H3_EUNSUPPORTED;

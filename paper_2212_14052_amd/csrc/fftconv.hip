@@ -135,6 +135,7 @@ __global__ __launch_bounds__(N / 16 >= 64 ? N / 16 : 64) void fftconv_kernel(Con
     for (int r = 0; r < 16; ++r) {
         const int f = tid + r * T;
         float2 kf = (f <= L) ? K[f] : cconj(K[N - f]);
+        if (a.conj_k) kf = cconj(kf);   // correlation (input gradient)
         v[r] = cconj(cmul(v[r], kf));
     }
     fft_second_from_regs<N>(X, tid, v);

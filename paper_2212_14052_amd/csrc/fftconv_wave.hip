@@ -288,9 +288,13 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
         float km = fmaxf(fmaxf((float)hmx.x, (float)hmx.y), fmaxf(-(float)hmn.x, -(float)hmn.y));
         km = wave_max(km);
         if (lane == 0) red[NW + w] = km;
+        // conjugated spectrum (correlation, the input gradient): flip the
+        // sign of every imaginary half
+        const uint32_t cj = a.conj_k ? 0x80000000u : 0u;
 #pragma unroll
         for (int t = 0; t < 4; ++t)
-            Ks[(4 * w + t) * 64 + lane] = make_uint4(dq[4 * t], dq[4 * t + 1], dq[4 * t + 2], dq[4 * t + 3]);
+            Ks[(4 * w + t) * 64 + lane] =
+                make_uint4(dq[4 * t] ^ cj, dq[4 * t + 1] ^ cj, dq[4 * t + 2] ^ cj, dq[4 * t + 3] ^ cj);
         __syncthreads();   // Ks complete
         e2 = __builtin_amdgcn_readfirstlane(
             exp_of(fmaxf(fmaxf(red[NW], red[NW + 1]), fmaxf(red[NW + 2], red[NW + 3]))));   // in [-6, 6]

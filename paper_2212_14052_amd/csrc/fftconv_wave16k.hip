@@ -690,6 +690,10 @@ __global__ __launch_bounds__(w16::NT) __attribute__((amdgpu_waves_per_eu(2))) vo
                 for (int jj = 0; jj < 4; ++jj) K[4 * tau + jj] = pk(re[jj], im[jj]);
             });
         }
+        if (a.conj_k) {   // conjugated spectrum (correlation, the input gradient)
+#pragma unroll
+            for (int i = 0; i < 64; ++i) K[i] ^= 0x80000000u;
+        }
         h2_t hmx = {0, 0}, hmn = {0, 0};
 #pragma unroll
         for (int i = 0; i < 64; i += 2) {

@@ -47,6 +47,10 @@ struct ConvArgs {
     // launch_corr_tables
     const uint4 *corr_tab;
     const int *corr_e;
+    // conj_k: convolve with the conjugated kernel spectrum, i.e. correlate:
+    // y[t] = sum_{s>=t} k[s-t] u[s] (+ D u[t]), the input gradient of the
+    // convolution.  Supported by the wave kernels and the VALU kernel.
+    int conj_k;
 };
 hipError_t launch_fftconv(const ConvArgs &a, hipStream_t s);
 // Matrix-core block-FFT variant (16-bit I/O, L = 2048): computes the kernel
@@ -63,6 +67,12 @@ hipError_t launch_fftconv_wave16k(const ConvArgs &a, const float *k, hipStream_t
 bool fftconv_wave16k_supported(int L, int dtype);
 
 size_t fftconv_workspace(int B, int H, int L);
+
+// Kernel and skip gradients of the convolution: dk[h, j] = sum_b sum_{t>=j}
+// dy[b,h,t] u[b,h,t-j] (float32 (H, L)), dD[h] = sum_{b,t} dy u (either may be
+// null).  u, dy (B, H, L) of dtype.
+hipError_t launch_conv_wgrad(const void *u, const void *dy, int B, int H, int L, int dtype, float *dk, float *dD,
+                             hipStream_t s);
 
 // State passing pieces.
 hipError_t launch_chunk_states(const void *u, const float *Abar, const float *Bbar, int B, int H,

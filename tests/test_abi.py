@@ -140,3 +140,23 @@ def test_step_validation():
     assert step(y=U) == EINVAL                       # y aliases u
     assert step(y=X + 64) == EINVAL                  # y inside the state
     assert step(x=K + 256) == EINVAL                 # state overlaps Abar
+
+
+def bwd(u=U, k=K, D=None, dy=X, B=2, H=4, L=64, dt=1, du=Y, dk=K + 0x100000, dD=None, ws=W, wsb=1 << 24):
+    return h3.lib().h3_fftconv_bwd(P(u), P(k), P(D), P(dy), B, H, L, dt, P(du), P(dk), P(dD), P(ws), wsb, None)
+
+
+def test_bwd_validation():
+    assert bwd(dy=0) == EINVAL
+    assert bwd(k=0) == EINVAL
+    assert bwd(du=0, dk=0, dD=0) == EINVAL            # nothing asked
+    assert bwd(u=0) == EINVAL                         # dk needs u
+    assert bwd(L=48) == EUNSUP
+    assert bwd(L=16384) == EUNSUP
+    assert bwd(dt=3) == EUNSUP
+    assert bwd(ws=0) == EWS
+    assert bwd(du=X) == EINVAL                        # du aliases dy
+    assert bwd(dk=K + 64) == EINVAL                   # dk overlaps k
+    assert bwd(dD=Y + 8) == EINVAL                    # dD inside du
+    assert bwd(dD=K + 0x100000 + 2) == EINVAL         # dD misaligned
+    assert bwd(du=U + 0x100000, ws=U + 0x100000 - 256) == EINVAL   # workspace overlaps du

@@ -196,6 +196,82 @@ def test_statepass_resume(h3):
     assert rel_err(to_np64(x2), to_np64(xf)) < 1e-5
 
 
+# ------------------------------------------------- conv backward pass ---
+def _bwd_case(h3, B, H, L, dtype, seed, with_D=True, sel=None):
+    w = workloads.conv_workload("t", B, H, L, dtype, seed=seed)
+    A, Bm, C, dt = _diag_params(w)
+    k32 = oracle.ssm_kernel(A, Bm, C, dt, L).astype(np.float32)
+    rng = np.random.default_rng(seed + 1)
+    dy_s, dy64 = workloads.round_to(rng.standard_normal((B, H, L)), dtype)
+    D = w.D if with_D else None
+    du, dk, dD = h3.fftconv_bwd(to_dev(w.u, dtype), f32dev(k32), f32dev(D) if with_D else None,
+                                to_dev(dy_s, dtype))
+    torch.cuda.synchronize()
+    du, dk, dD = to_np64(du), to_np64(dk), to_np64(dD)
+    h = np.arange(H) if sel is None else np.asarray(sel)
+    rdu, rdk, rdD = oracle.causal_conv_bwd(w.u64[:, h], k32[h].astype(np.float64),
+                                           D[h].astype(np.float64) if with_D else None, dy64[:, h])
+    return (du[:, h], rdu), (dk[h], rdk), (dD[h], rdD)
+
+
+# L = 16 .. 8192 covers every transform length of the kernel-gradient kernel
+# and, for 16-bit I/O at L = 2048 and 8192, the wave kernels with the
+# conjugated spectrum for du; odd batches leave the last row pair half empty.
+@pytest.mark.parametrize("dtype", [workloads.F32, workloads.F16, workloads.BF16])
+@pytest.mark.parametrize("B,H,L", [(1, 3, 16), (3, 5, 256), (2, 4, 1024), (5, 3, 2048), (4, 2, 8192)])
+def test_fftconv_bwd(h3, dtype, B, H, L):
+    (du, rdu), (dk, rdk), (dD, rdD) = _bwd_case(h3, B, H, L, dtype, seed=B * 7 + L)
+    assert rel_err(du, rdu) < TOL[dtype]
+    assert rel_err(dk, rdk) < 1e-5
+    assert rel_err(dD, rdD) < 1e-5
+
+
+def test_fftconv_bwd_no_skip_and_partial_outputs(h3):
+    B, H, L = 3, 4, 512
+    (du, rdu), (dk, rdk), _ = _bwd_case(h3, B, H, L, workloads.F32, seed=41, with_D=False)
+    assert rel_err(du, rdu) < 1e-5 and rel_err(dk, rdk) < 1e-5
+    w = workloads.conv_workload("t", B, H, L, workloads.F16, seed=42)
+    k = f32dev(np.random.default_rng(1).standard_normal((H, L)) / 16)
+    dy = to_dev(w.u, workloads.F16)
+    du_only, dk0, dD0 = h3.fftconv_bwd(None, k, None, dy, want_dk=False, want_dD=False)
+    _, dk_only, dD_only = h3.fftconv_bwd(dy, k, None, dy, want_du=False)
+    torch.cuda.synchronize()
+    assert dk0 is None and dD0 is None
+    rdu, rdk, rdD = oracle.causal_conv_bwd(w.u64, to_np64(k), None, w.u64)
+    assert rel_err(to_np64(du_only), rdu) < 2e-2
+    assert rel_err(to_np64(dk_only), rdk) < 1e-5
+    assert rel_err(to_np64(dD_only), rdD) < 1e-5
+
+
+def test_fftconv_bwd_config1_full_size_sampled_channels(h3):
+    """At the H3-125M layer shape (B=8, H=768, L=2048, fp16) on the launch
+    the benchmark times; sampled channels against the oracle."""
+    sel = [0, 1, 383, 500, 767]
+    (du, rdu), (dk, rdk), (dD, rdD) = _bwd_case(h3, 8, 768, 2048, workloads.F16, seed=5, sel=sel)
+    assert rel_err(du, rdu) < 2e-2
+    assert rel_err(dk, rdk) < 1e-5
+    assert rel_err(dD, rdD) < 1e-5
+
+
+def test_fftconv_bwd_adjoint_at_full_size(h3):
+    """<dy, conv(u)> = <du, u> at the fused-block limit (B=16 H=256 L=8192 bf16),
+    with the forward and backward both on the GPU."""
+    w = workloads.config(2)
+    A, Bm, C, dt = _diag_params(w)
+    k = h3.ssm_kernel(f32dev(w.ssm.A), f32dev(w.ssm.B), f32dev(w.ssm.C), f32dev(w.ssm.dt), w.L)
+    u = to_dev(w.u, w.dtype)
+    dy = to_dev(workloads.round_to(np.random.default_rng(3).standard_normal(w.u.shape), w.dtype)[0], w.dtype)
+    y = h3.fftconv(u, k, f32dev(w.D))
+    du, dk, dD = h3.fftconv_bwd(u, k, f32dev(w.D), dy)
+    torch.cuda.synchronize()
+    J1 = torch.sum(dy.double() * y.double()).item()
+    J2 = torch.sum(du.double() * u.double()).item()
+    J3 = (torch.sum(dk.double() * k.double()) + torch.sum(dD.double() * f32dev(w.D).double())).item()
+    scale = torch.sum((dy.double() * y.double()).abs()).item()
+    assert abs(J1 - J2) < 2e-2 * scale
+    assert abs(J1 - J3) < 2e-2 * scale
+
+
 # ------------------------------------------------- recurrent step mode ---
 def _step_inputs(B, H, m, T, dtype, seed):
     rng = np.random.default_rng(seed)
