@@ -312,7 +312,7 @@ def _extra_bwd(h3, dev, reps, warm, ex, np, torch, workloads):
     D = _f32(w.D, dev)
     us = [torch.from_numpy(rng.standard_normal((B, H, L)).astype(np.float16)).to(dev) for _ in range(nset)]
     dys = [torch.from_numpy(rng.standard_normal((B, H, L)).astype(np.float16)).to(dev) for _ in range(nset)]
-    ws = torch.empty(h3.workspace_size(h3.OP_FFTCONV, B, H, L, 0, 0, h3.F16), dtype=torch.uint8, device=dev)
+    ws = torch.empty(h3.workspace_size(h3.OP_FFTCONV_BWD, B, H, L, 0, 0, h3.F16), dtype=torch.uint8, device=dev)
     ms_all = _time_calls(lambda i: h3.fftconv_bwd(us[i % nset], k, D, dys[i % nset], workspace=ws), 4 * nset, nset)
     ms_du = _time_calls(lambda i: h3.fftconv_bwd(None, k, D, dys[i % nset], want_dk=False, want_dD=False,
                                                  workspace=ws), 4 * nset, nset)

@@ -46,7 +46,7 @@ typedef enum {
 typedef enum { H3_F32 = 0, H3_F16 = 1, H3_BF16 = 2 } h3_dtype;
 
 /* Operation codes for h3_workspace_size. */
-enum { H3_OP_FFTCONV = 1, H3_OP_STATEPASS = 2, H3_OP_LAYER = 3 };
+enum { H3_OP_FFTCONV = 1, H3_OP_STATEPASS = 2, H3_OP_LAYER = 3, H3_OP_FFTCONV_BWD = 4 };
 
 /* Limits of this build. */
 #define H3_MAX_MODES 64     /* m: complex modes per channel of a diagonal SSM      */
@@ -154,7 +154,7 @@ int h3_statepass_conv(const void *u, const float *Abar, const float *Bbar,
  *   dk (H, L) float32, dD (H) float32.  Each of du, dk, dD may be NULL (not
  *   computed), not all three.  Outputs overlap no input, output or the
  *   workspace.  L as for h3_fftconv.
- *   workspace >= h3_workspace_size(H3_OP_FFTCONV, B, H, L, 0, 0, dtype).
+ *   workspace >= h3_workspace_size(H3_OP_FFTCONV_BWD, B, H, L, 0, 0, dtype).
  * Errors: EINVAL, EUNSUPPORTED (L, dtype), EWORKSPACE, EDEVICE.
  */
 int h3_fftconv_bwd(const void *u, const float *k, const float *D, const void *dy,

@@ -20,14 +20,14 @@ import torch
 __all__ = [
     "H3Error", "lib", "ssm_discretize", "ssm_kernel", "fftconv", "statepass_conv",
     "layer_fwd", "ssm_step", "fftconv_bwd", "kernel_spectrum", "fftconv_spectral", "workspace_size", "status_string", "F32", "F16", "BF16",
-    "OP_FFTCONV", "OP_STATEPASS", "OP_LAYER", "FUSED_LIMIT", "MAX_MODES",
+    "OP_FFTCONV", "OP_STATEPASS", "OP_LAYER", "OP_FFTCONV_BWD", "FUSED_LIMIT", "MAX_MODES",
 ]
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libh3flash.so")
 
 F32, F16, BF16 = 0, 1, 2
-OP_FFTCONV, OP_STATEPASS, OP_LAYER = 1, 2, 3
+OP_FFTCONV, OP_STATEPASS, OP_LAYER, OP_FFTCONV_BWD = 1, 2, 3, 4
 FUSED_LIMIT = 8192
 MAX_MODES = 64
 
@@ -223,7 +223,7 @@ def fftconv_bwd(u: Optional[torch.Tensor], k: torch.Tensor, D: Optional[torch.Te
     du = torch.empty_like(dy) if want_du else None
     dk = torch.empty((H, L), dtype=torch.float32, device=dy.device) if want_dk else None
     dD = torch.empty((H,), dtype=torch.float32, device=dy.device) if want_dD else None
-    ws = _workspace(workspace_size(OP_FFTCONV, Bn, H, L, 0, 0, dt), dy.device, workspace)
+    ws = _workspace(workspace_size(OP_FFTCONV_BWD, Bn, H, L, 0, 0, dt), dy.device, workspace)
     _check("h3_fftconv_bwd", lib().h3_fftconv_bwd(
         _ptr(u), _ptr(k), _ptr(D), _ptr(dy), Bn, H, L, dt, _ptr(du), _ptr(dk), _ptr(dD), _ptr(ws),
         ws.numel() * ws.element_size(), _stream(dy.device)))

@@ -1,6 +1,7 @@
 // C ABI of libh3flash: argument validation and kernel dispatch.
 // Every check runs on the host before anything is enqueued.
 #include <stdint.h>
+#include <algorithm>
 #include <stdlib.h>
 #include <string.h>
 
@@ -89,6 +90,13 @@ size_t h3_workspace_size(int op, int B, int H, int L, int m, int chunk, int dtyp
             return statepass_ws(B, H, L, m, chunk).total;
         case H3_OP_LAYER:
             return layer_ws(B, H, L).total;
+        case H3_OP_FFTCONV_BWD: {
+            // the spectrum of the du pass, then (same bytes, later in stream
+            // order) the kernel-gradient partial sums
+            size_t n = align_up(fftconv_workspace(B, H, L));
+            if (fftconv_wave_supported(L, dtype)) n = std::max(n, align_up(wgrad_wave_workspace(B, H)));
+            return n;
+        }
     }
     return 0;
 }
@@ -154,7 +162,7 @@ int h3_fftconv_bwd(const void *u, const float *k, const float *D, const void *dy
     if ((dk || dD) && !u) return H3_EINVAL;
     if (!dtype_ok(dtype) || !pow2_in(L, H3_MIN_LEN, H3_FUSED_LIMIT)) return H3_EUNSUPPORTED;
     const size_t io = (size_t)B * H * L * esize(dtype), kb = (size_t)H * L * 4, db = (size_t)H * 4;
-    const size_t need = h3_workspace_size(H3_OP_FFTCONV, B, H, L, 0, 0, dtype);
+    const size_t need = h3_workspace_size(H3_OP_FFTCONV_BWD, B, H, L, 0, 0, dtype);
     if (!workspace || ws_bytes < need) return H3_EWORKSPACE;
     if ((u && !aligned16(u)) || !aligned16(dy) || (du && !aligned16(du)) || !aligned16(k) || (dk && !aligned16(dk)) ||
         ((uintptr_t)dD & 3) || !aligned16(workspace))
@@ -193,7 +201,13 @@ int h3_fftconv_bwd(const void *u, const float *k, const float *D, const void *dy
         }
         if (e != hipSuccess) return H3_EDEVICE;
     }
-    if (dk || dD) return launched(launch_conv_wgrad(u, dy, B, H, L, dtype, dk, dD, s));
+    if (dk || dD) {
+        const char *sel = getenv("H3FLASH_WGRAD");   // "valu": the float32 VALU kernel at every length
+        const bool valu = sel && strcmp(sel, "valu") == 0;
+        if (!valu && fftconv_wave_supported(L, dtype))
+            return launched(launch_wgrad_wave(u, dy, B, H, dtype, dk, dD, workspace, s));
+        return launched(launch_conv_wgrad(u, dy, B, H, L, dtype, dk, dD, s));
+    }
     return launched(hipSuccess);
 }
 

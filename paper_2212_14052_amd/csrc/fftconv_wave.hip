@@ -445,7 +445,316 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
     }
 }
 
+// ============================================================================
+// Kernel gradient of the convolution at L = 2048, 16-bit I/O (the appendix on
+// the backward pass): dk[h] = Re IFFT( sum_b conj(F u_b) . F dy_b )[:L], with
+// rows paired as above (the real part of the pair product is the sum of the two
+// rows' correlations; the cross terms land in the imaginary part), and
+// dD[h] = sum_{b,t} u dy = dk[h][0].
+//
+// One workgroup per channel.  Each wave takes row pairs q = w, w + 4, ...:
+// the forward transform of the u pair (as in the convolution, through L3) is
+// kept in packed fp16; the forward transform of the dy pair ends in an L3
+// epilogue that forms conj(Zu) . Zdy in float32 from the matrix-core outputs,
+// undoes both inputs' power-of-two scales and adds it into a float32 spectrum
+// in LDS (LDS float atomics; the four waves add in any order).  Wave 0 then
+// normalises the summed spectrum to a power of two, runs the inverse of the
+// convolution (L3^H, swap, conj twiddle, L2^H, L1^H) and writes dk in float32.
+// Scales: the forward leaves F(z) 2^-e / 64 (three matrices carrying 1/4), so
+// the accumulated spectrum is S = sum conj(F z_u) F z_dy / 4096; with S scaled
+// by 2^-es the inverse returns 64 IFFT(S 2^-es), hence dk = Re(out) 2^(es + 6).
+namespace wv {
+
+// Raw 16-bit loads of a row pair (layout of the convolution's loads); rows
+// past the batch read as zero.
+__device__ __forceinline__ void load_pair_raw(const uint16_t *x, long oa, long ob, int g, int c, uint4 (&ra)[8],
+                                              uint4 (&rb)[8]) {
+    const long obl = ob >= 0 ? ob : oa;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        ra[i] = make_uint4(0, 0, 0, 0);
+        rb[i] = make_uint4(0, 0, 0, 0);
+    }
+    if (g < 2) {
+        const uint16_t *xa = x + oa, *xb = x + obl;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int off = 256 * (4 * g + j) + 16 * c;
+            ra[2 * j] = *(const uint4 *)(xa + off);
+            ra[2 * j + 1] = *(const uint4 *)(xa + off + 8);
+            rb[2 * j] = *(const uint4 *)(xb + off);
+            rb[2 * j + 1] = *(const uint4 *)(xb + off + 8);
+        }
+    }
+    if (ob < 0) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) rb[i] = make_uint4(0, 0, 0, 0);
+    }
+}
+
+// Pack a raw pair into the complex signal d = (a + i b) 2^-e (load layout of
+// the transform), e the power of two that brings max |x| below 1 (0 when the
+// fp16 values need no scaling).  Returns e (wave-uniform).
+template <int DT>
+__device__ __forceinline__ int pack_pair(const uint4 (&ra)[8], const uint4 (&rb)[8], uint32_t (&d)[64]) {
+    uint32_t mb = 0;
+    float mx;
+    if (DT == F16) {
+        h2_t hmx = {0, 0}, hmn = {0, 0};
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const uint32_t v[8] = {ra[i].x, ra[i].y, ra[i].z, ra[i].w, rb[i].x, rb[i].y, rb[i].z, rb[i].w};
+#pragma unroll
+            for (int e = 0; e < 8; e += 2) {
+                hmx = __builtin_elementwise_maximum(hmx, __builtin_elementwise_maximum(as_h2(v[e]), as_h2(v[e + 1])));
+                hmn = __builtin_elementwise_minimum(hmn, __builtin_elementwise_minimum(as_h2(v[e]), as_h2(v[e + 1])));
+            }
+        }
+        mx = fmaxf(fmaxf((float)hmx.x, (float)hmx.y), fmaxf(-(float)hmn.x, -(float)hmn.y));
+    } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const uint32_t v[8] = {ra[i].x, ra[i].y, ra[i].z, ra[i].w, rb[i].x, rb[i].y, rb[i].z, rb[i].w};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const uint32_t m = v[e] & 0x7fff7fffu;
+                mb = max(mb, max(m & 0xffffu, m >> 16));
+            }
+        }
+        mx = __uint_as_float(mb << 16);
+    }
+    mx = wave_max(mx);
+    int eu = 0;
+    if (DT == BF16 || !(mx >= 0.0625f && mx < 16.0f)) eu = exp_of(mx);
+    eu = __builtin_amdgcn_readfirstlane(eu);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+            const uint4 va = ra[2 * j + hf], vb = rb[2 * j + hf];
+            const uint32_t A4[4] = {va.x, va.y, va.z, va.w}, B4[4] = {vb.x, vb.y, vb.z, vb.w};
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const int T = 8 * hf + 2 * s;
+                if (DT == F16) {
+                    d[4 * T + j] = __builtin_amdgcn_perm(B4[s], A4[s], 0x05040100u);
+                    d[4 * (T + 1) + j] = __builtin_amdgcn_perm(B4[s], A4[s], 0x07060302u);
+                } else {
+                    d[4 * T + j] = pk(ldexpf(lo_f<DT>(A4[s]), -eu), ldexpf(lo_f<DT>(B4[s]), -eu));
+                    d[4 * (T + 1) + j] = pk(ldexpf(hi_f<DT>(A4[s]), -eu), ldexpf(hi_f<DT>(B4[s]), -eu));
+                }
+            }
+        }
+    }
+    if (DT == F16 && eu != 0) {
+        const _Float16 sc = (_Float16)ldexpf(1.0f, -eu);
+        const h2_t s2 = {sc, sc};
+#pragma unroll
+        for (int i = 0; i < 64; ++i) d[i] = as_u32(as_h2(d[i]) * s2);
+    }
+    // packing complete here: the raw registers are dead before the transform
+#pragma unroll
+    for (int i = 0; i < 64; ++i) asm volatile("" : "+v"(d[i]));
+    return eu;
+}
+
+}  // namespace wv
+
+template <int DT>
+__global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(2))) void wgrad_wave4096_kernel(
+    const uint16_t *u, const uint16_t *dy, int B, int H, int ngroup, float *dk, float *dD) {
+    using namespace wv;
+    __shared__ uint4 Tab[kTab];
+    // summed spectrum, planar (re, im), index (tau * 4 + jj) * 64 + lane (lanes
+    // on consecutive banks); then the dk staging buffer
+    __shared__ float S[2 * kN];
+    uint4 *Ytab = Tab, *Lc = Tab + kTabY;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = lane >> 4, c = lane & 15;
+    const int h = blockIdx.x / ngroup, grp = blockIdx.x % ngroup;
+    const int npairs = (B + 1) / 2;
+    const int qq = NW * grp + w;   // this wave's row pair (at most one)
+    const bool have = qq < npairs;
+#pragma unroll
+    for (int r = 0; r < (kTab + NT - 1) / NT; ++r) {
+        const int base = r * NT + 64 * w;
+        if (base < kTab)
+            __builtin_amdgcn_global_load_lds((gvoid_t *)((const uint4 *)kHalf.v + base + lane),
+                                             (lvoid_t *)(Tab + base), 16, 0, 0);
+    }
+    uint4 ra[8], rb[8];
+    uint32_t d[64], zu[64];
+    const long oa = ((long)(2 * qq) * H + h) * L;
+    const long ob = (2 * qq + 1 < B) ? oa + (long)H * L : -1;
+    if (have) load_pair_raw(u, oa, ob, g, c, ra, rb);
+    __builtin_amdgcn_s_waitcnt(kWaitVm0);
+    __syncthreads();   // tables
+    int ep = 0;
+    if (have) {
+        const int eu = pack_pair<DT>(ra, rb, d);
+        forward_front(d, Lc, Ytab, lane);
+        load_pair_raw(dy, oa, ob, g, c, ra, rb);   // in flight during the u transform's last layer
+        layer<false>(d, lds_dft(Lc, lane, false), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) zu[4 * tau + jj] = pk(re[jj], im[jj]);
+        });
+        const int eg = pack_pair<DT>(ra, rb, d);
+        forward_front(d, Lc, Ytab, lane);
+        // conj(Zu) . Zdy in float32 from the matrix-core outputs, packed back
+        // into zu at 2^-7 (both transforms are below 1448 in modulus, so the
+        // product stays below 2^14)
+        layer<false>(d, lds_dft(Lc, lane, false), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const h2_t a = as_h2(zu[4 * tau + jj]);
+                const float ar = (float)a.x, ai = (float)a.y;
+                zu[4 * tau + jj] = pk((ar * re[jj] + ai * im[jj]) * 0.0078125f, (ar * im[jj] - ai * re[jj]) * 0.0078125f);
+            }
+        });
+        ep = eu + eg + 7;
+    }
+    // the waves add their products into S in turn (wave 0 stores), scaled
+    // back by 2^ep: S = sum conj(F z_u) F z_dy / 4096
+    const float sc = ldexpf(1.0f, ep);
+#pragma unroll 1
+    for (int turn = 0; turn < NW; ++turn) {
+        if (w == turn && (have || turn == 0)) {
+#pragma unroll
+            for (int i = 0; i < 64; ++i) {
+                const int si = i * 64 + lane;   // i = 4 tau + jj
+                const h2_t p = as_h2(zu[i]);
+                const float pr = have ? (float)p.x * sc : 0.f, pi = have ? (float)p.y * sc : 0.f;
+                if (turn == 0) {
+                    S[si] = pr;
+                    S[kN + si] = pi;
+                } else {
+                    S[si] += pr;
+                    S[kN + si] += pi;
+                }
+            }
+        }
+        __syncthreads();
+    }
+    if (w != 0) return;   // no barrier below: wave 0 alone runs the inverse
+
+    float mx = 0.f;
+#pragma unroll
+    for (int i = 0; i < 64; ++i) mx = fmaxf(mx, fmaxf(fabsf(S[i * 64 + lane]), fabsf(S[kN + i * 64 + lane])));
+    mx = wave_max(mx);
+    const int es = __builtin_amdgcn_readfirstlane(exp_of(mx));
+#pragma unroll
+    for (int tau = 0; tau < 16; ++tau)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+            const int si = (4 * tau + jj) * 64 + lane;
+            d[4 * tau + jj] = pk(ldexpf(S[si], -es), ldexpf(S[kN + si], -es));
+        }
+    // the inverse of the convolution
+    layer<false>(d, lds_dft(Lc, lane, true), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) d[4 * tau + jj] = pk(re[jj], im[jj]);
+    });
+    swap_GT(d);
+    {
+        uint32_t e[64];
+#pragma unroll
+        for (int T = 0; T < 16; ++T) {
+            const uint4 yv = Ytab[T * 64 + lane];
+            e[4 * T + 0] = cmulc(d[pidx(T, 0)], yv.x);
+            e[4 * T + 1] = cmulc(d[pidx(T, 1)], yv.y);
+            e[4 * T + 2] = cmulc(d[pidx(T, 2)], yv.z);
+            e[4 * T + 3] = cmulc(d[pidx(T, 3)], yv.w);
+        }
+#pragma unroll
+        for (int i = 0; i < 64; ++i) d[i] = e[i];
+    }
+    {
+        const uint4 X = Lc[4 * 64 + lane], Xs = Lc[5 * 64 + lane];
+        const uint32_t xw[4] = {X.x, X.y, X.z, X.w}, xs[4] = {Xs.x, Xs.y, Xs.z, Xs.w};
+        layer<true>(d, lds_dft(Lc, lane, true), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) d[4 * tau + jj] = cmulc2(pk(re[jj], im[jj]), xw[jj], xs[jj]);
+        });
+    }
+    // L1^H: lane (g < 2, c), tile tau, element i holds t = 256 (4 g + i) + 16 c + tau;
+    // the real part is dk.  Staged through LDS (S is free) for coalesced stores.
+    float *stage = S;
+    const float osc = ldexpf(1.0f, es + 6);
+    layer<false>(d, lds_dft(Lc, lane, true), NoPre{}, [&](int tau, f4_t re, f4_t, uint4) {
+        if (g < 2) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) stage[256 * (4 * g + i) + 16 * c + tau] = re[i] * osc;
+        }
+    });
+    // other lanes' staging writes visible before the reads (one wave: no barrier)
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+    // group grp's share: rows grp H + h of dk and dD (ngroup = 1: the outputs)
+    float *dkh = dk + ((long)grp * H + h) * L;
+#pragma unroll
+    for (int r = 0; r < L / 256; ++r) {
+        const int t = 256 * r + 4 * lane;
+        if (dk) *(float4 *)(dkh + t) = *(const float4 *)(stage + t);
+    }
+    if (lane == 0 && dD) dD[(long)grp * H + h] = stage[0];
+}
+
 bool fftconv_wave_supported(int L, int dtype) { return L == wv::L && (dtype == F16 || dtype == BF16); }
+
+// partial sums of the workgroup groups of a channel
+__global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float *pk_, const float *pd, int ngroup, int H,
+                                                           float *dk, float *dD) {
+    const long n = (long)H * wv::L / 4;
+    const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (dk && i < n) {
+        float4 acc = ((const float4 *)pk_)[i];
+        for (int gi = 1; gi < ngroup; ++gi) {
+            const float4 v = ((const float4 *)pk_)[(long)gi * n + i];
+            acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+        }
+        ((float4 *)dk)[i] = acc;
+    }
+    if (dD && i < H) {
+        float a = 0.f;
+        for (int gi = 0; gi < ngroup; ++gi) a += pd[(long)gi * H + i];
+        dD[i] = a;
+    }
+}
+
+int wgrad_wave_groups(int B) { return ((B + 1) / 2 + wv::NW - 1) / wv::NW; }
+
+size_t wgrad_wave_workspace(int B, int H) {
+    const int ng = wgrad_wave_groups(B);
+    if (ng <= 1) return 0;
+    return (size_t)ng * H * wv::L * sizeof(float) + (size_t)ng * H * sizeof(float);
+}
+
+hipError_t launch_wgrad_wave(const void *u, const void *dy, int B, int H, int dtype, float *dk, float *dD,
+                             void *ws, hipStream_t s) {
+    if (dtype != F16 && dtype != BF16) return hipErrorInvalidValue;
+    const int ng = wgrad_wave_groups(B);
+    float *pk_ = dk, *pd = dD;
+    if (ng > 1) {   // partial sums per group in the workspace, then one reduction
+        if (!ws) return hipErrorInvalidValue;
+        pk_ = dk ? (float *)ws : nullptr;
+        pd = dD ? (float *)ws + (size_t)ng * H * wv::L : nullptr;
+    }
+    const dim3 grid(H * ng), block(wv::NT);
+    if (dtype == F16)
+        hipLaunchKernelGGL(wgrad_wave4096_kernel<F16>, grid, block, 0, s, (const uint16_t *)u, (const uint16_t *)dy,
+                           B, H, ng, pk_, pd);
+    else
+        hipLaunchKernelGGL(wgrad_wave4096_kernel<BF16>, grid, block, 0, s, (const uint16_t *)u, (const uint16_t *)dy,
+                           B, H, ng, pk_, pd);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || ng == 1) return e;
+    const long n = (long)H * wv::L / 4;
+    hipLaunchKernelGGL(wgrad_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, pk_, pd, ng, H, dk,
+                       dD);
+    return hipGetLastError();
+}
 
 hipError_t launch_fftconv_wave(const ConvArgs &a, const float *k, hipStream_t s) {
     if (!fftconv_wave_supported(a.L, a.dtype)) return hipErrorInvalidValue;

@@ -73,6 +73,13 @@ size_t fftconv_workspace(int B, int H, int L);
 // null).  u, dy (B, H, L) of dtype.
 hipError_t launch_conv_wgrad(const void *u, const void *dy, int B, int H, int L, int dtype, float *dk, float *dD,
                              hipStream_t s);
+// The same on the matrix cores at L = 2048, 16-bit I/O (fftconv_wave_supported):
+// one workgroup per channel and group of four row pairs; with more than one
+// group per channel the partial sums go to ws (wgrad_wave_workspace bytes)
+// and a reduction kernel writes dk, dD.
+hipError_t launch_wgrad_wave(const void *u, const void *dy, int B, int H, int dtype, float *dk, float *dD,
+                             void *ws, hipStream_t s);
+size_t wgrad_wave_workspace(int B, int H);
 
 // State passing pieces.
 hipError_t launch_chunk_states(const void *u, const float *Abar, const float *Bbar, int B, int H,

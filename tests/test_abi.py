@@ -46,6 +46,10 @@ def test_workspace_sizes():
     assert h3.workspace_size(99, 1, 1, 16, 0, 0, 0) == 0
     assert h3.workspace_size(h3.OP_FFTCONV, 1, 1, 16, 0, 0, 7) == 0
     assert h3.workspace_size(h3.OP_LAYER, 4, 2560, 2048, 64, 0, h3.BF16) > 4 * 2560 * 2048 * 2 * 5
+    # backward: at least the conv's spectrum; with more than four row pairs per
+    # channel at L = 2048 (16-bit) also the kernel-gradient partial sums
+    assert h3.workspace_size(h3.OP_FFTCONV_BWD, 8, 768, 2048, 0, 0, h3.F16) >= 768 * 2049 * 8
+    assert h3.workspace_size(h3.OP_FFTCONV_BWD, 32, 768, 2048, 0, 0, h3.F16) >= 4 * 768 * 2048 * 4
 
 
 def fftconv(u=U, k=K, D=None, y=Y, B=2, H=4, L=64, dt=0, ws=W, wsb=1 << 24):

@@ -216,11 +216,28 @@ def _bwd_case(h3, B, H, L, dtype, seed, with_D=True, sel=None):
 
 # L = 16 .. 8192 covers every transform length of the kernel-gradient kernel
 # and, for 16-bit I/O at L = 2048 and 8192, the wave kernels with the
-# conjugated spectrum for du; odd batches leave the last row pair half empty.
+# conjugated spectrum for du; odd batches leave the last row pair half empty;
+# B = 19 at L = 2048 gives three workgroup groups per channel on the matrix
+# cores (partial sums and their reduction).
 @pytest.mark.parametrize("dtype", [workloads.F32, workloads.F16, workloads.BF16])
-@pytest.mark.parametrize("B,H,L", [(1, 3, 16), (3, 5, 256), (2, 4, 1024), (5, 3, 2048), (4, 2, 8192)])
+@pytest.mark.parametrize("B,H,L", [(1, 3, 16), (3, 5, 256), (2, 4, 1024), (5, 3, 2048), (4, 2, 8192),
+                                   (19, 3, 2048)])
 def test_fftconv_bwd(h3, dtype, B, H, L):
     (du, rdu), (dk, rdk), (dD, rdD) = _bwd_case(h3, B, H, L, dtype, seed=B * 7 + L)
+    assert rel_err(du, rdu) < TOL[dtype]
+    # dk, dD: float32 outputs; on the matrix cores (16-bit I/O at L = 2048) the
+    # transforms run on fp16 operands, so the 16-bit tolerance applies there
+    tol_k = TOL[dtype] if (L == 2048 and dtype != workloads.F32) else 1e-5
+    assert rel_err(dk, rdk) < tol_k
+    assert rel_err(dD, rdD) < tol_k
+
+
+@pytest.mark.parametrize("dtype", [workloads.F16, workloads.BF16])
+def test_fftconv_bwd_valu_kernel_gradient_at_2048(h3, monkeypatch, dtype):
+    """The float32 VALU kernel-gradient kernel forced where the matrix-core one
+    runs by default (L = 2048, 16-bit I/O)."""
+    monkeypatch.setenv("H3FLASH_WGRAD", "valu")
+    (du, rdu), (dk, rdk), (dD, rdD) = _bwd_case(h3, 3, 4, 2048, dtype, seed=77)
     assert rel_err(du, rdu) < TOL[dtype]
     assert rel_err(dk, rdk) < 1e-5
     assert rel_err(dD, rdD) < 1e-5
@@ -239,7 +256,7 @@ def test_fftconv_bwd_no_skip_and_partial_outputs(h3):
     assert dk0 is None and dD0 is None
     rdu, rdk, rdD = oracle.causal_conv_bwd(w.u64, to_np64(k), None, w.u64)
     assert rel_err(to_np64(du_only), rdu) < 2e-2
-    assert rel_err(to_np64(dk_only), rdk) < 1e-5
+    assert rel_err(to_np64(dk_only), rdk) < 1e-5   # L = 512: float32 VALU kernel
     assert rel_err(to_np64(dD_only), rdD) < 1e-5
 
 
@@ -249,8 +266,8 @@ def test_fftconv_bwd_config1_full_size_sampled_channels(h3):
     sel = [0, 1, 383, 500, 767]
     (du, rdu), (dk, rdk), (dD, rdD) = _bwd_case(h3, 8, 768, 2048, workloads.F16, seed=5, sel=sel)
     assert rel_err(du, rdu) < 2e-2
-    assert rel_err(dk, rdk) < 1e-5
-    assert rel_err(dD, rdD) < 1e-5
+    assert rel_err(dk, rdk) < 2e-2
+    assert rel_err(dD, rdD) < 2e-2
 
 
 def test_fftconv_bwd_adjoint_at_full_size(h3):
