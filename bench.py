@@ -159,7 +159,7 @@ def _time_calls(fn, reps, warm):
     return a.elapsed_time(b) / reps
 
 
-EXTRA_KEYS = ("cfg1_shift", "cfg2", "cfg3", "cfg4", "cfg0", "step", "bwd")
+EXTRA_KEYS = ("cfg1_shift", "cfg2", "cfg3", "cfg4", "cfg0", "step", "bwd", "heads")
 
 
 def bench_extra(h3, dev, reps=10, warm=3, only=None):
@@ -186,6 +186,8 @@ def bench_extra(h3, dev, reps=10, warm=3, only=None):
         _extra_step(h3, dev, reps, warm, ex, np, torch, workloads)
     if want("bwd"):
         _extra_bwd(h3, dev, reps, warm, ex, np, torch, workloads)
+    if want("heads"):
+        _extra_heads(h3, dev, reps, warm, ex, np, torch, workloads)
     return ex
 
 
@@ -285,6 +287,26 @@ def _extra_cfg4(h3, dev, reps, warm, ex, np, torch, workloads):
     flops = 2.0 * B * L * d * d * 4
     ex["cfg4_layer_bf16"] = {"ms": ms, "gemm_TFLOP_s": flops / ms / 1e9,
                              "pct_mfma_bf16_peak": 100 * flops / ms / 1e9 / MFMA_BF16_PEAK_TFLOPS}
+
+
+def _extra_heads(h3, dev, reps, warm, ex, np, torch, workloads):
+    # config 4's layer with heads of dimension 8 (pure H3): d d_h = 20480
+    # diagonal-SSM channels of length 2048 per batch row
+    w = workloads.config(4)
+    B, L, d, dh = w.B, w.L, w.d, 8
+    x = _dev_tensor(w.x, w.dtype, dev)
+    W = {n: _dev_tensor(w.weight_out_in(n), w.dtype, dev) for n in "qkvo"}
+    ssm = workloads.make_diag_ssm(np.random.default_rng(12), d * dh, 64, 1e-3, 1e-1)
+    dk = h3.ssm_kernel(_f32(ssm.A, dev), _f32(ssm.B, dev), _f32(ssm.C, dev), _f32(ssm.dt, dev), L)
+    dD = _f32(np.random.default_rng(13).standard_normal(d * dh), dev)
+    sC = _f32(w.shift_C, dev)
+    out = torch.empty_like(x)
+    ws = torch.empty(h3.workspace_size(h3.OP_LAYER_HEADS, B, d, L, 64, dh, h3.BF16), dtype=torch.uint8, device=dev)
+    ms = _time_calls(lambda i: h3.layer_fwd_heads(x, W["q"], W["k"], W["v"], W["o"], sC, None, dk, dD, dh,
+                                                  out=out, workspace=ws), reps, warm)
+    flops = 2.0 * B * L * d * d * 4
+    ex["layer_heads8_bf16"] = {"ms": ms, "d_head": dh, "gemm_TFLOP_s_of_total_time": flops / ms / 1e9,
+                               "ssm_rows": B * d * dh}
 
 
 def _extra_cfg0(h3, dev, reps, warm, ex, np, torch, workloads):

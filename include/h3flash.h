@@ -46,7 +46,7 @@ typedef enum {
 typedef enum { H3_F32 = 0, H3_F16 = 1, H3_BF16 = 2 } h3_dtype;
 
 /* Operation codes for h3_workspace_size. */
-enum { H3_OP_FFTCONV = 1, H3_OP_STATEPASS = 2, H3_OP_LAYER = 3, H3_OP_FFTCONV_BWD = 4 };
+enum { H3_OP_FFTCONV = 1, H3_OP_STATEPASS = 2, H3_OP_LAYER = 3, H3_OP_FFTCONV_BWD = 4, H3_OP_LAYER_HEADS = 5 };
 
 /* Limits of this build. */
 #define H3_MAX_MODES 64     /* m: complex modes per channel of a diagonal SSM      */
@@ -210,9 +210,31 @@ int h3_layer_fwd(const void *x, const void *Wq, const void *Wk, const void *Wv,
                  void *workspace, size_t ws_bytes, void *stream);
 
 /*
+ * h3_layer_fwd_heads — H3 layer forward with heads of dimension d_head
+ * (Sec. 3.2, Algorithm 1; pure H3 uses d_head = 8): Q, K, V, Kbar as for
+ * h3_layer_fwd; per head h (channels h d_head .. h d_head + d_head - 1) and
+ * token t the outer product KV_t[i][j] = Kbar_t[h d_head + i] V_t[h d_head + j]
+ * passes through the diagonal SSM of channel c = (h d_head + i) d_head + j,
+ *   S[c] = diag_k[c] (*) KV[i][j] + diag_D[c] KV[i][j]   (causal conv),
+ * the head's output is O_t[h d_head + j] = sum_i Q_t[h d_head + i] S_t[c], and
+ * out = O Wo^T.
+ *   Arguments as for h3_layer_fwd, except diag_k (d d_head, L) float32 and
+ *   diag_D (d d_head) or NULL.  d_head in {1, 2, 4, 8} (1 is h3_layer_fwd);
+ *   for d_head > 1, L is a power of two in [64, H3_FUSED_LIMIT].
+ *   workspace >= h3_workspace_size(H3_OP_LAYER_HEADS, B, d, L, m_s, d_head, dtype).
+ * Errors: EINVAL, EUNSUPPORTED (L, d, d_head, m_s, dtype), EWORKSPACE, EDEVICE.
+ */
+int h3_layer_fwd_heads(const void *x, const void *Wq, const void *Wk, const void *Wv,
+                       const void *Wo, const float *shift_C, const float *shift_D,
+                       const float *diag_k, const float *diag_D,
+                       int B, int L, int d, int d_head, int m_s, int dtype, void *out,
+                       void *workspace, size_t ws_bytes, void *stream);
+
+/*
  * h3_workspace_size — bytes of workspace an operation needs (0 if the
  * arguments are invalid).  H_or_d is H for the convolutions, d for the layer;
- * m is the mode count (state passing) or the shift length (layer).
+ * m is the mode count (state passing) or the shift length (layer); chunk is
+ * the chunk length (state passing) or the head dimension (H3_OP_LAYER_HEADS).
  */
 size_t h3_workspace_size(int op, int B, int H_or_d, int L, int m, int chunk, int dtype);
 

@@ -19,15 +19,15 @@ import torch
 
 __all__ = [
     "H3Error", "lib", "ssm_discretize", "ssm_kernel", "fftconv", "statepass_conv",
-    "layer_fwd", "ssm_step", "fftconv_bwd", "kernel_spectrum", "fftconv_spectral", "workspace_size", "status_string", "F32", "F16", "BF16",
-    "OP_FFTCONV", "OP_STATEPASS", "OP_LAYER", "OP_FFTCONV_BWD", "FUSED_LIMIT", "MAX_MODES",
+    "layer_fwd", "layer_fwd_heads", "ssm_step", "fftconv_bwd", "kernel_spectrum", "fftconv_spectral", "workspace_size", "status_string", "F32", "F16", "BF16",
+    "OP_FFTCONV", "OP_STATEPASS", "OP_LAYER", "OP_FFTCONV_BWD", "OP_LAYER_HEADS", "FUSED_LIMIT", "MAX_MODES",
 ]
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libh3flash.so")
 
 F32, F16, BF16 = 0, 1, 2
-OP_FFTCONV, OP_STATEPASS, OP_LAYER, OP_FFTCONV_BWD = 1, 2, 3, 4
+OP_FFTCONV, OP_STATEPASS, OP_LAYER, OP_FFTCONV_BWD, OP_LAYER_HEADS = 1, 2, 3, 4, 5
 FUSED_LIMIT = 8192
 MAX_MODES = 64
 
@@ -61,12 +61,14 @@ def lib() -> ctypes.CDLL:
         L.h3_layer_fwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, vp, vp, sz, vp]
         L.h3_ssm_step.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, vp, vp, vp]
         L.h3_fftconv_bwd.argtypes = [vp, vp, vp, vp, i, i, i, i, vp, vp, vp, vp, sz, vp]
+        L.h3_layer_fwd_heads.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, vp, vp, sz, vp]
         L.h3_workspace_size.argtypes = [i, i, i, i, i, i, i]
         L.h3_workspace_size.restype = sz
         L.h3_status_string.argtypes = [i]
         L.h3_status_string.restype = ctypes.c_char_p
         for fn in ("h3_ssm_discretize", "h3_ssm_kernel", "h3_fftconv", "h3_statepass_conv",
-                   "h3_layer_fwd", "h3_kernel_spectrum", "h3_fftconv_spectral", "h3_ssm_step", "h3_fftconv_bwd"):
+                   "h3_layer_fwd", "h3_kernel_spectrum", "h3_fftconv_spectral", "h3_ssm_step", "h3_fftconv_bwd",
+                   "h3_layer_fwd_heads"):
             getattr(L, fn).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -228,6 +230,29 @@ def fftconv_bwd(u: Optional[torch.Tensor], k: torch.Tensor, D: Optional[torch.Te
         _ptr(u), _ptr(k), _ptr(D), _ptr(dy), Bn, H, L, dt, _ptr(du), _ptr(dk), _ptr(dD), _ptr(ws),
         ws.numel() * ws.element_size(), _stream(dy.device)))
     return du, dk, dD
+
+
+def layer_fwd_heads(x: torch.Tensor, Wq: torch.Tensor, Wk: torch.Tensor, Wv: torch.Tensor,
+                    Wo: torch.Tensor, shift_C: torch.Tensor, shift_D: Optional[torch.Tensor],
+                    diag_k: torch.Tensor, diag_D: Optional[torch.Tensor], d_head: int,
+                    out: Optional[torch.Tensor] = None,
+                    workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """H3 layer forward with heads of dimension d_head (Algorithm 1).  x: (B, L, d);
+    weights (out, in); diag_k (d d_head, L), diag_D (d d_head)."""
+    x = x.contiguous()
+    Bn, L, d = x.shape
+    dt = _dtype(x)
+    Ws = [w.to(x.dtype).contiguous() for w in (Wq, Wk, Wv, Wo)]
+    shift_C = _f32(shift_C)
+    m_s = shift_C.shape[1]
+    shift_D, diag_k, diag_D = _f32(shift_D), _f32(diag_k), _f32(diag_D)
+    o = out if out is not None else torch.empty_like(x)
+    ws = _workspace(workspace_size(OP_LAYER_HEADS, Bn, d, L, m_s, d_head, dt), x.device, workspace)
+    _check("h3_layer_fwd_heads", lib().h3_layer_fwd_heads(
+        _ptr(x), *[_ptr(w) for w in Ws], _ptr(shift_C), _ptr(shift_D), _ptr(diag_k),
+        _ptr(diag_D), Bn, L, d, d_head, m_s, dt, _ptr(o), _ptr(ws), ws.numel() * ws.element_size(),
+        _stream(x.device)))
+    return o
 
 
 def ssm_step(u: torch.Tensor, Abar: torch.Tensor, Bbar: torch.Tensor, C: torch.Tensor,

@@ -65,6 +65,60 @@ LayerWs layer_ws(int B, int d, int L) {
     return w;
 }
 
+// Layer heads with d_h > 1: Q, K, V, Kbar, the outer products G and their
+// convolutions S (d_h rows per channel), O token-major, the spectra for the
+// VALU convolution, the GEMM algorithm workspace.
+struct HeadsWs {
+    size_t qkv, kbar, g, sv, o_tm, kspec, gemm, total;
+};
+HeadsWs heads_ws(int B, int d, int L, int dh) {
+    HeadsWs w;
+    const size_t act = (size_t)B * d * L * 2;
+    w.qkv = 0;
+    w.kbar = w.qkv + align_up(3 * act);
+    w.g = w.kbar + align_up(act);
+    w.sv = w.g + align_up((size_t)dh * act);
+    w.o_tm = w.sv + align_up((size_t)dh * act);
+    w.kspec = w.o_tm + align_up(act);
+    w.gemm = w.kspec + align_up((size_t)d * dh * (L + 1) * sizeof(float2));
+    w.total = w.gemm + kLayerGemmWs;
+    return w;
+}
+
+bool gemm_native() {
+    const char *gsel = getenv("H3FLASH_GEMM");
+    return gsel && strcmp(gsel, "native") == 0;
+}
+
+// [Q;K;V] channel-major: per projection j and batch b the (d, L) block
+// j B d L + b d L is W_j (d, d) . x_b (L, d)^T, both operands contiguous along
+// the reduction (weights are stored (out, in)).  hipBLASLt, or the library's
+// GEMM where hipBLASLt rejects the shape or H3FLASH_GEMM=native.
+hipError_t layer_qkv(const void *x, const void *Wq, const void *Wk, const void *Wv, char *qkv, int B, int L, int d,
+                     int dtype, void *gws, hipStream_t s) {
+    const size_t act = (size_t)B * L * d * 2;
+    const void *Wqkv[3] = {Wq, Wk, Wv};
+    const bool native = gemm_native();
+    for (int j = 0; j < 3; ++j) {
+        hipError_t e = native ? hipErrorNotSupported
+                              : launch_gemm_lt(Wqkv[j], true, x, true, qkv + j * act, d, L, d, B, 0, (long)L * d,
+                                               (long)d * L, dtype, gws, kLayerGemmWs, s);
+        if (e == hipErrorNotSupported) e = launch_gemm_nt(Wqkv[j], x, qkv + j * act, d, B * L, d, dtype, 1, d, L, s);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+// out = O (M, K) . Wo (N, K)^T with O token-major (B L, d)
+hipError_t layer_out(const void *o_tm, const void *Wo, void *out, int B, int L, int d, int dtype, void *gws,
+                     hipStream_t s) {
+    hipError_t e = gemm_native() ? hipErrorNotSupported
+                                 : launch_gemm_lt(o_tm, true, Wo, true, out, B * L, d, d, 1, 0, 0, 0, dtype, gws,
+                                                  kLayerGemmWs, s);
+    if (e == hipErrorNotSupported) e = launch_gemm_nt(o_tm, Wo, out, B * L, d, d, dtype, 0, d, L, s);
+    return e;
+}
+
 }  // namespace
 
 extern "C" {
@@ -90,6 +144,10 @@ size_t h3_workspace_size(int op, int B, int H, int L, int m, int chunk, int dtyp
             return statepass_ws(B, H, L, m, chunk).total;
         case H3_OP_LAYER:
             return layer_ws(B, H, L).total;
+        case H3_OP_LAYER_HEADS:   // chunk = head dimension
+            if (chunk == 1) return layer_ws(B, H, L).total;
+            if (chunk != 2 && chunk != 4 && chunk != 8) return 0;
+            return heads_ws(B, H, L, chunk).total;
         case H3_OP_FFTCONV_BWD: {
             // the spectrum of the du pass, then (same bytes, later in stream
             // order) the kernel-gradient partial sums
@@ -337,20 +395,8 @@ int h3_layer_fwd(const void *x, const void *Wq, const void *Wk, const void *Wv, 
     void *o_tm = ws + w.o_tm;
     float2 *Kspec = (float2 *)(ws + w.kspec);
     hipError_t e;
-    // [Q;K;V] channel-major: per projection j and batch b the (d, L) block
-    // j B d L + b d L is W_j (d, d) . x_b (L, d)^T, both operands contiguous
-    // along the reduction (weights are stored (out, in)).
     void *gws = ws + w.gemm;
-    const void *Wqkv[3] = {Wq, Wk, Wv};
-    const char *gsel = getenv("H3FLASH_GEMM");
-    const bool native = gsel && strcmp(gsel, "native") == 0;
-    for (int j = 0; j < 3; ++j) {
-        e = native ? hipErrorNotSupported
-                   : launch_gemm_lt(Wqkv[j], true, x, true, qkv + j * act, d, L, d, B, 0, (long)L * d, (long)d * L,
-                                    dtype, gws, kLayerGemmWs, s);
-        if (e == hipErrorNotSupported) e = launch_gemm_nt(Wqkv[j], x, qkv + j * act, d, B * L, d, dtype, 1, d, L, s);
-        if (e != hipSuccess) return H3_EDEVICE;
-    }
+    if ((e = layer_qkv(x, Wq, Wk, Wv, qkv, B, L, d, dtype, gws, s)) != hipSuccess) return H3_EDEVICE;
     const char *q = qkv, *kk = qkv + act, *v = qkv + 2 * act;
     if (fftconv_mfma_supported(L, dtype) && L % 64 == 0) {
         // G = (shift SSM of K) * V  ->  o_cm;  S = diag conv of G (+ D G)  ->  K's slot (K is dead);
@@ -370,11 +416,60 @@ int h3_layer_fwd(const void *x, const void *Wq, const void *Wk, const void *Wv, 
         // O (B, d, L) -> (B, L, d)
         if ((e = launch_transpose_batched(o_cm, o_tm, B, d, L, s)) != hipSuccess) return H3_EDEVICE;
     }
-    // out = O (M, K) . Wo (N, K)^T
-    e = native ? hipErrorNotSupported
-               : launch_gemm_lt(o_tm, true, Wo, true, out, B * L, d, d, 1, 0, 0, 0, dtype, gws, kLayerGemmWs, s);
-    if (e == hipErrorNotSupported) return launched(launch_gemm_nt(o_tm, Wo, out, B * L, d, d, dtype, 0, d, L, s));
-    return e == hipSuccess ? launched(hipSuccess) : H3_EDEVICE;
+    return launched(layer_out(o_tm, Wo, out, B, L, d, dtype, gws, s));
+}
+
+int h3_layer_fwd_heads(const void *x, const void *Wq, const void *Wk, const void *Wv, const void *Wo,
+                       const float *shift_C, const float *shift_D, const float *diag_k, const float *diag_D, int B,
+                       int L, int d, int d_head, int m_s, int dtype, void *out, void *workspace, size_t ws_bytes,
+                       void *stream) {
+    if (d_head == 1)
+        return h3_layer_fwd(x, Wq, Wk, Wv, Wo, shift_C, shift_D, diag_k, diag_D, B, L, d, m_s, dtype, out, workspace,
+                            ws_bytes, stream);
+    if (!x || !Wq || !Wk || !Wv || !Wo || !shift_C || !diag_k || !out || B < 1 || L < 1 || d < 1 || m_s < 1 ||
+        d_head < 1)
+        return H3_EINVAL;
+    if ((dtype != H3_F16 && dtype != H3_BF16) || !pow2_in(L, 64, H3_FUSED_LIMIT) || d % 128 != 0 ||
+        ((long)B * L) % 128 != 0 || m_s > H3_MAX_SHIFT || (d_head != 2 && d_head != 4 && d_head != 8))
+        return H3_EUNSUPPORTED;
+    const size_t need = h3_workspace_size(H3_OP_LAYER_HEADS, B, d, L, m_s, d_head, dtype);
+    if (!workspace || ws_bytes < need) return H3_EWORKSPACE;
+    if (!aligned16(x) || !aligned16(out) || !aligned16(Wq) || !aligned16(Wk) || !aligned16(Wv) ||
+        !aligned16(Wo) || !aligned16(workspace))
+        return H3_EINVAL;
+    const size_t act = (size_t)B * L * d * 2;
+    if (overlap(x, act, out, act) || overlap(workspace, need, x, act) || overlap(workspace, need, out, act))
+        return H3_EINVAL;
+    const size_t wbytes = (size_t)d * d * 2;
+    for (const void *W : {Wq, Wk, Wv, Wo})
+        if (overlap(W, wbytes, out, act) || overlap(W, wbytes, workspace, need)) return H3_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    const HeadsWs w = heads_ws(B, d, L, d_head);
+    char *ws = (char *)workspace;
+    char *qkv = ws + w.qkv;
+    void *kbar = ws + w.kbar, *g = ws + w.g, *sv = ws + w.sv, *o_tm = ws + w.o_tm, *gws = ws + w.gemm;
+    float2 *Kspec = (float2 *)(ws + w.kspec);
+    const char *q = qkv, *kk = qkv + act, *v = qkv + 2 * act;
+    hipError_t e;
+    if ((e = layer_qkv(x, Wq, Wk, Wv, qkv, B, L, d, dtype, gws, s)) != hipSuccess) return H3_EDEVICE;
+    // Kbar = shift SSM of K (no gating); G = per-head outer products of Kbar and V
+    if ((e = launch_shift_gate(kk, nullptr, shift_C, shift_D, m_s, B, d, L, dtype, kbar, s)) != hipSuccess)
+        return H3_EDEVICE;
+    if ((e = launch_heads_expand(d_head, kbar, v, g, B, d, L, dtype, s)) != hipSuccess) return H3_EDEVICE;
+    // S = diagonal SSM of every (h, i, j) row: the fused convolution over d d_h channels
+    ConvArgs ca{};
+    ca.u = g; ca.y = sv; ca.D = diag_D;
+    ca.B = B; ca.H = d * d_head; ca.L = L; ca.nchunk = 1; ca.pair_mode = 0; ca.dtype = dtype;
+    if (fftconv_mfma_supported(L, dtype)) {
+        if ((e = launch_fftconv_mfma(ca, diag_k, s)) != hipSuccess) return H3_EDEVICE;
+    } else {
+        if ((e = launch_spectrum(diag_k, d * d_head, L, Kspec, s)) != hipSuccess) return H3_EDEVICE;
+        ca.Kspec = Kspec;
+        if ((e = launch_fftconv(ca, s)) != hipSuccess) return H3_EDEVICE;
+    }
+    // O_t[j] = sum_i Q_t[i] S_t[i][j], token-major; out = O Wo^T
+    if ((e = launch_heads_contract(d_head, q, sv, o_tm, B, d, L, dtype, s)) != hipSuccess) return H3_EDEVICE;
+    return launched(layer_out(o_tm, Wo, out, B, L, d, dtype, gws, s));
 }
 
 }  // extern "C"

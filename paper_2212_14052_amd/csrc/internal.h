@@ -107,7 +107,8 @@ hipError_t launch_transpose_batched(const void *in, void *out, int nb, int R, in
 // O (B, L, d) token-major = (Q * S)^T per batch slice, Q and S (B, d, L); R = d, C = L.
 hipError_t launch_gate_transpose(const void *q, const void *sv, void *out, int nb, int R, int C, int dtype,
                                  hipStream_t s);
-// G = (shift FIR of K + shift_D K) * V over (B, d, L) rows (m_s <= 64, L % 16 == 0).
+// G = (shift FIR of K + shift_D K) * V over (B, d, L) rows (m_s <= 64, L % 16 == 0);
+// v null: G = the shift FIR of K alone.
 hipError_t launch_shift_gate(const void *k, const void *v, const float *shift_C, const float *shift_D, int m_s,
                              int B, int d, int L, int dtype, void *g, hipStream_t s);
 // hipBLASLt GEMM, C (M, N) row-major = A . B with A given as (M, K)
@@ -118,6 +119,13 @@ hipError_t launch_shift_gate(const void *k, const void *v, const float *shift_C,
 // launch_gemm_nt); ws / ws_bytes: workspace slice for the algorithm.
 hipError_t launch_gemm_lt(const void *A, bool a_kc, const void *B, bool b_kc, void *C, int M, int N, int K, int batch,
                           long sa, long sb, long sc, int dtype, void *ws, size_t ws_bytes, hipStream_t s);
+// Heads of dimension dh in {2, 4, 8} (d % 64 == 0, L % 64 == 0): the outer
+// products G (B, d dh, L) of Kbar and V, and their contraction with Q into
+// O (B, L, d) token-major.
+hipError_t launch_heads_expand(int dh, const void *kbar, const void *v, void *g, int B, int d, int L, int dtype,
+                               hipStream_t s);
+hipError_t launch_heads_contract(int dh, const void *q, const void *sv, void *o, int B, int d, int L, int dtype,
+                                 hipStream_t s);
 hipError_t launch_gemm_nt(const void *A, const void *Bt, void *C, int M, int N, int K, int dtype,
                           int out_mode, int d, int L, hipStream_t s);
 hipError_t launch_layer_mid(const void *q, const void *k, const void *v, const float *shift_C,

@@ -312,7 +312,8 @@ __global__ __launch_bounds__(256) void transpose_tile_kernel(const uint16_t *in,
 // consecutive outputs.  The taps are wave-uniform (scalar registers); the
 // thread's window K[t0 - 63 .. t0 + 15] comes from the row staged in LDS.
 constexpr int SG_T = 128, SG_R = 16, SG_TILE = SG_T * SG_R;
-template <int DT>
+// GATE false: Kbar itself (no V), for heads of dimension > 1.
+template <int DT, bool GATE>
 __global__ __launch_bounds__(SG_T) void shift_gate_kernel(const uint16_t *k, const uint16_t *v,
                                                           const float *shift_C, const float *shift_D,
                                                           int m_s, int d, int L, uint16_t *g) {
@@ -331,7 +332,7 @@ __global__ __launch_bounds__(SG_T) void shift_gate_kernel(const uint16_t *k, con
     const long o = row * L + min(tt + t0, L - SG_R);
     uint4 vpre[SG_R / 8];
 #pragma unroll
-    for (int h = 0; h < SG_R / 8; ++h) vpre[h] = *(const uint4 *)(v + o + 8 * h);
+    for (int h = 0; h < SG_R / 8; ++h) vpre[h] = GATE ? *(const uint4 *)(v + o + 8 * h) : make_uint4(0, 0, 0, 0);
     constexpr int NKS = (64 + SG_TILE) / 8;   // 16-byte pieces of the window
     constexpr int PER = (NKS + SG_T - 1) / SG_T;
     uint4 kw[PER];
@@ -398,8 +399,11 @@ __global__ __launch_bounds__(SG_T) void shift_gate_kernel(const uint16_t *k, con
         uint32_t o4[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const float lo = acc[8 * h + 2 * e] * (DT == BF16 ? bf16_to_f32(v4[e] & 0xffffu) : f16_to_f32(v4[e] & 0xffffu));
-            const float hi = acc[8 * h + 2 * e + 1] * (DT == BF16 ? bf16_to_f32(v4[e] >> 16) : f16_to_f32(v4[e] >> 16));
+            float lo = acc[8 * h + 2 * e], hi = acc[8 * h + 2 * e + 1];
+            if (GATE) {
+                lo *= DT == BF16 ? bf16_to_f32(v4[e] & 0xffffu) : f16_to_f32(v4[e] & 0xffffu);
+                hi *= DT == BF16 ? bf16_to_f32(v4[e] >> 16) : f16_to_f32(v4[e] >> 16);
+            }
             o4[e] = (uint32_t)(DT == BF16 ? f32_to_bf16(lo) : f32_to_f16(lo)) |
                     ((uint32_t)(DT == BF16 ? f32_to_bf16(hi) : f32_to_f16(hi)) << 16);
         }
@@ -434,7 +438,7 @@ __device__ __forceinline__ float sg_f(uint32_t h16) {
     return DT == BF16 ? bf16_to_f32(h16) : f16_to_f32(h16);
 }
 constexpr int SGM_W = 4;   // waves (channels) per workgroup
-template <int DT>
+template <int DT, bool GATE>
 __global__ __launch_bounds__(64 * SGM_W) void shift_gate_mfma_kernel(const uint16_t *k, const uint16_t *v,
                                                                       const float *shift_C, const float *shift_D,
                                                                       int m_s, int B, int d, int L, uint16_t *g) {
@@ -456,7 +460,7 @@ __global__ __launch_bounds__(64 * SGM_W) void shift_gate_mfma_kernel(const uint1
 #pragma unroll
         for (int kc = 0; kc < 4; ++kc) Bf[kc] = *(const uint4 *)(k + ro + max(64 * (a - 1) + 32 * kc + 8 * kg, 0));
 #pragma unroll
-        for (int rb = 0; rb < 4; ++rb) Vq[rb] = *(const uint2 *)(v + ro + 64 * a + 16 * rb + 4 * kg);
+        for (int rb = 0; rb < 4; ++rb) Vq[rb] = GATE ? *(const uint2 *)(v + ro + 64 * a + 16 * rb + 4 * kg) : make_uint2(0, 0);
     };
     issue(0);   // in flight while the Toeplitz fragments are built
     taps[w][lane] = lane < m_s ? shift_C[(long)c * m_s + lane] : 0.f;
@@ -502,8 +506,11 @@ __global__ __launch_bounds__(64 * SGM_W) void shift_gate_mfma_kernel(const uint1
             f4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int q = 0; q < 3; ++q) acc = sg_mfma<DT>(Af[rb][q], B4[(rb < 2 ? 0 : 1) + q], acc);
-            const float g0 = acc[0] * sg_f<DT>(V4[rb].x & 0xffffu), g1 = acc[1] * sg_f<DT>(V4[rb].x >> 16);
-            const float g2 = acc[2] * sg_f<DT>(V4[rb].y & 0xffffu), g3 = acc[3] * sg_f<DT>(V4[rb].y >> 16);
+            float g0 = acc[0], g1 = acc[1], g2 = acc[2], g3 = acc[3];
+            if (GATE) {
+                g0 *= sg_f<DT>(V4[rb].x & 0xffffu); g1 *= sg_f<DT>(V4[rb].x >> 16);
+                g2 *= sg_f<DT>(V4[rb].y & 0xffffu); g3 *= sg_f<DT>(V4[rb].y >> 16);
+            }
             *(uint2 *)(g + ro + 64 * a + 16 * rb + 4 * kg) = make_uint2(sg_pack<DT>(g0, g1), sg_pack<DT>(g2, g3));
         }
     }
@@ -630,23 +637,20 @@ hipError_t launch_shift_gate(const void *k, const void *v, const float *shift_C,
                              int B, int d, int L, int dtype, void *g, hipStream_t s) {
     if (m_s > 64 || L % 16 != 0) return hipErrorInvalidValue;
     const long rows = (long)B * d;
+    const bool gate = v != nullptr;
+    const uint16_t *k16 = (const uint16_t *)k, *v16 = (const uint16_t *)v;
+    uint16_t *g16 = (uint16_t *)g;
     if (L % 1024 == 0) {
-        const int grid = (d + SGM_W - 1) / SGM_W;
-        if (dtype == BF16)
-            hipLaunchKernelGGL(shift_gate_mfma_kernel<BF16>, dim3(grid), dim3(64 * SGM_W), 0, s,
-                               (const uint16_t *)k, (const uint16_t *)v, shift_C, shift_D, m_s, B, d, L, (uint16_t *)g);
-        else
-            hipLaunchKernelGGL(shift_gate_mfma_kernel<F16>, dim3(grid), dim3(64 * SGM_W), 0, s,
-                               (const uint16_t *)k, (const uint16_t *)v, shift_C, shift_D, m_s, B, d, L, (uint16_t *)g);
+        const dim3 grid((d + SGM_W - 1) / SGM_W), block(64 * SGM_W);
+        auto fn = dtype == BF16 ? (gate ? shift_gate_mfma_kernel<BF16, true> : shift_gate_mfma_kernel<BF16, false>)
+                                : (gate ? shift_gate_mfma_kernel<F16, true> : shift_gate_mfma_kernel<F16, false>);
+        hipLaunchKernelGGL(fn, grid, block, 0, s, k16, v16, shift_C, shift_D, m_s, B, d, L, g16);
         return hipGetLastError();
     }
     const long grid = rows * ((L + SG_TILE - 1) / SG_TILE);
-    if (dtype == BF16)
-        hipLaunchKernelGGL(shift_gate_kernel<BF16>, dim3((unsigned)grid), dim3(SG_T), 0, s, (const uint16_t *)k,
-                           (const uint16_t *)v, shift_C, shift_D, m_s, d, L, (uint16_t *)g);
-    else
-        hipLaunchKernelGGL(shift_gate_kernel<F16>, dim3((unsigned)grid), dim3(SG_T), 0, s, (const uint16_t *)k,
-                           (const uint16_t *)v, shift_C, shift_D, m_s, d, L, (uint16_t *)g);
+    auto fn = dtype == BF16 ? (gate ? shift_gate_kernel<BF16, true> : shift_gate_kernel<BF16, false>)
+                            : (gate ? shift_gate_kernel<F16, true> : shift_gate_kernel<F16, false>);
+    hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(SG_T), 0, s, k16, v16, shift_C, shift_D, m_s, d, L, g16);
     return hipGetLastError();
 }
 

@@ -164,3 +164,23 @@ def test_bwd_validation():
     assert bwd(dD=Y + 8) == EINVAL                    # dD inside du
     assert bwd(dD=K + 0x100000 + 2) == EINVAL         # dD misaligned
     assert bwd(du=U + 0x100000, ws=U + 0x100000 - 256) == EINVAL   # workspace overlaps du
+
+
+def heads(x=U, B=2, L=64, d=128, dh=2, m_s=64, dt=2, out=Y, ws=W, wsb=1 << 28, diag=K + 65536):
+    return h3.lib().h3_layer_fwd_heads(P(x), P(K), P(K), P(K), P(K), P(K), None, P(diag), None,
+                                       B, L, d, dh, m_s, dt, P(out), P(ws), wsb, None)
+
+
+def test_layer_heads_validation():
+    assert heads(x=0) == EINVAL
+    assert heads(dh=3) == EUNSUP
+    assert heads(dh=16) == EUNSUP
+    assert heads(L=32) == EUNSUP                     # heads need L >= 64
+    assert heads(dt=1, d=100) == EUNSUP
+    assert heads(ws=0) == EWS
+    assert heads(wsb=1 << 20) == EWS
+    assert heads(out=U) == EINVAL
+    assert h3.workspace_size(h3.OP_LAYER_HEADS, 4, 2560, 2048, 64, 8, h3.BF16) > 4 * 2560 * 2048 * 2 * 16
+    assert h3.workspace_size(h3.OP_LAYER_HEADS, 4, 2560, 2048, 64, 3, h3.BF16) == 0
+    assert (h3.workspace_size(h3.OP_LAYER_HEADS, 4, 2560, 2048, 64, 1, h3.BF16)
+            == h3.workspace_size(h3.OP_LAYER, 4, 2560, 2048, 64, 0, h3.BF16))

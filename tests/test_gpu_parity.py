@@ -429,6 +429,31 @@ def test_layer_native_gemm(h3, monkeypatch, L):
     assert rel_err(y, ref) < 2e-2
 
 
+# Heads of dimension d_h > 1: d_h^2 diagonal-SSM channels per head, each
+# with its own kernel; L = 2048 and 8192 take the wave conv for them, L = 256
+# the VALU one; with and without the skip terms.
+@pytest.mark.parametrize("dtype", [workloads.BF16, workloads.F16])
+@pytest.mark.parametrize("B,L,dh,with_D", [(2, 2048, 2, True), (3, 256, 4, False), (1, 8192, 8, True)])
+def test_layer_heads(h3, dtype, B, L, dh, with_D):
+    d = 128
+    w = workloads.layer_workload("t", B, L, d, dtype, seed=61 + dh + L, m_shift=64)
+    rng = np.random.default_rng(dh * 10 + B)
+    ssm = workloads.make_diag_ssm(rng, d * dh, 64, 1e-3, 1e-1)
+    A, Bm, C, dt = ssm.complex64()
+    k32 = oracle.ssm_kernel(A, Bm, C, dt, L).astype(np.float32)
+    dD = rng.standard_normal(d * dh).astype(np.float32) if with_D else None
+    sD = rng.standard_normal(d).astype(np.float32) if with_D else None
+    W = {n: to_dev(w.weight_out_in(n), w.dtype) for n in "qkvo"}
+    out = h3.layer_fwd_heads(to_dev(w.x, w.dtype), W["q"], W["k"], W["v"], W["o"], f32dev(w.shift_C),
+                             f32dev(sD) if with_D else None, f32dev(k32), f32dev(dD) if with_D else None, dh)
+    torch.cuda.synchronize()
+    ref = oracle.h3_layer(w.x64, w.W["q"][1], w.W["k"][1], w.W["v"][1], w.W["o"][1],
+                          w.shift_C.astype(np.float64), k32.astype(np.float64),
+                          dD.astype(np.float64) if with_D else None,
+                          shift_D=sD.astype(np.float64) if with_D else None, d_head=dh)
+    assert rel_err(to_np64(out), ref) < 2e-2
+
+
 def test_layer_config4_one_batch_element(h3):
     w = workloads.config(4)
     y, ref = _layer_case(h3, w, b_sel=[3])
