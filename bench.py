@@ -269,6 +269,25 @@ def _extra_cfg3(h3, dev, reps, warm, ex, np, torch, workloads):
                                 "pct_hbm_peak": 100 * by / ms / 1e6 / HBM_PEAK_GBS,
                                 "two_streams_ms_per_call": ms2, "two_streams_gelem_per_s": B * H * L / ms2 / 1e6,
                                 "two_streams_pct_hbm_peak": 100 * by / ms2 / 1e6 / HBM_PEAK_GBS}
+    # the same workload with the fused limit raised to 16384 (chunk 16384)
+    ch2 = 16384
+    ws16 = torch.empty(h3.workspace_size(h3.OP_STATEPASS, B, H, L, m, ch2, h3.F16), dtype=torch.uint8, device=dev)
+    del ws
+    ms16 = _time_calls(lambda i: h3.statepass_conv(u[0], Ab, Bb, C, D, ch2, out=y[0], workspace=ws16), reps, warm)
+    ex["cfg3_statepass_f16"]["chunk16384_ms"] = ms16
+    ex["cfg3_statepass_f16"]["chunk16384_gelem_per_s"] = B * H * L / ms16 / 1e6
+    # the fused conv alone at L = 16384 (B=8 H=256, fp16)
+    Bc, Hc, Lc = 8, 256, 16384
+    uc = torch.from_numpy(np.random.default_rng(21).standard_normal((Bc, Hc, Lc)).astype(np.float16)).to(dev)
+    kc = torch.from_numpy((np.random.default_rng(22).standard_normal((Hc, Lc)) *
+                           np.exp(-np.arange(Lc) / 4000.0)).astype(np.float32)).to(dev)
+    wsc = torch.empty(h3.workspace_size(h3.OP_FFTCONV, Bc, Hc, Lc, 0, 0, h3.F16), dtype=torch.uint8, device=dev)
+    yc = torch.empty_like(uc)
+    msc = _time_calls(lambda i: h3.fftconv(uc, kc, D[:Hc], out=yc, workspace=wsc), reps, warm)
+    byc = 2 * Bc * Hc * Lc * 2 + Hc * Lc * 4
+    ex["fftconv_l16384_f16"] = {"ms": msc, "B": Bc, "H": Hc, "GB_s": byc / msc / 1e6,
+                                "pct_hbm_peak": 100 * byc / msc / 1e6 / HBM_PEAK_GBS,
+                                "gelem_per_s": Bc * Hc * Lc / msc / 1e6}
 
 
 def _extra_cfg4(h3, dev, reps, warm, ex, np, torch, workloads):

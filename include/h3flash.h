@@ -51,7 +51,9 @@ enum { H3_OP_FFTCONV = 1, H3_OP_STATEPASS = 2, H3_OP_LAYER = 3, H3_OP_FFTCONV_BW
 /* Limits of this build. */
 #define H3_MAX_MODES 64     /* m: complex modes per channel of a diagonal SSM      */
 #define H3_MIN_LEN 16       /* smallest fused convolution length (and chunk)       */
-#define H3_FUSED_LIMIT 8192 /* longest fused convolution length (and chunk)        */
+#define H3_FUSED_LIMIT 16384     /* longest fused convolution length (and chunk), 16-bit I/O */
+#define H3_FUSED_LIMIT_F32 8192  /* the same for float32 I/O, the spectral entry points and
+                                    the kernel gradient of h3_fftconv_bwd                    */
 #define H3_MAX_SHIFT 64     /* longest shift-SSM filter in h3_layer_fwd            */
 
 /*

@@ -20,7 +20,7 @@ import torch
 __all__ = [
     "H3Error", "lib", "ssm_discretize", "ssm_kernel", "fftconv", "statepass_conv",
     "layer_fwd", "layer_fwd_heads", "ssm_step", "fftconv_bwd", "kernel_spectrum", "fftconv_spectral", "workspace_size", "status_string", "F32", "F16", "BF16",
-    "OP_FFTCONV", "OP_STATEPASS", "OP_LAYER", "OP_FFTCONV_BWD", "OP_LAYER_HEADS", "FUSED_LIMIT", "MAX_MODES",
+    "OP_FFTCONV", "OP_STATEPASS", "OP_LAYER", "OP_FFTCONV_BWD", "OP_LAYER_HEADS", "FUSED_LIMIT", "FUSED_LIMIT_F32", "MAX_MODES",
 ]
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -28,7 +28,8 @@ LIB_PATH = os.path.join(HERE, "libh3flash.so")
 
 F32, F16, BF16 = 0, 1, 2
 OP_FFTCONV, OP_STATEPASS, OP_LAYER, OP_FFTCONV_BWD, OP_LAYER_HEADS = 1, 2, 3, 4, 5
-FUSED_LIMIT = 8192
+FUSED_LIMIT = 16384       # 16-bit I/O
+FUSED_LIMIT_F32 = 8192    # float32 I/O, spectral entry points, kernel gradient
 MAX_MODES = 64
 
 _DTYPES = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}

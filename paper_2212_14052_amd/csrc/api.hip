@@ -33,6 +33,12 @@ bool overlap(const void *p, size_t n, const void *q, size_t m) {
 
 int launched(hipError_t e) { return e == hipSuccess ? H3_OK : H3_EDEVICE; }
 
+// fused length / chunk: a power of two in [H3_MIN_LEN, H3_FUSED_LIMIT]; above
+// H3_FUSED_LIMIT_F32 only where the matrix-core kernels take it (16-bit I/O)
+bool fused_len_ok(int L, int dtype) {
+    return pow2_in(L, H3_MIN_LEN, H3_FUSED_LIMIT) && (L <= H3_FUSED_LIMIT_F32 || fftconv_mfma_supported(L, dtype));
+}
+
 // Workspace layouts (each region 256-byte aligned).
 struct StatepassWs {
     size_t k, kspec, states, corr_w, corr, total;
@@ -192,7 +198,7 @@ int h3_ssm_kernel(const float *A, const float *B, const float *C, const float *d
 int h3_fftconv(const void *u, const float *k, const float *D, void *y, int B, int H, int L,
                int dtype, void *workspace, size_t ws_bytes, void *stream) {
     if (!u || !k || !y || B < 1 || H < 1 || L < 1) return H3_EINVAL;
-    if (!dtype_ok(dtype) || !pow2_in(L, H3_MIN_LEN, H3_FUSED_LIMIT)) return H3_EUNSUPPORTED;
+    if (!dtype_ok(dtype) || !fused_len_ok(L, dtype)) return H3_EUNSUPPORTED;
     const size_t io = (size_t)B * H * L * esize(dtype);
     const size_t need = h3_workspace_size(H3_OP_FFTCONV, B, H, L, 0, 0, dtype);
     if (!workspace || ws_bytes < need) return H3_EWORKSPACE;
@@ -218,7 +224,7 @@ int h3_fftconv_bwd(const void *u, const float *k, const float *D, const void *dy
                    void *du, float *dk, float *dD, void *workspace, size_t ws_bytes, void *stream) {
     if (!dy || !k || B < 1 || H < 1 || L < 1 || (!du && !dk && !dD)) return H3_EINVAL;
     if ((dk || dD) && !u) return H3_EINVAL;
-    if (!dtype_ok(dtype) || !pow2_in(L, H3_MIN_LEN, H3_FUSED_LIMIT)) return H3_EUNSUPPORTED;
+    if (!dtype_ok(dtype) || !fused_len_ok(L, dtype) || ((dk || dD) && L > H3_FUSED_LIMIT_F32)) return H3_EUNSUPPORTED;
     const size_t io = (size_t)B * H * L * esize(dtype), kb = (size_t)H * L * 4, db = (size_t)H * 4;
     const size_t need = h3_workspace_size(H3_OP_FFTCONV_BWD, B, H, L, 0, 0, dtype);
     if (!workspace || ws_bytes < need) return H3_EWORKSPACE;
@@ -247,7 +253,7 @@ int h3_fftconv_bwd(const void *u, const float *k, const float *D, const void *dy
         a.u = dy; a.y = du; a.D = D;
         a.B = B; a.H = H; a.L = L; a.nchunk = 1; a.pair_mode = 0; a.dtype = dtype;
         a.conj_k = 1;
-        if (fftconv_wave_supported(L, dtype) || fftconv_wave16k_supported(L, dtype)) {
+        if (fftconv_mfma_supported(L, dtype)) {   // the wave kernels (2048, 8192) or the 32768-point one
             e = launch_fftconv_mfma(a, k, s);
         } else {
             float2 *Kspec = (float2 *)workspace;
@@ -271,7 +277,7 @@ int h3_fftconv_bwd(const void *u, const float *k, const float *D, const void *dy
 
 int h3_kernel_spectrum(const float *k, int H, int L, float *Kspec, void *stream) {
     if (!k || !Kspec || H < 1 || L < 1) return H3_EINVAL;
-    if (!pow2_in(L, H3_MIN_LEN, H3_FUSED_LIMIT)) return H3_EUNSUPPORTED;
+    if (!pow2_in(L, H3_MIN_LEN, H3_FUSED_LIMIT_F32)) return H3_EUNSUPPORTED;
     if (!aligned16(k) || !aligned16(Kspec)) return H3_EINVAL;
     if (overlap(k, (size_t)H * L * 4, Kspec, (size_t)H * (L + 1) * 8)) return H3_EINVAL;
     return launched(launch_spectrum(k, H, L, (float2 *)Kspec, (hipStream_t)stream));
@@ -280,7 +286,7 @@ int h3_kernel_spectrum(const float *k, int H, int L, float *Kspec, void *stream)
 int h3_fftconv_spectral(const void *u, const float *Kspec, const float *D, void *y, int B, int H,
                         int L, int dtype, void *stream) {
     if (!u || !Kspec || !y || B < 1 || H < 1 || L < 1) return H3_EINVAL;
-    if (!dtype_ok(dtype) || !pow2_in(L, H3_MIN_LEN, H3_FUSED_LIMIT)) return H3_EUNSUPPORTED;
+    if (!dtype_ok(dtype) || !pow2_in(L, H3_MIN_LEN, H3_FUSED_LIMIT_F32)) return H3_EUNSUPPORTED;
     if (!aligned16(u) || !aligned16(y) || !aligned16(Kspec)) return H3_EINVAL;
     const size_t io = (size_t)B * H * L * esize(dtype);
     if (overlap(u, io, y, io) || overlap(Kspec, (size_t)H * (L + 1) * 8, y, io)) return H3_EINVAL;
@@ -299,8 +305,7 @@ int h3_statepass_conv(const void *u, const float *Abar, const float *Bbar, const
     if (!u || !Abar || !Bbar || !C || !y || B < 1 || H < 1 || L < 1 || m < 1 || chunk < 1)
         return H3_EINVAL;
     if (L % chunk) return H3_EINVAL;
-    if (!dtype_ok(dtype) || m > H3_MAX_MODES || !pow2_in(chunk, H3_MIN_LEN, H3_FUSED_LIMIT))
-        return H3_EUNSUPPORTED;
+    if (!dtype_ok(dtype) || m > H3_MAX_MODES || !fused_len_ok(chunk, dtype)) return H3_EUNSUPPORTED;
     const size_t io = (size_t)B * H * L * esize(dtype);
     const size_t need = h3_workspace_size(H3_OP_STATEPASS, B, H, L, m, chunk, dtype);
     if (!workspace || ws_bytes < need) return H3_EWORKSPACE;

@@ -63,7 +63,8 @@ def test_fftconv_validation():
     assert fftconv(B=0) == EINVAL
     assert fftconv(L=48) == EUNSUP                  # not a power of two
     assert fftconv(L=8) == EUNSUP                   # below the minimum
-    assert fftconv(L=16384) == EUNSUP               # above the fused limit
+    assert fftconv(L=16384) == EUNSUP               # above the float32 fused limit
+    assert fftconv(L=32768, dt=1) == EUNSUP         # above the 16-bit fused limit
     assert fftconv(dt=3) == EUNSUP
     assert fftconv(ws=0) == EWS
     assert fftconv(wsb=16) == EWS
@@ -83,7 +84,8 @@ def test_statepass_validation():
     assert statepass(A=0) == EINVAL
     assert statepass(L=250) == EINVAL               # chunk does not divide L
     assert statepass(chunk=48, L=96) == EUNSUP
-    assert statepass(chunk=16384, L=16384) == EUNSUP
+    assert statepass(chunk=32768, L=32768) == EUNSUP
+    assert statepass(chunk=16384, L=16384, dt=0) == EUNSUP   # float32 chunks stop at 8192
     assert statepass(m=65) == EUNSUP
     assert statepass(m=0) == EINVAL
     assert statepass(dt=5) == EUNSUP
@@ -126,6 +128,8 @@ def test_spectral_validation():
     assert L.h3_fftconv_spectral(P(U), P(K), None, P(U), 2, 4, 64, 0, None) == EINVAL
     assert L.h3_fftconv_spectral(P(U), P(K), None, P(Y), 2, 4, 64, 9, None) == EUNSUP
     assert L.h3_fftconv_spectral(P(U), P(K), None, P(Y), 2, 4, 32768, 1, None) == EUNSUP
+    assert L.h3_fftconv_spectral(P(U), P(K), None, P(Y), 2, 4, 16384, 1, None) == EUNSUP
+    assert L.h3_kernel_spectrum(P(K), 4, 16384, P(Y), None) == EUNSUP
 
 
 def step(u=U, A=K, Bb=K + 4096, C=K + 8192, D=None, B=2, H=4, m=64, T=1, dt=1, x=X, y=Y):
@@ -156,7 +160,8 @@ def test_bwd_validation():
     assert bwd(du=0, dk=0, dD=0) == EINVAL            # nothing asked
     assert bwd(u=0) == EINVAL                         # dk needs u
     assert bwd(L=48) == EUNSUP
-    assert bwd(L=16384) == EUNSUP
+    assert bwd(L=16384) == EUNSUP                     # kernel gradient stops at 8192
+    assert bwd(L=32768, dk=0) == EUNSUP
     assert bwd(dt=3) == EUNSUP
     assert bwd(ws=0) == EWS
     assert bwd(du=X) == EINVAL                        # du aliases dy

@@ -196,6 +196,56 @@ def test_statepass_resume(h3):
     assert rel_err(to_np64(x2), to_np64(xf)) < 1e-5
 
 
+# ------------------------------------ fused limit 16384 (32768-point) ---
+@pytest.mark.parametrize("dtype", [workloads.F16, workloads.BF16])
+@pytest.mark.parametrize("B,H", [(1, 2), (3, 3)])
+def test_fftconv_l16384(h3, dtype, B, H):
+    y, ref = _conv_case(h3, B, H, 16384, dtype, seed=B * 10 + H, dt_lo=1e-4)
+    assert rel_err(y, ref) < TOL[dtype]
+
+
+def test_fftconv_l16384_impulse(h3):
+    """u = delta returns k + D delta on every row (spectrum and skip fold)."""
+    L, H = 16384, 2
+    rng = np.random.default_rng(4)
+    k = (rng.standard_normal((H, L)) * np.exp(-np.arange(L) / 3000.0)).astype(np.float32)
+    D = rng.standard_normal(H).astype(np.float32)
+    u = np.zeros((2, H, L), np.float32); u[:, :, 0] = 1.0
+    y = h3.fftconv(to_dev(workloads.round_to(u, workloads.F16)[0], workloads.F16), f32dev(k), f32dev(D))
+    torch.cuda.synchronize()
+    ref = np.broadcast_to(k.astype(np.float64), (2, H, L)).copy(); ref[:, :, 0] += D
+    assert rel_err(to_np64(y), ref) < 2e-2
+
+
+def test_statepass_chunk16384(h3):
+    w = workloads.statepass_workload("t", 2, 2, 32768, 16384, workloads.F16, seed=8, dt_lo=1e-4, dt_hi=1e-2,
+                                     x0_scale=0.5)
+    Ab32, Bb32, Ab, Bb, C = _sp_inputs(w)
+    y, xf = h3.statepass_conv(to_dev(w.u, w.dtype), f32dev(Ab32), f32dev(Bb32), f32dev(w.ssm.C), f32dev(w.D),
+                              16384, x0=f32dev(w.x0))
+    torch.cuda.synchronize()
+    ry, rx = oracle.recurrence(w.u64, Ab, Bb, C, w.D.astype(np.float64), x0=cplx64(w.x0))
+    assert rel_err(to_np64(y), ry) < 2e-2
+    xg = cplx64(to_np64(xf))
+    assert np.abs(xg - rx).max() / np.abs(rx).max() < 2e-2
+
+
+def test_fftconv_bwd_du_l16384(h3):
+    """Input gradient at L = 16384: the 32768-point kernel with the conjugated
+    kernel spectrum."""
+    B, H, L = 2, 2, 16384
+    w = workloads.conv_workload("t", B, H, L, workloads.BF16, seed=12)
+    A, Bm, C, dt = _diag_params(w)
+    k32 = oracle.ssm_kernel(A, Bm, C, dt, L).astype(np.float32)
+    rng = np.random.default_rng(13)
+    dy_s, dy64 = workloads.round_to(rng.standard_normal((B, H, L)), workloads.BF16)
+    du, _, _ = h3.fftconv_bwd(None, f32dev(k32), f32dev(w.D), to_dev(dy_s, workloads.BF16), want_dk=False,
+                              want_dD=False)
+    torch.cuda.synchronize()
+    rdu, _, _ = oracle.causal_conv_bwd(w.u64, k32.astype(np.float64), w.D.astype(np.float64), dy64)
+    assert rel_err(to_np64(du), rdu) < 2e-2
+
+
 # ------------------------------------------------- conv backward pass ---
 def _bwd_case(h3, B, H, L, dtype, seed, with_D=True, sel=None):
     w = workloads.conv_workload("t", B, H, L, dtype, seed=seed)
