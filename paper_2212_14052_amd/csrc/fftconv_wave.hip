@@ -137,19 +137,28 @@ __device__ __forceinline__ void out_layer(uint32_t (&d)[64], const Dft &Fs, floa
 }  // namespace wv
 
 // ============================================================================
-// CORR: 0 none, 1 float32 correction term, 2 correction term in the I/O dtype
-template <int DT, int CORR>
-__global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) void fftconv_wave4096_kernel(
-    ConvArgs a, const float *k, int wg_per_ch, int pairs_per_ch) {
+// CORR: 0 none, 1 float32 correction term, 2 correction term in the I/O dtype.
+// CPW: channels per workgroup.  1: the four waves share one channel's row
+// pairs.  2 (at most two row pairs per channel, e.g. batch 4): channels
+// 2 hb and 2 hb + 1, both spectra computed by all four waves, then waves 0, 1
+// take the first channel's pairs and waves 2, 3 the second's, so no wave
+// idles while its workgroup holds the CU's LDS.
+template <int DT, int CORR, int CPW>
+__global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(CPW == 1 ? 3 : 2))) void
+fftconv_wave4096_kernel(ConvArgs a, const float *k, int wg_per_ch, int pairs_per_ch) {
     using namespace wv;
     __shared__ uint4 Tab[kTab];       // Ytab (L2 twiddles per tile and lane) + Lc (per-lane constants)
-    __shared__ uint4 Ks[16 * 64];     // kernel spectrum per L3 quad and lane (also the spectrum's scratch)
+    __shared__ uint4 Ks[CPW][16 * 64];   // kernel spectra per L3 quad and lane (also the spectrum's scratch)
     uint4 *Ytab = Tab, *Lc = Tab + kTabY;
     __shared__ float red[2 * NW];
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
     const int g = lane >> 4, c = lane & 15;
-    const int h = blockIdx.x / wg_per_ch, part = blockIdx.x % wg_per_ch;
+    const int hb = blockIdx.x / wg_per_ch, part = blockIdx.x % wg_per_ch;
+    const int chw = CPW == 1 ? 0 : (w >> 1);   // this wave's channel within the workgroup
+    const int h = hb * CPW + chw;              // this wave's channel
+    const int wl = CPW == 1 ? w : (w & 1);     // this wave's index among its channel's waves
+    constexpr int WPC = NW / CPW;              // waves per channel
     const int per = (pairs_per_ch + wg_per_ch - 1) / wg_per_ch;
     const int q0 = part * per, q1 = min(q0 + per, pairs_per_ch);
     const uint16_t *u = (const uint16_t *)a.u;
@@ -207,29 +216,41 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
     // (2) this wave's L1 tiles of the kernel row: lane (g < 2, c) takes
     // k[256 (4 g + j) + 16 c + 4 w + t], t = 0..3, for j = 0..3 (tile
     // T = 4 w + t, point p2 = 4 g + j)
-    float4 kq[4];
+    float4 kq[CPW][4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        kq[j] = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (g < 2) kq[j] = *(const float4 *)(k + (long)h * L + 256 * (4 * g + j) + 16 * c + 4 * w);
+    for (int ch = 0; ch < CPW; ++ch) {
+        const int hs = hb * CPW + ch;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            kq[ch][j] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (g < 2 && (CPW == 1 || hs < a.H))   // one channel per workgroup: always present
+                kq[ch][j] = *(const float4 *)(k + (long)hs * L + 256 * (4 * g + j) + 16 * c + 4 * w);
+        }
     }
     __builtin_amdgcn_sched_barrier(0);
     // (3) this wave's first pair, in flight during the kernel transform
-    int qq = q0 + w;
-    bool have = qq < q1;
+    int qq = q0 + wl;
+    bool have = (CPW == 1 || h < a.H) && qq < q1;
     if (have) issue_loads(qq);
 
     // ---- kernel spectrum of channel h, all waves: wave w runs tiles
     //      4 w .. 4 w + 3 of L1 and L2 and quads 4 w .. 4 w + 3 of L3; the
     //      swap between L2 and L3 goes through Ks.  Ks ends up holding
     //      F(k + D delta) 2^-ek / 64; the pairs' L3 matrix carries 2^-e2.
-    int kexp, e2;
-    {
-        if (tid == 0 && a.D) kq[0].x += a.D[h];   // k[0] += D: lane 0, point 0 of tile 0
+    int kexpc[CPW], e2c[CPW];
+#pragma unroll
+    for (int ch = 0; ch < CPW; ++ch) {
+        const int hs = hb * CPW + ch;
+        if (CPW > 1 && hs >= a.H) {   // workgroup-uniform: an odd channel count's missing second channel
+            kexpc[ch] = 0;
+            e2c[ch] = 0;
+            continue;
+        }
+        if (tid == 0 && a.D) kq[ch][0].x += a.D[hs];   // k[0] += D: lane 0, point 0 of tile 0
         float mx = 0.f;
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-            mx = fmaxf(mx, fmaxf(fmaxf(fabsf(kq[j].x), fabsf(kq[j].y)), fmaxf(fabsf(kq[j].z), fabsf(kq[j].w))));
+            mx = fmaxf(mx, fmaxf(fmaxf(fabsf(kq[ch][j].x), fabsf(kq[ch][j].y)), fmaxf(fabsf(kq[ch][j].z), fabsf(kq[ch][j].w))));
         mx = wave_max(mx);
         if (lane == 0) red[w] = mx;
         // tables and kernel row landed; at most the 16 pair loads (issued
@@ -243,10 +264,10 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
         uint32_t dq[16];   // quad t = tile 4 w + t, element j
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            dq[0 + j] = pk(ldexpf(kq[j].x, -ek), 0.f);
-            dq[4 + j] = pk(ldexpf(kq[j].y, -ek), 0.f);
-            dq[8 + j] = pk(ldexpf(kq[j].z, -ek), 0.f);
-            dq[12 + j] = pk(ldexpf(kq[j].w, -ek), 0.f);
+            dq[0 + j] = pk(ldexpf(kq[ch][j].x, -ek), 0.f);
+            dq[4 + j] = pk(ldexpf(kq[ch][j].y, -ek), 0.f);
+            dq[8 + j] = pk(ldexpf(kq[ch][j].z, -ek), 0.f);
+            dq[12 + j] = pk(ldexpf(kq[ch][j].w, -ek), 0.f);
         }
         const Dft F = lds_dft(Lc, lane, false);
         {
@@ -268,11 +289,11 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
         // L3 quad 4 g + jj, element t: one 16-byte write per jj
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj)
-            Ks[(4 * g + jj) * 64 + 16 * w + c] = make_uint4(dq[jj], dq[4 + jj], dq[8 + jj], dq[12 + jj]);
+            Ks[ch][(4 * g + jj) * 64 + 16 * w + c] = make_uint4(dq[jj], dq[4 + jj], dq[8 + jj], dq[12 + jj]);
         __syncthreads();
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-            const uint4 v = Ks[(4 * w + t) * 64 + lane];
+            const uint4 v = Ks[ch][(4 * w + t) * 64 + lane];
             dq[4 * t + 0] = v.x; dq[4 * t + 1] = v.y; dq[4 * t + 2] = v.z; dq[4 * t + 3] = v.w;
         }
         layer<false, 4>(dq, F, NoPre{}, [&](int t, f4_t re, f4_t im, uint4) {
@@ -293,13 +314,16 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
         const uint32_t cj = a.conj_k ? 0x80000000u : 0u;
 #pragma unroll
         for (int t = 0; t < 4; ++t)
-            Ks[(4 * w + t) * 64 + lane] =
+            Ks[ch][(4 * w + t) * 64 + lane] =
                 make_uint4(dq[4 * t] ^ cj, dq[4 * t + 1] ^ cj, dq[4 * t + 2] ^ cj, dq[4 * t + 3] ^ cj);
         __syncthreads();   // Ks complete
-        e2 = __builtin_amdgcn_readfirstlane(
+        const int e2v = __builtin_amdgcn_readfirstlane(
             exp_of(fmaxf(fmaxf(red[NW], red[NW + 1]), fmaxf(red[NW + 2], red[NW + 3]))));   // in [-6, 6]
-        kexp = 6 + ek + e2;
+        e2c[ch] = e2v;
+        kexpc[ch] = 6 + ek + e2v;
     }
+    const int kexp = (CPW == 1 || chw == 0) ? kexpc[0] : kexpc[CPW - 1];
+    const int e2 = (CPW == 1 || chw == 0) ? e2c[0] : e2c[CPW - 1];
 
     // ---- row pairs of this wave ----
     uint32_t d[64];
@@ -370,7 +394,7 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
         Dft F3 = lds_dft(Lc, lane, false);
         F3.re = h8_scale(F3.re, (_Float16)ldexpf(1.0f, -e2));
         F3.im = h8_scale(F3.im, (_Float16)ldexpf(1.0f, -e2));
-        layer<false>(d, F3, [&](int tau) { return Ks[tau * 64 + lane]; },
+        layer<false>(d, F3, [&](int tau) { return Ks[chw][tau * 64 + lane]; },
                      [&](int tau, f4_t re, f4_t im, uint4 kk) {
             d[4 * tau + 0] = cmul(pk(re[0], im[0]), kk.x);
             d[4 * tau + 1] = cmul(pk(re[1], im[1]), kk.y);
@@ -439,7 +463,7 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
             }
         }
         // next pair's loads, consumed at the top of the next iteration
-        qq += NW;
+        qq += WPC;
         have = qq < q1;
         if (have) issue_loads(qq);
     }
@@ -769,8 +793,17 @@ hipError_t launch_fftconv_wave(const ConvArgs &a, const float *k, hipStream_t s)
     while ((long)a.H * wg_per_ch * wv::NW < 2048 && pairs_per_ch >= 2 * wv::NW * wg_per_ch) wg_per_ch *= 2;
     dim3 grid(a.H * wg_per_ch), block(wv::NT);
     const int corr = a.corr == nullptr ? 0 : (a.corr16 ? 2 : 1);
+    if (corr == 0 && a.pair_mode == 0 && pairs_per_ch <= 2 && wg_per_ch == 1 && a.H >= 2) {
+        // two channels per workgroup: every wave has a row pair
+        const dim3 grid2((a.H + 1) / 2);
+        if (a.dtype == F16)
+            hipLaunchKernelGGL((fftconv_wave4096_kernel<F16, 0, 2>), grid2, block, 0, s, a, k, 1, pairs_per_ch);
+        else
+            hipLaunchKernelGGL((fftconv_wave4096_kernel<BF16, 0, 2>), grid2, block, 0, s, a, k, 1, pairs_per_ch);
+        return hipGetLastError();
+    }
 #define H3_WAVE_LAUNCH(DTV, CV) \
-    hipLaunchKernelGGL((fftconv_wave4096_kernel<DTV, CV>), grid, block, 0, s, a, k, wg_per_ch, pairs_per_ch)
+    hipLaunchKernelGGL((fftconv_wave4096_kernel<DTV, CV, 1>), grid, block, 0, s, a, k, wg_per_ch, pairs_per_ch)
     if (a.dtype == F16) {
         if (corr == 0) H3_WAVE_LAUNCH(F16, 0);
         else if (corr == 1) H3_WAVE_LAUNCH(F16, 1);
