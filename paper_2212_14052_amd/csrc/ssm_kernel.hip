@@ -141,8 +141,10 @@ __global__ __launch_bounds__(KG_THREADS) void kernel_gen(int mode, const float *
 //   Qm[j][b] = Re Q[j][b] (j < 64),  Im Q[j-64][b] (j >= 64)
 // with P[a][n] = W_n z_n^{64 a}, Q[n][b] = z_n^b, z_n = exp(lambda_n), run as
 // 16x16x4 fp32 MFMAs (exact fp32 products, fp32 accumulation).  A workgroup (4
-// waves) produces rows a = a0 .. a0+31 (2048 outputs); wave w owns columns
-// b = 16 w .. 16 w + 15.  The powers z^e are formed in float64 by repeated
+// waves) produces rows a = a0 .. a0 + 16 NR - 1 (1024 NR outputs; NR = 4 once
+// a row has 64 or more of them, so that the per-workgroup setup is shared by
+// twice the outputs and long kernels need half the workgroups); wave w owns
+// columns b = 16 w .. 16 w + 15.  The powers z^e are formed in float64 by repeated
 // squaring and multiplication (relative error ~ e * 1e-16), so no phase is
 // ever reduced in float32.
 //
@@ -154,7 +156,6 @@ __global__ __launch_bounds__(KG_THREADS) void kernel_gen(int mode, const float *
 //
 // The reduction index is permuted so that MFMA step s of lane (r, q) uses
 // j = 32 q + s: four consecutive steps read one 16-byte LDS word.
-constexpr int KM_ROWS = 32;
 constexpr int KM_LD = 128 + 4;   // LDS row pitch in floats
 typedef float f4v_t __attribute__((ext_vector_type(4)));
 
@@ -173,11 +174,13 @@ __device__ __forceinline__ double2 zpow(double2 z, int e) {
 
 // mode 0: continuous (A, B, dt), ZOH.  mode 1: discrete (Abar, Bbar), W = C Bbar.
 // mode 2: discrete Abar of channel (orow / div) % H, W given per output row in P1.
+template <int NR>
 __global__ __launch_bounds__(256) void kernel_gen_mfma(int mode, const float *P0, const float *P1,
                                                        const float *C, const float *dt, int H,
                                                        int m, int L, float *k, int div) {
     __shared__ double pre[3][H3_MAX_MODES_DEV];
     __shared__ float Qt[64][KM_LD];          // [b][j]  (Qm transposed)
+    constexpr int KM_ROWS = 16 * NR;
     __shared__ float Pm[KM_ROWS][KM_LD];     // [a][j]
     const int nrt = (L / 64 + KM_ROWS - 1) / KM_ROWS;  // row tiles per output row
     const int orow = blockIdx.x / nrt;
@@ -227,7 +230,7 @@ __global__ __launch_bounds__(256) void kernel_gen_mfma(int mode, const float *P0
         else
             Wn = make_float2((float)pr, (float)pi);
     }
-    // ---- Q rows b = 16 w .. 16 w + 15 and P rows 8 w .. 8 w + 7 of mode n
+    // ---- Q rows b = 16 w .. 16 w + 15 and P rows 4 NR w .. 4 NR w + 4 NR - 1 of mode n
     {
         double2 p = zpow(z, 16 * w);
 #pragma unroll
@@ -237,42 +240,60 @@ __global__ __launch_bounds__(256) void kernel_gen_mfma(int mode, const float *P0
             p = zmul(p, z);
         }
         const double2 z64 = zpow(z, 64);
-        double2 q = zpow(z64, a0 + 8 * w);
+        double2 q = zpow(z64, a0 + 4 * NR * w);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
+        for (int j = 0; j < 4 * NR; ++j) {
             const float qr = (float)q.x, qi = (float)q.y;
-            Pm[8 * w + j][n] = Wn.x * qr - Wn.y * qi;
-            Pm[8 * w + j][64 + n] = -(Wn.x * qi + Wn.y * qr);
+            Pm[4 * NR * w + j][n] = Wn.x * qr - Wn.y * qi;
+            Pm[4 * NR * w + j][64 + n] = -(Wn.x * qi + Wn.y * qr);
             q = zmul(q, z64);
         }
     }
     __syncthreads();
-    // wave w: two 16 x 16 tiles (rows a0 .. a0+15 and a0+16 .. a0+31) of
-    // columns 16 w .. 16 w + 15; lane (r, q) at step s uses reduction index 32 q + s
-    f4v_t acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+    // wave w: NR 16 x 16 tiles (rows a0 + 16 i .. a0 + 16 i + 15) of columns
+    // 16 w .. 16 w + 15; lane (r, q) at step s uses reduction index 32 q + s
+    f4v_t acc[NR];
+#pragma unroll
+    for (int i = 0; i < NR; ++i) acc[i] = (f4v_t){0.f, 0.f, 0.f, 0.f};
     const int r = lane & 15, kq = lane >> 4;
 #pragma unroll
     for (int s4 = 0; s4 < 32; s4 += 4) {
         const float4 bv = *(const float4 *)&Qt[16 * w + r][32 * kq + s4];
-        const float4 p0 = *(const float4 *)&Pm[r][32 * kq + s4];
-        const float4 p1 = *(const float4 *)&Pm[16 + r][32 * kq + s4];
-        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(p0.x, bv.x, acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(p1.x, bv.x, acc1, 0, 0, 0);
-        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(p0.y, bv.y, acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(p1.y, bv.y, acc1, 0, 0, 0);
-        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(p0.z, bv.z, acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(p1.z, bv.z, acc1, 0, 0, 0);
-        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(p0.w, bv.w, acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(p1.w, bv.w, acc1, 0, 0, 0);
+        float4 pv[NR];
+#pragma unroll
+        for (int i = 0; i < NR; ++i) pv[i] = *(const float4 *)&Pm[16 * i + r][32 * kq + s4];
+#pragma unroll
+        for (int i = 0; i < NR; ++i) acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(pv[i].x, bv.x, acc[i], 0, 0, 0);
+#pragma unroll
+        for (int i = 0; i < NR; ++i) acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(pv[i].y, bv.y, acc[i], 0, 0, 0);
+#pragma unroll
+        for (int i = 0; i < NR; ++i) acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(pv[i].z, bv.z, acc[i], 0, 0, 0);
+#pragma unroll
+        for (int i = 0; i < NR; ++i) acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(pv[i].w, bv.w, acc[i], 0, 0, 0);
     }
-    // lane holds rows a0 + 4 kq + j (+16), column 16 w + r
+    // lane holds rows a0 + 16 i + 4 kq + j, column 16 w + r
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-        const int a = a0 + 4 * kq + j;
-        const int t = 64 * a + 16 * w + r;
-        if (t < L) k[(long)orow * L + t] = 2.f * acc0[j];
-        if (t + 1024 < L) k[(long)orow * L + t + 1024] = 2.f * acc1[j];
+        const int t = 64 * (a0 + 4 * kq + j) + 16 * w + r;
+#pragma unroll
+        for (int i = 0; i < NR; ++i)
+            if (t + 1024 * i < L) k[(long)orow * L + t + 1024 * i] = 2.f * acc[i][j];
     }
+}
+
+// Rows of 64 outputs per workgroup: 64 once the output row holds that many
+// (half the workgroups, each sharing its setup among twice the outputs), else 32.
+static inline int kgen_rows(int L) { return L / 64 >= 64 ? 64 : 32; }
+
+static void launch_kgen_mfma(int mode, const float *P0, const float *P1, const float *C, const float *dt,
+                             int H, int m, int L, float *k, int div, long nrows, hipStream_t s) {
+    const int R = kgen_rows(L);
+    const long nrt = (L / 64 + R - 1) / R;
+    const dim3 grid((unsigned)(nrt * nrows)), block(256);
+    if (R == 64)
+        hipLaunchKernelGGL(kernel_gen_mfma<4>, grid, block, 0, s, mode, P0, P1, C, dt, H, m, L, k, div);
+    else
+        hipLaunchKernelGGL(kernel_gen_mfma<2>, grid, block, 0, s, mode, P0, P1, C, dt, H, m, L, k, div);
 }
 
 hipError_t launch_discretize(const float *A, const float *B, const float *dt, int H, int m,
@@ -286,9 +307,7 @@ hipError_t launch_discretize(const float *A, const float *B, const float *dt, in
 hipError_t launch_kernel_gen(int mode, const float *P0, const float *P1, const float *C,
                              const float *dt, int H, int m, int L, float *k, hipStream_t s) {
     if (L % 64 == 0) {
-        const long nrt = (L / 64 + KM_ROWS - 1) / KM_ROWS;
-        hipLaunchKernelGGL(kernel_gen_mfma, dim3((unsigned)(nrt * H)), dim3(256), 0, s, mode, P0, P1,
-                           C, dt, H, m, L, k, 1);
+        launch_kgen_mfma(mode, P0, P1, C, dt, H, m, L, k, 1, H, s);
         return hipGetLastError();
     }
     const long ntile = (L + KG_TT - 1) / KG_TT;
@@ -301,10 +320,7 @@ hipError_t launch_state_correction(const float *Abar, const float2 *corr_W, int 
                                    int chunk, int nchunk, float *corr, hipStream_t s) {
     const long orows = (long)B * H * nchunk;
     if (chunk % 64 == 0) {
-        const long nrt = (chunk / 64 + KM_ROWS - 1) / KM_ROWS;
-        hipLaunchKernelGGL(kernel_gen_mfma, dim3((unsigned)(nrt * orows)), dim3(256), 0, s, 2, Abar,
-                           (const float *)corr_W, (const float *)nullptr, (const float *)nullptr, H, m,
-                           chunk, corr, nchunk);
+        launch_kgen_mfma(2, Abar, (const float *)corr_W, nullptr, nullptr, H, m, chunk, corr, nchunk, orows, s);
         return hipGetLastError();
     }
     const long ntile = (chunk + KG_TT - 1) / KG_TT;

@@ -136,8 +136,12 @@ __device__ __forceinline__ uint32_t pk(float re, float im) {
     const f2_t v = {re, im};
     return as_u32(__builtin_convertvector(v, h2_t));
 }
-// a * w and a * conj(w) in packed fp16
+// a * w and a * conj(w) in packed fp16.  The empty asm makes w an opaque
+// register value, so that both products take the half selections and the
+// sign as VOP3P operand modifiers; otherwise the first element of a 128-bit
+// LDS read has (-w.im, w.re) built by two extra VALU instructions.
 __device__ __forceinline__ uint32_t cmul(uint32_t a_, uint32_t w_) {
+    asm("" : "+v"(w_));
     const h2_t a = as_h2(a_), w = as_h2(w_);
     const h2_t t = a.xx * w;
     const h2_t ws = {-w.y, w.x};
@@ -157,6 +161,7 @@ __device__ __forceinline__ uint32_t cmulc2(uint32_t a_, uint32_t w_, uint32_t ws
     return as_u32(a.xx * u2 + t.yx);         // (ar wr + ai wi, -ar wi + ai wr)
 }
 __device__ __forceinline__ uint32_t cmulc(uint32_t a_, uint32_t w_) {
+    asm("" : "+v"(w_));
     const h2_t a = as_h2(a_), w = as_h2(w_);
     const h2_t wc = {w.x, -w.y};
     const h2_t t = a.xx * wc;
