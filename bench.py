@@ -159,7 +159,28 @@ def _time_calls(fn, reps, warm):
     return a.elapsed_time(b) / reps
 
 
-EXTRA_KEYS = ("cfg1_shift", "cfg2", "cfg3", "cfg4", "cfg0", "step", "bwd", "heads")
+def _time_streams(fn, streams, reps, warm, torch):
+    """ms per call of fn(i) for calls that issue onto `streams` themselves: the
+    timed region is bracketed by events on the current stream, which the
+    streams wait on first and are joined back into at the end."""
+    for i in range(warm):
+        fn(i)
+    torch.cuda.synchronize()
+    cur = torch.cuda.current_stream()
+    a = torch.cuda.Event(enable_timing=True); b = torch.cuda.Event(enable_timing=True)
+    a.record(cur)
+    for st in streams:
+        st.wait_stream(cur)
+    for i in range(reps):
+        fn(i)
+    for st in streams:
+        cur.wait_stream(st)
+    b.record(cur)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / reps
+
+
+EXTRA_KEYS = ("cfg1_shift", "cfg2", "cfg3", "cfg4", "cfg0", "step", "bwd", "heads", "scaling")
 
 
 def bench_extra(h3, dev, reps=10, warm=3, only=None):
@@ -188,6 +209,8 @@ def bench_extra(h3, dev, reps=10, warm=3, only=None):
         _extra_bwd(h3, dev, reps, warm, ex, np, torch, workloads)
     if want("heads"):
         _extra_heads(h3, dev, reps, warm, ex, np, torch, workloads)
+    if want("scaling"):
+        _extra_scaling(h3, dev, reps, warm, ex, np, torch, workloads)
     return ex
 
 
@@ -206,6 +229,35 @@ def _extra_cfg1_shift(h3, dev, reps, warm, ex, np, torch, workloads):
     ms = _time_calls(lambda i: h3.fftconv(us[i % nsets], ks, D, out=ys[i % nsets], workspace=ws), reps, warm)
     by = B * H * L * 4 + H * L * 4 + H * 4
     ex["cfg1_shift_conv"] = {"ms": ms, "GB_s": by / ms / 1e6, "pct_hbm_peak": 100 * by / ms / 1e6 / HBM_PEAK_GBS}
+
+
+def _extra_scaling(h3, dev, reps, warm, ex, np, torch, workloads):
+    # the L = 2048 fp16 fused conv alone (B = 8) at 1 to 12 row pairs per SIMD
+    # (H = 256 .. 3072; 1024 SIMDs), beside a device copy of the same u and y
+    # bytes: the slope is the kernel's cost per row pair and SIMD
+    B, L = 8, 2048
+    reps, warm = max(reps, 50), max(warm, 10)
+    rows = []
+    for H in (256, 768, 1536, 3072):
+        g = torch.Generator(device=dev).manual_seed(H)
+        nsets = max(2, -(-512 * 2 ** 20 // (B * H * L * 4)))
+        us = [torch.randn(B, H, L, device=dev, generator=g).half() for _ in range(nsets)]
+        ys = [torch.empty_like(us[0]) for _ in range(nsets)]
+        k = torch.randn(H, L, device=dev, generator=g) * 0.01
+        D = torch.randn(H, device=dev, generator=g)
+        ws = torch.empty(max(256, h3.workspace_size(h3.OP_FFTCONV, B, H, L, 0, 0, h3.F16)), dtype=torch.uint8,
+                         device=dev)
+        us_conv = 1e3 * _time_calls(lambda i: h3.fftconv(us[i % nsets], k, D, out=ys[i % nsets], workspace=ws),
+                                    reps, warm)
+        us_copy = 1e3 * _time_calls(lambda i: ys[i % nsets].copy_(us[i % nsets]), reps, warm)
+        by = B * H * L * 4
+        rows.append({"H": H, "pairs_per_simd": B * H // 2 / 1024, "conv_us": us_conv,
+                     "conv_GB_s_u_y": by / us_conv / 1e3, "copy_us": us_copy, "copy_GB_s": by / us_copy / 1e3})
+        del us, ys
+    n0, n1 = rows[0], rows[-1]
+    slope = (n1["conv_us"] - n0["conv_us"]) / (n1["pairs_per_simd"] - n0["pairs_per_simd"])
+    ex["conv_scaling_f16_l2048"] = {"rows": rows, "us_per_pair_per_simd": slope,
+                                    "intercept_us": n0["conv_us"] - slope * n0["pairs_per_simd"]}
 
 
 def _extra_cfg2(h3, dev, reps, warm, ex, np, torch, workloads):
@@ -249,21 +301,7 @@ def _extra_cfg3(h3, dev, reps, warm, ex, np, torch, workloads):
         with torch.cuda.stream(streams[j]):
             h3.statepass_conv(u[j], Ab, Bb, C, D, w.chunk, out=y[j], workspace=ws[j])
 
-    for i in range(warm):
-        two(i)
-    torch.cuda.synchronize()
-    cur = torch.cuda.current_stream(dev)
-    a = torch.cuda.Event(enable_timing=True); b = torch.cuda.Event(enable_timing=True)
-    a.record(cur)
-    for st in streams:
-        st.wait_stream(cur)
-    for i in range(reps):
-        two(i)
-    for st in streams:
-        cur.wait_stream(st)
-    b.record(cur)
-    torch.cuda.synchronize()
-    ms2 = a.elapsed_time(b) / reps
+    ms2 = _time_streams(two, streams, reps, warm, torch)
     by = B * H * L * 4 + 3 * H * m * 8 + H * 4 + 2 * B * H * m * 8
     ex["cfg3_statepass_f16"] = {"ms": ms, "gelem_per_s": B * H * L / ms / 1e6, "GB_s": by / ms / 1e6,
                                 "pct_hbm_peak": 100 * by / ms / 1e6 / HBM_PEAK_GBS,
