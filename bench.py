@@ -10,14 +10,18 @@ HBM; K steps rotate over enough input/output buffer sets (>= 512 MB) that
 every step reads u and writes y cold (not from the 256 MB Infinity Cache).
 
 value = algorithmic bytes of one step (u + y + k once per channel + D) / time,
-in GB/s, for K independent steps issued round-robin on two HIP streams (each
+in GB/s, for K independent steps issued round-robin on three HIP streams (each
 with its own kernel buffer and workspace: one step's last workgroups share the
-chip with the next step's first); the single-stream step time is reported
-beside it.  The roofline object covers the dominant kernel (the fused conv),
-timed with HIP events over back-to-back launches on one stream.  Extra workloads (the shift
-kernel conv, the fused-limit bf16 conv, state passing at L = 128K, the layer
-forward, the small fp32 conv) are reported under "extra".  The float64 CPU
-oracle is timed on the same config-1 workload as "cpu_baseline".
+chip with the next steps' first); the single-stream step time is reported
+beside it.  The timed loops call the C entry points with prebuilt arguments
+(checked once through the Python binding first), so that host-side argument
+marshalling does not pace the GPU.  The roofline object covers the dominant
+kernel (the fused conv), timed with HIP events over back-to-back launches on
+one stream.  Extra workloads (the shift kernel conv, the fused-limit bf16 conv,
+state passing at L = 128K, the layer forward, the small fp32 conv, step mode,
+the conv backward pass, the layer with heads, the conv's scaling with H) are
+reported under "extra".  The float64 CPU oracle is timed on the same config-1
+workload as "cpu_baseline".
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--streams S] [--no-extra] [--no-cpu]
 """
@@ -73,16 +77,20 @@ def _f32(a, dev):
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
 
 
-def bench_headline(h3, steps, warmup, dev, nstreams=2):
+def bench_headline(h3, steps, warmup, dev, nstreams=3):
     """Config 1 step: kernel generation + fused FFT conv (diagonal SSM).
 
     Steps are independent batches of the workload (their own u and y buffer
     sets).  They are issued round-robin on `nstreams` HIP streams, each with its
     own kernel buffer and workspace, so the last workgroups of one step's conv
-    share the chip with the next step's kernel generation and first
+    share the chip with the next steps' kernel generation and first
     workgroups.  The timed region brackets all K steps (an event on the
     launching stream before the first, and after every stream has been joined
-    back)."""
+    back).  The arguments go through the Python binding's checks once; the
+    timed loops then call the C entry points with prebuilt arguments, because
+    the binding's marshalling (about 12 us of host time per call) would
+    otherwise pace a step whose GPU time is about 25 us."""
+    import ctypes
     import torch
     import workloads
     w = workloads.config(1)
@@ -94,43 +102,51 @@ def bench_headline(h3, steps, warmup, dev, nstreams=2):
     ys = [torch.empty_like(u0) for _ in range(nsets)]
     A, Bp, C, dt = (_f32(w.ssm.A, dev), _f32(w.ssm.B, dev), _f32(w.ssm.C, dev), _f32(w.ssm.dt, dev))
     D = _f32(w.D, dev)
+    m = A.shape[1]
     wsz = max(256, h3.workspace_size(h3.OP_FFTCONV, B, H, L, 0, 0, h3.F16))
     streams = [torch.cuda.Stream(device=dev) for _ in range(nstreams)]
     ks = [torch.empty((H, L), dtype=torch.float32, device=dev) for _ in range(nstreams)]
     wss = [torch.empty(wsz, dtype=torch.uint8, device=dev) for _ in range(nstreams)]
+    for j in range(nstreams):   # every argument set through the binding's checks once
+        with torch.cuda.stream(streams[j]):
+            h3.ssm_kernel(A, Bp, C, dt, L, out=ks[j])
+            h3.fftconv(us[j % nsets], ks[j], D, out=ys[j % nsets], workspace=wss[j])
+    torch.cuda.synchronize()
+    lib, vp = h3.lib(), ctypes.c_void_p
+    pa = [vp(t.data_ptr()) for t in (A, Bp, C, dt)]
+    pk = [vp(t.data_ptr()) for t in ks]
+    pw = [vp(t.data_ptr()) for t in wss]
+    pu = [vp(t.data_ptr()) for t in us]
+    py = [vp(t.data_ptr()) for t in ys]
+    pD = vp(D.data_ptr())
+    sp = [vp(st.cuda_stream) for st in streams]
+
+    def gen(j, st):
+        if lib.h3_ssm_kernel(pa[0], pa[1], pa[2], pa[3], H, m, L, pk[j], st):
+            raise RuntimeError("h3_ssm_kernel failed")
+
+    def conv(i, j, st):
+        if lib.h3_fftconv(pu[i % nsets], pk[j], pD, py[i % nsets], B, H, L, h3.F16, pw[j], wsz, st):
+            raise RuntimeError("h3_fftconv failed")
 
     def one(i, ns):
         j = i % ns
-        with torch.cuda.stream(streams[j]):
-            h3.ssm_kernel(A, Bp, C, dt, L, out=ks[j])
-            h3.fftconv(us[i % nsets], ks[j], D, out=ys[i % nsets], workspace=wss[j])
+        gen(j, sp[j])
+        conv(i, j, sp[j])
 
     def timed(ns):
-        for i in range(warmup):
-            one(i, ns)
-        torch.cuda.synchronize()
-        cur = torch.cuda.current_stream(dev)
-        t0 = torch.cuda.Event(enable_timing=True); t1 = torch.cuda.Event(enable_timing=True)
-        t0.record(cur)
-        for st in streams[:ns]:
-            st.wait_stream(cur)
-        for i in range(steps):
-            one(i, ns)
-        for st in streams[:ns]:
-            cur.wait_stream(st)
-        t1.record(cur)
-        torch.cuda.synchronize()
-        return t0.elapsed_time(t1) / steps
+        return _time_streams(lambda i: one(i, ns), streams[:ns], steps, warmup, torch)
 
     ms_single = timed(1)
     ms = timed(nstreams) if nstreams > 1 else ms_single
     # Per-launch duration of each kernel of the step, each timed over K
-    # back-to-back launches on one stream (torch's current stream, passed to the
-    # library by the binding).
+    # back-to-back launches on torch's current stream (events on that stream;
+    # the figure includes the dispatch gap between dependent launches, a few
+    # us, which the kernel trace does not count).
+    cur = vp(torch.cuda.current_stream(dev).cuda_stream)
     per = {
-        "ssm_kernel": _time_calls(lambda i: h3.ssm_kernel(A, Bp, C, dt, L, out=ks[0]), steps, 3),
-        "fftconv": _time_calls(lambda i: h3.fftconv(us[i % nsets], ks[0], D, out=ys[i % nsets], workspace=wss[0]),
-                               steps, 3),
+        "ssm_kernel": _time_calls(lambda i: gen(0, cur), steps, 3),
+        "fftconv": _time_calls(lambda i: conv(i, 0, cur), steps, 3),
     }
     # u + y (fp16) + k (fp32, once per channel) + D
     step_bytes = B * H * L * (2 + 2) + H * L * 4 + H * 4
@@ -462,7 +478,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--streams", type=int, default=2,
+    ap.add_argument("--streams", type=int, default=3,
                     help="HIP streams the headline steps are issued on (independent batches)")
     ap.add_argument("--no-extra", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
