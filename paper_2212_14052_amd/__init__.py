@@ -86,11 +86,20 @@ def workspace_size(op: int, B: int, H_or_d: int, L: int, m: int = 0, chunk: int 
 
 # ------------------------------------------------------------- helpers -----
 def _ptr(t: Optional[torch.Tensor]):
-    return None if t is None else ctypes.c_void_p(t.data_ptr())
+    # a plain int: the c_void_p argtypes convert it
+    return None if t is None else t.data_ptr()
+
+
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
 
 
 def _stream(dev: torch.device):
-    return ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+    """The current HIP stream of `dev` as an int (the raw-stream accessor is
+    the cheap path: this runs on every call)."""
+    idx = dev.index if dev.index is not None else torch.cuda.current_device()
+    if _raw_stream is not None:
+        return _raw_stream(idx)
+    return torch.cuda.current_stream(idx).cuda_stream
 
 
 def _check(fn: str, status: int):
