@@ -86,13 +86,17 @@ __global__ __launch_bounds__(CS_THREADS) void chunk_states_kernel(const void *u_
 }
 
 // ------------------------------------------------- chunk sums, MFMA form ---
-// Same sums for 16-bit input and chunk % 1024 == 0.  Per channel,
-//   R[n][a] = sum_{b<64} Abar_n^{63-b} u_{64 a + b}
+// Same sums for 16-bit input and chunk % 1024 == 0.  Per channel, with blocks
+// of BW = 128 inputs (64 when chunk % 2048 != 0),
+//   R[n][a] = sum_{b<BW} Abar_n^{BW-1-b} u_{BW a + b}
 // is a real matrix product (rows: Re / Im of 64 modes; reduction b; columns
-// a = 0 .. N'/64 - 1) on 16x16x32 MFMAs with the powers in 16-bit and the
+// a = 0 .. N'/BW - 1) on 16x16x32 MFMAs with the powers in 16-bit and the
 // input as it is stored; then
-//   s[n] = Bbar_n sum_a Abar_n^{N' - 64 (a + 1)} R[n][a]
-// in fp32 with the weights held in registers (powers in float64 first).
+//   s[n] = Bbar_n sum_a Abar_n^{N' - BW (a + 1)} R[n][a]
+// in fp32 with the weights held in registers (powers in float64 first).  The
+// second sum is the VALU's share (a complex multiply-add and a weight update
+// per mode and column), so the wider block halves it at the same matrix-core
+// work.
 // Workgroup: one channel and a set of its chunk rows; wave w owns modes
 // 16 w .. 16 w + 15 (row tile w of the real parts, w + 4 of the imaginary).
 // The chunk row is staged once in LDS (16-byte coalesced) for all four waves.
@@ -120,8 +124,12 @@ __device__ __forceinline__ sp_f4 sp_mfma(uint4 a, uint4 b, sp_f4 c) {
     else
         return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(sp_h8, a), __builtin_bit_cast(sp_h8, b), c, 0, 0, 0);
 }
+// (the empty asm keeps a float that came from a double opaque: otherwise the
+// two roundings fold into one float64 -> 16-bit conversion, a long integer
+// sequence instead of one instruction)
 template <int DT>
 __device__ __forceinline__ uint32_t sp_pack(float lo, float hi) {
+    asm("" : "+v"(lo), "+v"(hi));
     if constexpr (DT == BF16) {
         typedef __bf16 b2 __attribute__((ext_vector_type(2)));
         b2 v = {(__bf16)lo, (__bf16)hi};
@@ -133,34 +141,37 @@ __device__ __forceinline__ uint32_t sp_pack(float lo, float hi) {
     }
 }
 
-constexpr int SPM_NA = 128;    // columns a for chunk 8192; general: chunk / 64
+constexpr int SPM_CHUNK = 8192;   // largest chunk of the matrix-core form
 
-template <int DT>
+template <int DT, int BW>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void chunk_states_mfma(const uint16_t *u, const float *Abar,
                                                          const float *Bbar, int B, int H, int L,
                                                          int m, int chunk, int wg_per_ch,
                                                          float2 *states) {
-    __shared__ __attribute__((aligned(16))) uint16_t us[2][SPM_NA * 72];   // rows of 64 + 8 pad
+    constexpr int KS = BW / 32;                 // 32-wide reduction steps per block
+    constexpr int LD = BW + 8;                  // LDS row pitch (8 pad: 16 rows' 16-byte reads hit distinct banks)
+    constexpr int NA_MAX = SPM_CHUNK / BW;
+    __shared__ __attribute__((aligned(16))) uint16_t us[2][NA_MAX * LD];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int r16 = lane & 15, kg = lane >> 4;
     const int h = blockIdx.x / wg_per_ch, part = blockIdx.x % wg_per_ch;
     const int nchunk = L / chunk;
-    const int NA = chunk / 64;          // columns a, multiple of 16
+    const int NA = chunk / BW;          // columns a, multiple of 16
     const int NCT = NA / 16;            // column tiles
     const int rows_per_ch = B * nchunk;
     const int per = (rows_per_ch + wg_per_ch - 1) / wg_per_ch;
     const int r0 = part * per, r1 = min(r0 + per, rows_per_ch);
 
     // A operand (powers, 16-bit): rows n = 16 w + r16, reduction b = 32 ks + 8 kg + i
-    uint4 Are[2], Aim[2];
+    uint4 Are[KS], Aim[KS];
     {
         const int n = 16 * w + r16;
         double2 z = make_double2(0.0, 0.0);
         if (n < m) z = make_double2(Abar[2 * ((long)h * m + n)], Abar[2 * ((long)h * m + n) + 1]);
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            // b from 32 ks + 8 kg + 7 down to 32 ks + 8 kg: exponents 63 - b ascending
-            double2 p = sp_zpow(z, 63 - (32 * ks + 8 * kg + 7));
+        for (int ks = 0; ks < KS; ++ks) {
+            // b from 32 ks + 8 kg + 7 down to 32 ks + 8 kg: exponents BW - 1 - b ascending
+            double2 p = sp_zpow(z, BW - 1 - (32 * ks + 8 * kg + 7));
             float pr[8], pi[8];
 #pragma unroll
             for (int i = 7; i >= 0; --i) {
@@ -173,10 +184,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void c
         }
     }
     // E weights for the lane's outputs: modes n = 16 w + 4 kg + j, columns
-    // a = 16 ct + r16, weight Abar_n^{chunk - 64 (a + 1)}.  Column tiles run
-    // from the last down, the weight growing by Abar_n^1024 per tile (fp32;
+    // a = 16 ct + r16, weight Abar_n^{chunk - BW (a + 1)}.  Column tiles run
+    // from the last down, the weight growing by Abar_n^{16 BW} per tile (fp32;
     // the starting weight and the step in float64 first).
-    float2 E0[4], Z1024[4];
+    float2 E0[4], Zstep[4];
     float2 Bb[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -188,10 +199,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void c
             z = make_double2(Abar[2 * i], Abar[2 * i + 1]);
             Bb[j] = make_float2(Bbar[2 * i], Bbar[2 * i + 1]);
         }
-        const double2 z1024 = sp_zpow(z, 1024);
-        const double2 p = sp_zpow(z, chunk - 64 * (16 * (NCT - 1) + r16 + 1));
+        const double2 zstep = sp_zpow(z, 16 * BW);
+        const double2 p = sp_zpow(z, chunk - BW * (16 * (NCT - 1) + r16 + 1));
         E0[j] = make_float2((float)p.x, (float)p.y);
-        Z1024[j] = make_float2((float)z1024.x, (float)z1024.y);
+        Zstep[j] = make_float2((float)zstep.x, (float)zstep.y);
     }
 
     // A chunk row is chunk / 8 <= 1024 16-byte pieces: piece i = tid + 256 q,
@@ -212,8 +223,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void c
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int i = tid + 256 * q;
-            // row a = i / 8 (64 elements) padded by 8 elements to spread banks
-            if (i < npiece) *(uint4 *)&us[buf][(i >> 3) * 72 + 8 * (i & 7)] = pf[q];
+            // row a = i / (BW / 8) (BW elements) padded by 8 elements to spread banks
+            if (i < npiece) *(uint4 *)&us[buf][(i / (BW / 8)) * LD + 8 * (i % (BW / 8))] = pf[q];
         }
     };
     if (r0 < r1) {
@@ -227,13 +238,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void c
         sp_f4 sre = {0.f, 0.f, 0.f, 0.f}, sim = {0.f, 0.f, 0.f, 0.f};
         float2 E[4] = {E0[0], E0[1], E0[2], E0[3]};
 #pragma unroll
-        for (int ct = SPM_NA / 16 - 1; ct >= 0; --ct) {
+        for (int ct = NA_MAX / 16 - 1; ct >= 0; --ct) {
             if (ct < NCT) {
                 sp_f4 accr = {0.f, 0.f, 0.f, 0.f}, acci = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int ks = 0; ks < 2; ++ks) {
+                for (int ks = 0; ks < KS; ++ks) {
                     // B operand: column a = 16 ct + r16, reduction b = 32 ks + 8 kg .. + 7
-                    const uint4 bv = *(const uint4 *)&us[buf][(16 * ct + r16) * 72 + 32 * ks + 8 * kg];
+                    const uint4 bv = *(const uint4 *)&us[buf][(16 * ct + r16) * LD + 32 * ks + 8 * kg];
                     accr = sp_mfma<DT>(Are[ks], bv, accr);
                     acci = sp_mfma<DT>(Aim[ks], bv, acci);
                 }
@@ -242,7 +253,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void c
                 for (int j = 0; j < 4; ++j) {
                     sre[j] = fmaf(E[j].x, accr[j], fmaf(-E[j].y, acci[j], sre[j]));
                     sim[j] = fmaf(E[j].x, acci[j], fmaf(E[j].y, accr[j], sim[j]));
-                    E[j] = cmul(E[j], Z1024[j]);
+                    E[j] = cmul(E[j], Zstep[j]);
                 }
             }
         }
@@ -271,7 +282,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void c
 }
 
 bool chunk_states_mfma_ok(int chunk, int dtype) {
-    return (dtype == F16 || dtype == BF16) && chunk % 1024 == 0 && chunk / 64 <= SPM_NA;
+    return (dtype == F16 || dtype == BF16) && chunk % 1024 == 0 && chunk <= SPM_CHUNK;
 }
 
 hipError_t launch_chunk_states_mfma(const void *u, const float *Abar, const float *Bbar, int B, int H,
@@ -280,10 +291,19 @@ hipError_t launch_chunk_states_mfma(const void *u, const float *Abar, const floa
     int wg = 1;
     while (H * wg < 1024 && rows_per_ch / (2 * wg) >= 4) wg *= 2;
     dim3 grid(H * wg), block(256);
-    if (dtype == BF16)
-        hipLaunchKernelGGL(chunk_states_mfma<BF16>, grid, block, 0, s, (const uint16_t *)u, Abar, Bbar, B, H, L, m, chunk, wg, states);
-    else
-        hipLaunchKernelGGL(chunk_states_mfma<F16>, grid, block, 0, s, (const uint16_t *)u, Abar, Bbar, B, H, L, m, chunk, wg, states);
+    const uint16_t *u16 = (const uint16_t *)u;
+    const bool wide = chunk % 2048 == 0;   // 128-wide blocks need 16 columns per tile: chunk / 128 % 16 == 0
+    if (dtype == BF16) {
+        if (wide)
+            hipLaunchKernelGGL((chunk_states_mfma<BF16, 128>), grid, block, 0, s, u16, Abar, Bbar, B, H, L, m, chunk, wg, states);
+        else
+            hipLaunchKernelGGL((chunk_states_mfma<BF16, 64>), grid, block, 0, s, u16, Abar, Bbar, B, H, L, m, chunk, wg, states);
+    } else {
+        if (wide)
+            hipLaunchKernelGGL((chunk_states_mfma<F16, 128>), grid, block, 0, s, u16, Abar, Bbar, B, H, L, m, chunk, wg, states);
+        else
+            hipLaunchKernelGGL((chunk_states_mfma<F16, 64>), grid, block, 0, s, u16, Abar, Bbar, B, H, L, m, chunk, wg, states);
+    }
     return hipGetLastError();
 }
 
