@@ -141,16 +141,20 @@ __device__ __forceinline__ uint32_t sp_pack(float lo, float hi) {
     }
 }
 
-constexpr int SPM_CHUNK = 8192;   // largest chunk of the matrix-core form
+constexpr int SPM_CHUNK = 16384;   // largest chunk of the matrix-core form
 
-template <int DT, int BW>
+// CMAX: the largest chunk an instance handles; it sizes the two LDS row
+// buffers (2 CMAX (1 + 8 / BW) 16-bit values: 34.8 KB at 8192, 69.6 KB at
+// 16384), so chunks up to 8192 keep the smaller instance and its occupancy.
+template <int DT, int BW, int CMAX>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void chunk_states_mfma(const uint16_t *u, const float *Abar,
                                                          const float *Bbar, int B, int H, int L,
                                                          int m, int chunk, int wg_per_ch,
                                                          float2 *states) {
     constexpr int KS = BW / 32;                 // 32-wide reduction steps per block
     constexpr int LD = BW + 8;                  // LDS row pitch (8 pad: 16 rows' 16-byte reads hit distinct banks)
-    constexpr int NA_MAX = SPM_CHUNK / BW;
+    constexpr int NA_MAX = CMAX / BW;
+    constexpr int NPF = CMAX / 8 / 256;         // 16-byte pieces of a row per thread
     __shared__ __attribute__((aligned(16))) uint16_t us[2][NA_MAX * LD];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int r16 = lane & 15, kg = lane >> 4;
@@ -205,23 +209,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void c
         Zstep[j] = make_float2((float)zstep.x, (float)zstep.y);
     }
 
-    // A chunk row is chunk / 8 <= 1024 16-byte pieces: piece i = tid + 256 q,
-    // q < 4, loaded one row ahead into registers (so the loads overlap a
+    // A chunk row is chunk / 8 <= 256 NPF 16-byte pieces: piece i = tid + 256 q,
+    // q < NPF, loaded one row ahead into registers (so the loads overlap a
     // whole row's compute) and stored into the other LDS buffer after it.
     const int npiece = chunk / 8;
-    uint4 pf[4];
+    uint4 pf[NPF];
     auto load_row = [&](int rr) {
         const int bb = rr / nchunk, cc = rr % nchunk;
         const uint16_t *src = u + ((long)bb * H + h) * L + (long)cc * chunk;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
+        for (int q = 0; q < NPF; ++q) {
             const int i = tid + 256 * q;
             pf[q] = i < npiece ? *(const uint4 *)(src + 8 * i) : make_uint4(0, 0, 0, 0);
         }
     };
     auto store_row = [&](int buf) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
+        for (int q = 0; q < NPF; ++q) {
             const int i = tid + 256 * q;
             // row a = i / (BW / 8) (BW elements) padded by 8 elements to spread banks
             if (i < npiece) *(uint4 *)&us[buf][(i / (BW / 8)) * LD + 8 * (i % (BW / 8))] = pf[q];
@@ -293,16 +297,21 @@ hipError_t launch_chunk_states_mfma(const void *u, const float *Abar, const floa
     dim3 grid(H * wg), block(256);
     const uint16_t *u16 = (const uint16_t *)u;
     const bool wide = chunk % 2048 == 0;   // 128-wide blocks need 16 columns per tile: chunk / 128 % 16 == 0
+    const bool big = chunk > 8192;         // multiple of 2048 here, so wide
     if (dtype == BF16) {
-        if (wide)
-            hipLaunchKernelGGL((chunk_states_mfma<BF16, 128>), grid, block, 0, s, u16, Abar, Bbar, B, H, L, m, chunk, wg, states);
+        if (big)
+            hipLaunchKernelGGL((chunk_states_mfma<BF16, 128, 16384>), grid, block, 0, s, u16, Abar, Bbar, B, H, L, m, chunk, wg, states);
+        else if (wide)
+            hipLaunchKernelGGL((chunk_states_mfma<BF16, 128, 8192>), grid, block, 0, s, u16, Abar, Bbar, B, H, L, m, chunk, wg, states);
         else
-            hipLaunchKernelGGL((chunk_states_mfma<BF16, 64>), grid, block, 0, s, u16, Abar, Bbar, B, H, L, m, chunk, wg, states);
+            hipLaunchKernelGGL((chunk_states_mfma<BF16, 64, 8192>), grid, block, 0, s, u16, Abar, Bbar, B, H, L, m, chunk, wg, states);
     } else {
-        if (wide)
-            hipLaunchKernelGGL((chunk_states_mfma<F16, 128>), grid, block, 0, s, u16, Abar, Bbar, B, H, L, m, chunk, wg, states);
+        if (big)
+            hipLaunchKernelGGL((chunk_states_mfma<F16, 128, 16384>), grid, block, 0, s, u16, Abar, Bbar, B, H, L, m, chunk, wg, states);
+        else if (wide)
+            hipLaunchKernelGGL((chunk_states_mfma<F16, 128, 8192>), grid, block, 0, s, u16, Abar, Bbar, B, H, L, m, chunk, wg, states);
         else
-            hipLaunchKernelGGL((chunk_states_mfma<F16, 64>), grid, block, 0, s, u16, Abar, Bbar, B, H, L, m, chunk, wg, states);
+            hipLaunchKernelGGL((chunk_states_mfma<F16, 64, 8192>), grid, block, 0, s, u16, Abar, Bbar, B, H, L, m, chunk, wg, states);
     }
     return hipGetLastError();
 }
