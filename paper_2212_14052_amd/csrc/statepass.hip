@@ -327,15 +327,18 @@ hipError_t launch_chunk_states_mfma(const void *u, const float *Abar, const floa
 // per chunk row W is scaled by a power of two to max |W| in [1/2, 1) before
 // rounding to fp16, and the scale is undone in fp32.  Output in the I/O dtype.
 // Workgroup (4 waves): one channel, a set of its chunk rows; wave w owns
-// tiles a = 16 (2w) .. 16 (2w + 1) + 15 of every chunk, all 64 columns b.
+// tiles a = 16 (TPW w) .. 16 (TPW (w + 1)) - 1 of every chunk (TPW = NAM / 64
+// tiles per wave), all 64 columns b.  NAM = 128 serves chunks up to 8192, 256
+// chunks up to 16384 (the E table then takes 69.6 KB of LDS instead of 34.8).
 typedef _Float16 cr_h2 __attribute__((ext_vector_type(2)));
-constexpr int CR_NA = 128;
+constexpr int CR_NA = 256;   // largest a-range (chunk / 64) of the matrix-core form
 
-template <int DT>
+template <int DT, int NAM>
 __global__ __launch_bounds__(256) void state_correction_mfma(const float *Abar, const float2 *corr_W,
                                                              int B, int H, int m, int chunk, int nchunk,
                                                              int wg_per_ch, uint16_t *corr) {
-    __shared__ __attribute__((aligned(16))) uint32_t Et[CR_NA][64 + 4];     // E[a][n], fp16 complex
+    constexpr int TPW = NAM / 64;
+    __shared__ __attribute__((aligned(16))) uint32_t Et[NAM][64 + 4];       // E[a][n], fp16 complex
     __shared__ __attribute__((aligned(16))) uint16_t Qt[64][128 + 8];       // Qm[k][b] as [b][k]
     __shared__ float2 Ws[64];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -385,10 +388,10 @@ __global__ __launch_bounds__(256) void state_correction_mfma(const float *Abar, 
         wv = make_float2(ldexpf(wv.x, -ew), ldexpf(wv.y, -ew));
         if (w == 0) Ws[lane] = wv;
         __syncthreads();
-        // wave w: a-tiles 2w, 2w+1
+        // wave w: a-tiles TPW w .. TPW w + TPW - 1
 #pragma unroll
-        for (int at2 = 0; at2 < 2; ++at2) {
-            const int at = 2 * w + at2;
+        for (int at2 = 0; at2 < TPW; ++at2) {
+            const int at = TPW * w + at2;
             if (16 * at >= NA) break;
             const int a = 16 * at + r16;
             // A fragments: k = 32 ks + 8 kg + i; n = k mod 64
@@ -454,10 +457,18 @@ hipError_t launch_state_correction_mfma(const float *Abar, const float2 *corr_W,
     int wg = 1;
     while (H * wg < 1024 && rows_per_ch / (2 * wg) >= 4) wg *= 2;
     dim3 grid(H * wg), block(256);
-    if (dtype == BF16)
-        hipLaunchKernelGGL(state_correction_mfma<BF16>, grid, block, 0, s, Abar, corr_W, B, H, m, chunk, nchunk, wg, (uint16_t *)corr);
-    else
-        hipLaunchKernelGGL(state_correction_mfma<F16>, grid, block, 0, s, Abar, corr_W, B, H, m, chunk, nchunk, wg, (uint16_t *)corr);
+    const bool big = chunk / 64 > 128;
+    if (dtype == BF16) {
+        if (big)
+            hipLaunchKernelGGL((state_correction_mfma<BF16, 256>), grid, block, 0, s, Abar, corr_W, B, H, m, chunk, nchunk, wg, (uint16_t *)corr);
+        else
+            hipLaunchKernelGGL((state_correction_mfma<BF16, 128>), grid, block, 0, s, Abar, corr_W, B, H, m, chunk, nchunk, wg, (uint16_t *)corr);
+    } else {
+        if (big)
+            hipLaunchKernelGGL((state_correction_mfma<F16, 256>), grid, block, 0, s, Abar, corr_W, B, H, m, chunk, nchunk, wg, (uint16_t *)corr);
+        else
+            hipLaunchKernelGGL((state_correction_mfma<F16, 128>), grid, block, 0, s, Abar, corr_W, B, H, m, chunk, nchunk, wg, (uint16_t *)corr);
+    }
     return hipGetLastError();
 }
 
