@@ -293,6 +293,22 @@ def _extra_cfg2(h3, dev, reps, warm, ex, np, torch, workloads):
     by = B * H * L * 4 + H * L * 4 + H * 4
     ex["cfg2_fused_limit_bf16"] = {"ms": ms, "GB_s": by / ms / 1e6, "pct_hbm_peak": 100 * by / ms / 1e6 / HBM_PEAK_GBS,
                                    "gelem_per_s": B * H * L / ms / 1e6}
+    # independent steps round-robin on three streams (own kernel buffer and
+    # workspace each), as in the headline step
+    ns = 3
+    streams = [torch.cuda.Stream(device=dev) for _ in range(ns)]
+    ks = [k] + [torch.empty_like(k) for _ in range(ns - 1)]
+    wss = [ws] + [torch.empty_like(ws) for _ in range(ns - 1)]
+
+    def multi(i):
+        j = i % ns
+        with torch.cuda.stream(streams[j]):
+            h3.ssm_kernel(A, Bp, C, dt, L, out=ks[j])
+            h3.fftconv(us[i % nsets], ks[j], D, out=ys[i % nsets], workspace=wss[j])
+
+    ms3 = _time_streams(multi, streams, reps, warm, torch)
+    ex["cfg2_fused_limit_bf16"].update({"three_streams_ms_per_step": ms3, "three_streams_GB_s": by / ms3 / 1e6,
+                                        "three_streams_pct_hbm_peak": 100 * by / ms3 / 1e6 / HBM_PEAK_GBS})
 
 
 def _extra_cfg3(h3, dev, reps, warm, ex, np, torch, workloads):
