@@ -365,7 +365,7 @@ def _extra_cfg4(h3, dev, reps, warm, ex, np, torch, workloads):
     w = workloads.config(4)
     B, L, d = w.B, w.L, w.d
     x = _dev_tensor(w.x, w.dtype, dev)
-    W = {n: _dev_tensor(w.weight_out_in(n), w.dtype, dev) for n in "qkvo"}
+    W = {n: _dev_tensor(w.W[n][0], w.dtype, dev) for n in "qkvo"}
     A, Bp, C, dt = (_f32(w.diag.A, dev), _f32(w.diag.B, dev), _f32(w.diag.C, dev), _f32(w.diag.dt, dev))
     dk = h3.ssm_kernel(A, Bp, C, dt, L)
     sC = _f32(w.shift_C, dev); dD = _f32(w.diag_D, dev)
@@ -384,7 +384,7 @@ def _extra_heads(h3, dev, reps, warm, ex, np, torch, workloads):
     w = workloads.config(4)
     B, L, d, dh = w.B, w.L, w.d, 8
     x = _dev_tensor(w.x, w.dtype, dev)
-    W = {n: _dev_tensor(w.weight_out_in(n), w.dtype, dev) for n in "qkvo"}
+    W = {n: _dev_tensor(w.W[n][0], w.dtype, dev) for n in "qkvo"}
     ssm = workloads.make_diag_ssm(np.random.default_rng(12), d * dh, 64, 1e-3, 1e-1)
     dk = h3.ssm_kernel(_f32(ssm.A, dev), _f32(ssm.B, dev), _f32(ssm.C, dev), _f32(ssm.dt, dev), L)
     dD = _f32(np.random.default_rng(13).standard_normal(d * dh), dev)

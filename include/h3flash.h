@@ -6,9 +6,10 @@
  *  - Every tensor pointer is a DEVICE pointer owned by the caller.  Scratch
  *    space is passed in as `workspace` (size it with h3_workspace_size) and
  *    must not alias any other argument.  The library's own kernels allocate no
- *    device memory; h3_layer_fwd's projections run through hipBLASLt, whose
- *    per-device handle (created on the first layer call on a device and kept
- *    until the process ends) may hold memory of its own.
+ *    device memory.  Departure from a stateless library: h3_layer_fwd's
+ *    projections run through hipBLASLt, whose per-device handle (created on
+ *    the first layer call on a device and kept until the process ends) may
+ *    hold memory of its own.
  *  - Complex values are interleaved (re, im) float32 pairs.
  *  - Tensors are dense, row-major, with the last dimension contiguous.
  *    Sequence tensors are (B, H, L): row (b, h) is L contiguous elements.
@@ -102,7 +103,7 @@ int h3_fftconv(const void *u, const float *k, const float *D, void *y,
  * f = 0..L (the non-redundant half of the length-2L DFT of the zero-padded
  * kernel, with the inverse transform's 1/2L folded in).
  *   k (H, L) float32.  Kspec (H, L+1) complex, written.
- *   L power of two in [H3_MIN_LEN, H3_FUSED_LIMIT].
+ *   L power of two in [H3_MIN_LEN, H3_FUSED_LIMIT_F32].
  * Errors: EINVAL, EUNSUPPORTED (L), EDEVICE.
  */
 int h3_kernel_spectrum(const float *k, int H, int L, float *Kspec, void *stream);
@@ -111,7 +112,8 @@ int h3_kernel_spectrum(const float *k, int H, int L, float *Kspec, void *stream)
  * h3_fftconv_spectral — the fused convolution of h3_fftconv given the kernel
  * spectrum from h3_kernel_spectrum (no workspace needed).
  *   u, y (B, H, L) of `dtype`, not overlapping.  Kspec (H, L+1) complex.
- *   D (H) float32 or NULL.
+ *   D (H) float32 or NULL.  L as for h3_kernel_spectrum (the float32-VALU
+ *   convolution runs, for every dtype).
  * Errors: EINVAL, EUNSUPPORTED (L, dtype), EDEVICE.
  */
 int h3_fftconv_spectral(const void *u, const float *Kspec, const float *D, void *y,
@@ -131,7 +133,9 @@ int h3_fftconv_spectral(const void *u, const float *Kspec, const float *D, void 
  *   x0          (B, H, m) complex, or NULL for the zero state.
  *   x_final     (B, H, m) complex written, or NULL.
  *   chunk       power of two in [H3_MIN_LEN, H3_FUSED_LIMIT] dividing L.
- *   workspace >= h3_workspace_size(H3_OP_STATEPASS, B, H, L, m, chunk, dtype).
+ *   workspace >= h3_workspace_size(H3_OP_STATEPASS, B, H, L, m, chunk, dtype)
+ *   (the chunk kernel, the chunk end-states and the initial-state term's
+ *   inputs; its contents on entry do not matter).
  * Errors: EINVAL (null, sizes, L % chunk), EUNSUPPORTED (chunk, m, dtype),
  *         EWORKSPACE, EDEVICE.
  */
@@ -188,22 +192,25 @@ int h3_ssm_step(const void *u, const float *Abar, const float *Bbar, const float
 /*
  * h3_layer_fwd — H3 layer forward with head dimension 1 (Sec. 3.2,
  * Algorithm 1):
- *   Q = x Wq^T, K = x Wk^T, V = x Wv^T     (Q[b,t,c] = sum_j x[b,t,j] Wq[c,j])
+ *   Q = x Wq, K = x Wk, V = x Wv           (Q[b,t,c] = sum_j x[b,t,j] Wq[j,c])
  *   Kbar = SSM_shift(K): Kbar_t = sum_{j<m_s} shift_C[c,j] K_{t-j} + shift_D[c] K_t
  *   G = Kbar * V;  S = SSM_diag(G) = diag_k[c] (*) G + diag_D[c] G   (causal conv)
- *   out = (Q * S) Wo^T
+ *   out = (Q * S) Wo
  *   x, out   (B, L, d) of `dtype` (H3_F16 or H3_BF16); must not overlap.
- *   Wq, Wk, Wv, Wo  (d, d) of `dtype`, stored (out, in) as a linear layer's
- *   weight: the paper's projection matrices transposed.  Must not overlap
- *   out or the workspace.
+ *   Wq, Wk, Wv, Wo  (d, d) of `dtype`, row-major as Algorithm 1 writes the
+ *   projections (rows index the input features, columns the output
+ *   features).  Must not overlap out or the workspace.
  *   shift_C  (d, m_s) float32, m_s in [1, H3_MAX_SHIFT].  shift_D (d) or NULL.
  *   diag_k   (d, L) float32 (e.g. from h3_ssm_kernel).  diag_D (d) or NULL.
- *   L power of two in [H3_MIN_LEN, H3_FUSED_LIMIT]; d a multiple of 64.
+ *   L power of two in [H3_MIN_LEN, H3_FUSED_LIMIT]; d a multiple of 128;
+ *   B * L a multiple of 128 (the tiles of the library's own GEMM).
  *   workspace >= h3_workspace_size(H3_OP_LAYER, B, d, L, m_s, 0, dtype).
- * The four projections run through hipBLASLt; the library's own matrix-core
- * GEMM runs instead for shapes hipBLASLt rejects, or for every call while the
- * environment variable H3FLASH_GEMM is "native" (read on each call).
- * Errors: EINVAL, EUNSUPPORTED (L, d, m_s, dtype), EWORKSPACE, EDEVICE.
+ * The four projections run through hipBLASLt, which reads the weights as they
+ * are stored (transposed operands); the library's own matrix-core GEMM runs
+ * instead for shapes hipBLASLt rejects, or for every call while the
+ * environment variable H3FLASH_GEMM is "native" (read on each call), on
+ * transposed copies of the weights made in the workspace.
+ * Errors: EINVAL, EUNSUPPORTED (L, d, B * L, m_s, dtype), EWORKSPACE, EDEVICE.
  */
 int h3_layer_fwd(const void *x, const void *Wq, const void *Wk, const void *Wv,
                  const void *Wo, const float *shift_C, const float *shift_D,
@@ -222,7 +229,8 @@ int h3_layer_fwd(const void *x, const void *Wq, const void *Wk, const void *Wv,
  * out = O Wo^T.
  *   Arguments as for h3_layer_fwd, except diag_k (d d_head, L) float32 and
  *   diag_D (d d_head) or NULL.  d_head in {1, 2, 4, 8} (1 is h3_layer_fwd);
- *   for d_head > 1, L is a power of two in [64, H3_FUSED_LIMIT].
+ *   for d_head > 1, L is a power of two in [64, H3_FUSED_LIMIT].  d and B * L
+ *   multiples of 128 as for h3_layer_fwd.
  *   workspace >= h3_workspace_size(H3_OP_LAYER_HEADS, B, d, L, m_s, d_head, dtype).
  * Errors: EINVAL, EUNSUPPORTED (L, d, d_head, m_s, dtype), EWORKSPACE, EDEVICE.
  */

@@ -130,18 +130,62 @@ def _dtype(t: torch.Tensor) -> int:
 
 def _workspace(nbytes: int, dev: torch.device, workspace: Optional[torch.Tensor]) -> torch.Tensor:
     if workspace is not None:
+        _on(dev, workspace=workspace)
+        if not workspace.is_contiguous():
+            raise ValueError("workspace must be contiguous")
         if workspace.numel() * workspace.element_size() < nbytes:
             raise ValueError("workspace too small")
         return workspace
     return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
 
 
+# ----------------------------------------------------------- validation ----
+# The C ABI receives bare pointers and cannot see sizes, devices or strides:
+# every tensor is checked here before anything is launched.
+def _gpu(name: str, t: torch.Tensor) -> torch.device:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a GPU tensor (got {t.device})")
+    return t.device
+
+
+def _on(dev: torch.device, **ts):
+    for name, t in ts.items():
+        if t is None:
+            continue
+        if not isinstance(t, torch.Tensor):
+            raise TypeError(f"{name} must be a torch.Tensor")
+        if t.device != dev:
+            raise ValueError(f"{name} must be on {dev} (got {t.device})")
+
+
+def _shape(name: str, t: Optional[torch.Tensor], shape):
+    if t is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)} (got {tuple(t.shape)})")
+
+
+def _out(name: str, t: Optional[torch.Tensor], shape, dtype, dev):
+    """A caller-supplied output: exact shape, dtype, device, contiguous."""
+    if t is None:
+        return
+    _on(dev, **{name: t})
+    _shape(name, t, shape)
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype} (got {t.dtype})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
 # ----------------------------------------------------------------- ops -----
 def ssm_discretize(A: torch.Tensor, B: torch.Tensor, dt: torch.Tensor):
     """ZOH: Abar = exp(dt A), Bbar = (exp(dt A) - 1)/A * B.  Returns (Abar, Bbar)
     as float32 (H, m, 2)."""
+    dev = _gpu("A", A)
     A, B, dt = _cplx(A), _cplx(B), _f32(dt)
+    _on(dev, B=B, dt=dt)
     H, m = A.shape[0], A.shape[1]
+    _shape("A", A, (H, m, 2)); _shape("B", B, (H, m, 2)); _shape("dt", dt, (H,))
     Ab = torch.empty_like(A); Bb = torch.empty_like(A)
     _check("h3_ssm_discretize", lib().h3_ssm_discretize(
         _ptr(A), _ptr(B), _ptr(dt), H, m, _ptr(Ab), _ptr(Bb), _stream(A.device)))
@@ -151,8 +195,14 @@ def ssm_discretize(A: torch.Tensor, B: torch.Tensor, dt: torch.Tensor):
 def ssm_kernel(A: torch.Tensor, B: torch.Tensor, C: torch.Tensor, dt: torch.Tensor, L: int,
                out: Optional[torch.Tensor] = None) -> torch.Tensor:
     """k[h, t] = 2 Re sum_n C Bbar exp(t dt A), (H, L) float32."""
+    dev = _gpu("A", A)
     A, B, C, dt = _cplx(A), _cplx(B), _cplx(C), _f32(dt)
+    _on(dev, B=B, C=C, dt=dt)
     H, m = A.shape[0], A.shape[1]
+    for n, t in (("A", A), ("B", B), ("C", C)):
+        _shape(n, t, (H, m, 2))
+    _shape("dt", dt, (H,))
+    _out("out", out, (H, L), torch.float32, dev)
     k = out if out is not None else torch.empty((H, L), dtype=torch.float32, device=A.device)
     _check("h3_ssm_kernel", lib().h3_ssm_kernel(
         _ptr(A), _ptr(B), _ptr(C), _ptr(dt), H, m, L, _ptr(k), _stream(A.device)))
@@ -163,10 +213,16 @@ def fftconv(u: torch.Tensor, k: torch.Tensor, D: Optional[torch.Tensor] = None,
             out: Optional[torch.Tensor] = None,
             workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
     """y = causal_conv(u, k) + D u over (B, H, L) rows, fused FFT."""
+    dev = _gpu("u", u)
     u = u.contiguous()
+    if u.dim() != 3:
+        raise ValueError("u must be (B, H, L)")
     Bn, H, L = u.shape
     k, D = _f32(k), _f32(D)
     dt = _dtype(u)
+    _on(dev, k=k, D=D)
+    _shape("k", k, (H, L)); _shape("D", D, (H,))
+    _out("out", out, u.shape, u.dtype, dev)
     y = out if out is not None else torch.empty_like(u)
     ws = _workspace(workspace_size(OP_FFTCONV, Bn, H, L, 0, 0, dt), u.device, workspace)
     _check("h3_fftconv", lib().h3_fftconv(
@@ -178,8 +234,12 @@ def fftconv(u: torch.Tensor, k: torch.Tensor, D: Optional[torch.Tensor] = None,
 def kernel_spectrum(k: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Kspec[h, f] = DFT_{2L}(k[h] zero-padded)[f] / 2L for f = 0..L; returns
     float32 (H, L+1, 2)."""
+    dev = _gpu("k", k)
     k = _f32(k)
+    if k.dim() != 2:
+        raise ValueError("k must be (H, L)")
     H, L = k.shape
+    _out("out", out, (H, L + 1, 2), torch.float32, dev)
     K = out if out is not None else torch.empty((H, L + 1, 2), dtype=torch.float32, device=k.device)
     _check("h3_kernel_spectrum", lib().h3_kernel_spectrum(_ptr(k), H, L, _ptr(K), _stream(k.device)))
     return K
@@ -188,10 +248,16 @@ def kernel_spectrum(k: torch.Tensor, out: Optional[torch.Tensor] = None) -> torc
 def fftconv_spectral(u: torch.Tensor, Kspec: torch.Tensor, D: Optional[torch.Tensor] = None,
                      out: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Fused convolution given the kernel spectrum from kernel_spectrum."""
+    dev = _gpu("u", u)
     u = u.contiguous()
+    if u.dim() != 3:
+        raise ValueError("u must be (B, H, L)")
     Bn, H, L = u.shape
     D = _f32(D)
     Kspec = _cplx(Kspec)
+    _on(dev, Kspec=Kspec, D=D)
+    _shape("Kspec", Kspec, (H, L + 1, 2)); _shape("D", D, (H,))
+    _out("out", out, u.shape, u.dtype, dev)
     y = out if out is not None else torch.empty_like(u)
     _check("h3_fftconv_spectral", lib().h3_fftconv_spectral(
         _ptr(u), _ptr(Kspec), _ptr(D), _ptr(y), Bn, H, L, _dtype(u), _stream(u.device)))
@@ -204,12 +270,20 @@ def statepass_conv(u: torch.Tensor, Abar: torch.Tensor, Bbar: torch.Tensor, C: t
                    workspace: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
     """State passing (Algorithm 2) for the diagonal SSM (Abar, Bbar, C, D).
     Returns (y, x_final) with x_final float32 (B, H, m, 2)."""
+    dev = _gpu("u", u)
     u = u.contiguous()
+    if u.dim() != 3:
+        raise ValueError("u must be (B, H, L)")
     Bn, H, L = u.shape
     Abar, Bbar, C, D = _cplx(Abar), _cplx(Bbar), _cplx(C), _f32(D)
     m = Abar.shape[1]
     x0 = _cplx(x0) if x0 is not None else None
+    _on(dev, Abar=Abar, Bbar=Bbar, C=C, D=D, x0=x0)
+    for n, t in (("Abar", Abar), ("Bbar", Bbar), ("C", C)):
+        _shape(n, t, (H, m, 2))
+    _shape("D", D, (H,)); _shape("x0", x0, (Bn, H, m, 2))
     dt = _dtype(u)
+    _out("out", out, u.shape, u.dtype, dev)
     y = out if out is not None else torch.empty_like(u)
     xf = torch.empty((Bn, H, m, 2), dtype=torch.float32, device=u.device)
     ws = _workspace(workspace_size(OP_STATEPASS, Bn, H, L, m, chunk, dt), u.device, workspace)
@@ -224,14 +298,20 @@ def fftconv_bwd(u: Optional[torch.Tensor], k: torch.Tensor, D: Optional[torch.Te
                 workspace: Optional[torch.Tensor] = None):
     """Backward pass of fftconv for output gradient dy (B, H, L).  Returns
     (du, dk, dD); an output not asked for is None."""
+    dev = _gpu("dy", dy)
     dy = dy.contiguous()
+    if dy.dim() != 3:
+        raise ValueError("dy must be (B, H, L)")
     Bn, H, L = dy.shape
     dt = _dtype(dy)
     if u is not None:
+        _on(dev, u=u)
         u = u.contiguous()
         if u.shape != dy.shape or u.dtype != dy.dtype:
             raise ValueError("u must match dy in shape and dtype")
     k, D = _f32(k), _f32(D)
+    _on(dev, k=k, D=D)
+    _shape("k", k, (H, L)); _shape("D", D, (H,))
     du = torch.empty_like(dy) if want_du else None
     dk = torch.empty((H, L), dtype=torch.float32, device=dy.device) if want_dk else None
     dD = torch.empty((H,), dtype=torch.float32, device=dy.device) if want_dD else None
@@ -242,20 +322,38 @@ def fftconv_bwd(u: Optional[torch.Tensor], k: torch.Tensor, D: Optional[torch.Te
     return du, dk, dD
 
 
+def _layer_args(x, Wq, Wk, Wv, Wo, shift_C, shift_D, diag_k, diag_D, d_head):
+    dev = _gpu("x", x)
+    x = x.contiguous()
+    if x.dim() != 3:
+        raise ValueError("x must be (B, L, d)")
+    Bn, L, d = x.shape
+    dt = _dtype(x)
+    _on(dev, Wq=Wq, Wk=Wk, Wv=Wv, Wo=Wo)
+    Ws = [w.to(x.dtype).contiguous() for w in (Wq, Wk, Wv, Wo)]
+    for n, w in zip(("Wq", "Wk", "Wv", "Wo"), Ws):
+        _shape(n, w, (d, d))
+    shift_C = _f32(shift_C)
+    if shift_C.dim() != 2:
+        raise ValueError("shift_C must be (d, m_s)")
+    m_s = shift_C.shape[1]
+    shift_D, diag_k, diag_D = _f32(shift_D), _f32(diag_k), _f32(diag_D)
+    _on(dev, shift_C=shift_C, shift_D=shift_D, diag_k=diag_k, diag_D=diag_D)
+    _shape("shift_C", shift_C, (d, m_s)); _shape("shift_D", shift_D, (d,))
+    _shape("diag_k", diag_k, (d * d_head, L)); _shape("diag_D", diag_D, (d * d_head,))
+    return Bn, L, d, dt, Ws, shift_C, m_s, shift_D, diag_k, diag_D, x
+
+
 def layer_fwd_heads(x: torch.Tensor, Wq: torch.Tensor, Wk: torch.Tensor, Wv: torch.Tensor,
                     Wo: torch.Tensor, shift_C: torch.Tensor, shift_D: Optional[torch.Tensor],
                     diag_k: torch.Tensor, diag_D: Optional[torch.Tensor], d_head: int,
                     out: Optional[torch.Tensor] = None,
                     workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
     """H3 layer forward with heads of dimension d_head (Algorithm 1).  x: (B, L, d);
-    weights (out, in); diag_k (d d_head, L), diag_D (d d_head)."""
-    x = x.contiguous()
-    Bn, L, d = x.shape
-    dt = _dtype(x)
-    Ws = [w.to(x.dtype).contiguous() for w in (Wq, Wk, Wv, Wo)]
-    shift_C = _f32(shift_C)
-    m_s = shift_C.shape[1]
-    shift_D, diag_k, diag_D = _f32(shift_D), _f32(diag_k), _f32(diag_D)
+    weights (d, d) with Q = x Wq; diag_k (d d_head, L), diag_D (d d_head)."""
+    Bn, L, d, dt, Ws, shift_C, m_s, shift_D, diag_k, diag_D, x = _layer_args(
+        x, Wq, Wk, Wv, Wo, shift_C, shift_D, diag_k, diag_D, d_head)
+    _out("out", out, x.shape, x.dtype, x.device)
     o = out if out is not None else torch.empty_like(x)
     ws = _workspace(workspace_size(OP_LAYER_HEADS, Bn, d, L, m_s, d_head, dt), x.device, workspace)
     _check("h3_layer_fwd_heads", lib().h3_layer_fwd_heads(
@@ -270,9 +368,11 @@ def ssm_step(u: torch.Tensor, Abar: torch.Tensor, Bbar: torch.Tensor, C: torch.T
              out: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Recurrent step mode: advance the state ``x`` (B, H, m, 2) float32, in
     place, over the tokens ``u`` (B, H) or (B, H, T); returns y shaped like u."""
+    dev = _gpu("x", x)
     if x.dtype != torch.float32 or x.dim() != 4 or x.shape[-1] != 2 or not x.is_contiguous():
         raise ValueError("x must be a contiguous float32 (B, H, m, 2) tensor (it is updated in place)")
     Bn, H, m = x.shape[0], x.shape[1], x.shape[2]
+    _on(dev, u=u)
     uu = u.contiguous()
     if uu.dim() == 2:
         uu = uu.unsqueeze(-1)
@@ -280,11 +380,16 @@ def ssm_step(u: torch.Tensor, Abar: torch.Tensor, Bbar: torch.Tensor, C: torch.T
         raise ValueError("u must be (B, H) or (B, H, T) with the state's B and H")
     T = uu.shape[2]
     Abar, Bbar, C, D = _cplx(Abar), _cplx(Bbar), _cplx(C), _f32(D)
-    y = out if out is not None else torch.empty_like(u)
+    _on(dev, Abar=Abar, Bbar=Bbar, C=C, D=D)
+    for n, t in (("Abar", Abar), ("Bbar", Bbar), ("C", C)):
+        _shape(n, t, (H, m, 2))
+    _shape("D", D, (H,))
+    _out("out", out, u.shape, uu.dtype, dev)
+    y = out.view(uu.shape) if out is not None else torch.empty_like(uu)
     _check("h3_ssm_step", lib().h3_ssm_step(
         _ptr(uu), _ptr(Abar), _ptr(Bbar), _ptr(C), _ptr(D), Bn, H, m, T, _dtype(uu), _ptr(x), _ptr(y),
         _stream(x.device)))
-    return y
+    return y.view(u.shape)
 
 
 def layer_fwd(x: torch.Tensor, Wq: torch.Tensor, Wk: torch.Tensor, Wv: torch.Tensor,
@@ -293,14 +398,10 @@ def layer_fwd(x: torch.Tensor, Wq: torch.Tensor, Wk: torch.Tensor, Wv: torch.Ten
               out: Optional[torch.Tensor] = None,
               workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
     """H3 layer forward (Algorithm 1, head dimension 1).  x: (B, L, d); the
-    weights (d, d) are stored (out, in) like a linear layer's: Q = x Wq^T."""
-    x = x.contiguous()
-    Bn, L, d = x.shape
-    dt = _dtype(x)
-    Ws = [w.to(x.dtype).contiguous() for w in (Wq, Wk, Wv, Wo)]
-    shift_C = _f32(shift_C)
-    m_s = shift_C.shape[1]
-    shift_D, diag_k, diag_D = _f32(shift_D), _f32(diag_k), _f32(diag_D)
+    weights are (d, d) as Algorithm 1 writes them: Q = x Wq."""
+    Bn, L, d, dt, Ws, shift_C, m_s, shift_D, diag_k, diag_D, x = _layer_args(
+        x, Wq, Wk, Wv, Wo, shift_C, shift_D, diag_k, diag_D, 1)
+    _out("out", out, x.shape, x.dtype, x.device)
     o = out if out is not None else torch.empty_like(x)
     ws = _workspace(workspace_size(OP_LAYER, Bn, d, L, m_s, 0, dt), x.device, workspace)
     _check("h3_layer_fwd", lib().h3_layer_fwd(

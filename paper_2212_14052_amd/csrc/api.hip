@@ -40,25 +40,53 @@ bool fused_len_ok(int L, int dtype) {
 }
 
 // Workspace layouts (each region 256-byte aligned).
+//
+// State passing, by path (a region a path does not use has size 0):
+//   k       (H, chunk) float32            the chunk kernel f
+//   kspec   (H, chunk + 1) complex        its spectrum (VALU conv only)
+//   states  (B, H, nchunk, m) complex     chunk end-states s_c = M_ux u^(c)
+//   fused initial-state term (16-bit, chunk 8192): per-channel power
+//   tables ctab, normalised weights w16 (B, H, nchunk, 64) fp16 complex and
+//   their exponents wexp (B, H, nchunk);
+//   otherwise: weights corr_w (B, H, nchunk, m) complex and the term itself,
+//   corr (B, H, L), in the I/O dtype on the matrix-core paths, else float32.
 struct StatepassWs {
-    size_t k, kspec, states, corr_w, corr, total;
+    size_t k, kspec, states, corr_w, corr, ctab, w16, wexp, total;
+    bool fused, mfma, corr16;
 };
-StatepassWs statepass_ws(int B, int H, int L, int m, int chunk) {
-    StatepassWs w;
+StatepassWs statepass_ws(int B, int H, int L, int m, int chunk, int dtype) {
+    StatepassWs w{};
     const size_t nchunk = (size_t)(L / chunk);
-    w.k = 0;
-    w.kspec = w.k + align_up((size_t)H * chunk * sizeof(float));
-    w.states = w.kspec + align_up((size_t)H * (chunk + 1) * sizeof(float2));
-    w.corr_w = w.states + align_up((size_t)B * H * nchunk * m * sizeof(float2));
-    w.corr = w.corr_w + align_up((size_t)B * H * nchunk * m * sizeof(float2));
-    w.total = w.corr + align_up((size_t)B * H * L * sizeof(float));
+    w.fused = fftconv_wave16k_supported(chunk, dtype);
+    w.mfma = fftconv_mfma_supported(chunk, dtype);
+    w.corr16 = w.mfma && state_correction_mfma_ok(chunk, dtype);
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off += align_up(bytes);
+        return at;
+    };
+    w.k = take((size_t)H * chunk * sizeof(float));
+    if (!w.mfma) w.kspec = take((size_t)H * (chunk + 1) * sizeof(float2));
+    w.states = take((size_t)B * H * nchunk * m * sizeof(float2));
+    if (w.fused) {
+        w.ctab = take((size_t)H * CORR_TAB_U4 * sizeof(uint4));
+        w.w16 = take((size_t)B * H * nchunk * 64 * sizeof(uint32_t));
+        w.wexp = take((size_t)B * H * nchunk * sizeof(int));
+    } else {
+        w.corr_w = take((size_t)B * H * nchunk * m * sizeof(float2));
+        w.corr = take((size_t)B * H * L * (w.corr16 ? 2 : sizeof(float)));
+    }
+    w.total = off;
     return w;
 }
 
 struct LayerWs {
-    size_t qkv, o_cm, o_tm, kspec, gemm, total;
+    size_t qkv, o_cm, o_tm, kspec, wt, gemm, total;
 };
 constexpr size_t kLayerGemmWs = (size_t)64 << 20;   // hipBLASLt algorithm workspace
+// wt: the four weights transposed to (out, in), for the library's own GEMM
+// (both of its operands reduction-contiguous)
 LayerWs layer_ws(int B, int d, int L) {
     LayerWs w;
     const size_t act = (size_t)B * d * L * 2;
@@ -66,7 +94,8 @@ LayerWs layer_ws(int B, int d, int L) {
     w.o_cm = w.qkv + align_up(3 * act);
     w.o_tm = w.o_cm + align_up(act);
     w.kspec = w.o_tm + align_up(act);
-    w.gemm = w.kspec + align_up((size_t)d * (L + 1) * sizeof(float2));
+    w.wt = w.kspec + align_up((size_t)d * (L + 1) * sizeof(float2));
+    w.gemm = w.wt + align_up((size_t)4 * d * d * 2);
     w.total = w.gemm + kLayerGemmWs;
     return w;
 }
@@ -75,7 +104,7 @@ LayerWs layer_ws(int B, int d, int L) {
 // convolutions S (d_h rows per channel), O token-major, the spectra for the
 // VALU convolution, the GEMM algorithm workspace.
 struct HeadsWs {
-    size_t qkv, kbar, g, sv, o_tm, kspec, gemm, total;
+    size_t qkv, kbar, g, sv, o_tm, kspec, wt, gemm, total;
 };
 HeadsWs heads_ws(int B, int d, int L, int dh) {
     HeadsWs w;
@@ -86,7 +115,8 @@ HeadsWs heads_ws(int B, int d, int L, int dh) {
     w.sv = w.g + align_up((size_t)dh * act);
     w.o_tm = w.sv + align_up((size_t)dh * act);
     w.kspec = w.o_tm + align_up(act);
-    w.gemm = w.kspec + align_up((size_t)d * dh * (L + 1) * sizeof(float2));
+    w.wt = w.kspec + align_up((size_t)d * dh * (L + 1) * sizeof(float2));
+    w.gemm = w.wt + align_up((size_t)4 * d * d * 2);
     w.total = w.gemm + kLayerGemmWs;
     return w;
 }
@@ -97,34 +127,121 @@ bool gemm_native() {
 }
 
 // [Q;K;V] channel-major: per projection j and batch b the (d, L) block
-// j B d L + b d L is W_j (d, d) . x_b (L, d)^T, both operands contiguous along
-// the reduction (weights are stored (out, in)).  hipBLASLt, or the library's
-// GEMM where hipBLASLt rejects the shape or H3FLASH_GEMM=native.
+// j B d L + b d L is (x_b W_j)^T = W_j^T (d, d) . x_b (L, d)^T.  The weights
+// come as Algorithm 1 writes them, (in, out) with Q = x W_Q: hipBLASLt reads
+// W_j as the transposed operand.  The library's own GEMM (where hipBLASLt
+// rejects the shape, or with H3FLASH_GEMM=native) takes both operands
+// reduction-contiguous, so it reads W_j^T, transposed into wt first.
 hipError_t layer_qkv(const void *x, const void *Wq, const void *Wk, const void *Wv, char *qkv, int B, int L, int d,
-                     int dtype, void *gws, hipStream_t s) {
-    const size_t act = (size_t)B * L * d * 2;
+                     int dtype, void *wt, void *gws, hipStream_t s) {
+    const size_t act = (size_t)B * L * d * 2, wb = (size_t)d * d * 2;
     const void *Wqkv[3] = {Wq, Wk, Wv};
     const bool native = gemm_native();
     for (int j = 0; j < 3; ++j) {
         hipError_t e = native ? hipErrorNotSupported
-                              : launch_gemm_lt(Wqkv[j], true, x, true, qkv + j * act, d, L, d, B, 0, (long)L * d,
+                              : launch_gemm_lt(Wqkv[j], false, x, true, qkv + j * act, d, L, d, B, 0, (long)L * d,
                                                (long)d * L, dtype, gws, kLayerGemmWs, s);
-        if (e == hipErrorNotSupported) e = launch_gemm_nt(Wqkv[j], x, qkv + j * act, d, B * L, d, dtype, 1, d, L, s);
+        if (e == hipErrorNotSupported) {
+            char *wj = (char *)wt + j * wb;
+            if ((e = launch_transpose_batched(Wqkv[j], wj, 1, d, d, s)) != hipSuccess) return e;
+            e = launch_gemm_nt(wj, x, qkv + j * act, d, B * L, d, dtype, 1, d, L, s);
+        }
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
 }
 
-// out = O (M, K) . Wo (N, K)^T with O token-major (B L, d)
-hipError_t layer_out(const void *o_tm, const void *Wo, void *out, int B, int L, int d, int dtype, void *gws,
-                     hipStream_t s) {
+// out = O (B L, d) . Wo (d, d), O token-major; hipBLASLt reads Wo as it is
+// stored, the library's GEMM reads Wo^T (transposed into the fourth slot of wt)
+hipError_t layer_out(const void *o_tm, const void *Wo, void *out, int B, int L, int d, int dtype, void *wt,
+                     void *gws, hipStream_t s) {
     hipError_t e = gemm_native() ? hipErrorNotSupported
-                                 : launch_gemm_lt(o_tm, true, Wo, true, out, B * L, d, d, 1, 0, 0, 0, dtype, gws,
+                                 : launch_gemm_lt(o_tm, true, Wo, false, out, B * L, d, d, 1, 0, 0, 0, dtype, gws,
                                                   kLayerGemmWs, s);
-    if (e == hipErrorNotSupported) e = launch_gemm_nt(o_tm, Wo, out, B * L, d, d, dtype, 0, d, L, s);
+    if (e == hipErrorNotSupported) {
+        char *wo = (char *)wt + 3 * (size_t)d * d * 2;
+        if ((e = launch_transpose_batched(Wo, wo, 1, d, d, s)) != hipSuccess) return e;
+        e = launch_gemm_nt(o_tm, wo, out, B * L, d, d, dtype, 0, d, L, s);
+    }
     return e;
 }
 
+
+}  // namespace
+
+namespace h3 {
+
+size_t statepass_workspace(int B, int H, int L, int m, int chunk, int dtype) {
+    return statepass_ws(B, H, L, m, chunk, dtype).total;
+}
+
+// Argument checks of h3_statepass_conv that do not involve the workspace.
+int statepass_check(const void *u, const float *Abar, const float *Bbar, const float *C, const void *y,
+                    const float *x_final, int B, int H, int L, int m, int chunk, int dtype) {
+    if (!u || !Abar || !Bbar || !C || !y || B < 1 || H < 1 || L < 1 || m < 1 || chunk < 1) return H3_EINVAL;
+    if (L % chunk) return H3_EINVAL;
+    if (!dtype_ok(dtype) || m > H3_MAX_MODES || !fused_len_ok(chunk, dtype)) return H3_EUNSUPPORTED;
+    if (!aligned16(u) || !aligned16(y)) return H3_EINVAL;
+    const size_t io = (size_t)B * H * L * esize(dtype), xs = (size_t)B * H * m * 8;
+    if (overlap(u, io, y, io) || overlap(x_final, xs, y, io) || overlap(x_final, xs, u, io)) return H3_EINVAL;
+    return H3_OK;
+}
+
+// State passing on validated arguments, scratch at ws (statepass_workspace
+// bytes, 256-byte aligned).  Every scratch region is written before it is
+// read, so its prior contents do not matter.
+int statepass_run(const void *u, const float *Abar, const float *Bbar, const float *C, const float *D,
+                  const float *x0, int B, int H, int L, int m, int chunk, int dtype, void *y, float *x_final,
+                  char *ws, hipStream_t s) {
+    const int nchunk = L / chunk;
+    const StatepassWs w = statepass_ws(B, H, L, m, chunk, dtype);
+    float *kbuf = (float *)(ws + w.k);
+    float2 *Kspec = w.mfma ? nullptr : (float2 *)(ws + w.kspec);
+    float2 *states = (float2 *)(ws + w.states);
+    hipError_t e;
+    // f = [C Bbar, C Abar Bbar, ...] of length chunk, and its spectrum
+    if ((e = launch_kernel_gen(1, Abar, Bbar, C, nullptr, H, m, chunk, kbuf, s)) != hipSuccess) return H3_EDEVICE;
+    if (!w.mfma && (e = launch_spectrum(kbuf, H, chunk, Kspec, s)) != hipSuccess) return H3_EDEVICE;
+    // s_c = M_ux u^(c) for every chunk, then the scan over chunks
+    if ((e = launch_chunk_states(u, Abar, Bbar, B, H, L, m, chunk, dtype, states, s)) != hipSuccess)
+        return H3_EDEVICE;
+    ConvArgs a{};
+    a.u = u; a.y = y; a.Kspec = Kspec; a.D = D;
+    a.B = B; a.H = H; a.L = chunk; a.nchunk = nchunk; a.pair_mode = 1; a.dtype = dtype;
+    if (w.fused) {
+        // chunk = 8192: the conv computes M_xy x^(c) itself from normalised
+        // weights (scan output) and per-channel power tables
+        uint4 *ctab = (uint4 *)(ws + w.ctab);
+        uint32_t *w16 = (uint32_t *)(ws + w.w16);
+        int *wexp = (int *)(ws + w.wexp);
+        if ((e = launch_state_scan_w16(Abar, C, x0, states, B, H, m, chunk, nchunk, w16, wexp, x_final, s)) !=
+            hipSuccess)
+            return H3_EDEVICE;
+        if ((e = launch_corr_tables(Abar, H, m, ctab, s)) != hipSuccess) return H3_EDEVICE;
+        a.corr = w16;
+        a.corr_tab = ctab;
+        a.corr_e = wexp;
+        return launched(launch_fftconv_mfma(a, kbuf, s));
+    }
+    float2 *corr_W = (float2 *)(ws + w.corr_w);
+    void *corr = ws + w.corr;
+    if ((e = launch_state_scan(Abar, C, x0, states, B, H, m, chunk, nchunk, corr_W, x_final, s)) != hipSuccess)
+        return H3_EDEVICE;
+    // M_xy x^(c) for every chunk (in the I/O dtype when the matrix-core paths apply)
+    if (w.corr16)
+        e = launch_state_correction_mfma(Abar, corr_W, B, H, m, chunk, nchunk, dtype, corr, s);
+    else
+        e = launch_state_correction(Abar, corr_W, B, H, m, chunk, nchunk, (float *)corr, s);
+    if (e != hipSuccess) return H3_EDEVICE;
+    a.corr = corr;
+    a.corr16 = w.corr16 ? 1 : 0;
+    if (w.mfma) return launched(launch_fftconv_mfma(a, kbuf, s));
+    return launched(launch_fftconv(a, s));
+}
+
+}  // namespace h3
+
+namespace {
 }  // namespace
 
 extern "C" {
@@ -147,7 +264,7 @@ size_t h3_workspace_size(int op, int B, int H, int L, int m, int chunk, int dtyp
             return align_up(fftconv_workspace(B, H, L));
         case H3_OP_STATEPASS:
             if (m < 1 || chunk < 1 || L % chunk) return 0;
-            return statepass_ws(B, H, L, m, chunk).total;
+            return statepass_ws(B, H, L, m, chunk, dtype).total;
         case H3_OP_LAYER:
             return layer_ws(B, H, L).total;
         case H3_OP_LAYER_HEADS:   // chunk = head dimension
@@ -302,73 +419,16 @@ int h3_statepass_conv(const void *u, const float *Abar, const float *Bbar, const
                       const float *D, const float *x0, int B, int H, int L, int m, int chunk,
                       int dtype, void *y, float *x_final, void *workspace, size_t ws_bytes,
                       void *stream) {
-    if (!u || !Abar || !Bbar || !C || !y || B < 1 || H < 1 || L < 1 || m < 1 || chunk < 1)
-        return H3_EINVAL;
-    if (L % chunk) return H3_EINVAL;
-    if (!dtype_ok(dtype) || m > H3_MAX_MODES || !fused_len_ok(chunk, dtype)) return H3_EUNSUPPORTED;
-    const size_t io = (size_t)B * H * L * esize(dtype);
-    const size_t need = h3_workspace_size(H3_OP_STATEPASS, B, H, L, m, chunk, dtype);
+    const int st = statepass_check(u, Abar, Bbar, C, y, x_final, B, H, L, m, chunk, dtype);
+    if (st != H3_OK) return st;
+    const size_t io = (size_t)B * H * L * esize(dtype), xs = (size_t)B * H * m * 8;
+    const size_t need = statepass_workspace(B, H, L, m, chunk, dtype);
     if (!workspace || ws_bytes < need) return H3_EWORKSPACE;
-    if (!aligned16(u) || !aligned16(y) || !aligned16(workspace)) return H3_EINVAL;
-    const size_t xs = (size_t)B * H * m * 8;
-    if (overlap(u, io, y, io) || overlap(workspace, need, u, io) || overlap(workspace, need, y, io) ||
-        overlap(x_final, xs, y, io) || overlap(x_final, xs, u, io) || overlap(x_final, xs, workspace, need))
+    if (!aligned16(workspace)) return H3_EINVAL;
+    if (overlap(workspace, need, u, io) || overlap(workspace, need, y, io) || overlap(x_final, xs, workspace, need))
         return H3_EINVAL;
-    hipStream_t s = (hipStream_t)stream;
-    const int nchunk = L / chunk;
-    const StatepassWs w = statepass_ws(B, H, L, m, chunk);
-    char *ws = (char *)workspace;
-    float *kbuf = (float *)(ws + w.k);
-    float2 *Kspec = (float2 *)(ws + w.kspec);
-    float2 *states = (float2 *)(ws + w.states);
-    float2 *corr_W = (float2 *)(ws + w.corr_w);
-    float *corr = (float *)(ws + w.corr);
-    hipError_t e;
-    // f = [C Bbar, C Abar Bbar, ...] of length chunk, and its spectrum
-    if ((e = launch_kernel_gen(1, Abar, Bbar, C, nullptr, H, m, chunk, kbuf, s)) != hipSuccess) return H3_EDEVICE;
-    if (!fftconv_mfma_supported(chunk, dtype) &&
-        (e = launch_spectrum(kbuf, H, chunk, Kspec, s)) != hipSuccess)
-        return H3_EDEVICE;
-    // s_c = M_ux u^(c) for every chunk, then the scan over chunks
-    if ((e = launch_chunk_states(u, Abar, Bbar, B, H, L, m, chunk, dtype, states, s)) != hipSuccess)
-        return H3_EDEVICE;
-    if (fftconv_wave16k_supported(chunk, dtype)) {
-        // chunk = 8192: the conv computes M_xy x^(c) itself from normalised
-        // weights (scan output) and per-channel power tables, both kept in
-        // the correction-term region
-        char *cr = ws + w.corr;
-        uint4 *ctab = (uint4 *)cr;
-        uint32_t *w16 = (uint32_t *)(cr + align_up((size_t)H * CORR_TAB_U4 * sizeof(uint4)));
-        int *wexp = (int *)((char *)w16 + align_up((size_t)B * H * nchunk * 64 * sizeof(uint32_t)));
-        if ((e = launch_state_scan_w16(Abar, C, x0, states, B, H, m, chunk, nchunk, w16, wexp, x_final, s)) !=
-            hipSuccess)
-            return H3_EDEVICE;
-        if ((e = launch_corr_tables(Abar, H, m, ctab, s)) != hipSuccess) return H3_EDEVICE;
-        ConvArgs a{};
-        a.u = u; a.y = y; a.Kspec = Kspec; a.D = D;
-        a.B = B; a.H = H; a.L = chunk; a.nchunk = nchunk; a.pair_mode = 1; a.dtype = dtype;
-        a.corr = w16;
-        a.corr_tab = ctab;
-        a.corr_e = wexp;
-        return launched(launch_fftconv_mfma(a, kbuf, s));
-    }
-    if ((e = launch_state_scan(Abar, C, x0, states, B, H, m, chunk, nchunk, corr_W, x_final, s)) !=
-        hipSuccess)
-        return H3_EDEVICE;
-    // M_xy x^(c) for every chunk (in the I/O dtype when the matrix-core paths apply)
-    const bool fast = fftconv_mfma_supported(chunk, dtype) && state_correction_mfma_ok(chunk, dtype);
-    if (fast)
-        e = launch_state_correction_mfma(Abar, corr_W, B, H, m, chunk, nchunk, dtype, corr, s);
-    else
-        e = launch_state_correction(Abar, corr_W, B, H, m, chunk, nchunk, corr, s);
-    if (e != hipSuccess) return H3_EDEVICE;
-    ConvArgs a{};
-    a.u = u; a.y = y; a.Kspec = Kspec; a.D = D;
-    a.B = B; a.H = H; a.L = chunk; a.nchunk = nchunk; a.pair_mode = 1; a.dtype = dtype;
-    a.corr = corr;
-    a.corr16 = fast ? 1 : 0;
-    if (fftconv_mfma_supported(chunk, dtype)) return launched(launch_fftconv_mfma(a, kbuf, s));
-    return launched(launch_fftconv(a, s));
+    return statepass_run(u, Abar, Bbar, C, D, x0, B, H, L, m, chunk, dtype, y, x_final, (char *)workspace,
+                         (hipStream_t)stream);
 }
 
 int h3_layer_fwd(const void *x, const void *Wq, const void *Wk, const void *Wv, const void *Wo,
@@ -400,8 +460,8 @@ int h3_layer_fwd(const void *x, const void *Wq, const void *Wk, const void *Wv, 
     void *o_tm = ws + w.o_tm;
     float2 *Kspec = (float2 *)(ws + w.kspec);
     hipError_t e;
-    void *gws = ws + w.gemm;
-    if ((e = layer_qkv(x, Wq, Wk, Wv, qkv, B, L, d, dtype, gws, s)) != hipSuccess) return H3_EDEVICE;
+    void *gws = ws + w.gemm, *wt = ws + w.wt;
+    if ((e = layer_qkv(x, Wq, Wk, Wv, qkv, B, L, d, dtype, wt, gws, s)) != hipSuccess) return H3_EDEVICE;
     const char *q = qkv, *kk = qkv + act, *v = qkv + 2 * act;
     if (fftconv_mfma_supported(L, dtype) && L % 64 == 0) {
         // G = (shift SSM of K) * V  ->  o_cm;  S = diag conv of G (+ D G)  ->  K's slot (K is dead);
@@ -421,7 +481,7 @@ int h3_layer_fwd(const void *x, const void *Wq, const void *Wk, const void *Wv, 
         // O (B, d, L) -> (B, L, d)
         if ((e = launch_transpose_batched(o_cm, o_tm, B, d, L, s)) != hipSuccess) return H3_EDEVICE;
     }
-    return launched(layer_out(o_tm, Wo, out, B, L, d, dtype, gws, s));
+    return launched(layer_out(o_tm, Wo, out, B, L, d, dtype, wt, gws, s));
 }
 
 int h3_layer_fwd_heads(const void *x, const void *Wq, const void *Wk, const void *Wv, const void *Wo,
@@ -452,11 +512,11 @@ int h3_layer_fwd_heads(const void *x, const void *Wq, const void *Wk, const void
     const HeadsWs w = heads_ws(B, d, L, d_head);
     char *ws = (char *)workspace;
     char *qkv = ws + w.qkv;
-    void *kbar = ws + w.kbar, *g = ws + w.g, *sv = ws + w.sv, *o_tm = ws + w.o_tm, *gws = ws + w.gemm;
+    void *kbar = ws + w.kbar, *g = ws + w.g, *sv = ws + w.sv, *o_tm = ws + w.o_tm, *gws = ws + w.gemm, *wt = ws + w.wt;
     float2 *Kspec = (float2 *)(ws + w.kspec);
     const char *q = qkv, *kk = qkv + act, *v = qkv + 2 * act;
     hipError_t e;
-    if ((e = layer_qkv(x, Wq, Wk, Wv, qkv, B, L, d, dtype, gws, s)) != hipSuccess) return H3_EDEVICE;
+    if ((e = layer_qkv(x, Wq, Wk, Wv, qkv, B, L, d, dtype, wt, gws, s)) != hipSuccess) return H3_EDEVICE;
     // Kbar = shift SSM of K (no gating); G = per-head outer products of Kbar and V
     if ((e = launch_shift_gate(kk, nullptr, shift_C, shift_D, m_s, B, d, L, dtype, kbar, s)) != hipSuccess)
         return H3_EDEVICE;
@@ -474,7 +534,7 @@ int h3_layer_fwd_heads(const void *x, const void *Wq, const void *Wk, const void
     }
     // O_t[j] = sum_i Q_t[i] S_t[i][j], token-major; out = O Wo^T
     if ((e = launch_heads_contract(d_head, q, sv, o_tm, B, d, L, dtype, s)) != hipSuccess) return H3_EDEVICE;
-    return launched(layer_out(o_tm, Wo, out, B, L, d, dtype, gws, s));
+    return launched(layer_out(o_tm, Wo, out, B, L, d, dtype, wt, gws, s));
 }
 
 }  // extern "C"

@@ -48,6 +48,15 @@ template <> struct IO<BF16> {
     static __device__ __forceinline__ void st(uint16_t *p, long i, float v) { p[i] = f32_to_bf16(v); }
 };
 
+// Exponent e with m = f 2^e, f in [1/2, 1) (frexp); 0 for 0, NaN and inf, so
+// that such rows pass through unscaled.
+__device__ __forceinline__ int pow2_exp(float m) {
+    if (!(m > 0.f) || !(m < 3.0e38f)) return 0;
+    int e;
+    frexpf(m, &e);
+    return e;
+}
+
 // --------------------------------------------------------- launch order ----
 // Workgroups are dealt round-robin to the 8 XCDs (each with its own L2).  Remap
 // the hardware block index so that consecutive logical indices run on the same

@@ -96,6 +96,7 @@ __global__ __launch_bounds__(N / 16 >= 64 ? N / 16 : 64) void fftconv_kernel(Con
     constexpr int S = (T >= 64) ? 1 : 64 / T;
     constexpr int L = N / 2;
     extern __shared__ float2 lds[];
+    __shared__ uint32_t rmx[2 * S];   // per signal: max |row a|, max |row b| (float bits)
     const int sig = threadIdx.x / T, tid = threadIdx.x % T;
     float2 *X = lds + sig * P::LDS;
     const int blk = xcd_logical_block(blockIdx.x, gridDim.x);
@@ -126,6 +127,31 @@ __global__ __launch_bounds__(N / 16 >= 64 ? N / 16 : 64) void fftconv_kernel(Con
             }
         }
     }
+    // Each row gets its own power-of-two scale (max |.| in [1/2, 1)): rounding
+    // error of the shared transform then stays at each row's own scale, even
+    // when one row is much smaller than the other.
+    {
+        float ma = 0.f, mb = 0.f;
+#pragma unroll
+        for (int i = 0; i < Q * HALF; ++i) {
+            ma = fmaxf(ma, fabsf(ua[i]));
+            mb = fmaxf(mb, fabsf(ub[i]));
+        }
+        if (tid == 0) {
+            rmx[2 * sig] = 0u;
+            rmx[2 * sig + 1] = 0u;
+        }
+        __syncthreads();
+        atomicMax(&rmx[2 * sig], __float_as_uint(ma));
+        atomicMax(&rmx[2 * sig + 1], __float_as_uint(mb));
+        __syncthreads();
+    }
+    const int ea = pow2_exp(__uint_as_float(rmx[2 * sig])), eb = pow2_exp(__uint_as_float(rmx[2 * sig + 1]));
+    {
+        const float sa = ldexpf(1.0f, -ea), sb = ldexpf(1.0f, -eb);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) v[r] = make_float2(v[r].x * sa, v[r].y * sb);
+    }
     fft_forward_from_regs<N>(X, tid, v);
 
     // pointwise product with the kernel spectrum (Hermitian: K(-f) = conj K(f)),
@@ -141,6 +167,7 @@ __global__ __launch_bounds__(N / 16 >= 64 ? N / 16 : 64) void fftconv_kernel(Con
     fft_second_from_regs<N>(X, tid, v);
 
     const float d = a.D ? a.D[pm.h] : 0.f;
+    const float ya_s = ldexpf(1.0f, ea), yb_s = ldexpf(1.0f, eb);
     if (!active) return;
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
@@ -149,8 +176,8 @@ __global__ __launch_bounds__(N / 16 >= 64 ? N / 16 : 64) void fftconv_kernel(Con
         for (int r = 0; r < HALF; ++r) {
             const int n = j + r * (N / R1);
             const float2 w = v[q * R1 + r];
-            float oa = w.x + d * ua[q * HALF + r];
-            float ob = -w.y + d * ub[q * HALF + r];
+            float oa = fmaf(w.x, ya_s, d * ua[q * HALF + r]);
+            float ob = fmaf(-w.y, yb_s, d * ub[q * HALF + r]);
             if (a.corr) {
                 const float *cr = (const float *)a.corr;
                 oa += cr[pm.oa + n];

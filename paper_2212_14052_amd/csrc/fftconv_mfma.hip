@@ -1,36 +1,30 @@
-// Fused block-FFT convolution on the matrix cores (Sec. 4.1: kernel fusion +
-// block FFT), gfx950, 16-bit I/O.  Transform length N = 2L = 4096 = 16^3.
+// Fused block-FFT convolution at L = 16384 (Sec. 4.1: kernel fusion + block
+// FFT, past the 8192 limit the paper's SRAM set; Sec. 4.2 uses it as the
+// state-passing chunk), gfx950, 16-bit I/O.  Transform length N = 2L = 32768 =
+// 8 x 4096, held in LDS as fp16 complex (128 KB of the 160 KB).
 //
-// The DFT of a length-4096 signal is written, as in the paper's four-step
-// factorisation, as three layers of length-16 DFTs (block-diagonal I (x) F_16
+// The DFT of each 4096-point block is, as in the paper's four-step
+// factorisation, three layers of length-16 DFTs (block-diagonal I (x) F_16
 // products) with twiddle diagonals in between.  Each layer of 256 DFT-16s runs
 // as 16 pairs of v_mfma_f32_16x16x32_f16: the 16x16 complex DFT matrix is the
 // A operand (as a 16 x 32 real matrix for the real rows and one for the
-// imaginary rows), 16 signal vectors are the columns of B.
-//
-// Index p = 256 p2 + 16 p1 + p0 of the signal held in LDS (fp16 complex per
-// dword).  Forward (decimation in frequency):
+// imaginary rows), 16 signal vectors are the columns of B.  Block index
+// p = 256 p2 + 16 p1 + p0 (fp16 complex per dword).  Forward (decimation in
+// frequency):
 //   A: DFT over p2, then * w_4096^{p2 (16 p1 + p0)}
 //   B: DFT over p1, then * w_256^{p1 p0}
 //   C: DFT over p0            -> position p holds X[p2 + 16 p1 + 256 p0]
 // The spectrum stays in this digit-reversed order; the kernel spectrum is made
 // by the same pipeline, so the pointwise product needs no permutation.  The
-// second transform (conj(F(conj Y)) = N IDFT(Y)) runs the layers in reverse,
-// C, * w_256^{p1 p0}, B, * w_4096^{p2 (16 p1 + p0)}, A, and ends in natural
-// order.  Layer C of the first transform, the pointwise product and layer C of
-// the second are fused in registers.
+// second transform (conj(F(conj Y)) = N IDFT(Y)) runs the layers in reverse
+// and ends in natural order.
 //
-// Two rows of one channel travel as one complex signal (u_a + i u_b).  The
-// zero-padded half of the input and the discarded half of the output are the
-// p2 >= 8 rows of layer A.  Dynamic range: inputs are scaled by a power of two
-// to max |.| in [1/2, 1), each DFT-16 layer carries a factor 1/4 (folded into
-// the fp16 DFT matrix) and the kernel spectrum is normalised to max |K| in
-// [1/2, 1); all scale factors are powers of two and are undone exactly in
-// fp32 at the output.
-//
-// One workgroup (8 waves) handles a set of row pairs of one channel: it first
-// transforms the channel's kernel (so the spectrum is never stored in HBM),
-// keeps it in registers, then streams the pairs through the LDS buffer.
+// Two rows of one channel travel as one complex signal (u_a + i u_b).
+// Dynamic range: each row is scaled by its own power of two to max |.| in
+// [1/2, 1), each DFT-16 layer carries a factor 1/4 (folded into the fp16 DFT
+// matrix) and the kernel spectrum is normalised to max |K| in [1/2, 1); all
+// scale factors are powers of two and are undone exactly in fp32 at the
+// output.
 #include "common.h"
 #include "fft_valu.h"
 #include "internal.h"
@@ -43,17 +37,6 @@ typedef float f4_t __attribute__((ext_vector_type(4)));
 
 namespace mf {
 
-constexpr int N = 4096;
-constexpr int L = 2048;
-constexpr int NW = 8;          // waves per workgroup
-constexpr int BPW = 16 / NW;   // batches per wave and layer: wave w owns 2w, 2w+1
-constexpr int NT = 64 * NW;    // threads per workgroup
-static_assert(BPW == 2, "address bases below assume two batches per wave");
-
-// Swizzle of the staging buffer (natural index t < L, dword): bits 4-5 ^=
-// bits 10-11 ^ bits 6-7, so the layer-A gather (lane groups 1024 apart) and
-// the 16-byte coalesced staging are both conflict-free.
-__device__ __forceinline__ int swz(int p) { return p ^ ((((p >> 10) ^ (p >> 6)) & 3) << 4); }
 
 __device__ __forceinline__ uint32_t pack(float re, float im) {
     h2_t h = {(_Float16)re, (_Float16)im};
@@ -134,585 +117,6 @@ template <> __device__ __forceinline__ uint32_t pack_io<BF16>(float lo, float hi
 
 }  // namespace mf
 
-template <int DT>
-__global__ __launch_bounds__(mf::NT) __attribute__((amdgpu_waves_per_eu(4))) void fftconv_mfma4096_kernel(
-    ConvArgs a, const float *k, int wg_per_ch, int pairs_per_ch) {
-    using namespace mf;
-    __shared__ uint32_t X[N];          // signal being transformed (fp16 complex)
-    __shared__ uint32_t Ub[L];         // staged rows: (a, b) raw 16-bit pairs, or k (fp32)
-    __shared__ float red[2][NW];
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const int c = lane & 15, g = lane >> 4;
-    const int blk = xcd_logical_block(blockIdx.x, gridDim.x);
-    const int h = blk / wg_per_ch, part = blk % wg_per_ch;
-    const int per = (pairs_per_ch + wg_per_ch - 1) / wg_per_ch;
-    const int q0 = part * per, q1 = min(q0 + per, pairs_per_ch);
-    int rsel = 0;
-
-    // workgroup max |.| -> exponent e (max = m 2^e, m in [1/2, 1)); one barrier
-    auto bexp = [&](float v) -> int {
-        v = wave_max(v);
-        if (lane == 0) red[rsel][w] = v;
-        __syncthreads();
-        float m = red[rsel][0];
-#pragma unroll
-        for (int i = 1; i < NW; ++i) m = fmaxf(m, red[rsel][i]);
-        rsel ^= 1;
-        if (!(m > 0.f) || !(m < 3.0e38f)) return 0;
-        int e;
-        frexpf(m, &e);
-        return e;
-    };
-
-    // Per-lane LDS bases (dword index; the rest of each address is an
-    // immediate).  Signal position p = 256 p2 + 16 p1 + p0 lives at
-    //   256 p2 + 64 (p0 >> 2) + 4 p1 + (p0 & 3), with address bits 2-3 ^= p0 >> 2
-    //   and bits 4-5 ^= p2 >> 2,
-    // which makes the stride patterns of layers A and B and the 16-byte
-    // accesses of layer C free of bank conflicts.  Wave w owns batches
-    // b = 2w + ib.
-    //  layer A / A':  p = 256 (4g + j) + 16 b + c  -> mA[ib] + 256 j
-    //  layer B / B':  p = 256 b + 16 (4g + j) + c  -> mB[j] + 256 ib
-    //  layer C:       p = 256 b + 16 c + 4g + j    -> mC + 256 ib + j
-    int mA[2], mB[4];
-    {
-        const int tA = (c >> 2) | (g << 2);
-#pragma unroll
-        for (int ib = 0; ib < 2; ++ib) mA[ib] = 1024 * g + 64 * (c >> 2) + (c & 3) + 4 * ((2 * w + ib) ^ tA);
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-            mB[j] = 512 * w + 64 * (c >> 2) + (c & 3) + 16 * (g ^ (w >> 1)) + 4 * (j ^ (c >> 2));
-    }
-    const int mC = 512 * w + 64 * g + 4 * (c ^ g ^ ((w >> 1) << 2));
-    // staging buffer Ub (natural index t < L): its own swizzle
-    //  layer A reads t = 256 (4g + i) + 16 b + c  -> uA[ib] + 256 i
-    int uA[2];
-#pragma unroll
-    for (int ib = 0; ib < 2; ++ib) uA[ib] = swz(16 * (2 * w + ib) + c + 1024 * g);  // used for g < 2 only
-
-    // twiddles (packed fp16), fixed per lane
-    uint32_t twA[2][4], twB[2][4], tw2[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        tw2[j] = twiddle_h((4 * g + j) * c, 256);
-#pragma unroll
-        for (int ib = 0; ib < 2; ++ib) {
-            const int b = 2 * w + ib;
-            twA[ib][j] = twiddle_h((4 * g + j) * (16 * b + c), N);
-            twB[ib][j] = twiddle_h(b * (16 * (4 * g + j) + c), N);
-        }
-    }
-    const Dft16 F = make_dft16(lane);
-
-    // layer A from per-batch operands; outputs scaled by `sc` then twiddled
-    auto layer_A = [&](const h8_t *xa, float sc) {
-#pragma unroll
-        for (int ib = 0; ib < 2; ++ib) {
-            f4_t re, im;
-            dft16(F, xa[ib], re, im);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) X[mA[ib] + 256 * j] = cmul_h(pack(re[j] * sc, im[j] * sc), twA[ib][j]);
-        }
-        __syncthreads();
-    };
-    auto layer_B = [&](const uint32_t (*tw)[4]) {
-#pragma unroll
-        for (int ib = 0; ib < 2; ++ib) {
-            uint32_t v[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) v[j] = X[mB[j] + 256 * ib];
-            f4_t re, im;
-            dft16(F, h8_from(v[0], v[1], v[2], v[3]), re, im);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) X[mB[j] + 256 * ib] = cmul_h(pack(re[j], im[j]), tw[ib][j]);
-        }
-        // no barrier: layers B and C of batch b (= p2) touch the same 256
-        // positions from the same wave, and LDS accesses of a wave are ordered
-    };
-    const uint32_t tw2b[2][4] = {{tw2[0], tw2[1], tw2[2], tw2[3]}, {tw2[0], tw2[1], tw2[2], tw2[3]}};
-
-    // ---- kernel spectrum of channel h ----
-    uint32_t K[2][4];  // fp16 complex, holds F(k) 2^kexp
-    int kexp;
-    {
-        const float4 k0 = ((const float4 *)(k + (long)h * L))[tid];
-        const float mx = fmaxf(fmaxf(fabsf(k0.x), fabsf(k0.y)), fmaxf(fabsf(k0.z), fabsf(k0.w)));
-        *(uint4 *)&Ub[swz(4 * tid)] = make_uint4(__float_as_uint(k0.x), __float_as_uint(k0.y),
-                                                 __float_as_uint(k0.z), __float_as_uint(k0.w));
-        const int ek = bexp(mx);   // also publishes Ub
-        h8_t xa[2];
-#pragma unroll
-        for (int ib = 0; ib < 2; ++ib) {
-            uint32_t v[4] = {0u, 0u, 0u, 0u};
-            if (g < 2) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) v[i] = pack(ldexpf(__uint_as_float(Ub[uA[ib] + 256 * i]), -ek), 0.f);
-            }
-            xa[ib] = h8_from(v[0], v[1], v[2], v[3]);
-        }
-        layer_A(xa, 1.0f);
-        layer_B(tw2b);
-        float Kf[2][4][2];
-        float km = 0.f;
-#pragma unroll
-        for (int ib = 0; ib < 2; ++ib) {
-            const uint4 v = *(const uint4 *)&X[mC + 256 * ib];
-            f4_t re, im;
-            dft16(F, __builtin_bit_cast(h8_t, v), re, im);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                Kf[ib][j][0] = re[j];
-                Kf[ib][j][1] = im[j];
-                km = fmaxf(km, fmaxf(fabsf(re[j]), fabsf(im[j])));
-            }
-        }
-        const int e2 = bexp(km);
-#pragma unroll
-        for (int ib = 0; ib < 2; ++ib)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) K[ib][j] = pack(ldexpf(Kf[ib][j][0], -e2), ldexpf(Kf[ib][j][1], -e2));
-        kexp = -ek - 6 - e2;
-    }
-
-    const float d = a.D ? a.D[h] : 0.f;
-    const uint16_t *u = (const uint16_t *)a.u;
-    uint16_t *y = (uint16_t *)a.y;
-    auto rows = [&](int qq, long &oa, long &ob) {
-        if (a.pair_mode == 0) {
-            oa = ((long)(2 * qq) * a.H + h) * L;
-            ob = (2 * qq + 1 < a.B) ? ((long)(2 * qq + 1) * a.H + h) * L : -1;
-        } else {
-            const int ncp = (a.nchunk + 1) / 2;
-            const int bb = qq / ncp, cp = qq % ncp;
-            oa = (((long)bb * a.H + h) * a.nchunk + 2 * cp) * L;
-            ob = (2 * cp + 1 < a.nchunk) ? oa + L : -1;
-        }
-    };
-    const int ubase = swz(4 * tid);    // this thread's staged elements 4 tid .. 4 tid + 3
-    // coalesced loads: thread tid owns elements 4 tid .. 4 tid + 3 of both rows
-    uint2 pa = make_uint2(0, 0), pb = make_uint2(0, 0);
-    if (q0 < q1) {
-        long oa, ob;
-        rows(q0, oa, ob);
-        pa = *(const uint2 *)(u + oa + 4 * tid);
-        if (ob >= 0) pb = *(const uint2 *)(u + ob + 4 * tid);
-    }
-    for (int qq = q0; qq < q1; ++qq) {
-        long oa, ob;
-        rows(qq, oa, ob);
-        // stage raw (a, b) pairs in Ub, max |u|
-        const uint4 st = make_uint4(__builtin_amdgcn_perm(pb.x, pa.x, 0x05040100u),
-                                    __builtin_amdgcn_perm(pb.x, pa.x, 0x07060302u),
-                                    __builtin_amdgcn_perm(pb.y, pa.y, 0x05040100u),
-                                    __builtin_amdgcn_perm(pb.y, pa.y, 0x07060302u));
-        float mx = 0.f;
-        mx = fmaxf(mx, fmaxf(fabsf(lo_f<DT>(st.x)), fabsf(hi_f<DT>(st.x))));
-        mx = fmaxf(mx, fmaxf(fabsf(lo_f<DT>(st.y)), fabsf(hi_f<DT>(st.y))));
-        mx = fmaxf(mx, fmaxf(fabsf(lo_f<DT>(st.z)), fabsf(hi_f<DT>(st.z))));
-        mx = fmaxf(mx, fmaxf(fabsf(lo_f<DT>(st.w)), fabsf(hi_f<DT>(st.w))));
-        *(uint4 *)&Ub[ubase] = st;
-        // prefetch the next pair
-        if (qq + 1 < q1) {
-            long na, nb;
-            rows(qq + 1, na, nb);
-            pa = *(const uint2 *)(u + na + 4 * tid);
-            pb = (nb >= 0) ? *(const uint2 *)(u + nb + 4 * tid) : make_uint2(0, 0);
-        }
-        const int eu = bexp(mx);
-        h8_t xa[2];
-#pragma unroll
-        for (int ib = 0; ib < 2; ++ib) {
-            uint32_t v[4] = {0u, 0u, 0u, 0u};
-            if (g < 2) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const uint32_t r = Ub[uA[ib] + 256 * i];
-                    if (DT == F16)
-                        v[i] = r;    // fp16 pairs are the operand as they are
-                    else
-                        v[i] = pack(ldexpf(lo_f<DT>(r), -eu), ldexpf(hi_f<DT>(r), -eu));
-                }
-            }
-            xa[ib] = h8_from(v[0], v[1], v[2], v[3]);
-        }
-        layer_A(xa, DT == F16 ? ldexpf(1.0f, -eu) : 1.0f);
-        layer_B(tw2b);
-        // layer C forward, pointwise product, layer C of the second transform
-#pragma unroll
-        for (int ib = 0; ib < 2; ++ib) {
-            uint4 *px = (uint4 *)&X[mC + 256 * ib];
-            f4_t re, im;
-            dft16(F, __builtin_bit_cast(h8_t, *px), re, im);
-            uint32_t yv[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) yv[j] = cmul_h(pack(re[j], im[j]), K[ib][j]) ^ 0x80000000u;  // conj(X K)
-            dft16(F, h8_from(yv[0], yv[1], yv[2], yv[3]), re, im);
-            // w_256^{p1 p0} with p1 = c, p0 = 4g + j: same values as tw2
-            uint4 o;
-            o.x = cmul_h(pack(re[0], im[0]), tw2[0]);
-            o.y = cmul_h(pack(re[1], im[1]), tw2[1]);
-            o.z = cmul_h(pack(re[2], im[2]), tw2[2]);
-            o.w = cmul_h(pack(re[3], im[3]), tw2[3]);
-            *px = o;
-        }
-        layer_B(twB);   // same wave, same positions as layer C: no barrier before
-        __syncthreads();
-        // layer A of the second transform -> natural order; t < L kept.
-        // y = Re / -Im of w * 2^(eu - kexp) * 64^2 / N  (input scale, kernel
-        // scale and the two 1/64 layer factors undone; 1/N of the inverse)
-        const float sc = ldexpf(64.0f * 64.0f / (float)N, eu - kexp);
-#pragma unroll
-        for (int ib = 0; ib < 2; ++ib) {
-            uint32_t v[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) v[j] = X[mA[ib] + 256 * j];
-            f4_t re, im;
-            dft16(F, h8_from(v[0], v[1], v[2], v[3]), re, im);
-            if (g < 2) {
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const uint32_t r = Ub[uA[ib] + 256 * j];
-                    float ya = fmaf(re[j], sc, d * lo_f<DT>(r));
-                    float yb = fmaf(-im[j], sc, d * hi_f<DT>(r));
-                    if (a.corr) {
-                        const int t = 256 * (4 * g + j) + 16 * (2 * w + ib) + c;
-                        if (a.corr16) {
-                            const uint16_t *cr = (const uint16_t *)a.corr;
-                            ya += lo_f<DT>(cr[oa + t]);
-                            if (ob >= 0) yb += lo_f<DT>(cr[ob + t]);
-                        } else {
-                            const float *cr = (const float *)a.corr;
-                            ya += cr[oa + t];
-                            if (ob >= 0) yb += cr[ob + t];
-                        }
-                    }
-                    Ub[uA[ib] + 256 * j] = pack_io<DT>(ya, yb);
-                }
-            }
-        }
-        __syncthreads();
-        {
-            const uint4 v = *(const uint4 *)&Ub[ubase];
-            uint2 oa2, ob2;
-            oa2.x = __builtin_amdgcn_perm(v.y, v.x, 0x05040100u);
-            oa2.y = __builtin_amdgcn_perm(v.w, v.z, 0x05040100u);
-            ob2.x = __builtin_amdgcn_perm(v.y, v.x, 0x07060302u);
-            ob2.y = __builtin_amdgcn_perm(v.w, v.z, 0x07060302u);
-            *(uint2 *)(y + oa + 4 * tid) = oa2;
-            if (ob >= 0) *(uint2 *)(y + ob + 4 * tid) = ob2;
-        }
-        // the next pair rewrites Ub only after its own barrier in bexp
-    }
-}
-
-// ============================================================================
-// Transform length N = 2L = 16384 = 4 x 4096 (L = 8192, the fused-block limit).
-// A radix-4 layer R over the top digit p3 (p = 4096 p3 + m) runs on the VALU
-// (half of its inputs are the zero padding), followed by the 4096-point block
-// pipeline above on each of the four blocks:
-//   forward:  R, * w_16384^{p3 m}, then per block A, B, C
-//             -> position (p3, m) holds X[p3 + 4 (m2 + 16 m1 + 256 m0)]
-//   second:   per block C, B, A, then * w_16384^{p3 m}, R (outputs t < L only)
-// 16 waves; wave w owns batch b = w of every block; thread tid owns the four
-// consecutive positions m = 4 tid .. 4 tid + 3 of layer R (coalesced I/O, and
-// the u kept for the skip term sits in the same thread as the output).
-namespace mf16 {
-constexpr int N = 16384;
-constexpr int L = 8192;
-constexpr int NW = 16;
-constexpr int NT = 64 * NW;
-}  // namespace mf16
-
-template <int DT>
-__global__ __launch_bounds__(mf16::NT) void fftconv_mfma16384_kernel(ConvArgs a, const float *k,
-                                                                     int wg_per_ch, int pairs_per_ch) {
-    using namespace mf;
-    using mf16::NT;
-    using mf16::NW;
-    constexpr int NN = mf16::N, LL = mf16::L, BLK = 4096;
-    __shared__ uint32_t X[NN];        // four 4096-point blocks, fp16 complex
-    __shared__ float red[2][NW];
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const int c = lane & 15, g = lane >> 4;
-    const int blk = xcd_logical_block(blockIdx.x, gridDim.x);
-    const int h = blk / wg_per_ch, part = blk % wg_per_ch;
-    const int per = (pairs_per_ch + wg_per_ch - 1) / wg_per_ch;
-    const int q0 = part * per, q1 = min(q0 + per, pairs_per_ch);
-    int rsel = 0;
-    auto bexp = [&](float v) -> int {
-        v = wave_max(v);
-        if (lane == 0) red[rsel][w] = v;
-        __syncthreads();
-        float m = red[rsel][0];
-#pragma unroll
-        for (int i = 1; i < NW; ++i) m = fmaxf(m, red[rsel][i]);
-        rsel ^= 1;
-        if (!(m > 0.f) || !(m < 3.0e38f)) return 0;
-        int e;
-        frexpf(m, &e);
-        return e;
-    };
-
-    // lane bases inside a block (block beta adds 4096 beta); batch b = w
-    const int mA = 1024 * g + 64 * (c >> 2) + (c & 3) + 4 * (w ^ ((c >> 2) | (g << 2)));
-    int mB[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) mB[j] = 256 * w + 64 * (c >> 2) + (c & 3) + 16 * (g ^ (w >> 2)) + 4 * (j ^ (c >> 2));
-    const int mC = 256 * w + 64 * g + 4 * (c ^ g ^ ((w >> 2) << 2));
-    // layer R: positions m = 4 tid + e, e < 4, are 4 consecutive dwords at mR
-    const int mR = 256 * (tid >> 6) + 64 * (tid & 3) + 4 * (((tid >> 2) & 15) ^ (tid & 3) ^ ((tid >> 8) << 2));
-
-    uint32_t twA[4], twB[4], tw2[4], twR[4][4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        tw2[j] = twiddle_h((4 * g + j) * c, 256);
-        twA[j] = twiddle_h((4 * g + j) * (16 * w + c), BLK);
-        twB[j] = twiddle_h(w * (16 * (4 * g + j) + c), BLK);
-    }
-#pragma unroll
-    for (int e = 0; e < 4; ++e)
-#pragma unroll
-        for (int k3 = 1; k3 < 4; ++k3) twR[e][k3] = twiddle_h((4 * tid + e) * k3, NN);
-    const Dft16 F = make_dft16(lane);
-
-    // layer R forward from (x0, x1) = values at m and 4096 + m (fp32, already
-    // scaled); the zero padding is x2 = x3 = 0.  Factor 1/2 for range.
-    auto layer_R = [&](const float2 (*x)[2]) {
-        uint32_t o[4][4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const float2 x0 = x[e][0], x1 = x[e][1];
-            // Y[k3] = x0 + x1 (-i)^k3
-            o[0][e] = pack(0.5f * (x0.x + x1.x), 0.5f * (x0.y + x1.y));
-            o[1][e] = cmul_h(pack(0.5f * (x0.x + x1.y), 0.5f * (x0.y - x1.x)), twR[e][1]);
-            o[2][e] = cmul_h(pack(0.5f * (x0.x - x1.x), 0.5f * (x0.y - x1.y)), twR[e][2]);
-            o[3][e] = cmul_h(pack(0.5f * (x0.x - x1.y), 0.5f * (x0.y + x1.x)), twR[e][3]);
-        }
-#pragma unroll
-        for (int k3 = 0; k3 < 4; ++k3)
-            *(uint4 *)&X[mR + BLK * k3] = make_uint4(o[k3][0], o[k3][1], o[k3][2], o[k3][3]);
-        __syncthreads();
-    };
-    auto blocks_AB = [&](const uint32_t *twb) {
-#pragma unroll
-        for (int be = 0; be < 4; ++be) {
-            uint32_t v[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) v[j] = X[mA + 256 * j + BLK * be];
-            f4_t re, im;
-            dft16(F, h8_from(v[0], v[1], v[2], v[3]), re, im);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) X[mA + 256 * j + BLK * be] = cmul_h(pack(re[j], im[j]), twA[j]);
-        }
-        __syncthreads();
-#pragma unroll
-        for (int be = 0; be < 4; ++be) {
-            uint32_t v[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) v[j] = X[mB[j] + BLK * be];
-            f4_t re, im;
-            dft16(F, h8_from(v[0], v[1], v[2], v[3]), re, im);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) X[mB[j] + BLK * be] = cmul_h(pack(re[j], im[j]), twb[j]);
-        }
-        // no barrier: layer C of batch b = p2 is read back by the same wave
-    };
-
-    // ---- kernel spectrum of channel h ----
-    uint32_t K[4][4];
-    int kexp;
-    {
-        const float4 ka = ((const float4 *)(k + (long)h * LL))[tid];
-        const float4 kb = ((const float4 *)(k + (long)h * LL + BLK))[tid];
-        float mx = fmaxf(fmaxf(fabsf(ka.x), fabsf(ka.y)), fmaxf(fabsf(ka.z), fabsf(ka.w)));
-        mx = fmaxf(mx, fmaxf(fmaxf(fabsf(kb.x), fabsf(kb.y)), fmaxf(fabsf(kb.z), fabsf(kb.w))));
-        const int ek = bexp(mx);
-        const float sk = ldexpf(1.0f, -ek);
-        const float2 x[4][2] = {{make_float2(ka.x * sk, 0.f), make_float2(kb.x * sk, 0.f)},
-                                {make_float2(ka.y * sk, 0.f), make_float2(kb.y * sk, 0.f)},
-                                {make_float2(ka.z * sk, 0.f), make_float2(kb.z * sk, 0.f)},
-                                {make_float2(ka.w * sk, 0.f), make_float2(kb.w * sk, 0.f)}};
-        layer_R(x);
-        blocks_AB(tw2);
-        float Kf[4][4][2];
-        float km = 0.f;
-#pragma unroll
-        for (int be = 0; be < 4; ++be) {
-            const uint4 v = *(const uint4 *)&X[mC + BLK * be];
-            f4_t re, im;
-            dft16(F, __builtin_bit_cast(h8_t, v), re, im);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                Kf[be][j][0] = re[j];
-                Kf[be][j][1] = im[j];
-                km = fmaxf(km, fmaxf(fabsf(re[j]), fabsf(im[j])));
-            }
-        }
-        const int e2 = bexp(km);
-#pragma unroll
-        for (int be = 0; be < 4; ++be)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) K[be][j] = pack(ldexpf(Kf[be][j][0], -e2), ldexpf(Kf[be][j][1], -e2));
-        kexp = -ek - 7 - e2;   // forward scale 1/128 (R: 1/2, A, B, C: 1/4 each)
-    }
-
-    const float d = a.D ? a.D[h] : 0.f;
-    const uint16_t *u = (const uint16_t *)a.u;
-    uint16_t *y = (uint16_t *)a.y;
-    auto rows = [&](int qq, long &oa, long &ob) {
-        if (a.pair_mode == 0) {
-            oa = ((long)(2 * qq) * a.H + h) * LL;
-            ob = (2 * qq + 1 < a.B) ? ((long)(2 * qq + 1) * a.H + h) * LL : -1;
-        } else {
-            const int ncp = (a.nchunk + 1) / 2;
-            const int bb = qq / ncp, cp = qq % ncp;
-            oa = (((long)bb * a.H + h) * a.nchunk + 2 * cp) * LL;
-            ob = (2 * cp + 1 < a.nchunk) ? oa + LL : -1;
-        }
-    };
-    for (int qq = q0; qq < q1; ++qq) {
-        long oa, ob;
-        rows(qq, oa, ob);
-        // raw u at m = 4 tid + e and 4096 + m, both rows (8-byte loads)
-        uint2 r[2][2];   // [n3][row]
-#pragma unroll
-        for (int n3 = 0; n3 < 2; ++n3) {
-            r[n3][0] = *(const uint2 *)(u + oa + BLK * n3 + 4 * tid);
-            r[n3][1] = (ob >= 0) ? *(const uint2 *)(u + ob + BLK * n3 + 4 * tid) : make_uint2(0, 0);
-        }
-        float ua[2][4], ub[2][4];
-        float mx = 0.f;
-#pragma unroll
-        for (int n3 = 0; n3 < 2; ++n3) {
-            const uint32_t pa[2] = {r[n3][0].x, r[n3][0].y}, pb[2] = {r[n3][1].x, r[n3][1].y};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const uint32_t ra = (e & 1) ? (pa[e >> 1] >> 16) : (pa[e >> 1] & 0xffffu);
-                const uint32_t rb = (e & 1) ? (pb[e >> 1] >> 16) : (pb[e >> 1] & 0xffffu);
-                ua[n3][e] = lo_f<DT>(ra);
-                ub[n3][e] = lo_f<DT>(rb);
-                mx = fmaxf(mx, fmaxf(fabsf(ua[n3][e]), fabsf(ub[n3][e])));
-            }
-        }
-        const int eu = bexp(mx);
-        {
-            const float su = ldexpf(1.0f, -eu);
-            float2 x[4][2];
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-#pragma unroll
-                for (int n3 = 0; n3 < 2; ++n3) x[e][n3] = make_float2(ua[n3][e] * su, ub[n3][e] * su);
-            layer_R(x);
-        }
-        blocks_AB(tw2);
-        // layer C forward, pointwise product, layer C of the second transform
-#pragma unroll
-        for (int be = 0; be < 4; ++be) {
-            uint4 *px = (uint4 *)&X[mC + BLK * be];
-            f4_t re, im;
-            dft16(F, __builtin_bit_cast(h8_t, *px), re, im);
-            uint32_t yv[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) yv[j] = cmul_h(pack(re[j], im[j]), K[be][j]) ^ 0x80000000u;
-            dft16(F, h8_from(yv[0], yv[1], yv[2], yv[3]), re, im);
-            uint4 o;
-            o.x = cmul_h(pack(re[0], im[0]), tw2[0]);
-            o.y = cmul_h(pack(re[1], im[1]), tw2[1]);
-            o.z = cmul_h(pack(re[2], im[2]), tw2[2]);
-            o.w = cmul_h(pack(re[3], im[3]), tw2[3]);
-            *px = o;
-        }
-        // layers B and A of the second transform (per block); B is wave-local
-#pragma unroll
-        for (int be = 0; be < 4; ++be) {
-            uint32_t v[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) v[j] = X[mB[j] + BLK * be];
-            f4_t re, im;
-            dft16(F, h8_from(v[0], v[1], v[2], v[3]), re, im);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) X[mB[j] + BLK * be] = cmul_h(pack(re[j], im[j]), twB[j]);
-        }
-        __syncthreads();
-#pragma unroll
-        for (int be = 0; be < 4; ++be) {
-            uint32_t v[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) v[j] = X[mA + 256 * j + BLK * be];
-            f4_t re, im;
-            dft16(F, h8_from(v[0], v[1], v[2], v[3]), re, im);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) X[mA + 256 * j + BLK * be] = pack(re[j], im[j]);
-        }
-        __syncthreads();
-        // twiddle w_16384^{p3 m} and radix 4 over p3 -> t = 4096 t3 + m, t3 < 2
-        // y = Re / -Im * 2^(eu - kexp) * 128 * 64 / N  (+ D u)
-        const float sc = ldexpf(128.0f * 64.0f / (float)NN, eu - kexp);
-        float ya[2][4], yb[2][4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            float2 v[4];
-#pragma unroll
-            for (int p3 = 0; p3 < 4; ++p3) {
-                uint32_t x = X[mR + BLK * p3 + e];
-                if (p3) x = cmul_h(x, twR[e][p3]);
-                const h2_t hx = as_h2(x);
-                v[p3] = make_float2((float)hx.x, (float)hx.y);
-            }
-            // t3 = 0: v0 + v1 + v2 + v3 ; t3 = 1: v0 - i v1 - v2 + i v3
-            const float w0r = v[0].x + v[1].x + v[2].x + v[3].x, w0i = v[0].y + v[1].y + v[2].y + v[3].y;
-            const float w1r = v[0].x + v[1].y - v[2].x - v[3].y, w1i = v[0].y - v[1].x - v[2].y + v[3].x;
-            ya[0][e] = fmaf(w0r, sc, d * ua[0][e]);
-            yb[0][e] = fmaf(-w0i, sc, d * ub[0][e]);
-            ya[1][e] = fmaf(w1r, sc, d * ua[1][e]);
-            yb[1][e] = fmaf(-w1i, sc, d * ub[1][e]);
-        }
-#pragma unroll
-        for (int t3 = 0; t3 < 2; ++t3) {
-            const long off = BLK * t3 + 4 * tid;
-            if (a.corr) {
-                if (a.corr16) {
-                    const uint16_t *cr = (const uint16_t *)a.corr;
-                    const uint2 ca = *(const uint2 *)(cr + oa + off);
-                    ya[t3][0] += lo_f<DT>(ca.x); ya[t3][1] += hi_f<DT>(ca.x);
-                    ya[t3][2] += lo_f<DT>(ca.y); ya[t3][3] += hi_f<DT>(ca.y);
-                    if (ob >= 0) {
-                        const uint2 cb = *(const uint2 *)(cr + ob + off);
-                        yb[t3][0] += lo_f<DT>(cb.x); yb[t3][1] += hi_f<DT>(cb.x);
-                        yb[t3][2] += lo_f<DT>(cb.y); yb[t3][3] += hi_f<DT>(cb.y);
-                    }
-                } else {
-                    const float *cr = (const float *)a.corr;
-                    const float4 ca = *(const float4 *)(cr + oa + off);
-                    ya[t3][0] += ca.x; ya[t3][1] += ca.y; ya[t3][2] += ca.z; ya[t3][3] += ca.w;
-                    if (ob >= 0) {
-                        const float4 cb = *(const float4 *)(cr + ob + off);
-                        yb[t3][0] += cb.x; yb[t3][1] += cb.y; yb[t3][2] += cb.z; yb[t3][3] += cb.w;
-                    }
-                }
-            }
-            const uint32_t pa0 = pack_io<DT>(ya[t3][0], ya[t3][1]), pa1 = pack_io<DT>(ya[t3][2], ya[t3][3]);
-            *(uint2 *)(y + oa + off) = make_uint2(pa0, pa1);
-            if (ob >= 0) {
-                const uint32_t pb0 = pack_io<DT>(yb[t3][0], yb[t3][1]), pb1 = pack_io<DT>(yb[t3][2], yb[t3][3]);
-                *(uint2 *)(y + ob + off) = make_uint2(pb0, pb1);
-            }
-        }
-        __syncthreads();   // X is rewritten by the next pair's layer R
-    }
-}
-
-// ============================================================================
-// Transform length N = 2L = 32768 = 8 x 4096 (L = 16384: the fused limit
-// raised by the 160 KB of LDS, which holds the whole signal as fp16 complex,
-// 128 KB).  As the 16384-point kernel above with a radix-8 layer R over the
-// top digit p3 (p = 4096 p3 + m; p3 >= 4 is the zero padding):
-//   forward:  R (1/4), * w_32768^{p3 m}, then per block A, B, C
-//   second:   per block C, B, A, then * w_32768^{p3 m}, R (outputs t < L only)
-// The skip term is folded into the kernel (k[0] += D).  Twiddles of layer R
-// are evaluated where they are used (registers are the limit at 1024 threads
-// per workgroup).  conj_k conjugates the kernel spectrum (the correlation of
-// the backward pass).
 namespace mf32 {
 constexpr int N = 32768;
 constexpr int L = 16384;
@@ -904,7 +308,7 @@ __global__ __launch_bounds__(mf32::NT) void fftconv_mfma32768_kernel(ConvArgs a,
         asm volatile("v_mov_b32 %0, 0" : "=v"(tz));
         long oa, ob;
         rows(qq, oa, ob);
-        float mx = 0.f;
+        float mxa = 0.f, mxb = 0.f;
         float2 x[4][4];   // [e][n3]: (row a, row b) at 4096 n3 + 4 tid + e
 #pragma unroll
         for (int n3 = 0; n3 < 4; ++n3) {
@@ -916,16 +320,18 @@ __global__ __launch_bounds__(mf32::NT) void fftconv_mfma32768_kernel(ConvArgs a,
                 const uint32_t va = (e & 1) ? (pa[e >> 1] >> 16) : (pa[e >> 1] & 0xffffu);
                 const uint32_t vb = (e & 1) ? (pb[e >> 1] >> 16) : (pb[e >> 1] & 0xffffu);
                 x[e][n3] = make_float2(lo_f<DT>(va), lo_f<DT>(vb));
-                mx = fmaxf(mx, fmaxf(fabsf(x[e][n3].x), fabsf(x[e][n3].y)));
+                mxa = fmaxf(mxa, fabsf(x[e][n3].x));
+                mxb = fmaxf(mxb, fabsf(x[e][n3].y));
             }
         }
-        const int eu = bexp(mx);
+        // one power-of-two scale per row of the pair
+        const int eua = bexp(mxa), eub = bexp(mxb);
         {
-            const float su = ldexpf(1.0f, -eu);
+            const float sua = ldexpf(1.0f, -eua), sub = ldexpf(1.0f, -eub);
 #pragma unroll
             for (int e = 0; e < 4; ++e)
 #pragma unroll
-                for (int n3 = 0; n3 < 4; ++n3) x[e][n3] = make_float2(x[e][n3].x * su, x[e][n3].y * su);
+                for (int n3 = 0; n3 < 4; ++n3) x[e][n3] = make_float2(x[e][n3].x * sua, x[e][n3].y * sub);
             layer_R(x);
         }
         blocks_AB();
@@ -973,8 +379,9 @@ __global__ __launch_bounds__(mf32::NT) void fftconv_mfma32768_kernel(ConvArgs a,
         }
         __syncthreads();
         // twiddle w_32768^{p3 m} and radix 8 over p3 -> t = 4096 t3 + m, t3 < 4
-        // y = Re / -Im * 2^(eu - kexp) * 256 * 64 / N
-        const float sc = ldexpf(256.0f * 64.0f / (float)NN, eu - kexp);
+        // y = Re / -Im * 2^(eu - kexp) * 256 * 64 / N, eu of the row
+        const float sca = ldexpf(256.0f * 64.0f / (float)NN, eua - kexp);
+        const float scb = ldexpf(256.0f * 64.0f / (float)NN, eub - kexp);
         float ya[4][4], yb[4][4];   // [t3][e]
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -995,8 +402,8 @@ __global__ __launch_bounds__(mf32::NT) void fftconv_mfma32768_kernel(ConvArgs a,
                     wr += v[p3].x * wv.x - v[p3].y * wv.y;
                     wi += v[p3].x * wv.y + v[p3].y * wv.x;
                 }
-                ya[t3][e] = wr * sc;
-                yb[t3][e] = -wi * sc;
+                ya[t3][e] = wr * sca;
+                yb[t3][e] = -wi * scb;
             }
         }
 #pragma unroll
@@ -1033,11 +440,13 @@ __global__ __launch_bounds__(mf32::NT) void fftconv_mfma32768_kernel(ConvArgs a,
 }
 
 bool fftconv_mfma_supported(int L, int dtype) {
-    return (L == mf::L || L == mf16::L || L == mf32::L) && (dtype == F16 || dtype == BF16);
+    return (fftconv_wave_supported(L, dtype) || fftconv_wave16k_supported(L, dtype) || L == mf32::L) &&
+           (dtype == F16 || dtype == BF16);
 }
 
-// Launch over all channels; returns hipErrorInvalidValue if the shape is not
-// handled here (N != 4096 or 32-bit I/O).
+// 16-bit I/O on the matrix cores: the one-wave kernel (L = 2048), the
+// four-wave kernel (L = 8192) or the 32768-point kernel here (L = 16384);
+// hipErrorInvalidValue for any other shape.
 hipError_t launch_fftconv_mfma(const ConvArgs &a, const float *k, hipStream_t s) {
     if (!fftconv_mfma_supported(a.L, a.dtype)) return hipErrorInvalidValue;
     if (fftconv_wave_supported(a.L, a.dtype)) return launch_fftconv_wave(a, k, s);
@@ -1048,33 +457,13 @@ hipError_t launch_fftconv_mfma(const ConvArgs &a, const float *k, hipStream_t s)
     else
         pairs_per_ch = a.B * ((a.nchunk + 1) / 2);
     // enough workgroups to fill the chip, at least 2 pairs per kernel spectrum
-    int wg_per_ch = 1;
-    while (a.H * wg_per_ch < 512 && pairs_per_ch / (2 * wg_per_ch) >= 2) wg_per_ch *= 2;
-    if (a.L == mf32::L) {
-        int wg32 = 1;
-        while (a.H * wg32 < 512 && pairs_per_ch / (2 * wg32) >= 2) wg32 *= 2;
-        dim3 g32(a.H * wg32), b32(mf32::NT);
-        if (a.dtype == F16)
-            hipLaunchKernelGGL(fftconv_mfma32768_kernel<F16>, g32, b32, 0, s, a, k, wg32, pairs_per_ch);
-        else
-            hipLaunchKernelGGL(fftconv_mfma32768_kernel<BF16>, g32, b32, 0, s, a, k, wg32, pairs_per_ch);
-        return hipGetLastError();
-    }
-    if (a.L == mf16::L) {
-        int wg16 = 1;
-        while (a.H * wg16 < 512 && pairs_per_ch / (2 * wg16) >= 2) wg16 *= 2;
-        dim3 g16(a.H * wg16), b16(mf16::NT);
-        if (a.dtype == F16)
-            hipLaunchKernelGGL(fftconv_mfma16384_kernel<F16>, g16, b16, 0, s, a, k, wg16, pairs_per_ch);
-        else
-            hipLaunchKernelGGL(fftconv_mfma16384_kernel<BF16>, g16, b16, 0, s, a, k, wg16, pairs_per_ch);
-        return hipGetLastError();
-    }
-    dim3 grid(a.H * wg_per_ch), block(mf::NT);
+    int wg32 = 1;
+    while (a.H * wg32 < 512 && pairs_per_ch / (2 * wg32) >= 2) wg32 *= 2;
+    dim3 g32(a.H * wg32), b32(mf32::NT);
     if (a.dtype == F16)
-        hipLaunchKernelGGL(fftconv_mfma4096_kernel<F16>, grid, block, 0, s, a, k, wg_per_ch, pairs_per_ch);
+        hipLaunchKernelGGL(fftconv_mfma32768_kernel<F16>, g32, b32, 0, s, a, k, wg32, pairs_per_ch);
     else
-        hipLaunchKernelGGL(fftconv_mfma4096_kernel<BF16>, grid, block, 0, s, a, k, wg_per_ch, pairs_per_ch);
+        hipLaunchKernelGGL(fftconv_mfma32768_kernel<BF16>, g32, b32, 0, s, a, k, wg32, pairs_per_ch);
     return hipGetLastError();
 }
 

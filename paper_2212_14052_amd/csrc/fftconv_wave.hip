@@ -86,13 +86,13 @@ __device__ __forceinline__ void forward_front(uint32_t (&d)[64], const uint4 *Lc
     for (int i = 0; i < 64; ++i) d[i] = e[i];
     swap_GT(d);
 }
-// L1^H with the output epilogue: fp32 outputs (times rem when REM), plus the
+// L1^H with the output epilogue: fp32 outputs (times rema / remb when REM), plus the
 // correction term (read for every lane: outputs of lanes g >= 2 and of a
 // missing row b are discarded), packed two tiles at a time into d (row a in
 // d[8 s + i], row b in d[8 s + 4 + i], points 2 s and 2 s + 1).
 template <int DT, int CORR, bool REM>
-__device__ __forceinline__ void out_layer(uint32_t (&d)[64], const Dft &Fs, float rem, const void *corr, long oa,
-                                          long obc, int lane) {
+__device__ __forceinline__ void out_layer(uint32_t (&d)[64], const Dft &Fs, float rema, float remb, const void *corr,
+                                          long oa, long obc, int lane) {
     const int g = lane >> 4, c = lane & 15;
     const int pbase = 256 * (4 * (g & 1)) + 16 * c;   // lanes g >= 2 alias g - 2 (in bounds)
     float pr[8];   // previous (even) tile's outputs: rows a and b
@@ -100,8 +100,8 @@ __device__ __forceinline__ void out_layer(uint32_t (&d)[64], const Dft &Fs, floa
         float ya[4], yb[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            ya[i] = REM ? re[i] * rem : re[i];
-            yb[i] = REM ? im[i] * rem : im[i];
+            ya[i] = REM ? re[i] * rema : re[i];
+            yb[i] = REM ? im[i] * remb : im[i];
         }
         if (CORR != 0) {
 #pragma unroll
@@ -330,38 +330,56 @@ fftconv_wave4096_kernel(ConvArgs a, const float *k, int wg_per_ch, int pairs_per
     // One flag guards both the prefetch and the back edge, so the staged
     // registers are dead between their unpacking and the next prefetch.
     while (have) {
-        // max |u|, then packing into (a + i b) complex fp16: p2 = 4 g + j : G,
-        // p1 = c : C, p0 = T : tile
-        float mx;
+        // max |u| per row, then packing into (a + i b) complex fp16: p2 =
+        // 4 g + j : G, p1 = c : C, p0 = T : tile
+        float mxa, mxb;
         if (DT == F16) {
-            h2_t hmx = {0, 0}, hmn = {0, 0};
+            h2_t amx = {0, 0}, amn = {0, 0}, bmx = {0, 0}, bmn = {0, 0};
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
-                const uint32_t v[8] = {ra[i].x, ra[i].y, ra[i].z, ra[i].w, rb[i].x, rb[i].y, rb[i].z, rb[i].w};
+                const uint32_t va[4] = {ra[i].x, ra[i].y, ra[i].z, ra[i].w}, vb[4] = {rb[i].x, rb[i].y, rb[i].z, rb[i].w};
 #pragma unroll
-                for (int e = 0; e < 8; e += 2) {
-                    hmx = __builtin_elementwise_maximum(hmx, __builtin_elementwise_maximum(as_h2(v[e]), as_h2(v[e + 1])));
-                    hmn = __builtin_elementwise_minimum(hmn, __builtin_elementwise_minimum(as_h2(v[e]), as_h2(v[e + 1])));
+                for (int e = 0; e < 4; e += 2) {
+                    amx = __builtin_elementwise_maximum(amx, __builtin_elementwise_maximum(as_h2(va[e]), as_h2(va[e + 1])));
+                    amn = __builtin_elementwise_minimum(amn, __builtin_elementwise_minimum(as_h2(va[e]), as_h2(va[e + 1])));
+                    bmx = __builtin_elementwise_maximum(bmx, __builtin_elementwise_maximum(as_h2(vb[e]), as_h2(vb[e + 1])));
+                    bmn = __builtin_elementwise_minimum(bmn, __builtin_elementwise_minimum(as_h2(vb[e]), as_h2(vb[e + 1])));
                 }
             }
-            mx = fmaxf(fmaxf((float)hmx.x, (float)hmx.y), fmaxf(-(float)hmn.x, -(float)hmn.y));
+            mxa = fmaxf(fmaxf((float)amx.x, (float)amx.y), fmaxf(-(float)amn.x, -(float)amn.y));
+            mxb = fmaxf(fmaxf((float)bmx.x, (float)bmx.y), fmaxf(-(float)bmn.x, -(float)bmn.y));
         } else {
-            uint32_t mb = 0;
+            uint32_t ma = 0, mb = 0;
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
-                const uint32_t v[8] = {ra[i].x, ra[i].y, ra[i].z, ra[i].w, rb[i].x, rb[i].y, rb[i].z, rb[i].w};
+                const uint32_t va[4] = {ra[i].x, ra[i].y, ra[i].z, ra[i].w}, vb[4] = {rb[i].x, rb[i].y, rb[i].z, rb[i].w};
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const uint32_t m = v[e] & 0x7fff7fffu;
-                    mb = max(mb, max(m & 0xffffu, m >> 16));
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t x = va[e] & 0x7fff7fffu, z = vb[e] & 0x7fff7fffu;
+                    ma = max(ma, max(x & 0xffffu, x >> 16));
+                    mb = max(mb, max(z & 0xffffu, z >> 16));
                 }
             }
-            mx = __uint_as_float(mb << 16);
+            mxa = __uint_as_float(ma << 16);
+            mxb = __uint_as_float(mb << 16);
         }
-        mx = wave_max(mx);
-        int eu = 0;
-        if (DT == BF16 || !(mx >= 0.0625f && mx < 16.0f)) eu = exp_of(mx);
-        eu = __builtin_amdgcn_readfirstlane(eu);   // equal in all lanes
+        mxa = wave_max(mxa);
+        mxb = wave_max(mxb);
+        // Each row of the pair has its own power-of-two scale, so the rounding
+        // of the shared fp16 transform stays at each row's own scale.  fp16
+        // inputs are left as they are while both rows sit in [2^-4, 16) within
+        // a factor of four of each other (the common case); bf16 inputs are
+        // converted (and scaled) anyway.
+        int ea = exp_of(mxa), eb = exp_of(mxb);
+        if (!(mxa > 0.f)) ea = eb;   // an all-zero (or absent) row takes its partner's scale
+        if (!(mxb > 0.f)) eb = ea;
+        int eua = 0, eub = 0;
+        if (DT == BF16 || !(ea >= -3 && ea <= 4 && eb >= -3 && eb <= 4 && abs(ea - eb) <= 1)) {
+            eua = ea;
+            eub = eb;
+        }
+        eua = __builtin_amdgcn_readfirstlane(eua);   // equal in all lanes
+        eub = __builtin_amdgcn_readfirstlane(eub);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
 #pragma unroll
@@ -375,17 +393,16 @@ fftconv_wave4096_kernel(ConvArgs a, const float *k, int wg_per_ch, int pairs_per
                         d[4 * T + j] = __builtin_amdgcn_perm(B4[s], A4[s], 0x05040100u);
                         d[4 * (T + 1) + j] = __builtin_amdgcn_perm(B4[s], A4[s], 0x07060302u);
                     } else {
-                        d[4 * T + j] = pk(ldexpf(lo_f<DT>(A4[s]), -eu), ldexpf(lo_f<DT>(B4[s]), -eu));
-                        d[4 * (T + 1) + j] = pk(ldexpf(hi_f<DT>(A4[s]), -eu), ldexpf(hi_f<DT>(B4[s]), -eu));
+                        d[4 * T + j] = pk(ldexpf(lo_f<DT>(A4[s]), -eua), ldexpf(lo_f<DT>(B4[s]), -eub));
+                        d[4 * (T + 1) + j] = pk(ldexpf(hi_f<DT>(A4[s]), -eua), ldexpf(hi_f<DT>(B4[s]), -eub));
                     }
                 }
             }
         }
-        if (DT == F16 && eu != 0) {
-            const _Float16 s = (_Float16)ldexpf(1.0f, -eu);
-            const h2_t s2 = {s, s};
+        if (DT == F16 && (eua | eub) != 0) {
+            // in float32: 2^-e may leave fp16's range
 #pragma unroll
-            for (int i = 0; i < 64; ++i) d[i] = as_u32(as_h2(d[i]) * s2);
+            for (int i = 0; i < 64; ++i) d[i] = pk(ldexpf((float)as_h2(d[i]).x, -eua), ldexpf((float)as_h2(d[i]).y, -eub));
         }
 
         forward_front(d, Lc, Ytab, lane);
@@ -430,24 +447,26 @@ fftconv_wave4096_kernel(ConvArgs a, const float *k, int wg_per_ch, int pairs_per
             });
         }
         // L1^H: outputs p2 = 4 g + i (kept for g < 2), p1 = c, p0 = tile.
-        // The output scale 2^(kexp + eu) rides on the DFT matrix as far as fp16
+        // The output scales 2^(kexp + eua), 2^(kexp + eub) ride on the DFT matrix as far as fp16
         // allows; any remainder is applied in fp32.
         long oa, ob;
         rows(qq, oa, ob);
-        const int se = kexp + eu;
-        const int sf = min(max(se, -10), 14), srem = se - sf;
-        const float rem = ldexpf(1.0f, srem);
+        // The real rows of L1^H make row a, the imaginary rows row b: each
+        // carries its own row's scale.
+        const int sea = kexp + eua, seb = kexp + eub;
+        const int sfa = min(max(sea, -10), 14), srema = sea - sfa;
+        const int sfb = min(max(seb, -10), 14), sremb = seb - sfb;
         Dft Fs = lds_dft(Lc, lane, true);
-        Fs.re = h8_scale(Fs.re, (_Float16)ldexpf(1.0f, sf));
-        Fs.im = h8_scale(Fs.im, (_Float16)ldexpf(1.0f, sf));
+        Fs.re = h8_scale(Fs.re, (_Float16)ldexpf(1.0f, sfa));
+        Fs.im = h8_scale(Fs.im, (_Float16)ldexpf(1.0f, sfb));
         // branch-free epilogue (a branch inside it lets the compiler hoist
         // all of the layer's MFMAs above it); the rare remainder scale picks
         // a second instance of the layer instead
         const long obc = ob >= 0 ? ob : oa;   // row b's correction read from row a if absent
-        if (srem == 0)
-            out_layer<DT, CORR, false>(d, Fs, 1.0f, a.corr, oa, obc, lane);
+        if ((srema | sremb) == 0)
+            out_layer<DT, CORR, false>(d, Fs, 1.0f, 1.0f, a.corr, oa, obc, lane);
         else
-            out_layer<DT, CORR, true>(d, Fs, rem, a.corr, oa, obc, lane);
+            out_layer<DT, CORR, true>(d, Fs, ldexpf(1.0f, srema), ldexpf(1.0f, sremb), a.corr, oa, obc, lane);
         if (g < 2) {
             uint16_t *ya_row = y + oa, *yb_row = y + obc;   // wave-uniform bases
 #pragma unroll
@@ -571,10 +590,9 @@ __device__ __forceinline__ int pack_pair(const uint4 (&ra)[8], const uint4 (&rb)
         }
     }
     if (DT == F16 && eu != 0) {
-        const _Float16 sc = (_Float16)ldexpf(1.0f, -eu);
-        const h2_t s2 = {sc, sc};
+        // in float32: 2^-eu may leave fp16's range
 #pragma unroll
-        for (int i = 0; i < 64; ++i) d[i] = as_u32(as_h2(d[i]) * s2);
+        for (int i = 0; i < 64; ++i) d[i] = pk(ldexpf((float)as_h2(d[i]).x, -eu), ldexpf((float)as_h2(d[i]).y, -eu));
     }
     // packing complete here: the raw registers are dead before the transform
 #pragma unroll

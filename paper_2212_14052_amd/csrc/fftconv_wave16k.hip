@@ -171,16 +171,18 @@ __device__ __forceinline__ void kinds_rot(int k3, const uint32_t (&R)[4], const 
         Ib[i] = (sw ? R[i] : I[i]) ^ ni;
     }
 }
-// the same four rows as bf16, every entry times s
-__device__ __forceinline__ void kinds_bf16(const uint32_t (&R)[4], const uint32_t (&I)[4], float s, bf8_t &Rb,
-                                           bf8_t &Ib) {
+// the same four rows as bf16, the entries that multiply the real half of a
+// point (row a) times sa, those that multiply the imaginary half (row b)
+// times sb
+__device__ __forceinline__ void kinds_bf16(const uint32_t (&R)[4], const uint32_t (&I)[4], float sa, float sb,
+                                           bf8_t &Rb, bf8_t &Ib) {
     float r[8], im[8];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        r[2 * i] = (float)as_h2(R[i]).x * s;
-        r[2 * i + 1] = (float)as_h2(R[i]).y * s;
-        im[2 * i] = (float)as_h2(I[i]).x * s;
-        im[2 * i + 1] = (float)as_h2(I[i]).y * s;
+        r[2 * i] = (float)as_h2(R[i]).x * sa;
+        r[2 * i + 1] = (float)as_h2(R[i]).y * sb;
+        im[2 * i] = (float)as_h2(I[i]).x * sa;
+        im[2 * i + 1] = (float)as_h2(I[i]).y * sb;
     }
     typedef float f8_t __attribute__((ext_vector_type(8)));
     const f8_t vr = {r[0], r[1], r[2], r[3], r[4], r[5], r[6], r[7]};
@@ -372,7 +374,7 @@ __device__ __forceinline__ void fused_state_term(const uint4 *U, const uint4 *CT
 // times the lane's w_64^{-k3' c} (gf[k3' - 1]).
 template <int DT, int CORR>
 __device__ __forceinline__ void last_layer(uint32_t (&d)[64], uint4 *U, const uint4 *G1, const uint4 *Lc,
-                                           const uint32_t (&gf)[3], int w, int lane, float sc, uint16_t *ya,
+                                           const uint32_t (&gf)[3], int w, int lane, float sca, float scb, uint16_t *ya,
                                            uint16_t *yb, bool has_b, const void *cra, const void *crb, int ewa,
                                            int ewb) {
     const int g = lane >> 4, c = lane & 15;
@@ -456,10 +458,10 @@ __device__ __forceinline__ void last_layer(uint32_t (&d)[64], uint4 *U, const ui
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj) {
             const int s = 2 * jj + half;
-            pa0[s] = pack_out<DT>(D[0][0][jj] * sc, D[1][0][jj] * sc);
-            pb0[s] = pack_out<DT>(D[0][1][jj] * sc, D[1][1][jj] * sc);
-            pa1[s] = pack_out<DT>(D[0][2][jj] * sc, D[1][2][jj] * sc);
-            pb1[s] = pack_out<DT>(D[0][3][jj] * sc, D[1][3][jj] * sc);
+            pa0[s] = pack_out<DT>(D[0][0][jj] * sca, D[1][0][jj] * sca);
+            pb0[s] = pack_out<DT>(D[0][1][jj] * scb, D[1][1][jj] * scb);
+            pa1[s] = pack_out<DT>(D[0][2][jj] * sca, D[1][2][jj] * sca);
+            pb1[s] = pack_out<DT>(D[0][3][jj] * scb, D[1][3][jj] * scb);
         }
     }
     // outputs m = 256 (4 g + jj) + 16 c + 4 w + (0..3) of both rows go
@@ -513,27 +515,27 @@ __device__ __forceinline__ void last_layer(uint32_t (&d)[64], uint4 *U, const ui
 }
 
 // Maximum |.| of 16-bit raw values (both halves of each dword)
-template <int DT> __device__ __forceinline__ float raw_max(const uint4 (&ra)[4], const uint4 (&rb)[4]);
-template <> __device__ __forceinline__ float raw_max<F16>(const uint4 (&ra)[4], const uint4 (&rb)[4]) {
+template <int DT> __device__ __forceinline__ float raw_max(const uint4 (&ra)[4]);
+template <> __device__ __forceinline__ float raw_max<F16>(const uint4 (&ra)[4]) {
     h2_t hmx = {0, 0}, hmn = {0, 0};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const uint32_t v[8] = {ra[i].x, ra[i].y, ra[i].z, ra[i].w, rb[i].x, rb[i].y, rb[i].z, rb[i].w};
+        const uint32_t v[4] = {ra[i].x, ra[i].y, ra[i].z, ra[i].w};
 #pragma unroll
-        for (int e = 0; e < 8; e += 2) {
+        for (int e = 0; e < 4; e += 2) {
             hmx = __builtin_elementwise_maximum(hmx, __builtin_elementwise_maximum(as_h2(v[e]), as_h2(v[e + 1])));
             hmn = __builtin_elementwise_minimum(hmn, __builtin_elementwise_minimum(as_h2(v[e]), as_h2(v[e + 1])));
         }
     }
     return fmaxf(fmaxf((float)hmx.x, (float)hmx.y), fmaxf(-(float)hmn.x, -(float)hmn.y));
 }
-template <> __device__ __forceinline__ float raw_max<BF16>(const uint4 (&ra)[4], const uint4 (&rb)[4]) {
+template <> __device__ __forceinline__ float raw_max<BF16>(const uint4 (&ra)[4]) {
     us2_t mb = {0, 0};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const uint32_t v[8] = {ra[i].x, ra[i].y, ra[i].z, ra[i].w, rb[i].x, rb[i].y, rb[i].z, rb[i].w};
+        const uint32_t v[4] = {ra[i].x, ra[i].y, ra[i].z, ra[i].w};
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
+        for (int e = 0; e < 4; ++e)
             mb = __builtin_elementwise_max(mb, __builtin_bit_cast(us2_t, v[e] & 0x7fff7fffu));
     }
     const uint32_t m = max((uint32_t)mb.x, (uint32_t)mb.y);
@@ -554,7 +556,7 @@ __global__ __launch_bounds__(w16::NT) __attribute__((amdgpu_waves_per_eu(2))) vo
     constexpr int kTabAll = CORR == 3 ? kTab + CORR_TAB_U4 : kTab16;
     __shared__ uint4 Tab[kTabAll];
     __shared__ uint4 U[kU];         // pair staging, then the last-layer exchange
-    __shared__ float red[2 * NW];
+    __shared__ float red[3 * NW];   // row a max | kernel spectrum max | row b max
     const uint4 *Ytab = Tab, *Lc = Tab + kTabY, *G1 = Tab + kTab;
     uint32_t *Ud = (uint32_t *)U;
     const int tid = threadIdx.x, lane = tid & 63;
@@ -720,14 +722,29 @@ __global__ __launch_bounds__(w16::NT) __attribute__((amdgpu_waves_per_eu(2))) vo
 #pragma unroll
         for (int i = 0; i < 4; ++i) asm volatile("" : "+v"(f1[i]), "+v"(xf[i]), "+v"(f3[i]));
         asm volatile("" : "+v"(g3), "+v"(xh));
-        float mx = raw_max<DT>(ra, rb);
-        mx = wave_max(mx);
-        if (lane == 0) red[w] = mx;
+        {
+            const float mxa = wave_max(raw_max<DT>(ra)), mxb = wave_max(raw_max<DT>(rb));
+            if (lane == 0) {
+                red[w] = mxa;
+                red[2 * NW + w] = mxb;
+            }
+        }
         __syncthreads();   // red; the previous pair's exchange reads are done
-        const float gm = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-        int eu = 0;
-        if (DT == BF16 || !(gm >= 0.0625f && gm < 16.0f)) eu = exp_of(gm);
-        eu = __builtin_amdgcn_readfirstlane(eu);
+        const float gma = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+        const float gmb = fmaxf(fmaxf(red[2 * NW], red[2 * NW + 1]), fmaxf(red[2 * NW + 2], red[2 * NW + 3]));
+        // one power-of-two scale per row (see the one-wave kernel): fp16
+        // inputs stay as they are while both rows sit in [2^-4, 16) within a
+        // factor of four of each other
+        int ea = exp_of(gma), eb = exp_of(gmb);
+        if (!(gma > 0.f)) ea = eb;
+        if (!(gmb > 0.f)) eb = ea;
+        int eua = 0, eub = 0;
+        if (DT == BF16 || !(ea >= -3 && ea <= 4 && eb >= -3 && eb <= 4 && abs(ea - eb) <= 1)) {
+            eua = ea;
+            eub = eb;
+        }
+        eua = __builtin_amdgcn_readfirstlane(eua);
+        eub = __builtin_amdgcn_readfirstlane(eub);
         // interleave (u_a, u_b) and stage; fp16 inputs out of range are
         // scaled here, bf16 inputs through the first layer's matrix
 #pragma unroll
@@ -740,9 +757,9 @@ __global__ __launch_bounds__(w16::NT) __attribute__((amdgpu_waves_per_eu(2))) vo
                 for (int s = 0; s < 4; ++s) {
                     uint32_t lo = __builtin_amdgcn_perm(B4[s], A4[s], 0x05040100u);
                     uint32_t hi = __builtin_amdgcn_perm(B4[s], A4[s], 0x07060302u);
-                    if (DT == F16 && eu != 0) {
-                        lo = pk(ldexpf((float)as_h2(lo).x, -eu), ldexpf((float)as_h2(lo).y, -eu));
-                        hi = pk(ldexpf((float)as_h2(hi).x, -eu), ldexpf((float)as_h2(hi).y, -eu));
+                    if (DT == F16 && (eua | eub) != 0) {
+                        lo = pk(ldexpf((float)as_h2(lo).x, -eua), ldexpf((float)as_h2(lo).y, -eub));
+                        hi = pk(ldexpf((float)as_h2(hi).x, -eua), ldexpf((float)as_h2(hi).y, -eub));
                     }
                     Ud[stage_at(gi, 8 * hh + 2 * s)] = lo;
                     Ud[stage_at(gi, 8 * hh + 2 * s + 1)] = hi;
@@ -765,10 +782,10 @@ __global__ __launch_bounds__(w16::NT) __attribute__((amdgpu_waves_per_eu(2))) vo
                 const Dft Fa = dft_of(R, I), Fb = dft_of(Rb, Ib);
                 layer1(U, lane, Fa.re, Fa.im, Fb.re, Fb.im, epi);
             } else {
-                const float s = ldexpf(1.0f, -eu);
+                const float sa = ldexpf(1.0f, -eua), sb = ldexpf(1.0f, -eub);
                 bf8_t Far, Fai, Fbr, Fbi;
-                kinds_bf16(R, I, s, Far, Fai);
-                kinds_bf16(Rb, Ib, s, Fbr, Fbi);
+                kinds_bf16(R, I, sa, sb, Far, Fai);
+                kinds_bf16(Rb, Ib, sa, sb, Fbr, Fbi);
                 layer1(U, lane, Far, Fai, Fbr, Fbi, epi);
             }
         }
@@ -828,7 +845,7 @@ __global__ __launch_bounds__(w16::NT) __attribute__((amdgpu_waves_per_eu(2))) vo
         for (int i = 0; i < 64; ++i) asm volatile("" ::"v"(d[i]));
         long oa, ob;
         rows(qq, oa, ob);
-        const float sc = ldexpf(1.0f, kexp + eu);
+        const float sca = ldexpf(1.0f, kexp + eua), scb = ldexpf(1.0f, kexp + eub);
         uint16_t *ya = y + oa, *yb = y + (ob >= 0 ? ob : oa);
         const long obc = ob >= 0 ? ob : oa;
         const void *cra = nullptr, *crb = nullptr;
@@ -846,7 +863,7 @@ __global__ __launch_bounds__(w16::NT) __attribute__((amdgpu_waves_per_eu(2))) vo
             ewa = a.corr_e[oa / L];
             ewb = a.corr_e[obc / L];
         }
-        last_layer<DT, CORR>(d, U, G1, Lc, gf, w, lane, sc, ya, yb, ob >= 0, cra, crb, ewa, ewb);
+        last_layer<DT, CORR>(d, U, G1, Lc, gf, w, lane, sca, scb, ya, yb, ob >= 0, cra, crb, ewa, ewb);
     }
 }
 

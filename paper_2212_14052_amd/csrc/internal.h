@@ -102,6 +102,14 @@ hipError_t launch_state_scan_w16(const float *Abar, const float *C, const float 
 hipError_t launch_state_correction_mfma(const float *Abar, const float2 *corr_W, int B, int H, int m,
                                         int chunk, int nchunk, int dtype, void *corr, hipStream_t s);
 
+// State passing (the C ABI entry points validate, then run it).
+size_t statepass_workspace(int B, int H, int L, int m, int chunk, int dtype);
+int statepass_check(const void *u, const float *Abar, const float *Bbar, const float *C, const void *y,
+                    const float *x_final, int B, int H, int L, int m, int chunk, int dtype);
+int statepass_run(const void *u, const float *Abar, const float *Bbar, const float *C, const float *D,
+                  const float *x0, int B, int H, int L, int m, int chunk, int dtype, void *y, float *x_final,
+                  char *ws, hipStream_t s);
+
 // Layer pieces.
 hipError_t launch_transpose_batched(const void *in, void *out, int nb, int R, int C, hipStream_t s);
 // O (B, L, d) token-major = (Q * S)^T per batch slice, Q and S (B, d, L); R = d, C = L.

@@ -41,7 +41,11 @@ def test_workspace_sizes():
     ws = h3.workspace_size(h3.OP_FFTCONV, 8, 768, 2048, 0, 0, h3.F16)
     assert ws >= 768 * 2049 * 8
     ws = h3.workspace_size(h3.OP_STATEPASS, 2, 1024, 131072, 64, 8192, h3.F16)
-    assert ws >= 2 * 1024 * 16 * 64 * 8 * 2
+    # fused initial-state path: chunk kernel, end-states, power tables and
+    # normalised weights, not a (B, H, L) correction term
+    assert 1024 * 8192 * 4 + 2 * 1024 * 16 * 64 * 8 <= ws < 2 * 1024 * 131072 * 2
+    # float32 I/O keeps the float32 correction term (B, H, L)
+    assert h3.workspace_size(h3.OP_STATEPASS, 2, 64, 16384, 64, 1024, h3.F32) >= 2 * 64 * 16384 * 4
     assert h3.workspace_size(h3.OP_STATEPASS, 2, 4, 100, 64, 64, h3.F16) == 0   # L % chunk
     assert h3.workspace_size(99, 1, 1, 16, 0, 0, 0) == 0
     assert h3.workspace_size(h3.OP_FFTCONV, 1, 1, 16, 0, 0, 7) == 0
@@ -105,6 +109,8 @@ def test_layer_validation():
     assert layer(shift=0) == EINVAL
     assert layer(dt=0) == EUNSUP                    # fp32 layer not built
     assert layer(d=100) == EUNSUP
+    assert layer(d=64) == EUNSUP                    # d a multiple of 128 (documented)
+    assert layer(d=192) == EUNSUP
     assert layer(m_s=65) == EUNSUP
     assert layer(L=100) == EUNSUP
     assert layer(B=1, L=64) == EUNSUP               # B*L not a multiple of 128
@@ -189,3 +195,24 @@ def test_layer_heads_validation():
     assert h3.workspace_size(h3.OP_LAYER_HEADS, 4, 2560, 2048, 64, 3, h3.BF16) == 0
     assert (h3.workspace_size(h3.OP_LAYER_HEADS, 4, 2560, 2048, 64, 1, h3.BF16)
             == h3.workspace_size(h3.OP_LAYER, 4, 2560, 2048, 64, 0, h3.BF16))
+
+
+def test_binding_rejects_host_tensors():
+    """The binding refuses CPU tensors before reaching the library (no GPU
+    needed: nothing is launched)."""
+    import torch
+    u = torch.zeros((2, 3, 64), dtype=torch.float16)
+    k = torch.zeros((3, 64))
+    with pytest.raises(ValueError):
+        h3.fftconv(u, k)
+    with pytest.raises(ValueError):
+        h3.kernel_spectrum(k)
+    P = torch.zeros((3, 8, 2))
+    with pytest.raises(ValueError):
+        h3.statepass_conv(u, P, P, P, None, 16)
+    with pytest.raises(ValueError):
+        h3.ssm_step(u[..., 0], P, P, P, None, torch.zeros((2, 3, 8, 2)))
+    x = torch.zeros((2, 128, 128), dtype=torch.bfloat16)
+    W = torch.zeros((128, 128), dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        h3.layer_fwd(x, W, W, W, W, torch.zeros((128, 4)), None, torch.zeros((128, 128)), None)

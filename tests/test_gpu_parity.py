@@ -1,8 +1,13 @@
 """GPU parity: the HIP path (through the C ABI) against the float64 oracle on
 the same seeded, rounded inputs.
 
-Metric: err = max|y - y_oracle| / max|y_oracle| per output tensor.  Gates:
-1e-5 for float32 I/O, 2e-2 for fp16/bf16 I/O (fp32 accumulation).
+Metric: rel_err = max|y - y_oracle| / max|y_oracle| per output tensor, and the
+same per row (worst row), both below the gate: 1e-5 for float32 I/O, 2e-2 for
+fp16/bf16 I/O (fp32 accumulation).  Every comparison is recorded (test id,
+both errors, RMS error, tolerance) in the parity log (tests/_util.check).
+
+The workload configurations are compared on whole tensors at full size, in
+the launch configuration the benchmark times.
 """
 import math
 
@@ -12,7 +17,7 @@ import torch
 
 import oracle
 import workloads
-from tests._util import cplx64, cplx_to_f32pairs, f32dev, rel_err, to_dev, to_np64
+from tests._util import check, cplx64, cplx_to_f32pairs, f32dev, to_dev, to_np64
 
 pytestmark = pytest.mark.gpu
 
@@ -39,18 +44,18 @@ def test_discretize(h3):
     A, B, C, dt = _diag_params(w)
     Ab, Bb = h3.ssm_discretize(f32dev(w.ssm.A), f32dev(w.ssm.B), f32dev(w.ssm.dt))
     rA, rB = oracle.zoh(A, B, dt)
-    assert np.abs(cplx64(to_np64(Ab)) - rA).max() < 1e-6
-    assert rel_err(cplx64(to_np64(Bb)).view(np.float64), rB.view(np.float64)) < 1e-6
+    check(cplx64(to_np64(Ab)), rA, 1e-6, "Abar", rows=False)
+    check(cplx64(to_np64(Bb)), rB, 1e-6, "Bbar", rows=False)
 
 
-@pytest.mark.parametrize("L,dt_lo,dt_hi", [(1024, 1e-3, 1e-1), (100, 1e-3, 1e-1), (8192, 1e-4, 1e-1), (64, 1e-2, 1e-1), (192, 1e-3, 1e-1),
-                                           (2049, 1e-2, 1e-1), (16, 1e-3, 1e-1)])
+@pytest.mark.parametrize("L,dt_lo,dt_hi", [(1024, 1e-3, 1e-1), (100, 1e-3, 1e-1), (8192, 1e-4, 1e-1), (64, 1e-2, 1e-1),
+                                           (192, 1e-3, 1e-1), (2049, 1e-2, 1e-1), (16, 1e-3, 1e-1)])
 def test_ssm_kernel(h3, L, dt_lo, dt_hi):
     w = workloads.config(0, H=16, L=16, seed=7, dt_lo=dt_lo, dt_hi=dt_hi)
     A, B, C, dt = _diag_params(w)
     k = h3.ssm_kernel(f32dev(w.ssm.A), f32dev(w.ssm.B), f32dev(w.ssm.C), f32dev(w.ssm.dt), L)
     ref = oracle.ssm_kernel(A, B, C, dt, L)
-    assert rel_err(to_np64(k), ref) < 2e-6
+    check(k, ref, 2e-6, "k")
 
 
 # --------------------------------------------------------- S2-S4: conv ---
@@ -69,20 +74,19 @@ def _conv_case(h3, B, H, L, dtype, seed, dt_lo=1e-3, dt_hi=1e-1, with_D=True):
 @pytest.mark.parametrize("L", [16, 32, 64, 128, 256, 512, 1024, 2048, 4096, 8192])
 def test_fftconv_f32_all_lengths(h3, L):
     y, ref = _conv_case(h3, 3, 5, L, workloads.F32, seed=L)
-    assert rel_err(y, ref) < TOL[workloads.F32]
+    check(y, ref, TOL[workloads.F32])
 
 
 @pytest.mark.parametrize("dtype", [workloads.F16, workloads.BF16])
 @pytest.mark.parametrize("L", [16, 256, 2048, 8192])
 def test_fftconv_16bit(h3, dtype, L):
     y, ref = _conv_case(h3, 4, 3, L, dtype, seed=L + 1, dt_lo=1e-4)
-    # compare against the oracle rounded to the output dtype as well
-    assert rel_err(y, ref) < TOL[dtype]
+    check(y, ref, TOL[dtype])
 
 
 def test_fftconv_no_skip_odd_batch(h3):
     y, ref = _conv_case(h3, 1, 7, 512, workloads.F32, seed=3, with_D=False)
-    assert rel_err(y, ref) < 1e-5
+    check(y, ref, 1e-5)
 
 
 def test_fftconv_impulse_returns_kernel(h3):
@@ -91,7 +95,8 @@ def test_fftconv_impulse_returns_kernel(h3):
     k = rng.standard_normal((H, L)).astype(np.float32) * np.exp(-np.arange(L) / 300).astype(np.float32)
     u = np.zeros((2, H, L), np.float32); u[:, :, 0] = 1.0
     y = to_np64(h3.fftconv(f32dev(u), f32dev(k), None))
-    assert rel_err(y[0], k) < 1e-5 and rel_err(y[1], k) < 1e-5
+    check(y[0], k, 1e-5, "row0")
+    check(y[1], k, 1e-5, "row1")
 
 
 def test_fftconv_causality(h3):
@@ -116,44 +121,96 @@ def test_fftconv_deterministic(h3):
     assert torch.equal(a, b)
 
 
-def _end_to_end_conv(h3, w, rows):
-    """S1 -> S2/S3 on the GPU at full size; oracle on the sampled rows."""
+# Two rows of one channel share one complex transform.  A row far smaller
+# than its partner must keep its own relative accuracy (each row carries its
+# own power-of-two scale), at every fused length and dtype.
+@pytest.mark.parametrize("dtype,L", [(workloads.F16, 2048), (workloads.BF16, 2048), (workloads.F16, 8192),
+                                     (workloads.BF16, 8192), (workloads.F16, 16384), (workloads.F32, 1024),
+                                     (workloads.F32, 8192), (workloads.F16, 512)])
+@pytest.mark.parametrize("small", [1e-3, 0.3, 7.0])
+def test_fftconv_pair_with_unequal_rows(h3, dtype, L, small):
+    B, H = 4, 3
+    w = workloads.conv_workload("t", B, H, L, workloads.F32, seed=L + 5, dt_lo=1e-4)
+    A, Bm, C, dt = _diag_params(w)
+    k32 = oracle.ssm_kernel(A, Bm, C, dt, L).astype(np.float32)
+    u = w.u.astype(np.float64)
+    u[1] *= small          # row b of pair 0 (batches 0, 1)
+    u[2] *= 1.0 / small    # row a of pair 1 (batches 2, 3)
+    s, u64 = workloads.round_to(u, dtype)
+    y = h3.fftconv(to_dev(s, dtype), f32dev(k32), f32dev(w.D))
+    torch.cuda.synchronize()
+    ref = oracle.causal_conv(u64, k32.astype(np.float64), w.D.astype(np.float64))
+    check(y, ref, TOL[dtype])
+
+
+def _end_to_end_conv(h3, w, k_tol, y_tol):
+    """S1 -> S2/S3 on the GPU at full size, against the oracle on every row."""
     k = h3.ssm_kernel(f32dev(w.ssm.A), f32dev(w.ssm.B), f32dev(w.ssm.C), f32dev(w.ssm.dt), w.L)
     y = h3.fftconv(to_dev(w.u, w.dtype), k, f32dev(w.D))
     torch.cuda.synchronize()
     A, B, C, dt = _diag_params(w)
-    y = y.view(w.B * w.H, w.L)
-    errs = []
-    ysel = to_np64(y[torch.tensor(rows, device=y.device)])
-    for i, r in enumerate(rows):
-        b, h = divmod(r, w.H)
-        kh = oracle.ssm_kernel(A[h:h + 1], B[h:h + 1], C[h:h + 1], dt[h:h + 1], w.L)
-        ref = oracle.causal_conv(w.u64[b, h][None, None], kh, np.array([w.D[h]], np.float64))
-        errs.append((ysel[i], ref[0, 0]))
-    ya = np.stack([e[0] for e in errs]); ra = np.stack([e[1] for e in errs])
-    return rel_err(ya, ra)
+    k_ref = oracle.ssm_kernel(A, B, C, dt, w.L)
+    check(k, k_ref, k_tol, "k")
+    y_ref = oracle.causal_conv(w.u64, k_ref, w.D.astype(np.float64))
+    check(y, y_ref, y_tol, "y")
 
 
-def test_config0_end_to_end_f32(h3):
-    w = workloads.config(0)
-    err = _end_to_end_conv(h3, w, list(range(w.B * w.H)))
-    assert err < 1e-5, err
+def test_config0_full_f32(h3):
+    _end_to_end_conv(h3, workloads.config(0), 2e-6, 1e-5)
 
 
-def test_config1_full_size_sampled_rows(h3):
+def test_config1_full_size(h3):
+    """B=8 H=768 L=2048 fp16: the benchmark's step (kernel generation + the
+    one-wave fused conv) on every row."""
+    _end_to_end_conv(h3, workloads.config(1), 2e-6, 2e-2)
+
+
+def test_config1_shift_kernel_full_size(h3):
+    """The same shape with the shift-SSM kernel (k_t = C_t for t < 64, else 0)."""
     w = workloads.config(1)
-    rng = np.random.default_rng(11)
-    rows = sorted(rng.choice(w.B * w.H, 24, replace=False).tolist()) + [0, w.B * w.H - 1]
-    err = _end_to_end_conv(h3, w, rows)
-    assert err < 2e-2, err
+    ks = np.zeros((w.H, w.L), np.float32)
+    ks[:, :64] = w.shift_C
+    y = h3.fftconv(to_dev(w.u, w.dtype), f32dev(ks), None)
+    torch.cuda.synchronize()
+    check(y, oracle.causal_conv(w.u64, ks.astype(np.float64), None), 2e-2)
 
 
-def test_config2_full_size_sampled_rows(h3):
-    w = workloads.config(2)
-    rng = np.random.default_rng(12)
-    rows = sorted(rng.choice(w.B * w.H, 12, replace=False).tolist()) + [w.B * w.H - 1]
-    err = _end_to_end_conv(h3, w, rows)
-    assert err < 2e-2, err
+def test_config2_full_size(h3):
+    """B=16 H=256 L=8192 bf16 (the four-wave conv at the paper's fused limit)."""
+    _end_to_end_conv(h3, workloads.config(2), 2e-6, 2e-2)
+
+
+# ------------------------------------------ S2 / S3 split: spectral entry ---
+@pytest.mark.parametrize("L", [16, 128, 1024, 2048, 8192])
+def test_kernel_spectrum(h3, L):
+    H = 5
+    rng = np.random.default_rng(L)
+    k = (rng.standard_normal((H, L)) * np.exp(-np.arange(L) / (L / 4))).astype(np.float32)
+    K = to_np64(h3.kernel_spectrum(f32dev(k)))
+    Kc = K[..., 0] + 1j * K[..., 1]
+    # definition: (1/2L) sum_t k_t exp(-2 pi i f t / 2L), f = 0..L, by a dense
+    # DFT matrix product in float64
+    t = np.arange(L)
+    f = np.arange(L + 1)
+    F = np.exp(-2j * np.pi * np.outer(f, t) / (2 * L))
+    ref = (k.astype(np.float64) @ F.T) / (2 * L)
+    check(Kc, ref, 1e-5)
+
+
+@pytest.mark.parametrize("dtype", [workloads.F32, workloads.F16, workloads.BF16])
+@pytest.mark.parametrize("L", [64, 2048, 8192])
+def test_fftconv_spectral(h3, dtype, L):
+    """The convolution from a spectrum computed once, reused by two calls."""
+    w = workloads.conv_workload("t", 3, 4, L, dtype, seed=L + 11)
+    A, Bm, C, dt = _diag_params(w)
+    k32 = oracle.ssm_kernel(A, Bm, C, dt, L).astype(np.float32)
+    K = h3.kernel_spectrum(f32dev(k32))
+    u = to_dev(w.u, dtype)
+    y1 = h3.fftconv_spectral(u, K, f32dev(w.D))
+    y2 = h3.fftconv_spectral(u[:1].contiguous(), K, None)
+    torch.cuda.synchronize()
+    check(y1, oracle.causal_conv(w.u64, k32.astype(np.float64), w.D.astype(np.float64)), TOL[dtype], "y")
+    check(y2, oracle.causal_conv(w.u64[:1], k32.astype(np.float64), None), TOL[dtype], "y_no_skip")
 
 
 # --------------------------------------------------------- S5: statepass ---
@@ -165,6 +222,18 @@ def _sp_inputs(w):
     return Ab32, Bb32, cplx64(Ab32), cplx64(Bb32), C
 
 
+def _sp_check(h3, w, y_tol, x_tol):
+    Ab32, Bb32, Ab, Bb, C = _sp_inputs(w)
+    x0 = f32dev(w.x0) if w.x0 is not None else None
+    y, xf = h3.statepass_conv(to_dev(w.u, w.dtype), f32dev(Ab32), f32dev(Bb32), f32dev(w.ssm.C), f32dev(w.D),
+                              w.chunk, x0=x0)
+    torch.cuda.synchronize()
+    ry, rx = oracle.recurrence(w.u64, Ab, Bb, C, w.D.astype(np.float64),
+                               x0=cplx64(w.x0) if w.x0 is not None else None)
+    check(y, ry, y_tol, "y")
+    check(cplx64(to_np64(xf)), rx, x_tol, "x_final")
+
+
 @pytest.mark.parametrize("dtype,L,chunk", [(workloads.F32, 1024, 128), (workloads.F32, 512, 512),
                                            (workloads.F16, 2048, 256), (workloads.BF16, 1024, 16),
                                            (workloads.F32, 256, 16), (workloads.F16, 4096, 1024),
@@ -172,15 +241,7 @@ def _sp_inputs(w):
 def test_statepass_small(h3, dtype, L, chunk):
     w = workloads.statepass_workload("t", 3, 5, L, chunk, dtype, seed=L + chunk, dt_lo=1e-3,
                                      dt_hi=1e-1, x0_scale=0.5)
-    Ab32, Bb32, Ab, Bb, C = _sp_inputs(w)
-    x0 = cplx64(w.x0)
-    y, xf = h3.statepass_conv(to_dev(w.u, dtype), f32dev(Ab32), f32dev(Bb32), f32dev(w.ssm.C),
-                              f32dev(w.D), chunk, x0=f32dev(w.x0))
-    torch.cuda.synchronize()
-    ry, rx = oracle.recurrence(w.u64, Ab, Bb, C, w.D.astype(np.float64), x0=x0)
-    assert rel_err(to_np64(y), ry) < TOL[dtype]
-    xg = cplx64(to_np64(xf))
-    assert np.abs(xg - rx).max() / np.abs(rx).max() < (1e-5 if dtype == workloads.F32 else 2e-2)
+    _sp_check(h3, w, TOL[dtype], 1e-5 if dtype == workloads.F32 else 2e-2)
 
 
 def test_statepass_resume(h3):
@@ -192,8 +253,23 @@ def test_statepass_resume(h3):
     y1, x1 = h3.statepass_conv(u[..., :512].contiguous(), *args, 128)
     y2, x2 = h3.statepass_conv(u[..., 512:].contiguous(), *args, 256, x0=x1)
     torch.cuda.synchronize()
-    assert rel_err(to_np64(torch.cat([y1, y2], -1)), to_np64(y)) < 1e-5
-    assert rel_err(to_np64(x2), to_np64(xf)) < 1e-5
+    check(to_np64(torch.cat([y1, y2], -1)), to_np64(y), 1e-5, "y")
+    check(cplx64(to_np64(x2)), cplx64(to_np64(xf)), 1e-5, "x_final")
+
+
+def test_config3_full_size(h3):
+    """B=2 H=1024 L=131072, chunk 8192, fp16: every row and every final state
+    against the float64 recurrence."""
+    _sp_check(h3, workloads.config(3), 2e-2, 2e-2)
+
+
+@pytest.mark.parametrize("dtype", [workloads.F16, workloads.BF16])
+def test_statepass_mfma_chunks(h3, dtype):
+    """Chunk 8192 (the paper's fused limit) runs the matrix-core conv per chunk
+    pair with the fused initial-state term."""
+    w = workloads.statepass_workload("t", 2, 3, 4 * 8192, 8192, dtype, seed=77, dt_lo=1e-4,
+                                     dt_hi=1e-2, x0_scale=0.3)
+    _sp_check(h3, w, TOL[dtype], 2e-2)
 
 
 # ------------------------------------ fused limit 16384 (32768-point) ---
@@ -201,7 +277,7 @@ def test_statepass_resume(h3):
 @pytest.mark.parametrize("B,H", [(1, 2), (3, 3)])
 def test_fftconv_l16384(h3, dtype, B, H):
     y, ref = _conv_case(h3, B, H, 16384, dtype, seed=B * 10 + H, dt_lo=1e-4)
-    assert rel_err(y, ref) < TOL[dtype]
+    check(y, ref, TOL[dtype])
 
 
 def test_fftconv_l16384_impulse(h3):
@@ -214,7 +290,7 @@ def test_fftconv_l16384_impulse(h3):
     y = h3.fftconv(to_dev(workloads.round_to(u, workloads.F16)[0], workloads.F16), f32dev(k), f32dev(D))
     torch.cuda.synchronize()
     ref = np.broadcast_to(k.astype(np.float64), (2, H, L)).copy(); ref[:, :, 0] += D
-    assert rel_err(to_np64(y), ref) < 2e-2
+    check(y, ref, 2e-2)
 
 
 @pytest.mark.parametrize("dtype,B,H,nchunk", [(workloads.F16, 2, 2, 2), (workloads.BF16, 2, 3, 3)])
@@ -223,14 +299,7 @@ def test_statepass_chunk16384(h3, dtype, B, H, nchunk):
     of the chunk-state kernel), the 32768-point conv per chunk."""
     w = workloads.statepass_workload("t", B, H, nchunk * 16384, 16384, dtype, seed=8 + H, dt_lo=1e-4,
                                      dt_hi=1e-2, x0_scale=0.5)
-    Ab32, Bb32, Ab, Bb, C = _sp_inputs(w)
-    y, xf = h3.statepass_conv(to_dev(w.u, w.dtype), f32dev(Ab32), f32dev(Bb32), f32dev(w.ssm.C), f32dev(w.D),
-                              16384, x0=f32dev(w.x0))
-    torch.cuda.synchronize()
-    ry, rx = oracle.recurrence(w.u64, Ab, Bb, C, w.D.astype(np.float64), x0=cplx64(w.x0))
-    assert rel_err(to_np64(y), ry) < TOL[dtype]
-    xg = cplx64(to_np64(xf))
-    assert np.abs(xg - rx).max() / np.abs(rx).max() < 2e-2
+    _sp_check(h3, w, TOL[dtype], 2e-2)
 
 
 def test_fftconv_bwd_du_l16384(h3):
@@ -246,7 +315,7 @@ def test_fftconv_bwd_du_l16384(h3):
                               want_dD=False)
     torch.cuda.synchronize()
     rdu, _, _ = oracle.causal_conv_bwd(w.u64, k32.astype(np.float64), w.D.astype(np.float64), dy64)
-    assert rel_err(to_np64(du), rdu) < 2e-2
+    check(du, rdu, 2e-2, "du")
 
 
 # ------------------------------------------------- conv backward pass ---
@@ -277,12 +346,12 @@ def _bwd_case(h3, B, H, L, dtype, seed, with_D=True, sel=None):
                                    (19, 3, 2048)])
 def test_fftconv_bwd(h3, dtype, B, H, L):
     (du, rdu), (dk, rdk), (dD, rdD) = _bwd_case(h3, B, H, L, dtype, seed=B * 7 + L)
-    assert rel_err(du, rdu) < TOL[dtype]
+    check(du, rdu, TOL[dtype], "du")
     # dk, dD: float32 outputs; on the matrix cores (16-bit I/O at L = 2048) the
     # transforms run on fp16 operands, so the 16-bit tolerance applies there
     tol_k = TOL[dtype] if (L == 2048 and dtype != workloads.F32) else 1e-5
-    assert rel_err(dk, rdk) < tol_k
-    assert rel_err(dD, rdD) < tol_k
+    check(dk, rdk, tol_k, "dk")
+    check(dD, rdD, tol_k, "dD", rows=False)
 
 
 @pytest.mark.parametrize("dtype", [workloads.F16, workloads.BF16])
@@ -291,15 +360,16 @@ def test_fftconv_bwd_valu_kernel_gradient_at_2048(h3, monkeypatch, dtype):
     runs by default (L = 2048, 16-bit I/O)."""
     monkeypatch.setenv("H3FLASH_WGRAD", "valu")
     (du, rdu), (dk, rdk), (dD, rdD) = _bwd_case(h3, 3, 4, 2048, dtype, seed=77)
-    assert rel_err(du, rdu) < TOL[dtype]
-    assert rel_err(dk, rdk) < 1e-5
-    assert rel_err(dD, rdD) < 1e-5
+    check(du, rdu, TOL[dtype], "du")
+    check(dk, rdk, 1e-5, "dk")
+    check(dD, rdD, 1e-5, "dD", rows=False)
 
 
 def test_fftconv_bwd_no_skip_and_partial_outputs(h3):
     B, H, L = 3, 4, 512
     (du, rdu), (dk, rdk), _ = _bwd_case(h3, B, H, L, workloads.F32, seed=41, with_D=False)
-    assert rel_err(du, rdu) < 1e-5 and rel_err(dk, rdk) < 1e-5
+    check(du, rdu, 1e-5, "du")
+    check(dk, rdk, 1e-5, "dk")
     w = workloads.conv_workload("t", B, H, L, workloads.F16, seed=42)
     k = f32dev(np.random.default_rng(1).standard_normal((H, L)) / 16)
     dy = to_dev(w.u, workloads.F16)
@@ -308,26 +378,24 @@ def test_fftconv_bwd_no_skip_and_partial_outputs(h3):
     torch.cuda.synchronize()
     assert dk0 is None and dD0 is None
     rdu, rdk, rdD = oracle.causal_conv_bwd(w.u64, to_np64(k), None, w.u64)
-    assert rel_err(to_np64(du_only), rdu) < 2e-2
-    assert rel_err(to_np64(dk_only), rdk) < 1e-5   # L = 512: float32 VALU kernel
-    assert rel_err(to_np64(dD_only), rdD) < 1e-5
+    check(du_only, rdu, 2e-2, "du_only")
+    check(dk_only, rdk, 1e-5, "dk_only")   # L = 512: float32 VALU kernel
+    check(dD_only, rdD, 1e-5, "dD_only", rows=False)
 
 
-def test_fftconv_bwd_config1_full_size_sampled_channels(h3):
+def test_fftconv_bwd_config1_full_size(h3):
     """At the H3-125M layer shape (B=8, H=768, L=2048, fp16) on the launch
-    the benchmark times; sampled channels against the oracle."""
-    sel = [0, 1, 383, 500, 767]
-    (du, rdu), (dk, rdk), (dD, rdD) = _bwd_case(h3, 8, 768, 2048, workloads.F16, seed=5, sel=sel)
-    assert rel_err(du, rdu) < 2e-2
-    assert rel_err(dk, rdk) < 2e-2
-    assert rel_err(dD, rdD) < 2e-2
+    the benchmark times; every channel against the oracle."""
+    (du, rdu), (dk, rdk), (dD, rdD) = _bwd_case(h3, 8, 768, 2048, workloads.F16, seed=5)
+    check(du, rdu, 2e-2, "du")
+    check(dk, rdk, 2e-2, "dk")
+    check(dD, rdD, 2e-2, "dD", rows=False)
 
 
 def test_fftconv_bwd_adjoint_at_full_size(h3):
     """<dy, conv(u)> = <du, u> at the fused-block limit (B=16 H=256 L=8192 bf16),
     with the forward and backward both on the GPU."""
     w = workloads.config(2)
-    A, Bm, C, dt = _diag_params(w)
     k = h3.ssm_kernel(f32dev(w.ssm.A), f32dev(w.ssm.B), f32dev(w.ssm.C), f32dev(w.ssm.dt), w.L)
     u = to_dev(w.u, w.dtype)
     dy = to_dev(workloads.round_to(np.random.default_rng(3).standard_normal(w.u.shape), w.dtype)[0], w.dtype)
@@ -366,9 +434,9 @@ def test_ssm_step(h3, dtype, B, H, m, T):
     y = h3.ssm_step(to_dev(u_s, dtype), f32dev(Ab32), f32dev(Bb32), f32dev(C32), f32dev(D), x)
     torch.cuda.synchronize()
     ry, rx = oracle.recurrence(u64, cplx64(Ab32), cplx64(Bb32), cplx64(C32), D.astype(np.float64), x0=cplx64(x0))
-    assert rel_err(to_np64(y), ry) < TOL[dtype]
-    xg = cplx64(to_np64(x))
-    assert np.abs(xg - rx).max() / np.abs(rx).max() < 1e-5
+    # a single token per row: the per-row metric would compare one value
+    check(y, ry, TOL[dtype], "y", rows=T > 1)
+    check(cplx64(to_np64(x)), rx, 1e-5, "x")
 
 
 def test_ssm_step_chained_tokens_and_no_skip(h3):
@@ -384,9 +452,9 @@ def test_ssm_step_chained_tokens_and_no_skip(h3):
     y_one = torch.cat([h3.ssm_step(u[..., t].contiguous(), *args, x2).unsqueeze(-1) for t in range(T)], -1)
     torch.cuda.synchronize()
     ry, rx = oracle.recurrence(u64, cplx64(Ab32), cplx64(Bb32), cplx64(C32), None, x0=cplx64(x0))
-    assert rel_err(to_np64(y_all), ry) < 1e-5
-    assert rel_err(to_np64(y_one), ry) < 1e-5
-    assert rel_err(to_np64(x1), to_np64(x2)) < 1e-6
+    check(y_all, ry, 1e-5, "y_all")
+    check(y_one, ry, 1e-5, "y_one")
+    check(cplx64(to_np64(x1)), cplx64(to_np64(x2)), 1e-6, "x")
 
 
 def test_ssm_step_continues_statepass(h3):
@@ -401,75 +469,54 @@ def test_ssm_step_continues_statepass(h3):
     y2 = h3.ssm_step(u[..., 2048:].contiguous(), *args, xf)
     torch.cuda.synchronize()
     ry, rx = oracle.recurrence(w.u64, Ab, Bb, C, w.D.astype(np.float64))
-    assert rel_err(to_np64(torch.cat([y1, y2], -1)), ry) < 2e-2
-    assert rel_err(to_np64(y2), ry[..., 2048:]) < 2e-2
-
-
-def test_config3_full_size_sampled_rows(h3):
-    w = workloads.config(3)
-    Ab32, Bb32, Ab, Bb, C = _sp_inputs(w)
-    y, xf = h3.statepass_conv(to_dev(w.u, w.dtype), f32dev(Ab32), f32dev(Bb32), f32dev(w.ssm.C),
-                              f32dev(w.D), w.chunk)
-    torch.cuda.synchronize()
-    rows = [0, 777, 1024 + 5, 2 * 1024 - 1]
-    y = y.view(w.B * w.H, w.L)
-    xf = xf.view(w.B * w.H, w.m, 2)
-    ys, rs, xs, rxs = [], [], [], []
-    for r in rows:
-        b, h = divmod(r, w.H)
-        ry, rx = oracle.recurrence(w.u64[b, h][None, None], Ab[h:h + 1], Bb[h:h + 1], C[h:h + 1],
-                                   w.D[h:h + 1].astype(np.float64))
-        ys.append(to_np64(y[r])); rs.append(ry[0, 0])
-        xs.append(cplx64(to_np64(xf[r]))); rxs.append(rx[0, 0])
-    assert rel_err(np.stack(ys), np.stack(rs)) < 2e-2
-    xs, rxs = np.stack(xs), np.stack(rxs)
-    assert np.abs(xs - rxs).max() / np.abs(rxs).max() < 2e-2
+    check(to_np64(torch.cat([y1, y2], -1)), ry, 2e-2, "y")
+    check(y2, ry[..., 2048:], 2e-2, "y_generated")
 
 
 # ------------------------------------------------------------- S6: layer ---
-def _layer_case(h3, w, b_sel=None):
-    d, L = w.d, w.L
-    A, B, C, dt = w.diag.complex64()
-    k64 = oracle.ssm_kernel(A, B, C, dt, L)
-    k32 = k64.astype(np.float32)
-    W = {n: to_dev(w.weight_out_in(n), w.dtype) for n in "qkvo"}
-    out = h3.layer_fwd(to_dev(w.x, w.dtype), W["q"], W["k"], W["v"], W["o"], f32dev(w.shift_C), None,
-                       f32dev(k32), f32dev(w.diag_D))
+def _layer_run(h3, w, k32, shift_D=None, diag_D=None, d_head=1):
+    W = {n: to_dev(w.W[n][0], w.dtype) for n in "qkvo"}
+    args = (to_dev(w.x, w.dtype), W["q"], W["k"], W["v"], W["o"], f32dev(w.shift_C),
+            f32dev(shift_D) if shift_D is not None else None, f32dev(k32),
+            f32dev(diag_D) if diag_D is not None else None)
+    out = h3.layer_fwd(*args) if d_head == 1 else h3.layer_fwd_heads(*args, d_head)
     torch.cuda.synchronize()
-    bs = list(range(w.B)) if b_sel is None else b_sel
-    ref = oracle.h3_layer(w.x64[bs], w.W["q"][1], w.W["k"][1], w.W["v"][1], w.W["o"][1],
+    ref = oracle.h3_layer(w.x64, w.W["q"][1], w.W["k"][1], w.W["v"][1], w.W["o"][1],
                           w.shift_C.astype(np.float64), k32.astype(np.float64),
-                          w.diag_D.astype(np.float64))
-    return to_np64(out[bs]), ref
+                          diag_D.astype(np.float64) if diag_D is not None else None,
+                          shift_D=shift_D.astype(np.float64) if shift_D is not None else None, d_head=d_head)
+    return out, ref
+
+
+def _layer_case(h3, w):
+    A, B, C, dt = w.diag.complex64()
+    k32 = oracle.ssm_kernel(A, B, C, dt, w.L).astype(np.float32)
+    return _layer_run(h3, w, k32, diag_D=w.diag_D)
 
 
 @pytest.mark.parametrize("dtype", [workloads.BF16, workloads.F16])
 def test_layer_small(h3, dtype):
     w = workloads.layer_workload("t", 2, 256, 256, dtype, seed=21)
     y, ref = _layer_case(h3, w)
-    assert rel_err(y, ref) < 2e-2
+    check(y, ref, 2e-2)
 
 
 # L = 2048 and 8192 take the matrix-core shift SSM, the wave FFT conv and the
 # gated transpose; an odd batch leaves the last row pair half empty, fewer than
 # 64 shift taps leave zeros in the Toeplitz band, and a shift D adds to its
-# diagonal.
+# diagonal.  L = 4096 takes the fused VALU middle kernel, L = 16384 the
+# 32768-point conv.
 @pytest.mark.parametrize("dtype", [workloads.BF16, workloads.F16])
-@pytest.mark.parametrize("B,L,m_s,with_D", [(3, 2048, 17, True), (1, 8192, 64, False), (2, 2048, 64, True)])
+@pytest.mark.parametrize("B,L,m_s,with_D", [(3, 2048, 17, True), (1, 8192, 64, False), (2, 2048, 64, True),
+                                            (1, 4096, 64, True), (1, 16384, 33, True)])
 def test_layer_wave_path(h3, dtype, B, L, m_s, with_D):
     w = workloads.layer_workload("t", B, L, 128, dtype, seed=31 + B + m_s, m_shift=m_s)
     rng = np.random.default_rng(77)
     sD = rng.standard_normal(w.d).astype(np.float32) if with_D else None
     A, Bm, C, dt = w.diag.complex64()
     k32 = oracle.ssm_kernel(A, Bm, C, dt, L).astype(np.float32)
-    W = {n: to_dev(w.weight_out_in(n), w.dtype) for n in "qkvo"}
-    out = h3.layer_fwd(to_dev(w.x, w.dtype), W["q"], W["k"], W["v"], W["o"], f32dev(w.shift_C),
-                       f32dev(sD) if with_D else None, f32dev(k32), f32dev(w.diag_D))
-    torch.cuda.synchronize()
-    ref = oracle.h3_layer(w.x64, w.W["q"][1], w.W["k"][1], w.W["v"][1], w.W["o"][1],
-                          w.shift_C.astype(np.float64), k32.astype(np.float64), w.diag_D.astype(np.float64),
-                          shift_D=sD.astype(np.float64) if with_D else None)
-    assert rel_err(to_np64(out), ref) < 2e-2
+    y, ref = _layer_run(h3, w, k32, shift_D=sD, diag_D=w.diag_D)
+    check(y, ref, 2e-2)
 
 
 # The library's own matrix-core GEMM (used where hipBLASLt rejects a shape),
@@ -479,14 +526,15 @@ def test_layer_native_gemm(h3, monkeypatch, L):
     monkeypatch.setenv("H3FLASH_GEMM", "native")
     w = workloads.layer_workload("t", 2, L, 256, workloads.BF16, seed=23 + L)
     y, ref = _layer_case(h3, w)
-    assert rel_err(y, ref) < 2e-2
+    check(y, ref, 2e-2)
 
 
 # Heads of dimension d_h > 1: d_h^2 diagonal-SSM channels per head, each
 # with its own kernel; L = 2048 and 8192 take the wave conv for them, L = 256
-# the VALU one; with and without the skip terms.
+# the VALU one, L = 16384 the 32768-point conv; with and without the skip terms.
 @pytest.mark.parametrize("dtype", [workloads.BF16, workloads.F16])
-@pytest.mark.parametrize("B,L,dh,with_D", [(2, 2048, 2, True), (3, 256, 4, False), (1, 8192, 8, True)])
+@pytest.mark.parametrize("B,L,dh,with_D", [(2, 2048, 2, True), (3, 256, 4, False), (1, 8192, 8, True),
+                                           (1, 16384, 8, True)])
 def test_layer_heads(h3, dtype, B, L, dh, with_D):
     d = 128
     w = workloads.layer_workload("t", B, L, d, dtype, seed=61 + dh + L, m_shift=64)
@@ -496,21 +544,15 @@ def test_layer_heads(h3, dtype, B, L, dh, with_D):
     k32 = oracle.ssm_kernel(A, Bm, C, dt, L).astype(np.float32)
     dD = rng.standard_normal(d * dh).astype(np.float32) if with_D else None
     sD = rng.standard_normal(d).astype(np.float32) if with_D else None
-    W = {n: to_dev(w.weight_out_in(n), w.dtype) for n in "qkvo"}
-    out = h3.layer_fwd_heads(to_dev(w.x, w.dtype), W["q"], W["k"], W["v"], W["o"], f32dev(w.shift_C),
-                             f32dev(sD) if with_D else None, f32dev(k32), f32dev(dD) if with_D else None, dh)
-    torch.cuda.synchronize()
-    ref = oracle.h3_layer(w.x64, w.W["q"][1], w.W["k"][1], w.W["v"][1], w.W["o"][1],
-                          w.shift_C.astype(np.float64), k32.astype(np.float64),
-                          dD.astype(np.float64) if with_D else None,
-                          shift_D=sD.astype(np.float64) if with_D else None, d_head=dh)
-    assert rel_err(to_np64(out), ref) < 2e-2
+    y, ref = _layer_run(h3, w, k32, shift_D=sD, diag_D=dD, d_head=dh)
+    check(y, ref, 2e-2)
 
 
-def test_layer_config4_one_batch_element(h3):
+def test_layer_config4_full_size(h3):
+    """d=2560 B=4 L=2048 bf16 (the 2.7B layer shape): every batch element."""
     w = workloads.config(4)
-    y, ref = _layer_case(h3, w, b_sel=[3])
-    assert rel_err(y, ref) < 2e-2
+    y, ref = _layer_case(h3, w)
+    check(y, ref, 2e-2)
 
 
 # ------------------------------------------- matrix-core conv (L = 2048) ---
@@ -518,11 +560,12 @@ def test_layer_config4_one_batch_element(h3):
 @pytest.mark.parametrize("B,H", [(1, 3), (5, 2), (16, 4), (8, 33)])
 def test_fftconv_mfma_shapes(h3, dtype, B, H):
     y, ref = _conv_case(h3, B, H, 2048, dtype, seed=B * 100 + H, dt_lo=1e-4)
-    assert rel_err(y, ref) < TOL[dtype]
+    check(y, ref, TOL[dtype])
 
 
 @pytest.mark.parametrize("L", [2048, 8192])
-@pytest.mark.parametrize("scale_u,scale_k", [(1e3, 1.0), (1e-3, 1.0), (1.0, 1e-5), (30.0, 10.0), (2e4, 1.0)])
+@pytest.mark.parametrize("scale_u,scale_k", [(1e3, 1.0), (1e-3, 1.0), (1.0, 1e-5), (30.0, 10.0), (2e4, 1.0),
+                                             (1e-5, 1.0)])
 def test_fftconv_mfma_dynamic_range(h3, scale_u, scale_k, L):
     """Inputs far from unit scale: the block FFT rescales by powers of two."""
     rng = np.random.default_rng(5)
@@ -541,7 +584,12 @@ def test_fftconv_mfma_dynamic_range(h3, scale_u, scale_k, L):
             s, u64 = workloads.round_to(uu, dt)
             ref = oracle.causal_conv(u64, k.astype(np.float64), D.astype(np.float64))
         y = to_np64(h3.fftconv(to_dev(s, dt), f32dev(k), f32dev(D)))
-        assert rel_err(y, ref) < TOL[dt], (dt, rel_err(y, ref))
+        # fp16 outputs below 2^-14 are subnormal: their spacing (2^-24) bounds
+        # the absolute error, so the relative gate applies above that scale
+        if dt == workloads.F16 and np.abs(ref).max() < 2.0 ** -6:
+            assert np.abs(y - ref).max() < 2.0 ** -18, (dt, np.abs(y - ref).max())
+        else:
+            check(y, ref, TOL[dt], dt)
 
 
 @pytest.mark.parametrize("L", [2048, 8192])
@@ -555,9 +603,8 @@ def test_fftconv_mfma_zero_and_impulse(h3, L):
     u[0, :, 0] = 1.0
     u[1, :, 100] = 1.0
     y = to_np64(h3.fftconv(to_dev(u, workloads.F16), f32dev(k), None))
-    kr = k.astype(np.float16).astype(np.float64)
-    assert rel_err(y[0], k) < 2e-2
-    assert rel_err(y[1, :, 100:], k[:, :L - 100]) < 2e-2
+    check(y[0], k, 2e-2, "impulse_at_0")
+    check(y[1, :, 100:], k[:, :L - 100], 2e-2, "impulse_at_100")
     assert np.abs(y[1, :, :100]).max() < 1e-3 * np.abs(k).max()
 
 
@@ -566,19 +613,39 @@ def test_fftconv_mfma_zero_and_impulse(h3, L):
 @pytest.mark.parametrize("B,H", [(1, 2), (3, 3), (16, 2)])
 def test_fftconv_mfma16k_shapes(h3, dtype, B, H):
     y, ref = _conv_case(h3, B, H, 8192, dtype, seed=B * 10 + H + 7, dt_lo=1e-4)
-    assert rel_err(y, ref) < TOL[dtype]
+    check(y, ref, TOL[dtype])
 
 
-@pytest.mark.parametrize("dtype", [workloads.F16, workloads.BF16])
-def test_statepass_mfma_chunks(h3, dtype):
-    """Chunk 8192 (the fused limit) runs the matrix-core conv per chunk pair."""
-    w = workloads.statepass_workload("t", 2, 3, 4 * 8192, 8192, dtype, seed=77, dt_lo=1e-4,
-                                     dt_hi=1e-2, x0_scale=0.3)
-    Ab32, Bb32, Ab, Bb, C = _sp_inputs(w)
-    y, xf = h3.statepass_conv(to_dev(w.u, dtype), f32dev(Ab32), f32dev(Bb32), f32dev(w.ssm.C),
-                              f32dev(w.D), w.chunk, x0=f32dev(w.x0))
-    torch.cuda.synchronize()
-    ry, rx = oracle.recurrence(w.u64, Ab, Bb, C, w.D.astype(np.float64), x0=cplx64(w.x0))
-    assert rel_err(to_np64(y), ry) < TOL[dtype]
-    xg = cplx64(to_np64(xf))
-    assert np.abs(xg - rx).max() / np.abs(rx).max() < 2e-2
+# --------------------------------------------- binding argument checks ---
+# The C ABI sees bare pointers; the binding rejects tensors of the wrong
+# device, shape, dtype or layout before anything is launched.
+def test_binding_rejects_mismatched_tensors(h3):
+    dev = torch.device("cuda")
+    u = torch.zeros((2, 3, 64), dtype=torch.float16, device=dev)
+    k = torch.zeros((3, 64), dtype=torch.float32, device=dev)
+    D = torch.zeros(3, dtype=torch.float32, device=dev)
+    with pytest.raises(ValueError):
+        h3.fftconv(u, k[:2], D)                                  # k too short
+    with pytest.raises(ValueError):
+        h3.fftconv(u, k, D[:2])                                  # D too short
+    with pytest.raises(ValueError):
+        h3.fftconv(u, k.cpu(), D)                                # host tensor
+    with pytest.raises(ValueError):
+        h3.fftconv(u, k, D, out=torch.empty((2, 3, 64), dtype=torch.bfloat16, device=dev))   # out dtype
+    with pytest.raises(ValueError):
+        h3.fftconv(u, k, D, out=torch.empty((2, 3, 32), dtype=torch.float16, device=dev))    # out shape
+    with pytest.raises(ValueError):
+        h3.fftconv(u, k, D, out=torch.empty((2, 64, 3), dtype=torch.float16, device=dev).transpose(1, 2))
+    P = torch.zeros((3, 8, 2), dtype=torch.float32, device=dev)
+    with pytest.raises(ValueError):
+        h3.statepass_conv(u, P, P[:2], P, D, 16)                 # Bbar too short
+    with pytest.raises(ValueError):
+        h3.statepass_conv(u, P, P, P, D, 16, x0=torch.zeros((2, 3, 4, 2), device=dev))   # x0 modes
+    x = torch.zeros((2, 3, 8, 2), dtype=torch.float32, device=dev)
+    with pytest.raises(ValueError):
+        h3.ssm_step(u[..., 0], P, P, P.cpu(), D, x)              # host C
+    # the step result of a non-contiguous u comes back with u's shape, computed
+    # from the contiguous copy
+    ut = torch.randn((3, 2), dtype=torch.float32, device=dev).t()
+    y = h3.ssm_step(ut, P, P, P, D, x)
+    assert y.shape == ut.shape and y.is_contiguous()

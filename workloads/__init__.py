@@ -162,10 +162,6 @@ class LayerWorkload:
     diag: DiagSSM          # diagonal SSM (d channels)
     diag_D: np.ndarray     # (d,) float32
 
-    def weight_out_in(self, key: str) -> np.ndarray:
-        """W[key] in (out, in) storage, the layout the layer entry point takes."""
-        return np.ascontiguousarray(self.W[key][0].T)
-
 
 def conv_workload(name: str, B: int, H: int, L: int, dtype: str, seed: int,
                   m: int = 64, dt_lo: float = 1e-3, dt_hi: float = 1e-1,
