@@ -146,6 +146,27 @@ int h3_statepass_conv(const void *u, const float *Abar, const float *Bbar,
                       void *workspace, size_t ws_bytes, void *stream);
 
 /*
+ * h3_statepass_conv_noalloc — h3_statepass_conv without a workspace argument,
+ * for callers that cannot allocate device memory (code under graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc).  Arguments, result
+ * and errors as for h3_statepass_conv; it calls no allocating routine.  The
+ * scratch lives in a static device array of H3_NOALLOC_SCRATCH_BYTES per GPU,
+ * held from the library's first use on that GPU until the process ends;
+ * `stream` must belong to the current device.  Calls on one GPU share that
+ * array: calls that overlap in time on one GPU race (serialise them, e.g. on
+ * one stream).  Every scratch region is written before it is read, so the
+ * previous call's contents do not matter.
+ * Errors: as h3_statepass_conv; EWORKSPACE when the scratch this call needs
+ * (h3_workspace_size(H3_OP_STATEPASS, ...)) exceeds H3_NOALLOC_SCRATCH_BYTES;
+ * EDEVICE if the array's device address cannot be looked up.
+ */
+#define H3_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+int h3_statepass_conv_noalloc(const void *u, const float *Abar, const float *Bbar,
+                              const float *C, const float *D, const float *x0,
+                              int B, int H, int L, int m, int chunk, int dtype,
+                              void *y, float *x_final, void *stream);
+
+/*
  * h3_fftconv_bwd — backward pass of the fused convolution (the appendix on
  * FlashConv's backward pass): for y = h3_fftconv(u, k, D) and an output
  * gradient dy,

@@ -19,7 +19,7 @@ import torch
 
 __all__ = [
     "H3Error", "lib", "ssm_discretize", "ssm_kernel", "fftconv", "statepass_conv",
-    "layer_fwd", "layer_fwd_heads", "ssm_step", "fftconv_bwd", "kernel_spectrum", "fftconv_spectral", "workspace_size", "status_string", "F32", "F16", "BF16",
+    "statepass_conv_noalloc", "layer_fwd", "layer_fwd_heads", "ssm_step", "fftconv_bwd", "kernel_spectrum", "fftconv_spectral", "workspace_size", "status_string", "F32", "F16", "BF16",
     "OP_FFTCONV", "OP_STATEPASS", "OP_LAYER", "OP_FFTCONV_BWD", "OP_LAYER_HEADS", "FUSED_LIMIT", "FUSED_LIMIT_F32", "MAX_MODES",
 ]
 
@@ -59,6 +59,7 @@ def lib() -> ctypes.CDLL:
         L.h3_kernel_spectrum.argtypes = [vp, i, i, vp, vp]
         L.h3_fftconv_spectral.argtypes = [vp, vp, vp, vp, i, i, i, i, vp]
         L.h3_statepass_conv.argtypes = [vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, vp, vp, vp, sz, vp]
+        L.h3_statepass_conv_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, vp, vp, vp]
         L.h3_layer_fwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, vp, vp, sz, vp]
         L.h3_ssm_step.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, vp, vp, vp]
         L.h3_fftconv_bwd.argtypes = [vp, vp, vp, vp, i, i, i, i, vp, vp, vp, vp, sz, vp]
@@ -67,7 +68,7 @@ def lib() -> ctypes.CDLL:
         L.h3_workspace_size.restype = sz
         L.h3_status_string.argtypes = [i]
         L.h3_status_string.restype = ctypes.c_char_p
-        for fn in ("h3_ssm_discretize", "h3_ssm_kernel", "h3_fftconv", "h3_statepass_conv",
+        for fn in ("h3_ssm_discretize", "h3_ssm_kernel", "h3_fftconv", "h3_statepass_conv", "h3_statepass_conv_noalloc",
                    "h3_layer_fwd", "h3_kernel_spectrum", "h3_fftconv_spectral", "h3_ssm_step", "h3_fftconv_bwd",
                    "h3_layer_fwd_heads"):
             getattr(L, fn).restype = ctypes.c_int
@@ -290,6 +291,35 @@ def statepass_conv(u: torch.Tensor, Abar: torch.Tensor, Bbar: torch.Tensor, C: t
     _check("h3_statepass_conv", lib().h3_statepass_conv(
         _ptr(u), _ptr(Abar), _ptr(Bbar), _ptr(C), _ptr(D), _ptr(x0), Bn, H, L, m, chunk, dt,
         _ptr(y), _ptr(xf), _ptr(ws), ws.numel() * ws.element_size(), _stream(u.device)))
+    return y, xf
+
+
+def statepass_conv_noalloc(u: torch.Tensor, Abar: torch.Tensor, Bbar: torch.Tensor, C: torch.Tensor,
+                           D: Optional[torch.Tensor], chunk: int, x0: Optional[torch.Tensor] = None,
+                           out: Optional[torch.Tensor] = None,
+                           x_final: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """statepass_conv through h3_statepass_conv_noalloc: the library's static
+    scratch instead of a workspace (the library allocates nothing; the outputs
+    are allocated here unless given)."""
+    dev = _gpu("u", u)
+    u = u.contiguous()
+    if u.dim() != 3:
+        raise ValueError("u must be (B, H, L)")
+    Bn, H, L = u.shape
+    Abar, Bbar, C, D = _cplx(Abar), _cplx(Bbar), _cplx(C), _f32(D)
+    m = Abar.shape[1]
+    x0 = _cplx(x0) if x0 is not None else None
+    _on(dev, Abar=Abar, Bbar=Bbar, C=C, D=D, x0=x0)
+    for n, t in (("Abar", Abar), ("Bbar", Bbar), ("C", C)):
+        _shape(n, t, (H, m, 2))
+    _shape("D", D, (H,)); _shape("x0", x0, (Bn, H, m, 2))
+    _out("out", out, u.shape, u.dtype, dev)
+    _out("x_final", x_final, (Bn, H, m, 2), torch.float32, dev)
+    y = out if out is not None else torch.empty_like(u)
+    xf = x_final if x_final is not None else torch.empty((Bn, H, m, 2), dtype=torch.float32, device=u.device)
+    _check("h3_statepass_conv_noalloc", lib().h3_statepass_conv_noalloc(
+        _ptr(u), _ptr(Abar), _ptr(Bbar), _ptr(C), _ptr(D), _ptr(x0), Bn, H, L, m, chunk, _dtype(u),
+        _ptr(y), _ptr(xf), _stream(u.device)))
     return y, xf
 
 

@@ -216,3 +216,22 @@ def test_binding_rejects_host_tensors():
     W = torch.zeros((128, 128), dtype=torch.bfloat16)
     with pytest.raises(ValueError):
         h3.layer_fwd(x, W, W, W, W, torch.zeros((128, 4)), None, torch.zeros((128, 128)), None)
+
+
+def test_statepass_noalloc_validation():
+    """The no-allocation variant validates like h3_statepass_conv and rejects
+    a call whose scratch would exceed its static array, before touching the
+    GPU."""
+    L = h3.lib()
+
+    def call(u=U, A=K, B=2, H=4, Ln=256, m=64, chunk=64, dt=1, y=Y, xf=None):
+        return L.h3_statepass_conv_noalloc(P(u), P(A), P(K + 4096), P(K + 8192), None, None, B, H, Ln, m, chunk,
+                                           dt, P(y), P(xf), None)
+
+    assert call(u=0) == EINVAL
+    assert call(Ln=250) == EINVAL
+    assert call(m=65) == EUNSUP
+    assert call(y=U) == EINVAL
+    # float32, chunk 1024 at B=2 H=1024 L=131072: a 1 GiB correction term
+    assert h3.workspace_size(h3.OP_STATEPASS, 2, 1024, 131072, 64, 1024, h3.F32) > (128 << 20)
+    assert call(u=1 << 40, y=2 << 40, B=2, H=1024, Ln=131072, chunk=1024, dt=0) == EWS
