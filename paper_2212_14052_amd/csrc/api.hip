@@ -330,6 +330,7 @@ int h3_fftconv(const void *u, const float *k, const float *D, void *y, int B, in
     a.corr = nullptr;
     a.corr16 = 0;
     if (fftconv_mfma_supported(L, dtype)) return launched(launch_fftconv_mfma(a, k, s));
+    if (fftconv_kgen_supported(L)) return launched(launch_fftconv_kgen(a, k, s));
     float2 *Kspec = (float2 *)workspace;
     hipError_t e = launch_spectrum(k, H, L, Kspec, s);
     if (e != hipSuccess) return H3_EDEVICE;
@@ -372,6 +373,8 @@ int h3_fftconv_bwd(const void *u, const float *k, const float *D, const void *dy
         a.conj_k = 1;
         if (fftconv_mfma_supported(L, dtype)) {   // the wave kernels (2048, 8192) or the 32768-point one
             e = launch_fftconv_mfma(a, k, s);
+        } else if (fftconv_kgen_supported(L)) {
+            e = launch_fftconv_kgen(a, k, s);
         } else {
             float2 *Kspec = (float2 *)workspace;
             e = launch_spectrum(k, H, L, Kspec, s);

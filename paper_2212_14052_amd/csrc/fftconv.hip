@@ -12,6 +12,11 @@
 // pass (only outputs t < L are formed).  The skip term D u reuses the u
 // values the first pass loaded: the last pass of the second transform leaves
 // exactly those positions in the same thread.
+//
+// fftconv_kgen_kernel is the same convolution with the kernel spectrum formed
+// in the kernel itself, one spectrum shared by a group of row pairs.
+#include <atomic>
+
 #include "common.h"
 #include "fft_valu.h"
 #include "internal.h"
@@ -189,6 +194,117 @@ __global__ __launch_bounds__(N / 16 >= 64 ? N / 16 : 64) void fftconv_kernel(Con
     }
 }
 
+// ------------------------------------------- conv with its own spectrum ----
+// The same convolution for plain (B, H, L) rows, with the kernel spectrum
+// computed in the kernel instead of read from a workspace: work item =
+// (channel h, group of up to `ppg` row pairs of h).  The item's signal slot
+// first transforms k_h + D delta (the skip term folded into the kernel: the
+// circular convolution of the zero-padded row with k + D delta equals the
+// causal convolution plus D u on t < L) and keeps F(.)/N in registers, in the
+// layout the pointwise product reads; then it runs its row pairs.  One launch
+// instead of two, and no spectrum round trip through HBM.
+template <int N, int DT>
+__global__ __launch_bounds__(N / 16 >= 64 ? N / 16 : 64) void fftconv_kgen_kernel(ConvArgs a, const float *k,
+                                                                                 int groups, int ppg) {
+    using P = FFTPlan<N>;
+    using io = IO<DT>;
+    typedef typename io::T T_;
+    constexpr int T = P::T, R1 = P::R1, Q = 16 / R1, HALF = R1 / 2;
+    constexpr int S = (T >= 64) ? 1 : 64 / T;
+    constexpr int L = N / 2;
+    extern __shared__ float2 lds[];
+    __shared__ uint32_t rmx[2 * S];   // per signal slot: max |row a|, max |row b| (float bits)
+    const int sig = threadIdx.x / T, tid = threadIdx.x % T;
+    float2 *X = lds + sig * P::LDS;
+    const int item = xcd_logical_block(blockIdx.x, gridDim.x) * S + sig;
+    const bool act = item < a.H * groups;
+    const int h = act ? item / groups : 0, grp = act ? item % groups : 0;
+    const int npairs = (a.B + 1) / 2;
+    const T_ *u = (const T_ *)a.u;
+    T_ *y = (T_ *)a.y;
+
+    // spectrum of k_h + D delta, scaled by 1/N (conjugated for the correlation)
+    float2 kf[16];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        const int j = tid + q * T;
+#pragma unroll
+        for (int r = 0; r < R1; ++r) {
+            float kr = 0.f;
+            if (r < HALF && act) kr = k[(long)h * L + j + r * (N / R1)];
+            kf[q * R1 + r] = make_float2(kr, 0.f);
+        }
+    }
+    if (act && tid == 0 && a.D) kf[0].x += a.D[h];   // point 0: q = 0, r = 0, j = 0
+    fft_forward_from_regs<N>(X, tid, kf);
+    {
+        const float inv = 1.0f / (float)N, sg = a.conj_k ? -inv : inv;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) kf[r] = make_float2(kf[r].x * inv, kf[r].y * sg);
+    }
+
+    for (int i = 0; i < ppg; ++i) {
+        // an opaque copy of the thread index per pair: the passes' twiddles
+        // are evaluated where they are used instead of being hoisted out of
+        // the loop (where they would all stay live)
+        int tv = tid;
+        asm volatile("" : "+v"(tv));
+        const int pr = grp * ppg + i;
+        const bool va = act && pr < npairs, vb = va && 2 * pr + 1 < a.B;
+        const long oa = ((long)(2 * pr) * a.H + h) * L, ob = oa + (long)a.H * L;
+        float2 v[16];
+        float ma = 0.f, mb = 0.f;
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+            const int j = tid + q * T;
+#pragma unroll
+            for (int r = 0; r < R1; ++r) {
+                float xa = 0.f, xb = 0.f;
+                if (r < HALF) {
+                    const int n = j + r * (N / R1);
+                    if (va) xa = io::ld(u, oa + n);
+                    if (vb) xb = io::ld(u, ob + n);
+                }
+                ma = fmaxf(ma, fabsf(xa));
+                mb = fmaxf(mb, fabsf(xb));
+                v[q * R1 + r] = make_float2(xa, xb);
+            }
+        }
+        // each row of the pair gets its own power-of-two scale
+        __syncthreads();   // LDS: the previous transform's reads and the previous rmx reads are done
+        if (tid == 0) {
+            rmx[2 * sig] = 0u;
+            rmx[2 * sig + 1] = 0u;
+        }
+        __syncthreads();
+        atomicMax(&rmx[2 * sig], __float_as_uint(ma));
+        atomicMax(&rmx[2 * sig + 1], __float_as_uint(mb));
+        __syncthreads();
+        const int ea = pow2_exp(__uint_as_float(rmx[2 * sig])), eb = pow2_exp(__uint_as_float(rmx[2 * sig + 1]));
+        {
+            const float sa = ldexpf(1.0f, -ea), sb = ldexpf(1.0f, -eb);
+#pragma unroll
+            for (int r = 0; r < 16; ++r) v[r] = make_float2(v[r].x * sa, v[r].y * sb);
+        }
+        fft_forward_from_regs<N>(X, tv, v);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) v[r] = cconj(cmul(v[r], kf[r]));
+        fft_second_from_regs<N>(X, tv, v);
+        const float ya_s = ldexpf(1.0f, ea), yb_s = -ldexpf(1.0f, eb);
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+            const int j = tid + q * T;
+#pragma unroll
+            for (int r = 0; r < HALF; ++r) {
+                const int n = j + r * (N / R1);
+                const float2 w = v[q * R1 + r];
+                if (va) io::st(y, oa + n, w.x * ya_s);
+                if (vb) io::st(y, ob + n, w.y * yb_s);
+            }
+        }
+    }
+}
+
 // --------------------------------------------------------------- launch ----
 template <int N>
 static hipError_t launch_spectrum_n(const float *k, int H, float2 *Kspec, hipStream_t s) {
@@ -258,6 +374,84 @@ hipError_t launch_fftconv(const ConvArgs &a, hipStream_t s) {
         case 2048: return launch_conv_dt<4096>(a, s);
         case 4096: return launch_conv_dt<8192>(a, s);
         case 8192: return launch_conv_dt<16384>(a, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+// Pairs per spectrum for the kgen kernel.  An item costs 2 ppg + 1
+// transforms, run one after another; the items run in ceil(items / resident)
+// rounds, `resident` being the items the whole device holds at once.  Take
+// the ppg in 1..npairs that minimises rounds x (2 ppg + 1), the larger one on
+// a tie (fewer transforms in all).  Small launches thus keep one spectrum per
+// pair for parallelism; large ones share a spectrum among up to npairs pairs.
+static int kgen_pairs_per_group(int H, int npairs, int S, long resident_blocks) {
+    long best_cost = -1;
+    int best = 1;
+    for (int ppg = 1; ppg <= npairs; ppg = (ppg < npairs && 2 * ppg > npairs) ? npairs : 2 * ppg) {
+        const long items = (long)H * ((npairs + ppg - 1) / ppg);
+        const long blocks = (items + S - 1) / S;
+        const long rounds = (blocks + resident_blocks - 1) / resident_blocks;
+        const long cost = rounds * (2 * ppg + 1);
+        if (best_cost < 0 || cost <= best_cost) {
+            best_cost = cost;
+            best = ppg;
+        }
+        if (ppg == npairs) break;
+    }
+    return best;
+}
+
+template <int N, int DT>
+static hipError_t launch_kgen_n(const ConvArgs &a, const float *k, hipStream_t s) {
+    using P = FFTPlan<N>;
+    constexpr int T = P::T, S = (T >= 64) ? 1 : 64 / T;
+    const size_t lds = (size_t)S * P::LDS * sizeof(float2);
+    auto fn = fftconv_kgen_kernel<N, DT>;
+    if (lds > 65536) (void)hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    // resident blocks per CU (fixed per instantiation) times the CUs of the current device
+    static std::atomic<int> per_cu{0};
+    if (per_cu.load(std::memory_order_relaxed) == 0) {
+        int n = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, (const void *)fn, S * T, lds) != hipSuccess || n < 1) n = 1;
+        per_cu.store(n, std::memory_order_relaxed);
+    }
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+        cus = 1;
+    const int npairs = (a.B + 1) / 2;
+    const int ppg = kgen_pairs_per_group(a.H, npairs, S, (long)per_cu.load(std::memory_order_relaxed) * cus);
+    const int groups = (npairs + ppg - 1) / ppg;
+    const long items = (long)a.H * groups;
+    dim3 grid((unsigned)((items + S - 1) / S)), block(S * T);
+    hipLaunchKernelGGL(fn, grid, block, lds, s, a, k, groups, ppg);
+    return hipGetLastError();
+}
+
+template <int N>
+static hipError_t launch_kgen_dt(const ConvArgs &a, const float *k, hipStream_t s) {
+    switch (a.dtype) {
+        case F32: return launch_kgen_n<N, F32>(a, k, s);
+        case F16: return launch_kgen_n<N, F16>(a, k, s);
+        case BF16: return launch_kgen_n<N, BF16>(a, k, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+bool fftconv_kgen_supported(int L) { return L >= 16 && L <= 4096 && (L & (L - 1)) == 0; }
+
+hipError_t launch_fftconv_kgen(const ConvArgs &a, const float *k, hipStream_t s) {
+    if (a.pair_mode != 0 || a.corr) return hipErrorInvalidValue;
+    switch (a.L) {
+        case 16: return launch_kgen_dt<32>(a, k, s);
+        case 32: return launch_kgen_dt<64>(a, k, s);
+        case 64: return launch_kgen_dt<128>(a, k, s);
+        case 128: return launch_kgen_dt<256>(a, k, s);
+        case 256: return launch_kgen_dt<512>(a, k, s);
+        case 512: return launch_kgen_dt<1024>(a, k, s);
+        case 1024: return launch_kgen_dt<2048>(a, k, s);
+        case 2048: return launch_kgen_dt<4096>(a, k, s);
+        case 4096: return launch_kgen_dt<8192>(a, k, s);
     }
     return hipErrorInvalidValue;
 }

@@ -53,6 +53,11 @@ struct ConvArgs {
     int conj_k;
 };
 hipError_t launch_fftconv(const ConvArgs &a, hipStream_t s);
+// The VALU convolution of plain (B, H, L) rows (pair_mode 0, no correction
+// term) with each channel's spectrum computed in the kernel from k (skip term
+// folded into k[0]); L a power of two in [16, 4096].
+bool fftconv_kgen_supported(int L);
+hipError_t launch_fftconv_kgen(const ConvArgs &a, const float *k, hipStream_t s);
 // Matrix-core block-FFT variant (16-bit I/O, L = 2048): computes the kernel
 // spectrum from k itself; returns hipErrorInvalidValue for other shapes.
 hipError_t launch_fftconv_mfma(const ConvArgs &a, const float *k, hipStream_t s);

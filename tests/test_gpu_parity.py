@@ -143,6 +143,18 @@ def test_fftconv_pair_with_unequal_rows(h3, dtype, L, small):
     check(y, ref, TOL[dtype])
 
 
+# The VALU convolution forms the kernel spectrum itself and shares it among a
+# group of row pairs of one channel; the group size follows the launch's
+# parallelism.  These shapes give one pair per group, whole groups of several
+# pairs and a last group with missing pairs, with odd B (a half pair).
+@pytest.mark.parametrize("B,H,L,dtype", [(64, 64, 256, workloads.F32), (9, 2048, 1024, workloads.F32),
+                                         (32, 512, 512, workloads.F32), (12, 512, 4096, workloads.F16),
+                                         (11, 1024, 512, workloads.BF16), (5, 4096, 1024, workloads.F32)])
+def test_fftconv_shared_spectrum_groups(h3, B, H, L, dtype):
+    y, ref = _conv_case(h3, B, H, L, dtype, seed=B * H + L, dt_lo=1e-4)
+    check(y, ref, TOL[dtype])
+
+
 def _end_to_end_conv(h3, w, k_tol, y_tol):
     """S1 -> S2/S3 on the GPU at full size, against the oracle on every row."""
     k = h3.ssm_kernel(f32dev(w.ssm.A), f32dev(w.ssm.B), f32dev(w.ssm.C), f32dev(w.ssm.dt), w.L)
