@@ -17,10 +17,13 @@ beside it.  The timed loops call the C entry points with prebuilt arguments
 (checked once through the Python binding first), so that host-side argument
 marshalling does not pace the GPU.  The roofline object covers the dominant
 kernel (the fused conv), timed with HIP events over back-to-back launches on
-one stream.  Extra workloads (the shift kernel conv, the fused-limit bf16 conv,
-state passing at L = 128K, the layer forward, the small fp32 conv, step mode,
-the conv backward pass, the layer with heads, the conv's scaling with H) are
-reported under "extra".  The float64 CPU oracle is timed on the same config-1
+one stream (mean over back-to-back launches; median, p10 and p90 from a loop
+with an event after every launch), and names what limits it (from counters
+taken on the same kernel source).  Extra workloads (the shift kernel conv, the
+fused-limit bf16 conv, state passing at L = 128K, the layer forward, the small
+fp32 conv and its scaled variant B=8 H=4096 with its own VALU roofline, step
+mode, the conv backward pass, the layer with heads, the conv's scaling with H)
+are reported under "extra".  The float64 CPU oracle is timed on the same config-1
 workload as "cpu_baseline".
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--streams S] [--no-extra] [--no-cpu]
@@ -37,27 +40,53 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 
-# HBM traffic of the dominant kernel per launch, from two rocprofv3 --pmc runs
-# (FETCH_SIZE, WRITE_SIZE; KiB per dispatch, averaged over the bench's
-# dispatches), calibrated against a 512 MiB device copy: bytes = KiB x 1024 x
-# 2.0 (fetch) and x 1.0 (write).  Valid only for the kernel source the
-# counters were taken on: the sha256 prefix of that source is checked at run
-# time and the figure reported as null after any change.
-TRAFFIC_SRC = ("paper_2212_14052_amd/csrc/fftconv_wave.hip", "paper_2212_14052_amd/csrc/wave_common.h")
-TRAFFIC_SHA256 = "4bb1168793f2872c"
-TRAFFIC_FETCH_KIB, TRAFFIC_WRITE_KIB = 15633.5, 24576.0
+# Counters of the measured kernels per launch, from rocprofv3 --pmc runs of
+# this script (each counter set in a run of its own):
+#   fetch_kib, write_kib: FETCH_SIZE and WRITE_SIZE (KiB per dispatch),
+#     calibrated against a 512 MiB device copy (--copy-probe), which reads
+#     FETCH_SIZE = 262156.7 KiB and writes WRITE_SIZE = 524288 KiB: bytes =
+#     KiB x 1024 x 2.0 (fetch) and x 1.0 (write);
+#   valu, mfma: SQ_INSTS_VALU, SQ_INSTS_MFMA (wave instructions per dispatch);
+#   mfma_busy: SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x SQ_BUSY_CYCLES / 32).
+# An entry holds only for the kernel sources it was taken on: the sha256
+# prefix of those sources is checked at run time and the entry dropped (its
+# figures reported as null) after any change to them.
 FETCH_FACTOR, WRITE_FACTOR = 2.0, 1.0
+COUNTERS = {
+    "headline": {"src": ("paper_2212_14052_amd/csrc/fftconv_wave.hip", "paper_2212_14052_amd/csrc/wave_common.h"),
+                 "sha": "3faeec79388f9e85", "fetch_kib": 15640.5, "write_kib": 24576.0,
+                 "valu": 6191616, "mfma": 663552, "mfma_busy": 0.218},
+    "cfg0_scaled": {"src": ("paper_2212_14052_amd/csrc/fftconv.hip", "paper_2212_14052_amd/csrc/fft_valu.h"),
+                    "sha": "a55c178cb10dd628", "valu": 84164608, "mfma": 0},
+}
+SIMDS, CLOCK_GHZ = 1024, 2.4
 
 
-def measured_traffic():
+def counters(name):
     import hashlib
+    c = COUNTERS[name]
     h = hashlib.sha256()
-    for src in TRAFFIC_SRC:
+    for src in c["src"]:
         with open(os.path.join(ROOT, src), "rb") as f:
             h.update(f.read())
-    if h.hexdigest()[:16] != TRAFFIC_SHA256:
+    return c if h.hexdigest()[:16] == c["sha"] else None
+
+
+def measured_traffic(name="headline"):
+    c = counters(name)
+    if c is None or "fetch_kib" not in c:
         return None
-    return round(TRAFFIC_FETCH_KIB * 1024 * FETCH_FACTOR + TRAFFIC_WRITE_KIB * 1024 * WRITE_FACTOR)
+    return round(c["fetch_kib"] * 1024 * FETCH_FACTOR + c["write_kib"] * 1024 * WRITE_FACTOR)
+
+
+def valu_issue_frac(name, us):
+    """Share of a launch of `us` microseconds that the VALU issue of its
+    counted instructions fills: a wave64 VALU instruction occupies its SIMD
+    for 4 cycles (16 lanes), over 1024 SIMDs at 2.4 GHz."""
+    c = counters(name)
+    if c is None:
+        return None
+    return round(c["valu"] * 4 / (SIMDS * CLOCK_GHZ * 1e3) / us, 3)
 
 
 def _dev_tensor(storage, dtype, dev):
@@ -139,14 +168,22 @@ def bench_headline(h3, steps, warmup, dev, nstreams=3):
 
     ms_single = timed(1)
     ms = timed(nstreams) if nstreams > 1 else ms_single
-    # Per-launch duration of each kernel of the step, each timed over K
-    # back-to-back launches on torch's current stream (events on that stream;
-    # the figure includes the dispatch gap between dependent launches, a few
-    # us, which the kernel trace does not count).
+    # Per-launch duration of each kernel of the step: K back-to-back launches
+    # on torch's current stream between two events on that stream (the mean
+    # includes the dispatch gap between dependent launches, a few us, which
+    # the kernel trace does not count).  The spread comes from a second loop
+    # with an event after every launch (kernels and single-stream steps):
+    # median, p10, p90 of those spans, each of which also carries the event's
+    # own gap of about 3 us.
     cur = vp(torch.cuda.current_stream(dev).cuda_stream)
     per = {
         "ssm_kernel": _time_calls(lambda i: gen(0, cur), steps, 3),
         "fftconv": _time_calls(lambda i: conv(i, 0, cur), steps, 3),
+    }
+    dists = {
+        "ssm_kernel": _time_each(lambda i: gen(0, cur), steps, 3),
+        "fftconv": _time_each(lambda i: conv(i, 0, cur), steps, 3),
+        "step_single_stream": _time_each(lambda i: (gen(0, cur), conv(i, 0, cur)), steps, 3),
     }
     # u + y (fp16) + k (fp32, once per channel) + D
     step_bytes = B * H * L * (2 + 2) + H * L * 4 + H * 4
@@ -158,7 +195,34 @@ def bench_headline(h3, steps, warmup, dev, nstreams=3):
         "value": step_bytes / (ms * 1e-3) / 1e9,
         "gelem_per_s": B * H * L / (ms * 1e-3) / 1e9,
         "stage_ms": per, "conv_bytes": conv_bytes, "conv_gbs": conv_gbs, "nsets": nsets,
+        "dist_us": {k: _dist_us(v) for k, v in dists.items()},
     }
+
+
+def _time_each(fn, reps, warm):
+    """Per-call durations (ms) of `reps` back-to-back calls of fn(i) on the
+    current stream: an event after every call, so call i is the span between
+    the events before and after it (dispatch gaps included, as in the mean)."""
+    import torch
+    for _ in range(warm):
+        fn(0)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+    ev[0].record()
+    for i in range(reps):
+        fn(i)
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    return [ev[i].elapsed_time(ev[i + 1]) for i in range(reps)]
+
+
+def _dist_us(ms_list):
+    """mean, median, p10, p90 (us) of per-call durations in ms."""
+    import numpy as np
+    a = np.asarray(ms_list, dtype=np.float64) * 1e3
+    return {"mean": round(float(a.mean()), 3), "p50": round(float(np.percentile(a, 50)), 3),
+            "p10": round(float(np.percentile(a, 10)), 3), "p90": round(float(np.percentile(a, 90)), 3),
+            "n": int(a.size)}
 
 
 def _time_calls(fn, reps, warm):
@@ -398,18 +462,86 @@ def _extra_heads(h3, dev, reps, warm, ex, np, torch, workloads):
                                "ssm_rows": B * d * dh}
 
 
+def conv_flops(B, H, L):
+    """Algorithmic flops of one fused convolution launch: per row pair (two
+    rows in one complex signal of N = 2L points) a forward and an inverse
+    complex FFT at 5 N log2 N each and the pointwise complex product (6 N);
+    per channel one kernel-spectrum FFT (5 N log2 N)."""
+    import math
+    N = 2 * L
+    fft = 5.0 * N * math.log2(N)
+    return ((B + 1) // 2) * H * (2 * fft + 6 * N) + H * fft
+
+
+# fp32 VALU issue peak without packed-FP32 instructions (the library is built
+# without them): 256 CUs x 4 SIMDs x 16 lanes x 2 flops (FMA) x 2.4 GHz.
+# With packed FP32 the published figure is 157.3 TFLOP/s.
+VALU_F32_PEAK_TFLOPS = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
+
+
 def _extra_cfg0(h3, dev, reps, warm, ex, np, torch, workloads):
-    # config 0: fp32, B=1 H=64 L=1024 (latency bound)
+    # config 0: fp32, B=1 H=64 L=1024, kernel generation + conv (latency
+    # bound: 64 row pairs for 256 CUs).  The binding checks the arguments
+    # once; the timed calls go to the C entry points with prebuilt arguments
+    # (the binding's host time would otherwise pace these short launches).
+    import ctypes
     w = workloads.config(0)
     u = _dev_tensor(w.u, w.dtype, dev)
     y = torch.empty_like(u)
     A, Bp, C, dt = (_f32(w.ssm.A, dev), _f32(w.ssm.B, dev), _f32(w.ssm.C, dev), _f32(w.ssm.dt, dev))
     D = _f32(w.D, dev)
     k = torch.empty((w.H, w.L), dtype=torch.float32, device=dev)
-    ws = torch.empty(h3.workspace_size(h3.OP_FFTCONV, w.B, w.H, w.L, 0, 0, h3.F32), dtype=torch.uint8, device=dev)
-    ms = _time_calls(lambda i: (h3.ssm_kernel(A, Bp, C, dt, w.L, out=k),
-                                h3.fftconv(u, k, D, out=y, workspace=ws)), 50, 5)
-    ex["cfg0_f32_latency_us"] = ms * 1e3
+    wsz = max(256, h3.workspace_size(h3.OP_FFTCONV, w.B, w.H, w.L, 0, 0, h3.F32))
+    ws = torch.empty(wsz, dtype=torch.uint8, device=dev)
+    h3.ssm_kernel(A, Bp, C, dt, w.L, out=k)
+    h3.fftconv(u, k, D, out=y, workspace=ws)
+    lib, vp = h3.lib(), ctypes.c_void_p
+    st = vp(torch.cuda.current_stream(dev).cuda_stream)
+    pa = [vp(t.data_ptr()) for t in (A, Bp, C, dt)]
+    pu, pk, pD, py, pw = (vp(t.data_ptr()) for t in (u, k, D, y, ws))
+    m = A.shape[1]
+
+    def gen(i):
+        lib.h3_ssm_kernel(*pa, w.H, m, w.L, pk, st)
+
+    def conv(i):
+        lib.h3_fftconv(pu, pk, pD, py, w.B, w.H, w.L, h3.F32, pw, wsz, st)
+
+    ex["cfg0_f32_latency_us"] = 1e3 * _time_calls(lambda i: (gen(i), conv(i)), 50, 5)
+    ex["cfg0_f32_conv_us"] = 1e3 * _time_calls(conv, 50, 5)
+    ex["cfg0_f32_step_spread_us"] = _dist_us(_time_each(lambda i: (gen(i), conv(i)), 50, 5))
+    # config 0 scaled: the same generator, L = 1024 and fp32 I/O, with
+    # B = 8, H = 4096 so that u + y take 268 MB (above the 256 MB Infinity
+    # Cache); calls rotate over two buffer sets
+    ws_ = workloads.config(0, B=8, H=4096)
+    B, H, L = ws_.B, ws_.H, ws_.L
+    us = [_dev_tensor(ws_.u, ws_.dtype, dev)]
+    us.append(us[0].clone())
+    ys = [torch.empty_like(us[0]) for _ in range(2)]
+    A, Bp, C, dt = (_f32(ws_.ssm.A, dev), _f32(ws_.ssm.B, dev), _f32(ws_.ssm.C, dev), _f32(ws_.ssm.dt, dev))
+    D = _f32(ws_.D, dev)
+    k = torch.empty((H, L), dtype=torch.float32, device=dev)
+    wsb = torch.empty(h3.workspace_size(h3.OP_FFTCONV, B, H, L, 0, 0, h3.F32), dtype=torch.uint8, device=dev)
+    h3.ssm_kernel(A, Bp, C, dt, L, out=k)
+    fconv = lambda i: h3.fftconv(us[i % 2], k, D, out=ys[i % 2], workspace=wsb)
+    fgen = lambda i: h3.ssm_kernel(A, Bp, C, dt, L, out=k)
+    conv_ms, step_ms, gen_ms = (_time_calls(f, 20, 4) for f in (fconv, lambda i: (fgen(i), fconv(i)), fgen))
+    dc = {"mean": round(conv_ms * 1e3, 3)}
+    spread = _dist_us(_time_each(fconv, 20, 4))
+    by = B * H * L * 4 * 2 + H * L * 4 + H * 4     # u, y, k, D
+    fl = conv_flops(B, H, L)
+    tfl = fl / (dc["mean"] * 1e-6) / 1e12
+    ex["cfg0_scaled_f32"] = {
+        "workload": "config 0 scaled (B=8 H=4096 L=1024 fp32, u+y 268 MB)",
+        "conv_us": dc["mean"], "conv_spread_us": spread, "step_us": step_ms * 1e3, "ssm_kernel_us": gen_ms * 1e3,
+        "conv_GB_s": by / (dc["mean"] * 1e-6) / 1e9, "conv_pct_hbm_peak": 100 * by / (dc["mean"] * 1e-6) / 1e9 / HBM_PEAK_GBS,
+        "step_gelem_per_s": B * H * L / (step_ms * 1e-3) / 1e9,
+        "roofline": {"bound": "alu", "achieved": round(tfl, 2), "peak": round(VALU_F32_PEAK_TFLOPS, 1),
+                     "unit": "TFLOP/s", "frac": round(tfl / VALU_F32_PEAK_TFLOPS, 4),
+                     "kernel": "fftconv_kgen_kernel<2048, f32>", "flops_per_launch": fl,
+                     "hbm_frac": round(by / (dc["mean"] * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                     "valu_issue_frac": valu_issue_frac("cfg0_scaled", dc["mean"])},
+    }
 
 
 def _extra_bwd(h3, dev, reps, warm, ex, np, torch, workloads):
@@ -466,6 +598,18 @@ def _extra_step(h3, dev, reps, warm, ex, np, torch, workloads):
                              "tokens_per_s": B / (ms * 1e-3), "bytes_per_call": nbytes}
 
 
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or None
+
+
 def cpu_baseline(w, step_bytes, min_seconds=10.0, max_reps=64):
     """The float64 oracle on the whole config-1 workload (kernel generation for
     every channel, then the direct causal convolution of every row), repeated
@@ -484,9 +628,23 @@ def cpu_baseline(w, step_bytes, min_seconds=10.0, max_reps=64):
             break
     el = time.time() - t
     return {"value": reps * step_bytes / el / 1e9, "unit": "GB/s", "cores": oracle.num_threads(),
+            "cpu_model": _cpu_model(), "os_cpu_count": os.cpu_count(),
+            "affinity_cpus": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None,
             "kind": "oracle",
             "sample": f"whole config-1 workload (B={w.B} H={w.H} L={w.L}) x {reps}: float64 kernel "
                       f"generation + direct O(L^2) causal conv, {el:.2f} s wall"}
+
+
+def _headline_limiter(us):
+    """What bounds the headline conv below its HBM roof, from its counters:
+    neither the VALU nor the matrix cores nor HBM is near saturation; each
+    wave runs one row pair's transforms as one dependent chain, three waves
+    per SIMD."""
+    c = counters("headline")
+    if c is None:
+        return None
+    return {"kind": "latency", "valu_issue_frac": valu_issue_frac("headline", us), "mfma_busy_frac": c["mfma_busy"],
+            "valu_per_pair": round(c["valu"] / 3072), "mfma_per_pair": round(c["mfma"] / 3072), "waves_per_simd": 3}
 
 
 def main():
@@ -546,13 +704,15 @@ def main():
                    "pct_hbm_peak": round(100 * head["value"] / HBM_PEAK_GBS, 2),
                    "gelem_per_s": round(head["gelem_per_s"], 2),
                    "stage_us": {k: round(v * 1e3, 2) for k, v in per.items()},
+                   "per_launch_us": head["dist_us"],
                    "streams": head["streams"],
                    "us_per_step_single_stream": round(head["ms_per_step_single_stream"] * 1e3, 2),
                    "gb_s_single_stream": round(head["step_bytes"] / (head["ms_per_step_single_stream"] * 1e-3) / 1e9, 1),
                    "buffer_sets": head["nsets"]},
         "roofline": {"bound": "hbm", "achieved": round(head["conv_gbs"], 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(head["conv_gbs"] / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
-                     "kernel": "fftconv_wave4096_kernel<f16>", "bytes_per_launch": head["conv_bytes"]},
+                     "kernel": "fftconv_wave4096_kernel<f16>", "bytes_per_launch": head["conv_bytes"],
+                     "limiter": _headline_limiter(per["fftconv"] * 1e3)},
     }
     if extra:
         res["extra"] = extra

@@ -137,6 +137,15 @@ hipError_t layer_qkv(const void *x, const void *Wq, const void *Wk, const void *
     const size_t act = (size_t)B * L * d * 2, wb = (size_t)d * d * 2;
     const void *Wqkv[3] = {Wq, Wk, Wv};
     const bool native = gemm_native();
+    if (native && gemm_w320_ok(3 * d, B * L, d)) {
+        // the three transposed weights are consecutive in wt: one (3 d, d)
+        // operand, one launch for Q, K and V
+        for (int j = 0; j < 3; ++j) {
+            hipError_t e = launch_transpose_batched(Wqkv[j], (char *)wt + j * wb, 1, d, d, s);
+            if (e != hipSuccess) return e;
+        }
+        return launch_gemm_w320(wt, x, qkv, 3 * d, B * L, d, dtype, 1, d, L, s);
+    }
     for (int j = 0; j < 3; ++j) {
         hipError_t e = native ? hipErrorNotSupported
                               : launch_gemm_lt(Wqkv[j], false, x, true, qkv + j * act, d, L, d, B, 0, (long)L * d,
@@ -161,7 +170,8 @@ hipError_t layer_out(const void *o_tm, const void *Wo, void *out, int B, int L, 
     if (e == hipErrorNotSupported) {
         char *wo = (char *)wt + 3 * (size_t)d * d * 2;
         if ((e = launch_transpose_batched(Wo, wo, 1, d, d, s)) != hipSuccess) return e;
-        e = launch_gemm_nt(o_tm, wo, out, B * L, d, d, dtype, 0, d, L, s);
+        e = gemm_w320_ok(d, B * L, d) ? launch_gemm_w320(wo, o_tm, out, d, B * L, d, dtype, 0, d, L, s)
+                                      : launch_gemm_nt(o_tm, wo, out, B * L, d, d, dtype, 0, d, L, s);
     }
     return e;
 }

@@ -139,6 +139,13 @@ hipError_t launch_heads_expand(int dh, const void *kbar, const void *v, void *g,
                                hipStream_t s);
 hipError_t launch_heads_contract(int dh, const void *q, const void *sv, void *o, int B, int d, int L, int dtype,
                                  hipStream_t s);
+// C = Wt . X^T on 320 x 256 tiles (Wt: (Mw, K) weight side, X: (Nx, K)
+// activations, both K-contiguous); out_mode 1: channel-major [Q;K;V] layout
+// as launch_gemm_nt, out_mode 0: row-major (Nx, Mw).  Needs Mw % 320 == 0,
+// Nx % 256 == 0, K % 64 == 0 (gemm_w320_ok).
+bool gemm_w320_ok(int Mw, int Nx, int K);
+hipError_t launch_gemm_w320(const void *Wt, const void *X, void *C, int Mw, int Nx, int K, int dtype, int out_mode,
+                            int d, int L, hipStream_t s);
 hipError_t launch_gemm_nt(const void *A, const void *Bt, void *C, int M, int N, int K, int dtype,
                           int out_mode, int d, int L, hipStream_t s);
 hipError_t launch_layer_mid(const void *q, const void *k, const void *v, const float *shift_C,
