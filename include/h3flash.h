@@ -5,11 +5,9 @@
  * General conventions
  *  - Every tensor pointer is a DEVICE pointer owned by the caller.  Scratch
  *    space is passed in as `workspace` (size it with h3_workspace_size) and
- *    must not alias any other argument.  The library's own kernels allocate no
- *    device memory.  Departure from a stateless library: h3_layer_fwd's
- *    projections run through hipBLASLt, whose per-device handle (created on
- *    the first layer call on a device and kept until the process ends) may
- *    hold memory of its own.
+ *    must not alias any other argument.  The library allocates no device
+ *    memory (h3_statepass_conv_noalloc uses a static device array instead of
+ *    a workspace).
  *  - Complex values are interleaved (re, im) float32 pairs.
  *  - Tensors are dense, row-major, with the last dimension contiguous.
  *    Sequence tensors are (B, H, L): row (b, h) is L contiguous elements.
@@ -22,10 +20,10 @@
  *  - NaN and Inf in the inputs propagate to the outputs; they are not masked.
  *  - Return value: H3_OK (0) or a negative h3_status.  No C++ exception crosses
  *    this boundary.
- *  - The only state the library keeps is host-side and belongs to
- *    h3_layer_fwd: one hipBLASLt handle per device and one GEMM plan per
- *    shape, built on first use under a mutex.  Every entry point may be called
- *    from several host threads.
+ *  - The library keeps no state between calls apart from values looked up
+ *    once and cached (a kernel's resident workgroups per CU; the device
+ *    address of h3_statepass_conv_noalloc's array, per device).  Every entry
+ *    point may be called from several host threads.
  */
 #ifndef H3FLASH_H
 #define H3FLASH_H
@@ -226,11 +224,11 @@ int h3_ssm_step(const void *u, const float *Abar, const float *Bbar, const float
  *   L power of two in [H3_MIN_LEN, H3_FUSED_LIMIT]; d a multiple of 128;
  *   B * L a multiple of 128 (the tiles of the library's own GEMM).
  *   workspace >= h3_workspace_size(H3_OP_LAYER, B, d, L, m_s, 0, dtype).
- * The four projections run through hipBLASLt, which reads the weights as they
- * are stored (transposed operands); the library's own matrix-core GEMM runs
- * instead for shapes hipBLASLt rejects, or for every call while the
- * environment variable H3FLASH_GEMM is "native" (read on each call), on
- * transposed copies of the weights made in the workspace.
+ * The four projections run on the library's own matrix-core GEMM, which reads
+ * transposed copies of the weights made in the workspace: Q, K and V in one
+ * launch of 320 x 256 tiles when d is a multiple of 320 (256 x 256 when d is
+ * a multiple of 256) and B * L of 256, else one 128 x 128-tile launch per
+ * projection.
  * Errors: EINVAL, EUNSUPPORTED (L, d, B * L, m_s, dtype), EWORKSPACE, EDEVICE.
  */
 int h3_layer_fwd(const void *x, const void *Wq, const void *Wk, const void *Wv,

@@ -82,11 +82,10 @@ StatepassWs statepass_ws(int B, int H, int L, int m, int chunk, int dtype) {
 }
 
 struct LayerWs {
-    size_t qkv, o_cm, o_tm, kspec, wt, gemm, total;
+    size_t qkv, o_cm, o_tm, kspec, wt, total;
 };
-constexpr size_t kLayerGemmWs = (size_t)64 << 20;   // hipBLASLt algorithm workspace
-// wt: the four weights transposed to (out, in), for the library's own GEMM
-// (both of its operands reduction-contiguous)
+// wt: the four weights transposed to (out, in) (the GEMM reads both operands
+// reduction-contiguous); Q, K, V consecutive, so they form one (3 d, d) operand
 LayerWs layer_ws(int B, int d, int L) {
     LayerWs w;
     const size_t act = (size_t)B * d * L * 2;
@@ -95,16 +94,15 @@ LayerWs layer_ws(int B, int d, int L) {
     w.o_tm = w.o_cm + align_up(act);
     w.kspec = w.o_tm + align_up(act);
     w.wt = w.kspec + align_up((size_t)d * (L + 1) * sizeof(float2));
-    w.gemm = w.wt + align_up((size_t)4 * d * d * 2);
-    w.total = w.gemm + kLayerGemmWs;
+    w.total = w.wt + align_up((size_t)4 * d * d * 2);
     return w;
 }
 
 // Layer heads with d_h > 1: Q, K, V, Kbar, the outer products G and their
 // convolutions S (d_h rows per channel), O token-major, the spectra for the
-// VALU convolution, the GEMM algorithm workspace.
+// VALU convolution, the transposed weights.
 struct HeadsWs {
-    size_t qkv, kbar, g, sv, o_tm, kspec, wt, gemm, total;
+    size_t qkv, kbar, g, sv, o_tm, kspec, wt, total;
 };
 HeadsWs heads_ws(int B, int d, int L, int dh) {
     HeadsWs w;
@@ -116,66 +114,43 @@ HeadsWs heads_ws(int B, int d, int L, int dh) {
     w.o_tm = w.sv + align_up((size_t)dh * act);
     w.kspec = w.o_tm + align_up(act);
     w.wt = w.kspec + align_up((size_t)d * dh * (L + 1) * sizeof(float2));
-    w.gemm = w.wt + align_up((size_t)4 * d * d * 2);
-    w.total = w.gemm + kLayerGemmWs;
+    w.total = w.wt + align_up((size_t)4 * d * d * 2);
     return w;
-}
-
-bool gemm_native() {
-    const char *gsel = getenv("H3FLASH_GEMM");
-    return gsel && strcmp(gsel, "native") == 0;
 }
 
 // [Q;K;V] channel-major: per projection j and batch b the (d, L) block
 // j B d L + b d L is (x_b W_j)^T = W_j^T (d, d) . x_b (L, d)^T.  The weights
-// come as Algorithm 1 writes them, (in, out) with Q = x W_Q: hipBLASLt reads
-// W_j as the transposed operand.  The library's own GEMM (where hipBLASLt
-// rejects the shape, or with H3FLASH_GEMM=native) takes both operands
-// reduction-contiguous, so it reads W_j^T, transposed into wt first.
+// come as Algorithm 1 writes them, (in, out) with Q = x W_Q; the GEMM takes
+// both operands reduction-contiguous, so the three are transposed into wt
+// first, where they form one (3 d, d) operand: one launch for Q, K and V
+// where the tiles allow it (d a multiple of 256 or 320, B L of 256), else
+// one 128 x 128-tile launch per projection.
 hipError_t layer_qkv(const void *x, const void *Wq, const void *Wk, const void *Wv, char *qkv, int B, int L, int d,
-                     int dtype, void *wt, void *gws, hipStream_t s) {
+                     int dtype, void *wt, hipStream_t s) {
     const size_t act = (size_t)B * L * d * 2, wb = (size_t)d * d * 2;
     const void *Wqkv[3] = {Wq, Wk, Wv};
-    const bool native = gemm_native();
-    if (native && gemm_w320_ok(3 * d, B * L, d)) {
-        // the three transposed weights are consecutive in wt: one (3 d, d)
-        // operand, one launch for Q, K and V
-        for (int j = 0; j < 3; ++j) {
-            hipError_t e = launch_transpose_batched(Wqkv[j], (char *)wt + j * wb, 1, d, d, s);
-            if (e != hipSuccess) return e;
-        }
-        return launch_gemm_w320(wt, x, qkv, 3 * d, B * L, d, dtype, 1, d, L, s);
-    }
     for (int j = 0; j < 3; ++j) {
-        hipError_t e = native ? hipErrorNotSupported
-                              : launch_gemm_lt(Wqkv[j], false, x, true, qkv + j * act, d, L, d, B, 0, (long)L * d,
-                                               (long)d * L, dtype, gws, kLayerGemmWs, s);
-        if (e == hipErrorNotSupported) {
-            char *wj = (char *)wt + j * wb;
-            if ((e = launch_transpose_batched(Wqkv[j], wj, 1, d, d, s)) != hipSuccess) return e;
-            e = launch_gemm_nt(wj, x, qkv + j * act, d, B * L, d, dtype, 1, d, L, s);
-        }
+        hipError_t e = launch_transpose_batched(Wqkv[j], (char *)wt + j * wb, 1, d, d, s);
+        if (e != hipSuccess) return e;
+    }
+    if (gemm_w_tile(3 * d, B * L, d, d, 1)) return launch_gemm_w(wt, x, qkv, 3 * d, B * L, d, dtype, 1, d, L, s);
+    for (int j = 0; j < 3; ++j) {
+        hipError_t e = launch_gemm_nt((char *)wt + j * wb, x, qkv + j * act, d, B * L, d, dtype, 1, d, L, s);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
 }
 
-// out = O (B L, d) . Wo (d, d), O token-major; hipBLASLt reads Wo as it is
-// stored, the library's GEMM reads Wo^T (transposed into the fourth slot of wt)
+// out = O (B L, d) . Wo (d, d), O token-major; the GEMM reads Wo^T
+// (transposed into the fourth slot of wt)
 hipError_t layer_out(const void *o_tm, const void *Wo, void *out, int B, int L, int d, int dtype, void *wt,
-                     void *gws, hipStream_t s) {
-    hipError_t e = gemm_native() ? hipErrorNotSupported
-                                 : launch_gemm_lt(o_tm, true, Wo, false, out, B * L, d, d, 1, 0, 0, 0, dtype, gws,
-                                                  kLayerGemmWs, s);
-    if (e == hipErrorNotSupported) {
-        char *wo = (char *)wt + 3 * (size_t)d * d * 2;
-        if ((e = launch_transpose_batched(Wo, wo, 1, d, d, s)) != hipSuccess) return e;
-        e = gemm_w320_ok(d, B * L, d) ? launch_gemm_w320(wo, o_tm, out, d, B * L, d, dtype, 0, d, L, s)
-                                      : launch_gemm_nt(o_tm, wo, out, B * L, d, d, dtype, 0, d, L, s);
-    }
-    return e;
+                     hipStream_t s) {
+    char *wo = (char *)wt + 3 * (size_t)d * d * 2;
+    hipError_t e = launch_transpose_batched(Wo, wo, 1, d, d, s);
+    if (e != hipSuccess) return e;
+    return gemm_w_tile(d, B * L, d, d, 0) ? launch_gemm_w(wo, o_tm, out, d, B * L, d, dtype, 0, d, L, s)
+                                          : launch_gemm_nt(o_tm, wo, out, B * L, d, d, dtype, 0, d, L, s);
 }
-
 
 }  // namespace
 
@@ -473,8 +448,8 @@ int h3_layer_fwd(const void *x, const void *Wq, const void *Wk, const void *Wv, 
     void *o_tm = ws + w.o_tm;
     float2 *Kspec = (float2 *)(ws + w.kspec);
     hipError_t e;
-    void *gws = ws + w.gemm, *wt = ws + w.wt;
-    if ((e = layer_qkv(x, Wq, Wk, Wv, qkv, B, L, d, dtype, wt, gws, s)) != hipSuccess) return H3_EDEVICE;
+    void *wt = ws + w.wt;
+    if ((e = layer_qkv(x, Wq, Wk, Wv, qkv, B, L, d, dtype, wt, s)) != hipSuccess) return H3_EDEVICE;
     const char *q = qkv, *kk = qkv + act, *v = qkv + 2 * act;
     if (fftconv_mfma_supported(L, dtype) && L % 64 == 0) {
         // G = (shift SSM of K) * V  ->  o_cm;  S = diag conv of G (+ D G)  ->  K's slot (K is dead);
@@ -494,7 +469,7 @@ int h3_layer_fwd(const void *x, const void *Wq, const void *Wk, const void *Wv, 
         // O (B, d, L) -> (B, L, d)
         if ((e = launch_transpose_batched(o_cm, o_tm, B, d, L, s)) != hipSuccess) return H3_EDEVICE;
     }
-    return launched(layer_out(o_tm, Wo, out, B, L, d, dtype, wt, gws, s));
+    return launched(layer_out(o_tm, Wo, out, B, L, d, dtype, wt, s));
 }
 
 int h3_layer_fwd_heads(const void *x, const void *Wq, const void *Wk, const void *Wv, const void *Wo,
@@ -525,11 +500,11 @@ int h3_layer_fwd_heads(const void *x, const void *Wq, const void *Wk, const void
     const HeadsWs w = heads_ws(B, d, L, d_head);
     char *ws = (char *)workspace;
     char *qkv = ws + w.qkv;
-    void *kbar = ws + w.kbar, *g = ws + w.g, *sv = ws + w.sv, *o_tm = ws + w.o_tm, *gws = ws + w.gemm, *wt = ws + w.wt;
+    void *kbar = ws + w.kbar, *g = ws + w.g, *sv = ws + w.sv, *o_tm = ws + w.o_tm, *wt = ws + w.wt;
     float2 *Kspec = (float2 *)(ws + w.kspec);
     const char *q = qkv, *kk = qkv + act, *v = qkv + 2 * act;
     hipError_t e;
-    if ((e = layer_qkv(x, Wq, Wk, Wv, qkv, B, L, d, dtype, wt, gws, s)) != hipSuccess) return H3_EDEVICE;
+    if ((e = layer_qkv(x, Wq, Wk, Wv, qkv, B, L, d, dtype, wt, s)) != hipSuccess) return H3_EDEVICE;
     // Kbar = shift SSM of K (no gating); G = per-head outer products of Kbar and V
     if ((e = launch_shift_gate(kk, nullptr, shift_C, shift_D, m_s, B, d, L, dtype, kbar, s)) != hipSuccess)
         return H3_EDEVICE;
@@ -547,7 +522,7 @@ int h3_layer_fwd_heads(const void *x, const void *Wq, const void *Wk, const void
     }
     // O_t[j] = sum_i Q_t[i] S_t[i][j], token-major; out = O Wo^T
     if ((e = launch_heads_contract(d_head, q, sv, o_tm, B, d, L, dtype, s)) != hipSuccess) return H3_EDEVICE;
-    return launched(layer_out(o_tm, Wo, out, B, L, d, dtype, wt, gws, s));
+    return launched(layer_out(o_tm, Wo, out, B, L, d, dtype, wt, s));
 }
 
 }  // extern "C"

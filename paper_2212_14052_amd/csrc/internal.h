@@ -124,14 +124,6 @@ hipError_t launch_gate_transpose(const void *q, const void *sv, void *out, int n
 // v null: G = the shift FIR of K alone.
 hipError_t launch_shift_gate(const void *k, const void *v, const float *shift_C, const float *shift_D, int m_s,
                              int B, int d, int L, int dtype, void *g, hipStream_t s);
-// hipBLASLt GEMM, C (M, N) row-major = A . B with A given as (M, K)
-// row-major when a_kc (K contiguous) else as (K, M) row-major, and B given as
-// (N, K) row-major when b_kc else as (K, N) row-major; batched with element
-// strides sa, sb, sc (0 = shared operand).  hipErrorNotSupported, before
-// anything is enqueued, when no algorithm fits (the caller then uses
-// launch_gemm_nt); ws / ws_bytes: workspace slice for the algorithm.
-hipError_t launch_gemm_lt(const void *A, bool a_kc, const void *B, bool b_kc, void *C, int M, int N, int K, int batch,
-                          long sa, long sb, long sc, int dtype, void *ws, size_t ws_bytes, hipStream_t s);
 // Heads of dimension dh in {2, 4, 8} (d % 64 == 0, L % 64 == 0): the outer
 // products G (B, d dh, L) of Kbar and V, and their contraction with Q into
 // O (B, L, d) token-major.
@@ -139,13 +131,15 @@ hipError_t launch_heads_expand(int dh, const void *kbar, const void *v, void *g,
                                hipStream_t s);
 hipError_t launch_heads_contract(int dh, const void *q, const void *sv, void *o, int B, int d, int L, int dtype,
                                  hipStream_t s);
-// C = Wt . X^T on 320 x 256 tiles (Wt: (Mw, K) weight side, X: (Nx, K)
-// activations, both K-contiguous); out_mode 1: channel-major [Q;K;V] layout
-// as launch_gemm_nt, out_mode 0: row-major (Nx, Mw).  Needs Mw % 320 == 0,
-// Nx % 256 == 0, K % 64 == 0 (gemm_w320_ok).
-bool gemm_w320_ok(int Mw, int Nx, int K);
-hipError_t launch_gemm_w320(const void *Wt, const void *X, void *C, int Mw, int Nx, int K, int dtype, int out_mode,
-                            int d, int L, hipStream_t s);
+// C = Wt . X^T on TW x 256 tiles, TW = 320 or 256 (Wt: (Mw, K) weight side,
+// X: (Nx, K) activations, both K-contiguous); out_mode 1: channel-major
+// [Q;K;V] layout as launch_gemm_nt, out_mode 0: row-major (Nx, Mw).
+// gemm_w_tile gives the tile height for a shape (0: not supported: needs
+// Nx % 256 == 0, K % 32 == 0 and Mw, and for out_mode 1 also d, a multiple of
+// TW).
+int gemm_w_tile(int Mw, int Nx, int K, int d, int out_mode);
+hipError_t launch_gemm_w(const void *Wt, const void *X, void *C, int Mw, int Nx, int K, int dtype, int out_mode,
+                         int d, int L, hipStream_t s);
 hipError_t launch_gemm_nt(const void *A, const void *Bt, void *C, int M, int N, int K, int dtype,
                           int out_mode, int d, int L, hipStream_t s);
 hipError_t launch_layer_mid(const void *q, const void *k, const void *v, const float *shift_C,

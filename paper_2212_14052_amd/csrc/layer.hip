@@ -227,62 +227,75 @@ __global__ __launch_bounds__(G2_T) void gemm_nt_256(const uint16_t *A, const uin
                                 n0 + wn * 64 + j * 32 + (lane & 31), N, d, L);
 }
 
-// ------------------------------------------- GEMM, 320 x 256 weight tiles ---
+// ------------------------------------------- GEMM, TW x 256 weight tiles ---
 // C = Wt . X^T with Wt (Mw, K) the weight side and X (Nx, K) the activation
-// side, both K-contiguous 16-bit, fp32 accumulation.  Block tile 320 (weight
-// rows) x 256 (activation rows) x 32: at the layer's shapes (Mw = 3 d for the
-// fused Q/K/V projection, Mw = d for the output projection, d a multiple of
-// 320, Nx = B L a multiple of 256) the grid is a whole number of 256-tile
-// rounds for d = 2560 (768 and 256 tiles), where 256 x 256 tiles leave the
-// last round a quarter full.  Eight waves, 2 (weight) x 4 (activation), each
-// 160 x 64 = 5 x 2 tiles of 32x32x16 MFMA (160 fp32 accumulators per lane,
-// two waves per SIMD).
+// side, both K-contiguous 16-bit, fp32 accumulation.  Block tile TW (weight
+// rows: 320 or 256) x 256 (activation rows) x 32.  At d = 2560 (a multiple
+// of 320) the fused Q/K/V projection (Mw = 3 d) and the output projection
+// (Mw = d) over Nx = B L = 8192 tokens are 768 and 256 tiles of 320 x 256:
+// whole rounds of the 256 CUs, where 256 x 256 tiles leave the last round a
+// quarter full.  Eight waves, 2 (weight) x 4 (activation), each (TW / 2) x
+// 64 = (TW / 64) x 2 tiles of 32x32x16 MFMA (up to 160 fp32 accumulators per
+// lane, two waves per SIMD).
 // Operands reach LDS without passing through registers: each wave copies
 // 16-row slices (1 KB, 64 lanes x 16 bytes, lane i to byte 16 i of the slice)
-// with global_load_lds_dwordx4, four stages deep (loads run three K steps
+// with global_load_lds_dwordx4, four stages deep (copies run three K steps
 // ahead; a stage is waited for with vmcnt and one barrier per K step, which
 // also orders the refill of the buffer read in the step before).  A stage is
-// 576 rows (320 weight, then 256 activation) of 32 values (64 B, four 16-byte
-// chunks), chunk c of row r at slot c ^ ((r / 2) % 4): the fragment reads of
-// eight consecutive rows touch eight distinct 16-byte bank groups.  Lane i of
-// a slice thus fetches chunk (i % 4) ^ ((r / 2) % 4) of row r = 16 q + i / 4.
+// TW + 256 rows (weight rows, then activation rows) of 32 values (64 B, four
+// 16-byte chunks), chunk c of row r at slot c ^ ((r / 2) % 4): the fragment
+// reads of eight consecutive rows touch eight distinct 16-byte bank groups.
+// Lane i of a slice thus fetches chunk (i % 4) ^ ((r / 2) % 4) of row
+// r = 16 q + i / 4.
 // OUT 1: element (m, n) = (weight row, activation row) goes to the
-//        channel-major [Q;K;V] layout [(m / d)][(n / L)][(m % d)][(n % L)],
-//        with the activation rows along the MFMA columns (lanes), so 32
-//        consecutive tokens of one channel are one 64-byte run;
+//        channel-major [Q;K;V] layout [(m / d)][(n / L)][(m % d)][(n % L)]
+//        (d a multiple of TW: a tile lies in one projection), with the
+//        activation rows along the MFMA columns (lanes), so 32 consecutive
+//        tokens of one channel are one 64-byte run;
 // OUT 0: element (n, m) of a row-major (Nx, Mw) result, with the weight
 //        rows along the MFMA columns (lanes) for 64-byte runs of channels.
-constexpr int GW_W = 320, GW_X = 256, GW_K = 32, GW_T = 512, GW_NS = 4;
-constexpr int GW_ROWS = GW_W + GW_X;            // rows per stage
-constexpr int GW_SLICES = GW_ROWS / 16;         // 1 KB slices per stage (36)
-constexpr int GW_STAGE_B = GW_ROWS * GW_K * 2;  // bytes per stage (36 KB)
+constexpr int GW_X = 256, GW_K = 32, GW_T = 512, GW_NS = 4;
 
 typedef __attribute__((address_space(3))) void lds_void;
 
 __device__ __forceinline__ int gw_off(int row, int chunk) { return row * GW_K + ((chunk ^ ((row >> 1) & 3)) << 3); }
 
-template <int DT, int OUT>
-__global__ __launch_bounds__(GW_T) __attribute__((amdgpu_waves_per_eu(2, 2))) void gemm_w320(
+template <int TW> struct GwShape {
+    static constexpr int ROWS = TW + GW_X;          // rows per stage
+    static constexpr int SLICES = ROWS / 16;        // 1 KB slices per stage (36 or 32)
+    static constexpr int NSL = (SLICES + 7) / 8;    // copies per wave per step (5 or 4)
+    static constexpr int STAGE_B = ROWS * GW_K * 2; // bytes per stage
+    static constexpr int TI = TW / 64;              // weight-side MFMA tiles per wave
+    // LDS bytes: the stages, and a 1 KB slot that takes the copies of waves
+    // with one slice less (never read), so every wave issues NSL per step
+    static constexpr size_t LDS = (size_t)GW_NS * STAGE_B + (SLICES % 8 ? 1024 : 0);
+    // s_waitcnt immediate for vmcnt(2 NSL): the copies of the two steps after
+    // the one waited for may stay in flight (expcnt, lgkmcnt not waited)
+    static constexpr int WAIT = 0xf70 | ((2 * NSL) & 15) | (((2 * NSL) >> 4) << 14);
+};
+
+template <int DT, int OUT, int TW>
+__global__ __launch_bounds__(GW_T) __attribute__((amdgpu_waves_per_eu(2, 2))) void gemm_w(
     const uint16_t *Wt, const uint16_t *X, uint16_t *C, int Mw, int Nx, int K, int d, int L) {
-    extern __shared__ __attribute__((aligned(1024))) uint16_t gw_lds[];   // [GW_NS][576][32], swizzled
+    using S = GwShape<TW>;
+    extern __shared__ __attribute__((aligned(1024))) uint16_t gw_lds[];   // [GW_NS][TW + 256][32], swizzled
     int tw, tx;
-    gemm_tile(Mw / GW_W, Nx / GW_X, tw, tx);
-    const int w0 = tw * GW_W, x0 = tx * GW_X;
+    gemm_tile(Mw / TW, Nx / GW_X, tw, tx);
+    const int w0 = tw * TW, x0 = tx * GW_X;
     const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
     const int ww = wv >> 2, wx = wv & 3;
-    // this wave's slices q = wv + 8 s, s < 5 (36 per stage: waves 4..7 send
-    // their fifth copy, of slice wv again, to a 1 KB slot past the stages that
-    // is never read, so that every wave issues five copies per step and waits
-    // with one count): the lane's source row and chunk as an element offset
-    // from the operand's base (Wt for q < 20, X after)
+    // this wave's slices q = wv + 8 s, s < NSL (a wave past the last slice
+    // copies slice wv again into the never-read slot): the lane's source row
+    // and chunk as an element offset from the operand's base (Wt for weight
+    // rows, X after)
     const int wvu = __builtin_amdgcn_readfirstlane(wv);   // the wave index, in a scalar register
-    uint32_t soff[5];
+    uint32_t soff[S::NSL];
 #pragma unroll
-    for (int sl = 0; sl < 5; ++sl) {
-        const int q = wvu + 8 * sl < GW_SLICES ? wvu + 8 * sl : wvu;
+    for (int sl = 0; sl < S::NSL; ++sl) {
+        const int q = wvu + 8 * sl < S::SLICES ? wvu + 8 * sl : wvu;
         const int r = 16 * q + (lane >> 2);
         const int c = (lane & 3) ^ ((r >> 1) & 3);
-        soff[sl] = r < GW_W ? (uint32_t)((w0 + r) * K + 8 * c) : (uint32_t)((x0 + r - GW_W) * K + 8 * c);
+        soff[sl] = r < TW ? (uint32_t)((w0 + r) * K + 8 * c) : (uint32_t)((x0 + r - TW) * K + 8 * c);
     }
     const int nk = K / GW_K;
     // The copies are issued as inline assembly (M0 = the slice's LDS byte
@@ -293,24 +306,24 @@ __global__ __launch_bounds__(GW_T) __attribute__((amdgpu_waves_per_eu(2, 2))) vo
     // copies of K step kt (clamped to the last step: past it they only keep
     // the count per step fixed) into stage kt % GW_NS
     auto issue = [&](int kt) {
-        const uint32_t st = lds0 + (uint32_t)((kt % GW_NS) * GW_STAGE_B);
+        const uint32_t st = lds0 + (uint32_t)((kt % GW_NS) * S::STAGE_B);
         const uint32_t k0 = (uint32_t)min(kt, nk - 1) * GW_K;
 #pragma unroll
-        for (int sl = 0; sl < 5; ++sl) {
+        for (int sl = 0; sl < S::NSL; ++sl) {
             const int q = wvu + 8 * sl;
-            const bool real = q < GW_SLICES;
-            const uint16_t *base = (real ? q : wvu) < GW_W / 16 ? Wt : X;
+            const bool real = q < S::SLICES;
+            const uint16_t *base = (real ? q : wvu) < TW / 16 ? Wt : X;
             const uint32_t vo = 2 * (soff[sl] + k0);
-            const uint32_t la = real ? st + (uint32_t)q * 1024 : lds0 + (uint32_t)(GW_NS * GW_STAGE_B);
+            const uint32_t la = real ? st + (uint32_t)q * 1024 : lds0 + (uint32_t)(GW_NS * S::STAGE_B);
             asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, %2"
                          :
                          : "v"(vo), "s"(la), "s"(base)
                          : "memory", "m0");
         }
     };
-    f32x16_t acc[5][2];
+    f32x16_t acc[S::TI][2];
 #pragma unroll
-    for (int i = 0; i < 5; ++i)
+    for (int i = 0; i < S::TI; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j)
 #pragma unroll
@@ -323,20 +336,21 @@ __global__ __launch_bounds__(GW_T) __attribute__((amdgpu_waves_per_eu(2, 2))) vo
         // it may still be in flight), then for every wave; step kt - 1's reads
         // of the buffer refilled next are done.  A bare barrier: a fenced one
         // would also drain the copies still in flight.
-        __builtin_amdgcn_s_waitcnt(0xf7a);   // vmcnt(10)
+        __builtin_amdgcn_s_waitcnt(S::WAIT);
         asm volatile("s_barrier" ::: "memory");
         issue(kt + GW_NS - 1);
-        const uint16_t *ws = gw_lds + (kt % GW_NS) * (GW_STAGE_B / 2), *xs = ws + GW_W * GW_K;
+        const uint16_t *ws = gw_lds + (kt % GW_NS) * (S::STAGE_B / 2), *xs = ws + TW * GW_K;
 #pragma unroll
         for (int ks = 0; ks < GW_K / 16; ++ks) {
             const int ch = 2 * ks + (lane >> 5);
-            uint4 fw[5], fx[2];
+            uint4 fw[S::TI], fx[2];
 #pragma unroll
-            for (int i = 0; i < 5; ++i) fw[i] = *(const uint4 *)(ws + gw_off(ww * 160 + i * 32 + (lane & 31), ch));
+            for (int i = 0; i < S::TI; ++i)
+                fw[i] = *(const uint4 *)(ws + gw_off(ww * (TW / 2) + i * 32 + (lane & 31), ch));
 #pragma unroll
             for (int j = 0; j < 2; ++j) fx[j] = *(const uint4 *)(xs + gw_off(wx * 64 + j * 32 + (lane & 31), ch));
 #pragma unroll
-            for (int i = 0; i < 5; ++i)
+            for (int i = 0; i < S::TI; ++i)
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
                     acc[i][j] = OUT == 1 ? Mfma<DT>::run(fw[i], fx[j], acc[i][j]) : Mfma<DT>::run(fx[j], fw[i], acc[i][j]);
@@ -347,13 +361,13 @@ __global__ __launch_bounds__(GW_T) __attribute__((amdgpu_waves_per_eu(2, 2))) vo
     // epilogue: the lane holds MFMA column (lane & 31) and rows 8 (e / 4) +
     // 4 (lane / 32) + e % 4; element e of a tile lands at base + rstride x
     // (8 (e / 4) + e % 4)
-    const int jq = w0 / d;   // OUT 1: the projection this tile row belongs to (d % 320 == 0)
+    const int jq = w0 / d;   // OUT 1: the projection this tile row belongs to
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
         const int nx = x0 + wx * 64 + j * 32;
 #pragma unroll
-        for (int i = 0; i < 5; ++i) {
-            const int mw = w0 + ww * 160 + i * 32;
+        for (int i = 0; i < S::TI; ++i) {
+            const int mw = w0 + ww * (TW / 2) + i * 32;
             long base, rstride;
             if constexpr (OUT == 1) {
                 const int n = nx + (lane & 31), m = mw + 4 * (lane >> 5);
@@ -828,27 +842,40 @@ hipError_t launch_gemm_nt(const void *A, const void *Bt, void *C, int M, int N, 
                     : launch_gemm_t<F16, 0>(A, Bt, C, M, N, K, d, L, s);
 }
 
-template <int DT, int OUT>
-static hipError_t launch_w320_t(const void *Wt, const void *X, void *C, int Mw, int Nx, int K, int d, int L,
-                                hipStream_t s) {
-    const size_t lds = (size_t)GW_NS * GW_STAGE_B + 1024;   // + the never-read slot
-    auto fn = gemm_w320<DT, OUT>;
+template <int DT, int OUT, int TW>
+static hipError_t launch_gemm_w_t(const void *Wt, const void *X, void *C, int Mw, int Nx, int K, int d, int L,
+                                  hipStream_t s) {
+    const size_t lds = GwShape<TW>::LDS;
+    auto fn = gemm_w<DT, OUT, TW>;
     (void)hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    hipLaunchKernelGGL(fn, dim3((Mw / GW_W) * (Nx / GW_X)), dim3(GW_T), lds, s, (const uint16_t *)Wt,
+    hipLaunchKernelGGL(fn, dim3((Mw / TW) * (Nx / GW_X)), dim3(GW_T), lds, s, (const uint16_t *)Wt,
                        (const uint16_t *)X, (uint16_t *)C, Mw, Nx, K, d, L);
     return hipGetLastError();
 }
 
-bool gemm_w320_ok(int Mw, int Nx, int K) { return Mw % GW_W == 0 && Nx % GW_X == 0 && K % GW_K == 0; }
+int gemm_w_tile(int Mw, int Nx, int K, int d, int out_mode) {
+    if (Nx % GW_X != 0 || K % GW_K != 0 || K < GW_K) return 0;
+    for (int tw : {320, 256})
+        if (Mw % tw == 0 && (out_mode == 0 || d % tw == 0)) return tw;
+    return 0;
+}
 
-hipError_t launch_gemm_w320(const void *Wt, const void *X, void *C, int Mw, int Nx, int K, int dtype, int out_mode,
-                            int d, int L, hipStream_t s) {
-    if (!gemm_w320_ok(Mw, Nx, K)) return hipErrorInvalidValue;
-    if (dtype == BF16)
-        return out_mode ? launch_w320_t<BF16, 1>(Wt, X, C, Mw, Nx, K, d, L, s)
-                        : launch_w320_t<BF16, 0>(Wt, X, C, Mw, Nx, K, d, L, s);
-    return out_mode ? launch_w320_t<F16, 1>(Wt, X, C, Mw, Nx, K, d, L, s)
-                    : launch_w320_t<F16, 0>(Wt, X, C, Mw, Nx, K, d, L, s);
+template <int DT>
+static hipError_t launch_gemm_w_dt(const void *Wt, const void *X, void *C, int Mw, int Nx, int K, int out_mode,
+                                   int d, int L, int tw, hipStream_t s) {
+    if (tw == 320)
+        return out_mode ? launch_gemm_w_t<DT, 1, 320>(Wt, X, C, Mw, Nx, K, d, L, s)
+                        : launch_gemm_w_t<DT, 0, 320>(Wt, X, C, Mw, Nx, K, d, L, s);
+    return out_mode ? launch_gemm_w_t<DT, 1, 256>(Wt, X, C, Mw, Nx, K, d, L, s)
+                    : launch_gemm_w_t<DT, 0, 256>(Wt, X, C, Mw, Nx, K, d, L, s);
+}
+
+hipError_t launch_gemm_w(const void *Wt, const void *X, void *C, int Mw, int Nx, int K, int dtype, int out_mode,
+                         int d, int L, hipStream_t s) {
+    const int tw = gemm_w_tile(Mw, Nx, K, d, out_mode);
+    if (!tw) return hipErrorInvalidValue;
+    return dtype == BF16 ? launch_gemm_w_dt<BF16>(Wt, X, C, Mw, Nx, K, out_mode, d, L, tw, s)
+                         : launch_gemm_w_dt<F16>(Wt, X, C, Mw, Nx, K, out_mode, d, L, tw, s);
 }
 
 template <int N, int DT>

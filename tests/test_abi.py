@@ -189,7 +189,7 @@ def test_layer_heads_validation():
     assert heads(L=32) == EUNSUP                     # heads need L >= 64
     assert heads(dt=1, d=100) == EUNSUP
     assert heads(ws=0) == EWS
-    assert heads(wsb=1 << 20) == EWS
+    assert heads(wsb=h3.workspace_size(h3.OP_LAYER_HEADS, 2, 128, 64, 64, 2, h3.BF16) - 1) == EWS
     assert heads(out=U) == EINVAL
     assert h3.workspace_size(h3.OP_LAYER_HEADS, 4, 2560, 2048, 64, 8, h3.BF16) > 4 * 2560 * 2048 * 2 * 16
     assert h3.workspace_size(h3.OP_LAYER_HEADS, 4, 2560, 2048, 64, 3, h3.BF16) == 0

@@ -531,12 +531,12 @@ def test_layer_wave_path(h3, dtype, B, L, m_s, with_D):
     check(y, ref, 2e-2)
 
 
-# The library's own matrix-core GEMM (used where hipBLASLt rejects a shape),
-# forced through the documented switch, on both mixing paths.
-@pytest.mark.parametrize("L", [256, 2048])
-def test_layer_native_gemm(h3, monkeypatch, L):
-    monkeypatch.setenv("H3FLASH_GEMM", "native")
-    w = workloads.layer_workload("t", 2, L, 256, workloads.BF16, seed=23 + L)
+# The projections' GEMM paths: 320 x 256 tiles (d a multiple of 320),
+# 256 x 256 tiles (d a multiple of 256), 128 x 128 tiles per projection
+# (otherwise, or B L not a multiple of 256); Q/K/V fused or not.
+@pytest.mark.parametrize("B,L,d", [(2, 256, 256), (1, 128, 256), (2, 256, 384), (1, 1024, 640), (3, 256, 1280)])
+def test_layer_gemm_paths(h3, B, L, d):
+    w = workloads.layer_workload("t", B, L, d, workloads.BF16, seed=23 + L + d)
     y, ref = _layer_case(h3, w)
     check(y, ref, 2e-2)
 
