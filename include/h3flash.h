@@ -224,11 +224,11 @@ int h3_ssm_step(const void *u, const float *Abar, const float *Bbar, const float
  *   L power of two in [H3_MIN_LEN, H3_FUSED_LIMIT]; d a multiple of 128;
  *   B * L a multiple of 128 (the tiles of the library's own GEMM).
  *   workspace >= h3_workspace_size(H3_OP_LAYER, B, d, L, m_s, 0, dtype).
- * The four projections run on the library's own matrix-core GEMM, which reads
- * transposed copies of the weights made in the workspace: Q, K and V in one
- * launch of 320 x 256 tiles when d is a multiple of 320 (256 x 256 when d is
- * a multiple of 256) and B * L of 256, else one 128 x 128-tile launch per
- * projection.
+ * The four projections run on the library's own matrix-core GEMM: when d is
+ * a multiple of 320 (or 256) and B * L of 256 it reads the weights as stored,
+ * Q, K and V in one launch of 320 x 256 (256 x 256) tiles; other shapes take
+ * one 128 x 128-tile launch per projection on transposed copies of the
+ * weights made in the workspace.
  * Errors: EINVAL, EUNSUPPORTED (L, d, B * L, m_s, dtype), EWORKSPACE, EDEVICE.
  */
 int h3_layer_fwd(const void *x, const void *Wq, const void *Wk, const void *Wv,

@@ -84,8 +84,9 @@ StatepassWs statepass_ws(int B, int H, int L, int m, int chunk, int dtype) {
 struct LayerWs {
     size_t qkv, o_cm, o_tm, kspec, wt, total;
 };
-// wt: the four weights transposed to (out, in) (the GEMM reads both operands
-// reduction-contiguous); Q, K, V consecutive, so they form one (3 d, d) operand
+// wt: the four weights transposed to (out, in), only for shapes the
+// weight-tiled GEMM does not take (the 128 x 128-tile GEMM reads both operands
+// reduction-contiguous)
 LayerWs layer_ws(int B, int d, int L) {
     LayerWs w;
     const size_t act = (size_t)B * d * L * 2;
@@ -94,7 +95,7 @@ LayerWs layer_ws(int B, int d, int L) {
     w.o_tm = w.o_cm + align_up(act);
     w.kspec = w.o_tm + align_up(act);
     w.wt = w.kspec + align_up((size_t)d * (L + 1) * sizeof(float2));
-    w.total = w.wt + align_up((size_t)4 * d * d * 2);
+    w.total = w.wt + (gemm_w_tile(d, B * L, d) ? 0 : align_up((size_t)4 * d * d * 2));
     return w;
 }
 
@@ -114,42 +115,38 @@ HeadsWs heads_ws(int B, int d, int L, int dh) {
     w.o_tm = w.sv + align_up((size_t)dh * act);
     w.kspec = w.o_tm + align_up(act);
     w.wt = w.kspec + align_up((size_t)d * dh * (L + 1) * sizeof(float2));
-    w.total = w.wt + align_up((size_t)4 * d * d * 2);
+    w.total = w.wt + (gemm_w_tile(d, B * L, d) ? 0 : align_up((size_t)4 * d * d * 2));
     return w;
 }
 
 // [Q;K;V] channel-major: per projection j and batch b the (d, L) block
-// j B d L + b d L is (x_b W_j)^T = W_j^T (d, d) . x_b (L, d)^T.  The weights
-// come as Algorithm 1 writes them, (in, out) with Q = x W_Q; the GEMM takes
-// both operands reduction-contiguous, so the three are transposed into wt
-// first, where they form one (3 d, d) operand: one launch for Q, K and V
-// where the tiles allow it (d a multiple of 256 or 320, B L of 256), else
-// one 128 x 128-tile launch per projection.
+// j B d L + b d L is (x_b W_j)^T.  The weights come as Algorithm 1 writes
+// them, (in, out) with Q = x W_Q, and the weight-tiled GEMM reads them so:
+// one launch for Q, K and V (d a multiple of 320 or 256, B L of 256).  Other
+// shapes take the 128 x 128-tile GEMM per projection, which reads both
+// operands reduction-contiguous: the weights are transposed into wt first.
 hipError_t layer_qkv(const void *x, const void *Wq, const void *Wk, const void *Wv, char *qkv, int B, int L, int d,
                      int dtype, void *wt, hipStream_t s) {
-    const size_t act = (size_t)B * L * d * 2, wb = (size_t)d * d * 2;
     const void *Wqkv[3] = {Wq, Wk, Wv};
+    if (gemm_w_tile(d, B * L, d)) return launch_gemm_w(Wqkv, x, qkv, B * L, d, dtype, 1, d, L, s);
+    const size_t act = (size_t)B * L * d * 2, wb = (size_t)d * d * 2;
     for (int j = 0; j < 3; ++j) {
-        hipError_t e = launch_transpose_batched(Wqkv[j], (char *)wt + j * wb, 1, d, d, s);
-        if (e != hipSuccess) return e;
-    }
-    if (gemm_w_tile(3 * d, B * L, d, d, 1)) return launch_gemm_w(wt, x, qkv, 3 * d, B * L, d, dtype, 1, d, L, s);
-    for (int j = 0; j < 3; ++j) {
-        hipError_t e = launch_gemm_nt((char *)wt + j * wb, x, qkv + j * act, d, B * L, d, dtype, 1, d, L, s);
+        char *wj = (char *)wt + j * wb;
+        hipError_t e = launch_transpose_batched(Wqkv[j], wj, 1, d, d, s);
+        if (e == hipSuccess) e = launch_gemm_nt(wj, x, qkv + j * act, d, B * L, d, dtype, 1, d, L, s);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
 }
 
-// out = O (B L, d) . Wo (d, d), O token-major; the GEMM reads Wo^T
-// (transposed into the fourth slot of wt)
+// out = O (B L, d) . Wo (d, d), O token-major
 hipError_t layer_out(const void *o_tm, const void *Wo, void *out, int B, int L, int d, int dtype, void *wt,
                      hipStream_t s) {
+    if (gemm_w_tile(d, B * L, d)) return launch_gemm_w(&Wo, o_tm, out, B * L, d, dtype, 0, d, L, s);
     char *wo = (char *)wt + 3 * (size_t)d * d * 2;
     hipError_t e = launch_transpose_batched(Wo, wo, 1, d, d, s);
     if (e != hipSuccess) return e;
-    return gemm_w_tile(d, B * L, d, d, 0) ? launch_gemm_w(wo, o_tm, out, d, B * L, d, dtype, 0, d, L, s)
-                                          : launch_gemm_nt(o_tm, wo, out, B * L, d, d, dtype, 0, d, L, s);
+    return launch_gemm_nt(o_tm, wo, out, B * L, d, d, dtype, 0, d, L, s);
 }
 
 }  // namespace

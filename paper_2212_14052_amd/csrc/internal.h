@@ -131,15 +131,15 @@ hipError_t launch_heads_expand(int dh, const void *kbar, const void *v, void *g,
                                hipStream_t s);
 hipError_t launch_heads_contract(int dh, const void *q, const void *sv, void *o, int B, int d, int L, int dtype,
                                  hipStream_t s);
-// C = Wt . X^T on TW x 256 tiles, TW = 320 or 256 (Wt: (Mw, K) weight side,
-// X: (Nx, K) activations, both K-contiguous); out_mode 1: channel-major
-// [Q;K;V] layout as launch_gemm_nt, out_mode 0: row-major (Nx, Mw).
-// gemm_w_tile gives the tile height for a shape (0: not supported: needs
-// Nx % 256 == 0, K % 32 == 0 and Mw, and for out_mode 1 also d, a multiple of
-// TW).
-int gemm_w_tile(int Mw, int Nx, int K, int d, int out_mode);
-hipError_t launch_gemm_w(const void *Wt, const void *X, void *C, int Mw, int Nx, int K, int dtype, int out_mode,
-                         int d, int L, hipStream_t s);
+// The layer's projections on TW x 256 tiles (TW = 320 or 256) with the
+// weights as stored, (K, d) row-major (Q = x W): out_mode 1: W[0..2] = W_Q,
+// W_K, W_V into the channel-major [Q;K;V] layout as launch_gemm_nt
+// (out_mode 1); out_mode 0: W[0] = W_O, C = X W_O row-major (Nx, d).  X is
+// (Nx, K) row-major.  gemm_w_tile gives the tile height (0: not supported:
+// needs Nx % 256 == 0, K % 32 == 0, d a multiple of 320 or 256).
+int gemm_w_tile(int d, int Nx, int K);
+hipError_t launch_gemm_w(const void *const *W, const void *X, void *C, int Nx, int K, int dtype, int out_mode, int d,
+                         int L, hipStream_t s);
 hipError_t launch_gemm_nt(const void *A, const void *Bt, void *C, int M, int N, int K, int dtype,
                           int out_mode, int d, int L, hipStream_t s);
 hipError_t launch_layer_mid(const void *q, const void *k, const void *v, const float *shift_C,

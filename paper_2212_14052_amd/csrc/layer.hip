@@ -228,47 +228,62 @@ __global__ __launch_bounds__(G2_T) void gemm_nt_256(const uint16_t *A, const uin
 }
 
 // ------------------------------------------- GEMM, TW x 256 weight tiles ---
-// C = Wt . X^T with Wt (Mw, K) the weight side and X (Nx, K) the activation
-// side, both K-contiguous 16-bit, fp32 accumulation.  Block tile TW (weight
-// rows: 320 or 256) x 256 (activation rows) x 32.  At d = 2560 (a multiple
-// of 320) the fused Q/K/V projection (Mw = 3 d) and the output projection
-// (Mw = d) over Nx = B L = 8192 tokens are 768 and 256 tiles of 320 x 256:
+// C = W^T . X^T with the weights W (K, ldw) as stored (input features along
+// the rows, output features contiguous: the projections of Algorithm 1 as
+// written, Q = x W_Q) and the activations X (Nx, K) K-contiguous, 16-bit, fp32
+// accumulation.  Mw output features: for OUT 1 the three projections Q, K, V
+// (Mw = 3 d, weight tile rows w0 .. from W_{w0 / d}), for OUT 0 one (Mw = d).
+// Block tile TW (output features: 320 or 256) x 256 (activation rows) x 32.
+// At d = 2560 (a multiple of 320) the fused Q/K/V projection and the output
+// projection over Nx = B L = 8192 tokens are 768 and 256 tiles of 320 x 256:
 // whole rounds of the 256 CUs, where 256 x 256 tiles leave the last round a
-// quarter full.  Eight waves, 2 (weight) x 4 (activation), each (TW / 2) x
-// 64 = (TW / 64) x 2 tiles of 32x32x16 MFMA (up to 160 fp32 accumulators per
+// quarter full.  Eight waves, 2 (weight) x 4 (activation), each (TW / 2) x 64
+// = (TW / 64) x 2 tiles of 32x32x16 MFMA (up to 160 fp32 accumulators per
 // lane, two waves per SIMD).
 // Operands reach LDS without passing through registers: each wave copies
-// 16-row slices (1 KB, 64 lanes x 16 bytes, lane i to byte 16 i of the slice)
-// with global_load_lds_dwordx4, four stages deep (copies run three K steps
-// ahead; a stage is waited for with vmcnt and one barrier per K step, which
-// also orders the refill of the buffer read in the step before).  A stage is
-// TW + 256 rows (weight rows, then activation rows) of 32 values (64 B, four
-// 16-byte chunks), chunk c of row r at slot c ^ ((r / 4) % 4): a fragment
-// read serves 16 lanes (16 consecutive rows, one chunk) per LDS cycle, and
-// those land on 16 distinct 16-byte bank groups of the 256-byte bank row.
-// Lane i of a slice thus fetches chunk (i % 4) ^ ((r / 4) % 4) of row
-// r = 16 q + i / 4.
-// OUT 1: element (m, n) = (weight row, activation row) goes to the
-//        channel-major [Q;K;V] layout [(m / d)][(n / L)][(m % d)][(n % L)]
+// 1 KB slices of a stage (64 lanes x 16 bytes, lane i to byte 16 i of the
+// slice) with global_load_lds_dwordx4, four stages deep (copies run three K
+// steps ahead; a stage is waited for with vmcnt and one barrier per K step,
+// which also orders the refill of the buffer read in the step before).
+// A stage holds
+//  - the weight tile as stored: 32 rows (k) of TW output features, row pitch
+//    WP = 2 TW + 64 bytes (the last 64 bytes of a row are filled with
+//    unused data).  A fragment (8 consecutive k of one output feature per
+//    lane) is read with two transposing LDS reads (ds_read_b64_tr_b16: in a
+//    group of 16 lanes, lane 4 i + q reads 4 features f0 + 4 q .. + 3 of row
+//    k0 + i, and lane j receives rows k0 .. k0 + 3 of feature f0 + j).  With
+//    WP = 64 or 192 (mod 256) the four rows of a read sit at distinct 64-byte
+//    positions of the 256-byte bank row: no bank conflicts;
+//  - the activation tile: 256 rows of 32 values (64 B, four 16-byte chunks),
+//    chunk c of row r at slot c ^ ((r / 4) % 4), read with ds_read_b128 (16
+//    consecutive rows, one chunk, per LDS cycle on 16 distinct bank groups).
+// OUT 1: element (m, n) = (output feature of Q|K|V, activation row) goes to
+//        the channel-major [Q;K;V] layout [(m / d)][(n / L)][(m % d)][(n % L)]
 //        (d a multiple of TW: a tile lies in one projection), with the
 //        activation rows along the MFMA columns (lanes), so 32 consecutive
 //        tokens of one channel are one 64-byte run;
-// OUT 0: element (n, m) of a row-major (Nx, Mw) result, with the weight
-//        rows along the MFMA columns (lanes) for 64-byte runs of channels.
+// OUT 0: element (n, m) of a row-major (Nx, Mw) result, with the output
+//        features along the MFMA columns (lanes) for 64-byte runs.
 constexpr int GW_X = 256, GW_K = 32, GW_T = 512, GW_NS = 4;
 
 typedef __attribute__((address_space(3))) void lds_void;
+typedef short gw_v4s __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) gw_v4s lds_v4s;
 
-__device__ __forceinline__ int gw_off(int row, int chunk) { return row * GW_K + ((chunk ^ ((row >> 2) & 3)) << 3); }
+__device__ __forceinline__ int gw_xoff(int row, int chunk) { return row * 64 + ((chunk ^ ((row >> 2) & 3)) << 4); }
 
 template <int TW, int SS> struct GwShape {
-    static constexpr int ROWS = TW + GW_X;          // rows per stage
-    static constexpr int SLICES = ROWS / 16;        // 1 KB slices per stage (36 or 32)
-    static constexpr int NSL = (SLICES + 7) / 8;    // copies per wave per step (5 or 4)
-    static constexpr int STAGE_B = ROWS * GW_K * 2; // bytes per stage
-    static constexpr int TI = TW / 64;              // weight-side MFMA tiles per wave
+    static constexpr int WP = 2 * TW + 64;            // weight row pitch, bytes (704 or 576)
+    static constexpr int WB = GW_K * WP;              // weight part of a stage, bytes
+    static constexpr int WS = WB / 1024;              // its slices (22 or 18)
+    static constexpr int XS = GW_X * 64 / 1024;       // activation slices (16)
+    static constexpr int SLICES = WS + XS;
+    static constexpr int NSL = (SLICES + 7) / 8;      // copies per wave per step (5)
+    static constexpr int STAGE_B = WB + GW_X * 64;    // bytes per stage
+    static constexpr int TI = TW / 64;                // weight-side MFMA tiles per wave
+    static_assert(WB % 1024 == 0 && (WP % 256 == 64 || WP % 256 == 192), "weight stage layout");
     // LDS bytes: the stages, and a 1 KB slot that takes the copies of waves
-    // with one slice less (never read), so every wave issues NSL per step
+    // with fewer slices (never read), so every wave issues NSL per step
     static constexpr size_t LDS = (size_t)GW_NS * STAGE_B + (SLICES % 8 ? 1024 : 0);
     // SS stages are consumed per barrier (one super-step); the copies of the
     // next GW_NS / SS - 1 super-steps are in flight meanwhile.  s_waitcnt
@@ -280,26 +295,36 @@ template <int TW, int SS> struct GwShape {
 
 template <int DT, int OUT, int TW, int SS>
 __global__ __launch_bounds__(GW_T) __attribute__((amdgpu_waves_per_eu(2, 2))) void gemm_w(
-    const uint16_t *Wt, const uint16_t *X, uint16_t *C, int Mw, int Nx, int K, int d, int L) {
+    const uint16_t *W0, const uint16_t *W1, const uint16_t *W2, const uint16_t *X, uint16_t *C, int Mw, int Nx,
+    int K, int ldw, int d, int L) {
     using S = GwShape<TW, SS>;
-    extern __shared__ __attribute__((aligned(1024))) uint16_t gw_lds[];   // [GW_NS][TW + 256][32], swizzled
+    extern __shared__ __attribute__((aligned(1024))) uint16_t gw_lds[];
     int tw, tx;
     gemm_tile(Mw / TW, Nx / GW_X, tw, tx);
     const int w0 = tw * TW, x0 = tx * GW_X;
+    const int jq = OUT == 1 ? w0 / d : 0;   // the projection this tile row belongs to
+    const uint16_t *Wj = jq == 0 ? W0 : (jq == 1 ? W1 : W2);
+    const int wc = w0 - jq * d;             // first output feature of the tile within W_jq
     const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
     const int ww = wv >> 2, wx = wv & 3;
     // this wave's slices q = wv + 8 s, s < NSL (a wave past the last slice
-    // copies slice wv again into the never-read slot): the lane's source row
-    // and chunk as an element offset from the operand's base (Wt for weight
-    // rows, X after)
+    // copies slice wv again into the never-read slot): the lane's source as an
+    // element offset from the operand's base (W_jq for q < WS, X after) at
+    // K step 0; a step adds 32 rows of W (32 ldw) or 32 columns of X
     const int wvu = __builtin_amdgcn_readfirstlane(wv);   // the wave index, in a scalar register
     uint32_t soff[S::NSL];
 #pragma unroll
     for (int sl = 0; sl < S::NSL; ++sl) {
         const int q = wvu + 8 * sl < S::SLICES ? wvu + 8 * sl : wvu;
-        const int r = 16 * q + (lane >> 2);
-        const int c = (lane & 3) ^ ((r >> 2) & 3);
-        soff[sl] = r < TW ? (uint32_t)((w0 + r) * K + 8 * c) : (uint32_t)((x0 + r - TW) * K + 8 * c);
+        if (q < S::WS) {
+            const int b = 1024 * q + 16 * lane;
+            const int r = b / S::WP, c = b % S::WP;
+            soff[sl] = (uint32_t)(r * ldw + wc + (c < 2 * TW ? c / 2 : 0));
+        } else {
+            const int r = 16 * (q - S::WS) + (lane >> 2);
+            const int c = (lane & 3) ^ ((r >> 2) & 3);
+            soff[sl] = (uint32_t)((x0 + r) * K + 8 * c);
+        }
     }
     const int nk = K / GW_K;
     // The copies are issued as inline assembly (M0 = the slice's LDS byte
@@ -316,8 +341,9 @@ __global__ __launch_bounds__(GW_T) __attribute__((amdgpu_waves_per_eu(2, 2))) vo
         for (int sl = 0; sl < S::NSL; ++sl) {
             const int q = wvu + 8 * sl;
             const bool real = q < S::SLICES;
-            const uint16_t *base = (real ? q : wvu) < TW / 16 ? Wt : X;
-            const uint32_t vo = 2 * (soff[sl] + k0);
+            const bool wside = (real ? q : wvu) < S::WS;
+            const uint16_t *base = wside ? Wj : X;
+            const uint32_t vo = 2 * (soff[sl] + k0 * (wside ? (uint32_t)ldw : 1u));
             const uint32_t la = real ? st + (uint32_t)q * 1024 : lds0 + (uint32_t)(GW_NS * S::STAGE_B);
             asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, %2"
                          :
@@ -333,6 +359,11 @@ __global__ __launch_bounds__(GW_T) __attribute__((amdgpu_waves_per_eu(2, 2))) vo
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
+    // transposing weight reads: lane 4 i + q of each 16-lane group reads row
+    // k0 + i, features f0 + 4 q .. + 3; f0 = the tile's first feature + 16
+    // for the upper 16 lanes of each 32
+    const int tr_row = (lane & 15) >> 2, tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+    const int tr_base = tr_row * S::WP + 2 * (ww * (TW / 2) + tr_col);
 #pragma unroll
     for (int p = 0; p < GW_NS - SS; ++p) issue(p);
     for (int k0 = 0; k0 < nk; k0 += SS) {
@@ -347,17 +378,24 @@ __global__ __launch_bounds__(GW_T) __attribute__((amdgpu_waves_per_eu(2, 2))) vo
 #pragma unroll
         for (int p = 0; p < SS; ++p) {
             const int kt = k0 + p;   // nk is a multiple of SS
-            const uint16_t *ws = gw_lds + (kt % GW_NS) * (S::STAGE_B / 2), *xs = ws + TW * GW_K;
+            const char *stg = (const char *)gw_lds + (kt % GW_NS) * S::STAGE_B;
+            const char *xs = stg + S::WB;
 #pragma unroll
             for (int ks = 0; ks < GW_K / 16; ++ks) {
-                const int ch = 2 * ks + (lane >> 5);
                 uint4 fw[S::TI], fx[2];
+                // weight rows 16 ks + 8 (lane / 32) + 4 h + (0..3)
+                const char *wr = stg + (16 * ks + 8 * (lane >> 5)) * S::WP + tr_base;
 #pragma unroll
-                for (int i = 0; i < S::TI; ++i)
-                    fw[i] = *(const uint4 *)(ws + gw_off(ww * (TW / 2) + i * 32 + (lane & 31), ch));
+                for (int i = 0; i < S::TI; ++i) {
+                    const gw_v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s *)(wr + 64 * i));
+                    const gw_v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s *)(wr + 4 * S::WP + 64 * i));
+                    const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
+                    fw[i] = make_uint4(l2.x, l2.y, h2.x, h2.y);
+                }
+                const int ch = 2 * ks + (lane >> 5);
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
-                    fx[j] = *(const uint4 *)(xs + gw_off(wx * 64 + j * 32 + (lane & 31), ch));
+                    fx[j] = *(const uint4 *)(xs + gw_xoff(wx * 64 + j * 32 + (lane & 31), ch));
 #pragma unroll
                 for (int i = 0; i < S::TI; ++i)
 #pragma unroll
@@ -372,7 +410,6 @@ __global__ __launch_bounds__(GW_T) __attribute__((amdgpu_waves_per_eu(2, 2))) vo
     // epilogue: the lane holds MFMA column (lane & 31) and rows 8 (e / 4) +
     // 4 (lane / 32) + e % 4; element e of a tile lands at base + rstride x
     // (8 (e / 4) + e % 4)
-    const int jq = w0 / d;   // OUT 1: the projection this tile row belongs to
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
         const int nx = x0 + wx * 64 + j * 32;
@@ -857,40 +894,42 @@ hipError_t launch_gemm_nt(const void *A, const void *Bt, void *C, int M, int N, 
 // super-step of prefetch instead of three stages) measured 6 % slower at
 // d = 2560, B L = 8192.
 template <int DT, int OUT, int TW>
-static hipError_t launch_gemm_w_t(const void *Wt, const void *X, void *C, int Mw, int Nx, int K, int d, int L,
-                                  hipStream_t s) {
+static hipError_t launch_gemm_w_t(const void *const *W, const void *X, void *C, int Mw, int Nx, int K, int ldw, int d,
+                                  int L, hipStream_t s) {
     constexpr int SS = 1;
     const size_t lds = GwShape<TW, SS>::LDS;
     auto fn = gemm_w<DT, OUT, TW, SS>;
     (void)hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    hipLaunchKernelGGL(fn, dim3((Mw / TW) * (Nx / GW_X)), dim3(GW_T), lds, s, (const uint16_t *)Wt,
-                       (const uint16_t *)X, (uint16_t *)C, Mw, Nx, K, d, L);
+    hipLaunchKernelGGL(fn, dim3((Mw / TW) * (Nx / GW_X)), dim3(GW_T), lds, s, (const uint16_t *)W[0],
+                       (const uint16_t *)W[OUT ? 1 : 0], (const uint16_t *)W[OUT ? 2 : 0], (const uint16_t *)X,
+                       (uint16_t *)C, Mw, Nx, K, ldw, d, L);
     return hipGetLastError();
 }
 
-int gemm_w_tile(int Mw, int Nx, int K, int d, int out_mode) {
+int gemm_w_tile(int d, int Nx, int K) {
     if (Nx % GW_X != 0 || K % GW_K != 0) return 0;
     for (int tw : {320, 256})
-        if (Mw % tw == 0 && (out_mode == 0 || d % tw == 0)) return tw;
+        if (d % tw == 0) return tw;
     return 0;
 }
 
 template <int DT>
-static hipError_t launch_gemm_w_dt(const void *Wt, const void *X, void *C, int Mw, int Nx, int K, int out_mode,
-                                   int d, int L, int tw, hipStream_t s) {
+static hipError_t launch_gemm_w_dt(const void *const *W, const void *X, void *C, int Mw, int Nx, int K, int ldw,
+                                   int out_mode, int d, int L, int tw, hipStream_t s) {
     if (tw == 320)
-        return out_mode ? launch_gemm_w_t<DT, 1, 320>(Wt, X, C, Mw, Nx, K, d, L, s)
-                        : launch_gemm_w_t<DT, 0, 320>(Wt, X, C, Mw, Nx, K, d, L, s);
-    return out_mode ? launch_gemm_w_t<DT, 1, 256>(Wt, X, C, Mw, Nx, K, d, L, s)
-                    : launch_gemm_w_t<DT, 0, 256>(Wt, X, C, Mw, Nx, K, d, L, s);
+        return out_mode ? launch_gemm_w_t<DT, 1, 320>(W, X, C, Mw, Nx, K, ldw, d, L, s)
+                        : launch_gemm_w_t<DT, 0, 320>(W, X, C, Mw, Nx, K, ldw, d, L, s);
+    return out_mode ? launch_gemm_w_t<DT, 1, 256>(W, X, C, Mw, Nx, K, ldw, d, L, s)
+                    : launch_gemm_w_t<DT, 0, 256>(W, X, C, Mw, Nx, K, ldw, d, L, s);
 }
 
-hipError_t launch_gemm_w(const void *Wt, const void *X, void *C, int Mw, int Nx, int K, int dtype, int out_mode,
-                         int d, int L, hipStream_t s) {
-    const int tw = gemm_w_tile(Mw, Nx, K, d, out_mode);
+hipError_t launch_gemm_w(const void *const *W, const void *X, void *C, int Nx, int K, int dtype, int out_mode, int d,
+                         int L, hipStream_t s) {
+    const int tw = gemm_w_tile(d, Nx, K);
     if (!tw) return hipErrorInvalidValue;
-    return dtype == BF16 ? launch_gemm_w_dt<BF16>(Wt, X, C, Mw, Nx, K, out_mode, d, L, tw, s)
-                         : launch_gemm_w_dt<F16>(Wt, X, C, Mw, Nx, K, out_mode, d, L, tw, s);
+    const int Mw = out_mode ? 3 * d : d;
+    return dtype == BF16 ? launch_gemm_w_dt<BF16>(W, X, C, Mw, Nx, K, d, out_mode, d, L, tw, s)
+                         : launch_gemm_w_dt<F16>(W, X, C, Mw, Nx, K, d, out_mode, d, L, tw, s);
 }
 
 template <int N, int DT>
