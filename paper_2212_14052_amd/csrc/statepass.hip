@@ -99,7 +99,17 @@ __global__ __launch_bounds__(CS_THREADS) void chunk_states_kernel(const void *u_
 // work.
 // Workgroup: one channel and a set of its chunk rows; wave w owns modes
 // 16 w .. 16 w + 15 (row tile w of the real parts, w + 4 of the imaginary).
-// The chunk row is staged once in LDS (16-byte coalesced) for all four waves.
+// Chunk rows reach LDS without passing through registers: the four waves copy
+// 1 KB slices of a row (64 lanes x 16 bytes, lane i to byte 16 i of the
+// slice) with global_load_lds_dwordx4 into two row buffers, one row ahead of
+// the row being reduced (a three-row ring measured slower at chunk 8192, 187
+// against 149 us: it leaves room for three workgroups per CU instead of
+// four).  A row is staged as N'/BW LDS rows of
+// BW inputs (2 BW bytes, 16-byte chunks), chunk c of LDS row a at slot
+// c ^ ((a / (256 / 2 BW)) % (2 BW / 16)), so the 16 lanes of an operand read
+// (16 consecutive rows a, one chunk) hit 16 distinct 16-byte bank groups.
+// Each row's 64 end-state sums go to LDS; wave 0 stores them after the next
+// barrier.
 typedef _Float16 sp_h8 __attribute__((ext_vector_type(8)));
 typedef __bf16 sp_b8 __attribute__((ext_vector_type(8)));
 typedef float sp_f4 __attribute__((ext_vector_type(4)));
@@ -142,21 +152,26 @@ __device__ __forceinline__ uint32_t sp_pack(float lo, float hi) {
 }
 
 constexpr int SPM_CHUNK = 16384;   // largest chunk of the matrix-core form
+constexpr int CS_NS = 2;   // row buffers in the copy ring
 
-// CMAX: the largest chunk an instance handles; it sizes the two LDS row
-// buffers (2 CMAX (1 + 8 / BW) 16-bit values: 34.8 KB at 8192, 69.6 KB at
-// 16384), so chunks up to 8192 keep the smaller instance and its occupancy.
+typedef __attribute__((address_space(3))) void cs_lds_t;
+
+// LDS bytes for a chunk: the row ring, the results [2][64] float2 and a 1 KB
+// slot for the copies of waves with one slice less
+size_t chunk_states_lds(int chunk) { return (size_t)CS_NS * chunk * 2 + 2 * 64 * 8 + 1024; }
+
 template <int DT, int BW, int CMAX>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void chunk_states_mfma(const uint16_t *u, const float *Abar,
-                                                         const float *Bbar, int B, int H, int L,
-                                                         int m, int chunk, int wg_per_ch,
-                                                         float2 *states) {
-    constexpr int KS = BW / 32;                 // 32-wide reduction steps per block
-    constexpr int LD = BW + 8;                  // LDS row pitch (8 pad: 16 rows' 16-byte reads hit distinct banks)
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void chunk_states_mfma(
+    const uint16_t *u, const float *Abar, const float *Bbar, int B, int H, int L, int m, int chunk, int wg_per_ch,
+    float2 *states) {
+    constexpr int KS = BW / 32;          // 32-wide reduction steps per block
+    constexpr int RB = 2 * BW;           // bytes per LDS row
+    constexpr int SPR = RB / 16;         // 16-byte slots per LDS row
+    constexpr int RPB = 256 / RB;        // LDS rows per 256-byte bank row
     constexpr int NA_MAX = CMAX / BW;
-    constexpr int NPF = CMAX / 8 / 256;         // 16-byte pieces of a row per thread
-    __shared__ __attribute__((aligned(16))) uint16_t us[2][NA_MAX * LD];
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    extern __shared__ __attribute__((aligned(1024))) char cs_lds[];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // the wave index, in a scalar register
     const int r16 = lane & 15, kg = lane >> 4;
     const int h = blockIdx.x / wg_per_ch, part = blockIdx.x % wg_per_ch;
     const int nchunk = L / chunk;
@@ -165,6 +180,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void c
     const int rows_per_ch = B * nchunk;
     const int per = (rows_per_ch + wg_per_ch - 1) / wg_per_ch;
     const int r0 = part * per, r1 = min(r0 + per, rows_per_ch);
+    if (r0 >= r1) return;   // uniform over the workgroup
+    const int row_b = chunk * 2;                 // bytes of a staged row
+    float2 *res = (float2 *)(cs_lds + CS_NS * row_b);   // [2][64]
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(cs_lds_t *)cs_lds;
+    const uint32_t dummy = lds0 + (uint32_t)(CS_NS * row_b + 2 * 64 * 8);
 
     // A operand (powers, 16-bit): rows n = 16 w + r16, reduction b = 32 ks + 8 kg + i
     uint4 Are[KS], Aim[KS];
@@ -209,46 +229,66 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void c
         Zstep[j] = make_float2((float)zstep.x, (float)zstep.y);
     }
 
-    // A chunk row is chunk / 8 <= 256 NPF 16-byte pieces: piece i = tid + 256 q,
-    // q < NPF, loaded one row ahead into registers (so the loads overlap a
-    // whole row's compute) and stored into the other LDS buffer after it.
-    const int npiece = chunk / 8;
-    uint4 pf[NPF];
-    auto load_row = [&](int rr) {
+    // this wave's slices q = w + 4 s of a staged row (s < nsl; waves past the
+    // last slice copy slice w again into the never-read slot): the lane's
+    // source element within the chunk row
+    const int slices = row_b / 1024;             // chunk % 512 == 0
+    const int nsl = (slices + 3) / 4;            // copies per wave per row (1..8)
+    auto src_elem = [&](int q) {
+        const int b = 1024 * q + 16 * lane;
+        const int a = b / RB, slot = (b % RB) / 16;
+        const int c = slot ^ ((a / RPB) % SPR);
+        return BW * a + 8 * c;
+    };
+    // copies of chunk row rr (clamped to the last: past it they only keep the
+    // count per row fixed) into buffer (rr - r0) % CS_NS
+    auto issue = [&](int rr) {
+        const int rc = min(rr, r1 - 1);
+        const int bb = rc / nchunk, cc = rc % nchunk;
+        // the row's address and the buffer, in scalar registers (wave-uniform)
+        const uint64_t sp = (uint64_t)(uintptr_t)(u + ((long)bb * H + h) * L + (long)cc * chunk);
+        const uint64_t spu = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(sp >> 32)) << 32) |
+                             (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)sp);
+        const uint16_t *src = (const uint16_t *)(uintptr_t)spu;
+        const uint32_t st = lds0 + (uint32_t)(((rr - r0) % CS_NS) * row_b);
+        for (int sl = 0; sl < nsl; ++sl) {
+            const int q = w + 4 * sl;
+            const bool real = q < slices;
+            const uint32_t vo = 2u * (uint32_t)src_elem(real ? q : w);
+            const uint32_t la = __builtin_amdgcn_readfirstlane(real ? st + (uint32_t)q * 1024 : dummy);
+            asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, %2"
+                         :
+                         : "v"(vo), "s"(la), "s"(src)
+                         : "memory", "m0");
+        }
+    };
+    auto store_row = [&](int rr) {   // wave 0: the 64 sums of row rr from res[(rr - r0) & 1]
         const int bb = rr / nchunk, cc = rr % nchunk;
-        const uint16_t *src = u + ((long)bb * H + h) * L + (long)cc * chunk;
-#pragma unroll
-        for (int q = 0; q < NPF; ++q) {
-            const int i = tid + 256 * q;
-            pf[q] = i < npiece ? *(const uint4 *)(src + 8 * i) : make_uint4(0, 0, 0, 0);
-        }
+        const long crow = ((long)bb * H + h) * nchunk + cc;
+        if (lane < m) states[crow * m + lane] = res[((rr - r0) & 1) * 64 + lane];
     };
-    auto store_row = [&](int buf) {
-#pragma unroll
-        for (int q = 0; q < NPF; ++q) {
-            const int i = tid + 256 * q;
-            // row a = i / (BW / 8) (BW elements) padded by 8 elements to spread banks
-            if (i < npiece) *(uint4 *)&us[buf][(i / (BW / 8)) * LD + 8 * (i % (BW / 8))] = pf[q];
-        }
-    };
-    if (r0 < r1) {
-        load_row(r0);
-        store_row(0);
-    }
-    if (r0 + 1 < r1) load_row(r0 + 1);
-    __syncthreads();
+
+    issue(r0);
     for (int rr = r0; rr < r1; ++rr) {
-        const int buf = (rr - r0) & 1;
+        // this row's copies landed for this wave, then for every wave; the
+        // reads of the buffer refilled below (the previous row's) are done
+        __builtin_amdgcn_s_waitcnt(0xf70);   // vmcnt(0)
+        asm volatile("s_barrier" ::: "memory");
+        if (w == 0 && rr > r0) store_row(rr - 1);
+        issue(rr + 1);
+        const char *us = cs_lds + ((rr - r0) % CS_NS) * row_b;
         sp_f4 sre = {0.f, 0.f, 0.f, 0.f}, sim = {0.f, 0.f, 0.f, 0.f};
         float2 E[4] = {E0[0], E0[1], E0[2], E0[3]};
 #pragma unroll
         for (int ct = NA_MAX / 16 - 1; ct >= 0; --ct) {
             if (ct < NCT) {
                 sp_f4 accr = {0.f, 0.f, 0.f, 0.f}, acci = {0.f, 0.f, 0.f, 0.f};
+                const int a = 16 * ct + r16;
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks) {
-                    // B operand: column a = 16 ct + r16, reduction b = 32 ks + 8 kg .. + 7
-                    const uint4 bv = *(const uint4 *)&us[buf][(16 * ct + r16) * LD + 32 * ks + 8 * kg];
+                    // B operand: column a, reduction b = 32 ks + 8 kg .. + 7 (16-byte chunk 4 ks + kg)
+                    const int c = 4 * ks + kg;
+                    const uint4 bv = *(const uint4 *)(us + a * RB + 16 * (c ^ ((a / RPB) % SPR)));
                     accr = sp_mfma<DT>(Are[ks], bv, accr);
                     acci = sp_mfma<DT>(Aim[ks], bv, acci);
                 }
@@ -270,19 +310,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void c
                 sim[j] += __shfl_xor(sim[j], o);
             }
         if (r16 == 0) {
-            const int bb = rr / nchunk, cc = rr % nchunk;
-            const long crow = ((long)bb * H + h) * nchunk + cc;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int n = 16 * w + 4 * kg + j;
-                if (n < m) states[crow * m + n] = cmul(Bb[j], make_float2(sre[j], sim[j]));
-            }
+            for (int j = 0; j < 4; ++j)
+                res[((rr - r0) & 1) * 64 + 16 * w + 4 * kg + j] = cmul(Bb[j], make_float2(sre[j], sim[j]));
         }
-        // the other buffer was last read before the previous barrier
-        if (rr + 1 < r1) store_row(buf ^ 1);
-        if (rr + 2 < r1) load_row(rr + 2);
-        __syncthreads();
     }
+    __syncthreads();   // the last row's sums are in LDS; every copy has landed
+    if (w == 0) store_row(r1 - 1);
 }
 
 bool chunk_states_mfma_ok(int chunk, int dtype) {
@@ -292,27 +326,52 @@ bool chunk_states_mfma_ok(int chunk, int dtype) {
 hipError_t launch_chunk_states_mfma(const void *u, const float *Abar, const float *Bbar, int B, int H,
                                     int L, int m, int chunk, int dtype, float2 *states, hipStream_t s) {
     const int rows_per_ch = B * (L / chunk);
-    int wg = 1;
-    while (H * wg < 1024 && rows_per_ch / (2 * wg) >= 4) wg *= 2;
-    dim3 grid(H * wg), block(256);
     const uint16_t *u16 = (const uint16_t *)u;
     const bool wide = chunk % 2048 == 0;   // 128-wide blocks need 16 columns per tile: chunk / 128 % 16 == 0
     const bool big = chunk > 8192;         // multiple of 2048 here, so wide
+    const size_t lds = chunk_states_lds(chunk);
+    // Workgroups per channel: a workgroup walks its rows one after another,
+    // the grid runs in ceil(workgroups / resident) rounds.  Take the count in
+    // 1..8 (at least 4 rows each where the channel has them) that minimises
+    // rounds x (rows per workgroup + 1), the 1 standing for a workgroup's
+    // set-up (its power tables in float64).
+    auto pick_wg = [&](const void *fn) {
+        int per_cu = 0, dev = 0, cus = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 256, lds) != hipSuccess || per_cu < 1) per_cu = 1;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+            cus = 1;
+        const long resident = (long)per_cu * cus;
+        int best = 1;
+        long best_cost = -1;
+        for (int w = 1; w <= 8; ++w) {
+            if (w > 1 && rows_per_ch < 4 * w) break;
+            const long rounds = ((long)H * w + resident - 1) / resident;
+            const long cost = rounds * ((rows_per_ch + w - 1) / w + 1);
+            if (best_cost < 0 || cost < best_cost) {
+                best_cost = cost;
+                best = w;
+            }
+        }
+        return best;
+    };
+#define H3_CS_LAUNCH(DTV, BWV, CMV)                                                                              \
+    do {                                                                                                         \
+        auto fn = chunk_states_mfma<DTV, BWV, CMV>;                                                              \
+        (void)hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);      \
+        const int wg = pick_wg((const void *)fn);                                                                \
+        hipLaunchKernelGGL(fn, dim3(H * wg), dim3(256), lds, s, u16, Abar, Bbar, B, H, L, m, chunk, wg, states); \
+    } while (0)
     if (dtype == BF16) {
-        if (big)
-            hipLaunchKernelGGL((chunk_states_mfma<BF16, 128, 16384>), grid, block, 0, s, u16, Abar, Bbar, B, H, L, m, chunk, wg, states);
-        else if (wide)
-            hipLaunchKernelGGL((chunk_states_mfma<BF16, 128, 8192>), grid, block, 0, s, u16, Abar, Bbar, B, H, L, m, chunk, wg, states);
-        else
-            hipLaunchKernelGGL((chunk_states_mfma<BF16, 64, 8192>), grid, block, 0, s, u16, Abar, Bbar, B, H, L, m, chunk, wg, states);
+        if (big) H3_CS_LAUNCH(BF16, 128, 16384);
+        else if (wide) H3_CS_LAUNCH(BF16, 128, 8192);
+        else H3_CS_LAUNCH(BF16, 64, 8192);
     } else {
-        if (big)
-            hipLaunchKernelGGL((chunk_states_mfma<F16, 128, 16384>), grid, block, 0, s, u16, Abar, Bbar, B, H, L, m, chunk, wg, states);
-        else if (wide)
-            hipLaunchKernelGGL((chunk_states_mfma<F16, 128, 8192>), grid, block, 0, s, u16, Abar, Bbar, B, H, L, m, chunk, wg, states);
-        else
-            hipLaunchKernelGGL((chunk_states_mfma<F16, 64, 8192>), grid, block, 0, s, u16, Abar, Bbar, B, H, L, m, chunk, wg, states);
+        if (big) H3_CS_LAUNCH(F16, 128, 16384);
+        else if (wide) H3_CS_LAUNCH(F16, 128, 8192);
+        else H3_CS_LAUNCH(F16, 64, 8192);
     }
+#undef H3_CS_LAUNCH
     return hipGetLastError();
 }
 
