@@ -33,6 +33,9 @@ EXTRA = {
     # with the VALU, so AGPR destinations only add copies
     "fftconv_wave.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
     "fftconv_wave16k.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+    # its compile-time twiddle tables need more constexpr evaluation steps
+    # than clang's default allows
+    "fftconv_wave32k.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1", "-fconstexpr-steps=100000000"],
 }
 
 

@@ -49,30 +49,6 @@ constexpr int NW = 4;           // waves per workgroup (one per frequency block)
 constexpr int NT = 64 * NW;
 constexpr int kU = 2048;        // uint4: input staging / last-layer exchange (32 KB)
 
-typedef __bf16 bf8_t __attribute__((ext_vector_type(8)));
-typedef unsigned short us2_t __attribute__((ext_vector_type(2)));
-
-// exp(-2 pi i n / nn) in double, any integer n (nn a multiple of 8)
-struct Cd {
-    double re, im;
-};
-constexpr Cd cwd(long n, long nn) {
-    n %= nn;
-    if (n < 0) n += nn;
-    const long q4 = nn / 4, q = n / q4, r = n % q4;
-    const double step = 6.283185307179586476925286766559 / (double)nn;
-    double c = 0, s = 0;   // cos, sin of 2 pi r / nn, r < nn / 4
-    if (2 * r <= q4) {
-        c = cx_cos_small(r * step);
-        s = cx_sin_small(r * step);
-    } else {
-        c = cx_sin_small((q4 - r) * step);
-        s = cx_cos_small((q4 - r) * step);
-    }
-    Cd v{c, -s};
-    for (long i = 0; i < q; ++i) v = Cd{v.im, -v.re};   // times -i
-    return v;
-}
 
 // LDS tables: the one-wave kernel's L2 twiddles and per-lane DFT rows, then
 // the last layer's matrix for each source block k3' as (real, imaginary)
@@ -135,69 +111,6 @@ constexpr Fac16 make_fac16() {
 }
 __device__ const Fac16 kFac16 = make_fac16();
 
-// ------------------------------------------------------------ derived rows --
-// A DFT-row pair (R, I) from a base imaginary row b (entries (Im w, Re w))
-// with every point multiplied by f[i]: I' = (Im w f, Re w f), R' = (Re w f,
-// -Im w f).  Covers a scaled contraction side (f per point) and a scaled
-// output row (the same f for all points).
-__device__ __forceinline__ void kinds_scaled(uint4 b4, const uint32_t (&f)[4], uint32_t (&R)[4],
-                                             uint32_t (&I)[4]) {
-    const uint32_t b[4] = {b4.x, b4.y, b4.z, b4.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const h2_t bb = as_h2(b[i]), ff = as_h2(f[i]);
-        const h2_t fs = {ff.y, ff.x}, fn = {ff.x, -ff.y};
-        const h2_t ii = bb.yy * fs + bb.xx * fn;
-        const h2_t rr = {ii.y, -ii.x};
-        I[i] = as_u32(ii);
-        R[i] = as_u32(rr);
-    }
-}
-__device__ __forceinline__ Dft dft_of(const uint32_t (&R)[4], const uint32_t (&I)[4]) {
-    Dft F;
-    F.re = h8_of(R[0], R[1], R[2], R[3]);
-    F.im = h8_of(I[0], I[1], I[2], I[3]);
-    return F;
-}
-// (-i)^k3 times a DFT-row pair: k3 = 0: (R, I); 1: (I, -R); 2: (-R, -I); 3: (-I, R)
-__device__ __forceinline__ void kinds_rot(int k3, const uint32_t (&R)[4], const uint32_t (&I)[4],
-                                          uint32_t (&Rb)[4], uint32_t (&Ib)[4]) {
-    const bool sw = (k3 & 1) != 0;
-    const uint32_t nr = k3 >= 2 ? 0x80008000u : 0u;
-    const uint32_t ni = (k3 == 1 || k3 == 2) ? 0x80008000u : 0u;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        Rb[i] = (sw ? I[i] : R[i]) ^ nr;
-        Ib[i] = (sw ? R[i] : I[i]) ^ ni;
-    }
-}
-// the same four rows as bf16, the entries that multiply the real half of a
-// point (row a) times sa, those that multiply the imaginary half (row b)
-// times sb
-__device__ __forceinline__ void kinds_bf16(const uint32_t (&R)[4], const uint32_t (&I)[4], float sa, float sb,
-                                           bf8_t &Rb, bf8_t &Ib) {
-    float r[8], im[8];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        r[2 * i] = (float)as_h2(R[i]).x * sa;
-        r[2 * i + 1] = (float)as_h2(R[i]).y * sb;
-        im[2 * i] = (float)as_h2(I[i]).x * sa;
-        im[2 * i + 1] = (float)as_h2(I[i]).y * sb;
-    }
-    typedef float f8_t __attribute__((ext_vector_type(8)));
-    const f8_t vr = {r[0], r[1], r[2], r[3], r[4], r[5], r[6], r[7]};
-    const f8_t vi = {im[0], im[1], im[2], im[3], im[4], im[5], im[6], im[7]};
-    Rb = __builtin_convertvector(vr, bf8_t);
-    Ib = __builtin_convertvector(vi, bf8_t);
-}
-
-__device__ __forceinline__ f4_t mfma_acc(h8_t a, h8_t b, f4_t c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
-}
-__device__ __forceinline__ f4_t mfma_acc(bf8_t a, bf8_t b, f4_t c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
-
 // First layer: signal as the A operand, the two K steps x(m) (matrix Fa) and
 // x(4096 + m) (matrix Fb) accumulated; operands straight from the staging
 // buffer S (tile tau of half x at S[(16 x + tau) * 64 + lane]), two tiles
@@ -229,47 +142,6 @@ __device__ __forceinline__ void layer1(const uint4 *S, int lane, const OP &Far, 
         im = im1;
         n0 = m0;
         n1 = m1;
-    }
-}
-
-// Second layer (signal B) + L2 twiddles into P layout, then the G <-> T swap.
-__device__ __forceinline__ void forward_mid(uint32_t (&d)[64], const uint4 *Lc, const uint4 *Ytab, int lane) {
-    uint32_t e[64];
-    const Dft F = lds_dft(Lc, lane, false);
-    layer<false>(d, F, [&](int tau) { return Ytab[tau * 64 + lane]; },
-                 [&](int tau, f4_t re, f4_t im, uint4 y) {
-                     e[pidx(tau, 0)] = cmul(pk(re[0], im[0]), y.x);
-                     e[pidx(tau, 1)] = cmul(pk(re[1], im[1]), y.y);
-                     e[pidx(tau, 2)] = cmul(pk(re[2], im[2]), y.z);
-                     e[pidx(tau, 3)] = cmul(pk(re[3], im[3]), y.w);
-                 });
-#pragma unroll
-    for (int i = 0; i < 64; ++i) d[i] = e[i];
-    swap_GT(d);
-}
-
-// Lane twiddles of the first layer (X = base w_256 times the wave's w_1024
-// factor) and of the inverse second layer (conj(base) times w_1024^{-k3 c}),
-// each with its (-im, re) companion for cmul2.
-__device__ __forceinline__ void twiddles_fwd(uint4 X, const uint32_t (&xf)[4], uint32_t (&xw)[4],
-                                             uint32_t (&xs)[4]) {
-    const uint32_t b[4] = {X.x, X.y, X.z, X.w};
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const h2_t v = as_h2(cmul(b[j], xf[j]));
-        const h2_t s = {-v.y, v.x};
-        xw[j] = as_u32(v);
-        xs[j] = as_u32(s);
-    }
-}
-__device__ __forceinline__ void twiddles_inv(uint4 X, uint32_t xh, uint32_t (&xw)[4], uint32_t (&xs)[4]) {
-    const uint32_t b[4] = {X.x, X.y, X.z, X.w};
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const h2_t v = as_h2(cmulc(xh, b[j]));
-        const h2_t s = {-v.y, v.x};
-        xw[j] = as_u32(v);
-        xs[j] = as_u32(s);
     }
 }
 
@@ -512,34 +384,6 @@ __device__ __forceinline__ void last_layer(uint32_t (&d)[64], uint4 *U, const ui
             *(uint4 *)(yrow + 8 * i8) = v;
         }
     }
-}
-
-// Maximum |.| of 16-bit raw values (both halves of each dword)
-template <int DT> __device__ __forceinline__ float raw_max(const uint4 (&ra)[4]);
-template <> __device__ __forceinline__ float raw_max<F16>(const uint4 (&ra)[4]) {
-    h2_t hmx = {0, 0}, hmn = {0, 0};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const uint32_t v[4] = {ra[i].x, ra[i].y, ra[i].z, ra[i].w};
-#pragma unroll
-        for (int e = 0; e < 4; e += 2) {
-            hmx = __builtin_elementwise_maximum(hmx, __builtin_elementwise_maximum(as_h2(v[e]), as_h2(v[e + 1])));
-            hmn = __builtin_elementwise_minimum(hmn, __builtin_elementwise_minimum(as_h2(v[e]), as_h2(v[e + 1])));
-        }
-    }
-    return fmaxf(fmaxf((float)hmx.x, (float)hmx.y), fmaxf(-(float)hmn.x, -(float)hmn.y));
-}
-template <> __device__ __forceinline__ float raw_max<BF16>(const uint4 (&ra)[4]) {
-    us2_t mb = {0, 0};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const uint32_t v[4] = {ra[i].x, ra[i].y, ra[i].z, ra[i].w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-            mb = __builtin_elementwise_max(mb, __builtin_bit_cast(us2_t, v[e] & 0x7fff7fffu));
-    }
-    const uint32_t m = max((uint32_t)mb.x, (uint32_t)mb.y);
-    return __uint_as_float(m << 16);
 }
 
 }  // namespace w16

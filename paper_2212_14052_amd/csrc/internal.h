@@ -58,8 +58,14 @@ hipError_t launch_fftconv(const ConvArgs &a, hipStream_t s);
 // folded into k[0]); L a power of two in [16, 4096].
 bool fftconv_kgen_supported(int L);
 hipError_t launch_fftconv_kgen(const ConvArgs &a, const float *k, hipStream_t s);
-// Matrix-core block-FFT variant (16-bit I/O, L = 2048): computes the kernel
-// spectrum from k itself; returns hipErrorInvalidValue for other shapes.
+// The eight-wave register-resident convolution at L = 16384 (16-bit I/O):
+// plain rows or chunk pairs, with an optional correction term (float32 or
+// I/O dtype; no fused state term).
+bool fftconv_wave32k_supported(int L, int dtype);
+hipError_t launch_fftconv_wave32k(const ConvArgs &a, const float *k, hipStream_t s);
+// Matrix-core block-FFT convolution (16-bit I/O, L = 2048, 8192 or 16384),
+// the kernel spectrum computed from k inside; hipErrorInvalidValue for other
+// shapes.
 hipError_t launch_fftconv_mfma(const ConvArgs &a, const float *k, hipStream_t s);
 bool fftconv_mfma_supported(int L, int dtype);
 // One-wavefront-per-transform variant for L = 2048 (16-bit I/O); used by
