@@ -54,10 +54,11 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0
 FETCH_FACTOR, WRITE_FACTOR = 2.0, 1.0
 COUNTERS = {
     "headline": {"src": ("paper_2212_14052_amd/csrc/fftconv_wave.hip", "paper_2212_14052_amd/csrc/wave_common.h"),
-                 "sha": "3faeec79388f9e85", "fetch_kib": 15640.5, "write_kib": 24576.0,
-                 "valu": 6191616, "mfma": 663552, "mfma_busy": 0.218},
+                 "sha": "131582bc337850e7", "fetch_kib": 15640.4, "write_kib": 24576.0,
+                 "valu": 6191616, "mfma": 663552, "mfma_busy": 0.221},
     "cfg0_scaled": {"src": ("paper_2212_14052_amd/csrc/fftconv.hip", "paper_2212_14052_amd/csrc/fft_valu.h"),
-                    "sha": "a55c178cb10dd628", "valu": 84164608, "mfma": 0},
+                    "sha": "a55c178cb10dd628", "fetch_kib": 73914.3, "write_kib": 131072.0,
+                    "valu": 84164608, "mfma": 0},
 }
 SIMDS, CLOCK_GHZ = 1024, 2.4
 
@@ -540,6 +541,7 @@ def _extra_cfg0(h3, dev, reps, warm, ex, np, torch, workloads):
                      "unit": "TFLOP/s", "frac": round(tfl / VALU_F32_PEAK_TFLOPS, 4),
                      "kernel": "fftconv_kgen_kernel<2048, f32>", "flops_per_launch": fl,
                      "hbm_frac": round(by / (dc["mean"] * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic("cfg0_scaled"),
                      "valu_issue_frac": valu_issue_frac("cfg0_scaled", dc["mean"])},
     }
 
