@@ -129,7 +129,7 @@ def test_fftconv_deterministic(h3):
                                      (workloads.F32, 8192), (workloads.F16, 512)])
 @pytest.mark.parametrize("small", [1e-3, 0.3, 7.0])
 def test_fftconv_pair_with_unequal_rows(h3, dtype, L, small):
-    B, H = 4, 3
+    B, H = (8, 4) if L == 2048 else (4, 3)
     w = workloads.conv_workload("t", B, H, L, workloads.F32, seed=L + 5, dt_lo=1e-4)
     A, Bm, C, dt = _diag_params(w)
     k32 = oracle.ssm_kernel(A, Bm, C, dt, L).astype(np.float32)
@@ -354,7 +354,7 @@ def _bwd_case(h3, B, H, L, dtype, seed, with_D=True, sel=None):
 # B = 19 at L = 2048 gives three workgroup groups per channel on the matrix
 # cores (partial sums and their reduction).
 @pytest.mark.parametrize("dtype", [workloads.F32, workloads.F16, workloads.BF16])
-@pytest.mark.parametrize("B,H,L", [(1, 3, 16), (3, 5, 256), (2, 4, 1024), (5, 3, 2048), (4, 2, 8192),
+@pytest.mark.parametrize("B,H,L", [(1, 3, 16), (3, 5, 256), (2, 4, 1024), (5, 3, 2048), (9, 4, 2048), (4, 2, 8192),
                                    (19, 3, 2048)])
 def test_fftconv_bwd(h3, dtype, B, H, L):
     (du, rdu), (dk, rdk), (dD, rdD) = _bwd_case(h3, B, H, L, dtype, seed=B * 7 + L)
@@ -569,19 +569,19 @@ def test_layer_config4_full_size(h3):
 
 # ------------------------------------------- matrix-core conv (L = 2048) ---
 @pytest.mark.parametrize("dtype", [workloads.F16, workloads.BF16])
-@pytest.mark.parametrize("B,H", [(1, 3), (5, 2), (16, 4), (8, 33)])
+@pytest.mark.parametrize("B,H", [(1, 3), (5, 2), (16, 4), (8, 33), (7, 1), (9, 4), (17, 5), (8, 7), (24, 2)])
 def test_fftconv_mfma_shapes(h3, dtype, B, H):
     y, ref = _conv_case(h3, B, H, 2048, dtype, seed=B * 100 + H, dt_lo=1e-4)
     check(y, ref, TOL[dtype])
 
 
-@pytest.mark.parametrize("L", [2048, 8192])
+@pytest.mark.parametrize("L,B", [(2048, 4), (2048, 8), (8192, 4)])
 @pytest.mark.parametrize("scale_u,scale_k", [(1e3, 1.0), (1e-3, 1.0), (1.0, 1e-5), (30.0, 10.0), (2e4, 1.0),
-                                             (1e-5, 1.0)])
-def test_fftconv_mfma_dynamic_range(h3, scale_u, scale_k, L):
+                                             (1e-5, 1.0), (1e-7, 1.0)])
+def test_fftconv_mfma_dynamic_range(h3, scale_u, scale_k, L, B):
     """Inputs far from unit scale: the block FFT rescales by powers of two."""
     rng = np.random.default_rng(5)
-    B, H = 4, 6
+    H = 6
     u = (rng.standard_normal((B, H, L)) * scale_u).astype(np.float32)
     u = np.clip(u, -60000.0, 60000.0)
     k = (rng.standard_normal((H, L)) * np.exp(-np.arange(L) / 400.0) * scale_k).astype(np.float32)
@@ -604,12 +604,12 @@ def test_fftconv_mfma_dynamic_range(h3, scale_u, scale_k, L):
             check(y, ref, TOL[dt], dt)
 
 
-@pytest.mark.parametrize("L", [2048, 8192])
-def test_fftconv_mfma_zero_and_impulse(h3, L):
+@pytest.mark.parametrize("L,B", [(2048, 2), (2048, 8), (8192, 2)])
+def test_fftconv_mfma_zero_and_impulse(h3, L, B):
     H = 3
     rng = np.random.default_rng(6)
     k = (rng.standard_normal((H, L)) * np.exp(-np.arange(L) / 300.0)).astype(np.float32)
-    u = np.zeros((2, H, L), np.float16)
+    u = np.zeros((B, H, L), np.float16)
     y = to_np64(h3.fftconv(to_dev(u, workloads.F16), f32dev(k), None))
     assert np.all(y == 0.0)
     u[0, :, 0] = 1.0
@@ -618,6 +618,7 @@ def test_fftconv_mfma_zero_and_impulse(h3, L):
     check(y[0], k, 2e-2, "impulse_at_0")
     check(y[1, :, 100:], k[:, :L - 100], 2e-2, "impulse_at_100")
     assert np.abs(y[1, :, :100]).max() < 1e-3 * np.abs(k).max()
+    assert np.all(y[2:] == 0.0)   # all-zero pairs stay exactly zero
 
 
 # ----------------------------------------- matrix-core conv (L = 8192) ---
