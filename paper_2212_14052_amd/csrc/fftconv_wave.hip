@@ -58,13 +58,53 @@ constexpr int NT = 64 * NW;
 
 __device__ const HalfTable kHalf = make_half_table();
 
+// The two-channel instance stages a compact copy of the table: the conjugate
+// DFT rows are the direct rows with one half's sign flipped ((re, -im) ->
+// (re, im) and (im, re) -> (-im, re)), so they are formed in registers, and
+// the 2 KB saved let three workgroups (three waves per SIMD) share a CU.
+// Layout: Ytab, then DFT rows (real, imaginary), L1 twiddles X and (-im, re).
+constexpr int kTabC = kTabY + 4 * 64;
+struct HalfTableC {
+    uint32_t v[4 * kTabC];
+};
+constexpr HalfTableC make_half_table_c() {
+    const HalfTable h = make_half_table();
+    HalfTableC c{};
+    for (int i = 0; i < 4 * (kTabY + 2 * 64); ++i) c.v[i] = h.v[i];
+    for (int i = 0; i < 4 * 2 * 64; ++i) c.v[4 * (kTabY + 2 * 64) + i] = h.v[4 * (kTabY + 4 * 64) + i];
+    return c;
+}
+__device__ const HalfTableC kHalfC = make_half_table_c();
+// per-lane constant kinds in the full (CT false) and compact (CT true) layouts
+template <bool CT> struct LcKind {
+    static constexpr int X = CT ? 2 : 4, XS = CT ? 3 : 5;
+};
+template <bool CT>
+__device__ __forceinline__ Dft lc_dft(const uint4 *Lc, int lane, bool conj) {
+    if constexpr (!CT) {
+        return lds_dft(Lc, lane, conj);
+    } else {
+        asm volatile("" ::: "memory");   // re-read per layer, do not keep live
+        uint4 re = Lc[lane], im = Lc[64 + lane];
+        if (conj) {
+            re = make_uint4(re.x ^ 0x80000000u, re.y ^ 0x80000000u, re.z ^ 0x80000000u, re.w ^ 0x80000000u);
+            im = make_uint4(im.x ^ 0x8000u, im.y ^ 0x8000u, im.z ^ 0x8000u, im.w ^ 0x8000u);
+        }
+        Dft F;
+        F.re = __builtin_bit_cast(h8_t, re);
+        F.im = __builtin_bit_cast(h8_t, im);
+        return F;
+    }
+}
+
 // Forward transform of a register-resident signal up to L3: L1 (signal A) +
 // w_256 twiddle, L2 (signal B) + w_4096 twiddle written in P layout, swap.
+template <bool CT>
 __device__ __forceinline__ void forward_front(uint32_t (&d)[64], const uint4 *Lc, const uint4 *Ytab,
                                               int lane) {
     {
-        const Dft F = lds_dft(Lc, lane, false);
-        const uint4 X = Lc[4 * 64 + lane], Xs = Lc[5 * 64 + lane];
+        const Dft F = lc_dft<CT>(Lc, lane, false);
+        const uint4 X = Lc[LcKind<CT>::X * 64 + lane], Xs = Lc[LcKind<CT>::XS * 64 + lane];
         const uint32_t xw[4] = {X.x, X.y, X.z, X.w}, xs[4] = {Xs.x, Xs.y, Xs.z, Xs.w};
         layer<true>(d, F, NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
 #pragma unroll
@@ -73,7 +113,7 @@ __device__ __forceinline__ void forward_front(uint32_t (&d)[64], const uint4 *Lc
     }
     uint32_t e[64];
     {
-        const Dft F = lds_dft(Lc, lane, false);
+        const Dft F = lc_dft<CT>(Lc, lane, false);
         layer<false>(d, F, [&](int tau) { return Ytab[tau * 64 + lane]; },
                      [&](int tau, f4_t re, f4_t im, uint4 y) {
                          e[pidx(tau, 0)] = cmul(pk(re[0], im[0]), y.x);
@@ -143,11 +183,15 @@ __device__ __forceinline__ void out_layer(uint32_t (&d)[64], const Dft &Fs, floa
 // 2 hb and 2 hb + 1, both spectra computed by all four waves, then waves 0, 1
 // take the first channel's pairs and waves 2, 3 the second's, so no wave
 // idles while its workgroup holds the CU's LDS.
-template <int DT, int CORR, int CPW>
-__global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(CPW == 1 ? 3 : 2))) void
+template <int DT, int CORR, int CPW, bool CT = false>
+__global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(CPW == 1 || CT ? 3 : 2))) void
 fftconv_wave4096_kernel(ConvArgs a, const float *k, int wg_per_ch, int pairs_per_ch) {
     using namespace wv;
-    __shared__ uint4 Tab[kTab];       // Ytab (L2 twiddles per tile and lane) + Lc (per-lane constants)
+    // CT: the compact constant table (three workgroups per CU; two channels per
+    // workgroup only)
+    static_assert(!CT || CPW == 2, "compact table with two channels per workgroup");
+    constexpr int kT = CT ? kTabC : kTab;
+    __shared__ uint4 Tab[kT];         // Ytab (L2 twiddles per tile and lane) + Lc (per-lane constants)
     __shared__ uint4 Ks[CPW][16 * 64];   // kernel spectra per L3 quad and lane (also the spectrum's scratch)
     uint4 *Ytab = Tab, *Lc = Tab + kTabY;
     __shared__ float red[2 * NW];
@@ -206,10 +250,10 @@ fftconv_wave4096_kernel(ConvArgs a, const float *k, int wg_per_ch, int pairs_per
     // Loads in the order they are needed: (1) the constant tables, straight
     // into LDS (1 KB per wave and instruction, no registers)
 #pragma unroll
-    for (int r = 0; r < (kTab + NT - 1) / NT; ++r) {
+    for (int r = 0; r < (kT + NT - 1) / NT; ++r) {
         const int base = r * NT + 64 * w;   // this wave's 64 uint4
-        if (base < kTab)
-            __builtin_amdgcn_global_load_lds((gvoid_t *)((const uint4 *)kHalf.v + base + lane),
+        if (base < kT)
+            __builtin_amdgcn_global_load_lds((gvoid_t *)((const uint4 *)(CT ? kHalfC.v : kHalf.v) + base + lane),
                                              (lvoid_t *)(Tab + base), 16, 0, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
@@ -269,9 +313,9 @@ fftconv_wave4096_kernel(ConvArgs a, const float *k, int wg_per_ch, int pairs_per
             dq[8 + j] = pk(ldexpf(kq[ch][j].z, -ek), 0.f);
             dq[12 + j] = pk(ldexpf(kq[ch][j].w, -ek), 0.f);
         }
-        const Dft F = lds_dft(Lc, lane, false);
+        const Dft F = lc_dft<CT>(Lc, lane, false);
         {
-            const uint4 X = Lc[4 * 64 + lane], Xs = Lc[5 * 64 + lane];
+            const uint4 X = Lc[LcKind<CT>::X * 64 + lane], Xs = Lc[LcKind<CT>::XS * 64 + lane];
             const uint32_t xw[4] = {X.x, X.y, X.z, X.w}, xs[4] = {Xs.x, Xs.y, Xs.z, Xs.w};
             layer<true, 4>(dq, F, NoPre{}, [&](int t, f4_t re, f4_t im, uint4) {
 #pragma unroll
@@ -405,10 +449,10 @@ fftconv_wave4096_kernel(ConvArgs a, const float *k, int wg_per_ch, int pairs_per
             for (int i = 0; i < 64; ++i) d[i] = pk(ldexpf((float)as_h2(d[i]).x, -eua), ldexpf((float)as_h2(d[i]).y, -eub));
         }
 
-        forward_front(d, Lc, Ytab, lane);
+        forward_front<CT>(d, Lc, Ytab, lane);
         // L3 (matrix scaled by 2^-e2, the spectrum's normalisation) +
         // pointwise product with the kernel spectrum (quads in P layout)
-        Dft F3 = lds_dft(Lc, lane, false);
+        Dft F3 = lc_dft<CT>(Lc, lane, false);
         F3.re = h8_scale(F3.re, (_Float16)ldexpf(1.0f, -e2));
         F3.im = h8_scale(F3.im, (_Float16)ldexpf(1.0f, -e2));
         layer<false>(d, F3, [&](int tau) { return Ks[chw][tau * 64 + lane]; },
@@ -420,7 +464,7 @@ fftconv_wave4096_kernel(ConvArgs a, const float *k, int wg_per_ch, int pairs_per
         });
         // inverse: L3^H, swap, conj twiddle (back to quad-per-tile layout),
         // L2^H (signal A) + conj twiddle, L1^H
-        layer<false>(d, lds_dft(Lc, lane, true), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+        layer<false>(d, lc_dft<CT>(Lc, lane, true), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) d[4 * tau + jj] = pk(re[jj], im[jj]);
         });
@@ -439,9 +483,9 @@ fftconv_wave4096_kernel(ConvArgs a, const float *k, int wg_per_ch, int pairs_per
             for (int i = 0; i < 64; ++i) d[i] = e[i];
         }
         {
-            const uint4 X = Lc[4 * 64 + lane], Xs = Lc[5 * 64 + lane];
+            const uint4 X = Lc[LcKind<CT>::X * 64 + lane], Xs = Lc[LcKind<CT>::XS * 64 + lane];
             const uint32_t xw[4] = {X.x, X.y, X.z, X.w}, xs[4] = {Xs.x, Xs.y, Xs.z, Xs.w};
-            layer<true>(d, lds_dft(Lc, lane, true), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+            layer<true>(d, lc_dft<CT>(Lc, lane, true), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
 #pragma unroll
                 for (int jj = 0; jj < 4; ++jj) d[4 * tau + jj] = cmulc2(pk(re[jj], im[jj]), xw[jj], xs[jj]);
             });
@@ -456,7 +500,7 @@ fftconv_wave4096_kernel(ConvArgs a, const float *k, int wg_per_ch, int pairs_per
         const int sea = kexp + eua, seb = kexp + eub;
         const int sfa = min(max(sea, -10), 14), srema = sea - sfa;
         const int sfb = min(max(seb, -10), 14), sremb = seb - sfb;
-        Dft Fs = lds_dft(Lc, lane, true);
+        Dft Fs = lc_dft<CT>(Lc, lane, true);
         Fs.re = h8_scale(Fs.re, (_Float16)ldexpf(1.0f, sfa));
         Fs.im = h8_scale(Fs.im, (_Float16)ldexpf(1.0f, sfb));
         // branch-free epilogue (a branch inside it lets the compiler hoist
@@ -635,14 +679,14 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(2))) voi
     int ep = 0;
     if (have) {
         const int eu = pack_pair<DT>(ra, rb, d);
-        forward_front(d, Lc, Ytab, lane);
+        forward_front<false>(d, Lc, Ytab, lane);
         load_pair_raw(dy, oa, ob, g, c, ra, rb);   // in flight during the u transform's last layer
         layer<false>(d, lds_dft(Lc, lane, false), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) zu[4 * tau + jj] = pk(re[jj], im[jj]);
         });
         const int eg = pack_pair<DT>(ra, rb, d);
-        forward_front(d, Lc, Ytab, lane);
+        forward_front<false>(d, Lc, Ytab, lane);
         // conj(Zu) . Zdy in float32 from the matrix-core outputs, packed back
         // into zu at 2^-7 (both transforms are below 1448 in modulus, so the
         // product stays below 2^14)
@@ -812,12 +856,23 @@ hipError_t launch_fftconv_wave(const ConvArgs &a, const float *k, hipStream_t s)
     dim3 grid(a.H * wg_per_ch), block(wv::NT);
     const int corr = a.corr == nullptr ? 0 : (a.corr16 ? 2 : 1);
     if (corr == 0 && a.pair_mode == 0 && pairs_per_ch <= 2 && wg_per_ch == 1 && a.H >= 2) {
-        // two channels per workgroup: every wave has a row pair
+        // two channels per workgroup: every wave has a row pair.  From two
+        // workgroups per CU on (512 and more) the instance with the compact
+        // table runs three per CU (B = 4: 51 -> 48 us at H = 2560, 337 -> 300
+        // us at H = 20480); below that its extra instructions only cost (19
+        // -> 20 us at H = 768)
         const dim3 grid2((a.H + 1) / 2);
-        if (a.dtype == F16)
-            hipLaunchKernelGGL((fftconv_wave4096_kernel<F16, 0, 2>), grid2, block, 0, s, a, k, 1, pairs_per_ch);
-        else
-            hipLaunchKernelGGL((fftconv_wave4096_kernel<BF16, 0, 2>), grid2, block, 0, s, a, k, 1, pairs_per_ch);
+        const bool ct = grid2.x >= 512;
+#define H3_WAVE2_LAUNCH(DTV, CTV) \
+    hipLaunchKernelGGL((fftconv_wave4096_kernel<DTV, 0, 2, CTV>), grid2, block, 0, s, a, k, 1, pairs_per_ch)
+        if (a.dtype == F16) {
+            if (ct) H3_WAVE2_LAUNCH(F16, true);
+            else H3_WAVE2_LAUNCH(F16, false);
+        } else {
+            if (ct) H3_WAVE2_LAUNCH(BF16, true);
+            else H3_WAVE2_LAUNCH(BF16, false);
+        }
+#undef H3_WAVE2_LAUNCH
         return hipGetLastError();
     }
 #define H3_WAVE_LAUNCH(DTV, CV) \

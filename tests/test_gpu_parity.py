@@ -569,7 +569,8 @@ def test_layer_config4_full_size(h3):
 
 # ------------------------------------------- matrix-core conv (L = 2048) ---
 @pytest.mark.parametrize("dtype", [workloads.F16, workloads.BF16])
-@pytest.mark.parametrize("B,H", [(1, 3), (5, 2), (16, 4), (8, 33), (7, 1), (9, 4), (17, 5), (8, 7), (24, 2)])
+@pytest.mark.parametrize("B,H", [(1, 3), (5, 2), (16, 4), (8, 33), (7, 1), (9, 4), (17, 5), (8, 7), (24, 2),
+                                 (4, 1031), (3, 1024)])
 def test_fftconv_mfma_shapes(h3, dtype, B, H):
     y, ref = _conv_case(h3, B, H, 2048, dtype, seed=B * 100 + H, dt_lo=1e-4)
     check(y, ref, TOL[dtype])
