@@ -45,7 +45,7 @@ bool fused_len_ok(int L, int dtype) {
 //   k       (H, chunk) float32            the chunk kernel f
 //   kspec   (H, chunk + 1) complex        its spectrum (VALU conv only)
 //   states  (B, H, nchunk, m) complex     chunk end-states s_c = M_ux u^(c)
-//   fused initial-state term (16-bit, chunk 8192): per-channel power
+//   fused initial-state term (16-bit, chunk 8192 or 16384): per-channel power
 //   tables ctab, normalised weights w16 (B, H, nchunk, 64) fp16 complex and
 //   their exponents wexp (B, H, nchunk);
 //   otherwise: weights corr_w (B, H, nchunk, m) complex and the term itself,
@@ -57,7 +57,7 @@ struct StatepassWs {
 StatepassWs statepass_ws(int B, int H, int L, int m, int chunk, int dtype) {
     StatepassWs w{};
     const size_t nchunk = (size_t)(L / chunk);
-    w.fused = fftconv_wave16k_supported(chunk, dtype);
+    w.fused = fftconv_wave16k_supported(chunk, dtype) || fftconv_wave32k_supported(chunk, dtype);
     w.mfma = fftconv_mfma_supported(chunk, dtype);
     w.corr16 = w.mfma && state_correction_mfma_ok(chunk, dtype);
     size_t off = 0;
@@ -191,7 +191,7 @@ int statepass_run(const void *u, const float *Abar, const float *Bbar, const flo
     a.u = u; a.y = y; a.Kspec = Kspec; a.D = D;
     a.B = B; a.H = H; a.L = chunk; a.nchunk = nchunk; a.pair_mode = 1; a.dtype = dtype;
     if (w.fused) {
-        // chunk = 8192: the conv computes M_xy x^(c) itself from normalised
+        // chunk 8192 or 16384: the conv computes M_xy x^(c) itself from normalised
         // weights (scan output) and per-channel power tables
         uint4 *ctab = (uint4 *)(ws + w.ctab);
         uint32_t *w16 = (uint32_t *)(ws + w.w16);

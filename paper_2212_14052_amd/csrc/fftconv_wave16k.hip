@@ -173,65 +173,6 @@ __device__ __forceinline__ void last_acc(uint4 gr4, uint4 gi4, uint4 b4, f4_t (&
     }
 }
 
-// Fused initial-state term (state passing, chunk = 8192): for this wave's
-// quarter of the pair (row w >> 1, t in [4096 (w & 1), + 4096)), with
-// t = 64 a + b,  corr(t) = 2 Re sum_n Abar_n^b V_n(a),  V_n(a) = W_n Abar_n^{64 a},
-// as 16 tiles D[b][a] of 16 x 16 on the matrix cores (K = 64 modes as (re, im)
-// pairs): the A operand Abar_n^b comes from the per-channel table in LDS, the
-// B operand V from the row's weights W (normalised to max |W| in [1/2, 1),
-// fp16) times Abar_n^{64 a}, stepping a by 16 with Abar_n^1024.  A lane ends
-// up with four consecutive t: they are added in fp32 to the staged 16-bit
-// outputs and stored as 8 bytes.
-template <int DT>
-__device__ __forceinline__ void fused_state_term(const uint4 *U, const uint4 *CT, const uint4 (&wq)[4], int ew,
-                                                 int w, int lane, uint16_t *yrow) {
-    const int g = lane >> 4, c = lane & 15;
-    const uint4 *CA = CT, *T64 = CT + 1024, *Zt = CT + 1536;
-    const float scorr = ldexpf(2.0f, ew);
-    // wq[kb]: normalised W of modes 16 kb + 4 g + q in dword q
-    uint32_t V[16];   // [4 kb + q]: (Re V, -Im V) of mode 16 kb + 4 g + q, column a = 64 (w & 1) + c
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-        const uint4 tq = T64[((w & 1) * 4 + kb) * 64 + lane];
-        // conj(V) = conj(W) conj(Abar^{64 a}), stored (Re V, -Im V)
-        V[4 * kb + 0] = cmulc(wq[kb].x ^ 0x80000000u, tq.x);
-        V[4 * kb + 1] = cmulc(wq[kb].y ^ 0x80000000u, tq.y);
-        V[4 * kb + 2] = cmulc(wq[kb].z ^ 0x80000000u, tq.z);
-        V[4 * kb + 3] = cmulc(wq[kb].w ^ 0x80000000u, tq.w);
-    }
-    const f4_t z = {0.f, 0.f, 0.f, 0.f};
-    const uint2 *Uo = (const uint2 *)U;
-    const int row = w >> 1;
-#pragma unroll
-    for (int jb = 0; jb < 4; ++jb) {
-        if (jb > 0) {
-            // a += 16: V <- V Abar^1024, i.e. the stored conj(V) times conj(Abar^1024)
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb) {
-                const uint4 zq = Zt[kb * 4 + g];
-                V[4 * kb + 0] = cmulc(V[4 * kb + 0], zq.x);
-                V[4 * kb + 1] = cmulc(V[4 * kb + 1], zq.y);
-                V[4 * kb + 2] = cmulc(V[4 * kb + 2], zq.z);
-                V[4 * kb + 3] = cmulc(V[4 * kb + 3], zq.w);
-            }
-        }
-#pragma unroll
-        for (int ib = 0; ib < 4; ++ib) {
-            f4_t D = z;
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
-                D = mfma_acc(__builtin_bit_cast(h8_t, CA[(ib * 4 + kb) * 64 + lane]),
-                             h8_of(V[4 * kb], V[4 * kb + 1], V[4 * kb + 2], V[4 * kb + 3]), D);
-            // rows b = 16 ib + 4 g + jj, column a = 64 (w & 1) + 16 jb + c
-            const int t = 4096 * (w & 1) + 1024 * jb + 64 * c + 16 * ib + 4 * g;
-            const uint2 o = Uo[row * 2048 + (t >> 2)];
-            const uint2 r = make_uint2(pack_out<DT>(fmaf(D[0], scorr, lo_f<DT>(o.x)), fmaf(D[1], scorr, hi_f<DT>(o.x))),
-                                       pack_out<DT>(fmaf(D[2], scorr, lo_f<DT>(o.y)), fmaf(D[3], scorr, hi_f<DT>(o.y))));
-            *(uint2 *)(yrow + t) = r;
-        }
-    }
-}
-
 // Last layer for the wave's own tiles T = 4 w + tt: exchange, 64-point
 // contraction with the radix-4 butterfly, output epilogue and stores.
 //   D0 = sum_k3' G_k3' x_k3'           -> y(m)
@@ -351,7 +292,7 @@ __device__ __forceinline__ void last_layer(uint32_t (&d)[64], uint4 *U, const ui
     }
     __syncthreads();
     if constexpr (CORR == 3) {
-        if (active) fused_state_term<DT>(U, G1, wq, w < 2 ? ewa : ewb, w, lane, yrow);
+        if (active) fused_state_term<DT, 2048>(U, G1, wq, w < 2 ? ewa : ewb, w >> 1, w & 1, lane, yrow);
         return;
     }
     if (active) {

@@ -207,11 +207,13 @@ __device__ __forceinline__ void acc_rot(int n, h8_t Ar, h8_t Ai, h8_t b, h8_t nb
 // (k3' * 8 + w) of every source k3'.  The values of round 0 wait in fp32 and
 // are packed with those of round 1 (adjacent points), staged in LDS as rows
 // a and b, and stored by every wave as one contiguous eighth.
-// CORR: 0 none, 1 float32 term, 2 term in the I/O dtype, added at the store.
+// CORR: 0 none, 1 float32 term, 2 term in the I/O dtype, added at the store;
+// 3 the term computed here from the chunk rows' normalised weights (cra, crb:
+// 64 fp16 complex each; exponents ewa, ewb) and the channel's tables CT.
 template <int DT, int CORR>
-__device__ __forceinline__ void last_layer32(uint32_t (&d)[64], uint4 *U, const uint4 *G, int w, int lane, float sca,
-                                             float scb, uint16_t *ya, uint16_t *yb, bool has_b, const void *cra,
-                                             const void *crb) {
+__device__ __forceinline__ void last_layer32(uint32_t (&d)[64], uint4 *U, const uint4 *G, const uint4 *CT, int w,
+                                             int lane, float sca, float scb, uint16_t *ya, uint16_t *yb, bool has_b,
+                                             const void *cra, const void *crb, int ewa, int ewb) {
     const int g = lane >> 4, c = lane & 15;
     float v0[4][2][4];        // round 0: [t3][row a, b][jj], scaled
     uint32_t po[4][2][4];     // packed rounds 0 and 1
@@ -267,6 +269,7 @@ __device__ __forceinline__ void last_layer32(uint32_t (&d)[64], uint4 *U, const 
     // through LDS (rows a, b as 16384 halves each), then out as 16-byte
     // chunks, each wave a contiguous eighth of the pair
     uint4 cq[8];   // correction term (CORR 2), loaded while the outputs are staged
+    uint4 wq[4];   // fused state term (CORR 3): the row's weights W for the lane's 16 modes
     const bool active = w < 4 || has_b;
     __syncthreads();   // every exchange read is done
     uint32_t *Ud = (uint32_t *)U;
@@ -285,7 +288,16 @@ __device__ __forceinline__ void last_layer32(uint32_t (&d)[64], uint4 *U, const 
         for (int r = 0; r < 8; ++r)
             cq[r] = active ? ((const uint4 *)crow)[(w & 3) * 512 + r * 64 + lane] : make_uint4(0, 0, 0, 0);
     }
+    if (CORR == 3) {   // modes 16 kb + 4 g + (0..3): one uint4 per kb
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+            wq[kb] = active ? ((const uint4 *)crow)[4 * kb + (lane >> 4)] : make_uint4(0, 0, 0, 0);
+    }
     __syncthreads();
+    if constexpr (CORR == 3) {
+        if (active) fused_state_term<DT, 4096>(U, CT, wq, w < 4 ? ewa : ewb, w >> 2, w & 3, lane, yrow);
+        return;
+    }
     if (active) {
 #pragma unroll
         for (int r = 0; r < 8; ++r) {
@@ -323,10 +335,13 @@ template <int DT, int CORR>
 __global__ __launch_bounds__(w32::NT) __attribute__((amdgpu_waves_per_eu(2))) void fftconv_wave32k_kernel(
     ConvArgs a, const float *k, int wg_per_ch, int pairs_per_ch) {
     using namespace w32;
-    __shared__ uint4 Tab[kTab32];   // Ytab + Lc, then the last layer's rows
+    // Ytab + Lc, then the last layer's rows, then (CORR 3) the channel's
+    // state-term tables
+    constexpr int kTabAll = CORR == 3 ? kTab32 + CORR_TAB_U4 : kTab32;
+    __shared__ uint4 Tab[kTabAll];
     __shared__ uint4 U[kU];         // pair staging, then the exchange and the output staging
     __shared__ float red[3 * NW];   // row a max | kernel spectrum max | row b max
-    const uint4 *Ytab = Tab, *Lc = Tab + kTabY, *G = Tab + kTab;
+    const uint4 *Ytab = Tab, *Lc = Tab + kTabY, *G = Tab + kTab, *CT = Tab + kTab32;
     uint32_t *Ud = (uint32_t *)U;
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // frequency block k3
@@ -377,11 +392,13 @@ __global__ __launch_bounds__(w32::NT) __attribute__((amdgpu_waves_per_eu(2))) vo
 
     // ---- start-up loads: tables into LDS, factors, kernel row, first pair ----
 #pragma unroll
-    for (int r = 0; r < (kTab32 + NT - 1) / NT; ++r) {
-        const int base = r * NT + 64 * w;   // kTab32 is a multiple of 64
-        if (base < kTab32)
-            __builtin_amdgcn_global_load_lds((gvoid_t *)((const uint4 *)kHalf32.v + base + lane),
-                                             (lvoid_t *)(Tab + base), 16, 0, 0);
+    for (int r = 0; r < (kTabAll + NT - 1) / NT; ++r) {
+        const int base = r * NT + 64 * w;   // kTab32 and CORR_TAB_U4 are multiples of 64
+        if (base < kTabAll) {
+            const uint4 *src = (CORR != 3 || base < kTab32) ? (const uint4 *)kHalf32.v + base
+                                                            : a.corr_tab + (long)h * CORR_TAB_U4 + (base - kTab32);
+            __builtin_amdgcn_global_load_lds((gvoid_t *)(src + lane), (lvoid_t *)(Tab + base), 16, 0, 0);
+        }
     }
     __builtin_amdgcn_sched_barrier(0);
     // factor group i (0: f1, 1: xf, 2: f3, 3: g3 | xh | w8) of this wave and
@@ -655,14 +672,21 @@ __global__ __launch_bounds__(w32::NT) __attribute__((amdgpu_waves_per_eu(2))) vo
             cra = (const uint16_t *)a.corr + oa;
             crb = (const uint16_t *)a.corr + obc;
         }
-        last_layer32<DT, CORR>(d, U, G, w, lane, sca, scb, ya, yb, ob >= 0, cra, crb);
+        int ewa = 0, ewb = 0;
+        if (CORR == 3) {   // normalised weights W of chunk rows oa / L, obc / L
+            cra = (const uint32_t *)a.corr + (oa / L) * 64;
+            crb = (const uint32_t *)a.corr + (obc / L) * 64;
+            ewa = a.corr_e[oa / L];
+            ewb = a.corr_e[obc / L];
+        }
+        last_layer32<DT, CORR>(d, U, G, CT, w, lane, sca, scb, ya, yb, ob >= 0, cra, crb, ewa, ewb);
     }
 }
 
 bool fftconv_wave32k_supported(int L, int dtype) { return L == w32::L && (dtype == F16 || dtype == BF16); }
 
 hipError_t launch_fftconv_wave32k(const ConvArgs &a, const float *k, hipStream_t s) {
-    if (!fftconv_wave32k_supported(a.L, a.dtype) || a.corr_tab != nullptr) return hipErrorInvalidValue;
+    if (!fftconv_wave32k_supported(a.L, a.dtype)) return hipErrorInvalidValue;
     int pairs_per_ch;
     if (a.pair_mode == 0)
         pairs_per_ch = (a.B + 1) / 2;
@@ -673,17 +697,20 @@ hipError_t launch_fftconv_wave32k(const ConvArgs &a, const float *k, hipStream_t
     int wg_per_ch = 1;
     while ((long)a.H * wg_per_ch < 256 && pairs_per_ch >= 4 * wg_per_ch) wg_per_ch *= 2;
     dim3 grid(a.H * wg_per_ch), block(w32::NT);
-    const int corr = a.corr == nullptr ? 0 : (a.corr16 ? 2 : 1);
+    const int corr = a.corr == nullptr ? 0 : a.corr_tab != nullptr ? 3 : (a.corr16 ? 2 : 1);
+    if (corr == 3 && (a.pair_mode != 1 || a.corr_e == nullptr)) return hipErrorInvalidValue;
 #define H3_W32_LAUNCH(DTV, CV) \
     hipLaunchKernelGGL((fftconv_wave32k_kernel<DTV, CV>), grid, block, 0, s, a, k, wg_per_ch, pairs_per_ch)
     if (a.dtype == F16) {
         if (corr == 0) H3_W32_LAUNCH(F16, 0);
         else if (corr == 1) H3_W32_LAUNCH(F16, 1);
-        else H3_W32_LAUNCH(F16, 2);
+        else if (corr == 2) H3_W32_LAUNCH(F16, 2);
+        else H3_W32_LAUNCH(F16, 3);
     } else {
         if (corr == 0) H3_W32_LAUNCH(BF16, 0);
         else if (corr == 1) H3_W32_LAUNCH(BF16, 1);
-        else H3_W32_LAUNCH(BF16, 2);
+        else if (corr == 2) H3_W32_LAUNCH(BF16, 2);
+        else H3_W32_LAUNCH(BF16, 3);
     }
 #undef H3_W32_LAUNCH
     return hipGetLastError();

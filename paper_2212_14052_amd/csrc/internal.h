@@ -40,7 +40,7 @@ struct ConvArgs {
     // (B, H, nchunk * L) added to the output; float32, or the I/O dtype if corr16
     const void *corr;
     int corr16;
-    // fused initial-state term (mode 1, L = 8192 conv only): when corr_tab is
+    // fused initial-state term (mode 1, L = 8192 and 16384 convs): when corr_tab is
     // set, corr holds the normalised weights (B, H, nchunk, 64) fp16 complex
     // and corr_e their exponents (B, H, nchunk), as written by
     // launch_state_scan_w16, and corr_tab the per-channel tables written by
@@ -59,8 +59,8 @@ hipError_t launch_fftconv(const ConvArgs &a, hipStream_t s);
 bool fftconv_kgen_supported(int L);
 hipError_t launch_fftconv_kgen(const ConvArgs &a, const float *k, hipStream_t s);
 // The eight-wave register-resident convolution at L = 16384 (16-bit I/O):
-// plain rows or chunk pairs, with an optional correction term (float32 or
-// I/O dtype; no fused state term).
+// plain rows or chunk pairs, with an optional correction term (float32, I/O
+// dtype, or the fused state term from corr_tab as at L = 8192).
 bool fftconv_wave32k_supported(int L, int dtype);
 hipError_t launch_fftconv_wave32k(const ConvArgs &a, const float *k, hipStream_t s);
 // Matrix-core block-FFT convolution (16-bit I/O, L = 2048, 8192 or 16384),
@@ -102,8 +102,8 @@ hipError_t launch_state_scan(const float *Abar, const float *C, const float *x0,
 hipError_t launch_state_correction(const float *Abar, const float2 *corr_W, int B, int H, int m,
                                    int chunk, int nchunk, float *corr, hipStream_t s);
 bool state_correction_mfma_ok(int chunk, int dtype);
-// Per-channel tables for the fused initial-state term of the L = 8192 conv
-// (CORR_TAB_U4 uint4 per channel, the last 48 unused; m <= 64).
+// Per-channel tables for the fused initial-state term of the L = 8192 and
+// L = 16384 convs (CORR_TAB_U4 uint4 per channel, the last 32 unused; m <= 64).
 constexpr int CORR_TAB_U4 = 1600;
 hipError_t launch_corr_tables(const float *Abar, int H, int m, uint4 *tab, hipStream_t s);
 // Scan variant for the fused term: normalised fp16 weights and exponents.

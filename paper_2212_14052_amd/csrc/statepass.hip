@@ -532,7 +532,7 @@ hipError_t launch_state_correction_mfma(const float *Abar, const float2 *corr_W,
 }
 
 // ---------------------------- per-channel tables of the fused state term ---
-// For the L = 8192 conv with the initial-state term fused in (its read-out
+// For the L = 8192 and 16384 convs with the initial-state term fused in (their read-out
 // computes 2 Re sum_n Abar_n^b V_n(a), t = 64 a + b, V_n(a) = W_n Abar_n^{64 a},
 // on the matrix cores), per channel, in fp16 (re, im) pairs:
 //   [0, 1024)     Abar_n^b as the A operand: uint4 (ib * 4 + kb) * 64 + 16 g + c
@@ -540,6 +540,8 @@ hipError_t launch_state_correction_mfma(const float *Abar, const float2 *corr_W,
 //   [1024, 1536)  Abar_n^{64 a}, a = 64 h2 + c: uint4 (h2 * 4 + kb) * 64 + 16 g + c,
 //                 modes n = 16 kb + 4 g + q in dword q
 //   [1536, 1552)  Abar_n^1024: uint4 kb * 4 + g, modes n = 16 kb + 4 g + q
+//   [1552, 1568)  Abar_n^8192, the same layout (chunk 16384: a in [128, 256)
+//                 takes Abar_n^{64 (a - 128)} times Abar_n^8192)
 // Modes n >= m hold powers of 0 (their weights W_n are zero).  Powers in float64.
 __device__ __forceinline__ uint32_t ct_h2(double2 p) {
     typedef _Float16 h2 __attribute__((ext_vector_type(2)));
@@ -572,6 +574,7 @@ __global__ __launch_bounds__(256) void corr_tables_kernel(const float *Abar, int
         e = sp_zmul(e, z64);
     }
     if (q4 == 0) t[(1536 + kb * 4 + g) * 4 + q] = ct_h2(sp_zpow(z, 1024));
+    if (q4 == 1) t[(1552 + kb * 4 + g) * 4 + q] = ct_h2(sp_zpow(z, 8192));   // chunk 16384: a >= 128
     __syncthreads();
     uint4 *dst = tab + (long)h * CORR_TAB_U4;
     for (int i = tid; i < CORR_TAB_U4; i += 256) dst[i] = ts[i];

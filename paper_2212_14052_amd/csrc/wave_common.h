@@ -470,5 +470,73 @@ template <> __device__ __forceinline__ float raw_max<BF16>(const uint4 (&ra)[4])
 }
 
 
+// Fused initial-state term of state passing (Sec. 4.2: the M_xy x term of a
+// chunk, chunk 8192 or 16384): for the wave's 4096 outputs t in [4096 qa,
+// + 4096) of a chunk row, with
+// t = 64 a + b,  corr(t) = 2 Re sum_n Abar_n^b V_n(a),  V_n(a) = W_n Abar_n^{64 a},
+// as 16 tiles D[b][a] of 16 x 16 on the matrix cores (K = 64 modes as (re, im)
+// pairs): the A operand Abar_n^b comes from the per-channel table in LDS, the
+// B operand V from the row's weights W (normalised to max |W| in [1/2, 1),
+// fp16) times Abar_n^{64 a}, stepping a by 16 with Abar_n^1024.  The table
+// holds Abar_n^{64 a} for a in [0, 128); quarters qa = 2, 3 (chunk 16384)
+// take them times Abar_n^8192.  A lane ends up with four consecutive t: they
+// are added in fp32 to the outputs staged in U (rows of ROWU2 uint2, this
+// row at index row) and stored as 8 bytes.
+// The per-channel table CT (CORR_TAB_U4 uint4, written by the state-passing
+// tables kernel): [0, 1024) Abar_n^b as A operands, [1024, 1536)
+// Abar_n^{64 a}, [1536, 1552) Abar_n^1024, [1552, 1568) Abar_n^8192.
+template <int DT, int ROWU2>
+__device__ __forceinline__ void fused_state_term(const uint4 *U, const uint4 *CT, const uint4 (&wq)[4], int ew,
+                                                 int row, int qa, int lane, uint16_t *yrow) {
+    const int g = lane >> 4, c = lane & 15;
+    const uint4 *CA = CT, *T64 = CT + 1024, *Zt = CT + 1536;
+    const float scorr = ldexpf(2.0f, ew);
+    // wq[kb]: normalised W of modes 16 kb + 4 g + q in dword q
+    uint32_t V[16];   // [4 kb + q]: (Re V, -Im V) of mode 16 kb + 4 g + q, column a = 64 qa + c
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+        uint4 tq = T64[((qa & 1) * 4 + kb) * 64 + lane];
+        if (ROWU2 > 2048 && qa >= 2) {   // wave-uniform
+            const uint4 z8 = Zt[16 + kb * 4 + g];
+            tq = make_uint4(cmul(tq.x, z8.x), cmul(tq.y, z8.y), cmul(tq.z, z8.z), cmul(tq.w, z8.w));
+        }
+        // conj(V) = conj(W) conj(Abar^{64 a}), stored (Re V, -Im V)
+        V[4 * kb + 0] = cmulc(wq[kb].x ^ 0x80000000u, tq.x);
+        V[4 * kb + 1] = cmulc(wq[kb].y ^ 0x80000000u, tq.y);
+        V[4 * kb + 2] = cmulc(wq[kb].z ^ 0x80000000u, tq.z);
+        V[4 * kb + 3] = cmulc(wq[kb].w ^ 0x80000000u, tq.w);
+    }
+    const f4_t z = {0.f, 0.f, 0.f, 0.f};
+    const uint2 *Uo = (const uint2 *)U;
+#pragma unroll
+    for (int jb = 0; jb < 4; ++jb) {
+        if (jb > 0) {
+            // a += 16: V <- V Abar^1024, i.e. the stored conj(V) times conj(Abar^1024)
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) {
+                const uint4 zq = Zt[kb * 4 + g];
+                V[4 * kb + 0] = cmulc(V[4 * kb + 0], zq.x);
+                V[4 * kb + 1] = cmulc(V[4 * kb + 1], zq.y);
+                V[4 * kb + 2] = cmulc(V[4 * kb + 2], zq.z);
+                V[4 * kb + 3] = cmulc(V[4 * kb + 3], zq.w);
+            }
+        }
+#pragma unroll
+        for (int ib = 0; ib < 4; ++ib) {
+            f4_t D = z;
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+                D = mfma_acc(__builtin_bit_cast(h8_t, CA[(ib * 4 + kb) * 64 + lane]),
+                             h8_of(V[4 * kb], V[4 * kb + 1], V[4 * kb + 2], V[4 * kb + 3]), D);
+            // rows b = 16 ib + 4 g + jj, column a = 64 qa + 16 jb + c
+            const int t = 4096 * qa + 1024 * jb + 64 * c + 16 * ib + 4 * g;
+            const uint2 o = Uo[row * ROWU2 + (t >> 2)];
+            const uint2 r = make_uint2(pack_out<DT>(fmaf(D[0], scorr, lo_f<DT>(o.x)), fmaf(D[1], scorr, hi_f<DT>(o.x))),
+                                       pack_out<DT>(fmaf(D[2], scorr, lo_f<DT>(o.y)), fmaf(D[3], scorr, hi_f<DT>(o.y))));
+            *(uint2 *)(yrow + t) = r;
+        }
+    }
+}
+
 }  // namespace wvc
 }  // namespace h3

@@ -275,6 +275,12 @@ def test_config3_full_size(h3):
     _sp_check(h3, workloads.config(3), 2e-2, 2e-2)
 
 
+def test_config3_full_size_chunk16384(h3):
+    """The same workload with chunk 16384, the raised fused limit: every row
+    and every final state against the float64 recurrence."""
+    _sp_check(h3, workloads.config(3, chunk=16384), 2e-2, 2e-2)
+
+
 @pytest.mark.parametrize("dtype", [workloads.F16, workloads.BF16])
 def test_statepass_mfma_chunks(h3, dtype):
     """Chunk 8192 (the paper's fused limit) runs the matrix-core conv per chunk
@@ -305,10 +311,13 @@ def test_fftconv_l16384_impulse(h3):
     check(y, ref, 2e-2)
 
 
-@pytest.mark.parametrize("dtype,B,H,nchunk", [(workloads.F16, 2, 2, 2), (workloads.BF16, 2, 3, 3)])
+@pytest.mark.parametrize("dtype,B,H,nchunk", [(workloads.F16, 2, 2, 2), (workloads.BF16, 2, 3, 3),
+                                            (workloads.F16, 1, 4, 5)])
 def test_statepass_chunk16384(h3, dtype, B, H, nchunk):
     """Chunk 16384: chunk end-states on the matrix cores (the 16384 instance
-    of the chunk-state kernel), the 32768-point conv per chunk."""
+    of the chunk-state kernel), the 32768-point conv per chunk pair with the
+    initial-state term computed in its read-out (odd chunk counts leave a
+    last pair with one chunk)."""
     w = workloads.statepass_workload("t", B, H, nchunk * 16384, 16384, dtype, seed=8 + H, dt_lo=1e-4,
                                      dt_hi=1e-2, x0_scale=0.5)
     _sp_check(h3, w, TOL[dtype], 2e-2)
