@@ -271,8 +271,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     issue(r0);
     for (int rr = r0; rr < r1; ++rr) {
         // this row's copies landed for this wave, then for every wave; the
-        // reads of the buffer refilled below (the previous row's) are done
-        __builtin_amdgcn_s_waitcnt(0xf70);   // vmcnt(0)
+        // reads of the buffer refilled below (the previous row's) are done.
+        // lgkmcnt(0) as well: the previous row's sums, written to res by
+        // every wave, must have reached LDS before wave 0 reads them below
+        // (a barrier alone does not wait for LDS writes in flight)
+        __builtin_amdgcn_s_waitcnt(0x070);   // vmcnt(0) lgkmcnt(0)
         asm volatile("s_barrier" ::: "memory");
         if (w == 0 && rr > r0) store_row(rr - 1);
         issue(rr + 1);
