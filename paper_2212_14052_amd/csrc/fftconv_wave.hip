@@ -126,52 +126,52 @@ __device__ __forceinline__ void forward_front(uint32_t (&d)[64], const uint4 *Lc
     for (int i = 0; i < 64; ++i) d[i] = e[i];
     swap_GT(d);
 }
-// L1^H with the output epilogue: fp32 outputs (times rema / remb when REM), plus the
-// correction term (read for every lane: outputs of lanes g >= 2 and of a
-// missing row b are discarded), packed two tiles at a time into d (row a in
-// d[8 s + i], row b in d[8 s + 4 + i], points 2 s and 2 s + 1).
+// L1^H with the output epilogue.  Only outputs p2 < 8 (t < L) are kept, so
+// one MFMA per tile suffices: its matrix Fc stacks the real rows 0..7 (rows
+// 0..7 of the product: row a) over the imaginary rows 0..7 (rows 8..15: row
+// b).  Lane (g, c) then holds, for tile tau, the outputs p2 = 4 (g & 1) + i,
+// p1 = c, p0 = tau of row a (g < 2) or row b (g >= 2), times rem (REM), plus
+// the correction term of that row (CORR), packed two tiles at a time into
+// d[8 s + i] (points p0 = 2 s, 2 s + 1).
 template <int DT, int CORR, bool REM>
-__device__ __forceinline__ void out_layer(uint32_t (&d)[64], const Dft &Fs, float rema, float remb, const void *corr,
-                                          long oa, long obc, int lane) {
+__device__ __forceinline__ void out_layer(uint32_t (&d)[64], const h8_t &Fc, float rem, const void *corr,
+                                          long orow, int lane) {
     const int g = lane >> 4, c = lane & 15;
-    const int pbase = 256 * (4 * (g & 1)) + 16 * c;   // lanes g >= 2 alias g - 2 (in bounds)
-    float pr[8];   // previous (even) tile's outputs: rows a and b
-    layer<false>(d, Fs, NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
-        float ya[4], yb[4];
+    const int pbase = 256 * (4 * (g & 1)) + 16 * c;
+    float pr[4];   // previous (even) tile's outputs
+    auto mm = [&](int tau) {
+        h8_t x = h8_of(d[4 * tau], d[4 * tau + 1], d[4 * tau + 2], d[4 * tau + 3]);
+        asm volatile("" : "+v"(x));
+        return mfma(Fc, x);
+    };
+    f4_t v = mm(0);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            ya[i] = REM ? re[i] * rema : re[i];
-            yb[i] = REM ? im[i] * remb : im[i];
-        }
+    for (int tau = 0; tau < 16; ++tau) {
+        f4_t v1;
+        if (tau + 1 < 16) v1 = mm(tau + 1);
+        float yv[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) yv[i] = REM ? v[i] * rem : v[i];
         if (CORR != 0) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int p = pbase + 256 * i + tau;
-                if (CORR == 2) {
-                    const uint16_t *cr = (const uint16_t *)corr;
-                    ya[i] += lo_f<DT>(cr[oa + p]);
-                    yb[i] += lo_f<DT>(cr[obc + p]);
-                } else {
-                    const float *cr = (const float *)corr;
-                    ya[i] += cr[oa + p];
-                    yb[i] += cr[obc + p];
-                }
+                if (CORR == 2)
+                    yv[i] += lo_f<DT>(((const uint16_t *)corr)[orow + p]);
+                else
+                    yv[i] += ((const float *)corr)[orow + p];
             }
         }
         if ((tau & 1) == 0) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                pr[i] = ya[i];
-                pr[4 + i] = yb[i];
-            }
+            for (int i = 0; i < 4; ++i) pr[i] = yv[i];
         } else {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                d[4 * (tau - 1) + i] = pack_out<DT>(pr[i], ya[i]);
-                d[4 * tau + i] = pack_out<DT>(pr[4 + i], yb[i]);
-            }
+            for (int i = 0; i < 4; ++i) d[4 * (tau - 1) + i] = pack_out<DT>(pr[i], yv[i]);
         }
-    });
+        __builtin_amdgcn_sched_barrier(0);
+        v = v1;
+    }
 }
 
 }  // namespace wv
@@ -495,34 +495,43 @@ fftconv_wave4096_kernel(ConvArgs a, const float *k, int wg_per_ch, int pairs_per
         // allows; any remainder is applied in fp32.
         long oa, ob;
         rows(qq, oa, ob);
-        // The real rows of L1^H make row a, the imaginary rows row b: each
-        // carries its own row's scale.
+        // The real rows of L1^H make row a (lanes g < 2 of the product), the
+        // imaginary rows row b (lanes g >= 2): each carries its own row's scale.
         const int sea = kexp + eua, seb = kexp + eub;
         const int sfa = min(max(sea, -10), 14), srema = sea - sfa;
         const int sfb = min(max(seb, -10), 14), sremb = seb - sfb;
-        Dft Fs = lc_dft<CT>(Lc, lane, true);
-        Fs.re = h8_scale(Fs.re, (_Float16)ldexpf(1.0f, sfa));
-        Fs.im = h8_scale(Fs.im, (_Float16)ldexpf(1.0f, sfb));
+        const bool lane_b = g >= 2;
+        h8_t Fc;
+        {
+            asm volatile("" ::: "memory");
+            const bool hi = c >= 8;   // imaginary rows: lane c - 8's imaginary DFT row
+            uint4 r;
+            if constexpr (!CT) {
+                r = hi ? Lc[3 * 64 + lane - 8] : Lc[2 * 64 + lane];
+            } else {
+                r = hi ? Lc[64 + lane - 8] : Lc[lane];
+                const uint32_t f = hi ? 0x8000u : 0x80000000u;
+                r = make_uint4(r.x ^ f, r.y ^ f, r.z ^ f, r.w ^ f);
+            }
+            Fc = h8_scale(__builtin_bit_cast(h8_t, r), (_Float16)ldexpf(1.0f, hi ? sfb : sfa));
+        }
         // branch-free epilogue (a branch inside it lets the compiler hoist
         // all of the layer's MFMAs above it); the rare remainder scale picks
         // a second instance of the layer instead
         const long obc = ob >= 0 ? ob : oa;   // row b's correction read from row a if absent
+        const long orow = lane_b ? obc : oa;
         if ((srema | sremb) == 0)
-            out_layer<DT, CORR, false>(d, Fs, 1.0f, 1.0f, a.corr, oa, obc, lane);
+            out_layer<DT, CORR, false>(d, Fc, 1.0f, a.corr, orow, lane);
         else
-            out_layer<DT, CORR, true>(d, Fs, ldexpf(1.0f, srema), ldexpf(1.0f, sremb), a.corr, oa, obc, lane);
-        if (g < 2) {
-            uint16_t *ya_row = y + oa, *yb_row = y + obc;   // wave-uniform bases
+            out_layer<DT, CORR, true>(d, Fc, ldexpf(1.0f, lane_b ? sremb : srema), a.corr, orow, lane);
+        if (!lane_b || ob >= 0) {
+            uint16_t *yrow = y + orow;
+            const int gl = g & 1;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int off = 256 * (4 * g + i) + 16 * c;
-                // row a: dwords d[8 s + i] hold points 2 s, 2 s + 1
-                *(uint4 *)(ya_row + off) = make_uint4(d[i], d[8 + i], d[16 + i], d[24 + i]);
-                *(uint4 *)(ya_row + off + 8) = make_uint4(d[32 + i], d[40 + i], d[48 + i], d[56 + i]);
-                if (ob >= 0) {
-                    *(uint4 *)(yb_row + off) = make_uint4(d[4 + i], d[12 + i], d[20 + i], d[28 + i]);
-                    *(uint4 *)(yb_row + off + 8) = make_uint4(d[36 + i], d[44 + i], d[52 + i], d[60 + i]);
-                }
+                const int off = 256 * (4 * gl + i) + 16 * c;
+                *(uint4 *)(yrow + off) = make_uint4(d[i], d[8 + i], d[16 + i], d[24 + i]);
+                *(uint4 *)(yrow + off + 8) = make_uint4(d[32 + i], d[40 + i], d[48 + i], d[56 + i]);
             }
         }
         // next pair's loads, consumed at the top of the next iteration
