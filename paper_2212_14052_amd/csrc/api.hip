@@ -456,6 +456,14 @@ int h3_layer_fwd(const void *x, const void *Wq, const void *Wk, const void *Wv, 
         ConvArgs ca{};
         ca.u = o_cm; ca.y = (void *)kk; ca.D = diag_D;
         ca.B = B; ca.H = d; ca.L = L; ca.nchunk = 1; ca.pair_mode = 0; ca.dtype = dtype;
+        if (fftconv_wave_supported(L, dtype) && gemm_w_tile(d, B * L, d)) {
+            // L = 2048: the convolution's epilogue gates with Q and writes
+            // O = Q * S channel-major into K's slot; the output projection
+            // reads it K-major
+            ca.gate = q;
+            if ((e = launch_fftconv_mfma(ca, diag_k, s)) != hipSuccess) return H3_EDEVICE;
+            return launched(launch_gemm_w(&Wo, kk, out, B * L, d, dtype, 2, d, L, s));
+        }
         if ((e = launch_fftconv_mfma(ca, diag_k, s)) != hipSuccess) return H3_EDEVICE;
         if ((e = launch_gate_transpose(q, kk, o_tm, B, d, L, dtype, s)) != hipSuccess) return H3_EDEVICE;
     } else {

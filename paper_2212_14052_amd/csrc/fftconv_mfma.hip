@@ -12,9 +12,10 @@ bool fftconv_mfma_supported(int L, int dtype) {
            fftconv_wave32k_supported(L, dtype);
 }
 
-// hipErrorInvalidValue for any other shape.
+// hipErrorInvalidValue for any other shape.  An output gate is supported at L = 2048 only.
 hipError_t launch_fftconv_mfma(const ConvArgs &a, const float *k, hipStream_t s) {
     if (fftconv_wave_supported(a.L, a.dtype)) return launch_fftconv_wave(a, k, s);
+    if (a.gate) return hipErrorInvalidValue;
     if (fftconv_wave16k_supported(a.L, a.dtype)) return launch_fftconv_wave16k(a, k, s);
     if (fftconv_wave32k_supported(a.L, a.dtype)) return launch_fftconv_wave32k(a, k, s);
     return hipErrorInvalidValue;

@@ -131,11 +131,12 @@ __device__ __forceinline__ void forward_front(uint32_t (&d)[64], const uint4 *Lc
 // 0..7 of the product: row a) over the imaginary rows 0..7 (rows 8..15: row
 // b).  Lane (g, c) then holds, for tile tau, the outputs p2 = 4 (g & 1) + i,
 // p1 = c, p0 = tau of row a (g < 2) or row b (g >= 2), times rem (REM), plus
-// the correction term of that row (CORR), packed two tiles at a time into
-// d[8 s + i] (points p0 = 2 s, 2 s + 1).
-template <int DT, int CORR, bool REM>
+// the correction term of that row (CORR), times the gate (GATE: gq[2 i + h]
+// holds the gate at points p0 = 8 h .. 8 h + 7 of output i), packed two tiles
+// at a time into d[8 s + i] (points p0 = 2 s, 2 s + 1).
+template <int DT, int CORR, bool REM, bool GATE>
 __device__ __forceinline__ void out_layer(uint32_t (&d)[64], const h8_t &Fc, float rem, const void *corr,
-                                          long orow, int lane) {
+                                          long orow, int lane, const uint4 (&gq)[8]) {
     const int g = lane >> 4, c = lane & 15;
     const int pbase = 256 * (4 * (g & 1)) + 16 * c;
     float pr[4];   // previous (even) tile's outputs
@@ -162,6 +163,15 @@ __device__ __forceinline__ void out_layer(uint32_t (&d)[64], const h8_t &Fc, flo
                     yv[i] += ((const float *)corr)[orow + p];
             }
         }
+        if constexpr (GATE) {
+            // gate values of this lane's points: gq[2 i + tau / 8], half tau % 8
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint4 q4 = gq[2 * i + (tau >> 3)];
+                const uint32_t qw = (tau & 7) < 2 ? q4.x : (tau & 7) < 4 ? q4.y : (tau & 7) < 6 ? q4.z : q4.w;
+                yv[i] *= (tau & 1) ? hi_f<DT>(qw) : lo_f<DT>(qw);
+            }
+        }
         if ((tau & 1) == 0) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) pr[i] = yv[i];
@@ -183,7 +193,8 @@ __device__ __forceinline__ void out_layer(uint32_t (&d)[64], const h8_t &Fc, flo
 // 2 hb and 2 hb + 1, both spectra computed by all four waves, then waves 0, 1
 // take the first channel's pairs and waves 2, 3 the second's, so no wave
 // idles while its workgroup holds the CU's LDS.
-template <int DT, int CORR, int CPW, bool CT = false>
+// GATE: the output is multiplied by a.gate (same layout as y) before rounding.
+template <int DT, int CORR, int CPW, bool CT = false, bool GATE = false>
 __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(CPW == 1 || CT ? 3 : 2))) void
 fftconv_wave4096_kernel(ConvArgs a, const float *k, int wg_per_ch, int pairs_per_ch) {
     using namespace wv;
@@ -520,10 +531,21 @@ fftconv_wave4096_kernel(ConvArgs a, const float *k, int wg_per_ch, int pairs_per
         // a second instance of the layer instead
         const long obc = ob >= 0 ? ob : oa;   // row b's correction read from row a if absent
         const long orow = lane_b ? obc : oa;
+        // gate of the lane's 64 outputs (row a or b; a missing row b reads row a's)
+        uint4 gq[8];
+        if constexpr (GATE) {
+            const uint16_t *grow = (const uint16_t *)a.gate + orow;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int off = 256 * (4 * (g & 1) + i) + 16 * c;
+                gq[2 * i] = *(const uint4 *)(grow + off);
+                gq[2 * i + 1] = *(const uint4 *)(grow + off + 8);
+            }
+        }
         if ((srema | sremb) == 0)
-            out_layer<DT, CORR, false>(d, Fc, 1.0f, a.corr, orow, lane);
+            out_layer<DT, CORR, false, GATE>(d, Fc, 1.0f, a.corr, orow, lane, gq);
         else
-            out_layer<DT, CORR, true>(d, Fc, ldexpf(1.0f, lane_b ? sremb : srema), a.corr, orow, lane);
+            out_layer<DT, CORR, true, GATE>(d, Fc, ldexpf(1.0f, lane_b ? sremb : srema), a.corr, orow, lane, gq);
         if (!lane_b || ob >= 0) {
             uint16_t *yrow = y + orow;
             const int gl = g & 1;
@@ -872,20 +894,36 @@ hipError_t launch_fftconv_wave(const ConvArgs &a, const float *k, hipStream_t s)
         // -> 20 us at H = 768)
         const dim3 grid2((a.H + 1) / 2);
         const bool ct = grid2.x >= 512;
-#define H3_WAVE2_LAUNCH(DTV, CTV) \
-    hipLaunchKernelGGL((fftconv_wave4096_kernel<DTV, 0, 2, CTV>), grid2, block, 0, s, a, k, 1, pairs_per_ch)
+#define H3_WAVE2_LAUNCH(DTV, CTV, GV) \
+    hipLaunchKernelGGL((fftconv_wave4096_kernel<DTV, 0, 2, CTV, GV>), grid2, block, 0, s, a, k, 1, pairs_per_ch)
+#define H3_WAVE2_CT(DTV, GV) \
+    do {                                   \
+        if (ct) H3_WAVE2_LAUNCH(DTV, true, GV); \
+        else H3_WAVE2_LAUNCH(DTV, false, GV);   \
+    } while (0)
         if (a.dtype == F16) {
-            if (ct) H3_WAVE2_LAUNCH(F16, true);
-            else H3_WAVE2_LAUNCH(F16, false);
+            if (a.gate) H3_WAVE2_CT(F16, true);
+            else H3_WAVE2_CT(F16, false);
         } else {
-            if (ct) H3_WAVE2_LAUNCH(BF16, true);
-            else H3_WAVE2_LAUNCH(BF16, false);
+            if (a.gate) H3_WAVE2_CT(BF16, true);
+            else H3_WAVE2_CT(BF16, false);
         }
+#undef H3_WAVE2_CT
 #undef H3_WAVE2_LAUNCH
         return hipGetLastError();
     }
 #define H3_WAVE_LAUNCH(DTV, CV) \
     hipLaunchKernelGGL((fftconv_wave4096_kernel<DTV, CV, 1>), grid, block, 0, s, a, k, wg_per_ch, pairs_per_ch)
+    if (a.gate) {
+        if (corr != 0 || a.pair_mode != 0) return hipErrorInvalidValue;
+        if (a.dtype == F16)
+            hipLaunchKernelGGL((fftconv_wave4096_kernel<F16, 0, 1, false, true>), grid, block, 0, s, a, k, wg_per_ch,
+                               pairs_per_ch);
+        else
+            hipLaunchKernelGGL((fftconv_wave4096_kernel<BF16, 0, 1, false, true>), grid, block, 0, s, a, k, wg_per_ch,
+                               pairs_per_ch);
+        return hipGetLastError();
+    }
     if (a.dtype == F16) {
         if (corr == 0) H3_WAVE_LAUNCH(F16, 0);
         else if (corr == 1) H3_WAVE_LAUNCH(F16, 1);

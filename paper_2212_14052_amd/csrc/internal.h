@@ -51,6 +51,10 @@ struct ConvArgs {
     // y[t] = sum_{s>=t} k[s-t] u[s] (+ D u[t]), the input gradient of the
     // convolution.  Supported by the wave kernels and the VALU kernel.
     int conj_k;
+    // gate (mode 0, L = 2048 wave kernel only; may be null): y = gate * (the
+    // convolution + D u), elementwise, gate in the I/O dtype and layout of y
+    // (the output gating of the H3 layer, O = Q * S)
+    const void *gate;
 };
 hipError_t launch_fftconv(const ConvArgs &a, hipStream_t s);
 // The VALU convolution of plain (B, H, L) rows (pair_mode 0, no correction
@@ -141,7 +145,8 @@ hipError_t launch_heads_contract(int dh, const void *q, const void *sv, void *o,
 // weights as stored, (K, d) row-major (Q = x W): out_mode 1: W[0..2] = W_Q,
 // W_K, W_V into the channel-major [Q;K;V] layout as launch_gemm_nt
 // (out_mode 1); out_mode 0: W[0] = W_O, C = X W_O row-major (Nx, d).  X is
-// (Nx, K) row-major.  gemm_w_tile gives the tile height (0: not supported:
+// (Nx, K) row-major; out_mode 2: as out_mode 0 with X stored K-major,
+// (Nx / L, K, L) (needs L % 256 == 0).  gemm_w_tile gives the tile height (0: not supported:
 // needs Nx % 256 == 0, K % 32 == 0, d a multiple of 320 or 256).
 int gemm_w_tile(int d, int Nx, int K);
 hipError_t launch_gemm_w(const void *const *W, const void *X, void *C, int Nx, int K, int dtype, int out_mode, int d,

@@ -272,14 +272,16 @@ typedef __attribute__((address_space(3))) gw_v4s lds_v4s;
 
 __device__ __forceinline__ int gw_xoff(int row, int chunk) { return row * 64 + ((chunk ^ ((row >> 2) & 3)) << 4); }
 
-template <int TW, int SS> struct GwShape {
+template <int TW, int SS, bool XKM> struct GwShape {
     static constexpr int WP = 2 * TW + 64;            // weight row pitch, bytes (704 or 576)
     static constexpr int WB = GW_K * WP;              // weight part of a stage, bytes
     static constexpr int WS = WB / 1024;              // its slices (22 or 18)
-    static constexpr int XS = GW_X * 64 / 1024;       // activation slices (16)
+    static constexpr int XP = 2 * GW_X + 64;          // K-major activation row pitch, bytes (576)
+    static constexpr int XB = XKM ? GW_K * XP : GW_X * 64;   // activation part of a stage, bytes
+    static constexpr int XS = XB / 1024;              // its slices (18 or 16)
     static constexpr int SLICES = WS + XS;
     static constexpr int NSL = (SLICES + 7) / 8;      // copies per wave per step (5)
-    static constexpr int STAGE_B = WB + GW_X * 64;    // bytes per stage
+    static constexpr int STAGE_B = WB + XB;           // bytes per stage
     static constexpr int TI = TW / 64;                // weight-side MFMA tiles per wave
     static_assert(WB % 1024 == 0 && (WP % 256 == 64 || WP % 256 == 192), "weight stage layout");
     // LDS bytes: the stages, and a 1 KB slot that takes the copies of waves
@@ -293,11 +295,17 @@ template <int TW, int SS> struct GwShape {
     static constexpr int WAIT = 0xf70 | (INFL & 15) | ((INFL >> 4) << 14);
 };
 
+// OUT 2: as OUT 0, with the activations stored K-major, (B, K, L) with row
+// n = b L + t of X at column t of batch b (the gated O of the layer as the
+// convolution writes it, channel-major): a stage then holds 32 rows (k) of
+// 256 activation rows, pitch XP, and the fragments are read with transposing
+// LDS reads like the weights.
 template <int DT, int OUT, int TW, int SS>
 __global__ __launch_bounds__(GW_T) __attribute__((amdgpu_waves_per_eu(2, 2))) void gemm_w(
     const uint16_t *W0, const uint16_t *W1, const uint16_t *W2, const uint16_t *X, uint16_t *C, int Mw, int Nx,
     int K, int ldw, int d, int L) {
-    using S = GwShape<TW, SS>;
+    constexpr bool XKM = OUT == 2;
+    using S = GwShape<TW, SS, XKM>;
     extern __shared__ __attribute__((aligned(1024))) uint16_t gw_lds[];
     int tw, tx;
     gemm_tile(Mw / TW, Nx / GW_X, tw, tx);
@@ -320,6 +328,11 @@ __global__ __launch_bounds__(GW_T) __attribute__((amdgpu_waves_per_eu(2, 2))) vo
             const int b = 1024 * q + 16 * lane;
             const int r = b / S::WP, c = b % S::WP;
             soff[sl] = (uint32_t)(r * ldw + wc + (c < 2 * TW ? c / 2 : 0));
+        } else if constexpr (XKM) {
+            // rows k of the tile's 256 activation rows, which lie in batch x0 / L
+            const int b = 1024 * (q - S::WS) + 16 * lane;
+            const int r = b / S::XP, c = b % S::XP;
+            soff[sl] = (uint32_t)((x0 / L) * K * L + (x0 % L) + r * L + (c < 2 * GW_X ? c / 2 : 0));
         } else {
             const int r = 16 * (q - S::WS) + (lane >> 2);
             const int c = (lane & 3) ^ ((r >> 2) & 3);
@@ -343,7 +356,7 @@ __global__ __launch_bounds__(GW_T) __attribute__((amdgpu_waves_per_eu(2, 2))) vo
             const bool real = q < S::SLICES;
             const bool wside = (real ? q : wvu) < S::WS;
             const uint16_t *base = wside ? Wj : X;
-            const uint32_t vo = 2 * (soff[sl] + k0 * (wside ? (uint32_t)ldw : 1u));
+            const uint32_t vo = 2 * (soff[sl] + k0 * (wside ? (uint32_t)ldw : (XKM ? (uint32_t)L : 1u)));
             const uint32_t la = real ? st + (uint32_t)q * 1024 : lds0 + (uint32_t)(GW_NS * S::STAGE_B);
             asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, %2"
                          :
@@ -364,6 +377,7 @@ __global__ __launch_bounds__(GW_T) __attribute__((amdgpu_waves_per_eu(2, 2))) vo
     // for the upper 16 lanes of each 32
     const int tr_row = (lane & 15) >> 2, tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
     const int tr_base = tr_row * S::WP + 2 * (ww * (TW / 2) + tr_col);
+    const int trx_base = tr_row * S::XP + 2 * (wx * 64 + tr_col);
 #pragma unroll
     for (int p = 0; p < GW_NS - SS; ++p) issue(p);
     for (int k0 = 0; k0 < nk; k0 += SS) {
@@ -392,10 +406,22 @@ __global__ __launch_bounds__(GW_T) __attribute__((amdgpu_waves_per_eu(2, 2))) vo
                     const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
                     fw[i] = make_uint4(l2.x, l2.y, h2.x, h2.y);
                 }
-                const int ch = 2 * ks + (lane >> 5);
+                if constexpr (XKM) {
+                    // activation rows wx 64 + 32 j + (lane & 31), k as for the weights
+                    const char *xr = xs + (16 * ks + 8 * (lane >> 5)) * S::XP + trx_base;
 #pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    fx[j] = *(const uint4 *)(xs + gw_xoff(wx * 64 + j * 32 + (lane & 31), ch));
+                    for (int j = 0; j < 2; ++j) {
+                        const gw_v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s *)(xr + 64 * j));
+                        const gw_v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s *)(xr + 4 * S::XP + 64 * j));
+                        const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
+                        fx[j] = make_uint4(l2.x, l2.y, h2.x, h2.y);
+                    }
+                } else {
+                    const int ch = 2 * ks + (lane >> 5);
+#pragma unroll
+                    for (int j = 0; j < 2; ++j)
+                        fx[j] = *(const uint4 *)(xs + gw_xoff(wx * 64 + j * 32 + (lane & 31), ch));
+                }
 #pragma unroll
                 for (int i = 0; i < S::TI; ++i)
 #pragma unroll
@@ -897,7 +923,7 @@ template <int DT, int OUT, int TW>
 static hipError_t launch_gemm_w_t(const void *const *W, const void *X, void *C, int Mw, int Nx, int K, int ldw, int d,
                                   int L, hipStream_t s) {
     constexpr int SS = 1;
-    const size_t lds = GwShape<TW, SS>::LDS;
+    const size_t lds = GwShape<TW, SS, OUT == 2>::LDS;
     auto fn = gemm_w<DT, OUT, TW, SS>;
     (void)hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     hipLaunchKernelGGL(fn, dim3((Mw / TW) * (Nx / GW_X)), dim3(GW_T), lds, s, (const uint16_t *)W[0],
@@ -917,17 +943,20 @@ template <int DT>
 static hipError_t launch_gemm_w_dt(const void *const *W, const void *X, void *C, int Mw, int Nx, int K, int ldw,
                                    int out_mode, int d, int L, int tw, hipStream_t s) {
     if (tw == 320)
-        return out_mode ? launch_gemm_w_t<DT, 1, 320>(W, X, C, Mw, Nx, K, ldw, d, L, s)
-                        : launch_gemm_w_t<DT, 0, 320>(W, X, C, Mw, Nx, K, ldw, d, L, s);
-    return out_mode ? launch_gemm_w_t<DT, 1, 256>(W, X, C, Mw, Nx, K, ldw, d, L, s)
-                    : launch_gemm_w_t<DT, 0, 256>(W, X, C, Mw, Nx, K, ldw, d, L, s);
+        return out_mode == 1 ? launch_gemm_w_t<DT, 1, 320>(W, X, C, Mw, Nx, K, ldw, d, L, s)
+               : out_mode == 2 ? launch_gemm_w_t<DT, 2, 320>(W, X, C, Mw, Nx, K, ldw, d, L, s)
+                               : launch_gemm_w_t<DT, 0, 320>(W, X, C, Mw, Nx, K, ldw, d, L, s);
+    return out_mode == 1 ? launch_gemm_w_t<DT, 1, 256>(W, X, C, Mw, Nx, K, ldw, d, L, s)
+           : out_mode == 2 ? launch_gemm_w_t<DT, 2, 256>(W, X, C, Mw, Nx, K, ldw, d, L, s)
+                           : launch_gemm_w_t<DT, 0, 256>(W, X, C, Mw, Nx, K, ldw, d, L, s);
 }
 
 hipError_t launch_gemm_w(const void *const *W, const void *X, void *C, int Nx, int K, int dtype, int out_mode, int d,
                          int L, hipStream_t s) {
     const int tw = gemm_w_tile(d, Nx, K);
     if (!tw) return hipErrorInvalidValue;
-    const int Mw = out_mode ? 3 * d : d;
+    if (out_mode == 2 && L % GW_X != 0) return hipErrorInvalidValue;
+    const int Mw = out_mode == 1 ? 3 * d : d;
     return dtype == BF16 ? launch_gemm_w_dt<BF16>(W, X, C, Mw, Nx, K, d, out_mode, d, L, tw, s)
                          : launch_gemm_w_dt<F16>(W, X, C, Mw, Nx, K, d, out_mode, d, L, tw, s);
 }
