@@ -523,7 +523,8 @@ def test_layer_small(h3, dtype):
 
 
 # L = 2048 and 8192 take the matrix-core shift SSM, the wave FFT conv and the
-# gated transpose; an odd batch leaves the last row pair half empty, fewer than
+# gated transpose (d = 128 is no multiple of the output GEMM's weight tiles,
+# so L = 2048 keeps the transpose here too); an odd batch leaves the last row pair half empty, fewer than
 # 64 shift taps leave zeros in the Toeplitz band, and a shift D adds to its
 # diagonal.  L = 4096 takes the fused VALU middle kernel, L = 16384 the
 # 32768-point conv.
@@ -566,6 +567,20 @@ def test_layer_heads(h3, dtype, B, L, dh, with_D):
     dD = rng.standard_normal(d * dh).astype(np.float32) if with_D else None
     sD = rng.standard_normal(d).astype(np.float32) if with_D else None
     y, ref = _layer_run(h3, w, k32, shift_D=sD, diag_D=dD, d_head=dh)
+    check(y, ref, 2e-2)
+
+
+# L = 2048 with d a multiple of 256 or 320: the convolution's epilogue gates
+# with Q and writes O channel-major, and the output projection reads O
+# K-major.  Odd batches leave a half-empty last row pair; B = 6 takes the
+# one-channel-per-workgroup conv, B <= 4 the two-channel one (with and without
+# the compact table); d = 256 and 768 take the 256-wide weight tiles, 1280 the
+# 320-wide ones.
+@pytest.mark.parametrize("dtype", [workloads.BF16, workloads.F16])
+@pytest.mark.parametrize("B,d", [(3, 256), (6, 256), (4, 768), (1, 1280)])
+def test_layer_gated_conv(h3, dtype, B, d):
+    w = workloads.layer_workload("t", B, 2048, d, dtype, seed=41 + B + d)
+    y, ref = _layer_case(h3, w)
     check(y, ref, 2e-2)
 
 
