@@ -131,14 +131,23 @@ __device__ __forceinline__ void forward_front(uint32_t (&d)[64], const uint4 *Lc
 // 0..7 of the product: row a) over the imaginary rows 0..7 (rows 8..15: row
 // b).  Lane (g, c) then holds, for tile tau, the outputs p2 = 4 (g & 1) + i,
 // p1 = c, p0 = tau of row a (g < 2) or row b (g >= 2), times rem (REM), plus
-// the correction term of that row (CORR), times the gate (GATE: gq[2 i + h]
-// holds the gate at points p0 = 8 h .. 8 h + 7 of output i), packed two tiles
-// at a time into d[8 s + i] (points p0 = 2 s, 2 s + 1).
+// the correction term of that row (CORR), times the gate (GATE: the same
+// points of the row at grow), packed two tiles at a time into d[8 s + i]
+// (points p0 = 2 s, 2 s + 1).
 template <int DT, int CORR, bool REM, bool GATE>
 __device__ __forceinline__ void out_layer(uint32_t (&d)[64], const h8_t &Fc, float rem, const void *corr,
-                                          long orow, int lane, const uint4 (&gq)[8]) {
+                                          long orow, int lane, const uint16_t *grow) {
     const int g = lane >> 4, c = lane & 15;
     const int pbase = 256 * (4 * (g & 1)) + 16 * c;
+    // gate: gq[2 i + h] holds the gate at points p0 = 8 h .. 8 h + 7 of output
+    // i; the second half (h = 1) is loaded while tiles 3 .. 7 run, so that
+    // only 16 registers of it are live at a time
+    uint4 gq[8];
+    auto gate_loads = [&](int hh) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) gq[2 * i + hh] = *(const uint4 *)(grow + pbase + 256 * i + 8 * hh);
+    };
+    if constexpr (GATE) gate_loads(0);
     float pr[4];   // previous (even) tile's outputs
     auto mm = [&](int tau) {
         h8_t x = h8_of(d[4 * tau], d[4 * tau + 1], d[4 * tau + 2], d[4 * tau + 3]);
@@ -150,6 +159,7 @@ __device__ __forceinline__ void out_layer(uint32_t (&d)[64], const h8_t &Fc, flo
     for (int tau = 0; tau < 16; ++tau) {
         f4_t v1;
         if (tau + 1 < 16) v1 = mm(tau + 1);
+        if (GATE && tau == 3) gate_loads(1);
         float yv[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) yv[i] = REM ? v[i] * rem : v[i];
@@ -532,20 +542,11 @@ fftconv_wave4096_kernel(ConvArgs a, const float *k, int wg_per_ch, int pairs_per
         const long obc = ob >= 0 ? ob : oa;   // row b's correction read from row a if absent
         const long orow = lane_b ? obc : oa;
         // gate of the lane's 64 outputs (row a or b; a missing row b reads row a's)
-        uint4 gq[8];
-        if constexpr (GATE) {
-            const uint16_t *grow = (const uint16_t *)a.gate + orow;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int off = 256 * (4 * (g & 1) + i) + 16 * c;
-                gq[2 * i] = *(const uint4 *)(grow + off);
-                gq[2 * i + 1] = *(const uint4 *)(grow + off + 8);
-            }
-        }
+        const uint16_t *grow = GATE ? (const uint16_t *)a.gate + orow : nullptr;
         if ((srema | sremb) == 0)
-            out_layer<DT, CORR, false, GATE>(d, Fc, 1.0f, a.corr, orow, lane, gq);
+            out_layer<DT, CORR, false, GATE>(d, Fc, 1.0f, a.corr, orow, lane, grow);
         else
-            out_layer<DT, CORR, true, GATE>(d, Fc, ldexpf(1.0f, lane_b ? sremb : srema), a.corr, orow, lane, gq);
+            out_layer<DT, CORR, true, GATE>(d, Fc, ldexpf(1.0f, lane_b ? sremb : srema), a.corr, orow, lane, grow);
         if (!lane_b || ob >= 0) {
             uint16_t *yrow = y + orow;
             const int gl = g & 1;
