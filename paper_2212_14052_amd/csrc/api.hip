@@ -184,8 +184,13 @@ int statepass_run(const void *u, const float *Abar, const float *Bbar, const flo
     // f = [C Bbar, C Abar Bbar, ...] of length chunk, and its spectrum
     if ((e = launch_kernel_gen(1, Abar, Bbar, C, nullptr, H, m, chunk, kbuf, s)) != hipSuccess) return H3_EDEVICE;
     if (!w.mfma && (e = launch_spectrum(kbuf, H, chunk, Kspec, s)) != hipSuccess) return H3_EDEVICE;
-    // s_c = M_ux u^(c) for every chunk, then the scan over chunks
-    if ((e = launch_chunk_states(u, Abar, Bbar, B, H, L, m, chunk, dtype, states, s)) != hipSuccess)
+    // s_c = M_ux u^(c) for every chunk, then the scan over chunks (for the
+    // fused term, inside the chunk-state kernel when it covers each channel
+    // with one workgroup)
+    StateTail tail{C, x0, (uint32_t *)(ws + w.w16), (int *)(ws + w.wexp), x_final, (uint4 *)(ws + w.ctab), 0};
+    bool fused_tail = false;
+    if ((e = launch_chunk_states(u, Abar, Bbar, B, H, L, m, chunk, dtype, states, s, w.fused ? &tail : nullptr,
+                                 &fused_tail)) != hipSuccess)
         return H3_EDEVICE;
     ConvArgs a{};
     a.u = u; a.y = y; a.Kspec = Kspec; a.D = D;
@@ -196,10 +201,12 @@ int statepass_run(const void *u, const float *Abar, const float *Bbar, const flo
         uint4 *ctab = (uint4 *)(ws + w.ctab);
         uint32_t *w16 = (uint32_t *)(ws + w.w16);
         int *wexp = (int *)(ws + w.wexp);
-        if ((e = launch_state_scan_w16(Abar, C, x0, states, B, H, m, chunk, nchunk, w16, wexp, x_final, s)) !=
-            hipSuccess)
-            return H3_EDEVICE;
-        if ((e = launch_corr_tables(Abar, H, m, ctab, s)) != hipSuccess) return H3_EDEVICE;
+        if (!fused_tail) {
+            if ((e = launch_state_scan_w16(Abar, C, x0, states, B, H, m, chunk, nchunk, w16, wexp, x_final, s)) !=
+                hipSuccess)
+                return H3_EDEVICE;
+            if ((e = launch_corr_tables(Abar, H, m, ctab, s)) != hipSuccess) return H3_EDEVICE;
+        }
         a.corr = w16;
         a.corr_tab = ctab;
         a.corr_e = wexp;

@@ -97,8 +97,22 @@ hipError_t launch_wgrad_wave(const void *u, const void *dy, int B, int H, int dt
 size_t wgrad_wave_workspace(int B, int H);
 
 // State passing pieces.
+// Optional tail of the matrix-core chunk-state kernel (chunk 8192 or 16384):
+// when one workgroup covers a channel it also writes the channel's table of
+// the fused state term (ctab, as launch_corr_tables) and the scan of its rows
+// (w16, wexp, x_final, as launch_state_scan_w16); *fused tells whether it did.
+struct StateTail {
+    const float *C;
+    const float *x0;
+    uint32_t *w16;
+    int *wexp;
+    float *x_final;
+    uint4 *ctab;
+    int fuse;
+};
 hipError_t launch_chunk_states(const void *u, const float *Abar, const float *Bbar, int B, int H,
-                               int L, int m, int chunk, int dtype, float2 *states, hipStream_t s);
+                               int L, int m, int chunk, int dtype, float2 *states, hipStream_t s,
+                               const StateTail *tail = nullptr, bool *fused = nullptr);
 hipError_t launch_state_scan(const float *Abar, const float *C, const float *x0,
                              const float2 *states, int B, int H, int m, int chunk, int nchunk,
                              float2 *corr_W, float *x_final, hipStream_t s);

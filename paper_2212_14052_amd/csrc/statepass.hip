@@ -160,10 +160,15 @@ typedef __attribute__((address_space(3))) void cs_lds_t;
 // slot for the copies of waves with one slice less
 size_t chunk_states_lds(int chunk) { return (size_t)CS_NS * chunk * 2 + 2 * 64 * 8 + 1024; }
 
+__device__ void cs_state_tail(const StateTail &t, const float *Abar, const float2 *states, int B, int H, int m,
+                              int chunk, int nchunk, int h, uint4 *lds);
+
+// tail.fuse (one workgroup per channel, chunk 8192 or 16384): the workgroup
+// also writes the channel's fused-term table and scans its rows (cs_state_tail)
 template <int DT, int BW, int CMAX>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void chunk_states_mfma(
     const uint16_t *u, const float *Abar, const float *Bbar, int B, int H, int L, int m, int chunk, int wg_per_ch,
-    float2 *states) {
+    float2 *states, StateTail tail) {
     constexpr int KS = BW / 32;          // 32-wide reduction steps per block
     constexpr int RB = 2 * BW;           // bytes per LDS row
     constexpr int SPR = RB / 16;         // 16-byte slots per LDS row
@@ -320,6 +325,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     }
     __syncthreads();   // the last row's sums are in LDS; every copy has landed
     if (w == 0) store_row(r1 - 1);
+    if (tail.fuse) {
+        // every chunk sum of the channel is written and visible to the
+        // workgroup (a workgroup-scope fence: the readers are this
+        // workgroup's waves, and a device-scope one would write back the
+        // L2); the row ring is free for the table
+        __threadfence_block();
+        __syncthreads();
+        cs_state_tail(tail, Abar, states, B, H, m, chunk, nchunk, h, (uint4 *)cs_lds);
+    }
 }
 
 bool chunk_states_mfma_ok(int chunk, int dtype) {
@@ -327,7 +341,8 @@ bool chunk_states_mfma_ok(int chunk, int dtype) {
 }
 
 hipError_t launch_chunk_states_mfma(const void *u, const float *Abar, const float *Bbar, int B, int H,
-                                    int L, int m, int chunk, int dtype, float2 *states, hipStream_t s) {
+                                    int L, int m, int chunk, int dtype, float2 *states, hipStream_t s,
+                                    const StateTail *tail, bool *fused) {
     const int rows_per_ch = B * (L / chunk);
     const uint16_t *u16 = (const uint16_t *)u;
     const bool wide = chunk % 2048 == 0;   // 128-wide blocks need 16 columns per tile: chunk / 128 % 16 == 0
@@ -363,7 +378,14 @@ hipError_t launch_chunk_states_mfma(const void *u, const float *Abar, const floa
         auto fn = chunk_states_mfma<DTV, BWV, CMV>;                                                              \
         (void)hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);      \
         const int wg = pick_wg((const void *)fn);                                                                \
-        hipLaunchKernelGGL(fn, dim3(H * wg), dim3(256), lds, s, u16, Abar, Bbar, B, H, L, m, chunk, wg, states); \
+        StateTail tl{};                                                                                          \
+        if (tail && wg == 1 && (size_t)CS_NS * chunk * 2 >= (size_t)CORR_TAB_U4 * 16) {                         \
+            tl = *tail;                                                                                          \
+            tl.fuse = 1;                                                                                         \
+            if (fused) *fused = true;                                                                            \
+        }                                                                                                        \
+        hipLaunchKernelGGL(fn, dim3(H * wg), dim3(256), lds, s, u16, Abar, Bbar, B, H, L, m, chunk, wg, states,  \
+                           tl);                                                                                  \
     } while (0)
     if (dtype == BF16) {
         if (big) H3_CS_LAUNCH(BF16, 128, 16384);
@@ -551,10 +573,10 @@ __device__ __forceinline__ uint32_t ct_h2(double2 p) {
     h2 v = {(_Float16)p.x, (_Float16)p.y};
     return __builtin_bit_cast(uint32_t, v);
 }
-__global__ __launch_bounds__(256) void corr_tables_kernel(const float *Abar, int H, int m, uint4 *tab) {
-    // the channel's table is assembled in LDS, then written out in 16-byte pieces
-    __shared__ uint4 ts[CORR_TAB_U4];
-    const int h = blockIdx.x, tid = threadIdx.x, n = tid & 63, q4 = tid >> 6;
+// Channel h's table, assembled in ts (CORR_TAB_U4 uint4 of LDS) by a
+// 256-thread workgroup, then written to dst in 16-byte pieces.
+__device__ void corr_tables_body(const float *Abar, int h, int m, uint4 *ts, uint4 *dst) {
+    const int tid = threadIdx.x, n = tid & 63, q4 = tid >> 6;
     uint32_t *t = (uint32_t *)ts;
     for (int i = tid; i < CORR_TAB_U4; i += 256) ts[i] = make_uint4(0, 0, 0, 0);   // unused tail
     __syncthreads();
@@ -579,8 +601,11 @@ __global__ __launch_bounds__(256) void corr_tables_kernel(const float *Abar, int
     if (q4 == 0) t[(1536 + kb * 4 + g) * 4 + q] = ct_h2(sp_zpow(z, 1024));
     if (q4 == 1) t[(1552 + kb * 4 + g) * 4 + q] = ct_h2(sp_zpow(z, 8192));   // chunk 16384: a >= 128
     __syncthreads();
-    uint4 *dst = tab + (long)h * CORR_TAB_U4;
     for (int i = tid; i < CORR_TAB_U4; i += 256) dst[i] = ts[i];
+}
+__global__ __launch_bounds__(256) void corr_tables_kernel(const float *Abar, int H, int m, uint4 *tab) {
+    __shared__ uint4 ts[CORR_TAB_U4];
+    corr_tables_body(Abar, blockIdx.x, m, ts, tab + (long)blockIdx.x * CORR_TAB_U4);
 }
 
 hipError_t launch_corr_tables(const float *Abar, int H, int m, uint4 *tab, hipStream_t s) {
@@ -624,12 +649,9 @@ __global__ void state_scan_kernel(const float *Abar, const float *C, const float
 // W_n = C_n Abar_n x^(c)_n are written normalised, W / 2^e with max |W| in
 // [1/2, 1), as fp16 (re, im) pairs, 64 per chunk row (zero beyond m), with
 // the exponent e per chunk row.
-__global__ __launch_bounds__(256) void state_scan_w16_kernel(const float *Abar, const float *C, const float *x0,
-                                                             const float2 *states, int B, int H, int m, int chunk,
-                                                             int nchunk, uint32_t *w16, int *wexp, float *x_final) {
-    const long row = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
-    const int n = threadIdx.x & 63;
-    if (row >= (long)B * H) return;   // whole wavefronts leave together
+// One wavefront: row = b H + h, lane n = mode.
+__device__ void scan_w16_row(const float *Abar, const float *C, const float *x0, const float2 *states, long row,
+                             int H, int m, int chunk, int nchunk, uint32_t *w16, int *wexp, float *x_final, int n) {
     const int h = (int)(row % H);
     const bool on = n < m;
     const long i = (long)h * m + n;
@@ -659,6 +681,26 @@ __global__ __launch_bounds__(256) void state_scan_w16_kernel(const float *Abar, 
         x_final[2 * (row * m + n) + 1] = x.y;
     }
 }
+__global__ __launch_bounds__(256) void state_scan_w16_kernel(const float *Abar, const float *C, const float *x0,
+                                                             const float2 *states, int B, int H, int m, int chunk,
+                                                             int nchunk, uint32_t *w16, int *wexp, float *x_final) {
+    const long row = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= (long)B * H) return;   // whole wavefronts leave together
+    scan_w16_row(Abar, C, x0, states, row, H, m, chunk, nchunk, w16, wexp, x_final, threadIdx.x & 63);
+}
+
+// The tail of the chunk-state kernel when one workgroup holds all chunk rows
+// of channel h: its table of the fused state term (assembled in the kernel's
+// LDS row ring, free by then) and the scan of its B rows, one wavefront per
+// row.  The chunk sums were written by this workgroup and are read back.
+__device__ void cs_state_tail(const StateTail &t, const float *Abar, const float2 *states, int B, int H, int m,
+                              int chunk, int nchunk, int h, uint4 *lds) {
+    corr_tables_body(Abar, h, m, lds, t.ctab + (long)h * CORR_TAB_U4);
+    const int w = threadIdx.x >> 6;
+    for (int b = w; b < B; b += 4)
+        scan_w16_row(Abar, t.C, t.x0, states, (long)b * H + h, H, m, chunk, nchunk, t.w16, t.wexp, t.x_final,
+                     threadIdx.x & 63);
+}
 
 hipError_t launch_state_scan_w16(const float *Abar, const float *C, const float *x0, const float2 *states,
                                  int B, int H, int m, int chunk, int nchunk, uint32_t *w16, int *wexp,
@@ -671,9 +713,11 @@ hipError_t launch_state_scan_w16(const float *Abar, const float *C, const float 
 }
 
 hipError_t launch_chunk_states(const void *u, const float *Abar, const float *Bbar, int B, int H,
-                               int L, int m, int chunk, int dtype, float2 *states, hipStream_t s) {
+                               int L, int m, int chunk, int dtype, float2 *states, hipStream_t s,
+                               const StateTail *tail, bool *fused) {
+    if (fused) *fused = false;
     if (chunk_states_mfma_ok(chunk, dtype))
-        return launch_chunk_states_mfma(u, Abar, Bbar, B, H, L, m, chunk, dtype, states, s);
+        return launch_chunk_states_mfma(u, Abar, Bbar, B, H, L, m, chunk, dtype, states, s, tail, fused);
     const int nchunk = L / chunk;
     const long ncr = (long)B * H * nchunk;
     const size_t lds = (size_t)chunk * sizeof(float) +
