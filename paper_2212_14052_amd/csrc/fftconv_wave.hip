@@ -106,7 +106,7 @@ __device__ __forceinline__ void forward_front(uint32_t (&d)[64], const uint4 *Lc
         const Dft F = lc_dft<CT>(Lc, lane, false);
         const uint4 X = Lc[LcKind<CT>::X * 64 + lane], Xs = Lc[LcKind<CT>::XS * 64 + lane];
         const uint32_t xw[4] = {X.x, X.y, X.z, X.w}, xs[4] = {Xs.x, Xs.y, Xs.z, Xs.w};
-        layer<true>(d, F, NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+        layer2<true>(d, F, NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) d[4 * tau + jj] = cmul2(pk(re[jj], im[jj]), xw[jj], xs[jj]);
         });
@@ -114,7 +114,7 @@ __device__ __forceinline__ void forward_front(uint32_t (&d)[64], const uint4 *Lc
     uint32_t e[64];
     {
         const Dft F = lc_dft<CT>(Lc, lane, false);
-        layer<false>(d, F, [&](int tau) { return Ytab[tau * 64 + lane]; },
+        layer2<false>(d, F, [&](int tau) { return Ytab[tau * 64 + lane]; },
                      [&](int tau, f4_t re, f4_t im, uint4 y) {
                          e[pidx(tau, 0)] = cmul(pk(re[0], im[0]), y.x);
                          e[pidx(tau, 1)] = cmul(pk(re[1], im[1]), y.y);
@@ -154,11 +154,11 @@ __device__ __forceinline__ void out_layer(uint32_t (&d)[64], const h8_t &Fc, flo
         asm volatile("" : "+v"(x));
         return mfma(Fc, x);
     };
-    f4_t v = mm(0);
+    f4_t v = mm(0), vn = mm(1);
 #pragma unroll
     for (int tau = 0; tau < 16; ++tau) {
-        f4_t v1;
-        if (tau + 1 < 16) v1 = mm(tau + 1);
+        f4_t v1 = vn;
+        if (tau + 2 < 16) vn = mm(tau + 2);
         if (GATE && tau == 3) gate_loads(1);
         float yv[4];
 #pragma unroll
@@ -476,7 +476,7 @@ fftconv_wave4096_kernel(ConvArgs a, const float *k, int wg_per_ch, int pairs_per
         Dft F3 = lc_dft<CT>(Lc, lane, false);
         F3.re = h8_scale(F3.re, (_Float16)ldexpf(1.0f, -e2));
         F3.im = h8_scale(F3.im, (_Float16)ldexpf(1.0f, -e2));
-        layer<false>(d, F3, [&](int tau) { return Ks[chw][tau * 64 + lane]; },
+        layer2<false>(d, F3, [&](int tau) { return Ks[chw][tau * 64 + lane]; },
                      [&](int tau, f4_t re, f4_t im, uint4 kk) {
             d[4 * tau + 0] = cmul(pk(re[0], im[0]), kk.x);
             d[4 * tau + 1] = cmul(pk(re[1], im[1]), kk.y);
@@ -485,7 +485,7 @@ fftconv_wave4096_kernel(ConvArgs a, const float *k, int wg_per_ch, int pairs_per
         });
         // inverse: L3^H, swap, conj twiddle (back to quad-per-tile layout),
         // L2^H (signal A) + conj twiddle, L1^H
-        layer<false>(d, lc_dft<CT>(Lc, lane, true), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+        layer2<false>(d, lc_dft<CT>(Lc, lane, true), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) d[4 * tau + jj] = pk(re[jj], im[jj]);
         });
@@ -506,7 +506,7 @@ fftconv_wave4096_kernel(ConvArgs a, const float *k, int wg_per_ch, int pairs_per
         {
             const uint4 X = Lc[LcKind<CT>::X * 64 + lane], Xs = Lc[LcKind<CT>::XS * 64 + lane];
             const uint32_t xw[4] = {X.x, X.y, X.z, X.w}, xs[4] = {Xs.x, Xs.y, Xs.z, Xs.w};
-            layer<true>(d, lc_dft<CT>(Lc, lane, true), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+            layer2<true>(d, lc_dft<CT>(Lc, lane, true), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
 #pragma unroll
                 for (int jj = 0; jj < 4; ++jj) d[4 * tau + jj] = cmulc2(pk(re[jj], im[jj]), xw[jj], xs[jj]);
             });

@@ -277,6 +277,29 @@ __device__ __forceinline__ void layer(uint32_t *d, const Dft &F, Pre &&pre, Epi 
     }
 }
 
+// The same layer with the MFMAs of quads tau + 1 and tau + 2 in flight during
+// the epilogue of quad tau.
+template <bool SIG_A, int NQ = 16, class Pre, class Epi>
+__device__ __forceinline__ void layer2(uint32_t *d, const Dft &F, Pre &&pre, Epi &&epi) {
+    f4_t re0, im0, re1, im1;
+    quad_mfma<SIG_A>(d, F, re0, im0);
+    quad_mfma<SIG_A>(d + 4, F, re1, im1);
+    uint4 pv0 = pre(0), pv1 = pre(1);
+#pragma unroll
+    for (int tau = 0; tau < NQ; ++tau) {
+        f4_t re2, im2;
+        uint4 pv2 = make_uint4(0, 0, 0, 0);
+        if (tau + 2 < NQ) {
+            quad_mfma<SIG_A>(d + 4 * (tau + 2), F, re2, im2);
+            pv2 = pre(tau + 2);
+        }
+        epi(tau, re0, im0, pv0);
+        __builtin_amdgcn_sched_barrier(0);
+        re0 = re1; im0 = im1; pv0 = pv1;
+        re1 = re2; im1 = im2; pv1 = pv2;
+    }
+}
+
 // Exchange slot G's lane-row bits (lane bits 5, 4) with register-index bits
 // 5, 4.  An involution.
 __device__ __forceinline__ void swap_GT(uint32_t (&d)[64]) {
