@@ -205,6 +205,7 @@ def _time_each(fn, reps, warm):
     current stream: an event after every call, so call i is the span between
     the events before and after it (dispatch gaps included, as in the mean)."""
     import torch
+    _settle(fn, torch)
     for _ in range(warm):
         fn(0)
     torch.cuda.synchronize()
@@ -228,6 +229,7 @@ def _dist_us(ms_list):
 
 def _time_calls(fn, reps, warm):
     import torch
+    _settle(fn, torch)
     for _ in range(warm):
         fn(0)
     torch.cuda.synchronize()
@@ -240,10 +242,44 @@ def _time_calls(fn, reps, warm):
     return a.elapsed_time(b) / reps
 
 
+# Seconds of the measured work run before every timed region.  The chip's
+# clocks rise over the first ~0.1 s of sustained load: the config-1 conv run
+# back to back after an idle gap of 0.2 s takes 25.5-27.6 us per launch,
+# after 3000 launches (~75 ms) 23.7-24.1 us.  Each timed region therefore
+# starts from that steady state; the W counted warm-up calls follow it.
+WARM_S = 0.15
+
+
+def _settle(fn, torch, streams=()):
+    """Call fn(i) until the GPU has been busy with it for WARM_S seconds
+    (measured with events on the current stream; calls that issue onto
+    `streams` are joined back into it), in batches that double in size."""
+    cur = torch.cuda.current_stream()
+    a = torch.cuda.Event(enable_timing=True)
+    a.record(cur)
+    for st in streams:
+        st.wait_stream(cur)
+    i, batch = 0, 4
+    while i < 100000:
+        for _ in range(batch):
+            fn(i)
+            i += 1
+        for st in streams:
+            cur.wait_stream(st)
+        b = torch.cuda.Event(enable_timing=True)
+        b.record(cur)
+        b.synchronize()
+        if a.elapsed_time(b) >= WARM_S * 1e3:
+            break
+        batch = min(2 * batch, 512)
+    torch.cuda.synchronize()
+
+
 def _time_streams(fn, streams, reps, warm, torch):
     """ms per call of fn(i) for calls that issue onto `streams` themselves: the
     timed region is bracketed by events on the current stream, which the
     streams wait on first and are joined back into at the end."""
+    _settle(fn, torch, streams)
     for i in range(warm):
         fn(i)
     torch.cuda.synchronize()
