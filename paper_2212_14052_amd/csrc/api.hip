@@ -181,8 +181,11 @@ int statepass_run(const void *u, const float *Abar, const float *Bbar, const flo
     float2 *Kspec = w.mfma ? nullptr : (float2 *)(ws + w.kspec);
     float2 *states = (float2 *)(ws + w.states);
     hipError_t e;
-    // f = [C Bbar, C Abar Bbar, ...] of length chunk, and its spectrum
-    if ((e = launch_kernel_gen(1, Abar, Bbar, C, nullptr, H, m, chunk, kbuf, s)) != hipSuccess) return H3_EDEVICE;
+    // f = [C Bbar, C Abar Bbar, ...] of length chunk, and its spectrum (the
+    // L = 8192 conv with the fused state term forms f itself)
+    const bool gen_f = w.fused && fftconv_wave16k_supported(chunk, dtype);
+    if (!gen_f && (e = launch_kernel_gen(1, Abar, Bbar, C, nullptr, H, m, chunk, kbuf, s)) != hipSuccess)
+        return H3_EDEVICE;
     if (!w.mfma && (e = launch_spectrum(kbuf, H, chunk, Kspec, s)) != hipSuccess) return H3_EDEVICE;
     // s_c = M_ux u^(c) for every chunk, then the scan over chunks (for the
     // fused term, inside the chunk-state kernel when it covers each channel
@@ -210,6 +213,11 @@ int statepass_run(const void *u, const float *Abar, const float *Bbar, const flo
         a.corr = w16;
         a.corr_tab = ctab;
         a.corr_e = wexp;
+        if (gen_f) {
+            a.gen_C = C;
+            a.gen_Bbar = Bbar;
+            a.m_gen = m;
+        }
         return launched(launch_fftconv_mfma(a, kbuf, s));
     }
     float2 *corr_W = (float2 *)(ws + w.corr_w);

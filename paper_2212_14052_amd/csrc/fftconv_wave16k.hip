@@ -416,14 +416,59 @@ __global__ __launch_bounds__(w16::NT) __attribute__((amdgpu_waves_per_eu(2))) vo
         gf[2] = cmul(v3.z, v3.w);   // w_64^{-3c}
     }
     float4 kq[8];   // [4 gi + s]: points m = ... + 16 c + 4 s .. + 3
+    // CORR 3 with gen_C: the kernel row is formed here (below); lane n = mode
+    // n loads C_n and Bbar_n instead
+    const bool gen = CORR == 3 && a.gen_C != nullptr;   // uniform
+    float2 gC = make_float2(0.f, 0.f), gB = make_float2(0.f, 0.f);
+    if (gen) {
+        if (lane < a.m_gen) {
+            gC = ((const float2 *)a.gen_C)[(long)h * a.m_gen + lane];
+            gB = ((const float2 *)a.gen_Bbar)[(long)h * a.m_gen + lane];
+        }
+    } else {
 #pragma unroll
-    for (int gi = 0; gi < 2; ++gi) {
-        const int off = 4096 * xq + 256 * (4 * (2 * (w & 1) + gi) + jq) + 16 * c;
+        for (int gi = 0; gi < 2; ++gi) {
+            const int off = 4096 * xq + 256 * (4 * (2 * (w & 1) + gi) + jq) + 16 * c;
 #pragma unroll
-        for (int s = 0; s < 4; ++s) kq[4 * gi + s] = *(const float4 *)(k + (long)h * L + off + 4 * s);
+            for (int s = 0; s < 4; ++s) kq[4 * gi + s] = *(const float4 *)(k + (long)h * L + off + 4 * s);
+        }
     }
     __builtin_amdgcn_sched_barrier(0);
     if (q0 < q1) issue_loads(q0);
+    if (CORR == 3 && gen) {
+        // k_t = 2 Re sum_n W_n Abar_n^t with W_n = C_n Bbar_n: the fused state
+        // term's sum (Algorithm 2's M_xy form) with the kernel's weights; waves
+        // 0 and 1 form t in [4096 w, 4096 w + 4096) in fp32 into U, then every
+        // wave reads its points as from k.  W is normalised to max |W| in
+        // [1/2, 1) (fp16), in the tables' unused tail.
+        if (q0 < q1)
+            __builtin_amdgcn_s_waitcnt(kWaitVm8);   // tables landed; the pair loads may be in flight
+        else
+            __builtin_amdgcn_s_waitcnt(kWaitVm0);
+        const float2 Wn = make_float2(gC.x * gB.x - gC.y * gB.y, gC.x * gB.y + gC.y * gB.x);
+        const int ew = __builtin_amdgcn_readfirstlane(exp_of(wave_max(fmaxf(fabsf(Wn.x), fabsf(Wn.y)))));
+        uint32_t *Wl = (uint32_t *)(Tab + kTab + 1568);   // 32 unused uint4 of the table
+        __syncthreads();   // every wave's table copies landed
+        if (w == 0) Wl[lane] = pk(ldexpf(Wn.x, -ew), ldexpf(Wn.y, -ew));
+        __syncthreads();
+        if (w < 2) {
+            uint4 wq[4];
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) wq[kb] = ((const uint4 *)Wl)[4 * kb + g];
+            const float sc = ldexpf(2.0f, ew);
+            float *Uf = (float *)U;
+            state_term_core<false>(G1, wq, w, lane, [&](int t, f4_t D) {
+                *(float4 *)(Uf + t) = make_float4(D[0] * sc, D[1] * sc, D[2] * sc, D[3] * sc);
+            });
+        }
+        __syncthreads();
+#pragma unroll
+        for (int gi = 0; gi < 2; ++gi) {
+            const int off = 4096 * xq + 256 * (4 * (2 * (w & 1) + gi) + jq) + 16 * c;
+#pragma unroll
+            for (int s = 0; s < 4; ++s) kq[4 * gi + s] = *(const float4 *)((const float *)U + off + 4 * s);
+        }
+    }
 
     // ---- kernel spectrum block w of channel h (F(k + D delta) 2^-ek / 128) ----
     uint32_t K[64];

@@ -55,6 +55,12 @@ struct ConvArgs {
     // convolution + D u), elementwise, gate in the I/O dtype and layout of y
     // (the output gating of the H3 layer, O = Q * S)
     const void *gate;
+    // gen_C, gen_Bbar (the L = 8192 conv with the fused state term, CORR 3;
+    // may be null): the convolution kernel k_t = 2 Re sum_n C_n Bbar_n
+    // Abar_n^t (the state-passing f of length L) is formed in the kernel
+    // from them and the channel's power tables instead of read from k
+    const float *gen_C, *gen_Bbar;
+    int m_gen;   // their modes per channel (<= 64)
 };
 hipError_t launch_fftconv(const ConvArgs &a, hipStream_t s);
 // The VALU convolution of plain (B, H, L) rows (pair_mode 0, no correction

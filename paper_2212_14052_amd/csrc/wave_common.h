@@ -508,18 +508,18 @@ template <> __device__ __forceinline__ float raw_max<BF16>(const uint4 (&ra)[4])
 // The per-channel table CT (CORR_TAB_U4 uint4, written by the state-passing
 // tables kernel): [0, 1024) Abar_n^b as A operands, [1024, 1536)
 // Abar_n^{64 a}, [1536, 1552) Abar_n^1024, [1552, 1568) Abar_n^8192.
-template <int DT, int ROWU2>
-__device__ __forceinline__ void fused_state_term(const uint4 *U, const uint4 *CT, const uint4 (&wq)[4], int ew,
-                                                 int row, int qa, int lane, uint16_t *yrow) {
+// The sum itself: out(t, D) receives D[jj] = Re sum_n Abar_n^b V_n(a) for the
+// four consecutive t .. t + 3 of tile (jb, ib) (BIG: quarters qa = 2, 3 exist).
+template <bool BIG, class Out>
+__device__ __forceinline__ void state_term_core(const uint4 *CT, const uint4 (&wq)[4], int qa, int lane, Out &&out) {
     const int g = lane >> 4, c = lane & 15;
     const uint4 *CA = CT, *T64 = CT + 1024, *Zt = CT + 1536;
-    const float scorr = ldexpf(2.0f, ew);
     // wq[kb]: normalised W of modes 16 kb + 4 g + q in dword q
     uint32_t V[16];   // [4 kb + q]: (Re V, -Im V) of mode 16 kb + 4 g + q, column a = 64 qa + c
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
         uint4 tq = T64[((qa & 1) * 4 + kb) * 64 + lane];
-        if (ROWU2 > 2048 && qa >= 2) {   // wave-uniform
+        if (BIG && qa >= 2) {   // wave-uniform
             const uint4 z8 = Zt[16 + kb * 4 + g];
             tq = make_uint4(cmul(tq.x, z8.x), cmul(tq.y, z8.y), cmul(tq.z, z8.z), cmul(tq.w, z8.w));
         }
@@ -530,7 +530,6 @@ __device__ __forceinline__ void fused_state_term(const uint4 *U, const uint4 *CT
         V[4 * kb + 3] = cmulc(wq[kb].w ^ 0x80000000u, tq.w);
     }
     const f4_t z = {0.f, 0.f, 0.f, 0.f};
-    const uint2 *Uo = (const uint2 *)U;
 #pragma unroll
     for (int jb = 0; jb < 4; ++jb) {
         if (jb > 0) {
@@ -552,13 +551,21 @@ __device__ __forceinline__ void fused_state_term(const uint4 *U, const uint4 *CT
                 D = mfma_acc(__builtin_bit_cast(h8_t, CA[(ib * 4 + kb) * 64 + lane]),
                              h8_of(V[4 * kb], V[4 * kb + 1], V[4 * kb + 2], V[4 * kb + 3]), D);
             // rows b = 16 ib + 4 g + jj, column a = 64 qa + 16 jb + c
-            const int t = 4096 * qa + 1024 * jb + 64 * c + 16 * ib + 4 * g;
-            const uint2 o = Uo[row * ROWU2 + (t >> 2)];
-            const uint2 r = make_uint2(pack_out<DT>(fmaf(D[0], scorr, lo_f<DT>(o.x)), fmaf(D[1], scorr, hi_f<DT>(o.x))),
-                                       pack_out<DT>(fmaf(D[2], scorr, lo_f<DT>(o.y)), fmaf(D[3], scorr, hi_f<DT>(o.y))));
-            *(uint2 *)(yrow + t) = r;
+            out(4096 * qa + 1024 * jb + 64 * c + 16 * ib + 4 * g, D);
         }
     }
+}
+template <int DT, int ROWU2>
+__device__ __forceinline__ void fused_state_term(const uint4 *U, const uint4 *CT, const uint4 (&wq)[4], int ew,
+                                                 int row, int qa, int lane, uint16_t *yrow) {
+    const float scorr = ldexpf(2.0f, ew);
+    const uint2 *Uo = (const uint2 *)U;
+    state_term_core<(ROWU2 > 2048)>(CT, wq, qa, lane, [&](int t, f4_t D) {
+        const uint2 o = Uo[row * ROWU2 + (t >> 2)];
+        const uint2 r = make_uint2(pack_out<DT>(fmaf(D[0], scorr, lo_f<DT>(o.x)), fmaf(D[1], scorr, hi_f<DT>(o.x))),
+                                   pack_out<DT>(fmaf(D[2], scorr, lo_f<DT>(o.y)), fmaf(D[3], scorr, hi_f<DT>(o.y))));
+        *(uint2 *)(yrow + t) = r;
+    });
 }
 
 }  // namespace wvc
