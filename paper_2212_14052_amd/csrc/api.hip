@@ -182,8 +182,8 @@ int statepass_run(const void *u, const float *Abar, const float *Bbar, const flo
     float2 *states = (float2 *)(ws + w.states);
     hipError_t e;
     // f = [C Bbar, C Abar Bbar, ...] of length chunk, and its spectrum (the
-    // L = 8192 conv with the fused state term forms f itself)
-    const bool gen_f = w.fused && fftconv_wave16k_supported(chunk, dtype);
+    // L = 8192 and 16384 convs with the fused state term form f themselves)
+    const bool gen_f = w.fused;
     if (!gen_f && (e = launch_kernel_gen(1, Abar, Bbar, C, nullptr, H, m, chunk, kbuf, s)) != hipSuccess)
         return H3_EDEVICE;
     if (!w.mfma && (e = launch_spectrum(kbuf, H, chunk, Kspec, s)) != hipSuccess) return H3_EDEVICE;

@@ -414,14 +414,58 @@ __global__ __launch_bounds__(w32::NT) __attribute__((amdgpu_waves_per_eu(2))) vo
     };
     int e2 = 0;   // the spectrum's exponent: pairs' third layer carries 2^-e2
     float4 kq[8];   // [4 gi + s]: points m = ... + 16 c + 4 s .. + 3
+    // CORR 3 with gen_C: the kernel row is formed here (below); lane n = mode
+    // n loads C_n and Bbar_n instead
+    const bool gen = CORR == 3 && a.gen_C != nullptr;   // uniform
+    float2 gC = make_float2(0.f, 0.f), gB = make_float2(0.f, 0.f);
+    if (gen) {
+        if (lane < a.m_gen) {
+            gC = ((const float2 *)a.gen_C)[(long)h * a.m_gen + lane];
+            gB = ((const float2 *)a.gen_Bbar)[(long)h * a.m_gen + lane];
+        }
+    } else {
 #pragma unroll
-    for (int gi = 0; gi < 2; ++gi) {
-        const int off = 4096 * xq + 256 * (4 * (2 * (w & 1) + gi) + jq) + 16 * c;
+        for (int gi = 0; gi < 2; ++gi) {
+            const int off = 4096 * xq + 256 * (4 * (2 * (w & 1) + gi) + jq) + 16 * c;
 #pragma unroll
-        for (int s = 0; s < 4; ++s) kq[4 * gi + s] = *(const float4 *)(k + (long)h * L + off + 4 * s);
+            for (int s = 0; s < 4; ++s) kq[4 * gi + s] = *(const float4 *)(k + (long)h * L + off + 4 * s);
+        }
     }
     __builtin_amdgcn_sched_barrier(0);
     if (q0 < q1) issue_loads(q0);
+    if (CORR == 3 && gen) {
+        // k_t = 2 Re sum_n W_n Abar_n^t with W_n = C_n Bbar_n, as in the
+        // L = 8192 conv: waves 0 .. 3 form the quarters t in [4096 w, 4096 w
+        // + 4096) in fp32 into U, then every wave reads its points as from k
+        if (q0 < q1)
+            __builtin_amdgcn_s_waitcnt(kWaitVm8);   // tables landed; the pair loads may be in flight
+        else
+            __builtin_amdgcn_s_waitcnt(kWaitVm0);
+        const float2 Wn = make_float2(gC.x * gB.x - gC.y * gB.y, gC.x * gB.y + gC.y * gB.x);
+        const int ew = __builtin_amdgcn_readfirstlane(exp_of(wave_max(fmaxf(fabsf(Wn.x), fabsf(Wn.y)))));
+        uint32_t *Wl = (uint32_t *)(Tab + kTab32 + 1568);   // 32 unused uint4 of the table
+        __syncthreads();   // every wave's table copies landed
+        if (w == 0) Wl[lane] = pk(ldexpf(Wn.x, -ew), ldexpf(Wn.y, -ew));
+        __syncthreads();
+        if (w < 4) {
+            uint4 wq[4];
+            const int g = lane >> 4;
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) wq[kb] = ((const uint4 *)Wl)[4 * kb + g];
+            const float sc = ldexpf(2.0f, ew);
+            float *Uf = (float *)U;
+            state_term_core<true>(CT, wq, w, lane, [&](int t, f4_t D) {
+                *(float4 *)(Uf + t) = make_float4(D[0] * sc, D[1] * sc, D[2] * sc, D[3] * sc);
+            });
+        }
+        __syncthreads();
+#pragma unroll
+        for (int gi = 0; gi < 2; ++gi) {
+            const int off = 4096 * xq + 256 * (4 * (2 * (w & 1) + gi) + jq) + 16 * c;
+#pragma unroll
+            for (int s = 0; s < 4; ++s) kq[4 * gi + s] = *(const float4 *)((const float *)U + off + 4 * s);
+        }
+    }
 
     // first-layer rows of this wave: the base (contraction side times
     // w_128^{k3 p2} / 4) and the same times w_8

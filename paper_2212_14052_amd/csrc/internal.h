@@ -55,7 +55,7 @@ struct ConvArgs {
     // convolution + D u), elementwise, gate in the I/O dtype and layout of y
     // (the output gating of the H3 layer, O = Q * S)
     const void *gate;
-    // gen_C, gen_Bbar (the L = 8192 conv with the fused state term, CORR 3;
+    // gen_C, gen_Bbar (the L = 8192 and 16384 convs with the fused state term;
     // may be null): the convolution kernel k_t = 2 Re sum_n C_n Bbar_n
     // Abar_n^t (the state-passing f of length L) is formed in the kernel
     // from them and the channel's power tables instead of read from k
