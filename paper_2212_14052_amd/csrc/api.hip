@@ -66,7 +66,8 @@ StatepassWs statepass_ws(int B, int H, int L, int m, int chunk, int dtype) {
         off += align_up(bytes);
         return at;
     };
-    w.k = take((size_t)H * chunk * sizeof(float));
+    // the chunk kernel f: the fused-term convs form it themselves
+    if (!w.fused) w.k = take((size_t)H * chunk * sizeof(float));
     if (!w.mfma) w.kspec = take((size_t)H * (chunk + 1) * sizeof(float2));
     w.states = take((size_t)B * H * nchunk * m * sizeof(float2));
     if (w.fused) {
@@ -218,7 +219,7 @@ int statepass_run(const void *u, const float *Abar, const float *Bbar, const flo
             a.gen_Bbar = Bbar;
             a.m_gen = m;
         }
-        return launched(launch_fftconv_mfma(a, kbuf, s));
+        return launched(launch_fftconv_mfma(a, gen_f ? nullptr : kbuf, s));
     }
     float2 *corr_W = (float2 *)(ws + w.corr_w);
     void *corr = ws + w.corr;
