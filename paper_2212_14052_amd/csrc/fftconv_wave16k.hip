@@ -43,6 +43,12 @@ namespace w16 {
 
 using namespace wvc;
 
+template <bool P2, bool SIG_A, class Pre, class Epi>
+__device__ __forceinline__ void layer_sel(uint32_t *d, const Dft &F, Pre &&pre, Epi &&epi) {
+    if constexpr (P2) layer2<SIG_A>(d, F, pre, epi);
+    else layer<SIG_A>(d, F, pre, epi);
+}
+
 constexpr int N = 16384;
 constexpr int L = 8192;
 constexpr int NW = 4;           // waves per workgroup (one per frequency block)
@@ -620,13 +626,13 @@ __global__ __launch_bounds__(w16::NT) __attribute__((amdgpu_waves_per_eu(2))) vo
             }
         }
         __syncthreads();   // every wave is done reading the staged pair
-        forward_mid(d, Lc, Ytab, lane);
+        forward_mid<CORR == 0>(d, Lc, Ytab, lane);
         {
             // third layer (contraction side times w_16384^{k3 p0} 2^-e2) and
             // the pointwise product with the kernel spectrum block
             uint32_t R[4], I[4];
             kinds_scaled(Lc[1 * 64 + lane], f3, R, I);
-            layer<false>(d, dft_of(R, I), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+            layer_sel<CORR == 0, false>(d, dft_of(R, I), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
 #pragma unroll
                 for (int jj = 0; jj < 4; ++jj) {
                     // opaque per use: otherwise the (-im, re) companion of every
@@ -642,7 +648,7 @@ __global__ __launch_bounds__(w16::NT) __attribute__((amdgpu_waves_per_eu(2))) vo
             uint32_t R[4], I[4];
             const uint32_t gg[4] = {g3, g3, g3, g3};
             kinds_scaled(Lc[3 * 64 + lane], gg, R, I);
-            layer<false>(d, dft_of(R, I), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+            layer_sel<CORR == 0, false>(d, dft_of(R, I), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
 #pragma unroll
                 for (int jj = 0; jj < 4; ++jj) d[4 * tau + jj] = pk(re[jj], im[jj]);
             });
@@ -664,7 +670,7 @@ __global__ __launch_bounds__(w16::NT) __attribute__((amdgpu_waves_per_eu(2))) vo
         {
             uint32_t xw[4], xs[4];
             twiddles_inv(Lc[4 * 64 + lane], xh, xw, xs);
-            layer<true>(d, lds_dft(Lc, lane, true), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+            layer_sel<CORR == 0, true>(d, lds_dft(Lc, lane, true), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
 #pragma unroll
                 for (int jj = 0; jj < 4; ++jj) d[4 * tau + jj] = cmul2(pk(re[jj], im[jj]), xw[jj], xs[jj]);
             });

@@ -424,10 +424,16 @@ __device__ __forceinline__ f4_t mfma_acc(bf8_t a, bf8_t b, f4_t c) {
 }
 
 // Second layer (signal B) + L2 twiddles into P layout, then the G <-> T swap.
+template <bool P2 = false>
 __device__ __forceinline__ void forward_mid(uint32_t (&d)[64], const uint4 *Lc, const uint4 *Ytab, int lane) {
     uint32_t e[64];
     const Dft F = lds_dft(Lc, lane, false);
-    layer<false>(d, F, [&](int tau) { return Ytab[tau * 64 + lane]; },
+    auto pre = [&](int tau) { return Ytab[tau * 64 + lane]; };
+    auto run = [&](auto &&epi) {
+        if constexpr (P2) layer2<false>(d, F, pre, epi);
+        else layer<false>(d, F, pre, epi);
+    };
+    run(
                  [&](int tau, f4_t re, f4_t im, uint4 y) {
                      e[pidx(tau, 0)] = cmul(pk(re[0], im[0]), y.x);
                      e[pidx(tau, 1)] = cmul(pk(re[1], im[1]), y.y);
