@@ -10,7 +10,7 @@ HBM; K steps rotate over enough input/output buffer sets (>= 512 MB) that
 every step reads u and writes y cold (not from the 256 MB Infinity Cache).
 
 value = algorithmic bytes of one step (u + y + k once per channel + D) / time,
-in GB/s, for K independent steps issued round-robin on three HIP streams (each
+in GB/s, for K independent steps issued round-robin on two HIP streams (each
 with its own kernel buffer and workspace: one step's last workgroups share the
 chip with the next steps' first); the single-stream step time is reported
 beside it.  The timed loops call the C entry points with prebuilt arguments
@@ -107,7 +107,7 @@ def _f32(a, dev):
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
 
 
-def bench_headline(h3, steps, warmup, dev, nstreams=3):
+def bench_headline(h3, steps, warmup, dev, nstreams=2):
     """Config 1 step: kernel generation + fused FFT conv (diagonal SSM).
 
     Steps are independent batches of the workload (their own u and y buffer
@@ -690,7 +690,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--streams", type=int, default=3,
+    ap.add_argument("--streams", type=int, default=2,
                     help="HIP streams the headline steps are issued on (independent batches)")
     ap.add_argument("--no-extra", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
