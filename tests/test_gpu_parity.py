@@ -579,6 +579,9 @@ def test_layer_heads(h3, dtype, B, L, dh, with_D):
 @pytest.mark.parametrize("dtype", [workloads.BF16, workloads.F16])
 @pytest.mark.parametrize("B,d", [(3, 256), (6, 256), (4, 768), (1, 1280)])
 def test_layer_gated_conv(h3, dtype, B, d):
+    # the worst rows are the first tokens, whose outputs are 20-60 times
+    # smaller than the largest: the 16-bit transform's error is spread evenly
+    # over a row of the convolution, so it weighs most there
     w = workloads.layer_workload("t", B, 2048, d, dtype, seed=41 + B + d)
     y, ref = _layer_case(h3, w)
     check(y, ref, 2e-2)
