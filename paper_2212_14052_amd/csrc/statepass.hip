@@ -165,7 +165,9 @@ __device__ void cs_state_tail(const StateTail &t, const float *Abar, const float
 
 // tail.fuse (one workgroup per channel, chunk 8192 or 16384): the workgroup
 // also writes the channel's fused-term table and scans its rows (cs_state_tail)
-template <int DT, int BW, int CMAX>
+// FULL: chunk == CMAX, so every column tile is present and the tiles' matrix
+// products are free to interleave (no per-tile branch)
+template <int DT, int BW, int CMAX, bool FULL>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void chunk_states_mfma(
     const uint16_t *u, const float *Abar, const float *Bbar, int B, int H, int L, int m, int chunk, int wg_per_ch,
     float2 *states, StateTail tail) {
@@ -245,11 +247,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
         const int c = slot ^ ((a / RPB) % SPR);
         return BW * a + 8 * c;
     };
-    // copies of chunk row rr (clamped to the last: past it they only keep the
-    // count per row fixed) into buffer (rr - r0) % CS_NS
+    // copies of chunk row rr into buffer (rr - r0) % CS_NS
     auto issue = [&](int rr) {
-        const int rc = min(rr, r1 - 1);
-        const int bb = rc / nchunk, cc = rc % nchunk;
+        const int bb = rr / nchunk, cc = rr % nchunk;
         // the row's address and the buffer, in scalar registers (wave-uniform)
         const uint64_t sp = (uint64_t)(uintptr_t)(u + ((long)bb * H + h) * L + (long)cc * chunk);
         const uint64_t spu = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(sp >> 32)) << 32) |
@@ -283,13 +283,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
         __builtin_amdgcn_s_waitcnt(0x070);   // vmcnt(0) lgkmcnt(0)
         asm volatile("s_barrier" ::: "memory");
         if (w == 0 && rr > r0) store_row(rr - 1);
-        issue(rr + 1);
+        // the next row's copies (none past the last row: the tail below
+        // reuses the ring, so no copy may land there after the loop)
+        if (rr + 1 < r1) issue(rr + 1);
         const char *us = cs_lds + ((rr - r0) % CS_NS) * row_b;
         sp_f4 sre = {0.f, 0.f, 0.f, 0.f}, sim = {0.f, 0.f, 0.f, 0.f};
         float2 E[4] = {E0[0], E0[1], E0[2], E0[3]};
 #pragma unroll
         for (int ct = NA_MAX / 16 - 1; ct >= 0; --ct) {
-            if (ct < NCT) {
+            if (FULL || ct < NCT) {
                 sp_f4 accr = {0.f, 0.f, 0.f, 0.f}, acci = {0.f, 0.f, 0.f, 0.f};
                 const int a = 16 * ct + r16;
 #pragma unroll
@@ -375,7 +377,7 @@ hipError_t launch_chunk_states_mfma(const void *u, const float *Abar, const floa
     };
 #define H3_CS_LAUNCH(DTV, BWV, CMV)                                                                              \
     do {                                                                                                         \
-        auto fn = chunk_states_mfma<DTV, BWV, CMV>;                                                              \
+        auto fn = chunk == CMV ? chunk_states_mfma<DTV, BWV, CMV, true> : chunk_states_mfma<DTV, BWV, CMV, false>; \
         (void)hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);      \
         const int wg = pick_wg((const void *)fn);                                                                \
         StateTail tl{};                                                                                          \
