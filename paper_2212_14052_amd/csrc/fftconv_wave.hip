@@ -679,10 +679,10 @@ __device__ __forceinline__ int pack_pair(const uint4 (&ra)[8], const uint4 (&rb)
 }  // namespace wv
 
 template <int DT>
-__global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(2))) void wgrad_wave4096_kernel(
+__global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) void wgrad_wave4096_kernel(
     const uint16_t *u, const uint16_t *dy, int B, int H, int ngroup, float *dk, float *dD) {
     using namespace wv;
-    __shared__ uint4 Tab[kTab];
+    __shared__ uint4 Tab[kTabC];   // the compact table: three workgroups per CU
     // summed spectrum, planar (re, im), index (tau * 4 + jj) * 64 + lane (lanes
     // on consecutive banks); then the dk staging buffer
     __shared__ float S[2 * kN];
@@ -695,10 +695,10 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(2))) voi
     const int qq = NW * grp + w;   // this wave's row pair (at most one)
     const bool have = qq < npairs;
 #pragma unroll
-    for (int r = 0; r < (kTab + NT - 1) / NT; ++r) {
+    for (int r = 0; r < (kTabC + NT - 1) / NT; ++r) {
         const int base = r * NT + 64 * w;
-        if (base < kTab)
-            __builtin_amdgcn_global_load_lds((gvoid_t *)((const uint4 *)kHalf.v + base + lane),
+        if (base < kTabC)
+            __builtin_amdgcn_global_load_lds((gvoid_t *)((const uint4 *)kHalfC.v + base + lane),
                                              (lvoid_t *)(Tab + base), 16, 0, 0);
     }
     uint4 ra[8], rb[8];
@@ -711,18 +711,23 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(2))) voi
     int ep = 0;
     if (have) {
         const int eu = pack_pair<DT>(ra, rb, d);
-        forward_front<false>(d, Lc, Ytab, lane);
-        load_pair_raw(dy, oa, ob, g, c, ra, rb);   // in flight during the u transform's last layer
-        layer<false>(d, lds_dft(Lc, lane, false), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+        forward_front<true>(d, Lc, Ytab, lane);
+        layer<false>(d, lc_dft<true>(Lc, lane, false), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) zu[4 * tau + jj] = pk(re[jj], im[jj]);
         });
+        // dy's loads after the u transform (the empty asm pins every zu value
+        // before them): raw, transform and spectrum registers are never live
+        // at once (three waves per SIMD)
+#pragma unroll
+        for (int i = 0; i < 64; ++i) asm volatile("" : "+v"(zu[i])::"memory");
+        load_pair_raw(dy, oa, ob, g, c, ra, rb);
         const int eg = pack_pair<DT>(ra, rb, d);
-        forward_front<false>(d, Lc, Ytab, lane);
+        forward_front<true>(d, Lc, Ytab, lane);
         // conj(Zu) . Zdy in float32 from the matrix-core outputs, packed back
         // into zu at 2^-7 (both transforms are below 1448 in modulus, so the
         // product stays below 2^14)
-        layer<false>(d, lds_dft(Lc, lane, false), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+        layer<false>(d, lc_dft<true>(Lc, lane, false), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) {
                 const h2_t a = as_h2(zu[4 * tau + jj]);
@@ -769,7 +774,7 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(2))) voi
             d[4 * tau + jj] = pk(ldexpf(S[si], -es), ldexpf(S[kN + si], -es));
         }
     // the inverse of the convolution
-    layer<false>(d, lds_dft(Lc, lane, true), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+    layer<false>(d, lc_dft<true>(Lc, lane, true), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj) d[4 * tau + jj] = pk(re[jj], im[jj]);
     });
@@ -788,9 +793,9 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(2))) voi
         for (int i = 0; i < 64; ++i) d[i] = e[i];
     }
     {
-        const uint4 X = Lc[4 * 64 + lane], Xs = Lc[5 * 64 + lane];
+        const uint4 X = Lc[LcKind<true>::X * 64 + lane], Xs = Lc[LcKind<true>::XS * 64 + lane];
         const uint32_t xw[4] = {X.x, X.y, X.z, X.w}, xs[4] = {Xs.x, Xs.y, Xs.z, Xs.w};
-        layer<true>(d, lds_dft(Lc, lane, true), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
+        layer<true>(d, lc_dft<true>(Lc, lane, true), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) d[4 * tau + jj] = cmulc2(pk(re[jj], im[jj]), xw[jj], xs[jj]);
         });
@@ -799,7 +804,7 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(2))) voi
     // the real part is dk.  Staged through LDS (S is free) for coalesced stores.
     float *stage = S;
     const float osc = ldexpf(1.0f, es + 6);
-    layer<false>(d, lds_dft(Lc, lane, true), NoPre{}, [&](int tau, f4_t re, f4_t, uint4) {
+    layer<false>(d, lc_dft<true>(Lc, lane, true), NoPre{}, [&](int tau, f4_t re, f4_t, uint4) {
         if (g < 2) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) stage[256 * (4 * g + i) + 16 * c + tau] = re[i] * osc;
