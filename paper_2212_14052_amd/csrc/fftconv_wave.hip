@@ -703,6 +703,7 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
     }
     uint4 ra[8], rb[8];
     uint32_t d[64], zu[64];
+    uint32_t *zs = (uint32_t *)S + w * (2 * kN / NW);   // this wave's quarter of S
     const long oa = ((long)(2 * qq) * H + h) * L;
     const long ob = (2 * qq + 1 < B) ? oa + (long)H * L : -1;
     if (have) load_pair_raw(u, oa, ob, g, c, ra, rb);
@@ -716,11 +717,15 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) zu[4 * tau + jj] = pk(re[jj], im[jj]);
         });
-        // dy's loads after the u transform (the empty asm pins every zu value
-        // before them): raw, transform and spectrum registers are never live
-        // at once (three waves per SIMD)
+        // the upper half of u's spectrum waits in this wave's quarter of S
+        // (free until the products are summed), the lower half in registers
 #pragma unroll
-        for (int i = 0; i < 64; ++i) asm volatile("" : "+v"(zu[i])::"memory");
+        for (int i = 32; i < 64; ++i) zs[(i - 32) * 64 + lane] = zu[i];
+        // dy's loads after the u transform (the empty asm pins the kept zu
+        // values before them): raw, transform and spectrum registers are
+        // never live at once (three waves per SIMD)
+#pragma unroll
+        for (int i = 0; i < 32; ++i) asm volatile("" : "+v"(zu[i])::"memory");
         load_pair_raw(dy, oa, ob, g, c, ra, rb);
         const int eg = pack_pair<DT>(ra, rb, d);
         forward_front<true>(d, Lc, Ytab, lane);
@@ -730,13 +735,15 @@ __global__ __launch_bounds__(wv::NT) __attribute__((amdgpu_waves_per_eu(3))) voi
         layer<false>(d, lc_dft<true>(Lc, lane, false), NoPre{}, [&](int tau, f4_t re, f4_t im, uint4) {
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) {
-                const h2_t a = as_h2(zu[4 * tau + jj]);
+                const int i = 4 * tau + jj;
+                const h2_t a = as_h2(i < 32 ? zu[i] : zs[(i - 32) * 64 + lane]);
                 const float ar = (float)a.x, ai = (float)a.y;
                 zu[4 * tau + jj] = pk((ar * re[jj] + ai * im[jj]) * 0.0078125f, (ar * im[jj] - ai * re[jj]) * 0.0078125f);
             }
         });
         ep = eu + eg + 7;
     }
+    __syncthreads();   // every wave has read its quarter of S back
     // the waves add their products into S in turn (wave 0 stores), scaled
     // back by 2^ep: S = sum conj(F z_u) F z_dy / 4096
     const float sc = ldexpf(1.0f, ep);
