@@ -54,7 +54,7 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0
 FETCH_FACTOR, WRITE_FACTOR = 2.0, 1.0
 COUNTERS = {
     "headline": {"src": ("paper_2212_14052_amd/csrc/fftconv_wave.hip", "paper_2212_14052_amd/csrc/wave_common.h"),
-                 "sha": "52953120f9cbcc20", "fetch_kib": 15636.2, "write_kib": 24576.0,
+                 "sha": "b4c45271e860df90", "fetch_kib": 15636.2, "write_kib": 24576.0,
                  "valu": 6062592, "mfma": 614400, "mfma_busy": 0.194},
     "cfg0_scaled": {"src": ("paper_2212_14052_amd/csrc/fftconv.hip", "paper_2212_14052_amd/csrc/fft_valu.h"),
                     "sha": "a55c178cb10dd628", "fetch_kib": 73914.3, "write_kib": 131072.0,

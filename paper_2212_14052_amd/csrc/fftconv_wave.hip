@@ -576,8 +576,8 @@ fftconv_wave4096_kernel(ConvArgs a, const float *k, int wg_per_ch, int pairs_per
 // kept in packed fp16; the forward transform of the dy pair ends in an L3
 // epilogue that forms conj(Zu) . Zdy in float32 from the matrix-core outputs,
 // undoes both inputs' power-of-two scales and adds it into a float32 spectrum
-// in LDS (LDS float atomics; the four waves add in any order).  Wave 0 then
-// normalises the summed spectrum to a power of two, runs the inverse of the
+// in LDS (the four waves in turn).  Wave 0 then normalises the summed
+// spectrum to a power of two, runs the inverse of the
 // convolution (L3^H, swap, conj twiddle, L2^H, L1^H) and writes dk in float32.
 // Scales: the forward leaves F(z) 2^-e / 64 (three matrices carrying 1/4), so
 // the accumulated spectrum is S = sum conj(F z_u) F z_dy / 4096; with S scaled
